@@ -1,0 +1,169 @@
+/*
+ * fwg.h -- C ABI of the Fast Wavenet generation library (libfwg.so) for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The library implements cached autoregressive generation through a stack of
+ * width-2 dilated causal convolutions, the method of "Fast Wavenet Generation
+ * Algorithm" (Paine et al., 2016):
+ *   - the generation model is one step of a multi-layer RNN: it maps the current
+ *     input and the recurrent states popped from the convolution queues to the
+ *     current output and the new recurrent states (Section 2.2, Fig. 4);
+ *   - there is one FIFO convolution queue per layer, its depth equal to the
+ *     dilation of the layer it feeds (Section 2.1, Fig. 3), initialised with
+ *     zeros (Section 2.2);
+ *   - each generated sample runs a pop phase, the computation and a push phase
+ *     (Section 2.2, Fig. 5, Fig. 6), so a sample costs O(L) work instead of the
+ *     O(2^L) of recomputing the tree of Fig. 1 (Section 3.1);
+ *   - every prediction is fed back as the next input (Section 1).
+ *
+ * Layer kinds (the paper leaves the layer type open):
+ *   FWG_RELU:           x^l = relu(W_r x^{l-1}_{t-d} + W_e x^{l-1}_t + b)
+ *   FWG_RELU_RESIDUAL:  x^l = x^{l-1} + relu(W_r x^{l-1}_{t-d} + W_e x^{l-1}_t + b)
+ *   FWG_GATED:          a = W_r x^{l-1}_{t-d} + W_e x^{l-1}_t + b (2R channels),
+ *                       z = tanh(a[0:R]) * sigmoid(a[R:2R]),
+ *                       x^l = x^{l-1} + W_res z + b_res,  s += W_skip z + b_skip
+ *   output: relu kinds  logits = W_out x^L + b_out
+ *           gated       logits = W_out relu(W_head relu(s) + b_head) + b_out
+ *   sampling: softmax over the n_classes logits, inverse CDF with one caller
+ *           uniform u per stream and step: the first class k with u*Z < S_k
+ *           (S_k = running sum of exp(logit_j - max), Z = S_{n_classes-1}),
+ *           else the last class.  Computed in float32.
+ *
+ * Precision: FWG_F32 computes in float32.  FWG_BF16 takes bf16 weights and
+ * rounds every operand of a weight product (popped states, the current layer
+ * input, z, relu(s), the head hidden vector, the output layer's input) to bf16
+ * (round to nearest even); accumulation, biases, nonlinearities, the residual
+ * stream, the skip sum, logits and softmax stay float32.  The queues store bf16.
+ *
+ * Memory and ownership:
+ *   - The library never allocates device memory.  The caller provides one
+ *     device workspace of fwg_workspace_size() bytes (256-byte aligned), which
+ *     must stay allocated and untouched until fwg_destroy().
+ *   - fwg_create() copies and repacks the caller's weights into the workspace;
+ *     the caller's weight buffers may be freed once the stream has synchronised.
+ *   - All device pointers are plain device addresses; all outputs are
+ *     caller-owned.
+ *   - Every call enqueues its work on the stream given to fwg_create() and
+ *     returns without waiting (fwg_create() itself synchronises that stream
+ *     once, after uploading its tables).  The caller synchronises before
+ *     reading outputs.
+ *
+ * Errors: every argument and state check runs on the host before anything is
+ * enqueued; on a non-OK status nothing was enqueued and fwg_last_error()
+ * returns a message (per calling thread).  Device data are never validated:
+ * inputs outside [0, n_classes) are undefined behaviour; a uniform >= 1 selects
+ * the last class and a negative one class 0.  A handle is not thread-safe;
+ * distinct handles are independent.
+ */
+#ifndef FWG_H
+#define FWG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+enum {
+  FWG_OK = 0,
+  FWG_EINVAL = -1,       /* NULL pointer, non-positive size, dilation < 1, batch out of range ... */
+  FWG_ENOSPACE = -2,     /* workspace smaller than fwg_workspace_size() or misaligned */
+  FWG_EHIP = -3,         /* a HIP runtime call failed (message has the HIP error string) */
+  FWG_ESTATE = -4,       /* generate() with a batch other than the one used since the last reset */
+  FWG_EUNSUPPORTED = -5  /* a valid shape this build has no kernel for */
+};
+
+/* layer kinds */
+enum { FWG_RELU = 0, FWG_RELU_RESIDUAL = 1, FWG_GATED = 2 };
+/* weight / operand types (accumulation is always float32) */
+enum { FWG_F32 = 0, FWG_BF16 = 1 };
+
+/* Model descriptor.  All fields are read during the call only. */
+typedef struct {
+  int32_t kind;           /* FWG_RELU, FWG_RELU_RESIDUAL or FWG_GATED */
+  int32_t dtype;          /* FWG_F32 or FWG_BF16 */
+  int32_t n_classes;      /* Q: size of the one-hot input and of the softmax; 256 supported */
+  int32_t channels;       /* C (relu kinds) or R (gated residual channels) */
+  int32_t skip_channels;  /* S, gated only (ignored otherwise) */
+  int32_t head_channels;  /* H, gated only (ignored otherwise) */
+  int32_t n_layers;       /* L >= 1 */
+  int32_t max_batch;      /* largest batch of independent streams, >= 1 */
+  int32_t seed_input;     /* input class fed at the first step after a reset, in [0, Q) */
+  const int32_t *dilations; /* HOST array [n_layers], each >= 1: layer l reads x^{l-1}_{t-d_l} */
+} fwg_desc;
+
+/* Weights: DEVICE pointers to row-major arrays in PyTorch layouts; the
+ * per-layer tables are HOST arrays of n_layers DEVICE pointers.  Matrices have
+ * the descriptor's dtype (bf16 = 16-bit bf16 bit patterns); biases are always
+ * float32.  A NULL bias (or a NULL bias table) means zeros.
+ *   embed   [C][Q]           1x1 convolution over the one-hot input
+ *   conv[l] [Cout][C][2]     Cout = C (relu kinds) or 2R (gated);
+ *                            tap 0 multiplies x_{t-d} (W_r), tap 1 multiplies x_t (W_e)
+ *   res[l]  [R][R]           gated only
+ *   skip[l] [S][R]           gated only
+ *   head    [H][S]           gated only
+ *   out     [Q][C] or [Q][H] */
+typedef struct {
+  const void *embed;
+  const float *embed_b;
+  const void *const *conv;
+  const float *const *conv_b;
+  const void *const *res;
+  const float *const *res_b;
+  const void *const *skip;
+  const float *const *skip_b;
+  const void *head;
+  const float *head_b;
+  const void *out;
+  const float *out_b;
+} fwg_weights;
+
+typedef struct fwg_handle fwg_handle;
+
+/* Bytes of device workspace a model needs (pure host computation; no device
+ * needed).  Returns FWG_EINVAL / FWG_EUNSUPPORTED for descriptors create()
+ * would reject. */
+int fwg_workspace_size(const fwg_desc *desc, size_t *bytes);
+
+/* Validate the descriptor, lay out the workspace, repack the weights into it
+ * and reset the queues (Section 2.2: queues start at zero).  hip_stream is a
+ * hipStream_t (NULL = default stream) on the current device; it is used by
+ * every later call on the handle.  On success *out receives the handle. */
+int fwg_create(const fwg_desc *desc, const fwg_weights *weights, void *workspace, size_t ws_bytes,
+               void *hip_stream, fwg_handle **out);
+
+/* Zero every convolution queue, set t = 0 and every stream's next input to
+ * seed_input, and unbind the batch size. */
+int fwg_reset_queues(fwg_handle *h);
+
+/* Generate n_steps samples for each of `batch` independent streams, continuing
+ * from the current state (pop, compute, push per sample; each sample is fed
+ * back as the next input).  uniforms: DEVICE float32 [batch][n_steps];
+ * samples: DEVICE int32 [batch][n_steps], samples[b][s] drawn for time t0+s.
+ * The first call after a reset binds the batch size; later calls with another
+ * batch return FWG_ESTATE.  n_steps == 0 is a no-op. */
+int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples);
+
+/* Teacher-forced evaluation from zero queues: logits[b][t][:] is the output
+ * after consuming inputs[b][0..t].  inputs: DEVICE int32 [batch][seq_len];
+ * logits: DEVICE float32 [batch][seq_len][n_classes].  Runs the same step
+ * kernels with the input taken from `inputs` instead of the previous sample;
+ * uses queues of its own and leaves the generation state untouched.
+ * 1 <= batch <= max_batch; seq_len == 0 is a no-op. */
+int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
+
+/* Free the host-side handle (the workspace stays the caller's). NULL is a no-op. */
+int fwg_destroy(fwg_handle *h);
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+const char *fwg_last_error(void);
+
+/* Short name of the kernel family a handle uses (for logs and profiles). */
+const char *fwg_regime(const fwg_handle *h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FWG_H */

@@ -1,0 +1,102 @@
+// Internal definitions shared by the host layer (fwg_host.cpp) and the HIP
+// kernels (fwg_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fwg {
+
+constexpr int kThreads = 256;     // every step kernel runs 4 waves of 64 lanes
+constexpr int kMaxLayers = 1024;  // per-layer slot counters live in LDS
+
+// One dilated layer as the step kernels see it (device-resident table).
+struct LayerDev {
+  const void *conv;     // packed conv weights (W_r stacked over W_e), layout per kernel family
+  const float *conv_b;  // [Cout]
+  const void *res;      // gated: packed [R][R]
+  const float *res_b;   // [R]
+  const void *skip;     // gated: packed [S][R]
+  const float *skip_b;  // [S]
+  long long ring_off;   // element offset of this layer's queue inside a queue region
+  int dil;              // queue depth = dilation
+  int pad_;
+};
+
+// Arguments of one step-kernel launch (passed by value).
+struct StepArgs {
+  const LayerDev *layers;  // [L]
+  const void *embed;       // [Q][C] rows (embedding transposed for a row gather)
+  const float *embed_b;    // [C]
+  const void *head;        // gated: packed [H][S]
+  const float *head_b;     // [H]
+  const void *out;         // packed [Q][C or H]
+  const float *out_b;      // [Q]
+  void *ring;              // queue region (generation or teacher-forced)
+  int32_t *last;           // [bmax] next input per stream (generation mode)
+  const float *uniforms;   // [batch][n_steps]
+  int32_t *samples;        // [batch][n_steps]
+  const int32_t *inputs;   // teacher-forced [batch][n_steps]
+  float *logits;           // teacher-forced [batch][n_steps][Q]
+  long long t0;            // time index of the first step of this launch
+  int n_steps, batch, bmax;
+  int kind, dtype, C, S, H, Q, L;
+  int forced;              // 1: teacher-forced mode
+};
+
+// Kernel families.
+enum Regime { REGIME_VALU = 0 };
+
+// Packed-weight layout of the VALU family: W^T blocked by 16 bytes along K,
+// Wp[kb][n][kb_elems], with W^T[k][n] the weight from input k to output n.
+inline int valu_kb_elems(int dtype) { return dtype == 1 ? 8 : 4; }
+
+// LDS layout (in floats) of the VALU step kernel for rows-per-block `rpw`.
+struct ValuLds {
+  int xf, xo, vo, ao, zo, so, ho, h2, lg, partA, partB, slots, ins, total_floats;
+};
+__host__ __device__ inline int valu_part_cols(int N) { return N >= 256 ? N : 256; }
+__host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H, int Q, int L, int rpw) {
+  ValuLds o;
+  int p = 0;
+  auto take = [&](int n) { int at = p; p += (n + 3) & ~3; return at; };
+  const int Co = kind == 2 ? 2 * C : C;
+  o.xf = take(rpw * C);
+  o.xo = take(rpw * C);
+  o.vo = take(rpw * C);
+  o.ao = take(rpw * Co);
+  o.zo = take(kind == 2 ? rpw * C : 0);
+  o.so = take(kind == 2 ? rpw * S : 0);
+  o.ho = take(kind == 2 ? rpw * S : 0);
+  o.h2 = take(kind == 2 ? rpw * H : 0);
+  o.lg = take(rpw * Q);
+  int partN = valu_part_cols(Co);
+  if (kind == 2) {
+    partN = partN > valu_part_cols(S) ? partN : valu_part_cols(S);
+    partN = partN > valu_part_cols(H) ? partN : valu_part_cols(H);
+  }
+  partN = partN > valu_part_cols(Q) ? partN : valu_part_cols(Q);
+  o.partA = take(rpw * partN);
+  o.partB = take(kind == 2 ? rpw * valu_part_cols(C) : 0);
+  o.slots = take(L);   // int
+  o.ins = take(rpw);   // int
+  o.total_floats = p;
+  return o;
+}
+
+// Launchers (fwg_kernels.hip).
+hipError_t launch_valu_step(const StepArgs &a, int rpw, size_t lds_bytes, hipStream_t s);
+hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K, int N, int C, hipStream_t s);
+hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
+hipError_t launch_fill_i32(int32_t *dst, int32_t value, int n, hipStream_t s);
+hipError_t launch_copy_bias(const float *src, float *dst, int n, hipStream_t s);
+hipError_t set_valu_lds_limit(size_t bytes);
+
+// Repack modes: how W^T[k][n] is read from the caller's PyTorch layout.
+enum RepackMode {
+  REPACK_LINEAR = 0,  // src [N][K] (out, in)
+  REPACK_CONV = 1,    // src [N][C][2]; k < C -> tap 0 (x_{t-d}), k >= C -> tap 1 (x_t); K = 2C
+  REPACK_EMBED = 2    // src [C][Q] -> dst [Q][C] row gather table (K = Q rows, N = C)
+};
+
+}  // namespace fwg

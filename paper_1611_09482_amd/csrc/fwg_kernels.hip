@@ -1,0 +1,410 @@
+// HIP kernels of the Fast Wavenet generation library, written for gfx950.
+//
+// This file holds the general ("VALU") step-kernel family and the small
+// utility kernels (weight repacking, fills).  One launch runs n_steps whole
+// generation steps for a block of `RPW` independent streams: every step pops
+// each layer's queue, runs the generation model (one step of a multi-layer
+// RNN, paper Section 2.2, Fig. 4), pushes the new states, computes the output
+// distribution and samples the next input (fed back, Section 1).
+//
+// Layout decisions:
+//   * queues: one ring buffer per layer, ring_l[slot][stream][channel] with the
+//     channel index contiguous, slot = t mod d_l (Section 2.1: depth = dilation);
+//     popping reads the slot written d_l steps earlier, pushing overwrites it
+//     after every lane has read it (pop before push, Section 2.2);
+//   * weights: streamed from L2 in a 16-byte K-blocked layout, so consecutive
+//     lanes read consecutive 16-byte chunks;
+//   * activations of the block's streams: LDS, float32.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fwg_internal.h"
+
+namespace fwg {
+
+// ---------------------------------------------------------------------------
+// bf16 helpers (operands are bf16 bit patterns in uint16 storage)
+__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
+// round to the nearest bf16 value (ties to even), returned as float
+__device__ __forceinline__ float round_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return __uint_as_float(u & 0xffff0000u);
+}
+__device__ __forceinline__ uint16_t to_bf16_bits(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename WT> struct WTraits;
+template <> struct WTraits<float> {
+  static constexpr int KB = 4;
+  __device__ static __forceinline__ void unpack(const uint4 &v, float *w) {
+    w[0] = __uint_as_float(v.x); w[1] = __uint_as_float(v.y);
+    w[2] = __uint_as_float(v.z); w[3] = __uint_as_float(v.w);
+  }
+  __device__ static __forceinline__ float load1(const void *p, long long i) { return ((const float *)p)[i]; }
+  __device__ static __forceinline__ void store1(void *p, long long i, float v) { ((float *)p)[i] = v; }
+  __device__ static __forceinline__ float opnd(float x) { return x; }
+};
+template <> struct WTraits<uint16_t> {
+  static constexpr int KB = 8;
+  __device__ static __forceinline__ void unpack(const uint4 &v, float *w) {
+    w[0] = bf16_lo(v.x); w[1] = bf16_hi(v.x); w[2] = bf16_lo(v.y); w[3] = bf16_hi(v.y);
+    w[4] = bf16_lo(v.z); w[5] = bf16_hi(v.z); w[6] = bf16_lo(v.w); w[7] = bf16_hi(v.w);
+  }
+  __device__ static __forceinline__ float load1(const void *p, long long i) {
+    return __uint_as_float(((uint32_t)((const uint16_t *)p)[i]) << 16);
+  }
+  __device__ static __forceinline__ void store1(void *p, long long i, float v) { ((uint16_t *)p)[i] = to_bf16_bits(v); }
+  __device__ static __forceinline__ float opnd(float x) { return round_bf16(x); }
+};
+
+// ---------------------------------------------------------------------------
+// Row-block product: part[kg][r][n] = sum over this K-group of W^T[k][n] * A(r, k)
+// for r < RPW.  A(r, k) = A0[r*lda + k] for k < ksplit, else A1[r*lda + k - ksplit].
+// N >= 256: each thread owns columns tid, tid+256, ... over all of K (one group).
+// N < 256 : 256/N K-groups of N threads each.
+template <typename WT, int RPW>
+__device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K, int N, const float *A0,
+                                             const float *A1, int lda, int ksplit, float *part) {
+  constexpr int KB = WTraits<WT>::KB;
+  const uint4 *W = (const uint4 *)Wp;
+  const int tid = threadIdx.x;
+  const int nkb = K / KB;
+  if (N >= kThreads) {
+    for (int n = tid; n < N; n += kThreads) {
+      float acc[RPW];
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) acc[r] = 0.f;
+#pragma unroll 4
+      for (int kb = 0; kb < nkb; ++kb) {
+        float w[KB];
+        WTraits<WT>::unpack(W[(long long)kb * N + n], w);
+        const int k0 = kb * KB;
+        const float *A = k0 < ksplit ? A0 + k0 : A1 + (k0 - ksplit);
+#pragma unroll
+        for (int r = 0; r < RPW; ++r) {
+#pragma unroll
+          for (int j = 0; j < KB; ++j) acc[r] = fmaf(w[j], A[r * lda + j], acc[r]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) part[r * N + n] = acc[r];
+    }
+  } else {
+    const int KG = kThreads / N;
+    const int n = tid % N, kg = tid / N;
+    const int per = nkb / KG;
+    float acc[RPW];
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) acc[r] = 0.f;
+#pragma unroll 4
+    for (int i = 0; i < per; ++i) {
+      const int kb = kg * per + i;
+      float w[KB];
+      WTraits<WT>::unpack(W[(long long)kb * N + n], w);
+      const int k0 = kb * KB;
+      const float *A = k0 < ksplit ? A0 + k0 : A1 + (k0 - ksplit);
+#pragma unroll
+      for (int r = 0; r < RPW; ++r) {
+#pragma unroll
+        for (int j = 0; j < KB; ++j) acc[r] = fmaf(w[j], A[r * lda + j], acc[r]);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < RPW; ++r) part[(kg * RPW + r) * N + n] = acc[r];
+  }
+}
+
+// Sum of the K-group partials of output (r, n).
+template <int RPW>
+__device__ __forceinline__ float part_sum(const float *part, int N, int r, int n) {
+  const int KG = N >= kThreads ? 1 : kThreads / N;
+  float s = 0.f;
+  for (int kg = 0; kg < KG; ++kg) s += part[(kg * RPW + r) * N + n];
+  return s;
+}
+
+__device__ __forceinline__ float bias_or0(const float *b, int i) { return b ? b[i] : 0.f; }
+
+// ---------------------------------------------------------------------------
+// Inverse-CDF sampling of one row of 256 logits by one wavefront: 4 classes per
+// lane, wave max, exp, per-lane running sums, wave-wide exclusive scan, and the
+// first class whose running sum exceeds u * Z (else the last class).
+__device__ __forceinline__ int sample_row_256(const float *lg, float u) {
+  const int lane = threadIdx.x & 63;
+  const float4 l4 = *(const float4 *)(lg + 4 * lane);
+  float m = fmaxf(fmaxf(l4.x, l4.y), fmaxf(l4.z, l4.w));
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  const float e0 = __expf(l4.x - m), e1 = __expf(l4.y - m), e2 = __expf(l4.z - m), e3 = __expf(l4.w - m);
+  const float c0 = e0, c1 = c0 + e1, c2 = c1 + e2, c3 = c2 + e3;
+  float incl = c3;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float v = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += v;
+  }
+  float excl = __shfl_up(incl, 1, 64);
+  if (lane == 0) excl = 0.f;
+  const float Z = __shfl(excl + c3, 63, 64);
+  const float target = u * Z;
+  int first = 4;
+  if (target < excl + c3) first = 3;
+  if (target < excl + c2) first = 2;
+  if (target < excl + c1) first = 1;
+  if (target < excl + c0) first = 0;
+  const unsigned long long hit = __ballot(first < 4);
+  if (hit == 0ull) return 255;
+  const int src = __ffsll((long long)hit) - 1;
+  return 4 * src + __shfl(first, src, 64);
+}
+
+// ---------------------------------------------------------------------------
+// The general step kernel.  Block = RPW streams, 256 threads.
+template <typename WT, int RPW>
+__global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
+  extern __shared__ float4 lds_raw[];
+  float *lds = (float *)lds_raw;
+  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW);
+  float *xf = lds + lay.xf, *xo = lds + lay.xo, *vo = lds + lay.vo, *ao = lds + lay.ao;
+  float *zo = lds + lay.zo, *so = lds + lay.so, *ho = lds + lay.ho, *h2 = lds + lay.h2;
+  float *lg = lds + lay.lg, *partA = lds + lay.partA, *partB = lds + lay.partB;
+  int *slots = (int *)(lds + lay.slots);
+  int *ins = (int *)(lds + lay.ins);
+
+  const int tid = threadIdx.x;
+  const int C = a.C, S = a.S, H = a.H, Q = a.Q, L = a.L;
+  const int Co = a.kind == 2 ? 2 * C : C;
+  const int b0 = blockIdx.x * RPW;
+  const int nrows = min(RPW, a.batch - b0);
+  if (nrows <= 0) return;
+
+  for (int l = tid; l < L; l += kThreads) slots[l] = (int)(a.t0 % (long long)a.layers[l].dil);
+  if (tid < RPW) ins[tid] = (!a.forced && tid < nrows) ? a.last[b0 + tid] : 0;
+  __syncthreads();
+
+  for (int s = 0; s < a.n_steps; ++s) {
+    // ---- current input (h^0_e): previous sample, or the forced sequence
+    if (a.forced && tid < nrows) ins[tid] = a.inputs[(long long)(b0 + tid) * a.n_steps + s];
+    __syncthreads();
+    // ---- embedding: a row gather of the transposed 1x1 convolution
+    for (int i = tid; i < RPW * C; i += kThreads) {
+      const int r = i / C, c = i % C;
+      const float v = WTraits<WT>::load1(a.embed, (long long)ins[r] * C + c) + bias_or0(a.embed_b, c);
+      xf[i] = v;
+      xo[i] = WTraits<WT>::opnd(v);
+    }
+    if (a.kind == 2)
+      for (int i = tid; i < RPW * S; i += kThreads) so[i] = 0.f;
+    __syncthreads();
+
+    for (int l = 0; l < L; ++l) {
+      const LayerDev ld = a.layers[l];
+      const long long qbase = ld.ring_off + (long long)slots[l] * a.bmax * C;
+      // ---- pop phase: the state pushed d_l steps ago (zeros before that)
+      for (int i = tid; i < RPW * C; i += kThreads) {
+        const int r = i / C, c = i % C;
+        vo[i] = r < nrows ? WTraits<WT>::load1(a.ring, qbase + (long long)(b0 + r) * C + c) : 0.f;
+      }
+      __syncthreads();
+      // ---- push phase for this queue: the layer's input x^{l-1}_t replaces the popped slot
+      for (int i = tid; i < RPW * C; i += kThreads) {
+        const int r = i / C, c = i % C;
+        if (r < nrows) WTraits<WT>::store1(a.ring, qbase + (long long)(b0 + r) * C + c, xo[i]);
+      }
+      // ---- dilated width-2 convolution: [v x] . [W_r ; W_e]
+      rows_product<WT, RPW>(ld.conv, 2 * C, Co, vo, xo, C, C, partA);
+      __syncthreads();
+      if (a.kind == 2) {
+        // gate: z = tanh(a[0:R]) * sigmoid(a[R:2R])
+        for (int i = tid; i < RPW * C; i += kThreads) {
+          const int r = i / C, c = i % C;
+          const float af = bias_or0(ld.conv_b, c) + part_sum<RPW>(partA, Co, r, c);
+          const float ag = bias_or0(ld.conv_b, C + c) + part_sum<RPW>(partA, Co, r, C + c);
+          const float z = tanhf(af) * (1.f / (1.f + __expf(-ag)));
+          zo[i] = WTraits<WT>::opnd(z);
+        }
+        __syncthreads();
+        // residual and skip 1x1 products
+        rows_product<WT, RPW>(ld.res, C, C, zo, zo, C, C, partB);
+        rows_product<WT, RPW>(ld.skip, C, S, zo, zo, C, C, partA);
+        __syncthreads();
+        for (int i = tid; i < RPW * C; i += kThreads) {
+          const int r = i / C, c = i % C;
+          const float v = xf[i] + bias_or0(ld.res_b, c) + part_sum<RPW>(partB, C, r, c);
+          xf[i] = v;
+          xo[i] = WTraits<WT>::opnd(v);
+        }
+        for (int i = tid; i < RPW * S; i += kThreads) {
+          const int r = i / S, k = i % S;
+          so[i] += bias_or0(ld.skip_b, k) + part_sum<RPW>(partA, S, r, k);
+        }
+      } else {
+        for (int i = tid; i < RPW * C; i += kThreads) {
+          const int r = i / C, c = i % C;
+          const float pre = bias_or0(ld.conv_b, c) + part_sum<RPW>(partA, Co, r, c);
+          const float v = (a.kind == 1 ? xf[i] : 0.f) + fmaxf(pre, 0.f);
+          xf[i] = v;
+          xo[i] = WTraits<WT>::opnd(v);
+        }
+      }
+      __syncthreads();
+    }
+
+    // ---- output head
+    const float *top = xo;
+    int Ktop = C;
+    if (a.kind == 2) {
+      for (int i = tid; i < RPW * S; i += kThreads) ho[i] = WTraits<WT>::opnd(fmaxf(so[i], 0.f));
+      __syncthreads();
+      rows_product<WT, RPW>(a.head, S, H, ho, ho, S, S, partA);
+      __syncthreads();
+      for (int i = tid; i < RPW * H; i += kThreads) {
+        const int r = i / H, n = i % H;
+        h2[i] = WTraits<WT>::opnd(fmaxf(bias_or0(a.head_b, n) + part_sum<RPW>(partA, H, r, n), 0.f));
+      }
+      __syncthreads();
+      top = h2;
+      Ktop = H;
+    }
+    rows_product<WT, RPW>(a.out, Ktop, Q, top, top, Ktop, Ktop, partA);
+    __syncthreads();
+    for (int i = tid; i < RPW * Q; i += kThreads) {
+      const int r = i / Q, q = i % Q;
+      lg[i] = bias_or0(a.out_b, q) + part_sum<RPW>(partA, Q, r, q);
+    }
+    __syncthreads();
+
+    if (a.forced) {
+      for (int i = tid; i < nrows * Q; i += kThreads) {
+        const int r = i / Q, q = i % Q;
+        a.logits[((long long)(b0 + r) * a.n_steps + s) * Q + q] = lg[i];
+      }
+    } else {
+      // ---- sample and feed back
+      const int w = tid >> 6;
+      for (int r = w; r < nrows; r += kThreads / 64) {
+        const float u = a.uniforms[(long long)(b0 + r) * a.n_steps + s];
+        const int k = sample_row_256(lg + r * Q, u);
+        if ((tid & 63) == 0) {
+          a.samples[(long long)(b0 + r) * a.n_steps + s] = k;
+          ins[r] = k;
+        }
+      }
+    }
+    // ---- advance every queue's slot
+    for (int l = tid; l < L; l += kThreads) {
+      const int nx = slots[l] + 1;
+      slots[l] = nx == a.layers[l].dil ? 0 : nx;
+    }
+    __syncthreads();
+  }
+  if (!a.forced && tid < nrows) a.last[b0 + tid] = ins[tid];
+}
+
+template <typename WT>
+static hipError_t launch_valu_t(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
+  const dim3 grid((a.batch + rpw - 1) / rpw), block(kThreads);
+  switch (rpw) {
+    case 1: hipLaunchKernelGGL((valu_step_kernel<WT, 1>), grid, block, lds, s, a); break;
+    case 2: hipLaunchKernelGGL((valu_step_kernel<WT, 2>), grid, block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL((valu_step_kernel<WT, 4>), grid, block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL((valu_step_kernel<WT, 8>), grid, block, lds, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_valu_step(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
+  return a.dtype == 1 ? launch_valu_t<uint16_t>(a, rpw, lds, s) : launch_valu_t<float>(a, rpw, lds, s);
+}
+
+template <typename WT, int RPW>
+static hipError_t set_lds_one(size_t bytes) {
+  return hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW>,
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+
+hipError_t set_valu_lds_limit(size_t bytes) {
+  hipError_t e;
+  if ((e = set_lds_one<float, 1>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<float, 2>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<float, 4>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<float, 8>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<uint16_t, 1>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<uint16_t, 2>(bytes)) != hipSuccess) return e;
+  if ((e = set_lds_one<uint16_t, 4>(bytes)) != hipSuccess) return e;
+  return set_lds_one<uint16_t, 8>(bytes);
+}
+
+// ---------------------------------------------------------------------------
+// Weight repacking (once, at create): dst in the VALU K-blocked layout
+// Wp[kb][n][j] = W^T[kb*KB + j][n], or the embedding's row-gather table.
+template <typename T>
+__global__ void repack_kernel(const T *__restrict__ src, T *__restrict__ dst, int mode, int K, int N, int C, int KB) {
+  const long long total = (long long)K * N;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
+    if (mode == REPACK_EMBED) {
+      // dst [Q][C] from src [C][Q]; here K = Q, N = C
+      const long long q = i / N, c = i % N;
+      dst[i] = src[c * K + q];
+      continue;
+    }
+    const long long j = i % KB, rest = i / KB;
+    const long long n = rest % N, kb = rest / N;
+    const long long k = kb * KB + j;
+    long long si;
+    if (mode == REPACK_CONV) si = (n * C + (k % C)) * 2 + (k >= C ? 1 : 0);
+    else si = n * K + k;
+    dst[i] = src[si];
+  }
+}
+
+hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K, int N, int C, hipStream_t s) {
+  const long long total = (long long)K * N;
+  const int blocks = (int)((total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096);
+  if (dtype == 1)
+    hipLaunchKernelGGL(repack_kernel<uint16_t>, dim3(blocks), dim3(256), 0, s, (const uint16_t *)src,
+                       (uint16_t *)dst, mode, K, N, C, valu_kb_elems(1));
+  else
+    hipLaunchKernelGGL(repack_kernel<float>, dim3(blocks), dim3(256), 0, s, (const float *)src, (float *)dst,
+                       mode, K, N, C, valu_kb_elems(0));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Fills (used instead of memset nodes so the calls stay safe under stream capture).
+__global__ void fill_zero_kernel(uint4 *dst, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = make_uint4(0, 0, 0, 0);
+}
+__global__ void fill_i32_kernel(int32_t *dst, int32_t v, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) dst[i] = v;
+}
+__global__ void copy_bias_kernel(const float *src, float *dst, int n) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) dst[i] = src ? src[i] : 0.f;
+}
+
+hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s) {
+  const size_t n16 = bytes / 16;  // regions are 256-byte aligned and sized
+  if (n16 == 0) return hipSuccess;
+  const int blocks = (int)(n16 / 256 + 1 < 8192 ? n16 / 256 + 1 : 8192);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, (uint4 *)dst, n16);
+  return hipGetLastError();
+}
+hipError_t launch_fill_i32(int32_t *dst, int32_t v, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_i32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, dst, v, n);
+  return hipGetLastError();
+}
+hipError_t launch_copy_bias(const float *src, float *dst, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_bias_kernel, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n);
+  return hipGetLastError();
+}
+
+}  // namespace fwg

@@ -1,0 +1,117 @@
+"""The C-ABI library loads, exports what include/fwg.h declares, and rejects bad
+arguments on the host before touching a device (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1611_09482_amd import binding as B
+import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_1611_09482_amd import build
+    if build.is_stale():
+        build.build()
+    return B.load_library()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "fwg.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fwg_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _desc(**kw):
+    base = dict(kind=W.GATED, dtype=W.BF16, channels=64, dilations=(1, 2, 4), max_batch=8,
+                skip_channels=512, head_channels=512)
+    base.update(kw)
+    return B.make_desc(**base)
+
+
+def _rc_size(lib, d):
+    n = ctypes.c_size_t(0)
+    return lib.fwg_workspace_size(ctypes.byref(d), ctypes.byref(n)), n.value
+
+
+def test_workspace_size_for_every_workload(lib):
+    for name, wl in W.WORKLOADS.items():
+        m = wl.model
+        d = B.make_desc(m.kind, m.dtype, m.channels, m.dilations, wl.batch, m.skip_channels,
+                        m.head_channels, m.n_classes, m.seed_input)
+        rc, n = _rc_size(lib, d)
+        assert rc == B.FWG_OK, (name, lib.fwg_last_error())
+        es = 2 if m.dtype == W.BF16 else 4
+        queues = m.queue_total * wl.batch * m.channels * es
+        # two queue regions (generation, teacher-forced) plus weights
+        assert n >= 2 * queues + W.make_weights(m, 0).nbytes()
+        d2 = B.make_desc(m.kind, m.dtype, m.channels, m.dilations, 2 * wl.batch, m.skip_channels,
+                         m.head_channels, m.n_classes, m.seed_input)
+        assert _rc_size(lib, d2)[1] > n
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dilations=()), B.FWG_EINVAL),
+    (dict(dilations=(1, 0, 2)), B.FWG_EINVAL),
+    (dict(kind=7), B.FWG_EINVAL),
+    (dict(dtype=5), B.FWG_EINVAL),
+    (dict(max_batch=0), B.FWG_EINVAL),
+    (dict(seed_input=256), B.FWG_EINVAL),
+    (dict(seed_input=-1), B.FWG_EINVAL),
+    (dict(channels=0), B.FWG_EINVAL),
+    (dict(skip_channels=0), B.FWG_EINVAL),
+    (dict(n_classes=100, seed_input=5), B.FWG_EUNSUPPORTED),
+    (dict(channels=3), B.FWG_EUNSUPPORTED),
+    (dict(kind=W.RELU, dtype=W.F32, channels=6), B.FWG_EUNSUPPORTED),
+])
+def test_invalid_descriptors(lib, kw, code):
+    rc, _ = _rc_size(lib, _desc(**kw))
+    assert rc == code
+    assert lib.fwg_last_error().decode()
+
+
+def test_null_arguments(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.fwg_workspace_size(None, ctypes.byref(n)) == B.FWG_EINVAL
+    d = _desc()
+    assert lib.fwg_workspace_size(ctypes.byref(d), None) == B.FWG_EINVAL
+    h = ctypes.c_void_p(0)
+    w = B.fwg_weights()
+    assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), None, 0, None, ctypes.byref(h)) == B.FWG_EINVAL
+    assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), 1 << 20, 1 << 40, None, None) == B.FWG_EINVAL
+    assert lib.fwg_reset_queues(None) == B.FWG_EINVAL
+    assert lib.fwg_generate(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_teacher_forced(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_destroy(None) == B.FWG_OK
+    assert lib.fwg_regime(None) == b""
+
+
+def test_workspace_checks_precede_device_work(lib):
+    """Too small or misaligned workspaces are rejected before any HIP call (no device here)."""
+    d = _desc()
+    rc, need = _rc_size(lib, d)
+    assert rc == 0
+    w = B.fwg_weights()
+    h = ctypes.c_void_p(0)
+    fake = 1 << 30  # never dereferenced: the checks fail first
+    assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), fake, need - 1, None, ctypes.byref(h)) == B.FWG_ENOSPACE
+    assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), fake + 16, need, None, ctypes.byref(h)) == B.FWG_ENOSPACE
+    # missing weights with a large enough workspace: EINVAL, still before any HIP call
+    assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), fake, need, None, ctypes.byref(h)) == B.FWG_EINVAL
+    assert h.value is None
+
+
+def test_binding_raises_on_missing_library(tmp_path):
+    with pytest.raises(FileNotFoundError):
+        B.load_library(str(tmp_path / "nope.so"))

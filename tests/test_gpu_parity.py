@@ -1,0 +1,279 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bars (stated here, applied per test):
+  * teacher-forced logits, per (stream, step) row: max|gpu - oracle| / max(max|oracle|, 1e-6)
+    <= 1e-4 for float32 models and <= 2e-2 for bf16 models;
+  * sampled sequences equal the oracle's until the first step where the oracle's
+    sample sits within TAU of a CDF boundary (a near-tie: TAU = 1e-4 float32,
+    5e-2 bf16); the step is reported, and the divergence must be such a near-tie;
+  * every GPU sample, over the whole sequence, lies inside the oracle's CDF interval
+    (widened by TAU) of the distribution computed by teacher-forcing the oracle on the
+    GPU's own sequence;
+  * closed forms (delay line, uniform sampler) and state invariants are bit-exact.
+"""
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():  # pragma: no cover
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import oracle  # noqa: E402
+from paper_1611_09482_amd import binding  # noqa: E402
+
+TOL = {W.F32: 1e-4, W.BF16: 2e-2}
+TAU = {W.F32: 1e-4, W.BF16: 5e-2}
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def row_rel_err(g, o):
+    return np.abs(g - o).max(axis=-1) / np.maximum(np.abs(o).max(axis=-1), 1e-6)
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def cdf_bounds(lg_row, k):
+    c = oracle.cdf(lg_row)
+    return (c[k - 1] if k > 0 else 0.0), c[k]
+
+
+# Families: the four layer shapes of the workloads, with fewer layers for oracle-speed tests.
+FAMILIES = {
+    "relu_c32_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
+    "gated_r32_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
+    "gated_r64_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
+    "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
+}
+
+
+def build_pair(cfg, seed, max_batch, bias_scale=0.1):
+    w = W.make_weights(cfg, seed, bias_scale=bias_scale)
+    return w, binding.from_model(cfg, w, max_batch=max_batch), oracle.Oracle(w)
+
+
+def check_generation(cfg, fw, orc, u, batch, label):
+    """Sampled-sequence parity with near-tie accounting + whole-sequence admissibility."""
+    tau = TAU[cfg.dtype]
+    g = fw.generate(dev(u)).cpu().numpy()
+    so, lo_ = orc.state(batch).generate(u, return_logits=True)
+    n = u.shape[1]
+    first = []
+    for b in range(batch):
+        mism = np.nonzero(g[b] != so[b])[0]
+        t = int(mism[0]) if mism.size else n
+        first.append(t)
+        if t < n:
+            lo, hi = cdf_bounds(lo_[b, t], so[b, t])
+            margin = min(u[b, t] - lo, hi - u[b, t])
+            assert margin < tau, f"{label}: stream {b} diverges at step {t} with oracle margin {margin:.3e} >= {tau}"
+    log(f"{label}: first divergence step per stream (n={n}): min {min(first)}, median {int(np.median(first))}")
+    # admissibility over the whole sequence: teacher-force the oracle on the GPU's own samples
+    seq = np.concatenate([np.full((batch, 1), cfg.seed_input, np.int32), g[:, :-1]], axis=1)
+    olg = orc.teacher_forced(seq)
+    glg = fw.teacher_forced(dev(seq)).cpu().numpy()
+    err = row_rel_err(glg, olg)
+    assert err.max() <= TOL[cfg.dtype], f"{label}: teacher-forced logits on GPU sequence: {err.max():.3e}"
+    bad = 0
+    for b in range(batch):
+        for t in range(n):
+            lo, hi = cdf_bounds(olg[b, t], g[b, t])
+            bad += not (lo - tau <= u[b, t] < hi + tau)
+    assert bad == 0, f"{label}: {bad} inadmissible samples"
+    return g, first
+
+
+@pytest.mark.parametrize("fam", list(FAMILIES))
+def test_teacher_forced_parity(fam):
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5   # ragged: not a multiple of the rows per block
+    T = cfg.queue_total + 60              # wraps every queue
+    w, fw, orc = build_pair(cfg, 100, B)
+    x = W.sequences(3, B, T)
+    t0 = time.time()
+    g = fw.teacher_forced(dev(x)).cpu().numpy()
+    o = orc.teacher_forced(x)
+    err = row_rel_err(g, o)
+    log(f"{fam}: TF B={B} T={T} max row rel err {err.max():.3e} p99.9 {np.quantile(err, 0.999):.3e} "
+        f"({time.time() - t0:.1f}s)")
+    assert err.max() <= TOL[cfg.dtype]
+
+
+@pytest.mark.parametrize("fam", list(FAMILIES))
+def test_generation_parity(fam):
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5
+    n = cfg.queue_total + 60
+    w, fw, orc = build_pair(cfg, 101, B)
+    check_generation(cfg, fw, orc, W.uniforms(4, B, n), B, fam)
+
+
+def test_delay_line_closed_form_gpu():
+    """W_e = 0, W_r = I, ReLU, zero biases, embeddings >= 0: logits[0:C] = x^0_{t - sum d} exactly,
+    through every queue depth up to 512 (pop before push, slot wrap-around)."""
+    C = 32
+    dil = tuple(2 ** i for i in range(10))
+    cfg = W.ModelConfig(W.RELU, W.F32, C, dil)
+    w = W.make_weights(cfg, 0)
+    w.embed[:] = np.array([[(q * 7 + c) % 97 for q in range(256)] for c in range(C)], np.float32)
+    for l in range(cfg.n_layers):
+        w.conv[l][:] = 0
+        w.conv[l][np.arange(C), np.arange(C), 0] = 1.0
+    w.out[:] = 0
+    w.out[np.arange(C), np.arange(C)] = 1.0
+    fw = binding.from_model(cfg, w, max_batch=3)
+    D = sum(dil)
+    T = D + 100
+    x = W.sequences(8, 3, T)
+    g = fw.teacher_forced(dev(x)).cpu().numpy()
+    want = np.zeros((3, T, C), np.float32)
+    want[:, D:, :] = w.embed[:, x[:, :T - D]].transpose(1, 2, 0)
+    assert np.array_equal(g[:, :, :C], want)
+    assert np.array_equal(g[:, :, C:], np.zeros_like(g[:, :, C:]))
+
+
+def test_uniform_logits_sampler_gpu():
+    """All-equal logits: the sample is floor(256 u), bit-exact."""
+    cfg = FAMILIES["gated_r64_bf16"]
+    w = W.make_weights(cfg, 5, bias_scale=0.1)
+    w.out[:] = 0
+    w.out_b[:] = 0
+    B, n = 16, 400
+    fw = binding.from_model(cfg, w, max_batch=B)
+    u = W.uniforms(9, B, n)
+    u[0, :6] = [0.0, 0.5, 1 - 2 ** -24, 3 / 256, 3 / 256 - 2 ** -24, 255 / 256]
+    g = fw.generate(dev(u)).cpu().numpy()
+    assert np.array_equal(g, np.floor(u.astype(np.float64) * 256).astype(np.int32))
+
+
+def test_continuation_reset_and_determinism_gpu():
+    cfg = FAMILIES["gated_r32_f32"]
+    w, fw, _ = build_pair(cfg, 7, 9)
+    u = W.uniforms(10, 9, 700)
+    full = fw.generate(dev(u)).cpu().numpy()
+    fw.reset()
+    a = fw.generate(dev(u[:, :257].copy())).cpu().numpy()
+    # a teacher-forced call in between uses its own queues and leaves the state alone
+    fw.teacher_forced(dev(W.sequences(2, 4, 300)))
+    b = fw.generate(dev(u[:, 257:].copy())).cpu().numpy()
+    assert np.array_equal(np.concatenate([a, b], axis=1), full)
+    fw.reset()
+    assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), full)
+
+
+def test_streams_independent_gpu():
+    cfg = FAMILIES["gated_r64_bf16"]
+    w, fw, _ = build_pair(cfg, 8, 13)
+    u = W.uniforms(11, 13, 300)
+    together = fw.generate(dev(u)).cpu().numpy()
+    for b in [0, 7, 12]:
+        one = binding.from_model(cfg, w, max_batch=1)
+        alone = one.generate(dev(u[b:b + 1].copy())).cpu().numpy()
+        assert np.array_equal(alone[0], together[b]), b
+
+
+def test_batch_binding_and_errors_gpu():
+    cfg = FAMILIES["relu_c32_f32"]
+    w, fw, _ = build_pair(cfg, 9, 6)
+    fw.generate(dev(W.uniforms(1, 4, 10)))
+    with pytest.raises(binding.FwgError) as e:
+        fw.generate(dev(W.uniforms(1, 3, 10)))
+    assert e.value.code == binding.FWG_ESTATE
+    with pytest.raises(binding.FwgError) as e:
+        fw.generate(dev(W.uniforms(1, 7, 10)))
+    assert e.value.code == binding.FWG_EINVAL
+    fw.reset()
+    fw.generate(dev(W.uniforms(1, 3, 10)))
+    empty = fw.generate(dev(np.zeros((3, 0), np.float32)))
+    assert empty.shape == (3, 0)
+    assert fw.regime
+
+
+# ------------------------------------------------------------------ full workload sizes
+def _full(name):
+    wl = W.WORKLOADS[name]
+    w = W.make_weights(wl.model, wl.weight_seed)
+    return wl, w, binding.from_model(wl.model, w, max_batch=wl.batch), oracle.Oracle(w)
+
+
+def _check_streams_on_gpu_sequence(wl, fw, orc, u, g, streams, steps):
+    """Oracle teacher-forced on the GPU's sequences of selected streams: logits parity
+    and admissibility of every sample (sampled outputs of a full-size run)."""
+    cfg = wl.model
+    tau = TAU[cfg.dtype]
+    seq = np.concatenate([np.full((g.shape[0], 1), cfg.seed_input, np.int32), g[:, :-1]], axis=1)
+    sel = seq[streams, :steps]
+    t0 = time.time()
+    olg = orc.teacher_forced(sel)
+    glg = fw.teacher_forced(dev(sel)).cpu().numpy()
+    err = row_rel_err(glg, olg)
+    bad = 0
+    for i, b in enumerate(streams):
+        for t in range(steps):
+            lo, hi = cdf_bounds(olg[i, t], g[b, t])
+            bad += not (lo - tau <= u[b, t] < hi + tau)
+    log(f"{wl.name}: streams {streams} x {steps} steps: TF rel err {err.max():.3e}, "
+        f"inadmissible {bad} ({time.time() - t0:.1f}s)")
+    assert err.max() <= TOL[cfg.dtype]
+    assert bad == 0
+
+
+def test_full_toy_relu():
+    wl, w, fw, orc = _full("toy_relu_c32_l5_b1")
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    check_generation(wl.model, fw, orc, u, wl.batch, wl.name)
+
+
+def test_full_gated_b1():
+    wl, w, fw, orc = _full("gated_r32_s256_l20_b1")
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    check_generation(wl.model, fw, orc, u, wl.batch, wl.name)
+
+
+def test_full_gated_b64():
+    wl, w, fw, orc = _full("gated_r32_s256_l20_b64")
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    g = fw.generate(dev(u)).cpu().numpy()
+    assert g.min() >= 0 and g.max() <= 255
+    _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 63], wl.n_steps)
+    # teacher-forced pass on the seeded random sequence, sampled streams
+    x = W.sequences(wl.uniform_seed, wl.batch, wl.n_steps)
+    glg = fw.teacher_forced(dev(x))
+    sel = [5, 40]
+    o = orc.teacher_forced(x[sel])
+    err = row_rel_err(glg[sel].cpu().numpy(), o)
+    log(f"{wl.name}: teacher-forced seeded sequence, streams {sel}: max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[wl.model.dtype]
+
+
+def test_full_bench_workload():
+    """The benchmark workload at full size, in the benchmark's launch configuration."""
+    wl, w, fw, orc = _full(W.BENCH_WORKLOAD)
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    t0 = time.time()
+    g = fw.generate(dev(u)).cpu().numpy()
+    log(f"{wl.name}: GPU generation {wl.batch}x{wl.n_steps} in {time.time() - t0:.1f}s")
+    assert g.min() >= 0 and g.max() <= 255
+    _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 255], wl.n_steps)
+
+
+def test_full_bytenet():
+    wl, w, fw, orc = _full("bytenet_relu_res_c512_l25_b32")
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    g = fw.generate(dev(u)).cpu().numpy()
+    assert g.min() >= 0 and g.max() <= 255
+    _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [31], 640)
