@@ -1,0 +1,187 @@
+#!/usr/bin/env python3
+"""Throughput of Fast Wavenet cached generation on one MI355X.
+
+One "step" is one generation step of the whole batch: every stream pops its
+queues, runs all layers, the head, the softmax and the inverse-CDF sample, and
+pushes its new states.  The timed region is one fwg_generate call of --steps
+steps (a single persistent kernel launch), bracketed by device synchronisation
+and HIP events recorded on the launch stream, with inputs resident in HBM.
+
+Prints one JSON line (see the design doc for the field definitions).
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "generated samples/sec (batch x steps/s) + % HBM/MFMA roofline per config"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+HBM_PEAK_GBS = 8000.0
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1611_09482_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str, steps: int):
+    """HBM bytes per launch from committed rocprofv3 counter passes, if they were taken on the
+    current kernel sources and the same launch size; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_digest") != kernel_source_digest() or rec.get("steps") != steps:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(wl, weights, u, target_seconds: float):
+    """The oracle as it stands, on this host's cores, on a bounded sample of the workload:
+    the first streams (one per thread) for as many leading steps as fit the time budget."""
+    import oracle
+    threads = oracle.max_threads()
+    streams = max(1, min(wl.batch, threads))
+    o = oracle.Oracle(weights)
+    calib = 4
+    st = o.state(streams)
+    t0 = time.perf_counter()
+    st.generate(u[:streams, :calib].copy())
+    per_step = (time.perf_counter() - t0) / calib
+    steps = int(max(8, min(wl.n_steps - calib, target_seconds / max(per_step, 1e-9))))
+    t0 = time.perf_counter()
+    st.generate(u[:streams, calib:calib + steps].copy())
+    dt = time.perf_counter() - t0
+    return {"value": streams * steps / dt, "unit": "samples/s", "cores": min(threads, streams),
+            "kind": "oracle",
+            "sample": f"float64 CPU oracle generating streams 0..{streams - 1} of the {wl.batch}-stream workload "
+                      f"for steps {calib}..{calib + steps - 1} of {wl.n_steps} (per-step cost is constant), "
+                      f"OpenMP over streams, {dt:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="generation steps timed (default: the workload's)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed warm-up steps (default: same as --steps)")
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-time budget of the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device copy (counter calibration for rocprofv3)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: streams are independent and the path uses no collectives, so "
+              f"--gpus {args.gpus} (WORLD_SIZE={world}) is not supported; run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as W
+    from paper_1611_09482_amd import binding
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "launches": 3}))
+        return
+
+    name = args.workload or W.BENCH_WORKLOAD
+    wl = W.WORKLOADS[name]
+    cfg = wl.model
+    K = args.steps if args.steps is not None else wl.n_steps
+    Wu = args.warmup if args.warmup is not None else K
+    B = wl.batch
+
+    weights = W.make_weights(cfg, wl.weight_seed)
+    u_host = W.uniforms(wl.uniform_seed, B, max(K, Wu, 1))
+    u_timed = torch.from_numpy(np.ascontiguousarray(u_host[:, :K])).cuda()
+    u_warm = torch.from_numpy(np.ascontiguousarray(u_host[:, :Wu])).cuda()
+    stream = torch.cuda.current_stream()
+    fw = binding.from_model(cfg, weights, max_batch=B, stream=stream)
+    out = torch.empty((B, K), dtype=torch.int32, device="cuda")
+
+    if Wu > 0:
+        fw.generate(u_warm)
+    torch.cuda.synchronize()
+    fw.reset()
+    torch.cuda.synchronize()
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    e0.record(stream)
+    fw.generate(u_timed, out=out)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1)
+    sec = ms / 1e3
+
+    dtype = "bf16" if cfg.dtype == W.BF16 else "f32"
+    samples = B * K
+    flops = float(cfg.flops_per_sample()) * samples
+    achieved = flops / sec / 1e12 if sec > 0 else 0.0
+    peak = PEAK_TFLOPS[dtype]
+    traffic = stored_traffic(name, K)
+
+    result = {
+        "metric": METRIC,
+        "value": samples / sec if sec > 0 else 0.0,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wu,
+        "ms_per_step": ms / max(K, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": name,
+            "description": wl.description,
+            "batch": B,
+            "steps_per_launch": K,
+            "regime": fw.regime,
+        },
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": achieved / peak,
+            "traffic": traffic,
+            "algorithmic_flops_per_launch": flops,
+            "launch_ms": ms,
+        },
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, weights, u_host, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -5,6 +5,7 @@
 
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <new>
@@ -38,6 +39,9 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
 struct Plan {
   int kind, dtype, Q, C, S, H, L, bmax, seed_input, Co, es, rpw;
+  int regime;
+  int brows;              // queue rows per slot (max_batch, padded to whole blocks for the MFMA family)
+  size_t off_frags, off_embT, off_bias, off_ptrtab;
   long long queue_elems;  // sum(d_l) * bmax * C
   size_t off_layers, off_embed, off_embed_b, off_head, off_head_b, off_out, off_out_b;
   std::vector<size_t> off_conv, off_conv_b, off_res, off_res_b, off_skip, off_skip_b;
@@ -109,10 +113,26 @@ int make_plan(const fwg_desc *d, Plan *p) {
   if (p->lds_bytes > 160 * 1024) return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS");
   p->rpw = rpw;
 
+  // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512
+  p->regime = REGIME_VALU;
+  const char *force = getenv("FWG_REGIME");
+  const bool mfma_shape = p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR && p->S == kMfS &&
+                          p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
+                          mfma_lds_bytes(p->L) <= 160 * 1024;
+  if (mfma_shape && !(force && strcmp(force, "valu") == 0)) p->regime = REGIME_MFMA;
+  p->brows = p->regime == REGIME_MFMA ? (p->bmax + kMfRows - 1) / kMfRows * kMfRows : p->bmax;
+
   // workspace layout
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t at = off; off = align_up(off + bytes); return at; };
   p->off_layers = take(sizeof(LayerDev) * p->L);
+  p->off_frags = p->off_embT = p->off_bias = p->off_ptrtab = 0;
+  if (p->regime == REGIME_MFMA) {
+    p->off_frags = take(mfma_frag_bytes(p->L));
+    p->off_embT = take((size_t)p->Q * p->C * 2);
+    p->off_bias = take(sizeof(float) * mfma_bias_floats(p->L));
+    p->off_ptrtab = take(sizeof(void *) * 3 * p->L);
+  }
   p->off_embed = take((size_t)p->Q * p->C * p->es);
   p->off_embed_b = take(sizeof(float) * p->C);
   p->off_conv.resize(p->L); p->off_conv_b.resize(p->L);
@@ -136,7 +156,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   long long acc = 0;
   for (int l = 0; l < p->L; ++l) {
     p->ring_off[l] = acc;
-    acc += (long long)d->dilations[l] * p->bmax * p->C;
+    acc += (long long)d->dilations[l] * p->brows * p->C;
   }
   p->queue_elems = acc;
   (void)dsum;
@@ -181,7 +201,12 @@ StepArgs base_args(const fwg_handle *h) {
   a.out = h->ws + p.off_out;
   a.out_b = (const float *)(h->ws + p.off_out_b);
   a.last = (int32_t *)(h->ws + p.off_last);
-  a.bmax = p.bmax;
+  a.bmax = p.brows;
+  if (p.regime == REGIME_MFMA) {
+    a.mf_frags = h->ws + p.off_frags;
+    a.mf_embT = h->ws + p.off_embT;
+    a.mf_bias = (const float *)(h->ws + p.off_bias);
+  }
   a.kind = p.kind;
   a.dtype = p.dtype;
   a.C = p.C;
@@ -277,6 +302,26 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_repack(w->out, ws + p.off_out, REPACK_LINEAR, dt, Kout, p.Q, C, s));
   TRY_OR_FREE(launch_copy_bias(w->out_b, (float *)(ws + p.off_out_b), p.Q, s));
   TRY_OR_FREE(hipMemcpyAsync(ws + p.off_layers, table.data(), sizeof(LayerDev) * p.L, hipMemcpyHostToDevice, s));
+  std::vector<const void *> ptrs;
+  if (p.regime == REGIME_MFMA) {
+    char *frags = ws + p.off_frags;
+    const size_t layer_bytes = (size_t)4 * kMfFragsLayer * 1024;
+    for (int l = 0; l < p.L; ++l)
+      TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], frags + l * layer_bytes, s));
+    TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, frags + p.L * layer_bytes, s));
+    TRY_OR_FREE(launch_mfma_embed_table(w->embed, ws + p.off_embT, s));
+    ptrs.resize(3 * p.L, nullptr);
+    for (int l = 0; l < p.L; ++l) {
+      ptrs[l] = w->conv_b ? w->conv_b[l] : nullptr;
+      ptrs[p.L + l] = w->res_b ? w->res_b[l] : nullptr;
+      ptrs[2 * p.L + l] = w->skip_b ? w->skip_b[l] : nullptr;
+    }
+    TRY_OR_FREE(hipMemcpyAsync(ws + p.off_ptrtab, ptrs.data(), sizeof(void *) * 3 * p.L, hipMemcpyHostToDevice, s));
+    const float *const *pt = (const float *const *)(ws + p.off_ptrtab);
+    TRY_OR_FREE(launch_mfma_bias_block(pt, pt + p.L, pt + 2 * p.L, w->head_b, w->out_b, w->embed_b, p.L,
+                                       (float *)(ws + p.off_bias), s));
+    TRY_OR_FREE(set_mfma_lds_limit(mfma_lds_bytes(p.L)));
+  }
   if (p.lds_bytes > 64 * 1024) TRY_OR_FREE(set_valu_lds_limit(p.lds_bytes));
   int rr = enqueue_reset(h);
   if (rr != FWG_OK) return cleanup_fail(rr);
@@ -309,7 +354,7 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
   a.n_steps = n_steps;
   a.batch = batch;
   a.forced = 0;
-  HIP_TRY(launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
   h->bound_batch = batch;
   h->t += n_steps;
   return FWG_OK;
@@ -331,7 +376,7 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
   a.n_steps = seq_len;
   a.batch = batch;
   a.forced = 1;
-  HIP_TRY(launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
   return FWG_OK;
 }
 
@@ -340,6 +385,9 @@ int fwg_destroy(fwg_handle *h) {
   return FWG_OK;
 }
 
-const char *fwg_regime(const fwg_handle *h) { return h ? "valu" : ""; }
+const char *fwg_regime(const fwg_handle *h) {
+  if (!h) return "";
+  return h->plan.regime == REGIME_MFMA ? "mfma_bf16_r64_s512" : "valu";
+}
 
 }  // extern "C"

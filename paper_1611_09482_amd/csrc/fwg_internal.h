@@ -42,10 +42,26 @@ struct StepArgs {
   int n_steps, batch, bmax;
   int kind, dtype, C, S, H, Q, L;
   int forced;              // 1: teacher-forced mode
+  // MFMA family only
+  const void *mf_frags;    // per-wave packed weight fragment streams
+  const void *mf_embT;     // embedding table [Q][R] (bf16)
+  const float *mf_bias;    // bias block: conv [L][2R], res [L][R], skip sum [S], head [H], out [Q], embed [R]
 };
 
 // Kernel families.
-enum Regime { REGIME_VALU = 0 };
+enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1 };
+
+// MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
+// 16 streams per block, weight fragments per wave and stage.
+constexpr int kMfR = 64, kMfS = 512, kMfH = 512, kMfRows = 16;
+constexpr int kMfFragsLayer = 26;  // conv 8 + residual 2 + skip 16
+constexpr int kMfFragsHead = 16;
+constexpr int kMfH1Chunks = 8, kMfOutChunks = 4;
+constexpr int kMfMaxLayers = 128;
+inline size_t mfma_frag_bytes(int L) {
+  return (size_t)4 * 1024 * ((size_t)L * kMfFragsLayer + (size_t)(kMfH1Chunks + kMfOutChunks) * kMfFragsHead);
+}
+inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Packed-weight layout of the VALU family: W^T blocked by 16 bytes along K,
 // Wp[kb][n][kb_elems], with W^T[k][n] the weight from input k to output n.
@@ -91,6 +107,15 @@ hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
 hipError_t launch_fill_i32(int32_t *dst, int32_t value, int n, hipStream_t s);
 hipError_t launch_copy_bias(const float *src, float *dst, int n, hipStream_t s);
 hipError_t set_valu_lds_limit(size_t bytes);
+size_t mfma_lds_bytes(int L);
+hipError_t launch_mfma_step(const StepArgs &a, hipStream_t s);
+hipError_t set_mfma_lds_limit(size_t bytes);
+hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, void *dst, hipStream_t s);
+hipError_t launch_mfma_repack_head(const void *head, const void *out, void *dst, hipStream_t s);
+hipError_t launch_mfma_embed_table(const void *embed, void *dst, hipStream_t s);
+hipError_t launch_mfma_bias_block(const float *const *conv_b, const float *const *res_b, const float *const *skip_b,
+                                  const float *head_b, const float *out_b, const float *emb_b, int L, float *dst,
+                                  hipStream_t s);
 
 // Repack modes: how W^T[k][n] is read from the caller's PyTorch layout.
 enum RepackMode {

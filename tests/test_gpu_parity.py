@@ -57,13 +57,26 @@ FAMILIES = {
     "relu_c32_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
     "gated_r32_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
     "gated_r64_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
+    "gated_r64_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
+    "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
 }
+# families whose test forces the general (VALU) kernel family instead of the MFMA one
+FORCE_VALU = {"gated_r64_bf16_valu"}
 
 
-def build_pair(cfg, seed, max_batch, bias_scale=0.1):
+def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None):
     w = W.make_weights(cfg, seed, bias_scale=bias_scale)
-    return w, binding.from_model(cfg, w, max_batch=max_batch), oracle.Oracle(w)
+    if fam in FORCE_VALU:
+        os.environ["FWG_REGIME"] = "valu"
+    try:
+        fw = binding.from_model(cfg, w, max_batch=max_batch)
+    finally:
+        os.environ.pop("FWG_REGIME", None)
+    if fam is not None:
+        want_valu = fam in FORCE_VALU or cfg.dtype != W.BF16
+        assert (fw.regime == "valu") == want_valu, (fam, fw.regime)
+    return w, fw, oracle.Oracle(w)
 
 
 def check_generation(cfg, fw, orc, u, batch, label):
@@ -102,13 +115,13 @@ def test_teacher_forced_parity(fam):
     cfg = FAMILIES[fam]
     B = 11 if cfg.channels < 512 else 5   # ragged: not a multiple of the rows per block
     T = cfg.queue_total + 60              # wraps every queue
-    w, fw, orc = build_pair(cfg, 100, B)
+    w, fw, orc = build_pair(cfg, 100, B, fam=fam)
     x = W.sequences(3, B, T)
     t0 = time.time()
     g = fw.teacher_forced(dev(x)).cpu().numpy()
     o = orc.teacher_forced(x)
     err = row_rel_err(g, o)
-    log(f"{fam}: TF B={B} T={T} max row rel err {err.max():.3e} p99.9 {np.quantile(err, 0.999):.3e} "
+    log(f"{fam} [{fw.regime}]: TF B={B} T={T} max row rel err {err.max():.3e} p99.9 {np.quantile(err, 0.999):.3e} "
         f"({time.time() - t0:.1f}s)")
     assert err.max() <= TOL[cfg.dtype]
 
@@ -118,7 +131,7 @@ def test_generation_parity(fam):
     cfg = FAMILIES[fam]
     B = 11 if cfg.channels < 512 else 5
     n = cfg.queue_total + 60
-    w, fw, orc = build_pair(cfg, 101, B)
+    w, fw, orc = build_pair(cfg, 101, B, fam=fam)
     check_generation(cfg, fw, orc, W.uniforms(4, B, n), B, fam)
 
 
@@ -160,9 +173,10 @@ def test_uniform_logits_sampler_gpu():
     assert np.array_equal(g, np.floor(u.astype(np.float64) * 256).astype(np.int32))
 
 
-def test_continuation_reset_and_determinism_gpu():
-    cfg = FAMILIES["gated_r32_f32"]
-    w, fw, _ = build_pair(cfg, 7, 9)
+@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd"])
+def test_continuation_reset_and_determinism_gpu(fam):
+    cfg = FAMILIES[fam]
+    w, fw, _ = build_pair(cfg, 7, 9, fam=fam)
     u = W.uniforms(10, 9, 700)
     full = fw.generate(dev(u)).cpu().numpy()
     fw.reset()
