@@ -305,7 +305,7 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   std::vector<const void *> ptrs;
   if (p.regime == REGIME_MFMA) {
     char *frags = ws + p.off_frags;
-    const size_t layer_bytes = (size_t)4 * kMfFragsLayer * 1024;
+    const size_t layer_bytes = (size_t)4 * kMfFrags * 1024;
     for (int l = 0; l < p.L; ++l)
       TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], frags + l * layer_bytes, s));
     TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, frags + p.L * layer_bytes, s));

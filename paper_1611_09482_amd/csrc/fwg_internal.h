@@ -54,13 +54,10 @@ enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1 };
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
 // 16 streams per block, weight fragments per wave and stage.
 constexpr int kMfR = 64, kMfS = 512, kMfH = 512, kMfRows = 16;
-constexpr int kMfFragsLayer = 26;  // conv 8 + residual 2 + skip 16
-constexpr int kMfFragsHead = 16;
-constexpr int kMfH1Chunks = 8, kMfOutChunks = 4;
+constexpr int kMfFrags = 26;       // fragments per wave and stage: conv 8 + residual 2 + skip 16
+constexpr int kMfHeadStages = 8;   // head: 128 + 64 fragments per wave, padded to 8 stages of 26
 constexpr int kMfMaxLayers = 128;
-inline size_t mfma_frag_bytes(int L) {
-  return (size_t)4 * 1024 * ((size_t)L * kMfFragsLayer + (size_t)(kMfH1Chunks + kMfOutChunks) * kMfFragsHead);
-}
+__host__ __device__ inline size_t mfma_frag_bytes(int L) { return (size_t)4 * 1024 * kMfFrags * ((size_t)L + kMfHeadStages); }
 inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Packed-weight layout of the VALU family: W^T blocked by 16 bytes along K,

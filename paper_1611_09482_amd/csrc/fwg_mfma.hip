@@ -17,9 +17,11 @@
 //
 // Weights are streamed from L2: every wave reads its own pre-packed fragment
 // sequence, one "stage" (a layer: 26 fragments; a head chunk: 16 fragments) at a
-// time, double-buffered in registers so stage i+1 is in flight while stage i
-// computes.  Queue reads for stage i+2 are issued at the start of stage i and
-// land in LDS at the end of stage i+1.  A lane that pushes a queue row is the
+// time: as soon as a fragment register has fed its MFMA it is refilled with the
+// same fragment of the next stage, so about one stage of loads is always in
+// flight (every stage is 26 fragments, the head padded to whole stages, so the
+// refill pattern is the same on every path).  Queue reads for stage i+2 are
+// issued at the start of stage i and land in LDS at the end of stage i+1.  A lane that pushes a queue row is the
 // lane that later pops it, so queue traffic needs no cross-wave ordering.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -39,16 +41,23 @@ __device__ __forceinline__ f32x4 mfma(const u32x4 &a, const u32x4 &b, f32x4 c) {
                                                 0, 0);
 }
 
-__device__ __forceinline__ uint32_t bf16_rne_bits(float x) {
-  uint32_t u = __float_as_uint(x);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// two floats -> two bf16 (round to nearest even; one v_cvt_pk_bf16_f32 on gfx950)
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  const bf16x2 p = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, p);
 }
-__device__ __forceinline__ uint32_t pack2(float lo, float hi) { return bf16_rne_bits(lo) | (bf16_rne_bits(hi) << 16); }
 __device__ __forceinline__ u32x2 pack4(const f32x4 &v) { return u32x2{pack2(v[0], v[1]), pack2(v[2], v[3])}; }
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.f / (1.f + __expf(-x)); }
+// tanh(a) * sigmoid(g) with one exp and one reciprocal each: tanh(a) = 1 - 2 / (exp(2a) + 1)
+// (absolute error ~1e-7, far below the bf16 rounding this value goes through next)
+__device__ __forceinline__ float gate(float a, float g) {
+  const float t = 1.f - 2.f / (__expf(2.f * a) + 1.f);
+  return t / (1.f + __expf(-g));
+}
 
 __device__ __forceinline__ u32x4 lds16(const uint16_t *p) { return *(const u32x4 *)p; }
 __device__ __forceinline__ void lds8(uint16_t *p, u32x2 v) { *(u32x2 *)p = v; }
@@ -93,8 +102,10 @@ constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
 constexpr int PX = R + 8;   // 64-channel activation rows
 constexpr int PS = S + 8;   // 512-channel activation rows (skip / head hidden)
 constexpr int PL = Q + 4;   // fp32 logits rows
-constexpr int FL = kMfFragsLayer, FH = kMfFragsHead, NH1 = kMfH1Chunks, NOUT = kMfOutChunks;
-constexpr int NHEAD = NH1 + NOUT;
+constexpr int F = kMfFrags, NHEAD = kMfHeadStages;
+// per-wave head fragment stream, k-step major: first 1x1 (g < G1: tile 8w + g%8, k-step g/8),
+// output 1x1 (G1 <= g < G2: tile 4w + (g-G1)%4, k-step (g-G1)/4), then zero padding
+constexpr int G1 = 128, G2 = 192;
 
 struct Lds {
   uint16_t vbuf[2][ROWS * PX];
@@ -116,67 +127,75 @@ __host__ __device__ constexpr size_t lds_fixed_bytes() { return (sizeof(Lds) + 1
 __host__ __device__ inline size_t lds_dyn_bias_offset(int L) { return ((size_t)L * 16 + 15) & ~size_t(15); }
 
 struct Frags {
-  u32x4 f[FL];
+  u32x4 f[F];
 };
 
-// Stage bookkeeping: stage k of a step is layer k (k < L) or head chunk k - L.
+// Stage k of a step is layer k (k < L) or head chunk k - L; every stage is F fragments per wave.
 struct Ctx {
   const StepArgs *a;
   Lds *s;
   int *slot, *dil;
   const long long *roff;
   const float *conv_b, *res_b, *skip_sum, *head_b, *out_b, *emb_b;
-  const u32x4 *wbase;  // this wave's fragment stream origin (already offset by lane)
+  __amdgpu_buffer_rsrc_t wrsrc;  // buffer resource over the fragment streams
+  int wvoff;                     // this lane's byte offset inside a fragment (16 * lane)
   int L, NS, w, lane, n, q, b0, nrows;
-  long long frags_layers;  // fragments of all layer stages (4 waves)
 };
 
-// Fragment offset (in 1 KB units, 4 waves interleaved per stage) of stage k for wave w.
-__device__ __forceinline__ long long stage_frag0(const Ctx &c, int k) {
-  if (k < c.L) return (long long)k * 4 * FL + (long long)c.w * FL;
-  return c.frags_layers + (long long)(k - c.L) * 4 * FH + (long long)c.w * FH;
+// Byte offset (wave-uniform) of stage k's fragment stream for this wave: stage-major, 4 waves
+// per stage, F fragments of 1 KB each.
+__device__ __forceinline__ int stage_off(const Ctx &c, int k) { return (k * 4 + c.w) * F * 1024; }
+__device__ __forceinline__ u32x4 load_frag(const Ctx &c, int off, int f) {
+  return __builtin_amdgcn_raw_buffer_load_b128(c.wrsrc, c.wvoff, off + f * 1024, 0);
+}
+// Slot f has just been consumed: start loading the same slot of the next stage.
+// The scheduling barrier keeps the compiler from hoisting the load above the MFMA that still
+// reads the slot's previous contents (which would keep both copies live).
+__device__ __forceinline__ void refill(const Ctx &c, Frags &W, int nx, int f) {
+  __builtin_amdgcn_sched_barrier(0);
+  W.f[f] = load_frag(c, nx, f);
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 __device__ __forceinline__ void load_stage(const Ctx &c, int k, Frags &fr) {
-  const u32x4 *p = c.wbase + stage_frag0(c, k) * 64;
-  if (k < c.L) {
+  const int off = stage_off(c, k);
 #pragma unroll
-    for (int f = 0; f < FL; ++f) fr.f[f] = p[f * 64];
-  } else {
-#pragma unroll
-    for (int f = 0; f < FH; ++f) fr.f[f] = p[f * 64];
-  }
+  for (int f = 0; f < F; ++f) fr.f[f] = load_frag(c, off, f);
 }
 
-// Queue row this lane moves (lanes 0..31): stream row 4w + lane/8, 16-byte chunk lane%8.
+// Queue row a lane moves: stream row 4w + (lane%32)/8, 16-byte chunk lane%8 (lanes 32..63 mirror
+// lanes 0..31 on loads and skip the stores).
 __device__ __forceinline__ long long ring_elem(const Ctx &c, int l, int slotv) {
-  const int r = 4 * c.w + (c.lane >> 3);
+  const int r = 4 * c.w + ((c.lane & 31) >> 3);
   return c.roff[l] + ((long long)slotv * c.a->bmax + (c.b0 + r)) * R + 8 * (c.lane & 7);
 }
 
-// Issue the pop of layer `l` for step offset `ahead` (0: the step the slot table describes, 1: next).
-__device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int l, int ahead) {
-  if (c.lane >= 32) return u32x4{0, 0, 0, 0};
+// Issue the pop of stage k (a layer) for step offset `ahead` (0: the step the slot table
+// describes, 1: the next one).  Head stages pop layer 0 as a harmless placeholder.
+__device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int k, int ahead) {
+  const int l = k < c.L ? k : 0;
   int sl = c.slot[l] + ahead;
   if (sl >= c.dil[l]) sl -= c.dil[l];
   const uint16_t *ring = (const uint16_t *)c.a->ring;
   return __builtin_nontemporal_load((const u32x4 *)(ring + ring_elem(c, l, sl)));
 }
 __device__ __forceinline__ void pop_land(const Ctx &c, int parity, u32x4 v) {
-  if (c.lane >= 32) return;
-  const int r = 4 * c.w + (c.lane >> 3);
-  *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
+  if (c.lane < 32) {
+    const int r = 4 * c.w + (c.lane >> 3);
+    *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
+  }
 }
 
+// Accumulators.  acc[] holds, in turn, the skip sum (layers; channels 128w + 16j + 4q + i),
+// the first head 1x1's pre-activation (same channels) and the logits (acc[0..3], classes
+// 64w + 16j + 4q + i).
 struct Acc {
-  f32x4 xres;     // residual stream: channels 16w + 4q + i of stream n
-  f32x4 skip[8];  // skip sum: channels 128w + 16j + 4q + i
-  f32x4 head[8];  // head hidden: channels 128w + 16j + 4q + i
-  f32x4 out[4];   // logits: classes 64w + 16j + 4q + i
+  f32x4 xres;  // residual stream: channels 16w + 4q + i of stream n
+  f32x4 acc[8];
 };
 
-// One layer stage.  `par` = stage parity (selects vbuf), xin/xout parities follow the layer index.
-__device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, const Frags &W, Acc &A) {
+// One layer stage.  `par` = stage parity (selects vbuf); xbuf parity follows the layer index.
+__device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, Frags &W, int nx, Acc &A) {
   Lds &s = *c.s;
   const int n = c.n, q = c.q, w = c.w;
   u32x4 bx0, bx1;
@@ -202,7 +221,7 @@ __device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, const Fr
                    bf_hi(raw.y) + eb[ch + 3]};
     lds8(s.xbuf[0] + n * PX + ch, pack4(A.xres));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) A.skip[j] = ldsf4(c.skip_sum + 128 * w + 16 * j + 4 * q);
+    for (int j = 0; j < 8; ++j) A.acc[j] = ldsf4(c.skip_sum + 128 * w + 16 * j + 4 * q);
   } else {
     const uint16_t *xb = s.xbuf[l & 1] + n * PX;
     bx0 = lds16(xb + 8 * q);
@@ -210,7 +229,7 @@ __device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, const Fr
   }
   const uint16_t *vb = s.vbuf[par] + n * PX;
   const u32x4 bv0 = lds16(vb + 8 * q), bv1 = lds16(vb + 32 + 8 * q);
-  // dilated width-2 product: rows 16w.. (tanh half) and 64 + 16w.. (sigmoid half)
+  // dilated width-2 product: output rows 16w.. (tanh half) and 64 + 16w.. (sigmoid half)
   const float *cb = c.conv_b + l * 2 * R;
   f32x4 af = ldsf4(cb + 16 * w + 4 * q), ag = ldsf4(cb + R + 16 * w + 4 * q);
   af = mfma(W.f[0], bv0, af);
@@ -221,9 +240,11 @@ __device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, const Fr
   ag = mfma(W.f[6], bx0, ag);
   af = mfma(W.f[3], bx1, af);
   ag = mfma(W.f[7], bx1, ag);
+#pragma unroll
+  for (int f = 0; f < 8; ++f) refill(c, W, nx, f);
   f32x4 z;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) z[i] = tanhf(af[i]) * sigmoidf_(ag[i]);
+  for (int i = 0; i < 4; ++i) z[i] = gate(af[i], ag[i]);
   lds8(s.zbuf + n * PX + 16 * w + 4 * q, pack4(z));
   __syncthreads();
   // push phase: the layer's input x^{l-1}_t replaces the slot popped for this step
@@ -239,73 +260,101 @@ __device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, const Fr
   f32x4 xr = A.xres + ldsf4(c.res_b + l * R + 16 * w + 4 * q);
   xr = mfma(W.f[8], bz0, xr);
   xr = mfma(W.f[9], bz1, xr);
+  refill(c, W, nx, 8);
+  refill(c, W, nx, 9);
   A.xres = xr;
   lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * w + 4 * q, pack4(xr));
   // skip 1x1, accumulated over layers
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    A.skip[j] = mfma(W.f[10 + 2 * j], bz0, A.skip[j]);
-    A.skip[j] = mfma(W.f[11 + 2 * j], bz1, A.skip[j]);
+    A.acc[j] = mfma(W.f[10 + 2 * j], bz0, A.acc[j]);
+    A.acc[j] = mfma(W.f[11 + 2 * j], bz1, A.acc[j]);
+    refill(c, W, nx, 10 + 2 * j);
+    refill(c, W, nx, 11 + 2 * j);
   }
 }
 
-// Head chunk h (0..NH1-1: first 1x1 over relu(skip); NH1..: output 1x1).
-__device__ __forceinline__ void run_head(const Ctx &c, int h, const Frags &W, Acc &A) {
+// Head chunk C: fragments g = 26C .. 26C+25 of the head stream.
+template <int C>
+__device__ __forceinline__ void run_head(const Ctx &c, Frags &W, int nx, Acc &A) {
   Lds &s = *c.s;
   const int n = c.n, q = c.q, w = c.w;
-  if (h == 0) {
+  if (C == 0) {
+    // relu(skip sum) becomes the first head 1x1's input
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       f32x4 r;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.skip[j][i], 0.f);
+      for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.acc[j][i], 0.f);
       lds8(s.u.sbuf + n * PS + 128 * w + 16 * j + 4 * q, pack4(r));
-      A.head[j] = ldsf4(c.head_b + 128 * w + 16 * j + 4 * q);
+      A.acc[j] = ldsf4(c.head_b + 128 * w + 16 * j + 4 * q);
     }
     __syncthreads();
   }
-  if (h < NH1) {
-    const uint16_t *sb = s.u.sbuf + n * PS;
-    const u32x4 b0 = lds16(sb + 64 * h + 8 * q), b1 = lds16(sb + 64 * h + 32 + 8 * q);
+  u32x4 b = u32x4{0, 0, 0, 0};
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      A.head[j] = mfma(W.f[2 * j], b0, A.head[j]);
-      A.head[j] = mfma(W.f[2 * j + 1], b1, A.head[j]);
-    }
-    if (h == NH1 - 1) {
+  for (int f = 0; f < F; ++f) {
+    const int g = F * C + f;
+    if (g < G1) {
+      const int ks = g / 8, j = g % 8;
+      if (j == 0 || f == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
+      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
+    } else if (g < G2) {
+      if (g == G1) {
+        // relu(head hidden) becomes the output 1x1's input
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        f32x4 r;
+        for (int j = 0; j < 8; ++j) {
+          f32x4 r;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.head[j][i], 0.f);
-        lds8(s.hbuf + n * PS + 128 * w + 16 * j + 4 * q, pack4(r));
+          for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.acc[j][i], 0.f);
+          lds8(s.hbuf + n * PS + 128 * w + 16 * j + 4 * q, pack4(r));
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.out_b + 64 * w + 16 * j + 4 * q);
+        __syncthreads();
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) A.out[j] = ldsf4(c.out_b + 64 * w + 16 * j + 4 * q);
-      __syncthreads();
+      const int ks = (g - G1) / 4, j = (g - G1) % 4;
+      if (j == 0 || f == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
+      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
     }
-    return;
-  }
-  const int oc = h - NH1;
-  const uint16_t *hb = s.hbuf + n * PS + 128 * oc;
-  const u32x4 b0 = lds16(hb + 8 * q), b1 = lds16(hb + 32 + 8 * q), b2 = lds16(hb + 64 + 8 * q),
-              b3 = lds16(hb + 96 + 8 * q);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    A.out[j] = mfma(W.f[4 * j + 0], b0, A.out[j]);
-    A.out[j] = mfma(W.f[4 * j + 1], b1, A.out[j]);
-    A.out[j] = mfma(W.f[4 * j + 2], b2, A.out[j]);
-    A.out[j] = mfma(W.f[4 * j + 3], b3, A.out[j]);
+    refill(c, W, nx, f);
   }
 }
 
+// Per-step inputs a wave needs at the end of a step, loaded at the start of the step's last
+// stage so that waiting for them does not wait for the weight prefetches issued after them:
+// the uniforms of rows w, w+4, w+8, w+12 (generation) or the next forced inputs (thread < 16).
+struct StepIn {
+  float u[4];
+  int next_in;
+};
+__device__ __forceinline__ StepIn load_step_inputs(const Ctx &c, long long step) {
+  const StepArgs &a = *c.a;
+  StepIn in;
+  in.next_in = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) in.u[k] = 0.f;
+  if (a.forced) {
+    const int tid = threadIdx.x;
+    if (tid < c.nrows && step + 1 < a.n_steps) in.next_in = a.inputs[(long long)(c.b0 + tid) * a.n_steps + step + 1];
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int r = c.w + 4 * k;
+      if (r < c.nrows) in.u[k] = a.uniforms[(long long)(c.b0 + r) * a.n_steps + step];
+    }
+  }
+  return in;
+}
+
 // End of a step: logits to LDS, sample (or write logits), next inputs, queue slots advance.
-__device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A) {
+__device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A, const StepIn &in) {
   Lds &s = *c.s;
   const StepArgs &a = *c.a;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) *(float4 *)(s.u.lg + c.n * PL + 64 * c.w + 16 * j + 4 * c.q) =
-      make_float4(A.out[j][0], A.out[j][1], A.out[j][2], A.out[j][3]);
+  for (int j = 0; j < 4; ++j)
+    *(float4 *)(s.u.lg + c.n * PL + 64 * c.w + 16 * j + 4 * c.q) =
+        make_float4(A.acc[j][0], A.acc[j][1], A.acc[j][2], A.acc[j][3]);
   __syncthreads();
   const int tid = threadIdx.x;
   if (a.forced) {
@@ -313,11 +362,13 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
       const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
       *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
     }
-    if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = a.inputs[(long long)(c.b0 + tid) * a.n_steps + step + 1];
+    if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = in.next_in;
   } else {
-    for (int r = c.w; r < c.nrows; r += 4) {
-      const float u = a.uniforms[(long long)(c.b0 + r) * a.n_steps + step];
-      const int k = sample256(s.u.lg + r * PL, u);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int r = c.w + 4 * kk;
+      if (r >= c.nrows) break;
+      const int k = sample256(s.u.lg + r * PL, in.u[kk]);
       if (c.lane == 0) {
         a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
         s.ins[r] = k;
@@ -342,10 +393,24 @@ __device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
   return p;
 }
 
-__device__ __forceinline__ void run_stage(const Ctx &c, Pos p, int par, const Frags &W, Acc &A) {
-  if (p.k < c.L) run_layer(c, p.k, par, W, A);
-  else run_head(c, p.k - c.L, W, A);
-  if (p.k == c.NS - 1) finish_step(c, p.step, A);
+__device__ __forceinline__ void run_stage(const Ctx &c, Pos p, int par, Frags &W, int nx, Acc &A) {
+  StepIn in;
+  if (p.k == c.NS - 1) in = load_step_inputs(c, p.step);
+  if (p.k < c.L) {
+    run_layer(c, p.k, par, W, nx, A);
+  } else {
+    switch (p.k - c.L) {
+      case 0: run_head<0>(c, W, nx, A); break;
+      case 1: run_head<1>(c, W, nx, A); break;
+      case 2: run_head<2>(c, W, nx, A); break;
+      case 3: run_head<3>(c, W, nx, A); break;
+      case 4: run_head<4>(c, W, nx, A); break;
+      case 5: run_head<5>(c, W, nx, A); break;
+      case 6: run_head<6>(c, W, nx, A); break;
+      default: run_head<7>(c, W, nx, A); break;
+    }
+  }
+  if (p.k == c.NS - 1) finish_step(c, p.step, A, in);
 }
 
 __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
@@ -380,8 +445,9 @@ __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
   c.q = c.lane >> 4;
   c.b0 = blockIdx.x * ROWS;
   c.nrows = min(ROWS, a.batch - c.b0);
-  c.frags_layers = (long long)L * 4 * FL;
-  c.wbase = (const u32x4 *)a.mf_frags + c.lane;
+  c.w = __builtin_amdgcn_readfirstlane(c.w);
+  c.wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)a.mf_frags, (short)0, mfma_frag_bytes(L), 0x00020000);
+  c.wvoff = 16 * c.lane;
 
   // tables: embedding [Q][R], biases, queue offsets, dilations and slots
   const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
@@ -403,34 +469,27 @@ __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
 
   const long long total = (long long)a.n_steps * c.NS;
   Acc A;
-  Frags WA, WB;
-  u32x4 vA = u32x4{0, 0, 0, 0}, vB = u32x4{0, 0, 0, 0};
+  Frags W;  // one stage of fragments; each slot is refilled with the next stage's right after use
   Pos p0{0, 0};
-  // prologue: queue rows of stage 0 land now; stage 1's are in flight
+  // prologue: stage 0's queue rows land now, stage 1's are in flight; stage 0's weights
   pop_land(c, 0, pop_issue(c, 0, 0));
-  if (L > 1) vB = pop_issue(c, 1, 0);
-  load_stage(c, 0, WA);
+  u32x4 vA, vB = pop_issue(c, 1 < L ? 1 : 0, 0);
+  load_stage(c, 0, W);
   __syncthreads();
 
   for (long long i = 0; i < total; i += 2) {
     const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3);
-    // ---- even stage: weights WA, pops in flight into vA for stage i+2
-    if (i + 1 < total) load_stage(c, p1.k, WB);
-    if (i + 2 < total && p2.k < L) vA = pop_issue(c, p2.k, (int)(p2.step - p0.step));
-    run_stage(c, p0, (int)(i & 1), WA, A);
-    if (i + 1 < total && p1.k < L) {
-      pop_land(c, (int)((i + 1) & 1), vB);
-      __syncthreads();
-    }
+    // ---- even stage: queue rows of stage i+2 in flight into vA, rows of stage i+1 land
+    vA = pop_issue(c, p2.k, (int)(p2.step - p0.step));
+    run_stage(c, p0, (int)(i & 1), W, stage_off(c, p1.k), A);
+    if (p1.k < L && i + 1 < total) pop_land(c, (int)((i + 1) & 1), vB);
+    __syncthreads();
     if (i + 1 >= total) break;
-    // ---- odd stage: weights WB, pops in flight into vB for stage i+3
-    if (i + 2 < total) load_stage(c, p2.k, WA);
-    if (i + 3 < total && p3.k < L) vB = pop_issue(c, p3.k, (int)(p3.step - p1.step));
-    run_stage(c, p1, (int)((i + 1) & 1), WB, A);
-    if (i + 2 < total && p2.k < L) {
-      pop_land(c, (int)(i & 1), vA);
-      __syncthreads();
-    }
+    // ---- odd stage: rows of stage i+3 in flight into vB, rows of stage i+2 land
+    vB = pop_issue(c, p3.k, (int)(p3.step - p1.step));
+    run_stage(c, p1, (int)((i + 1) & 1), W, stage_off(c, p2.k), A);
+    if (p2.k < L && i + 2 < total) pop_land(c, (int)(i & 1), vA);
+    __syncthreads();
     p0 = p2;
   }
   if (!a.forced && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
@@ -465,10 +524,10 @@ __device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int o, int k
 }
 
 __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, uint4 *dst) {
-  // dst: this layer's stage, 4 waves x FL fragments x 64 lanes x 8 elements
+  // dst: this layer's stage, 4 waves x F fragments x 64 lanes x 8 elements
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= 4 * FL * 64) return;
-  const int lane = e % 64, f = (e / 64) % FL, w = e / (64 * FL);
+  if (e >= 4 * F * 64) return;
+  const int lane = e % 64, f = (e / 64) % F, w = e / (64 * F);
   const int m = lane % 16, kq = 8 * (lane / 16);
   uint16_t v[8];
   for (int j = 0; j < 8; ++j) {
@@ -493,19 +552,22 @@ __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, c
 }
 
 __global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, uint4 *dst) {
-  // dst: NHEAD stages of 4 waves x FH fragments x 64 lanes
+  // dst: NHEAD stages of 4 waves x F fragments x 64 lanes; head fragment g = F*stage + f
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= NHEAD * 4 * FH * 64) return;
-  const int lane = e % 64, f = (e / 64) % FH, w = (e / (64 * FH)) % 4, h = e / (64 * FH * 4);
+  if (e >= NHEAD * 4 * F * 64) return;
+  const int lane = e % 64, f = (e / 64) % F, w = (e / (64 * F)) % 4, st = e / (64 * F * 4);
   const int m = lane % 16, kq = 8 * (lane / 16);
+  const int g = F * st + f;
   uint16_t v[8];
   for (int j = 0; j < 8; ++j) {
-    if (h < NH1) {
-      const int t = 8 * w + f / 2, ks = 2 * h + f % 2;
+    if (g < G1) {
+      const int t = 8 * w + g % 8, ks = g / 8;
       v[j] = head[(16 * t + m) * S + 32 * ks + kq + j];
-    } else {
-      const int t = 4 * w + f / 4, ks = 4 * (h - NH1) + f % 4;
+    } else if (g < G2) {
+      const int t = 4 * w + (g - G1) % 4, ks = (g - G1) / 4;
       v[j] = out[(16 * t + m) * H + 32 * ks + kq + j];
+    } else {
+      v[j] = 0;
     }
   }
   dst[e] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
@@ -551,14 +613,14 @@ __global__ void bias_block_kernel(const float *const *conv_b, const float *const
 }  // namespace mf
 
 hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, void *dst, hipStream_t s) {
-  const int n = 4 * kMfFragsLayer * 64;
+  const int n = 4 * kMfFrags * 64;
   hipLaunchKernelGGL(mf::repack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)conv,
                      (const uint16_t *)res, (const uint16_t *)skip, (uint4 *)dst);
   return hipGetLastError();
 }
 
 hipError_t launch_mfma_repack_head(const void *head, const void *out, void *dst, hipStream_t s) {
-  const int n = (kMfH1Chunks + kMfOutChunks) * 4 * kMfFragsHead * 64;
+  const int n = kMfHeadStages * 4 * kMfFrags * 64;
   hipLaunchKernelGGL(mf::repack_head_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)head,
                      (const uint16_t *)out, (uint4 *)dst);
   return hipGetLastError();
