@@ -55,8 +55,8 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.f / (1.f + __expf
 // tanh(a) * sigmoid(g) with one exp and one reciprocal each: tanh(a) = 1 - 2 / (exp(2a) + 1)
 // (absolute error ~1e-7, far below the bf16 rounding this value goes through next)
 __device__ __forceinline__ float gate(float a, float g) {
-  const float t = 1.f - 2.f / (__expf(2.f * a) + 1.f);
-  return t / (1.f + __expf(-g));
+  const float t = 1.f - 2.f * __builtin_amdgcn_rcpf(__expf(2.f * a) + 1.f);
+  return t * __builtin_amdgcn_rcpf(1.f + __expf(-g));
 }
 
 __device__ __forceinline__ u32x4 lds16(const uint16_t *p) { return *(const u32x4 *)p; }
@@ -106,6 +106,7 @@ constexpr int F = kMfFrags, NHEAD = kMfHeadStages;
 // per-wave head fragment stream, k-step major: first 1x1 (g < G1: tile 8w + g%8, k-step g/8),
 // output 1x1 (G1 <= g < G2: tile 4w + (g-G1)%4, k-step (g-G1)/4), then zero padding
 constexpr int G1 = 128, G2 = 192;
+constexpr int KCH = 64;  // steps per chunk of per-step inputs staged in LDS
 
 struct Lds {
   uint16_t vbuf[2][ROWS * PX];
@@ -117,6 +118,12 @@ struct Lds {
     float lg[ROWS * PL];
   } u;
   uint16_t embT[Q * R];  // embedding table, [class][channel]
+  // per-step inputs of the block's streams for a chunk of KCH steps: uniforms (generation) or the
+  // next forced input (teacher forcing), loaded once per chunk
+  union {
+    float u[ROWS][KCH];
+    int in[ROWS][KCH];
+  } chunk;
   int ins[ROWS];
   int pad_[ROWS];
   // followed by the per-layer tables (dynamic part): roff[L] (int64), slot[L], dil[L], then fp32 biases
@@ -264,13 +271,16 @@ __device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, Frags &W
   refill(c, W, nx, 9);
   A.xres = xr;
   lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * w + 4 * q, pack4(xr));
-  // skip 1x1, accumulated over layers
+  // skip 1x1, accumulated over layers (k-step major: consecutive MFMAs use different accumulators)
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    A.acc[j] = mfma(W.f[10 + 2 * j], bz0, A.acc[j]);
-    A.acc[j] = mfma(W.f[11 + 2 * j], bz1, A.acc[j]);
-    refill(c, W, nx, 10 + 2 * j);
-    refill(c, W, nx, 11 + 2 * j);
+    A.acc[j] = mfma(W.f[10 + j], bz0, A.acc[j]);
+    refill(c, W, nx, 10 + j);
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    A.acc[j] = mfma(W.f[18 + j], bz1, A.acc[j]);
+    refill(c, W, nx, 18 + j);
   }
 }
 
@@ -321,34 +331,30 @@ __device__ __forceinline__ void run_head(const Ctx &c, Frags &W, int nx, Acc &A)
   }
 }
 
-// Per-step inputs a wave needs at the end of a step, loaded at the start of the step's last
-// stage so that waiting for them does not wait for the weight prefetches issued after them:
-// the uniforms of rows w, w+4, w+8, w+12 (generation) or the next forced inputs (thread < 16).
-struct StepIn {
-  float u[4];
-  int next_in;
-};
-__device__ __forceinline__ StepIn load_step_inputs(const Ctx &c, long long step) {
+// Stage the per-step inputs of steps [s0, s0 + KCH) in LDS: the uniform of (row r, step s) for
+// generation, the input of step s + 1 for teacher forcing.  Called by all threads once per chunk
+// (in the first head stage, before its barrier); waiting for these loads here keeps every other
+// wait in the step loop precise.
+__device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
-  StepIn in;
-  in.next_in = 0;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) in.u[k] = 0.f;
-  if (a.forced) {
-    const int tid = threadIdx.x;
-    if (tid < c.nrows && step + 1 < a.n_steps) in.next_in = a.inputs[(long long)(c.b0 + tid) * a.n_steps + step + 1];
-  } else {
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int r = c.w + 4 * k;
-      if (r < c.nrows) in.u[k] = a.uniforms[(long long)(c.b0 + r) * a.n_steps + step];
+  Lds &s = *c.s;
+  for (int i = threadIdx.x; i < ROWS * KCH; i += kThreads) {
+    const int r = i / KCH, j = i % KCH;
+    const long long st = s0 + j;
+    if (a.forced) {
+      int v = 0;
+      if (r < c.nrows && st + 1 < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + st + 1];
+      s.chunk.in[r][j] = v;
+    } else {
+      float v = 0.f;
+      if (r < c.nrows && st < a.n_steps) v = a.uniforms[(long long)(c.b0 + r) * a.n_steps + st];
+      s.chunk.u[r][j] = v;
     }
   }
-  return in;
 }
 
 // End of a step: logits to LDS, sample (or write logits), next inputs, queue slots advance.
-__device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A, const StepIn &in) {
+__device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A) {
   Lds &s = *c.s;
   const StepArgs &a = *c.a;
 #pragma unroll
@@ -362,13 +368,13 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
       const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
       *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
     }
-    if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = in.next_in;
+    if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const int r = c.w + 4 * kk;
       if (r >= c.nrows) break;
-      const int k = sample256(s.u.lg + r * PL, in.u[kk]);
+      const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
       if (c.lane == 0) {
         a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
         s.ins[r] = k;
@@ -394,13 +400,14 @@ __device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
 }
 
 __device__ __forceinline__ void run_stage(const Ctx &c, Pos p, int par, Frags &W, int nx, Acc &A) {
-  StepIn in;
-  if (p.k == c.NS - 1) in = load_step_inputs(c, p.step);
   if (p.k < c.L) {
     run_layer(c, p.k, par, W, nx, A);
   } else {
     switch (p.k - c.L) {
-      case 0: run_head<0>(c, W, nx, A); break;
+      case 0:
+        if (p.step % KCH == 0) stage_chunk(c, p.step);
+        run_head<0>(c, W, nx, A);
+        break;
       case 1: run_head<1>(c, W, nx, A); break;
       case 2: run_head<2>(c, W, nx, A); break;
       case 3: run_head<3>(c, W, nx, A); break;
@@ -410,7 +417,7 @@ __device__ __forceinline__ void run_stage(const Ctx &c, Pos p, int par, Frags &W
       default: run_head<7>(c, W, nx, A); break;
     }
   }
-  if (p.k == c.NS - 1) finish_step(c, p.step, A, in);
+  if (p.k == c.NS - 1) finish_step(c, p.step, A);
 }
 
 __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
@@ -481,12 +488,14 @@ __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
     const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3);
     // ---- even stage: queue rows of stage i+2 in flight into vA, rows of stage i+1 land
     vA = pop_issue(c, p2.k, (int)(p2.step - p0.step));
+    __builtin_amdgcn_sched_barrier(0);  // issue the queue read before this stage's refills
     run_stage(c, p0, (int)(i & 1), W, stage_off(c, p1.k), A);
     if (p1.k < L && i + 1 < total) pop_land(c, (int)((i + 1) & 1), vB);
     __syncthreads();
     if (i + 1 >= total) break;
     // ---- odd stage: rows of stage i+3 in flight into vB, rows of stage i+2 land
     vB = pop_issue(c, p3.k, (int)(p3.step - p1.step));
+    __builtin_amdgcn_sched_barrier(0);
     run_stage(c, p1, (int)((i + 1) & 1), W, stage_off(c, p2.k), A);
     if (p2.k < L && i + 2 < total) pop_land(c, (int)(i & 1), vA);
     __syncthreads();
@@ -542,7 +551,7 @@ __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, c
       k = 32 * (f - 8) + kq + j;
       v[j] = res[o * R + k];
     } else {
-      const int jj = (f - 10) / 2, ks = (f - 10) % 2;
+      const int jj = (f - 10) % 8, ks = (f - 10) / 8;
       o = 16 * (8 * w + jj) + m;
       k = 32 * ks + kq + j;
       v[j] = skip[o * R + k];
