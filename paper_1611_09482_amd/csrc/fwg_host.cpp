@@ -305,10 +305,10 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   std::vector<const void *> ptrs;
   if (p.regime == REGIME_MFMA) {
     char *frags = ws + p.off_frags;
-    const size_t layer_bytes = (size_t)4 * kMfFrags * 1024;
+    // layers first: a layer also writes fragments into the previous stage and the last head stage
     for (int l = 0; l < p.L; ++l)
-      TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], frags + l * layer_bytes, s));
-    TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, frags + p.L * layer_bytes, s));
+      TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));
+    TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, p.L, frags, s));
     TRY_OR_FREE(launch_mfma_embed_table(w->embed, ws + p.off_embT, s));
     ptrs.resize(3 * p.L, nullptr);
     for (int l = 0; l < p.L; ++l) {

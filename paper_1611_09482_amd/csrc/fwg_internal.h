@@ -52,12 +52,14 @@ struct StepArgs {
 enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1 };
 
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
-// 16 streams per block, weight fragments per wave and stage.
+// 16 streams per block of 8 waves, weight fragments per wave and stage.
 constexpr int kMfR = 64, kMfS = 512, kMfH = 512, kMfRows = 16;
-constexpr int kMfFrags = 26;       // fragments per wave and stage: conv 8 + residual 2 + skip 16
-constexpr int kMfHeadStages = 8;   // head: 128 + 64 fragments per wave, padded to 8 stages of 26
+constexpr int kMfWaves = 8, kMfThreads = 64 * kMfWaves;
+constexpr int kMfFrags = 13;       // fragments per wave and stage (8 waves x 13 = one layer's 104)
+constexpr int kMfHeadStages = 8;   // head: 96 fragments per wave (+ padding), 8 stages of 13
 constexpr int kMfMaxLayers = 128;
-__host__ __device__ inline size_t mfma_frag_bytes(int L) { return (size_t)4 * 1024 * kMfFrags * ((size_t)L + kMfHeadStages); }
+constexpr size_t kMfStageBytes = (size_t)kMfWaves * kMfFrags * 1024;
+__host__ __device__ inline size_t mfma_frag_bytes(int L) { return kMfStageBytes * ((size_t)L + kMfHeadStages); }
 inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Packed-weight layout of the VALU family: W^T blocked by 16 bytes along K,
@@ -107,8 +109,9 @@ hipError_t set_valu_lds_limit(size_t bytes);
 size_t mfma_lds_bytes(int L);
 hipError_t launch_mfma_step(const StepArgs &a, hipStream_t s);
 hipError_t set_mfma_lds_limit(size_t bytes);
-hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, void *dst, hipStream_t s);
-hipError_t launch_mfma_repack_head(const void *head, const void *out, void *dst, hipStream_t s);
+hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
+                                    hipStream_t s);
+hipError_t launch_mfma_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s);
 hipError_t launch_mfma_embed_table(const void *embed, void *dst, hipStream_t s);
 hipError_t launch_mfma_bias_block(const float *const *conv_b, const float *const *res_b, const float *const *skip_b,
                                   const float *head_b, const float *out_b, const float *emb_b, int L, float *dst,

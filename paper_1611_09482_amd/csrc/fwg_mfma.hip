@@ -2,7 +2,7 @@
 // channels, S = H = 512 skip/head channels and 256 classes (gfx950,
 // v_mfma_f32_16x16x32_bf16, fp32 accumulation).
 //
-// One block of 4 waves owns 16 independent streams; one launch runs n_steps
+// One block of 8 waves owns 16 independent streams; one launch runs n_steps
 // whole generation steps.  Per step and layer (paper Section 2.2): pop the
 // layer's queue (the state pushed d_l steps earlier), compute the dilated
 // width-2 product [W_r W_e] [v; x], the gate, the residual and skip 1x1
@@ -15,14 +15,17 @@
 // operand (32 k x 16 streams).  Each lane then holds 4 consecutive channels of
 // one stream, so activation tiles move to and from LDS as 8- and 16-byte rows.
 //
-// Weights are streamed from L2: every wave reads its own pre-packed fragment
-// sequence, one "stage" (a layer: 26 fragments; a head chunk: 16 fragments) at a
-// time: as soon as a fragment register has fed its MFMA it is refilled with the
-// same fragment of the next stage, so about one stage of loads is always in
-// flight (every stage is 26 fragments, the head padded to whole stages, so the
-// refill pattern is the same on every path).  Queue reads for stage i+2 are
-// issued at the start of stage i and land in LDS at the end of stage i+1.  A lane that pushes a queue row is the
-// lane that later pops it, so queue traffic needs no cross-wave ordering.
+// Wave roles.  Waves p and p + 4 share SIMD p and split the work of channel tile p:
+//  - wave p ("A", on the layer-to-layer dependency chain): the current-input half of the
+//    dilated product (W_e x) for tanh tile p and sigmoid tile p, the gate, the residual
+//    1x1 for tile p, and 7 of the 16 skip fragments of skip tiles 8p..8p+7;
+//  - wave p + 4 ("B"): the recurrent half (W_r v, v = the popped state, known early) of the
+//    NEXT layer plus its bias, handed to A through LDS, the other 9 skip fragments, and the
+//    queue pops and pushes of rows 4p..4p+3.
+// Both halves of the head are split the same way.  Every wave streams its own pre-packed
+// weight fragments from L2 (13 per stage, refilled one stage ahead as soon as consumed); a
+// wave stalls while the load unit is saturated, and the second wave on the SIMD keeps the
+// SIMD busy meanwhile, so the dependency chain overlaps the weight stream.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -51,7 +54,6 @@ __device__ __forceinline__ u32x2 pack4(const f32x4 &v) { return u32x2{pack2(v[0]
 __device__ __forceinline__ float bf_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
-__device__ __forceinline__ float sigmoidf_(float x) { return 1.f / (1.f + __expf(-x)); }
 // tanh(a) * sigmoid(g) with one exp and one reciprocal each: tanh(a) = 1 - 2 / (exp(2a) + 1)
 // (absolute error ~1e-7, far below the bf16 rounding this value goes through next)
 __device__ __forceinline__ float gate(float a, float g) {
@@ -64,6 +66,10 @@ __device__ __forceinline__ void lds8(uint16_t *p, u32x2 v) { *(u32x2 *)p = v; }
 __device__ __forceinline__ f32x4 ldsf4(const float *p) {
   const float4 v = *(const float4 *)p;
   return f32x4{v.x, v.y, v.z, v.w};
+}
+__device__ __forceinline__ void stf4(float *p, const f32x4 &v) { *(float4 *)p = make_float4(v[0], v[1], v[2], v[3]); }
+__device__ __forceinline__ f32x4 relu4(const f32x4 &v) {
+  return f32x4{fmaxf(v[0], 0.f), fmaxf(v[1], 0.f), fmaxf(v[2], 0.f), fmaxf(v[3], 0.f)};
 }
 
 // Inverse-CDF sample of one row of 256 logits by one wavefront (see fwg_kernels.hip).
@@ -99,19 +105,23 @@ __device__ __forceinline__ int sample256(const float *lg, float u) {
 // ---------------------------------------------------------------------------
 // Shapes and LDS layout (elements; activations bf16 with 8-element row padding)
 constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
+constexpr int NT = kMfThreads;
 constexpr int PX = R + 8;   // 64-channel activation rows
 constexpr int PS = S + 8;   // 512-channel activation rows (skip / head hidden)
 constexpr int PL = Q + 4;   // fp32 logits rows
+constexpr int PP = 20;      // fp32 partial-tile rows (16 channels + 4 padding)
 constexpr int F = kMfFrags, NHEAD = kMfHeadStages;
-// per-wave head fragment stream, k-step major: first 1x1 (g < G1: tile 8w + g%8, k-step g/8),
-// output 1x1 (G1 <= g < G2: tile 4w + (g-G1)%4, k-step (g-G1)/4), then zero padding
-constexpr int G1 = 128, G2 = 192;
+// per-wave head fragment stream g = 13 h + f, k-step major: first 1x1 (g < GH1: 4 tiles), output
+// 1x1 (GH1 <= g < GOUT: 2 tiles), then padding (wave B carries the next layer 0's W_r at GCV..)
+constexpr int GH1 = 64, GOUT = 96, GCV = 100;
 constexpr int KCH = 64;  // steps per chunk of per-step inputs staged in LDS
 
 struct Lds {
-  uint16_t vbuf[2][ROWS * PX];
-  uint16_t xbuf[2][ROWS * PX];
-  uint16_t zbuf[ROWS * PX];
+  uint16_t vbuf[2][ROWS * PX];     // popped queue rows (layer input d steps ago), by stage parity
+  uint16_t xbuf[2][ROWS * PX];     // layer inputs x^l, by layer parity
+  uint16_t zbuf[ROWS * PX];        // gate output of the current layer
+  float pbuf[2][4][2][ROWS * PP];  // W_r v + b of a layer: [stage parity][tile][tanh / sigmoid]
+  float ptile[4][ROWS * PP];       // partial skip tile 8p+3 of wave A, handed to wave B at the head
   uint16_t hbuf[ROWS * PS];
   union {
     uint16_t sbuf[ROWS * PS];
@@ -137,23 +147,23 @@ struct Frags {
   u32x4 f[F];
 };
 
-// Stage k of a step is layer k (k < L) or head chunk k - L; every stage is F fragments per wave.
+// Stage k of a step is layer k (k < L) or head stage k - L.
 struct Ctx {
   const StepArgs *a;
   Lds *s;
   int *slot, *dil;
   const long long *roff;
   const float *conv_b, *res_b, *skip_sum, *head_b, *out_b, *emb_b;
-  __amdgpu_buffer_rsrc_t wrsrc;  // buffer resource over the fragment streams
-  int wvoff;                     // this lane's byte offset inside a fragment (16 * lane)
-  int L, NS, w, lane, n, q, b0, nrows;
+  const char *frags;  // fragment streams (wave-uniform base)
+  int wvoff;          // this lane's byte offset inside a fragment (16 * lane)
+  int L, NS, w, p, lane, n, q, b0, nrows;
 };
 
-// Byte offset (wave-uniform) of stage k's fragment stream for this wave: stage-major, 4 waves
+// Byte offset (wave-uniform) of stage k's fragment stream for this wave: stage-major, 8 waves
 // per stage, F fragments of 1 KB each.
-__device__ __forceinline__ int stage_off(const Ctx &c, int k) { return (k * 4 + c.w) * F * 1024; }
+__device__ __forceinline__ int stage_off(const Ctx &c, int k) { return (k * kMfWaves + c.w) * F * 1024; }
 __device__ __forceinline__ u32x4 load_frag(const Ctx &c, int off, int f) {
-  return __builtin_amdgcn_raw_buffer_load_b128(c.wrsrc, c.wvoff, off + f * 1024, 0);
+  return *(const u32x4 *)(c.frags + (off + f * 1024) + c.wvoff);
 }
 // Slot f has just been consumed: start loading the same slot of the next stage.
 // The scheduling barrier keeps the compiler from hoisting the load above the MFMA that still
@@ -163,20 +173,21 @@ __device__ __forceinline__ void refill(const Ctx &c, Frags &W, int nx, int f) {
   W.f[f] = load_frag(c, nx, f);
   __builtin_amdgcn_sched_barrier(0);
 }
-
 __device__ __forceinline__ void load_stage(const Ctx &c, int k, Frags &fr) {
   const int off = stage_off(c, k);
 #pragma unroll
   for (int f = 0; f < F; ++f) fr.f[f] = load_frag(c, off, f);
 }
 
-// Queue row a lane moves: stream row 4w + (lane%32)/8, 16-byte chunk lane%8 (lanes 32..63 mirror
-// lanes 0..31 on loads and skip the stores).
+// Queue traffic is issued by the B waves: wave B of pair p moves stream rows 4p..4p+3, lane l
+// handling row 4p + (l%32)/8 and 16-byte chunk l%8 (lanes 32..63 mirror lanes 0..31 on loads and
+// skip the stores); the lane that pushes a row chunk later pops it.  Vector loads return to a
+// wave in issue order, so a queue read that goes out to HBM holds back the weight fragments its
+// wave requests after it: wave B therefore prefetches its fragments two stages ahead.
 __device__ __forceinline__ long long ring_elem(const Ctx &c, int l, int slotv) {
-  const int r = 4 * c.w + ((c.lane & 31) >> 3);
+  const int r = 4 * c.p + ((c.lane & 31) >> 3);
   return c.roff[l] + ((long long)slotv * c.a->bmax + (c.b0 + r)) * R + 8 * (c.lane & 7);
 }
-
 // Issue the pop of stage k (a layer) for step offset `ahead` (0: the step the slot table
 // describes, 1: the next one).  Head stages pop layer 0 as a harmless placeholder.
 __device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int k, int ahead) {
@@ -188,157 +199,211 @@ __device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int k, int ahead) {
 }
 __device__ __forceinline__ void pop_land(const Ctx &c, int parity, u32x4 v) {
   if (c.lane < 32) {
-    const int r = 4 * c.w + (c.lane >> 3);
+    const int r = 4 * c.p + (c.lane >> 3);
     *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
   }
 }
+// push phase of layer l: its input x^l replaces the slot popped for this step
+__device__ __forceinline__ void push_rows(const Ctx &c, int l) {
+  if (c.lane < 32) {
+    const int r = 4 * c.p + (c.lane >> 3);
+    const u32x4 v = *(const u32x4 *)(c.s->xbuf[l & 1] + r * PX + 8 * (c.lane & 7));
+    uint16_t *ring = (uint16_t *)c.a->ring;
+    __builtin_nontemporal_store(v, (u32x4 *)(ring + ring_elem(c, l, c.slot[l])));
+  }
+}
 
-// Accumulators.  acc[] holds, in turn, the skip sum (layers; channels 128w + 16j + 4q + i),
-// the first head 1x1's pre-activation (same channels) and the logits (acc[0..3], classes
-// 64w + 16j + 4q + i).
+// Accumulators.  Wave A: xres (residual channels 16p + 4q + i of stream n), acc[0..2] skip tiles
+// 8p..8p+2, acc[3] the k-step-0 half of skip tile 8p+3.  Wave B: acc[0] the k-step-1 half of skip
+// tile 8p+3, acc[1..4] skip tiles 8p+4..8p+7.  In the head acc[0..3] hold the first 1x1's tiles
+// and acc[0..1] the output tiles of the wave's half.
 struct Acc {
-  f32x4 xres;  // residual stream: channels 16w + 4q + i of stream n
-  f32x4 acc[8];
+  f32x4 xres;
+  f32x4 acc[5];
 };
 
-// One layer stage.  `par` = stage parity (selects vbuf); xbuf parity follows the layer index.
-__device__ __forceinline__ void run_layer(const Ctx &c, int l, int par, Frags &W, int nx, Acc &A) {
+// W_r v + b for layer `ln`, computed by wave B one stage ahead from fragments f0..f0+3 (tanh tile
+// p k-steps 0,1, sigmoid tile p k-steps 0,1) and the popped rows in vbuf[par]; stored in pbuf[par].
+__device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int par, const Frags &W, int f0) {
   Lds &s = *c.s;
-  const int n = c.n, q = c.q, w = c.w;
+  const uint16_t *vb = s.vbuf[par] + c.n * PX;
+  const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
+  const float *cb = c.conv_b + ln * 2 * R;
+  f32x4 pt = ldsf4(cb + 16 * c.p + 4 * c.q), pg = ldsf4(cb + R + 16 * c.p + 4 * c.q);
+  pt = mfma(W.f[f0 + 0], bv0, pt);
+  pg = mfma(W.f[f0 + 2], bv0, pg);
+  pt = mfma(W.f[f0 + 1], bv1, pt);
+  pg = mfma(W.f[f0 + 3], bv1, pg);
+  stf4(s.pbuf[par][c.p][0] + c.n * PP + 4 * c.q, pt);
+  stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
+}
+
+// Layer stage of wave A (global stage index i): x -> W_e x + (W_r v + b) -> gate -> z | barrier |
+// residual 1x1 -> x^{l+1}, skip fragments.
+__device__ __forceinline__ void a_layer(const Ctx &c, int l, long long i, Frags &W, int nx, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  const int par = (int)(i & 1);
   u32x4 bx0, bx1;
   if (l == 0) {
-    // embedding (current input h^0_e): row gather of the transposed 1x1 convolution plus bias
+    // embedding (current input x^0): row gather of the transposed 1x1 convolution plus bias
     const int in = s.ins[n];
     const uint16_t *e = s.embT + in * R;
     const u32x4 r0 = lds16(e + 8 * q), r1 = lds16(e + 32 + 8 * q);
     const float *eb = c.emb_b;
     auto cvt = [&](u32x4 raw, int k0) {
-      u32x4 p;
+      u32x4 pk;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        p[j] = pack2(bf_lo(raw[j]) + eb[k0 + 2 * j], bf_hi(raw[j]) + eb[k0 + 2 * j + 1]);
-      return p;
+      for (int j = 0; j < 4; ++j) pk[j] = pack2(bf_lo(raw[j]) + eb[k0 + 2 * j], bf_hi(raw[j]) + eb[k0 + 2 * j + 1]);
+      return pk;
     };
     bx0 = cvt(r0, 8 * q);
     bx1 = cvt(r1, 32 + 8 * q);
-    // this wave's residual tile and its bf16 copy (pushed into queue 0 below)
-    const int ch = 16 * w + 4 * q;
+    // this wave's residual tile and its bf16 copy (pushed into queue 0 by wave B)
+    const int ch = 16 * p + 4 * q;
     const u32x2 raw = *(const u32x2 *)(e + ch);
     A.xres = f32x4{bf_lo(raw.x) + eb[ch], bf_hi(raw.x) + eb[ch + 1], bf_lo(raw.y) + eb[ch + 2],
                    bf_hi(raw.y) + eb[ch + 3]};
     lds8(s.xbuf[0] + n * PX + ch, pack4(A.xres));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) A.acc[j] = ldsf4(c.skip_sum + 128 * w + 16 * j + 4 * q);
+    for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.skip_sum + 128 * p + 16 * j + 4 * q);
   } else {
     const uint16_t *xb = s.xbuf[l & 1] + n * PX;
     bx0 = lds16(xb + 8 * q);
     bx1 = lds16(xb + 32 + 8 * q);
   }
-  const uint16_t *vb = s.vbuf[par] + n * PX;
-  const u32x4 bv0 = lds16(vb + 8 * q), bv1 = lds16(vb + 32 + 8 * q);
-  // dilated width-2 product: output rows 16w.. (tanh half) and 64 + 16w.. (sigmoid half)
-  const float *cb = c.conv_b + l * 2 * R;
-  f32x4 af = ldsf4(cb + 16 * w + 4 * q), ag = ldsf4(cb + R + 16 * w + 4 * q);
-  af = mfma(W.f[0], bv0, af);
-  ag = mfma(W.f[4], bv0, ag);
-  af = mfma(W.f[1], bv1, af);
-  ag = mfma(W.f[5], bv1, ag);
-  af = mfma(W.f[2], bx0, af);
-  ag = mfma(W.f[6], bx0, ag);
-  af = mfma(W.f[3], bx1, af);
-  ag = mfma(W.f[7], bx1, ag);
+  f32x4 af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q), ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
+  af = mfma(W.f[0], bx0, af);
+  ag = mfma(W.f[2], bx0, ag);
+  af = mfma(W.f[1], bx1, af);
+  ag = mfma(W.f[3], bx1, ag);
 #pragma unroll
-  for (int f = 0; f < 8; ++f) refill(c, W, nx, f);
+  for (int f = 0; f < 4; ++f) refill(c, W, nx, f);
   f32x4 z;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) z[i] = gate(af[i], ag[i]);
-  lds8(s.zbuf + n * PX + 16 * w + 4 * q, pack4(z));
+  for (int i4 = 0; i4 < 4; ++i4) z[i4] = gate(af[i4], ag[i4]);
+  lds8(s.zbuf + n * PX + 16 * p + 4 * q, pack4(z));
   __syncthreads();
-  // push phase: the layer's input x^{l-1}_t replaces the slot popped for this step
-  if (c.lane < 32) {
-    const int r = 4 * w + (c.lane >> 3);
-    const u32x4 v = *(const u32x4 *)(s.xbuf[l & 1] + r * PX + 8 * (c.lane & 7));
-    uint16_t *ring = (uint16_t *)c.a->ring;
-    __builtin_nontemporal_store(v, (u32x4 *)(ring + ring_elem(c, l, c.slot[l])));
-  }
   const uint16_t *zb = s.zbuf + n * PX;
   const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
-  // residual 1x1
-  f32x4 xr = A.xres + ldsf4(c.res_b + l * R + 16 * w + 4 * q);
-  xr = mfma(W.f[8], bz0, xr);
-  xr = mfma(W.f[9], bz1, xr);
-  refill(c, W, nx, 8);
-  refill(c, W, nx, 9);
+  f32x4 xr = A.xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
+  xr = mfma(W.f[4], bz0, xr);
+  xr = mfma(W.f[5], bz1, xr);
+  refill(c, W, nx, 4);
+  refill(c, W, nx, 5);
   A.xres = xr;
-  lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * w + 4 * q, pack4(xr));
-  // skip 1x1, accumulated over layers (k-step major: consecutive MFMAs use different accumulators)
+  lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * p + 4 * q, pack4(xr));
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    A.acc[j] = mfma(W.f[10 + j], bz0, A.acc[j]);
-    refill(c, W, nx, 10 + j);
+  for (int j = 0; j < 3; ++j) {
+    A.acc[j] = mfma(W.f[6 + j], bz0, A.acc[j]);
+    refill(c, W, nx, 6 + j);
   }
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    A.acc[j] = mfma(W.f[18 + j], bz1, A.acc[j]);
-    refill(c, W, nx, 18 + j);
+  for (int j = 0; j < 3; ++j) {
+    A.acc[j] = mfma(W.f[9 + j], bz1, A.acc[j]);
+    refill(c, W, nx, 9 + j);
+  }
+  A.acc[3] = mfma(W.f[12], bz0, A.acc[3]);
+  refill(c, W, nx, 12);
+}
+
+// Layer stage of wave B: W_r v + b of the next layer (its popped rows are already in LDS) |
+// barrier | push of the layer input, skip fragments.  `W` is the buffer of this stage's parity and
+// `nx` the fragment stream of the stage two ahead.
+__device__ __forceinline__ void b_layer(const Ctx &c, int l, long long i, Frags &W, int nx, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  const int par = (int)(i & 1);
+  if (l == 0) {
+    A.acc[0] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) A.acc[1 + j] = ldsf4(c.skip_sum + 128 * p + 64 + 16 * j + 4 * q);
+  }
+  if (l + 1 < c.L) recurrent_half(c, l + 1, par ^ 1, W, 0);
+#pragma unroll
+  for (int f = 0; f < 4; ++f) refill(c, W, nx, f);
+  __syncthreads();
+  push_rows(c, l);
+  const uint16_t *zb = s.zbuf + n * PX;
+  const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
+  A.acc[0] = mfma(W.f[4], bz1, A.acc[0]);
+  refill(c, W, nx, 4);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    A.acc[1 + j] = mfma(W.f[5 + j], bz0, A.acc[1 + j]);
+    refill(c, W, nx, 5 + j);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    A.acc[1 + j] = mfma(W.f[9 + j], bz1, A.acc[1 + j]);
+    refill(c, W, nx, 9 + j);
   }
 }
 
-// Head chunk C: fragments g = 26C .. 26C+25 of the head stream.
-template <int C>
-__device__ __forceinline__ void run_head(const Ctx &c, Frags &W, int nx, Acc &A) {
+// Head stage C: fragments g = 13C .. 13C+12 of the wave's head stream.  Wave A owns first-1x1
+// tiles 8p..8p+3 and output tiles 4p, 4p+1; wave B tiles 8p+4..8p+7 and 4p+2, 4p+3.  Barriers:
+// two at C = 0, one at the first output fragment (C = 4).
+static_assert(F * 4 + 12 == GH1, "the head's hidden-layer barrier sits in head stage 4");
+template <int C, bool ISA>
+__device__ __forceinline__ void run_head(const Ctx &c, long long i, Frags &W, int nx, Acc &A) {
   Lds &s = *c.s;
-  const int n = c.n, q = c.q, w = c.w;
+  const int n = c.n, q = c.q, p = c.p;
+  constexpr int hoff = ISA ? 0 : 64;  // channel offset of this wave's half inside the pair's 128
+  constexpr int ooff = ISA ? 0 : 32;  // class offset of this wave's half inside the pair's 64
   if (C == 0) {
-    // relu(skip sum) becomes the first head 1x1's input
+    // relu(skip sum) becomes the first head 1x1's input; skip tile 8p+3 is split over the pair
+    if (ISA) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      f32x4 r;
+      for (int j = 0; j < 3; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
+      stf4(s.ptile[p] + n * PP + 4 * q, A.acc[3]);
+    } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.acc[j][i], 0.f);
-      lds8(s.u.sbuf + n * PS + 128 * w + 16 * j + 4 * q, pack4(r));
-      A.acc[j] = ldsf4(c.head_b + 128 * w + 16 * j + 4 * q);
+      for (int j = 0; j < 4; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 64 + 16 * j + 4 * q, pack4(relu4(A.acc[1 + j])));
     }
+    __syncthreads();
+    if (!ISA) {
+      const f32x4 t = A.acc[0] + ldsf4(s.ptile[p] + n * PP + 4 * q);
+      lds8(s.u.sbuf + n * PS + 128 * p + 48 + 4 * q, pack4(relu4(t)));
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.head_b + 128 * p + hoff + 16 * j + 4 * q);
     __syncthreads();
   }
   u32x4 b = u32x4{0, 0, 0, 0};
 #pragma unroll
   for (int f = 0; f < F; ++f) {
     const int g = F * C + f;
-    if (g < G1) {
-      const int ks = g / 8, j = g % 8;
+    if (g < GH1) {
+      const int ks = g / 4, j = g % 4;
       if (j == 0 || f == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
       A.acc[j] = mfma(W.f[f], b, A.acc[j]);
-    } else if (g < G2) {
-      if (g == G1) {
+    } else if (g < GOUT) {
+      if (g == GH1) {
         // relu(head hidden) becomes the output 1x1's input
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          f32x4 r;
+        for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 128 * p + hoff + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
 #pragma unroll
-          for (int i = 0; i < 4; ++i) r[i] = fmaxf(A.acc[j][i], 0.f);
-          lds8(s.hbuf + n * PS + 128 * w + 16 * j + 4 * q, pack4(r));
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.out_b + 64 * w + 16 * j + 4 * q);
+        for (int j = 0; j < 2; ++j) A.acc[j] = ldsf4(c.out_b + 64 * p + ooff + 16 * j + 4 * q);
         __syncthreads();
       }
-      const int ks = (g - G1) / 4, j = (g - G1) % 4;
+      const int ks = (g - GH1) / 2, j = (g - GH1) % 2;
       if (j == 0 || f == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
       A.acc[j] = mfma(W.f[f], b, A.acc[j]);
+    } else if (g == GCV && !ISA) {
+      // W_r v + b of the next step's layer 0
+      recurrent_half(c, 0, (int)((i + 1) & 1), W, f);
     }
     refill(c, W, nx, f);
   }
 }
 
 // Stage the per-step inputs of steps [s0, s0 + KCH) in LDS: the uniform of (row r, step s) for
-// generation, the input of step s + 1 for teacher forcing.  Called by all threads once per chunk
-// (in the first head stage, before its barrier); waiting for these loads here keeps every other
-// wait in the step loop precise.
+// generation, the input of step s + 1 for teacher forcing.  Called by every thread of the block
+// once per chunk (in the first head stage, before its barriers).
 __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
   Lds &s = *c.s;
-  for (int i = threadIdx.x; i < ROWS * KCH; i += kThreads) {
+  for (int i = threadIdx.x; i < ROWS * KCH; i += NT) {
     const int r = i / KCH, j = i % KCH;
     const long long st = s0 + j;
     if (a.forced) {
@@ -354,25 +419,25 @@ __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
 }
 
 // End of a step: logits to LDS, sample (or write logits), next inputs, queue slots advance.
+template <bool ISA>
 __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A) {
   Lds &s = *c.s;
   const StepArgs &a = *c.a;
+  constexpr int ooff = ISA ? 0 : 32;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
-    *(float4 *)(s.u.lg + c.n * PL + 64 * c.w + 16 * j + 4 * c.q) =
-        make_float4(A.acc[j][0], A.acc[j][1], A.acc[j][2], A.acc[j][3]);
+  for (int j = 0; j < 2; ++j) stf4(s.u.lg + c.n * PL + 64 * c.p + ooff + 16 * j + 4 * c.q, A.acc[j]);
   __syncthreads();
   const int tid = threadIdx.x;
   if (a.forced) {
-    for (int r = c.w; r < c.nrows; r += 4) {
+    for (int r = c.w; r < c.nrows; r += kMfWaves) {
       const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
       *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
     }
     if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int r = c.w + 4 * kk;
+    for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
+      const int r = c.w + kMfWaves * kk;
       if (r >= c.nrows) break;
       const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
       if (c.lane == 0) {
@@ -381,7 +446,8 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
       }
     }
   }
-  for (int l = tid; l < c.L; l += kThreads) {
+  // waves A cover threads 0..255, more than the layer count
+  for (int l = tid; l < c.L; l += NT) {
     const int nx = c.slot[l] + 1;
     c.slot[l] = nx == c.dil[l] ? 0 : nx;
   }
@@ -395,32 +461,93 @@ struct Pos {
 };
 __device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
   p.k += m;
-  if (p.k >= c.NS) { p.k -= c.NS; p.step += 1; }
+  while (p.k >= c.NS) { p.k -= c.NS; p.step += 1; }
   return p;
 }
 
-__device__ __forceinline__ void run_stage(const Ctx &c, Pos p, int par, Frags &W, int nx, Acc &A) {
+// Stage body shared by the two roles' loops; `nx` is the fragment stream that refills W.
+template <bool ISA>
+__device__ __forceinline__ void run_stage(const Ctx &c, Pos p, long long i, Frags &W, int nx, Acc &A) {
   if (p.k < c.L) {
-    run_layer(c, p.k, par, W, nx, A);
+    if (ISA) a_layer(c, p.k, i, W, nx, A);
+    else b_layer(c, p.k, i, W, nx, A);
   } else {
     switch (p.k - c.L) {
       case 0:
         if (p.step % KCH == 0) stage_chunk(c, p.step);
-        run_head<0>(c, W, nx, A);
+        run_head<0, ISA>(c, i, W, nx, A);
         break;
-      case 1: run_head<1>(c, W, nx, A); break;
-      case 2: run_head<2>(c, W, nx, A); break;
-      case 3: run_head<3>(c, W, nx, A); break;
-      case 4: run_head<4>(c, W, nx, A); break;
-      case 5: run_head<5>(c, W, nx, A); break;
-      case 6: run_head<6>(c, W, nx, A); break;
-      default: run_head<7>(c, W, nx, A); break;
+      case 1: run_head<1, ISA>(c, i, W, nx, A); break;
+      case 2: run_head<2, ISA>(c, i, W, nx, A); break;
+      case 3: run_head<3, ISA>(c, i, W, nx, A); break;
+      case 4: run_head<4, ISA>(c, i, W, nx, A); break;
+      case 5: run_head<5, ISA>(c, i, W, nx, A); break;
+      case 6: run_head<6, ISA>(c, i, W, nx, A); break;
+      default:
+        run_head<7, ISA>(c, i, W, nx, A);
+        finish_step<ISA>(c, p.step, A);
+        break;
     }
   }
-  if (p.k == c.NS - 1) finish_step(c, p.step, A);
 }
 
-__global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
+// Main loop of wave A: one fragment buffer, each slot refilled with the next stage's.
+__device__ __forceinline__ void a_role(const Ctx &c, long long total) {
+  Acc A;
+  Frags W;
+  __syncthreads();  // queue rows of stages 0 and 1 are in LDS
+  load_stage(c, 0, W);
+  __syncthreads();  // W_r v + b of layer 0 is in LDS
+  Pos p0{0, 0};
+  for (long long i = 0; i < total; ++i) {
+    const Pos p1 = advance(c, p0, 1);
+    run_stage<true>(c, p0, i, W, stage_off(c, p1.k), A);
+    __syncthreads();
+    p0 = p1;
+  }
+}
+
+// Main loop of wave B: two fragment buffers by stage parity, each slot refilled with the stage two
+// ahead; queue rows of stage i+3 are read at the start of stage i and land in LDS at the end of
+// stage i+1, for the W_r v of stage i+3 computed during stage i+2.
+__device__ __forceinline__ void b_role(const Ctx &c, long long total) {
+  Acc A;
+  Frags W0, W1;
+  const Pos p0i{0, 0};
+  const Pos p1i = advance(c, p0i, 1), p2i = advance(c, p0i, 2);
+  pop_land(c, 0, pop_issue(c, 0, 0));
+  pop_land(c, 1, pop_issue(c, p1i.k, (int)p1i.step));
+  u32x4 vA, vB = pop_issue(c, p2i.k, (int)p2i.step);
+  __syncthreads();
+  {
+    // W_r v + b of layer 0 from this wave's fragments in the last head stage
+    const int off = stage_off(c, c.NS - 1);
+#pragma unroll
+    for (int f = 0; f < 4; ++f) W0.f[f] = load_frag(c, off, GCV - F * (NHEAD - 1) + f);
+    recurrent_half(c, 0, 0, W0, 0);
+  }
+  load_stage(c, 0, W0);
+  load_stage(c, p1i.k, W1);
+  __syncthreads();
+  Pos p0 = p0i;
+  for (long long i = 0; i < total; i += 2) {
+    const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3), p4 = advance(c, p0, 4);
+    vA = pop_issue(c, p3.k, (int)(p3.step - p0.step));
+    __builtin_amdgcn_sched_barrier(0);
+    run_stage<false>(c, p0, i, W0, stage_off(c, p2.k), A);
+    if (p2.k < c.L && i + 2 < total) pop_land(c, 0, vB);
+    __syncthreads();
+    if (i + 1 >= total) break;
+    vB = pop_issue(c, p4.k, (int)(p4.step - p1.step));
+    __builtin_amdgcn_sched_barrier(0);
+    run_stage<false>(c, p1, i + 1, W1, stage_off(c, p3.k), A);
+    if (p3.k < c.L && i + 3 < total) pop_land(c, 1, vA);
+    __syncthreads();
+    p0 = p2;
+  }
+}
+
+__global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   Lds &s = *(Lds *)lds_raw;
   const int tid = threadIdx.x;
@@ -446,22 +573,22 @@ __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
   c.emb_b = c.out_b + Q;
   c.L = L;
   c.NS = L + NHEAD;
-  c.w = tid >> 6;
+  c.w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  c.p = c.w & 3;
   c.lane = tid & 63;
   c.n = c.lane & 15;
   c.q = c.lane >> 4;
   c.b0 = blockIdx.x * ROWS;
   c.nrows = min(ROWS, a.batch - c.b0);
-  c.w = __builtin_amdgcn_readfirstlane(c.w);
-  c.wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)a.mf_frags, (short)0, mfma_frag_bytes(L), 0x00020000);
+  c.frags = (const char *)a.mf_frags;
   c.wvoff = 16 * c.lane;
 
   // tables: embedding [Q][R], biases, queue offsets, dilations and slots
   const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
-  for (int i = tid; i < Q * R / 8; i += kThreads) ((u32x4 *)s.embT)[i] = embsrc[i];
+  for (int i = tid; i < Q * R / 8; i += NT) ((u32x4 *)s.embT)[i] = embsrc[i];
   const int nbias = L * 3 * R + S + H + Q + R;
-  for (int i = tid; i < nbias; i += kThreads) bias[i] = a.mf_bias[i];
-  for (int l = tid; l < L; l += kThreads) {
+  for (int i = tid; i < nbias; i += NT) bias[i] = a.mf_bias[i];
+  for (int l = tid; l < L; l += NT) {
     const LayerDev ld = a.layers[l];
     roff[l] = ld.ring_off;
     dil[l] = ld.dil;
@@ -475,32 +602,8 @@ __global__ void __launch_bounds__(kThreads) mfma_step_kernel(StepArgs a) {
   __syncthreads();
 
   const long long total = (long long)a.n_steps * c.NS;
-  Acc A;
-  Frags W;  // one stage of fragments; each slot is refilled with the next stage's right after use
-  Pos p0{0, 0};
-  // prologue: stage 0's queue rows land now, stage 1's are in flight; stage 0's weights
-  pop_land(c, 0, pop_issue(c, 0, 0));
-  u32x4 vA, vB = pop_issue(c, 1 < L ? 1 : 0, 0);
-  load_stage(c, 0, W);
-  __syncthreads();
-
-  for (long long i = 0; i < total; i += 2) {
-    const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3);
-    // ---- even stage: queue rows of stage i+2 in flight into vA, rows of stage i+1 land
-    vA = pop_issue(c, p2.k, (int)(p2.step - p0.step));
-    __builtin_amdgcn_sched_barrier(0);  // issue the queue read before this stage's refills
-    run_stage(c, p0, (int)(i & 1), W, stage_off(c, p1.k), A);
-    if (p1.k < L && i + 1 < total) pop_land(c, (int)((i + 1) & 1), vB);
-    __syncthreads();
-    if (i + 1 >= total) break;
-    // ---- odd stage: rows of stage i+3 in flight into vB, rows of stage i+2 land
-    vB = pop_issue(c, p3.k, (int)(p3.step - p1.step));
-    __builtin_amdgcn_sched_barrier(0);
-    run_stage(c, p1, (int)((i + 1) & 1), W, stage_off(c, p2.k), A);
-    if (p2.k < L && i + 2 < total) pop_land(c, (int)(i & 1), vA);
-    __syncthreads();
-    p0 = p2;
-  }
+  if (c.w < 4) a_role(c, total);
+  else b_role(c, total);
   if (!a.forced && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
 }
 
@@ -512,7 +615,7 @@ size_t mfma_lds_bytes(int L) {
 
 hipError_t launch_mfma_step(const StepArgs &a, hipStream_t s) {
   const size_t lds = mfma_lds_bytes(a.L);
-  const dim3 grid((a.batch + kMfRows - 1) / kMfRows), block(kThreads);
+  const dim3 grid((a.batch + kMfRows - 1) / kMfRows), block(kMfThreads);
   hipLaunchKernelGGL(mf::mfma_step_kernel, grid, block, lds, s, a);
   return hipGetLastError();
 }
@@ -525,6 +628,7 @@ hipError_t set_mfma_lds_limit(size_t bytes) {
 // ---------------------------------------------------------------------------
 // Repacking into per-wave fragment streams.  Fragment (tile t, k-step ks) of a
 // matrix M[out][k] gives lane l the 8 values M[16t + l%16][32ks + 8(l/16) + j].
+// Stage k of the stream holds, for each of the 8 waves, F fragments of 1 KB.
 namespace mf {
 
 // element of the conv matrix [2R][2R] with k < R the recurrent tap and k >= R the current tap
@@ -532,54 +636,90 @@ __device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int o, int k
   return conv[(o * R + (k % R)) * 2 + (k >= R ? 1 : 0)];
 }
 
-__global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, uint4 *dst) {
-  // dst: this layer's stage, 4 waves x F fragments x 64 lanes x 8 elements
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= 4 * F * 64) return;
-  const int lane = e % 64, f = (e / 64) % F, w = e / (64 * F);
-  const int m = lane % 16, kq = 8 * (lane / 16);
-  uint16_t v[8];
-  for (int j = 0; j < 8; ++j) {
-    int o, k;
-    if (f < 8) {
-      const int t = f < 4 ? w : 4 + w, ks = f % 4;
-      o = 16 * t + m;
-      k = 32 * ks + kq + j;
-      v[j] = conv_elem(conv, o, k);
-    } else if (f < 10) {
-      o = 16 * w + m;
-      k = 32 * (f - 8) + kq + j;
-      v[j] = res[o * R + k];
-    } else {
-      const int jj = (f - 10) % 8, ks = (f - 10) / 8;
-      o = 16 * (8 * w + jj) + m;
-      k = 32 * ks + kq + j;
-      v[j] = skip[o * R + k];
-    }
-  }
-  dst[e] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
+__device__ __forceinline__ uint4 pack8(const uint16_t *v) {
+  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
-__global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, uint4 *dst) {
-  // dst: NHEAD stages of 4 waves x F fragments x 64 lanes; head fragment g = F*stage + f
+// Layer l's fragments.  Wave A (p = w < 4), stage l: f0..f3 conv x-half (tanh tile p k-steps 2,3,
+// sigmoid tile p k-steps 2,3), f4..f5 residual tile p, f6..f8 skip tiles 8p..8p+2 k-step 0,
+// f9..f11 the same tiles k-step 1, f12 skip tile 8p+3 k-step 0.  Wave B (p = w - 4), stage l:
+// f4 skip tile 8p+3 k-step 1, f5..f8 skip tiles 8p+4..8p+7 k-step 0, f9..f12 k-step 1; its conv
+// v-half of layer l (tanh tile p k-steps 0,1, sigmoid tile p k-steps 0,1) goes to f0..f3 of stage
+// l - 1, or for layer 0 to the last head stage (head stream positions GCV..GCV+3).  The last
+// layer also zeroes its own wave-B f0..f3 (no next layer inside the step).
+__global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, int l, int L,
+                                    uint4 *frags) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= NHEAD * 4 * F * 64) return;
-  const int lane = e % 64, f = (e / 64) % F, w = (e / (64 * F)) % 4, st = e / (64 * F * 4);
+  if (e >= kMfWaves * F * 64) return;
+  const int lane = e % 64, f = (e / 64) % F, w = e / (64 * F);
+  const int m = lane % 16, kq = 8 * (lane / 16);
+  const int NS = L + NHEAD;
+  auto at = [&](int stage, int wave, int frag) {
+    return frags + ((size_t)(stage * kMfWaves + wave) * F + frag) * 64 + lane;
+  };
+  uint16_t v[8];
+  if (w < 4) {
+    const int p = w;
+    for (int j = 0; j < 8; ++j) {
+      if (f < 4) {
+        const int o = (f < 2 ? 0 : R) + 16 * p + m;
+        v[j] = conv_elem(conv, o, R + 32 * (f & 1) + kq + j);
+      } else if (f < 6) {
+        v[j] = res[(16 * p + m) * R + 32 * (f - 4) + kq + j];
+      } else {
+        const int t = f < 9 ? 8 * p + (f - 6) : f < 12 ? 8 * p + (f - 9) : 8 * p + 3;
+        const int ks = (f >= 9 && f < 12) ? 1 : 0;
+        v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
+      }
+    }
+    *at(l, w, f) = pack8(v);
+  } else {
+    const int p = w - 4;
+    if (f < 4) {
+      for (int j = 0; j < 8; ++j) {
+        const int o = (f < 2 ? 0 : R) + 16 * p + m;
+        v[j] = conv_elem(conv, o, 32 * (f & 1) + kq + j);
+      }
+      if (l > 0) *at(l - 1, w, f) = pack8(v);
+      else *at(NS - 1, w, GCV - F * (NHEAD - 1) + f) = pack8(v);
+      if (l == L - 1) *at(l, w, f) = make_uint4(0, 0, 0, 0);
+    } else {
+      for (int j = 0; j < 8; ++j) {
+        const int t = f == 4 ? 8 * p + 3 : f < 9 ? 8 * p + 4 + (f - 5) : 8 * p + 4 + (f - 9);
+        const int ks = (f == 4 || f >= 9) ? 1 : 0;
+        v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
+      }
+      *at(l, w, f) = pack8(v);
+    }
+  }
+}
+
+// Head stages L .. L+7.  Wave stream g = 13 h + f: g < 64 first 1x1 tile (8p + g%4, wave B
+// 8p + 4 + g%4) k-step g/4; 64 <= g < 96 output tile (4p + (g-64)%2, wave B 4p + 2 + ...) k-step
+// (g-64)/2; the rest zero, except wave B's GCV..GCV+3 (layer 0's v-half, written by the layer
+// repack and left alone here).
+__global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, int L, uint4 *frags) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= NHEAD * kMfWaves * F * 64) return;
+  const int lane = e % 64, f = (e / 64) % F, w = (e / (64 * F)) % kMfWaves, st = e / (64 * F * kMfWaves);
   const int m = lane % 16, kq = 8 * (lane / 16);
   const int g = F * st + f;
+  const bool isA = w < 4;
+  const int p = w & 3;
+  if (!isA && g >= GCV && g < GCV + 4) return;
   uint16_t v[8];
   for (int j = 0; j < 8; ++j) {
-    if (g < G1) {
-      const int t = 8 * w + g % 8, ks = g / 8;
+    if (g < GH1) {
+      const int t = 8 * p + (isA ? 0 : 4) + g % 4, ks = g / 4;
       v[j] = head[(16 * t + m) * S + 32 * ks + kq + j];
-    } else if (g < G2) {
-      const int t = 4 * w + (g - G1) % 4, ks = (g - G1) / 4;
+    } else if (g < GOUT) {
+      const int t = 4 * p + (isA ? 0 : 2) + (g - GH1) % 2, ks = (g - GH1) / 2;
       v[j] = out[(16 * t + m) * H + 32 * ks + kq + j];
     } else {
       v[j] = 0;
     }
   }
-  dst[e] = make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
+  frags[((size_t)((L + st) * kMfWaves + w) * F + f) * 64 + lane] = pack8(v);
 }
 
 __global__ void embed_table_kernel(const uint16_t *embed, uint16_t *dst) {
@@ -621,17 +761,18 @@ __global__ void bias_block_kernel(const float *const *conv_b, const float *const
 
 }  // namespace mf
 
-hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, void *dst, hipStream_t s) {
-  const int n = 4 * kMfFrags * 64;
+hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
+                                    hipStream_t s) {
+  const int n = kMfWaves * kMfFrags * 64;
   hipLaunchKernelGGL(mf::repack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)conv,
-                     (const uint16_t *)res, (const uint16_t *)skip, (uint4 *)dst);
+                     (const uint16_t *)res, (const uint16_t *)skip, l, L, (uint4 *)frags);
   return hipGetLastError();
 }
 
-hipError_t launch_mfma_repack_head(const void *head, const void *out, void *dst, hipStream_t s) {
-  const int n = kMfHeadStages * 4 * kMfFrags * 64;
+hipError_t launch_mfma_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s) {
+  const int n = kMfHeadStages * kMfWaves * kMfFrags * 64;
   hipLaunchKernelGGL(mf::repack_head_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)head,
-                     (const uint16_t *)out, (uint4 *)dst);
+                     (const uint16_t *)out, L, (uint4 *)frags);
   return hipGetLastError();
 }
 
