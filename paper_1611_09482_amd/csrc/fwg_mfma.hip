@@ -238,165 +238,18 @@ __device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int par, co
   stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
 }
 
-// Layer stage of wave A (global stage index i): x -> W_e x + (W_r v + b) -> gate -> z | barrier |
-// residual 1x1 -> x^{l+1}, skip fragments.
-__device__ __forceinline__ void a_layer(const Ctx &c, int l, long long i, Frags &W, int nx, Acc &A) {
-  Lds &s = *c.s;
-  const int n = c.n, q = c.q, p = c.p;
-  const int par = (int)(i & 1);
-  u32x4 bx0, bx1;
-  if (l == 0) {
-    // embedding (current input x^0): row gather of the transposed 1x1 convolution plus bias
-    const int in = s.ins[n];
-    const uint16_t *e = s.embT + in * R;
-    const u32x4 r0 = lds16(e + 8 * q), r1 = lds16(e + 32 + 8 * q);
-    const float *eb = c.emb_b;
-    auto cvt = [&](u32x4 raw, int k0) {
-      u32x4 pk;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) pk[j] = pack2(bf_lo(raw[j]) + eb[k0 + 2 * j], bf_hi(raw[j]) + eb[k0 + 2 * j + 1]);
-      return pk;
-    };
-    bx0 = cvt(r0, 8 * q);
-    bx1 = cvt(r1, 32 + 8 * q);
-    // this wave's residual tile and its bf16 copy (pushed into queue 0 by wave B)
-    const int ch = 16 * p + 4 * q;
-    const u32x2 raw = *(const u32x2 *)(e + ch);
-    A.xres = f32x4{bf_lo(raw.x) + eb[ch], bf_hi(raw.x) + eb[ch + 1], bf_lo(raw.y) + eb[ch + 2],
-                   bf_hi(raw.y) + eb[ch + 3]};
-    lds8(s.xbuf[0] + n * PX + ch, pack4(A.xres));
-#pragma unroll
-    for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.skip_sum + 128 * p + 16 * j + 4 * q);
-  } else {
-    const uint16_t *xb = s.xbuf[l & 1] + n * PX;
-    bx0 = lds16(xb + 8 * q);
-    bx1 = lds16(xb + 32 + 8 * q);
-  }
-  f32x4 af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q), ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
-  af = mfma(W.f[0], bx0, af);
-  ag = mfma(W.f[2], bx0, ag);
-  af = mfma(W.f[1], bx1, af);
-  ag = mfma(W.f[3], bx1, ag);
-#pragma unroll
-  for (int f = 0; f < 4; ++f) refill(c, W, nx, f);
-  f32x4 z;
-#pragma unroll
-  for (int i4 = 0; i4 < 4; ++i4) z[i4] = gate(af[i4], ag[i4]);
-  lds8(s.zbuf + n * PX + 16 * p + 4 * q, pack4(z));
-  __syncthreads();
-  const uint16_t *zb = s.zbuf + n * PX;
-  const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
-  f32x4 xr = A.xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
-  xr = mfma(W.f[4], bz0, xr);
-  xr = mfma(W.f[5], bz1, xr);
-  refill(c, W, nx, 4);
-  refill(c, W, nx, 5);
-  A.xres = xr;
-  lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * p + 4 * q, pack4(xr));
-#pragma unroll
-  for (int j = 0; j < 3; ++j) {
-    A.acc[j] = mfma(W.f[6 + j], bz0, A.acc[j]);
-    refill(c, W, nx, 6 + j);
-  }
-#pragma unroll
-  for (int j = 0; j < 3; ++j) {
-    A.acc[j] = mfma(W.f[9 + j], bz1, A.acc[j]);
-    refill(c, W, nx, 9 + j);
-  }
-  A.acc[3] = mfma(W.f[12], bz0, A.acc[3]);
-  refill(c, W, nx, 12);
+// Stage position helpers.
+struct Pos {
+  long long step;
+  int k;
+};
+__device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
+  p.k += m;
+  while (p.k >= c.NS) { p.k -= c.NS; p.step += 1; }
+  return p;
 }
 
-// Layer stage of wave B: W_r v + b of the next layer (its popped rows are already in LDS) |
-// barrier | push of the layer input, skip fragments.  `W` is the buffer of this stage's parity and
-// `nx` the fragment stream of the stage two ahead.
-__device__ __forceinline__ void b_layer(const Ctx &c, int l, long long i, Frags &W, int nx, Acc &A) {
-  Lds &s = *c.s;
-  const int n = c.n, q = c.q, p = c.p;
-  const int par = (int)(i & 1);
-  if (l == 0) {
-    A.acc[0] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) A.acc[1 + j] = ldsf4(c.skip_sum + 128 * p + 64 + 16 * j + 4 * q);
-  }
-  if (l + 1 < c.L) recurrent_half(c, l + 1, par ^ 1, W, 0);
-#pragma unroll
-  for (int f = 0; f < 4; ++f) refill(c, W, nx, f);
-  __syncthreads();
-  push_rows(c, l);
-  const uint16_t *zb = s.zbuf + n * PX;
-  const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
-  A.acc[0] = mfma(W.f[4], bz1, A.acc[0]);
-  refill(c, W, nx, 4);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    A.acc[1 + j] = mfma(W.f[5 + j], bz0, A.acc[1 + j]);
-    refill(c, W, nx, 5 + j);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    A.acc[1 + j] = mfma(W.f[9 + j], bz1, A.acc[1 + j]);
-    refill(c, W, nx, 9 + j);
-  }
-}
-
-// Head stage C: fragments g = 13C .. 13C+12 of the wave's head stream.  Wave A owns first-1x1
-// tiles 8p..8p+3 and output tiles 4p, 4p+1; wave B tiles 8p+4..8p+7 and 4p+2, 4p+3.  Barriers:
-// two at C = 0, one at the first output fragment (C = 4).
-static_assert(F * 4 + 12 == GH1, "the head's hidden-layer barrier sits in head stage 4");
-template <int C, bool ISA>
-__device__ __forceinline__ void run_head(const Ctx &c, long long i, Frags &W, int nx, Acc &A) {
-  Lds &s = *c.s;
-  const int n = c.n, q = c.q, p = c.p;
-  constexpr int hoff = ISA ? 0 : 64;  // channel offset of this wave's half inside the pair's 128
-  constexpr int ooff = ISA ? 0 : 32;  // class offset of this wave's half inside the pair's 64
-  if (C == 0) {
-    // relu(skip sum) becomes the first head 1x1's input; skip tile 8p+3 is split over the pair
-    if (ISA) {
-#pragma unroll
-      for (int j = 0; j < 3; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
-      stf4(s.ptile[p] + n * PP + 4 * q, A.acc[3]);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 64 + 16 * j + 4 * q, pack4(relu4(A.acc[1 + j])));
-    }
-    __syncthreads();
-    if (!ISA) {
-      const f32x4 t = A.acc[0] + ldsf4(s.ptile[p] + n * PP + 4 * q);
-      lds8(s.u.sbuf + n * PS + 128 * p + 48 + 4 * q, pack4(relu4(t)));
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.head_b + 128 * p + hoff + 16 * j + 4 * q);
-    __syncthreads();
-  }
-  u32x4 b = u32x4{0, 0, 0, 0};
-#pragma unroll
-  for (int f = 0; f < F; ++f) {
-    const int g = F * C + f;
-    if (g < GH1) {
-      const int ks = g / 4, j = g % 4;
-      if (j == 0 || f == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
-      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
-    } else if (g < GOUT) {
-      if (g == GH1) {
-        // relu(head hidden) becomes the output 1x1's input
-#pragma unroll
-        for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 128 * p + hoff + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
-#pragma unroll
-        for (int j = 0; j < 2; ++j) A.acc[j] = ldsf4(c.out_b + 64 * p + ooff + 16 * j + 4 * q);
-        __syncthreads();
-      }
-      const int ks = (g - GH1) / 2, j = (g - GH1) % 2;
-      if (j == 0 || f == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
-      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
-    } else if (g == GCV && !ISA) {
-      // W_r v + b of the next step's layer 0
-      recurrent_half(c, 0, (int)((i + 1) & 1), W, f);
-    }
-    refill(c, W, nx, f);
-  }
-}
-
+// Stage body shared by the two roles' loops; `nx` is the fragment stream that refills W.
 // Stage the per-step inputs of steps [s0, s0 + KCH) in LDS: the uniform of (row r, step s) for
 // generation, the input of step s + 1 for teacher forcing.  Called by every thread of the block
 // once per chunk (in the first head stage, before its barriers).
@@ -428,21 +281,27 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
   for (int j = 0; j < 2; ++j) stf4(s.u.lg + c.n * PL + 64 * c.p + ooff + 16 * j + 4 * c.q, A.acc[j]);
   __syncthreads();
   const int tid = threadIdx.x;
+  // straight-line code (no loop exits), which keeps the compiler's load accounting precise
   if (a.forced) {
-    for (int r = c.w; r < c.nrows; r += kMfWaves) {
-      const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
-      *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
+#pragma unroll
+    for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
+      const int r = c.w + kMfWaves * kk;
+      if (r < c.nrows) {
+        const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
+        *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
+      }
     }
     if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
 #pragma unroll
     for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
       const int r = c.w + kMfWaves * kk;
-      if (r >= c.nrows) break;
-      const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
-      if (c.lane == 0) {
-        a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
-        s.ins[r] = k;
+      if (r < c.nrows) {
+        const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
+        if (c.lane == 0) {
+          a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
+          s.ins[r] = k;
+        }
       }
     }
   }
@@ -454,41 +313,229 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
   __syncthreads();
 }
 
-// Stage position helpers.
-struct Pos {
-  long long step;
-  int k;
-};
-__device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
-  p.k += m;
-  while (p.k >= c.NS) { p.k -= c.NS; p.step += 1; }
-  return p;
-}
-
-// Stage body shared by the two roles' loops; `nx` is the fragment stream that refills W.
-template <bool ISA>
-__device__ __forceinline__ void run_stage(const Ctx &c, Pos p, long long i, Frags &W, int nx, Acc &A) {
-  if (p.k < c.L) {
-    if (ISA) a_layer(c, p.k, i, W, nx, A);
-    else b_layer(c, p.k, i, W, nx, A);
-  } else {
-    switch (p.k - c.L) {
-      case 0:
-        if (p.step % KCH == 0) stage_chunk(c, p.step);
-        run_head<0, ISA>(c, i, W, nx, A);
-        break;
-      case 1: run_head<1, ISA>(c, i, W, nx, A); break;
-      case 2: run_head<2, ISA>(c, i, W, nx, A); break;
-      case 3: run_head<3, ISA>(c, i, W, nx, A); break;
-      case 4: run_head<4, ISA>(c, i, W, nx, A); break;
-      case 5: run_head<5, ISA>(c, i, W, nx, A); break;
-      case 6: run_head<6, ISA>(c, i, W, nx, A); break;
-      default:
-        run_head<7, ISA>(c, i, W, nx, A);
-        finish_step<ISA>(c, p.step, A);
-        break;
+// Head stage C, fragments [F0, F1) of the wave's head stream g = 13C + f.  Wave A owns first-1x1
+// tiles 8p..8p+3 and output tiles 4p, 4p+1; wave B tiles 8p+4..8p+7 and 4p+2, 4p+3.  One barrier
+// at the first output fragment (g = GH1, in head stage 4).
+static_assert(F * 4 + 12 == GH1, "the head's hidden-layer barrier sits in head stage 4");
+template <int C, bool ISA, int F0, int F1>
+__device__ __forceinline__ void head_frags(const Ctx &c, long long i, const Frags &W, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  constexpr int hoff = ISA ? 0 : 64;  // channel offset of this wave's half inside the pair's 128
+  constexpr int ooff = ISA ? 0 : 32;  // class offset of this wave's half inside the pair's 64
+  u32x4 b = u32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int f = F0; f < F1; ++f) {
+    const int g = F * C + f;
+    if (g < GH1) {
+      const int ks = g / 4, j = g % 4;
+      if (j == 0 || f == F0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
+      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
+    } else if (g < GOUT) {
+      if (g == GH1) {
+        // relu(head hidden) becomes the output 1x1's input
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 128 * p + hoff + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
+#pragma unroll
+        for (int j = 0; j < 2; ++j) A.acc[j] = ldsf4(c.out_b + 64 * p + ooff + 16 * j + 4 * q);
+        __syncthreads();
+      }
+      const int ks = (g - GH1) / 2, j = (g - GH1) % 2;
+      if (j == 0 || f == F0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
+      A.acc[j] = mfma(W.f[f], b, A.acc[j]);
+    } else if (g == GCV && !ISA) {
+      // W_r v + b of the next step's layer 0
+      recurrent_half(c, 0, (int)((i + 1) & 1), W, f);
     }
   }
+}
+
+// Start of head stage 0: relu(skip sum) becomes the first head 1x1's input (skip tile 8p+3 is
+// split over the pair), then the head accumulators take the first 1x1's bias.  Two barriers.
+template <bool ISA>
+__device__ __forceinline__ void head_start(const Ctx &c, Pos p0, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  constexpr int hoff = ISA ? 0 : 64;
+  if (p0.step % KCH == 0) stage_chunk(c, p0.step);
+  if (ISA) {
+#pragma unroll
+    for (int j = 0; j < 3; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 16 * j + 4 * q, pack4(relu4(A.acc[j])));
+    stf4(s.ptile[p] + n * PP + 4 * q, A.acc[3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) lds8(s.u.sbuf + n * PS + 128 * p + 64 + 16 * j + 4 * q, pack4(relu4(A.acc[1 + j])));
+  }
+  __syncthreads();
+  if (!ISA) {
+    const f32x4 t = A.acc[0] + ldsf4(s.ptile[p] + n * PP + 4 * q);
+    lds8(s.u.sbuf + n * PS + 128 * p + 48 + 4 * q, pack4(relu4(t)));
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.head_b + 128 * p + hoff + 16 * j + 4 * q);
+  __syncthreads();
+}
+
+template <bool ISA, int F0, int F1>
+__device__ __forceinline__ void head_part(const Ctx &c, Pos p0, long long i, const Frags &W, Acc &A) {
+  switch (p0.k - c.L) {
+    case 0:
+      if (F0 == 0) head_start<ISA>(c, p0, A);
+      head_frags<0, ISA, F0, F1>(c, i, W, A);
+      break;
+    case 1: head_frags<1, ISA, F0, F1>(c, i, W, A); break;
+    case 2: head_frags<2, ISA, F0, F1>(c, i, W, A); break;
+    case 3: head_frags<3, ISA, F0, F1>(c, i, W, A); break;
+    case 4: head_frags<4, ISA, F0, F1>(c, i, W, A); break;
+    case 5: head_frags<5, ISA, F0, F1>(c, i, W, A); break;
+    case 6: head_frags<6, ISA, F0, F1>(c, i, W, A); break;
+    default: head_frags<7, ISA, F0, F1>(c, i, W, A); break;
+  }
+}
+static_assert(NHEAD == 8, "head_part dispatches eight head stages");
+
+// Refill fragment slots [F0, F1) from stage stream `nx`.
+template <int F0, int F1>
+__device__ __forceinline__ void refill_range(const Ctx &c, Frags &W, int nx) {
+#pragma unroll
+  for (int f = F0; f < F1; ++f) refill(c, W, nx, f);
+}
+
+// Every stage of either role runs as parts that consume fragment slots [0,4), [4,6) and [6,13)
+// in that order, whatever the stage type; the slots are refilled between the parts, in code
+// common to all stage types, so each fragment register has a single definition in the loop (per
+// stage-type refills would make the compiler copy registers at the merge, which waits for every
+// outstanding load).
+
+// Stage of wave A (global stage index i).  Layer: x -> W_e x + (W_r v + b) -> gate -> z |
+// barrier | residual 1x1 -> x^{l+1}, skip fragments.
+__device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags &W, int nx, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  const int par = (int)(i & 1);
+  const int l = p0.k;
+  const bool layer = l < c.L;
+  f32x4 af, ag;
+  // ---- slots 0..3: the current-input half of the dilated product
+  if (layer) {
+    u32x4 bx0, bx1;
+    if (l == 0) {
+      // embedding (current input x^0): row gather of the transposed 1x1 convolution plus bias
+      const int in = s.ins[n];
+      const uint16_t *e = s.embT + in * R;
+      const u32x4 r0 = lds16(e + 8 * q), r1 = lds16(e + 32 + 8 * q);
+      const float *eb = c.emb_b;
+      auto cvt = [&](u32x4 raw, int k0) {
+        u32x4 pk;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pk[j] = pack2(bf_lo(raw[j]) + eb[k0 + 2 * j], bf_hi(raw[j]) + eb[k0 + 2 * j + 1]);
+        return pk;
+      };
+      bx0 = cvt(r0, 8 * q);
+      bx1 = cvt(r1, 32 + 8 * q);
+      // this wave's residual tile and its bf16 copy (pushed into queue 0 by wave B)
+      const int ch = 16 * p + 4 * q;
+      const u32x2 raw = *(const u32x2 *)(e + ch);
+      A.xres = f32x4{bf_lo(raw.x) + eb[ch], bf_hi(raw.x) + eb[ch + 1], bf_lo(raw.y) + eb[ch + 2],
+                     bf_hi(raw.y) + eb[ch + 3]};
+      lds8(s.xbuf[0] + n * PX + ch, pack4(A.xres));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) A.acc[j] = ldsf4(c.skip_sum + 128 * p + 16 * j + 4 * q);
+    } else {
+      const uint16_t *xb = s.xbuf[l & 1] + n * PX;
+      bx0 = lds16(xb + 8 * q);
+      bx1 = lds16(xb + 32 + 8 * q);
+    }
+    af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q);
+    ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
+    af = mfma(W.f[0], bx0, af);
+    ag = mfma(W.f[2], bx0, ag);
+    af = mfma(W.f[1], bx1, af);
+    ag = mfma(W.f[3], bx1, ag);
+  } else {
+    head_part<true, 0, 4>(c, p0, i, W, A);
+  }
+  refill_range<0, 4>(c, W, nx);
+  u32x4 bz0, bz1;
+  if (layer) {
+    f32x4 z;
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) z[i4] = gate(af[i4], ag[i4]);
+    lds8(s.zbuf + n * PX + 16 * p + 4 * q, pack4(z));
+    __syncthreads();
+    // ---- slots 4, 5: residual 1x1 -> x^{l+1}
+    const uint16_t *zb = s.zbuf + n * PX;
+    bz0 = lds16(zb + 8 * q);
+    bz1 = lds16(zb + 32 + 8 * q);
+    f32x4 xr = A.xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
+    xr = mfma(W.f[4], bz0, xr);
+    xr = mfma(W.f[5], bz1, xr);
+    A.xres = xr;
+    lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * p + 4 * q, pack4(xr));
+  } else {
+    head_part<true, 4, 6>(c, p0, i, W, A);
+  }
+  refill_range<4, 6>(c, W, nx);
+  // ---- slots 6..12: skip tiles 8p..8p+2 (both k-steps) and the k-step-0 half of tile 8p+3
+  if (layer) {
+#pragma unroll
+    for (int j = 0; j < 3; ++j) A.acc[j] = mfma(W.f[6 + j], bz0, A.acc[j]);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) A.acc[j] = mfma(W.f[9 + j], bz1, A.acc[j]);
+    A.acc[3] = mfma(W.f[12], bz0, A.acc[3]);
+  } else {
+    head_part<true, 6, F>(c, p0, i, W, A);
+  }
+  refill_range<6, F>(c, W, nx);
+  if (p0.k == c.NS - 1) finish_step<true>(c, p0.step, A);
+}
+
+// Stage of wave B.  Layer: W_r v + b of the next layer (its popped rows are already in LDS) |
+// barrier | push of the layer input, skip fragments.  `W` is the buffer of this stage's parity
+// and `nx` the fragment stream of the stage two ahead.
+__device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags &W, int nx, Acc &A) {
+  Lds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  const int par = (int)(i & 1);
+  const int l = p0.k;
+  const bool layer = l < c.L;
+  // ---- slots 0..3: W_r v + b of the next layer
+  if (layer) {
+    if (l == 0) {
+      A.acc[0] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) A.acc[1 + j] = ldsf4(c.skip_sum + 128 * p + 64 + 16 * j + 4 * q);
+    }
+    if (l + 1 < c.L) recurrent_half(c, l + 1, par ^ 1, W, 0);
+  } else {
+    head_part<false, 0, 4>(c, p0, i, W, A);
+  }
+  refill_range<0, 4>(c, W, nx);
+  u32x4 bz0, bz1;
+  if (layer) {
+    __syncthreads();
+    push_rows(c, l);
+    const uint16_t *zb = s.zbuf + n * PX;
+    bz0 = lds16(zb + 8 * q);
+    bz1 = lds16(zb + 32 + 8 * q);
+    // ---- slots 4, 5: the k-step-1 half of skip tile 8p+3, skip tile 8p+4 k-step 0
+    A.acc[0] = mfma(W.f[4], bz1, A.acc[0]);
+    A.acc[1] = mfma(W.f[5], bz0, A.acc[1]);
+  } else {
+    head_part<false, 4, 6>(c, p0, i, W, A);
+  }
+  refill_range<4, 6>(c, W, nx);
+  // ---- slots 6..12: skip tiles 8p+5..8p+7 k-step 0, tiles 8p+4..8p+7 k-step 1
+  if (layer) {
+#pragma unroll
+    for (int j = 1; j < 4; ++j) A.acc[1 + j] = mfma(W.f[5 + j], bz0, A.acc[1 + j]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) A.acc[1 + j] = mfma(W.f[9 + j], bz1, A.acc[1 + j]);
+  } else {
+    head_part<false, 6, F>(c, p0, i, W, A);
+  }
+  refill_range<6, F>(c, W, nx);
+  if (p0.k == c.NS - 1) finish_step<false>(c, p0.step, A);
 }
 
 // Main loop of wave A: one fragment buffer, each slot refilled with the next stage's.
@@ -501,7 +548,7 @@ __device__ __forceinline__ void a_role(const Ctx &c, long long total) {
   Pos p0{0, 0};
   for (long long i = 0; i < total; ++i) {
     const Pos p1 = advance(c, p0, 1);
-    run_stage<true>(c, p0, i, W, stage_off(c, p1.k), A);
+    a_stage(c, p0, i, W, stage_off(c, p1.k), A);
     __syncthreads();
     p0 = p1;
   }
@@ -534,13 +581,13 @@ __device__ __forceinline__ void b_role(const Ctx &c, long long total) {
     const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3), p4 = advance(c, p0, 4);
     vA = pop_issue(c, p3.k, (int)(p3.step - p0.step));
     __builtin_amdgcn_sched_barrier(0);
-    run_stage<false>(c, p0, i, W0, stage_off(c, p2.k), A);
+    b_stage(c, p0, i, W0, stage_off(c, p2.k), A);
     if (p2.k < c.L && i + 2 < total) pop_land(c, 0, vB);
     __syncthreads();
     if (i + 1 >= total) break;
     vB = pop_issue(c, p4.k, (int)(p4.step - p1.step));
     __builtin_amdgcn_sched_barrier(0);
-    run_stage<false>(c, p1, i + 1, W1, stage_off(c, p3.k), A);
+    b_stage(c, p1, i + 1, W1, stage_off(c, p3.k), A);
     if (p3.k < c.L && i + 3 < total) pop_land(c, 1, vA);
     __syncthreads();
     p0 = p2;
