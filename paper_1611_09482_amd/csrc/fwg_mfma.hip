@@ -173,10 +173,12 @@ __device__ __forceinline__ void refill(const Ctx &c, Frags &W, int nx, int f) {
   W.f[f] = load_frag(c, nx, f);
   __builtin_amdgcn_sched_barrier(0);
 }
+// Load a whole stage in slot order, as the loop refills them (the compiler's load accounting at
+// the loop entry then matches the loop's own).
 __device__ __forceinline__ void load_stage(const Ctx &c, int k, Frags &fr) {
   const int off = stage_off(c, k);
 #pragma unroll
-  for (int f = 0; f < F; ++f) fr.f[f] = load_frag(c, off, f);
+  for (int f = 0; f < F; ++f) refill(c, fr, off, f);
 }
 
 // Queue traffic is issued by the B waves: wave B of pair p moves stream rows 4p..4p+3, lane l
@@ -256,8 +258,13 @@ __device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
 __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
   Lds &s = *c.s;
-  for (int i = threadIdx.x; i < ROWS * KCH; i += NT) {
-    const int r = i / KCH, j = i % KCH;
+  // a fixed number of entries per thread (no loop), which keeps the compiler's load accounting
+  // precise in the code around it
+  static_assert((ROWS * KCH) % NT == 0, "the chunk divides evenly over the threads");
+#pragma unroll
+  for (int e = 0; e < ROWS * KCH / NT; ++e) {
+    const int idx = (int)threadIdx.x + e * NT;
+    const int r = idx / KCH, j = idx % KCH;
     const long long st = s0 + j;
     if (a.forced) {
       int v = 0;
@@ -577,20 +584,26 @@ __device__ __forceinline__ void b_role(const Ctx &c, long long total) {
   load_stage(c, p1i.k, W1);
   __syncthreads();
   Pos p0 = p0i;
-  for (long long i = 0; i < total; i += 2) {
+  long long i = 0;
+  for (; i + 1 < total; i += 2) {
     const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3), p4 = advance(c, p0, 4);
     vA = pop_issue(c, p3.k, (int)(p3.step - p0.step));
     __builtin_amdgcn_sched_barrier(0);
     b_stage(c, p0, i, W0, stage_off(c, p2.k), A);
     if (p2.k < c.L && i + 2 < total) pop_land(c, 0, vB);
     __syncthreads();
-    if (i + 1 >= total) break;
     vB = pop_issue(c, p4.k, (int)(p4.step - p1.step));
     __builtin_amdgcn_sched_barrier(0);
     b_stage(c, p1, i + 1, W1, stage_off(c, p3.k), A);
     if (p3.k < c.L && i + 3 < total) pop_land(c, 1, vA);
     __syncthreads();
     p0 = p2;
+  }
+  if (i < total) {
+    // odd stage count: the last stage (its queue rows for later stages are not needed)
+    const Pos p2 = advance(c, p0, 2);
+    b_stage(c, p0, i, W0, stage_off(c, p2.k), A);
+    __syncthreads();
   }
 }
 
