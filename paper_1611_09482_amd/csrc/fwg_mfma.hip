@@ -72,24 +72,43 @@ __device__ __forceinline__ f32x4 relu4(const f32x4 &v) {
   return f32x4{fmaxf(v[0], 0.f), fmaxf(v[1], 0.f), fmaxf(v[2], 0.f), fmaxf(v[3], 0.f)};
 }
 
-// Inverse-CDF sample of one row of 256 logits by one wavefront (see fwg_kernels.hip).
+// Cross-lane moves inside rows of 16 lanes (DPP) and lane reads, for the wave-wide max and scan of
+// the sampler.  Control codes: quad permutations, row_shr:n = 0x110 + n, row_mirror = 0x140,
+// row_half_mirror = 0x141; bound_ctrl makes a source lane outside the row read 0.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float lane_f(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Inverse-CDF sample of one row of 256 logits by one wavefront (each lane holds 4 consecutive
+// classes): max-subtracted exp, inclusive prefix sum over the classes in order, first class k with
+// u * Z < S_k (255 if none).
 __device__ __forceinline__ int sample256(const float *lg, float u) {
   const int lane = threadIdx.x & 63;
   const float4 l4 = *(const float4 *)(lg + 4 * lane);
+  // wave max: butterfly inside each row of 16, then the four row maxima
   float m = fmaxf(fmaxf(l4.x, l4.y), fmaxf(l4.z, l4.w));
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+  m = fmaxf(m, dpp<0xB1>(m));   // quad_perm [1,0,3,2]
+  m = fmaxf(m, dpp<0x4E>(m));   // quad_perm [2,3,0,1]
+  m = fmaxf(m, dpp<0x141>(m));  // row_half_mirror
+  m = fmaxf(m, dpp<0x140>(m));  // row_mirror
+  m = fmaxf(fmaxf(lane_f(m, 0), lane_f(m, 16)), fmaxf(lane_f(m, 32), lane_f(m, 48)));
   const float e0 = __expf(l4.x - m), e1 = __expf(l4.y - m), e2 = __expf(l4.z - m), e3 = __expf(l4.w - m);
   const float c0 = e0, c1 = c0 + e1, c2 = c1 + e2, c3 = c2 + e3;
+  // inclusive scan of the lane sums: inside each row of 16, then the preceding rows' totals
   float incl = c3;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const float v = __shfl_up(incl, off, 64);
-    if (lane >= off) incl += v;
-  }
-  float excl = __shfl_up(incl, 1, 64);
-  if (lane == 0) excl = 0.f;
-  const float Z = __shfl(excl + c3, 63, 64);
+  incl += dpp<0x111>(incl);  // row_shr:1
+  incl += dpp<0x112>(incl);  // row_shr:2
+  incl += dpp<0x114>(incl);  // row_shr:4
+  incl += dpp<0x118>(incl);  // row_shr:8
+  const float t0 = lane_f(incl, 15), t1 = lane_f(incl, 31), t2 = lane_f(incl, 47), t3 = lane_f(incl, 63);
+  const int row = lane >> 4;
+  incl += (row >= 1 ? t0 : 0.f) + (row >= 2 ? t1 : 0.f) + (row >= 3 ? t2 : 0.f);
+  const float excl = incl - c3;
+  const float Z = ((t0 + t1) + t2) + t3;
   const float target = u * Z;
   int first = 4;
   if (target < excl + c3) first = 3;
@@ -99,7 +118,7 @@ __device__ __forceinline__ int sample256(const float *lg, float u) {
   const unsigned long long hit = __ballot(first < 4);
   if (hit == 0ull) return 255;
   const int src = __ffsll((long long)hit) - 1;
-  return 4 * src + __shfl(first, src, 64);
+  return 4 * src + __builtin_amdgcn_readlane(first, src);
 }
 
 // ---------------------------------------------------------------------------
