@@ -154,6 +154,20 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
  * 1 <= batch <= max_batch; seq_len == 0 is a no-op. */
 int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
 
+/* Online prediction (the use the paper names beside generation, end of Section 1
+ * and Section 4): the same cached step continues from the current queue state,
+ * but the sample that follows each step is observed instead of drawn.  Step s
+ * (time t0 + s) consumes the stream's pending input -- for s = 0 the input
+ * fwg_generate would have consumed next (seed_input after a reset, else the last
+ * sample generated or observed), for s > 0 inputs[b][s-1] -- and writes
+ * logits[b][s][:], the distribution the model predicts for the next sample; then
+ * inputs[b][s] becomes the pending input.  Queues and t advance exactly as in
+ * fwg_generate, so generation and online prediction may alternate freely.
+ * inputs: DEVICE int32 [batch][n_steps], each in [0, n_classes);
+ * logits: DEVICE float32 [batch][n_steps][n_classes].  Batch binding and the
+ * FWG_ESTATE rule as in fwg_generate; n_steps == 0 is a no-op. */
+int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
+
 /* Free the host-side handle (the workspace stays the caller's). NULL is a no-op. */
 int fwg_destroy(fwg_handle *h);
 

@@ -52,6 +52,7 @@ def lib():
         L.fwo_state_t.restype = ctypes.c_longlong
         L.fwo_state_t.argtypes = [ctypes.c_void_p]
         L.fwo_generate.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, fp, ip, dp]
+        L.fwo_step_forced.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ip, dp]
         L.fwo_teacher_forced.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ip, dp]
         L.fwo_parallel.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ip, dp]
         L.fwo_naive.argtypes = [ctypes.c_void_p, ip, ctypes.c_int, dp]
@@ -201,6 +202,17 @@ class OracleState:
                                 None if logits is None else logits.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
         assert rc == 0
         return (samples, logits) if return_logits else samples
+
+    def step_forced(self, inputs) -> np.ndarray:
+        """Online prediction: logits[b][i] is the distribution of inputs[b][i] given everything before."""
+        x = _i32(inputs)
+        B, n = x.shape
+        assert B == self.batch
+        logits = np.empty((B, n, self.oracle.cfg.n_classes), np.float64)
+        rc = lib().fwo_step_forced(self.oracle._mp, self._h, n, x.ctypes.data_as(ctypes.POINTER(ctypes.c_int)),
+                                   logits.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+        assert rc == 0
+        return logits
 
 
 def sample(logits_row, u: float) -> int:

@@ -272,6 +272,32 @@ int fwo_generate(const fwo_model *m, fwo_state *st, int n_steps, const float *u,
   return 0;
 }
 
+/* Online prediction (the use named at the end of Section 1 and in Section 4): the
+ * cached step of Section 2.2 continues from the state, but the sample that
+ * follows each step is observed, not drawn.  Step i consumes the pending input,
+ * reports the distribution predicted for the next sample, and then takes
+ * inputs[b][i] as that sample, which becomes the pending input. */
+int fwo_step_forced(const fwo_model *m, fwo_state *st, int n_steps, const int *inputs, double *logits) {
+  if (!m || !st || n_steps < 0 || (n_steps > 0 && (!inputs || !logits))) return -1;
+  const int B = st->batch, L = m->L, Q = m->Q;
+#pragma omp parallel for schedule(dynamic, 1) if (!m->products && B > 1)
+  for (int b = 0; b < B; ++b) {
+    scratch w;
+    scratch_init(m, &w);
+    fifo *q = &st->queues[(size_t)b * L];
+    int in = st->last[b];
+    for (int i = 0; i < n_steps; ++i) {
+      model_step(m, q, in, w.logits, w.popped, w.states, w.s, w.work);
+      memcpy(logits + ((size_t)b * n_steps + i) * Q, w.logits, sizeof(double) * Q);
+      in = inputs[(size_t)b * n_steps + i];
+    }
+    st->last[b] = in;
+    scratch_free(&w);
+  }
+  st->t += n_steps;
+  return 0;
+}
+
 int fwo_teacher_forced(const fwo_model *m, int B, int T, const int *inputs, double *logits) {
   if (!m || B <= 0 || T < 0 || (T > 0 && (!inputs || !logits))) return -1;
   const int L = m->L, Q = m->Q;

@@ -16,8 +16,10 @@
  * Fig. 5 and Fig. 6).  Every prediction is fed back as the next input
  * (Section 1).
  *
- * Three evaluation forms are provided:
+ * Evaluation forms:
  *   fwo_generate / fwo_teacher_forced  -- the cached queue form (Section 2.2)
+ *   fwo_step_forced                    -- the cached form fed observed samples
+ *                                          (online prediction, Sections 1 and 4)
  *   fwo_parallel                       -- each layer over the whole sequence at
  *                                          once (the training-time view, Section 1)
  *   fwo_naive                          -- recursive recomputation of the tree of
@@ -81,6 +83,12 @@ long long fwo_state_t(const fwo_state *st);
  * logits: optional [batch][n_steps][Q] (the distribution each sample was drawn from). */
 int fwo_generate(const fwo_model *m, fwo_state *st, int n_steps, const float *u, int *samples,
                  double *logits);
+
+/* Online prediction, continuing from the state: step i consumes the pending
+ * input, writes logits[b][i] (the distribution of the next sample) and then
+ * takes inputs[b][i] as that sample (the new pending input).  inputs and
+ * logits as in fwo_teacher_forced, with n_steps for T. */
+int fwo_step_forced(const fwo_model *m, fwo_state *st, int n_steps, const int *inputs, double *logits);
 
 /* Cached form from zero queues; inputs [batch][T]; logits [batch][T][Q]. */
 int fwo_teacher_forced(const fwo_model *m, int batch, int T, const int *inputs, double *logits);

@@ -16,7 +16,7 @@ _STATUS = {FWG_EINVAL: "EINVAL", FWG_ENOSPACE: "ENOSPACE", FWG_EHIP: "EHIP", FWG
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfwg.so")
 
 EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-            "fwg_destroy", "fwg_last_error", "fwg_regime"]
+            "fwg_step_forced", "fwg_destroy", "fwg_last_error", "fwg_regime"]
 
 
 class FwgError(RuntimeError):
@@ -60,12 +60,13 @@ def load_library(path: Optional[str] = None):
     L.fwg_reset_queues.argtypes = [vp]
     L.fwg_generate.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_teacher_forced.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_step_forced.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_destroy.argtypes = [vp]
     L.fwg_last_error.restype = ctypes.c_char_p
     L.fwg_regime.argtypes = [vp]
     L.fwg_regime.restype = ctypes.c_char_p
     for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-                 "fwg_destroy"]:
+                 "fwg_step_forced", "fwg_destroy"]:
         getattr(L, name).restype = ctypes.c_int
     if path is None:
         _lib = L
@@ -162,6 +163,18 @@ class FastWavenet:
         if out is None:
             out = torch.empty((B, T, self.n_classes), dtype=torch.float32, device=inputs.device)
         _check(self.lib.fwg_teacher_forced(self.handle, B, T, inputs.data_ptr(), out.data_ptr()))
+        return out
+
+    def step_forced(self, inputs, out=None):
+        """Online prediction from the current state.  inputs: int32 CUDA tensor [batch][n_steps] of
+        observed samples -> float32 logits [batch][n_steps][n_classes]; logits[b][s] is the
+        distribution predicted for inputs[b][s]."""
+        torch = self._torch
+        assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
+        B, n = inputs.shape
+        if out is None:
+            out = torch.empty((B, n, self.n_classes), dtype=torch.float32, device=inputs.device)
+        _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), out.data_ptr()))
         return out
 
     def close(self):

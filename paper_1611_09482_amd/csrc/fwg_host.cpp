@@ -353,7 +353,7 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
   a.t0 = h->t;
   a.n_steps = n_steps;
   a.batch = batch;
-  a.forced = 0;
+  a.mode = MODE_GENERATE;
   HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
   h->bound_batch = batch;
   h->t += n_steps;
@@ -375,8 +375,31 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
   a.t0 = 0;
   a.n_steps = seq_len;
   a.batch = batch;
-  a.forced = 1;
+  a.mode = MODE_TEACHER;
   HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  return FWG_OK;
+}
+
+int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits) {
+  if (!h) return fail(FWG_EINVAL, "handle is NULL");
+  const Plan &p = h->plan;
+  if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
+  if (n_steps < 0) return fail(FWG_EINVAL, "n_steps < 0");
+  if (h->bound_batch >= 0 && h->bound_batch != batch)
+    return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
+  if (n_steps == 0) return FWG_OK;
+  if (!inputs || !logits) return fail(FWG_EINVAL, "inputs and logits are required");
+  StepArgs a = base_args(h);
+  a.ring = h->ws + p.off_ring_gen;
+  a.inputs = inputs;
+  a.logits = logits;
+  a.t0 = h->t;
+  a.n_steps = n_steps;
+  a.batch = batch;
+  a.mode = MODE_ONLINE;
+  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  h->bound_batch = batch;
+  h->t += n_steps;
   return FWG_OK;
 }
 

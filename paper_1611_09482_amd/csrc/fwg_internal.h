@@ -36,17 +36,26 @@ struct StepArgs {
   int32_t *last;           // [bmax] next input per stream (generation mode)
   const float *uniforms;   // [batch][n_steps]
   int32_t *samples;        // [batch][n_steps]
-  const int32_t *inputs;   // teacher-forced [batch][n_steps]
-  float *logits;           // teacher-forced [batch][n_steps][Q]
+  const int32_t *inputs;   // forced modes [batch][n_steps]
+  float *logits;           // forced modes [batch][n_steps][Q]
   long long t0;            // time index of the first step of this launch
   int n_steps, batch, bmax;
   int kind, dtype, C, S, H, Q, L;
-  int forced;              // 1: teacher-forced mode
+  int mode;                // StepMode
   // MFMA family only
   const void *mf_frags;    // per-wave packed weight fragment streams
   const void *mf_embT;     // embedding table [Q][R] (bf16)
   const float *mf_bias;    // bias block: conv [L][2R], res [L][R], skip sum [S], head [H], out [Q], embed [R]
 };
+
+// What drives the input of each step.
+enum StepMode {
+  MODE_GENERATE = 0,  // the previous sample (or the stream's pending input) is fed back
+  MODE_TEACHER = 1,   // step s consumes inputs[s]; queues of their own, from zero
+  MODE_ONLINE = 2     // step s consumes the pending input, then inputs[s] becomes pending
+};
+// Offset, in steps, of the forced input that becomes the next step's input.
+__host__ __device__ inline int forced_shift(int mode) { return mode == MODE_TEACHER ? 1 : 0; }
 
 // Kernel families.
 enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1 };

@@ -184,13 +184,15 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   if (nrows <= 0) return;
 
   for (int l = tid; l < L; l += kThreads) slots[l] = (int)(a.t0 % (long long)a.layers[l].dil);
-  if (tid < RPW) ins[tid] = (!a.forced && tid < nrows) ? a.last[b0 + tid] : 0;
+  if (tid < RPW) {
+    int v = 0;
+    if (tid < nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(b0 + tid) * a.n_steps] : a.last[b0 + tid];
+    ins[tid] = v;
+  }
   __syncthreads();
 
   for (int s = 0; s < a.n_steps; ++s) {
-    // ---- current input (h^0_e): previous sample, or the forced sequence
-    if (a.forced && tid < nrows) ins[tid] = a.inputs[(long long)(b0 + tid) * a.n_steps + s];
-    __syncthreads();
+    // ---- current input (h^0_e) is ins[]: set before the loop and at the end of every step
     // ---- embedding: a row gather of the transposed 1x1 convolution
     for (int i = tid; i < RPW * C; i += kThreads) {
       const int r = i / C, c = i % C;
@@ -279,11 +281,15 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     }
     __syncthreads();
 
-    if (a.forced) {
+    if (a.mode != MODE_GENERATE) {
       for (int i = tid; i < nrows * Q; i += kThreads) {
         const int r = i / Q, q = i % Q;
         a.logits[((long long)(b0 + r) * a.n_steps + s) * Q + q] = lg[i];
       }
+      // the next input: the following element of the forced sequence (teacher forcing), or this
+      // step's observed sample (online prediction)
+      const int nx = s + forced_shift(a.mode);
+      if (tid < nrows && nx < a.n_steps) ins[tid] = a.inputs[(long long)(b0 + tid) * a.n_steps + nx];
     } else {
       // ---- sample and feed back
       const int w = tid >> 6;
@@ -303,7 +309,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     }
     __syncthreads();
   }
-  if (!a.forced && tid < nrows) a.last[b0 + tid] = ins[tid];
+  if (a.mode != MODE_TEACHER && tid < nrows) a.last[b0 + tid] = ins[tid];
 }
 
 template <typename WT>

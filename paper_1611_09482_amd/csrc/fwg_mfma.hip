@@ -148,7 +148,7 @@ struct Lds {
   } u;
   uint16_t embT[Q * R];  // embedding table, [class][channel]
   // per-step inputs of the block's streams for a chunk of KCH steps: uniforms (generation) or the
-  // next forced input (teacher forcing), loaded once per chunk
+  // forced input that follows each step, loaded once per chunk
   union {
     float u[ROWS][KCH];
     int in[ROWS][KCH];
@@ -272,7 +272,8 @@ __device__ __forceinline__ Pos advance(const Ctx &c, Pos p, int m) {
 
 // Stage body shared by the two roles' loops; `nx` is the fragment stream that refills W.
 // Stage the per-step inputs of steps [s0, s0 + KCH) in LDS: the uniform of (row r, step s) for
-// generation, the input of step s + 1 for teacher forcing.  Called by every thread of the block
+// generation; in the forced modes the input that follows step s (inputs[s + 1] for teacher
+// forcing, the observed sample inputs[s] for online prediction).  Called by every thread of the block
 // once per chunk (in the first head stage, before its barriers).
 __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
@@ -285,9 +286,10 @@ __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
     const int idx = (int)threadIdx.x + e * NT;
     const int r = idx / KCH, j = idx % KCH;
     const long long st = s0 + j;
-    if (a.forced) {
+    if (a.mode != MODE_GENERATE) {
+      const long long nx = st + forced_shift(a.mode);
       int v = 0;
-      if (r < c.nrows && st + 1 < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + st + 1];
+      if (r < c.nrows && nx < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + nx];
       s.chunk.in[r][j] = v;
     } else {
       float v = 0.f;
@@ -308,7 +310,7 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
   __syncthreads();
   const int tid = threadIdx.x;
   // straight-line code (no loop exits), which keeps the compiler's load accounting precise
-  if (a.forced) {
+  if (a.mode != MODE_GENERATE) {
 #pragma unroll
     for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
       const int r = c.w + kMfWaves * kk;
@@ -317,7 +319,7 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
         *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
       }
     }
-    if (tid < c.nrows && step + 1 < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
+    if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
 #pragma unroll
     for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
@@ -675,7 +677,7 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   }
   if (tid < ROWS) {
     int v = 0;
-    if (tid < c.nrows) v = a.forced ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
+    if (tid < c.nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
     s.ins[tid] = v;
   }
   __syncthreads();
@@ -683,7 +685,7 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   const long long total = (long long)a.n_steps * c.NS;
   if (c.w < 4) a_role(c, total);
   else b_role(c, total);
-  if (!a.forced && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
+  if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
 }
 
 }  // namespace mf

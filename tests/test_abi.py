@@ -93,6 +93,7 @@ def test_null_arguments(lib):
     assert lib.fwg_reset_queues(None) == B.FWG_EINVAL
     assert lib.fwg_generate(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_teacher_forced(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_step_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_destroy(None) == B.FWG_OK
     assert lib.fwg_regime(None) == b""
 

@@ -135,6 +135,48 @@ def test_generation_parity(fam):
     check_generation(cfg, fw, orc, W.uniforms(4, B, n), B, fam)
 
 
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu"])
+def test_online_prediction_parity(fam):
+    """Online prediction (fwg_step_forced): generate, feed observed samples from the same queues,
+    generate again.  The oracle is driven through the same history (the GPU's own samples, then the
+    observed ones); forced logits meet the logits bar, the closing generation the sampling bar."""
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5
+    n1, n2, n3 = 37, 150, 90     # the forced stretch crosses chunk boundaries of the per-step inputs
+    w, fw, orc = build_pair(cfg, 102, B, fam=fam)
+    u = W.uniforms(12, B, n1 + n3)
+    obs = W.sequences(13, B, n2)
+    g1 = fw.generate(dev(u[:, :n1].copy())).cpu().numpy()
+    glg = fw.step_forced(dev(obs)).cpu().numpy()
+    g3 = fw.generate(dev(u[:, n1:].copy())).cpu().numpy()
+    st = orc.state(B)
+    olg1 = st.step_forced(g1)        # the oracle walks the GPU's generated history
+    olg = st.step_forced(obs)
+    # every GPU sample of the first stretch is admissible under the oracle's distribution
+    tau = TAU[cfg.dtype]
+    for b in range(B):
+        for t in range(n1):
+            lo, hi = cdf_bounds(olg1[b, t], g1[b, t])
+            assert lo - tau <= u[b, t] < hi + tau, (fam, b, t)
+    err = row_rel_err(glg, olg)
+    log(f"{fam} [{fw.regime}]: online B={B} n={n2} after {n1} generated: max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+    # generation resumes from the last observed sample
+    so, slg = st.generate(u[:, n1:], return_logits=True)
+    for b in range(B):
+        mism = np.nonzero(g3[b] != so[b])[0]
+        if mism.size:
+            t = int(mism[0])
+            lo, hi = cdf_bounds(slg[b, t], so[b, t])
+            margin = min(u[b, n1 + t] - lo, hi - u[b, n1 + t])
+            assert margin < tau, f"{fam}: stream {b} diverges at step {t} after online prediction"
+    # from a reset, online prediction over x is bit-identical to teacher forcing [seed, x[:-1]]
+    fw.reset()
+    a = fw.step_forced(dev(obs)).cpu().numpy()
+    seq = np.concatenate([np.full((B, 1), cfg.seed_input, np.int32), obs[:, :-1]], axis=1)
+    assert np.array_equal(a, fw.teacher_forced(dev(seq)).cpu().numpy())
+
+
 def test_delay_line_closed_form_gpu():
     """W_e = 0, W_r = I, ReLU, zero biases, embeddings >= 0: logits[0:C] = x^0_{t - sum d} exactly,
     through every queue depth up to 512 (pop before push, slot wrap-around)."""

@@ -340,6 +340,37 @@ def test_generation_is_teacher_forced_on_own_samples(oracle_lib):
             assert lo - 1e-6 <= u[b, t] < c[s[b, t]] + 1e-6
 
 
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_online_prediction_continues_the_history(oracle_lib, dtype):
+    """Online prediction (Sections 1 and 4): generate, then feed observed samples, then generate
+    again from the same queues.  Every step's logits equal a full-sequence torch conv1d over the
+    realised history [seed, generated, observed, generated[:-1]], and the observed samples become
+    the inputs that follow them."""
+    cfg = W.tiny_model(W.GATED, dtype, channels=4, dilations=(1, 2, 4, 8, 1, 2, 4, 8), skip=8, head=8)
+    w = W.make_weights(cfg, 8, bias_scale=0.2)
+    o = oracle_lib.Oracle(w)
+    B, n1, n2, n3 = 2, 13, 29, 17
+    u = W.uniforms(31, B, n1 + n3)
+    obs = W.sequences(32, B, n2)
+    st = o.state(B)
+    g1, lg1 = st.generate(u[:, :n1], return_logits=True)
+    lg2 = st.step_forced(obs)
+    g3, lg3 = st.generate(u[:, n1:], return_logits=True)
+    assert st.t == n1 + n2 + n3
+    hist = np.concatenate([np.full((B, 1), cfg.seed_input), g1, obs, g3[:, :-1]], axis=1)
+    ref = _torch_reference(w, hist)
+    got = np.concatenate([lg1, lg2, lg3], axis=1)
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-10)
+    # the tree of Fig. 1 at a few times of the observed stretch
+    for t in (n1, n1 + 7, n1 + n2 - 1):
+        np.testing.assert_allclose(got[1, t], o.naive(hist[1], t), rtol=1e-12, atol=1e-12)
+    # from a reset, online prediction over x is the teacher-forced pass over [seed, x[:-1]]
+    st.reset()
+    lo = st.step_forced(obs)
+    np.testing.assert_allclose(lo, _torch_reference(
+        w, np.concatenate([np.full((B, 1), cfg.seed_input), obs[:, :-1]], axis=1)), rtol=1e-10, atol=1e-10)
+
+
 # ---------------------------------------------------------------- P10 bf16
 def test_bf16_rounding_vectors(oracle_lib):
     for a, b in _read_pairs("bf16_rne.txt"):
