@@ -148,9 +148,11 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
 
 /* Teacher-forced evaluation from zero queues: logits[b][t][:] is the output
  * after consuming inputs[b][0..t].  inputs: DEVICE int32 [batch][seq_len];
- * logits: DEVICE float32 [batch][seq_len][n_classes].  Runs the same step
- * kernels with the input taken from `inputs` instead of the previous sample;
- * uses queues of its own and leaves the generation state untouched.
+ * logits: DEVICE float32 [batch][seq_len][n_classes].  Sequences of 16 steps
+ * or more are evaluated time-parallel (each layer as one dilated convolution
+ * over the sequence, Section 1), shorter ones by the step kernels with the
+ * input taken from `inputs`; either way the call uses queues of its own and
+ * leaves the generation state untouched.
  * 1 <= batch <= max_batch; seq_len == 0 is a no-op. */
 int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
 
@@ -164,8 +166,13 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
  * inputs[b][s] becomes the pending input.  Queues and t advance exactly as in
  * fwg_generate, so generation and online prediction may alternate freely.
  * inputs: DEVICE int32 [batch][n_steps], each in [0, n_classes);
- * logits: DEVICE float32 [batch][n_steps][n_classes].  Batch binding and the
- * FWG_ESTATE rule as in fwg_generate; n_steps == 0 is a no-op. */
+ * logits: DEVICE float32 [batch][n_steps][n_classes], or NULL to only advance
+ * the state (priming the queues from a prefix before generating).  Batch
+ * binding and the FWG_ESTATE rule as in fwg_generate; n_steps == 0 is a no-op.
+ * Long stretches are evaluated time-parallel, every layer as one dilated
+ * convolution over the stretch (the training-time view of the network,
+ * Section 1), reading the states before the stretch from the queues and leaving
+ * in each queue the newest d_l states, as the step-by-step loop would. */
 int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
 
 /* Free the host-side handle (the workspace stays the caller's). NULL is a no-op. */

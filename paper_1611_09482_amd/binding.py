@@ -177,6 +177,14 @@ class FastWavenet:
         _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), out.data_ptr()))
         return out
 
+    def prime(self, inputs):
+        """Advance the state over observed samples without computing logits (fwg_step_forced with
+        logits = NULL): a prefix to continue generating from."""
+        torch = self._torch
+        assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
+        B, n = inputs.shape
+        _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), None))
+
     def close(self):
         if getattr(self, "handle", None):
             self.lib.fwg_destroy(self.handle)

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libfwg.so")
 SOURCES = [os.path.join(CSRC, "fwg_host.cpp"), os.path.join(CSRC, "fwg_kernels.hip"),
-           os.path.join(CSRC, "fwg_mfma.hip")]
+           os.path.join(CSRC, "fwg_mfma.hip"), os.path.join(CSRC, "fwg_parallel.hip")]
 HEADERS = [os.path.join(ROOT, "include", "fwg.h"), os.path.join(CSRC, "fwg_internal.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

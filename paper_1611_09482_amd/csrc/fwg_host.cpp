@@ -48,6 +48,13 @@ struct Plan {
   std::vector<long long> ring_off;
   size_t off_ring_gen, off_ring_tf, off_last, total;
   size_t lds_bytes;
+  // time-parallel path (forced sequences): operand-typed [N][K] weights and chunk buffers
+  bool par_ok;
+  bool par_force;         // every forced call takes the time-parallel path (else from kParMinSteps steps)
+  int par_tc;             // steps per chunk; a chunk holds brows * par_tc rows at most
+  std::vector<size_t> off_pconv, off_pconv_b, off_pres;
+  size_t off_pskip, off_pskip_b, off_phead, off_pout;
+  size_t off_px[2], off_pxb[2], off_pz, off_psb, off_phb;
 };
 
 bool kblock_ok(int K, int N, int kb_elems) {
@@ -163,6 +170,51 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_ring_gen = take((size_t)acc * p->es);
   p->off_ring_tf = take((size_t)acc * p->es);
   p->off_last = take(sizeof(int32_t) * p->bmax);
+
+  // time-parallel path: every product's K must fill whole 128-byte k-tiles, and the gate's column
+  // pairs come in groups of 16 channels
+  const int kt = kParKTileBytes / p->es;
+  p->par_ok = p->C % kt == 0 && (p->kind != FWG_GATED ||
+                                 (p->C % 16 == 0 && ((long long)p->L * p->C) % kt == 0 && p->S % kt == 0 &&
+                                  p->H % kt == 0));
+  const char *pf = getenv("FWG_FORCED_PATH");
+  if (pf && strcmp(pf, "step") == 0) p->par_ok = false;
+  p->par_force = pf && strcmp(pf, "parallel") == 0;
+  p->par_tc = 0;
+  if (p->par_ok) {
+    const bool gated = p->kind == FWG_GATED;
+    const bool fp32_stream = p->kind != FWG_RELU;                  // residual stream kept in float32
+    const bool opnd_copy = p->kind == FWG_RELU || p->dtype == FWG_BF16;  // separate operand rows
+    size_t row_bytes = 0;
+    if (fp32_stream) row_bytes += 2 * (size_t)p->C * 4;
+    if (opnd_copy) row_bytes += 2 * (size_t)p->C * p->es;
+    if (gated) row_bytes += ((size_t)p->L * p->C + p->S + p->H) * p->es;
+    // chunk rows: about 64K rows, at most 512 MB of chunk buffers, at least one step
+    long long rows = 65536;
+    const char *pr = getenv("FWG_PAR_ROWS");
+    if (pr && atoll(pr) > 0) rows = atoll(pr);
+    const long long cap = (512ll << 20) / (long long)row_bytes;
+    if (rows > cap) rows = cap;
+    p->par_tc = (int)(rows / p->brows > 0 ? rows / p->brows : 1);
+    const size_t R = (size_t)p->par_tc * p->brows;
+    p->off_pconv.assign(p->L, 0); p->off_pconv_b.assign(p->L, 0); p->off_pres.assign(p->L, 0);
+    for (int l = 0; l < p->L; ++l) {
+      p->off_pconv[l] = take((size_t)p->Co * 2 * p->C * p->es);
+      p->off_pconv_b[l] = take(sizeof(float) * p->Co);
+      if (gated) p->off_pres[l] = take((size_t)p->C * p->C * p->es);
+    }
+    p->off_pskip = gated ? take((size_t)p->S * p->L * p->C * p->es) : 0;
+    p->off_pskip_b = gated ? take(sizeof(float) * p->S) : 0;
+    p->off_phead = gated ? take((size_t)p->H * p->S * p->es) : 0;
+    p->off_pout = take((size_t)p->Q * Kout * p->es);
+    for (int i = 0; i < 2; ++i) {
+      p->off_px[i] = fp32_stream ? take(R * p->C * 4) : 0;
+      p->off_pxb[i] = opnd_copy ? take(R * p->C * p->es) : p->off_px[i];
+    }
+    p->off_pz = gated ? take(R * p->L * p->C * p->es) : 0;
+    p->off_psb = gated ? take(R * p->S * p->es) : 0;
+    p->off_phb = gated ? take(R * p->H * p->es) : 0;
+  }
   p->total = off;
   return FWG_OK;
 }
@@ -215,6 +267,113 @@ StepArgs base_args(const fwg_handle *h) {
   a.Q = p.Q;
   a.L = p.L;
   return a;
+}
+
+// Forced calls shorter than this run on the step kernels (one launch) instead of the
+// time-parallel path (a few launches per layer and chunk).
+constexpr int kParMinSteps = 16;
+
+bool use_parallel(const fwg_handle *h, int n_steps) {
+  return h->plan.par_ok && (h->plan.par_force || n_steps >= kParMinSteps);
+}
+
+// Time-parallel evaluation of a forced sequence, chunk by chunk (MODE_TEACHER or MODE_ONLINE):
+// every layer is a GEMM over the chunk's rows whose popped operand comes from the chunk or from
+// the layer's queue in `ring`; the queues are refreshed after each layer.  logits may be NULL
+// (online mode only): then the skip sum and the head are skipped.
+int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs, float *logits, char *ring,
+                long long tbase) {
+  const Plan &p = h->plan;
+  hipStream_t s = h->stream;
+  char *ws = h->ws;
+  const int C = p.C, L = p.L, es = p.es;
+  const bool gated = p.kind == FWG_GATED;
+  const bool f32s = p.kind != FWG_RELU;
+  const bool opnd_copy = p.kind == FWG_RELU || p.dtype == FWG_BF16;
+  float *px[2] = {(float *)(ws + p.off_px[0]), (float *)(ws + p.off_px[1])};
+  char *pxb[2] = {ws + p.off_pxb[0], ws + p.off_pxb[1]};
+  for (long long s0 = 0; s0 < n; s0 += p.par_tc) {
+    const int Tcur = (int)(n - s0 < p.par_tc ? n - s0 : p.par_tc);
+    const int M = batch * Tcur;
+    const long long t0 = tbase + s0;
+    ParEmbed e;
+    memset(&e, 0, sizeof(e));
+    e.M = M; e.C = C; e.Tcur = Tcur; e.mode = mode; e.s0 = s0; e.n_steps = n;
+    e.inputs = inputs;
+    e.last = (const int32_t *)(ws + p.off_last);
+    e.embed = ws + p.off_embed;
+    e.embed_b = (const float *)(ws + p.off_embed_b);
+    e.xout = f32s ? px[0] : nullptr;
+    e.oout = pxb[0];
+    HIP_TRY(launch_par_embed(e, p.dtype, s));
+    int cur = 0;
+    for (int l = 0; l < L; ++l) {
+      const int nxt = cur ^ 1;
+      ParGemm g;
+      memset(&g, 0, sizeof(g));
+      g.M = M; g.N = p.Co; g.K = 2 * C;
+      g.A = pxb[cur]; g.lda = C;
+      g.ring = ring + (size_t)p.ring_off[l] * es;
+      g.t0 = t0; g.dil = h->dil[l]; g.brows = p.brows; g.Tcur = Tcur; g.C = C;
+      g.W = ws + p.off_pconv[l];
+      g.bias = (const float *)(ws + p.off_pconv_b[l]);
+      int em;
+      if (gated) {
+        em = PAR_E_GATE; g.oout = ws + p.off_pz; g.ldo = (long long)L * C; g.zoff = l * C;
+      } else if (p.kind == FWG_RELU) {
+        em = PAR_E_RELU; g.oout = pxb[nxt]; g.ldo = C;
+      } else {
+        em = PAR_E_RELU_RES; g.xres = px[cur]; g.xout = px[nxt]; g.oout = opnd_copy ? pxb[nxt] : nullptr; g.ldo = C;
+      }
+      HIP_TRY(launch_par_gemm(g, p.dtype, PAR_A_CONV, em, s));
+      if (gated && l + 1 < L) {  // the last layer's residual output feeds nothing
+        ParGemm r;
+        memset(&r, 0, sizeof(r));
+        r.M = M; r.N = C; r.K = C; r.Tcur = Tcur;
+        r.A = ws + p.off_pz + (size_t)l * C * es; r.lda = (long long)L * C;
+        r.W = ws + p.off_pres[l];
+        r.bias = (const float *)(ws + p.off_res_b[l]);
+        r.xres = px[cur]; r.xout = px[nxt]; r.oout = opnd_copy ? pxb[nxt] : nullptr; r.ldo = C;
+        HIP_TRY(launch_par_gemm(r, p.dtype, PAR_A_PLAIN, PAR_E_RES_ADD, s));
+      }
+      ParRing q;
+      memset(&q, 0, sizeof(q));
+      q.ring = ring + (size_t)p.ring_off[l] * es; q.src = pxb[cur];
+      q.t0 = t0; q.Tcur = Tcur; q.dil = h->dil[l]; q.brows = p.brows; q.batch = batch; q.row_bytes = C * es;
+      HIP_TRY(launch_par_ring(q, s));
+      cur = nxt;
+    }
+    if (!logits) continue;
+    ParGemm o;
+    memset(&o, 0, sizeof(o));
+    o.M = M; o.N = p.Q; o.Tcur = Tcur; o.logits = logits; o.n_steps = n; o.s0 = s0;
+    o.W = ws + p.off_pout;
+    o.bias = (const float *)(ws + p.off_out_b);
+    if (gated) {
+      ParGemm k;
+      memset(&k, 0, sizeof(k));
+      k.M = M; k.N = p.S; k.K = L * C; k.Tcur = Tcur;
+      k.A = ws + p.off_pz; k.lda = (long long)L * C;
+      k.W = ws + p.off_pskip;
+      k.bias = (const float *)(ws + p.off_pskip_b);
+      k.oout = ws + p.off_psb; k.ldo = p.S;
+      HIP_TRY(launch_par_gemm(k, p.dtype, PAR_A_PLAIN, PAR_E_RELU, s));
+      ParGemm hd;
+      memset(&hd, 0, sizeof(hd));
+      hd.M = M; hd.N = p.H; hd.K = p.S; hd.Tcur = Tcur;
+      hd.A = ws + p.off_psb; hd.lda = p.S;
+      hd.W = ws + p.off_phead;
+      hd.bias = (const float *)(ws + p.off_head_b);
+      hd.oout = ws + p.off_phb; hd.ldo = p.H;
+      HIP_TRY(launch_par_gemm(hd, p.dtype, PAR_A_PLAIN, PAR_E_RELU, s));
+      o.A = ws + p.off_phb; o.lda = p.H; o.K = p.H;
+    } else {
+      o.A = pxb[cur]; o.lda = C; o.K = C;
+    }
+    HIP_TRY(launch_par_gemm(o, p.dtype, PAR_A_PLAIN, PAR_E_LOGITS, s));
+  }
+  if (mode == MODE_ONLINE) HIP_TRY(launch_par_set_last(inputs, (int32_t *)(ws + p.off_last), batch, n, s));
+  return FWG_OK;
 }
 
 }  // namespace
@@ -302,6 +461,23 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_repack(w->out, ws + p.off_out, REPACK_LINEAR, dt, Kout, p.Q, C, s));
   TRY_OR_FREE(launch_copy_bias(w->out_b, (float *)(ws + p.off_out_b), p.Q, s));
   TRY_OR_FREE(hipMemcpyAsync(ws + p.off_layers, table.data(), sizeof(LayerDev) * p.L, hipMemcpyHostToDevice, s));
+  if (p.par_ok) {
+    const int il = p.kind == FWG_GATED;  // gated conv rows interleave tanh and sigmoid channel groups
+    for (int l = 0; l < p.L; ++l) {
+      TRY_OR_FREE(launch_par_repack(w->conv[l], ws + p.off_pconv[l], PAR_REPACK_CONV, dt, p.Co, 2 * C, C, il, 0, 0, s));
+      TRY_OR_FREE(launch_par_bias(w->conv_b ? w->conv_b[l] : nullptr, (float *)(ws + p.off_pconv_b[l]), p.Co, il, 0, s));
+      if (p.kind == FWG_GATED) {
+        TRY_OR_FREE(launch_par_repack(w->res[l], ws + p.off_pres[l], PAR_REPACK_COPY, dt, C, C, C, 0, C, 0, s));
+        TRY_OR_FREE(launch_par_repack(w->skip[l], ws + p.off_pskip, PAR_REPACK_COPY, dt, p.S, C, C, 0,
+                                      (long long)p.L * C, (long long)l * C, s));
+        TRY_OR_FREE(launch_par_bias((const float *)(ws + p.off_skip_b[l]), (float *)(ws + p.off_pskip_b), p.S, 0,
+                                    l > 0, s));
+      }
+    }
+    if (p.kind == FWG_GATED)
+      TRY_OR_FREE(launch_par_repack(w->head, ws + p.off_phead, PAR_REPACK_COPY, dt, p.H, p.S, C, 0, p.S, 0, s));
+    TRY_OR_FREE(launch_par_repack(w->out, ws + p.off_pout, PAR_REPACK_COPY, dt, p.Q, Kout, C, 0, Kout, 0, s));
+  }
   std::vector<const void *> ptrs;
   if (p.regime == REGIME_MFMA) {
     char *frags = ws + p.off_frags;
@@ -368,6 +544,7 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
   if (seq_len == 0) return FWG_OK;
   if (!inputs || !logits) return fail(FWG_EINVAL, "inputs and logits are required");
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_tf, (size_t)p.queue_elems * p.es, h->stream));
+  if (use_parallel(h, seq_len)) return par_forward(h, MODE_TEACHER, batch, seq_len, inputs, logits, h->ws + p.off_ring_tf, 0);
   StepArgs a = base_args(h);
   a.ring = h->ws + p.off_ring_tf;
   a.inputs = inputs;
@@ -388,16 +565,22 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
   if (h->bound_batch >= 0 && h->bound_batch != batch)
     return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
   if (n_steps == 0) return FWG_OK;
-  if (!inputs || !logits) return fail(FWG_EINVAL, "inputs and logits are required");
-  StepArgs a = base_args(h);
-  a.ring = h->ws + p.off_ring_gen;
-  a.inputs = inputs;
-  a.logits = logits;
-  a.t0 = h->t;
-  a.n_steps = n_steps;
-  a.batch = batch;
-  a.mode = MODE_ONLINE;
-  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  if (!inputs) return fail(FWG_EINVAL, "inputs are required");
+  if (use_parallel(h, n_steps)) {
+    const int rc = par_forward(h, MODE_ONLINE, batch, n_steps, inputs, logits, h->ws + p.off_ring_gen, h->t);
+    if (rc != FWG_OK) return rc;
+  } else {
+    StepArgs a = base_args(h);
+    a.ring = h->ws + p.off_ring_gen;
+    a.inputs = inputs;
+    a.logits = logits;
+    a.t0 = h->t;
+    a.n_steps = n_steps;
+    a.batch = batch;
+    a.mode = MODE_ONLINE;
+    HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream)
+                                    : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  }
   h->bound_batch = batch;
   h->t += n_steps;
   return FWG_OK;

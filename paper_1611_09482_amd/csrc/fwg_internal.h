@@ -126,6 +126,53 @@ hipError_t launch_mfma_bias_block(const float *const *conv_b, const float *const
                                   const float *head_b, const float *out_b, const float *emb_b, int L, float *dst,
                                   hipStream_t s);
 
+// Time-parallel path (fwg_parallel.hip).  One GEMM launch: C = A . W^T over the rows of a
+// chunk (m = b * Tcur + j for time t0 + j), W operand-typed [N][K] rows.
+struct ParGemm {
+  int M, N, K;
+  const void *A;           // plain: operand rows with stride lda; conv: the layer input rows (stride C)
+  long long lda;
+  const void *ring;        // conv: this layer's queue, [dil][brows][C] operand-typed
+  long long t0;            // time of row j = 0
+  int dil, brows, Tcur, C;
+  const void *W;
+  const float *bias;       // [N]
+  const float *xres;       // residual epilogues: fp32 input rows (stride ldo)
+  float *xout;             // residual epilogues: fp32 output rows (stride ldo)
+  void *oout;              // operand-typed output rows (stride ldo); NULL when it aliases xout
+  long long ldo;
+  int zoff;                // gate: column offset of this layer in the z rows
+  float *logits;           // logits epilogue: [batch][n_steps][N]
+  long long n_steps, s0;
+};
+struct ParEmbed {
+  int M, C, Tcur, mode;
+  long long s0, n_steps;
+  const int32_t *inputs;   // [batch][n_steps]
+  const int32_t *last;     // pending input per stream (online prediction)
+  const void *embed;       // [Q][C] operand-typed
+  const float *embed_b;
+  float *xout;             // fp32 rows (NULL when not kept)
+  void *oout;              // operand rows
+};
+struct ParRing {
+  void *ring;              // this layer's queue [dil][brows][row_bytes]
+  const void *src;         // the layer input rows of the chunk
+  long long t0;
+  int Tcur, dil, brows, batch, row_bytes;
+};
+enum ParRepack { PAR_REPACK_CONV = 0, PAR_REPACK_COPY = 1 };
+enum ParAMode { PAR_A_PLAIN = 0, PAR_A_CONV = 1 };
+enum ParEMode { PAR_E_RELU = 0, PAR_E_RELU_RES = 1, PAR_E_RES_ADD = 2, PAR_E_GATE = 3, PAR_E_LOGITS = 4 };
+constexpr int kParKTileBytes = 128;  // K of every product must be a multiple of 128 bytes of operands
+hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s);
+hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s);
+hipError_t launch_par_ring(const ParRing &r, hipStream_t s);
+hipError_t launch_par_set_last(const int32_t *inputs, int32_t *last, int batch, int n_steps, hipStream_t s);
+hipError_t launch_par_repack(const void *src, void *dst, int mode, int dtype, int N, int K, int C, int interleave,
+                             long long ldd, long long doff, hipStream_t s);
+hipError_t launch_par_bias(const float *src, float *dst, int N, int interleave, int accumulate, hipStream_t s);
+
 // Repack modes: how W^T[k][n] is read from the caller's PyTorch layout.
 enum RepackMode {
   REPACK_LINEAR = 0,  // src [N][K] (out, in)

@@ -282,10 +282,11 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     __syncthreads();
 
     if (a.mode != MODE_GENERATE) {
-      for (int i = tid; i < nrows * Q; i += kThreads) {
-        const int r = i / Q, q = i % Q;
-        a.logits[((long long)(b0 + r) * a.n_steps + s) * Q + q] = lg[i];
-      }
+      if (a.logits)
+        for (int i = tid; i < nrows * Q; i += kThreads) {
+          const int r = i / Q, q = i % Q;
+          a.logits[((long long)(b0 + r) * a.n_steps + s) * Q + q] = lg[i];
+        }
       // the next input: the following element of the forced sequence (teacher forcing), or this
       // step's observed sample (online prediction)
       const int nx = s + forced_shift(a.mode);

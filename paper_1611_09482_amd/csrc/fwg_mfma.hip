@@ -314,7 +314,7 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
 #pragma unroll
     for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
       const int r = c.w + kMfWaves * kk;
-      if (r < c.nrows) {
+      if (r < c.nrows && a.logits) {
         const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
         *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
       }

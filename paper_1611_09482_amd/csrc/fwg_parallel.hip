@@ -1,0 +1,371 @@
+// Time-parallel evaluation of the dilated stack over a whole input sequence (gfx950).
+//
+// With every input known in advance (teacher forcing, online prediction over an
+// observed stretch, priming the queues from a prefix), the stack need not run one
+// step at a time: each layer is a width-2 dilated causal convolution over the
+// whole sequence, the training-time view of the network (paper Section 1), and
+// its products become dense GEMMs with one row per (stream, time) pair.
+//
+// A call is cut into chunks of Tc steps.  Rows of a chunk are stream-major,
+// m = b * Tc + j for time t0 + j.  Layer l reads x^{l-1} at t and at t - d_l; the
+// second comes from the chunk's own rows when t - d_l lies in the chunk, and from
+// the layer's convolution queue otherwise (the queue holds exactly the states
+// x^{l-1}_{t0-d_l} ... x^{l-1}_{t0-1}, slot = time mod d_l, Section 2.1).  After the
+// layer, the chunk's newest d_l states replace the queue contents, so the queues
+// leave the call in the state the step-by-step pop/push loop (Section 2.2) would
+// have left them, and a later generation call continues from there.
+//
+// Kernels:
+//   par_gemm_kernel   C[m][n] = A[m][:] . W[n][:] with a row-gathering prologue
+//                     (plain rows, or the two taps of the dilated convolution)
+//                     and an epilogue per layer kind (relu, relu + residual,
+//                     gate, residual add, logits).  64 x 64 tiles, 4 waves of
+//                     32 x 32, operands staged through LDS in 128-byte k-tiles,
+//                     MFMA 16x16x32 bf16 or 16x16x4 f32 with fp32 accumulation.
+//   par_embed_kernel  x^0 rows: the 1x1 convolution of the one-hot input (a row
+//                     gather), from the forced sequence or the pending input.
+//   par_ring_kernel   the queue refresh after each layer.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fwg_internal.h"
+
+namespace fwg {
+namespace par {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int BM = 64, BN = 64, NT = 256;
+constexpr int KT_BYTES = 128;            // bytes of one row inside a k-tile
+constexpr int ROWB = KT_BYTES + 16;      // LDS row stride (padding spreads the rows over banks)
+
+__device__ __forceinline__ float round_bf16(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return __uint_as_float(u & 0xffff0000u);
+}
+__device__ __forceinline__ uint16_t bf16_bits(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Operand types: float (f32 models) or uint16_t (bf16 bit patterns).
+template <typename OT> struct Op;
+template <> struct Op<float> {
+  static constexpr int KT = KT_BYTES / 4;  // k per tile
+  __device__ static __forceinline__ float get(const void *p, long long i) { return ((const float *)p)[i]; }
+  __device__ static __forceinline__ void put(void *p, long long i, float v) { ((float *)p)[i] = v; }
+  __device__ static __forceinline__ float opnd(float v) { return v; }
+  // one 16-byte chunk of A and of B per lane and half-tile: 4 MFMAs of k = 4, element j of lane
+  // group g standing for k = 4g + j on both sides
+  __device__ static __forceinline__ f32x4 mma(const uint4 &a, const uint4 &b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+  }
+};
+template <> struct Op<uint16_t> {
+  static constexpr int KT = KT_BYTES / 2;
+  __device__ static __forceinline__ float get(const void *p, long long i) {
+    return __uint_as_float(((uint32_t)((const uint16_t *)p)[i]) << 16);
+  }
+  __device__ static __forceinline__ void put(void *p, long long i, float v) { ((uint16_t *)p)[i] = bf16_bits(v); }
+  __device__ static __forceinline__ float opnd(float v) { return round_bf16(v); }
+  // lane group g holds k = 8g .. 8g + 7 of both operands
+  __device__ static __forceinline__ f32x4 mma(const uint4 &a, const uint4 &b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                  0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ float sigmoid(float g) { return 1.f / (1.f + __expf(-g)); }
+
+// Row sources of the A operand.
+constexpr int A_PLAIN = PAR_A_PLAIN, A_CONV = PAR_A_CONV;
+// Epilogues:
+//   E_RELU      out = opnd(relu(acc + b))
+//   E_RELU_RES  x = x_in + relu(acc + b): fp32 x and its operand copy
+//   E_RES_ADD   x = x_in + acc + b:       fp32 x and its operand copy
+//   E_GATE      z = tanh(.) * sigmoid(.) over interleaved column pairs -> operand z
+//   E_LOGITS    logits[b][s0 + j][n] = acc + b
+constexpr int E_RELU = PAR_E_RELU, E_RELU_RES = PAR_E_RELU_RES, E_RES_ADD = PAR_E_RES_ADD, E_GATE = PAR_E_GATE,
+              E_LOGITS = PAR_E_LOGITS;
+
+template <typename OT, int AM>
+__device__ __forceinline__ uint4 load_a(const ParGemm &g, int m, int k) {
+  if (m >= g.M) return make_uint4(0, 0, 0, 0);
+  if (AM == A_PLAIN) return *(const uint4 *)((const OT *)g.A + (long long)m * g.lda + k);
+  // dilated convolution: k < C is tap 0 (the state d steps back), k >= C tap 1 (the current state)
+  const OT *src;
+  if (k >= g.C) {
+    src = (const OT *)g.A + (long long)m * g.C + (k - g.C);
+  } else {
+    const int b = m / g.Tcur, j = m - b * g.Tcur;
+    if (j >= g.dil) {
+      src = (const OT *)g.A + (long long)(m - g.dil) * g.C + k;
+    } else {
+      const long long tau = g.t0 + j - g.dil;              // >= -dil: before time 0 the slot holds zeros
+      const long long slot = tau >= 0 ? tau % g.dil : tau + g.dil;
+      src = (const OT *)g.ring + (slot * g.brows + b) * (long long)g.C + k;
+    }
+  }
+  return *(const uint4 *)src;
+}
+
+template <typename OT>
+__device__ __forceinline__ uint4 load_w(const ParGemm &g, int n, int k) {
+  if (n >= g.N) return make_uint4(0, 0, 0, 0);
+  return *(const uint4 *)((const OT *)g.W + (long long)n * g.K + k);
+}
+
+template <typename OT, int AM, int EM>
+__global__ void __launch_bounds__(NT) par_gemm_kernel(ParGemm g) {
+  __shared__ __attribute__((aligned(16))) unsigned char lds_a[BM * ROWB];
+  __shared__ __attribute__((aligned(16))) unsigned char lds_b[BN * ROWB];
+  constexpr int KT = Op<OT>::KT;
+  constexpr int EPC = 16 / sizeof(OT);  // elements per 16-byte chunk
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w & 1, wn = w >> 1;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  // staging: thread -> (row, 16-byte chunk) for rows r and r + 32
+  const int sr = tid >> 3, sq = tid & 7;
+
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = g.K / KT;
+  uint4 ra0 = load_a<OT, AM>(g, m0 + sr, sq * EPC), ra1 = load_a<OT, AM>(g, m0 + sr + 32, sq * EPC);
+  uint4 rb0 = load_w<OT>(g, n0 + sr, sq * EPC), rb1 = load_w<OT>(g, n0 + sr + 32, sq * EPC);
+  const int lr = lane & 15, lg = lane >> 4;
+  for (int kt = 0; kt < nk; ++kt) {
+    *(uint4 *)(lds_a + sr * ROWB + sq * 16) = ra0;
+    *(uint4 *)(lds_a + (sr + 32) * ROWB + sq * 16) = ra1;
+    *(uint4 *)(lds_b + sr * ROWB + sq * 16) = rb0;
+    *(uint4 *)(lds_b + (sr + 32) * ROWB + sq * 16) = rb1;
+    __syncthreads();
+    if (kt + 1 < nk) {
+      const int k = (kt + 1) * KT + sq * EPC;
+      ra0 = load_a<OT, AM>(g, m0 + sr, k);
+      ra1 = load_a<OT, AM>(g, m0 + sr + 32, k);
+      rb0 = load_w<OT>(g, n0 + sr, k);
+      rb1 = load_w<OT>(g, n0 + sr + 32, k);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        a[i] = *(const uint4 *)(lds_a + (32 * wm + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+        b[i] = *(const uint4 *)(lds_b + (32 * wn + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = Op<OT>::mma(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: acc[i][j][e] is row 32 wm + 16 i + 4 lg + e, column 32 wn + 16 j + lr of the tile
+  if (EM == E_GATE) {
+    // columns come in groups of 32: 16 tanh columns, then the 16 sigmoid columns of the same channels
+    const int grp = (n0 + 32 * wn) >> 5;
+    if (32 * grp >= g.N) return;
+    const int ch = 16 * grp + lr;
+    const float bt = g.bias[32 * grp + lr], bs = g.bias[32 * grp + 16 + lr];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + 32 * wm + 16 * i + 4 * lg + e;
+        if (m < g.M) {
+          const float z = tanhf(acc[i][0][e] + bt) * sigmoid(acc[i][1][e] + bs);
+          Op<OT>::put(g.oout, (long long)m * g.ldo + g.zoff + ch, z);
+        }
+      }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = n0 + 32 * wn + 16 * j + lr;
+    if (n >= g.N) continue;
+    const float bn = g.bias[n];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int m = m0 + 32 * wm + 16 * i + 4 * lg + e;
+        if (m >= g.M) continue;
+        const float v = acc[i][j][e] + bn;
+        if (EM == E_RELU) {
+          Op<OT>::put(g.oout, (long long)m * g.ldo + n, fmaxf(v, 0.f));
+        } else if (EM == E_RELU_RES || EM == E_RES_ADD) {
+          const long long at = (long long)m * g.ldo + n;
+          const float x = g.xres[at] + (EM == E_RELU_RES ? fmaxf(v, 0.f) : v);
+          g.xout[at] = x;
+          if (g.oout) Op<OT>::put(g.oout, at, x);
+        } else {  // E_LOGITS
+          const int b = m / g.Tcur, jj = m - b * g.Tcur;
+          g.logits[((long long)b * g.n_steps + g.s0 + jj) * g.N + n] = v;
+        }
+      }
+  }
+}
+
+template <typename OT, int AM>
+static hipError_t launch_em(const ParGemm &g, int em, dim3 grid, hipStream_t s) {
+  switch (em) {
+    case E_RELU: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU>), grid, dim3(NT), 0, s, g); break;
+    case E_RELU_RES: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU_RES>), grid, dim3(NT), 0, s, g); break;
+    case E_RES_ADD: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RES_ADD>), grid, dim3(NT), 0, s, g); break;
+    case E_GATE: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_GATE>), grid, dim3(NT), 0, s, g); break;
+    case E_LOGITS: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_LOGITS>), grid, dim3(NT), 0, s, g); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// x^0 rows: E[token] + b, fp32 stream and operand copy.  Tokens: the forced sequence
+// (teacher forcing) or, in online prediction, the pending input followed by the
+// observed samples.
+template <typename OT>
+__global__ void par_embed_kernel(ParEmbed e) {
+  const long long total = (long long)e.M * e.C;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
+    const int m = (int)(i / e.C), c = (int)(i - (long long)m * e.C);
+    const int b = m / e.Tcur, j = m - b * e.Tcur;
+    const long long st = e.s0 + j;  // step index inside the call
+    int tok;
+    if (e.mode == MODE_TEACHER) tok = e.inputs[(long long)b * e.n_steps + st];
+    else tok = st == 0 ? e.last[b] : e.inputs[(long long)b * e.n_steps + st - 1];
+    const float v = Op<OT>::get(e.embed, (long long)tok * e.C + c) + e.embed_b[c];
+    if (e.xout) e.xout[i] = v;
+    Op<OT>::put(e.oout, i, v);
+  }
+}
+
+// Queue refresh after layer l: slot k takes the newest state of this chunk whose time is
+// k mod d (if the chunk reaches that slot); the operand rows of the layer's input are copied
+// in 16-byte pieces.
+__global__ void par_ring_kernel(ParRing r) {
+  const int pieces = r.row_bytes / 16;
+  const long long total = (long long)r.batch * r.dil * pieces;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
+    const int q = (int)(i % pieces);
+    const long long bk = i / pieces;
+    const int k = (int)(bk % r.dil), b = (int)(bk / r.dil);
+    const long long last_t = r.t0 + r.Tcur - 1;
+    long long back = (last_t - k) % r.dil;                   // last_t may be below k: keep it non-negative
+    if (back < 0) back += r.dil;
+    const long long tnew = last_t - back;                    // newest time <= last_t with slot k
+    if (tnew < r.t0) continue;                               // the chunk is shorter than d: slot kept
+    const long long m = (long long)b * r.Tcur + (tnew - r.t0);
+    const uint4 v = *(const uint4 *)((const char *)r.src + m * r.row_bytes + q * 16);
+    *(uint4 *)((char *)r.ring + ((long long)k * r.brows + b) * r.row_bytes + q * 16) = v;
+  }
+}
+
+__global__ void par_set_last_kernel(const int32_t *inputs, int32_t *last, int batch, int n_steps) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < batch) last[b] = inputs[(long long)b * n_steps + n_steps - 1];
+}
+
+// ---------------------------------------------------------------------------
+// Weight repacks (at create) into plain [N][K] operand rows.
+template <typename T>
+__global__ void par_repack_kernel(const T *__restrict__ src, T *__restrict__ dst, int mode, int N, int K, int C,
+                                  int interleave, long long ldd, long long doff) {
+  const long long total = (long long)N * K;
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
+    const int n = (int)(i / K), k = (int)(i - (long long)n * K);
+    if (mode == PAR_REPACK_CONV) {
+      // dst row n holds conv output channel o(n): [tap 0 over C | tap 1 over C]
+      int o = n;
+      if (interleave) {
+        const int grp = n >> 5, wi = n & 31, R = N / 2;
+        o = wi < 16 ? 16 * grp + wi : R + 16 * grp + (wi - 16);
+      }
+      const int tap = k >= C, c = k - tap * C;
+      dst[i] = src[((long long)o * C + c) * 2 + tap];
+    } else {  // PAR_REPACK_COPY: src [N][K] into dst rows of stride ldd at column offset doff
+      dst[(long long)n * ldd + doff + k] = src[i];
+    }
+  }
+}
+
+__global__ void par_bias_kernel(const float *src, float *dst, int N, int interleave, int accumulate) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  int o = n;
+  if (interleave) {
+    const int grp = n >> 5, wi = n & 31, R = N / 2;
+    o = wi < 16 ? 16 * grp + wi : R + 16 * grp + (wi - 16);
+  }
+  const float v = src ? src[o] : 0.f;
+  dst[n] = accumulate ? dst[n] + v : v;
+}
+
+}  // namespace par
+
+// ---------------------------------------------------------------------------
+static int grid_for(long long total) {
+  const long long b = (total + 255) / 256;
+  return (int)(b < 8192 ? (b > 0 ? b : 1) : 8192);
+}
+
+hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s) {
+  if (g.M <= 0) return hipSuccess;
+  const dim3 grid((g.M + par::BM - 1) / par::BM, (g.N + par::BN - 1) / par::BN);
+  if (dtype == 1)
+    return amode == par::A_CONV ? par::launch_em<uint16_t, par::A_CONV>(g, emode, grid, s)
+                                : par::launch_em<uint16_t, par::A_PLAIN>(g, emode, grid, s);
+  return amode == par::A_CONV ? par::launch_em<float, par::A_CONV>(g, emode, grid, s)
+                              : par::launch_em<float, par::A_PLAIN>(g, emode, grid, s);
+}
+
+hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {
+  const int grid = grid_for((long long)e.M * e.C);
+  if (dtype == 1) hipLaunchKernelGGL(par::par_embed_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, e);
+  else hipLaunchKernelGGL(par::par_embed_kernel<float>, dim3(grid), dim3(256), 0, s, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_par_ring(const ParRing &r, hipStream_t s) {
+  const int grid = grid_for((long long)r.batch * r.dil * (r.row_bytes / 16));
+  hipLaunchKernelGGL(par::par_ring_kernel, dim3(grid), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_par_set_last(const int32_t *inputs, int32_t *last, int batch, int n_steps, hipStream_t s) {
+  hipLaunchKernelGGL(par::par_set_last_kernel, dim3((batch + 255) / 256), dim3(256), 0, s, inputs, last, batch,
+                     n_steps);
+  return hipGetLastError();
+}
+
+hipError_t launch_par_repack(const void *src, void *dst, int mode, int dtype, int N, int K, int C, int interleave,
+                             long long ldd, long long doff, hipStream_t s) {
+  const int grid = grid_for((long long)N * K);
+  if (dtype == 1)
+    hipLaunchKernelGGL(par::par_repack_kernel<uint16_t>, dim3(grid), dim3(256), 0, s, (const uint16_t *)src,
+                       (uint16_t *)dst, mode, N, K, C, interleave, ldd, doff);
+  else
+    hipLaunchKernelGGL(par::par_repack_kernel<float>, dim3(grid), dim3(256), 0, s, (const float *)src, (float *)dst,
+                       mode, N, K, C, interleave, ldd, doff);
+  return hipGetLastError();
+}
+
+hipError_t launch_par_bias(const float *src, float *dst, int N, int interleave, int accumulate, hipStream_t s) {
+  hipLaunchKernelGGL(par::par_bias_kernel, dim3((N + 255) / 256), dim3(256), 0, s, src, dst, N, interleave,
+                     accumulate);
+  return hipGetLastError();
+}
+
+}  // namespace fwg

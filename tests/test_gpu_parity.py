@@ -65,14 +65,23 @@ FAMILIES = {
 FORCE_VALU = {"gated_r64_bf16_valu"}
 
 
-def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None):
+def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_rows=None):
+    """path: None (the library's choice), "step" or "parallel" for the forced calls;
+    par_rows: rows per chunk of the time-parallel path (small values force many chunks)."""
     w = W.make_weights(cfg, seed, bias_scale=bias_scale)
+    env = {}
     if fam in FORCE_VALU:
-        os.environ["FWG_REGIME"] = "valu"
+        env["FWG_REGIME"] = "valu"
+    if path is not None:
+        env["FWG_FORCED_PATH"] = path
+    if par_rows is not None:
+        env["FWG_PAR_ROWS"] = str(par_rows)
+    os.environ.update(env)
     try:
         fw = binding.from_model(cfg, w, max_batch=max_batch)
     finally:
-        os.environ.pop("FWG_REGIME", None)
+        for k in env:
+            os.environ.pop(k, None)
     if fam is not None:
         want_valu = fam in FORCE_VALU or cfg.dtype != W.BF16
         assert (fw.regime == "valu") == want_valu, (fam, fw.regime)
@@ -110,20 +119,89 @@ def check_generation(cfg, fw, orc, u, batch, label):
     return g, first
 
 
+@pytest.mark.parametrize("path", ["step", "parallel"])
 @pytest.mark.parametrize("fam", list(FAMILIES))
-def test_teacher_forced_parity(fam):
+def test_teacher_forced_parity(fam, path):
     cfg = FAMILIES[fam]
-    B = 11 if cfg.channels < 512 else 5   # ragged: not a multiple of the rows per block
+    B = 11 if cfg.channels < 512 else 5   # ragged: not a multiple of the rows per block or tile
     T = cfg.queue_total + 60              # wraps every queue
-    w, fw, orc = build_pair(cfg, 100, B, fam=fam)
+    w, fw, orc = build_pair(cfg, 100, B, fam=fam, path=path)
     x = W.sequences(3, B, T)
     t0 = time.time()
     g = fw.teacher_forced(dev(x)).cpu().numpy()
     o = orc.teacher_forced(x)
     err = row_rel_err(g, o)
-    log(f"{fam} [{fw.regime}]: TF B={B} T={T} max row rel err {err.max():.3e} p99.9 {np.quantile(err, 0.999):.3e} "
-        f"({time.time() - t0:.1f}s)")
+    log(f"{fam} [{fw.regime}, {path}]: TF B={B} T={T} max row rel err {err.max():.3e} "
+        f"p99.9 {np.quantile(err, 0.999):.3e} ({time.time() - t0:.1f}s)")
     assert err.max() <= TOL[cfg.dtype]
+
+
+@pytest.mark.parametrize("fam,steps", [("relu_c32_f32", 7), ("gated_r32_f32", 5), ("gated_r64_bf16", 3),
+                                       ("relures_c512_f32", 64)])
+def test_parallel_chunks_across_queues(fam, steps):
+    """Time-parallel path with chunks far shorter than the dilations (and a ragged last chunk):
+    popped operands come from the queues written by earlier chunks; teacher forcing and online
+    prediction continued by generation both match the oracle."""
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5
+    brows = -(-B // 16) * 16 if (cfg.kind == W.GATED and cfg.dtype == W.BF16 and cfg.channels == 64) else B
+    w, fw, orc = build_pair(cfg, 103, B, fam=fam, path="parallel", par_rows=brows * steps)
+    T = cfg.queue_total + 61
+    x = W.sequences(14, B, T)
+    err = row_rel_err(fw.teacher_forced(dev(x)).cpu().numpy(), orc.teacher_forced(x))
+    log(f"{fam}: parallel TF in chunks of {steps} steps, T={T}: max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+    # online prediction over two forced stretches around a generated one, then generation again
+    u = W.uniforms(15, B, 40)
+    x = W.sequences(18, B, 177)
+    st = orc.state(B)
+    lg_a = fw.step_forced(dev(x[:, :100].copy())).cpu().numpy()
+    g = fw.generate(dev(u[:, :20].copy())).cpu().numpy()
+    lg_b = fw.step_forced(dev(x[:, 100:177].copy())).cpu().numpy()
+    o_a = st.step_forced(x[:, :100])
+    st.step_forced(g)
+    o_b = st.step_forced(x[:, 100:177])
+    err = max(row_rel_err(lg_a, o_a).max(), row_rel_err(lg_b, o_b).max())
+    assert err <= TOL[cfg.dtype], err
+    g2 = fw.generate(dev(u[:, 20:].copy())).cpu().numpy()
+    so, slg = st.generate(u[:, 20:], return_logits=True)
+    tau = TAU[cfg.dtype]
+    for b in range(B):
+        mism = np.nonzero(g2[b] != so[b])[0]
+        if mism.size:
+            t = int(mism[0])
+            lo, hi = cdf_bounds(slg[b, t], so[b, t])
+            assert min(u[b, 20 + t] - lo, hi - u[b, 20 + t]) < tau, (fam, b, t)
+
+
+@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "relu_c32_f32"])
+def test_prime_then_generate(fam):
+    """Priming (fwg_step_forced with logits = NULL) leaves the same state as online prediction
+    with logits: the generation that follows is bit-identical, and it matches the oracle primed
+    with the same prefix."""
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5
+    w, fw, orc = build_pair(cfg, 104, B, fam=fam)
+    prefix = W.sequences(16, B, cfg.queue_total + 33)
+    u = W.uniforms(17, B, 120)
+    fw.prime(dev(prefix))
+    g = fw.generate(dev(u)).cpu().numpy()
+    fw.reset()
+    fw.step_forced(dev(prefix))
+    assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), g)
+    st = orc.state(B)
+    st.step_forced(prefix)
+    so, slg = st.generate(u, return_logits=True)
+    tau = TAU[cfg.dtype]
+    first = []
+    for b in range(B):
+        mism = np.nonzero(g[b] != so[b])[0]
+        first.append(int(mism[0]) if mism.size else u.shape[1])
+        if mism.size:
+            t = int(mism[0])
+            lo, hi = cdf_bounds(slg[b, t], so[b, t])
+            assert min(u[b, t] - lo, hi - u[b, t]) < tau, (fam, b, t)
+    log(f"{fam}: generation after a {prefix.shape[1]}-step prime: first divergence min {min(first)}")
 
 
 @pytest.mark.parametrize("fam", list(FAMILIES))
