@@ -7,6 +7,10 @@ pushes its new states.  The timed region is one fwg_generate call of --steps
 steps (a single persistent kernel launch), bracketed by device synchronisation
 and HIP events recorded on the launch stream, with inputs resident in HBM.
 
+--mode teacher_forced times one fwg_teacher_forced call over the same batch and
+number of steps instead (a seeded random input sequence, logits for every step;
+the library evaluates it time-parallel), against the oracle's teacher-forced pass.
+
 Prints one JSON line (see the design doc for the field definitions).
 """
 from __future__ import annotations
@@ -70,6 +74,79 @@ def cpu_baseline(wl, weights, u, target_seconds: float):
                       f"OpenMP over streams, {dt:.1f} s wall"}
 
 
+def cpu_baseline_tf(wl, weights, x, target_seconds: float):
+    """The oracle's teacher-forced pass on a bounded sample: the first streams (one per thread) for
+    as many leading steps as fit the time budget."""
+    import oracle
+    threads = oracle.max_threads()
+    streams = max(1, min(wl.batch, threads))
+    o = oracle.Oracle(weights)
+    calib = 8
+    t0 = time.perf_counter()
+    o.teacher_forced(x[:streams, :calib].copy())
+    per_step = (time.perf_counter() - t0) / calib
+    steps = int(max(16, min(x.shape[1], target_seconds / max(per_step, 1e-9))))
+    t0 = time.perf_counter()
+    o.teacher_forced(x[:streams, :steps].copy())
+    dt = time.perf_counter() - t0
+    return {"value": streams * steps / dt, "unit": "samples/s", "cores": min(threads, streams),
+            "kind": "oracle",
+            "sample": f"float64 CPU oracle teacher-forcing streams 0..{streams - 1} of the {wl.batch}-stream "
+                      f"workload over steps 0..{steps - 1} of {x.shape[1]} (cached form, per-step cost constant), "
+                      f"OpenMP over streams, {dt:.1f} s wall"}
+
+
+def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
+    import numpy as np
+    import torch
+    import workloads as W
+    cfg = wl.model
+    B = wl.batch
+    x_host = W.sequences(wl.uniform_seed, B, max(K, Wu, 1))
+    x = torch.from_numpy(np.ascontiguousarray(x_host[:, :K])).cuda()
+    logits = torch.empty((B, K, cfg.n_classes), dtype=torch.float32, device="cuda")
+    if Wu > 0:
+        fw.teacher_forced(torch.from_numpy(np.ascontiguousarray(x_host[:, :Wu])).cuda())
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    fw.teacher_forced(x, out=logits)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1)
+    sec = ms / 1e3
+    dtype = "bf16" if cfg.dtype == W.BF16 else "f32"
+    samples = B * K
+    flops = float(cfg.flops_per_sample()) * samples
+    achieved = flops / sec / 1e12 if sec > 0 else 0.0
+    peak = PEAK_TFLOPS[dtype]
+    result = {
+        "metric": "teacher-forced samples/sec (batch x steps/s)",
+        "value": samples / sec if sec > 0 else 0.0,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wu,
+        "ms_per_step": ms / max(K, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": name, "description": wl.description, "batch": B, "seq_len": K,
+                   "mode": "teacher_forced", "path": os.environ.get("FWG_FORCED_PATH", "library default")},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None, "scope": "whole call (all kernels)",
+                     "algorithmic_flops_per_call": flops, "call_ms": ms},
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_tf(wl, weights, x_host, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -78,6 +155,7 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-time budget of the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=["generate", "teacher_forced"], default="generate")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy (counter calibration for rocprofv3)")
     args = ap.parse_args()
@@ -115,6 +193,11 @@ def main():
     B = wl.batch
 
     weights = W.make_weights(cfg, wl.weight_seed)
+    if args.mode == "teacher_forced":
+        stream = torch.cuda.current_stream()
+        fw = binding.from_model(cfg, weights, max_batch=B, stream=stream)
+        bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu)
+        return
     u_host = W.uniforms(wl.uniform_seed, B, max(K, Wu, 1))
     u_timed = torch.from_numpy(np.ascontiguousarray(u_host[:, :K])).cuda()
     u_warm = torch.from_numpy(np.ascontiguousarray(u_host[:, :Wu])).cuda()

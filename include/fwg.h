@@ -175,6 +175,25 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
  * in each queue the newest d_l states, as the step-by-step loop would. */
 int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
 
+/* Naive generation, the baseline the paper measures against (Section 1, Fig. 1;
+ * Section 3): every sample recomputes, from the last receptive-field inputs, each
+ * distinct node of the tree of layer states the output depends on (a node that
+ * several branches reach is computed once per sample), and nothing is cached
+ * between samples.  Same model, sampling rule and contract as fwg_generate
+ * (uniforms DEVICE float32 [batch][n_steps], samples DEVICE int32
+ * [batch][n_steps]), but with its own state: the per-stream input history and
+ * its own time and batch binding, reset by fwg_reset_queues (the history then
+ * starts with seed_input).  One kernel sequence per sample; for comparison and
+ * testing, not for throughput.  Returns FWG_EUNSUPPORTED where the model has
+ * no time-parallel kernels or its chunk buffers cannot hold max_batch x (the
+ * tree's input nodes) rows. */
+int fwg_generate_naive(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples);
+
+/* Layer-node evaluations per sample of fwg_generate_naive: the number of
+ * distinct nodes of the tree over layers 1..L (Section 3.1; the cached method
+ * evaluates L).  Pure host computation. */
+int fwg_naive_nodes(const fwg_desc *desc, int64_t *nodes);
+
 /* Free the host-side handle (the workspace stays the caller's). NULL is a no-op. */
 int fwg_destroy(fwg_handle *h);
 

@@ -16,7 +16,8 @@ _STATUS = {FWG_EINVAL: "EINVAL", FWG_ENOSPACE: "ENOSPACE", FWG_EHIP: "EHIP", FWG
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfwg.so")
 
 EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-            "fwg_step_forced", "fwg_destroy", "fwg_last_error", "fwg_regime"]
+            "fwg_step_forced", "fwg_generate_naive", "fwg_naive_nodes", "fwg_destroy", "fwg_last_error",
+            "fwg_regime"]
 
 
 class FwgError(RuntimeError):
@@ -61,12 +62,14 @@ def load_library(path: Optional[str] = None):
     L.fwg_generate.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_teacher_forced.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_step_forced.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_generate_naive.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_naive_nodes.argtypes = [ctypes.POINTER(fwg_desc), ctypes.POINTER(ctypes.c_int64)]
     L.fwg_destroy.argtypes = [vp]
     L.fwg_last_error.restype = ctypes.c_char_p
     L.fwg_regime.argtypes = [vp]
     L.fwg_regime.restype = ctypes.c_char_p
     for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-                 "fwg_step_forced", "fwg_destroy"]:
+                 "fwg_step_forced", "fwg_generate_naive", "fwg_naive_nodes", "fwg_destroy"]:
         getattr(L, name).restype = ctypes.c_int
     if path is None:
         _lib = L
@@ -90,6 +93,13 @@ def make_desc(kind: int, dtype: int, channels: int, dilations: Sequence[int], ma
 def workspace_size(desc: fwg_desc) -> int:
     n = ctypes.c_size_t(0)
     _check(load_library().fwg_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def naive_nodes(desc: fwg_desc) -> int:
+    """Layer-node evaluations per sample of the naive generator (distinct nodes of the Fig. 1 tree)."""
+    n = ctypes.c_int64(0)
+    _check(load_library().fwg_naive_nodes(ctypes.byref(desc), ctypes.byref(n)))
     return n.value
 
 
@@ -175,6 +185,16 @@ class FastWavenet:
         if out is None:
             out = torch.empty((B, n, self.n_classes), dtype=torch.float32, device=inputs.device)
         _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), out.data_ptr()))
+        return out
+
+    def generate_naive(self, uniforms, out=None):
+        """The naive baseline generator (its own state): same contract as generate()."""
+        torch = self._torch
+        assert uniforms.dtype == torch.float32 and uniforms.is_cuda and uniforms.is_contiguous()
+        B, n = uniforms.shape
+        if out is None:
+            out = torch.empty((B, n), dtype=torch.int32, device=uniforms.device)
+        _check(self.lib.fwg_generate_naive(self.handle, B, n, uniforms.data_ptr(), out.data_ptr()))
         return out
 
     def prime(self, inputs):

@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <vector>
 
@@ -55,7 +56,46 @@ struct Plan {
   std::vector<size_t> off_pconv, off_pconv_b, off_pres;
   size_t off_pskip, off_pskip_b, off_phead, off_pout;
   size_t off_px[2], off_pxb[2], off_pz, off_psb, off_phb;
+  // naive generator: the nodes of the output's dependency tree (Fig. 1), level 0 = inputs
+  bool nv_ok;
+  std::vector<int> nv_n;         // [L + 1] distinct nodes per level
+  std::vector<size_t> nv_tab;    // [L + 1] int offset of the level's tables (toff; then tsrc0, tsrc1 for l >= 1)
+  std::vector<int32_t> nv_host;  // the tables, uploaded at create
+  long long nv_nodes;            // layer nodes per sample: sum of nv_n[1..L]
+  int nv_hc;                     // input-history capacity per stream (power of two >= receptive field)
+  size_t off_nv, off_hist, off_ztop, off_nlogits;
 };
+
+// Node sets of the tree of Fig. 1 for the output at offset 0: level L holds {0}; level l - 1 holds the
+// level-l offsets and the same offsets minus d_l (each distinct offset once).  Fills nv_n, nv_tab,
+// nv_host and nv_nodes.
+void naive_tables(Plan *p, const int32_t *dil) {
+  const int L = p->L;
+  std::vector<std::vector<int>> P(L + 1);
+  P[L] = {0};
+  for (int l = L; l >= 1; --l) {
+    std::vector<int> v = P[l];
+    for (int o : P[l]) v.push_back(o - dil[l - 1]);
+    std::sort(v.begin(), v.end());
+    v.erase(std::unique(v.begin(), v.end()), v.end());
+    P[l - 1] = v;
+  }
+  p->nv_n.assign(L + 1, 0);
+  p->nv_tab.assign(L + 1, 0);
+  p->nv_host.clear();
+  p->nv_nodes = 0;
+  for (int l = 0; l <= L; ++l) {
+    p->nv_n[l] = (int)P[l].size();
+    p->nv_tab[l] = p->nv_host.size();
+    p->nv_host.insert(p->nv_host.end(), P[l].begin(), P[l].end());
+    if (l == 0) continue;
+    p->nv_nodes += p->nv_n[l];
+    const std::vector<int> &below = P[l - 1];
+    auto index_of = [&](int o) { return (int32_t)(std::lower_bound(below.begin(), below.end(), o) - below.begin()); };
+    for (int o : P[l]) p->nv_host.push_back(index_of(o - dil[l - 1]));
+    for (int o : P[l]) p->nv_host.push_back(index_of(o));
+  }
+}
 
 bool kblock_ok(int K, int N, int kb_elems) {
   if (K % kb_elems) return false;
@@ -215,6 +255,21 @@ int make_plan(const fwg_desc *d, Plan *p) {
     p->off_psb = gated ? take(R * p->S * p->es) : 0;
     p->off_phb = gated ? take(R * p->H * p->es) : 0;
   }
+  // naive generator: needs the time-parallel kernels and chunk buffers holding max_batch x (level-0 nodes)
+  p->nv_ok = false;
+  p->off_nv = p->off_hist = p->off_ztop = p->off_nlogits = 0;
+  if (p->par_ok) {
+    naive_tables(p, d->dilations);
+    if ((long long)p->bmax * p->nv_n[0] <= (long long)p->par_tc * p->brows) {
+      p->nv_ok = true;
+      p->nv_hc = 1;
+      while (p->nv_hc < dsum + 1) p->nv_hc <<= 1;
+      p->off_nv = take(sizeof(int32_t) * p->nv_host.size());
+      p->off_hist = take(sizeof(int32_t) * (size_t)p->bmax * p->nv_hc);
+      p->off_ztop = p->kind == FWG_GATED ? take((size_t)p->bmax * p->L * p->C * p->es) : 0;
+      p->off_nlogits = take(sizeof(float) * (size_t)p->bmax * p->Q);
+    }
+  }
   p->total = off;
   return FWG_OK;
 }
@@ -228,6 +283,8 @@ struct fwg_handle {
   hipStream_t stream;
   long long t;
   int bound_batch;  // -1: not bound since the last reset
+  long long nv_t;   // naive generator: its own time and batch binding (its state is the input history)
+  int nv_bound_batch;
 };
 
 namespace {
@@ -236,8 +293,12 @@ int enqueue_reset(fwg_handle *h) {
   const Plan &p = h->plan;
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_gen, (size_t)p.queue_elems * p.es, h->stream));
   HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_last), p.seed_input, p.bmax, h->stream));
+  if (p.nv_ok)  // every history entry the seed: the entry of time 0 is the first input
+    HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_hist), p.seed_input, p.bmax * p.nv_hc, h->stream));
   h->t = 0;
   h->bound_batch = -1;
+  h->nv_t = 0;
+  h->nv_bound_batch = -1;
   return FWG_OK;
 }
 
@@ -267,6 +328,96 @@ StepArgs base_args(const fwg_handle *h) {
   a.Q = p.Q;
   a.L = p.L;
   return a;
+}
+
+// One naive generation step at time t for every stream: evaluate the distinct nodes of the
+// output's dependency tree (Fig. 1) level by level from the input history, the head, and the
+// sample, which is appended to the history.  Nothing but the inputs is kept between samples.
+int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const float *uniforms, int32_t *samples) {
+  const Plan &p = h->plan;
+  hipStream_t st = h->stream;
+  char *ws = h->ws;
+  const int C = p.C, L = p.L, es = p.es;
+  const bool gated = p.kind == FWG_GATED;
+  const bool f32s = p.kind != FWG_RELU;
+  const bool opnd_copy = p.kind == FWG_RELU || p.dtype == FWG_BF16;
+  const int32_t *tab = (const int32_t *)(ws + p.off_nv);
+  float *px[2] = {(float *)(ws + p.off_px[0]), (float *)(ws + p.off_px[1])};
+  char *pxb[2] = {ws + p.off_pxb[0], ws + p.off_pxb[1]};
+  ParEmbed e;
+  memset(&e, 0, sizeof(e));
+  e.M = batch * p.nv_n[0]; e.C = C; e.Tcur = p.nv_n[0];
+  e.embed = ws + p.off_embed;
+  e.embed_b = (const float *)(ws + p.off_embed_b);
+  e.xout = f32s ? px[0] : nullptr;
+  e.oout = pxb[0];
+  e.toff = tab + p.nv_tab[0]; e.tnow = t;
+  e.hist = (const int32_t *)(ws + p.off_hist); e.hmask = p.nv_hc - 1;
+  HIP_TRY(launch_par_embed(e, p.dtype, st));
+  int cur = 0;
+  for (int l = 0; l < L; ++l) {
+    const int nxt = cur ^ 1, n = p.nv_n[l + 1], nprev = p.nv_n[l];
+    const int32_t *lt = tab + p.nv_tab[l + 1];
+    ParGemm g;
+    memset(&g, 0, sizeof(g));
+    g.M = batch * n; g.N = p.Co; g.K = 2 * C; g.Tcur = n; g.C = C; g.dil = h->dil[l];
+    g.A = pxb[cur]; g.lda = C;
+    g.toff = lt; g.tsrc0 = lt + n; g.tsrc1 = lt + 2 * n; g.nprev = nprev; g.tnow = t;
+    g.W = ws + p.off_pconv[l];
+    g.bias = (const float *)(ws + p.off_pconv_b[l]);
+    int em;
+    if (gated) {
+      em = PAR_E_GATE; g.oout = ws + p.off_pz; g.ldo = (long long)L * C; g.zoff = l * C; g.ztop = ws + p.off_ztop;
+    } else if (p.kind == FWG_RELU) {
+      em = PAR_E_RELU; g.oout = pxb[nxt]; g.ldo = C;
+    } else {
+      em = PAR_E_RELU_RES; g.xres = px[cur]; g.xout = px[nxt]; g.oout = opnd_copy ? pxb[nxt] : nullptr; g.ldo = C;
+    }
+    HIP_TRY(launch_par_gemm(g, p.dtype, PAR_A_TREE, em, st));
+    if (gated && l + 1 < L) {
+      ParGemm r;
+      memset(&r, 0, sizeof(r));
+      r.M = batch * n; r.N = C; r.K = C; r.Tcur = n;
+      r.A = ws + p.off_pz + (size_t)l * C * es; r.lda = (long long)L * C;
+      r.W = ws + p.off_pres[l];
+      r.bias = (const float *)(ws + p.off_res_b[l]);
+      r.xres = px[cur]; r.xout = px[nxt]; r.oout = opnd_copy ? pxb[nxt] : nullptr; r.ldo = C;
+      r.tsrc1 = lt + 2 * n; r.nprev = nprev;
+      HIP_TRY(launch_par_gemm(r, p.dtype, PAR_A_PLAIN, PAR_E_RES_ADD, st));
+    }
+    cur = nxt;
+  }
+  float *lg = (float *)(ws + p.off_nlogits);
+  ParGemm o;
+  memset(&o, 0, sizeof(o));
+  o.M = batch; o.N = p.Q; o.Tcur = 1; o.logits = lg; o.n_steps = 1; o.s0 = 0;
+  o.W = ws + p.off_pout;
+  o.bias = (const float *)(ws + p.off_out_b);
+  if (gated) {
+    ParGemm k;
+    memset(&k, 0, sizeof(k));
+    k.M = batch; k.N = p.S; k.K = L * C; k.Tcur = 1;
+    k.A = ws + p.off_ztop; k.lda = (long long)L * C;
+    k.W = ws + p.off_pskip;
+    k.bias = (const float *)(ws + p.off_pskip_b);
+    k.oout = ws + p.off_psb; k.ldo = p.S;
+    HIP_TRY(launch_par_gemm(k, p.dtype, PAR_A_PLAIN, PAR_E_RELU, st));
+    ParGemm hd;
+    memset(&hd, 0, sizeof(hd));
+    hd.M = batch; hd.N = p.H; hd.K = p.S; hd.Tcur = 1;
+    hd.A = ws + p.off_psb; hd.lda = p.S;
+    hd.W = ws + p.off_phead;
+    hd.bias = (const float *)(ws + p.off_head_b);
+    hd.oout = ws + p.off_phb; hd.ldo = p.H;
+    HIP_TRY(launch_par_gemm(hd, p.dtype, PAR_A_PLAIN, PAR_E_RELU, st));
+    o.A = ws + p.off_phb; o.lda = p.H; o.K = p.H;
+  } else {
+    o.A = pxb[cur]; o.lda = C; o.K = C;  // the last level holds the single node at offset 0
+  }
+  HIP_TRY(launch_par_gemm(o, p.dtype, PAR_A_PLAIN, PAR_E_LOGITS, st));
+  HIP_TRY(launch_par_sample(lg, uniforms, samples, (int32_t *)(ws + p.off_hist), p.nv_hc - 1, t + 1, batch, n_steps,
+                            s, st));
+  return FWG_OK;
 }
 
 // Forced calls shorter than this run on the step kernels (one launch) instead of the
@@ -461,6 +612,9 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_repack(w->out, ws + p.off_out, REPACK_LINEAR, dt, Kout, p.Q, C, s));
   TRY_OR_FREE(launch_copy_bias(w->out_b, (float *)(ws + p.off_out_b), p.Q, s));
   TRY_OR_FREE(hipMemcpyAsync(ws + p.off_layers, table.data(), sizeof(LayerDev) * p.L, hipMemcpyHostToDevice, s));
+  if (p.nv_ok)
+    TRY_OR_FREE(hipMemcpyAsync(ws + p.off_nv, p.nv_host.data(), sizeof(int32_t) * p.nv_host.size(),
+                               hipMemcpyHostToDevice, s));
   if (p.par_ok) {
     const int il = p.kind == FWG_GATED;  // gated conv rows interleave tanh and sigmoid channel groups
     for (int l = 0; l < p.L; ++l) {
@@ -583,6 +737,37 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
   }
   h->bound_batch = batch;
   h->t += n_steps;
+  return FWG_OK;
+}
+
+int fwg_generate_naive(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples) {
+  if (!h) return fail(FWG_EINVAL, "handle is NULL");
+  const Plan &p = h->plan;
+  if (!p.nv_ok)
+    return fail(FWG_EUNSUPPORTED, "no naive generator for this model: it needs the time-parallel kernels and "
+                                  "max_batch x receptive field rows of chunk buffers");
+  if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
+  if (n_steps < 0) return fail(FWG_EINVAL, "n_steps < 0");
+  if (h->nv_bound_batch >= 0 && h->nv_bound_batch != batch)
+    return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->nv_bound_batch);
+  if (n_steps == 0) return FWG_OK;
+  if (!uniforms || !samples) return fail(FWG_EINVAL, "uniforms and samples are required");
+  for (int s = 0; s < n_steps; ++s) {
+    const int rc = naive_step(h, batch, h->nv_t + s, n_steps, s, uniforms, samples);
+    if (rc != FWG_OK) return rc;
+  }
+  h->nv_bound_batch = batch;
+  h->nv_t += n_steps;
+  return FWG_OK;
+}
+
+int fwg_naive_nodes(const fwg_desc *desc, int64_t *nodes) {
+  if (!nodes) return fail(FWG_EINVAL, "nodes is NULL");
+  Plan p;
+  int rc = make_plan(desc, &p);
+  if (rc != FWG_OK) return rc;
+  if (p.nv_host.empty()) naive_tables(&p, desc->dilations);
+  *nodes = p.nv_nodes;
   return FWG_OK;
 }
 

@@ -144,6 +144,14 @@ struct ParGemm {
   int zoff;                // gate: column offset of this layer in the z rows
   float *logits;           // logits epilogue: [batch][n_steps][N]
   long long n_steps, s0;
+  // naive tree (PAR_A_TREE): row m = b * Tcur + i is the node at time tnow + toff[i]; its operands are the
+  // rows b * nprev + tsrc0[i] (time - dil) and b * nprev + tsrc1[i] (same time) of the level below, and
+  // a node before time 0 reads as zero.  When tsrc1 is set, residual epilogues read x_in from the
+  // level-below row b * nprev + tsrc1[i] instead of row m.
+  const int *toff, *tsrc0, *tsrc1;
+  int nprev;
+  long long tnow;
+  void *ztop;              // gate in tree mode: z of the node at offset 0 (i = Tcur - 1) also to ztop[b][zoff + c]
 };
 struct ParEmbed {
   int M, C, Tcur, mode;
@@ -154,6 +162,12 @@ struct ParEmbed {
   const float *embed_b;
   float *xout;             // fp32 rows (NULL when not kept)
   void *oout;              // operand rows
+  // naive tree: row j of stream b embeds the input at time tnow + toff[j], read from the stream's
+  // input history hist[b][time & hmask] (rows before time 0 are never read as operands)
+  const int *toff;
+  long long tnow;
+  const int32_t *hist;
+  int hmask;
 };
 struct ParRing {
   void *ring;              // this layer's queue [dil][brows][row_bytes]
@@ -162,7 +176,7 @@ struct ParRing {
   int Tcur, dil, brows, batch, row_bytes;
 };
 enum ParRepack { PAR_REPACK_CONV = 0, PAR_REPACK_COPY = 1 };
-enum ParAMode { PAR_A_PLAIN = 0, PAR_A_CONV = 1 };
+enum ParAMode { PAR_A_PLAIN = 0, PAR_A_CONV = 1, PAR_A_TREE = 2 };
 enum ParEMode { PAR_E_RELU = 0, PAR_E_RELU_RES = 1, PAR_E_RES_ADD = 2, PAR_E_GATE = 3, PAR_E_LOGITS = 4 };
 constexpr int kParKTileBytes = 128;  // K of every product must be a multiple of 128 bytes of operands
 hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s);
@@ -172,6 +186,10 @@ hipError_t launch_par_set_last(const int32_t *inputs, int32_t *last, int batch, 
 hipError_t launch_par_repack(const void *src, void *dst, int mode, int dtype, int N, int K, int C, int interleave,
                              long long ldd, long long doff, hipStream_t s);
 hipError_t launch_par_bias(const float *src, float *dst, int N, int interleave, int accumulate, hipStream_t s);
+// Naive generator: sample each row of logits [batch][256] with uniforms[b][s], write samples[b][s] and
+// append the sample to the stream's input history at time tnext.
+hipError_t launch_par_sample(const float *logits, const float *uniforms, int32_t *samples, int32_t *hist, int hmask,
+                             long long tnext, int batch, int n_steps, int s, hipStream_t st);
 
 // Repack modes: how W^T[k][n] is read from the caller's PyTorch layout.
 enum RepackMode {

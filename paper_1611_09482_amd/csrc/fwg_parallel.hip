@@ -25,10 +25,16 @@
 //   par_embed_kernel  x^0 rows: the 1x1 convolution of the one-hot input (a row
 //                     gather), from the forced sequence or the pending input.
 //   par_ring_kernel   the queue refresh after each layer.
+//
+// The same GEMM kernel also evaluates the naive generator's tree (paper Fig. 1): per
+// sample, every distinct (layer, time) node the output depends on, from the last
+// receptive-field inputs, with nothing cached between samples (rows gathered through
+// per-layer node tables; par_sample_kernel draws the sample and extends the input history).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "fwg_internal.h"
+#include "fwg_sample.h"
 
 namespace fwg {
 namespace par {
@@ -85,7 +91,7 @@ template <> struct Op<uint16_t> {
 __device__ __forceinline__ float sigmoid(float g) { return 1.f / (1.f + __expf(-g)); }
 
 // Row sources of the A operand.
-constexpr int A_PLAIN = PAR_A_PLAIN, A_CONV = PAR_A_CONV;
+constexpr int A_PLAIN = PAR_A_PLAIN, A_CONV = PAR_A_CONV, A_TREE = PAR_A_TREE;
 // Epilogues:
 //   E_RELU      out = opnd(relu(acc + b))
 //   E_RELU_RES  x = x_in + relu(acc + b): fp32 x and its operand copy
@@ -99,6 +105,14 @@ template <typename OT, int AM>
 __device__ __forceinline__ uint4 load_a(const ParGemm &g, int m, int k) {
   if (m >= g.M) return make_uint4(0, 0, 0, 0);
   if (AM == A_PLAIN) return *(const uint4 *)((const OT *)g.A + (long long)m * g.lda + k);
+  if (AM == A_TREE) {
+    const int b = m / g.Tcur, i = m - b * g.Tcur;
+    const long long tau = g.tnow + g.toff[i];
+    const bool tap0 = k < g.C;
+    if (tau - (tap0 ? g.dil : 0) < 0) return make_uint4(0, 0, 0, 0);  // zero padding before time 0
+    const long long row = (long long)b * g.nprev + (tap0 ? g.tsrc0[i] : g.tsrc1[i]);
+    return *(const uint4 *)((const OT *)g.A + row * g.C + (tap0 ? k : k - g.C));
+  }
   // dilated convolution: k < C is tap 0 (the state d steps back), k >= C tap 1 (the current state)
   const OT *src;
   if (k >= g.C) {
@@ -188,6 +202,10 @@ __global__ void __launch_bounds__(NT) par_gemm_kernel(ParGemm g) {
         if (m < g.M) {
           const float z = tanhf(acc[i][0][e] + bt) * sigmoid(acc[i][1][e] + bs);
           Op<OT>::put(g.oout, (long long)m * g.ldo + g.zoff + ch, z);
+          if (AM == A_TREE && g.ztop) {
+            const int b = m / g.Tcur;
+            if (m - b * g.Tcur == g.Tcur - 1) Op<OT>::put(g.ztop, (long long)b * g.ldo + g.zoff + ch, z);
+          }
         }
       }
     return;
@@ -208,7 +226,12 @@ __global__ void __launch_bounds__(NT) par_gemm_kernel(ParGemm g) {
           Op<OT>::put(g.oout, (long long)m * g.ldo + n, fmaxf(v, 0.f));
         } else if (EM == E_RELU_RES || EM == E_RES_ADD) {
           const long long at = (long long)m * g.ldo + n;
-          const float x = g.xres[at] + (EM == E_RELU_RES ? fmaxf(v, 0.f) : v);
+          long long xr = at;
+          if (g.tsrc1) {  // naive tree: x_in is the same-time node of the level below
+            const int b = m / g.Tcur;
+            xr = ((long long)b * g.nprev + g.tsrc1[m - b * g.Tcur]) * g.ldo + n;
+          }
+          const float x = g.xres[xr] + (EM == E_RELU_RES ? fmaxf(v, 0.f) : v);
           g.xout[at] = x;
           if (g.oout) Op<OT>::put(g.oout, at, x);
         } else {  // E_LOGITS
@@ -244,8 +267,14 @@ __global__ void par_embed_kernel(ParEmbed e) {
     const int b = m / e.Tcur, j = m - b * e.Tcur;
     const long long st = e.s0 + j;  // step index inside the call
     int tok;
-    if (e.mode == MODE_TEACHER) tok = e.inputs[(long long)b * e.n_steps + st];
-    else tok = st == 0 ? e.last[b] : e.inputs[(long long)b * e.n_steps + st - 1];
+    if (e.hist) {
+      const long long tau = e.tnow + e.toff[j];
+      tok = tau >= 0 ? e.hist[(long long)b * (e.hmask + 1) + (tau & e.hmask)] : 0;
+    } else if (e.mode == MODE_TEACHER) {
+      tok = e.inputs[(long long)b * e.n_steps + st];
+    } else {
+      tok = st == 0 ? e.last[b] : e.inputs[(long long)b * e.n_steps + st - 1];
+    }
     const float v = Op<OT>::get(e.embed, (long long)tok * e.C + c) + e.embed_b[c];
     if (e.xout) e.xout[i] = v;
     Op<OT>::put(e.oout, i, v);
@@ -270,6 +299,18 @@ __global__ void par_ring_kernel(ParRing r) {
     const long long m = (long long)b * r.Tcur + (tnew - r.t0);
     const uint4 v = *(const uint4 *)((const char *)r.src + m * r.row_bytes + q * 16);
     *(uint4 *)((char *)r.ring + ((long long)k * r.brows + b) * r.row_bytes + q * 16) = v;
+  }
+}
+
+// One wavefront per stream: inverse-CDF sample of its logits row, stored and appended to the history.
+__global__ void par_sample_kernel(const float *logits, const float *uniforms, int32_t *samples, int32_t *hist,
+                                  int hmask, long long tnext, int batch, int n_steps, int s) {
+  const int b = blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+  if (b >= batch) return;
+  const int k = sample_row_256(logits + (long long)b * 256, uniforms[(long long)b * n_steps + s]);
+  if ((threadIdx.x & 63) == 0) {
+    samples[(long long)b * n_steps + s] = k;
+    hist[(long long)b * (hmask + 1) + (tnext & hmask)] = k;
   }
 }
 
@@ -324,11 +365,14 @@ static int grid_for(long long total) {
 hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
   const dim3 grid((g.M + par::BM - 1) / par::BM, (g.N + par::BN - 1) / par::BN);
-  if (dtype == 1)
-    return amode == par::A_CONV ? par::launch_em<uint16_t, par::A_CONV>(g, emode, grid, s)
-                                : par::launch_em<uint16_t, par::A_PLAIN>(g, emode, grid, s);
-  return amode == par::A_CONV ? par::launch_em<float, par::A_CONV>(g, emode, grid, s)
-                              : par::launch_em<float, par::A_PLAIN>(g, emode, grid, s);
+  if (dtype == 1) {
+    if (amode == par::A_CONV) return par::launch_em<uint16_t, par::A_CONV>(g, emode, grid, s);
+    if (amode == par::A_TREE) return par::launch_em<uint16_t, par::A_TREE>(g, emode, grid, s);
+    return par::launch_em<uint16_t, par::A_PLAIN>(g, emode, grid, s);
+  }
+  if (amode == par::A_CONV) return par::launch_em<float, par::A_CONV>(g, emode, grid, s);
+  if (amode == par::A_TREE) return par::launch_em<float, par::A_TREE>(g, emode, grid, s);
+  return par::launch_em<float, par::A_PLAIN>(g, emode, grid, s);
 }
 
 hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {
@@ -341,6 +385,13 @@ hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {
 hipError_t launch_par_ring(const ParRing &r, hipStream_t s) {
   const int grid = grid_for((long long)r.batch * r.dil * (r.row_bytes / 16));
   hipLaunchKernelGGL(par::par_ring_kernel, dim3(grid), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_par_sample(const float *logits, const float *uniforms, int32_t *samples, int32_t *hist, int hmask,
+                             long long tnext, int batch, int n_steps, int s, hipStream_t st) {
+  hipLaunchKernelGGL(par::par_sample_kernel, dim3((batch + 3) / 4), dim3(256), 0, st, logits, uniforms, samples, hist,
+                     hmask, tnext, batch, n_steps, s);
   return hipGetLastError();
 }
 

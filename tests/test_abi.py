@@ -94,6 +94,8 @@ def test_null_arguments(lib):
     assert lib.fwg_generate(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_teacher_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_step_forced(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_generate_naive(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_naive_nodes(ctypes.byref(d), None) == B.FWG_EINVAL
     assert lib.fwg_destroy(None) == B.FWG_OK
     assert lib.fwg_regime(None) == b""
 
@@ -116,3 +118,29 @@ def test_workspace_checks_precede_device_work(lib):
 def test_binding_raises_on_missing_library(tmp_path):
     with pytest.raises(FileNotFoundError):
         B.load_library(str(tmp_path / "nope.so"))
+
+
+@pytest.mark.parametrize("L", [1, 2, 3, 5, 8, 12])
+def test_naive_tree_node_counts(lib, L):
+    """Section 3.1: the naive generator evaluates the tree of Fig. 1.  One block of dilations
+    1, 2, ..., 2^(L-1) has 2^L - 1 layer nodes (O(2^L); the cached method evaluates L).  Two such
+    blocks (the timing experiment's model): the top block is again a binary tree of 2^L - 1 nodes
+    whose leaves span 2^L consecutive times, and level l of the bottom block spans
+    2^(L+1) - 2^l consecutive times, (L - 1) 2^(L+1) + 2 in all."""
+    one = tuple(2 ** i for i in range(L))
+    for dil, want in [(one, 2 ** L - 1), (one + one, (2 ** L - 1) + (L - 1) * 2 ** (L + 1) + 2)]:
+        d = B.make_desc(W.GATED, W.F32, 32, dil, 1, 256, 256)
+        n = ctypes.c_int64(0)
+        assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK
+        assert n.value == want, (dil, n.value, want)
+
+
+def test_naive_nodes_equal_depth_without_branching(lib):
+    """A stack whose every dilation exceeds the sum of the dilations below it branches at every
+    level and never merges: 2^L - 1 nodes; equal dilations merge maximally (level l spans
+    L - l + 1 times)."""
+    d = B.make_desc(W.RELU, W.F32, 32, (1, 3, 9, 27), 1)
+    n = ctypes.c_int64(0)
+    assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK and n.value == 15
+    d = B.make_desc(W.RELU, W.F32, 32, (2, 2, 2, 2, 2), 1)
+    assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK and n.value == 5 + 4 + 3 + 2 + 1

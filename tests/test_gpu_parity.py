@@ -255,6 +255,41 @@ def test_online_prediction_parity(fam):
     assert np.array_equal(a, fw.teacher_forced(dev(seq)).cpu().numpy())
 
 
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "relures_c512_f32"])
+def test_naive_generation_parity(fam):
+    """The naive baseline (the tree of Fig. 1 recomputed for every sample, fwg_generate_naive) draws
+    the oracle's samples up to near-ties, continues across calls exactly, and is reset with the
+    queues."""
+    cfg = FAMILIES[fam]
+    B = 11 if cfg.channels < 512 else 5
+    n = cfg.queue_total + 40
+    w, fw, orc = build_pair(cfg, 105, B, fam=fam)
+    u = W.uniforms(19, B, n)
+    g = fw.generate_naive(dev(u)).cpu().numpy()
+    so, slg = orc.state(B).generate(u, return_logits=True)
+    tau = TAU[cfg.dtype]
+    first = []
+    for b in range(B):
+        mism = np.nonzero(g[b] != so[b])[0]
+        first.append(int(mism[0]) if mism.size else n)
+        if mism.size:
+            t = int(mism[0])
+            lo, hi = cdf_bounds(slg[b, t], so[b, t])
+            assert min(u[b, t] - lo, hi - u[b, t]) < tau, (fam, b, t)
+    log(f"{fam} [{fw.regime}]: naive generation B={B} n={n}: first divergence min {min(first)}")
+    # admissibility of every naive sample under the oracle on the naive path's own sequence
+    seq = np.concatenate([np.full((B, 1), cfg.seed_input, np.int32), g[:, :-1]], axis=1)
+    olg = orc.teacher_forced(seq)
+    for b in range(B):
+        for t in range(n):
+            lo, hi = cdf_bounds(olg[b, t], g[b, t])
+            assert lo - tau <= u[b, t] < hi + tau, (fam, b, t)
+    fw.reset()
+    a = fw.generate_naive(dev(u[:, :57].copy())).cpu().numpy()
+    c = fw.generate_naive(dev(u[:, 57:].copy())).cpu().numpy()
+    assert np.array_equal(np.concatenate([a, c], axis=1), g)
+
+
 def test_delay_line_closed_form_gpu():
     """W_e = 0, W_r = I, ReLU, zero biases, embeddings >= 0: logits[0:C] = x^0_{t - sum d} exactly,
     through every queue depth up to 512 (pop before push, slot wrap-around)."""
