@@ -11,6 +11,12 @@ and HIP events recorded on the launch stream, with inputs resident in HBM.
 number of steps instead (a seeded random input sequence, logits for every step;
 the library evaluates it time-parallel), against the oracle's teacher-forced pass.
 
+--mode naive_vs_fast runs the paper's timing experiment (Section 3.2): models of
+2 blocks of L layers (dilations 1 .. 2^(L-1) per block), L = 1 .. 12, one stream,
+generation time per sample of the cached method (fwg_generate) and of the naive
+tree recomputation (fwg_generate_naive), each averaged over --repeats calls of
+--naive-samples samples.
+
 Prints one JSON line (see the design doc for the field definitions).
 """
 from __future__ import annotations
@@ -147,6 +153,59 @@ def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
     print(json.dumps(result), flush=True)
 
 
+def naive_vs_fast(args):
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_1611_09482_amd import binding
+    stream = torch.cuda.current_stream()
+    n = args.naive_samples
+    rows = []
+    for L in range(1, args.max_blocks_layers + 1):
+        dil = tuple(2 ** i for i in range(L)) * 2
+        cfg = W.ModelConfig(W.GATED, W.F32, 32, dil, 256, 256)
+        w = W.make_weights(cfg, 1)
+        fw = binding.from_model(cfg, w, max_batch=1, stream=stream)
+        d = binding.make_desc(cfg.kind, cfg.dtype, cfg.channels, cfg.dilations, 1, cfg.skip_channels,
+                              cfg.head_channels)
+        nodes = binding.naive_nodes(d)
+        u = torch.from_numpy(W.uniforms(L, 1, n)).cuda()
+        out = torch.empty((1, n), dtype=torch.int32, device="cuda")
+        res = {}
+        for name, fn in (("fast", fw.generate), ("naive", fw.generate_naive)):
+            fn(u, out=out)  # warm-up call
+            torch.cuda.synchronize()
+            ms = []
+            for _ in range(args.repeats):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn(u, out=out)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ms.append(e0.elapsed_time(e1))
+            res[name] = float(np.mean(ms)) / n
+        R, S, H, Q = 32, 256, 256, 256
+        head = 2 * (2 * L) * R * S + 2 * S * H + 2 * H * Q
+        fast_flops = cfg.flops_per_sample()
+        naive_flops = nodes * 2 * (2 * R) * (2 * R) + (nodes - 1) * 2 * R * R + head
+        rows.append({"L": L, "layers": 2 * L, "receptive_field": cfg.receptive_field,
+                     "naive_nodes_per_sample": nodes, "fast_nodes_per_sample": 2 * L,
+                     "fast_ms_per_sample": res["fast"], "naive_ms_per_sample": res["naive"],
+                     "speedup": res["naive"] / res["fast"],
+                     "fast_tflops": fast_flops / (res["fast"] * 1e-3) / 1e12,
+                     "naive_tflops": naive_flops / (res["naive"] * 1e-3) / 1e12})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+        fw.close()
+    print(json.dumps({"metric": "generation time per sample, naive vs cached (2 blocks of L layers)",
+                      "unit": "ms/sample", "higher_is_better": False, "n_gpus": 1, "dtype": "f32",
+                      "data": "synthetic",
+                      "config": {"workload": "gated_r32_s256_2xL_b1",
+                                 "description": "gated, R=32, S=H=256, fp32, 2 blocks of L layers "
+                                                "(dilations 1..2^(L-1) per block), batch 1",
+                                 "samples_per_call": n, "repeats": args.repeats},
+                      "results": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -155,7 +214,10 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-time budget of the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["generate", "teacher_forced"], default="generate")
+    ap.add_argument("--mode", choices=["generate", "teacher_forced", "naive_vs_fast"], default="generate")
+    ap.add_argument("--naive-samples", type=int, default=50, help="samples per timed call (naive_vs_fast)")
+    ap.add_argument("--repeats", type=int, default=100, help="timed calls averaged (naive_vs_fast)")
+    ap.add_argument("--max-blocks-layers", type=int, default=12, help="largest L of the sweep (naive_vs_fast)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy (counter calibration for rocprofv3)")
     args = ap.parse_args()
@@ -183,6 +245,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": n, "launches": 3}))
+        return
+
+    if args.mode == "naive_vs_fast":
+        naive_vs_fast(args)
         return
 
     name = args.workload or W.BENCH_WORKLOAD
