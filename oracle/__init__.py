@@ -78,6 +78,7 @@ class _Model(ctypes.Structure):
         ("head", ctypes.c_void_p), ("head_b", ctypes.c_void_p),
         ("out", ctypes.c_void_p), ("out_b", ctypes.c_void_p),
         ("products", ctypes.POINTER(ctypes.c_longlong)),
+        ("w", ctypes.c_int),
     ]
 
 
@@ -123,6 +124,7 @@ class Oracle:
             m.skip, m.skip_b = table(weights.skip), table(weights.skip_b)
             m.head, m.head_b = _ptr(d(weights.head)), _ptr(d(weights.head_b))
         m.out, m.out_b = _ptr(d(weights.out)), _ptr(d(weights.out_b))
+        m.w = cfg.filter_width
         if count_products:
             m.products = ctypes.pointer(self._counter)
         self._keep = keep

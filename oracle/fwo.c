@@ -40,20 +40,28 @@ int fwo_max_threads(void) {
  * current input) and the output head.  These are the definitions in fwo.h.  */
 
 static int conv_out(const fwo_model *m) { return m->kind == FWO_GATED ? 2 * m->C : m->C; }
+/* filter width w (Section 3.1); the paper's algorithm section uses w = 2 */
+static int width(const fwo_model *m) { return m->w > 2 ? m->w : 2; }
 
-/* Layer l: r = x^{l-1}_{t-d}, x = x^{l-1}_t  ->  x_next = x^l_t; for gated also
- * adds this layer's skip contribution into s (length S).  work: >= 3*Cout doubles. */
+/* Layer l: r = the w - 1 recurrent states x^{l-1}_{t-(w-1)d}, ..., x^{l-1}_{t-d}
+ * (oldest first, C each), x = x^{l-1}_t  ->  x_next = x^l_t; for gated also adds
+ * this layer's skip contribution into s (length S).  Tap k of the [Cout][C][w]
+ * kernel multiplies x^{l-1}_{t-(w-1-k)d}, so tap w-1 multiplies x_t. */
 static void layer_apply(const fwo_model *m, int l, const double *r, const double *x, double *x_next,
                         double *s, double *work) {
-  const int C = m->C, Co = conv_out(m);
+  const int C = m->C, Co = conv_out(m), w = width(m);
   const double *W = m->conv[l];
   double *a = work;
-  double *ro = work + Co, *xo = work + Co + C;
-  for (int c = 0; c < C; ++c) { ro[c] = opnd(m, r[c]); xo[c] = opnd(m, x[c]); }
-  if (m->products) *m->products += 2; /* one W_r and one W_e application */
+  double *ro = work + Co, *xo = work + Co + (size_t)(w - 1) * C;
+  for (int i = 0; i < (w - 1) * C; ++i) ro[i] = opnd(m, r[i]);
+  for (int c = 0; c < C; ++c) xo[c] = opnd(m, x[c]);
+  if (m->products) *m->products += w; /* one application per tap: w - 1 recurrent (W_r), one current (W_e) */
   for (int o = 0; o < Co; ++o) {
     double acc = bias_at(m->conv_b[l], o);
-    for (int c = 0; c < C; ++c) acc += W[(o * C + c) * 2 + 0] * ro[c] + W[(o * C + c) * 2 + 1] * xo[c];
+    for (int c = 0; c < C; ++c) {
+      for (int k = 0; k < w - 1; ++k) acc += W[(o * C + c) * w + k] * ro[k * C + c];
+      acc += W[(o * C + c) * w + (w - 1)] * xo[c];
+    }
     a[o] = acc;
   }
   if (m->kind == FWO_RELU) {
@@ -114,13 +122,14 @@ static void embed_apply(const fwo_model *m, int in, double *x0) {
 }
 
 static size_t work_doubles(const fwo_model *m) {
-  size_t w = 3 * (size_t)conv_out(m) + 2 * (size_t)m->C + (size_t)m->S + (size_t)m->H + 16;
+  size_t w = 3 * (size_t)conv_out(m) + ((size_t)width(m) + 1) * m->C + (size_t)m->S + (size_t)m->H + 16;
   return w;
 }
 
 /* ------------------------------------------------------------------------ */
 /* Convolution queues (Section 2.1, Fig. 3): one FIFO of depth d_l per layer,
- * each element a C-vector, initially d_l zero vectors (Section 2.2).      */
+ * each element a C-vector, initially d_l zero vectors (Section 2.2).  With
+ * filter width w the queue holds the (w - 1) d_l newest states (Section 3.1). */
 typedef struct {
   double *buf;
   int depth, head, count, C;
@@ -143,6 +152,10 @@ static void fifo_pop(fifo *q, double *out) {
   memcpy(out, q->buf + (size_t)q->head * q->C, sizeof(double) * q->C);
   q->head = (q->head + 1) % q->depth;
   q->count -= 1;
+}
+/* Copy the element at position p from the front (0 = oldest) into out. */
+static void fifo_peek(const fifo *q, int p, double *out) {
+  memcpy(out, q->buf + (size_t)((q->head + p) % q->depth) * q->C, sizeof(double) * q->C);
 }
 /* Push to the back. */
 static void fifo_push(fifo *q, const double *x) {
@@ -168,7 +181,8 @@ fwo_state *fwo_state_new(const fwo_model *m, int batch, int seed_input) {
   st->last = (int *)malloc(sizeof(int) * batch);
   st->queues = (fifo *)malloc(sizeof(fifo) * (size_t)batch * m->L);
   for (int b = 0; b < batch; ++b)
-    for (int l = 0; l < m->L; ++l) fifo_init(&st->queues[(size_t)b * m->L + l], m->dil[l], m->C);
+    for (int l = 0; l < m->L; ++l)
+      fifo_init(&st->queues[(size_t)b * m->L + l], (width(m) - 1) * m->dil[l], m->C);
   fwo_state_reset(st);
   return st;
 }
@@ -193,17 +207,23 @@ long long fwo_state_t(const fwo_state *st) { return st->t; }
 
 /* One step of the generation model for one stream (Section 2.2):
  * pop phase, computation of the output and the new recurrent states, push phase.
- * popped: [L][C]; states: [L+1][C] (states[l] = x^l_t); s: [S]. */
+ * popped: [L][(w-1) C]; states: [L+1][C] (states[l] = x^l_t); s: [S]. */
 static void model_step(const fwo_model *m, fifo *q, int in, double *logits, double *popped,
                        double *states, double *s, double *work) {
-  const int L = m->L, C = m->C;
-  /* pop phase: the oldest cached state of every queue */
-  for (int l = 0; l < L; ++l) fifo_pop(&q[l], popped + (size_t)l * C);
+  const int L = m->L, C = m->C, w = width(m);
+  /* pop phase: the oldest cached state of every queue (x^{l-1}_{t-(w-1)d}); with w > 2
+   * also the states d, 2d, ... behind it (x^{l-1}_{t-(w-2)d}, ..., x^{l-1}_{t-d}) */
+  for (int l = 0; l < L; ++l) {
+    double *r = popped + (size_t)l * (w - 1) * C;
+    for (int k = 1; k < w - 1; ++k) fifo_peek(&q[l], k * m->dil[l], r + (size_t)k * C);
+    fifo_pop(&q[l], r);
+  }
   /* current input h^0_e and the new recurrent states */
   embed_apply(m, in, states);
   if (m->kind == FWO_GATED) memset(s, 0, sizeof(double) * m->S);
   for (int l = 0; l < L; ++l)
-    layer_apply(m, l, popped + (size_t)l * C, states + (size_t)l * C, states + (size_t)(l + 1) * C, s, work);
+    layer_apply(m, l, popped + (size_t)l * (w - 1) * C, states + (size_t)l * C, states + (size_t)(l + 1) * C, s,
+                work);
   head_apply(m, states + (size_t)L * C, s, logits, work);
   /* push phase: the queue feeding layer l receives x^{l-1}_t */
   for (int l = 0; l < L; ++l) fifo_push(&q[l], states + (size_t)l * C);
@@ -237,7 +257,7 @@ typedef struct {
 } scratch;
 
 static void scratch_init(const fwo_model *m, scratch *w) {
-  w->popped = (double *)malloc(sizeof(double) * (size_t)m->L * m->C + 8);
+  w->popped = (double *)malloc(sizeof(double) * (size_t)m->L * (width(m) - 1) * m->C + 8);
   w->states = (double *)malloc(sizeof(double) * (size_t)(m->L + 1) * m->C + 8);
   w->s = (double *)malloc(sizeof(double) * ((size_t)m->S + 1));
   w->work = (double *)malloc(sizeof(double) * work_doubles(m));
@@ -306,7 +326,7 @@ int fwo_teacher_forced(const fwo_model *m, int B, int T, const int *inputs, doub
     scratch w;
     scratch_init(m, &w);
     fifo *q = (fifo *)malloc(sizeof(fifo) * L);
-    for (int l = 0; l < L; ++l) fifo_init(&q[l], m->dil[l], m->C);
+    for (int l = 0; l < L; ++l) fifo_init(&q[l], (width(m) - 1) * m->dil[l], m->C);
     for (int t = 0; t < T; ++t)
       model_step(m, q, inputs[(size_t)b * T + t], logits + ((size_t)b * T + t) * Q, w.popped, w.states,
                  w.s, w.work);
@@ -319,12 +339,13 @@ int fwo_teacher_forced(const fwo_model *m, int B, int T, const int *inputs, doub
 
 /* ------------------------------------------------------------------------ */
 /* Parallel form: layer l evaluated for all t from layer l-1's full sequence,
- * with x^{l-1}_{t-d} = 0 for t < d.                                         */
+ * with x^{l-1}_{t-kd} = 0 for t < kd.                                       */
 int fwo_parallel(const fwo_model *m, int B, int T, const int *inputs, double *logits) {
   if (!m || B <= 0 || T < 0 || (T > 0 && (!inputs || !logits))) return -1;
-  const int L = m->L, C = m->C, Q = m->Q, S = m->S;
+  const int L = m->L, C = m->C, Q = m->Q, S = m->S, w = width(m);
 #pragma omp parallel for schedule(dynamic, 1) if (!m->products && B > 1)
   for (int b = 0; b < B; ++b) {
+    double *rtaps = (double *)malloc(sizeof(double) * (size_t)(w - 1) * C + 8);
     double *prev = (double *)malloc(sizeof(double) * (size_t)T * C + 8);
     double *next = (double *)malloc(sizeof(double) * (size_t)T * C + 8);
     double *ssum = (double *)calloc((size_t)T * (S > 0 ? S : 1), sizeof(double));
@@ -334,14 +355,17 @@ int fwo_parallel(const fwo_model *m, int B, int T, const int *inputs, double *lo
     for (int l = 0; l < L; ++l) {
       const int d = m->dil[l];
       for (int t = 0; t < T; ++t) {
-        const double *r = t - d >= 0 ? prev + (size_t)(t - d) * C : zero;
-        layer_apply(m, l, r, prev + (size_t)t * C, next + (size_t)t * C, ssum + (size_t)t * S, work);
+        for (int k = 0; k < w - 1; ++k) {
+          const int tau = t - (w - 1 - k) * d;
+          memcpy(rtaps + (size_t)k * C, tau >= 0 ? prev + (size_t)tau * C : zero, sizeof(double) * C);
+        }
+        layer_apply(m, l, rtaps, prev + (size_t)t * C, next + (size_t)t * C, ssum + (size_t)t * S, work);
       }
       double *tmp = prev; prev = next; next = tmp;
     }
     for (int t = 0; t < T; ++t)
       head_apply(m, prev + (size_t)t * C, ssum + (size_t)t * S, logits + ((size_t)b * T + t) * Q, work);
-    free(prev); free(next); free(ssum); free(zero); free(work);
+    free(rtaps); free(prev); free(next); free(ssum); free(zero); free(work);
   }
   return 0;
 }
@@ -352,11 +376,12 @@ static void naive_node(const fwo_model *m, const int *inputs, int l, int tau, do
   const int C = m->C;
   if (tau < 0) { memset(out, 0, sizeof(double) * C); return; } /* zero queues = zero padding */
   if (l == 0) { embed_apply(m, inputs[tau], out); return; }
-  double *r = (double *)malloc(sizeof(double) * C);
+  const int w = width(m);
+  double *r = (double *)malloc(sizeof(double) * (size_t)(w - 1) * C);
   double *x = (double *)malloc(sizeof(double) * C);
   double *s = (double *)calloc(m->S > 0 ? m->S : 1, sizeof(double));
   double *work = (double *)malloc(sizeof(double) * work_doubles(m));
-  naive_node(m, inputs, l - 1, tau - m->dil[l - 1], r);
+  for (int k = 0; k < w - 1; ++k) naive_node(m, inputs, l - 1, tau - (w - 1 - k) * m->dil[l - 1], r + (size_t)k * C);
   naive_node(m, inputs, l - 1, tau, x);
   layer_apply(m, l - 1, r, x, out, s, work); /* skip output of interior nodes is discarded */
   free(r); free(x); free(s); free(work);
@@ -373,11 +398,12 @@ int fwo_naive(const fwo_model *m, const int *inputs, int t, double *logits) {
   } else {
     /* the skip sum needs z^l_t of every layer: walk the spine h^0_t .. h^L_t,
      * each recurrent operand recomputed from scratch by the tree */
+    const int w = width(m);
     double *x = (double *)malloc(sizeof(double) * C);
-    double *r = (double *)malloc(sizeof(double) * C);
+    double *r = (double *)malloc(sizeof(double) * (size_t)(w - 1) * C);
     naive_node(m, inputs, 0, t, x);
     for (int l = 0; l < m->L; ++l) {
-      naive_node(m, inputs, l, t - m->dil[l], r);
+      for (int k = 0; k < w - 1; ++k) naive_node(m, inputs, l, t - (w - 1 - k) * m->dil[l], r + (size_t)k * C);
       layer_apply(m, l, r, x, top, s, work);
       memcpy(x, top, sizeof(double) * C);
     }

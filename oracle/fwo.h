@@ -44,8 +44,13 @@
  * layer's input) to bf16 with round-to-nearest-even; every accumulation,
  * bias, nonlinearity, residual stream and skip sum stays in double.
  *
+ * Filter width w > 2 (Section 3.1): the dilated product takes w taps,
+ * x^{l-1}_{t-(w-1)d}, ..., x^{l-1}_{t-d} (the recurrent states) and x^{l-1}_t, and
+ * each queue holds (w - 1) d_l states.
+ *
  * Weight layouts (row-major, PyTorch conventions):
- *   embed [C][Q], conv[l] [Cout][C][2] (tap 0 = recurrent x_{t-d}, tap 1 = x_t),
+ *   embed [C][Q], conv[l] [Cout][C][w] (tap k multiplies x_{t-(w-1-k)d}; w = 2: tap 0 =
+ *   recurrent x_{t-d}, tap 1 = x_t),
  *   res[l] [R][R], skip[l] [S][R], head [H][S], out [Q][C or H].
  *   A NULL bias means zeros.
  */
@@ -68,7 +73,8 @@ typedef struct {
   const double *const *skip, *const *skip_b;
   const double *head, *head_b;
   const double *out, *out_b;
-  long long *products; /* optional: counts applications of W_r and W_e */
+  long long *products; /* optional: counts applications of W_r and W_e (one per tap) */
+  int w;               /* filter width (Section 3.1); 0 means 2 */
 } fwo_model;
 
 typedef struct fwo_state fwo_state;

@@ -136,7 +136,8 @@ def _torch_reference(w, inputs):
     s = None
     for l, d in enumerate(cfg.dilations):
         wt = torch.as_tensor(w.conv[l], dtype=f64)
-        a = torch.nn.functional.conv1d(torch.nn.functional.pad(q(h), (d, 0)), wt,
+        pad = (cfg.filter_width - 1) * d  # causal: every tap at or before t
+        a = torch.nn.functional.conv1d(torch.nn.functional.pad(q(h), (pad, 0)), wt,
                                        torch.as_tensor(w.conv_b[l], dtype=f64), dilation=d)
         if cfg.kind == W.RELU:
             h = torch.relu(a)
@@ -369,6 +370,70 @@ def test_online_prediction_continues_the_history(oracle_lib, dtype):
     lo = st.step_forced(obs)
     np.testing.assert_allclose(lo, _torch_reference(
         w, np.concatenate([np.full((B, 1), cfg.seed_input), obs[:, :-1]], axis=1)), rtol=1e-10, atol=1e-10)
+
+
+# ---------------------------------------------------------------- P11 filter width w > 2
+@pytest.mark.parametrize("kind", KINDS)
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+@pytest.mark.parametrize("fw", [3, 4])
+def test_width_cached_equals_parallel_naive_and_torch(oracle_lib, kind, dtype, fw):
+    """Section 3.1, general filter width: with queues of (w - 1) d_l states, the cached form equals
+    the full-sequence dilated convolution of kernel size w (torch conv1d in float64 and the
+    oracle's parallel form) and the uncached tree in which every node has w children."""
+    dil = (1, 3, 2, 5, 1)
+    cfg = W.tiny_model(kind, dtype, channels=4, dilations=dil, skip=6, head=5, filter_width=fw)
+    w = W.make_weights(cfg, 50 + kind + fw, bias_scale=0.3)
+    o = oracle_lib.Oracle(w)
+    x = W.sequences(22, 2, 70)
+    fast = o.teacher_forced(x)
+    np.testing.assert_allclose(fast, o.parallel(x), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(fast, _torch_reference(w, x), rtol=1e-10, atol=1e-10)
+    for t in (0, 5, 23, 40, 69):
+        np.testing.assert_allclose(fast[1, t], o.naive(x[1], t), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("fw,r,L", [(3, 3, 3), (3, 4, 4), (4, 4, 3)])
+def test_width_product_counts(oracle_lib, fw, r, L):
+    """Section 3.1 with filter width w and dilations r^l (r >= w): the cached method applies w
+    tap products per layer and sample (O(wL)); the naive tree has (w^L - 1) / (w - 1) nodes of w
+    products each (O(w^L)); the queues hold (w - 1)(r^L - 1)/(r - 1) states (O((w - 1) r^L))."""
+    dil = tuple(r ** i for i in range(L))
+    cfg = W.ModelConfig(W.RELU, W.F32, 2, dil, n_classes=8, filter_width=fw)
+    assert cfg.queue_total == (fw - 1) * (r ** L - 1) // (r - 1)
+    w = W.make_weights(cfg, 2)
+    o = oracle_lib.Oracle(w, count_products=True)
+    T = cfg.receptive_field + 2
+    x = W.sequences(1, 1, T, n_classes=8)
+    o.reset_products()
+    o.teacher_forced(x)
+    assert o.products == fw * L * T
+    o.reset_products()
+    o.naive(x[0], T - 1)
+    assert o.products == fw * (fw ** L - 1) // (fw - 1)
+
+
+@pytest.mark.parametrize("fw,dilations", [(3, (1, 2, 4)), (4, (3, 1, 5)), (3, (64,))])
+def test_width_delay_line_closed_form(oracle_lib, fw, dilations):
+    """Only the oldest tap carries the identity (the others and W_e zero): every layer is a pure
+    delay of (w - 1) d_l, so x^L_t = x^0_{t - (w - 1) sum d}.  Pins the queue depth (w - 1) d_l and
+    the tap order for w > 2."""
+    C, Q = 3, 16
+    cfg = W.ModelConfig(W.RELU, W.F32, C, tuple(dilations), n_classes=Q, filter_width=fw)
+    w = W.make_weights(cfg, 0)
+    w.embed[:] = np.array([[q + 10 * c for q in range(Q)] for c in range(C)], np.float32)
+    for l in range(cfg.n_layers):
+        w.conv[l][:] = 0
+        w.conv[l][np.arange(C), np.arange(C), 0] = 1.0
+    w.out[:] = 0
+    w.out[np.arange(C), np.arange(C)] = 1.0
+    D = (fw - 1) * sum(dilations)
+    T = D + 30
+    x = W.sequences(3, 2, T, n_classes=Q)
+    lg = oracle_lib.Oracle(w).teacher_forced(x)
+    for b in range(2):
+        for t in range(T):
+            want = [w.embed[c, x[b, t - D]] if t >= D else 0.0 for c in range(C)]
+            assert list(lg[b, t, :C]) == want, (b, t)
 
 
 # ---------------------------------------------------------------- P10 bf16

@@ -41,6 +41,7 @@ class ModelConfig:
     head_channels: int = 0        # H (gated only)
     n_classes: int = 256
     seed_input: int = 128         # first input after a reset
+    filter_width: int = 2         # w: taps x_{t-(w-1)d}, ..., x_{t-d}, x_t (Section 3.1)
 
     @property
     def n_layers(self) -> int:
@@ -56,8 +57,8 @@ class ModelConfig:
 
     @property
     def queue_total(self) -> int:
-        """Sum of queue depths: number of cached states per channel and stream."""
-        return int(sum(self.dilations))
+        """Sum of queue depths ((w - 1) d_l per layer): cached states per channel and stream."""
+        return int((self.filter_width - 1) * sum(self.dilations))
 
     @property
     def receptive_field(self) -> int:
@@ -67,7 +68,7 @@ class ModelConfig:
         C, Q = self.channels, self.n_classes
         n = C * Q + C  # embedding + bias
         for _ in self.dilations:
-            n += self.conv_out * C * 2 + self.conv_out
+            n += self.conv_out * C * self.filter_width + self.conv_out
             if self.kind == GATED:
                 n += C * C + C + self.skip_channels * C + self.skip_channels
         if self.kind == GATED:
@@ -78,7 +79,7 @@ class ModelConfig:
     def macs_per_sample(self) -> int:
         """Multiply-accumulates of one generated sample (embedding gather excluded)."""
         C = self.channels
-        per_layer = self.conv_out * 2 * C
+        per_layer = self.conv_out * self.filter_width * C
         if self.kind == GATED:
             per_layer += C * C + self.skip_channels * C
         n = per_layer * self.n_layers
@@ -212,7 +213,7 @@ def make_weights(cfg: ModelConfig, seed: int, bias_scale: float = 0.0,
     embed = draw((C, Q), Q)
     conv, res, skip = [], [], []
     for _ in range(cfg.n_layers):
-        conv.append(draw((cfg.conv_out, C, 2), 2 * C))
+        conv.append(draw((cfg.conv_out, C, cfg.filter_width), cfg.filter_width * C))
         if cfg.kind == GATED:
             res.append(draw((C, C), C))
             skip.append(draw((S, C), C))
@@ -284,8 +285,8 @@ def sequences(seed: int, batch: int, length: int, n_classes: int = 256, stream0:
 
 def tiny_model(kind: int, dtype: int = F32, channels: int = 4,
                dilations: Sequence[int] = (1, 2, 4), skip: int = 8, head: int = 8,
-               n_classes: int = 256, seed_input: int = 128) -> ModelConfig:
+               n_classes: int = 256, seed_input: int = 128, filter_width: int = 2) -> ModelConfig:
     return ModelConfig(kind, dtype, channels, tuple(dilations),
                        skip_channels=skip if kind == GATED else 0,
                        head_channels=head if kind == GATED else 0,
-                       n_classes=n_classes, seed_input=seed_input)
+                       n_classes=n_classes, seed_input=seed_input, filter_width=filter_width)
