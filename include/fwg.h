@@ -92,6 +92,9 @@ typedef struct {
   int32_t max_batch;      /* largest batch of independent streams, >= 1 */
   int32_t seed_input;     /* input class fed at the first step after a reset, in [0, Q) */
   const int32_t *dilations; /* HOST array [n_layers], each >= 1: layer l reads x^{l-1}_{t-d_l} */
+  int32_t filter_width;   /* w taps per dilated product, x^{l-1}_{t-(w-1)d_l} .. x^{l-1}_t
+                             (Section 3.1); 0 means 2, the width of Sections 2.1-2.2.  Each
+                             queue then holds (w-1) d_l states. */
 } fwg_desc;
 
 /* Weights: DEVICE pointers to row-major arrays in PyTorch layouts; the
@@ -99,8 +102,9 @@ typedef struct {
  * the descriptor's dtype (bf16 = 16-bit bf16 bit patterns); biases are always
  * float32.  A NULL bias (or a NULL bias table) means zeros.
  *   embed   [C][Q]           1x1 convolution over the one-hot input
- *   conv[l] [Cout][C][2]     Cout = C (relu kinds) or 2R (gated);
- *                            tap 0 multiplies x_{t-d} (W_r), tap 1 multiplies x_t (W_e)
+ *   conv[l] [Cout][C][w]     Cout = C (relu kinds) or 2R (gated); tap k multiplies
+ *                            x_{t-(w-1-k)d}: for w = 2 tap 0 multiplies x_{t-d} (W_r),
+ *                            tap 1 multiplies x_t (W_e)
  *   res[l]  [R][R]           gated only
  *   skip[l] [S][R]           gated only
  *   head    [H][S]           gated only

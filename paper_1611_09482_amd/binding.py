@@ -30,7 +30,8 @@ class fwg_desc(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n_classes", ctypes.c_int32),
                 ("channels", ctypes.c_int32), ("skip_channels", ctypes.c_int32),
                 ("head_channels", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("max_batch", ctypes.c_int32),
-                ("seed_input", ctypes.c_int32), ("dilations", ctypes.POINTER(ctypes.c_int32))]
+                ("seed_input", ctypes.c_int32), ("dilations", ctypes.POINTER(ctypes.c_int32)),
+                ("filter_width", ctypes.c_int32)]
 
 
 class fwg_weights(ctypes.Structure):
@@ -82,10 +83,11 @@ def _check(rc: int):
 
 
 def make_desc(kind: int, dtype: int, channels: int, dilations: Sequence[int], max_batch: int,
-              skip_channels: int = 0, head_channels: int = 0, n_classes: int = 256, seed_input: int = 128):
+              skip_channels: int = 0, head_channels: int = 0, n_classes: int = 256, seed_input: int = 128,
+              filter_width: int = 2):
     dil = (ctypes.c_int32 * max(1, len(dilations)))(*[int(d) for d in dilations])
     d = fwg_desc(kind, dtype, n_classes, channels, skip_channels, head_channels, len(dilations), max_batch,
-                 seed_input, ctypes.cast(dil, ctypes.POINTER(ctypes.c_int32)))
+                 seed_input, ctypes.cast(dil, ctypes.POINTER(ctypes.c_int32)), filter_width)
     d._keep = dil
     return d
 
@@ -112,14 +114,14 @@ class FastWavenet:
 
     def __init__(self, kind: int, dtype: int, channels: int, dilations: Sequence[int], max_batch: int,
                  weights, skip_channels: int = 0, head_channels: int = 0, n_classes: int = 256,
-                 seed_input: int = 128, stream=None):
+                 seed_input: int = 128, stream=None, filter_width: int = 2):
         import torch
         self._torch = torch
         self.lib = load_library()
         self.n_classes = n_classes
         self.max_batch = max_batch
         self.desc = make_desc(kind, dtype, channels, dilations, max_batch, skip_channels, head_channels,
-                              n_classes, seed_input)
+                              n_classes, seed_input, filter_width)
         self.ws_bytes = workspace_size(self.desc)
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
@@ -254,4 +256,5 @@ def from_model(cfg, weights, max_batch: int, stream=None) -> FastWavenet:
     dw = upload_weights(weights, cfg.dtype)
     return FastWavenet(cfg.kind, cfg.dtype, cfg.channels, cfg.dilations, max_batch, dw,
                        skip_channels=cfg.skip_channels, head_channels=cfg.head_channels,
-                       n_classes=cfg.n_classes, seed_input=cfg.seed_input, stream=stream)
+                       n_classes=cfg.n_classes, seed_input=cfg.seed_input, stream=stream,
+                       filter_width=getattr(cfg, "filter_width", 2))

@@ -40,6 +40,7 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
 struct Plan {
   int kind, dtype, Q, C, S, H, L, bmax, seed_input, Co, es, rpw;
+  int w;                  // filter width: taps per dilated product
   int regime;
   int brows;              // queue rows per slot (max_batch, padded to whole blocks for the MFMA family)
   size_t off_frags, off_embT, off_bias, off_ptrtab;
@@ -59,7 +60,7 @@ struct Plan {
   // naive generator: the nodes of the output's dependency tree (Fig. 1), level 0 = inputs
   bool nv_ok;
   std::vector<int> nv_n;         // [L + 1] distinct nodes per level
-  std::vector<size_t> nv_tab;    // [L + 1] int offset of the level's tables (toff; then tsrc0, tsrc1 for l >= 1)
+  std::vector<size_t> nv_tab;    // [L + 1] int offset of the level's tables (toff; then w tap-source rows for l >= 1)
   std::vector<int32_t> nv_host;  // the tables, uploaded at create
   long long nv_nodes;            // layer nodes per sample: sum of nv_n[1..L]
   int nv_hc;                     // input-history capacity per stream (power of two >= receptive field)
@@ -67,15 +68,17 @@ struct Plan {
 };
 
 // Node sets of the tree of Fig. 1 for the output at offset 0: level L holds {0}; level l - 1 holds the
-// level-l offsets and the same offsets minus d_l (each distinct offset once).  Fills nv_n, nv_tab,
-// nv_host and nv_nodes.
+// level-l offsets minus j d_l for j = 0 .. w - 1 (each distinct offset once).  Tables per level l >= 1:
+// the offsets, then for every tap k the index in level l - 1 of offset - (w - 1 - k) d_l.  Fills nv_n,
+// nv_tab, nv_host and nv_nodes.
 void naive_tables(Plan *p, const int32_t *dil) {
-  const int L = p->L;
+  const int L = p->L, w = p->w;
   std::vector<std::vector<int>> P(L + 1);
   P[L] = {0};
   for (int l = L; l >= 1; --l) {
     std::vector<int> v = P[l];
-    for (int o : P[l]) v.push_back(o - dil[l - 1]);
+    for (int j = 1; j < w; ++j)
+      for (int o : P[l]) v.push_back(o - j * dil[l - 1]);
     std::sort(v.begin(), v.end());
     v.erase(std::unique(v.begin(), v.end()), v.end());
     P[l - 1] = v;
@@ -92,8 +95,8 @@ void naive_tables(Plan *p, const int32_t *dil) {
     p->nv_nodes += p->nv_n[l];
     const std::vector<int> &below = P[l - 1];
     auto index_of = [&](int o) { return (int32_t)(std::lower_bound(below.begin(), below.end(), o) - below.begin()); };
-    for (int o : P[l]) p->nv_host.push_back(index_of(o - dil[l - 1]));
-    for (int o : P[l]) p->nv_host.push_back(index_of(o));
+    for (int k = 0; k < w; ++k)
+      for (int o : P[l]) p->nv_host.push_back(index_of(o - (w - 1 - k) * dil[l - 1]));
   }
 }
 
@@ -125,6 +128,9 @@ int make_plan(const fwg_desc *d, Plan *p) {
     dsum += d->dilations[l];
   }
   if (d->n_classes != 256) return fail(FWG_EUNSUPPORTED, "n_classes must be 256 (got %d)", d->n_classes);
+  const int w = d->filter_width == 0 ? 2 : d->filter_width;
+  if (w < 2) return fail(FWG_EINVAL, "filter_width must be >= 2 (or 0 for 2), got %d", d->filter_width);
+  if (w > 16) return fail(FWG_EUNSUPPORTED, "filter_width > 16");
 
   p->kind = d->kind;
   p->dtype = d->dtype;
@@ -137,10 +143,12 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->seed_input = d->seed_input;
   p->Co = d->kind == FWG_GATED ? 2 * p->C : p->C;
   p->es = d->dtype == FWG_BF16 ? 2 : 4;
+  p->w = w;
 
   // shapes the K-blocked products support
   const int kb = valu_kb_elems(p->dtype);
-  bool ok = kblock_ok(2 * p->C, p->Co, kb) && kblock_ok(p->kind == FWG_GATED ? p->H : p->C, p->Q, kb);
+  bool ok = p->C % kb == 0 && kblock_ok(w * p->C, p->Co, kb) &&
+            kblock_ok(p->kind == FWG_GATED ? p->H : p->C, p->Q, kb);
   if (p->kind == FWG_GATED)
     ok = ok && kblock_ok(p->C, p->C, kb) && kblock_ok(p->C, p->S, kb) && kblock_ok(p->S, p->H, kb);
   if (!ok)
@@ -153,7 +161,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   int rpw = 8;
   while (rpw > 1 && rpw > p->bmax) rpw >>= 1;
   for (;; rpw >>= 1) {
-    const ValuLds lay = valu_lds_layout(p->kind, p->C, p->S, p->H, p->Q, p->L, rpw);
+    const ValuLds lay = valu_lds_layout(p->kind, p->C, p->S, p->H, p->Q, p->L, rpw, w);
     p->lds_bytes = (size_t)lay.total_floats * 4;
     if (p->lds_bytes <= 160 * 1024 || rpw == 1) break;
   }
@@ -163,7 +171,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512
   p->regime = REGIME_VALU;
   const char *force = getenv("FWG_REGIME");
-  const bool mfma_shape = p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR && p->S == kMfS &&
+  const bool mfma_shape = w == 2 && p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR && p->S == kMfS &&
                           p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
                           mfma_lds_bytes(p->L) <= 160 * 1024;
   if (mfma_shape && !(force && strcmp(force, "valu") == 0)) p->regime = REGIME_MFMA;
@@ -185,7 +193,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_conv.resize(p->L); p->off_conv_b.resize(p->L);
   p->off_res.assign(p->L, 0); p->off_res_b.assign(p->L, 0); p->off_skip.assign(p->L, 0); p->off_skip_b.assign(p->L, 0);
   for (int l = 0; l < p->L; ++l) {
-    p->off_conv[l] = take((size_t)p->Co * 2 * p->C * p->es);
+    p->off_conv[l] = take((size_t)p->Co * w * p->C * p->es);
     p->off_conv_b[l] = take(sizeof(float) * p->Co);
     if (p->kind == FWG_GATED) {
       p->off_res[l] = take((size_t)p->C * p->C * p->es);
@@ -203,7 +211,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   long long acc = 0;
   for (int l = 0; l < p->L; ++l) {
     p->ring_off[l] = acc;
-    acc += (long long)d->dilations[l] * p->brows * p->C;
+    acc += (long long)(w - 1) * d->dilations[l] * p->brows * p->C;
   }
   p->queue_elems = acc;
   (void)dsum;
@@ -239,7 +247,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
     const size_t R = (size_t)p->par_tc * p->brows;
     p->off_pconv.assign(p->L, 0); p->off_pconv_b.assign(p->L, 0); p->off_pres.assign(p->L, 0);
     for (int l = 0; l < p->L; ++l) {
-      p->off_pconv[l] = take((size_t)p->Co * 2 * p->C * p->es);
+      p->off_pconv[l] = take((size_t)p->Co * w * p->C * p->es);
       p->off_pconv_b[l] = take(sizeof(float) * p->Co);
       if (gated) p->off_pres[l] = take((size_t)p->C * p->C * p->es);
     }
@@ -263,7 +271,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
     if ((long long)p->bmax * p->nv_n[0] <= (long long)p->par_tc * p->brows) {
       p->nv_ok = true;
       p->nv_hc = 1;
-      while (p->nv_hc < dsum + 1) p->nv_hc <<= 1;
+      while (p->nv_hc < (long long)(w - 1) * dsum + 1) p->nv_hc <<= 1;
       p->off_nv = take(sizeof(int32_t) * p->nv_host.size());
       p->off_hist = take(sizeof(int32_t) * (size_t)p->bmax * p->nv_hc);
       p->off_ztop = p->kind == FWG_GATED ? take((size_t)p->bmax * p->L * p->C * p->es) : 0;
@@ -327,6 +335,7 @@ StepArgs base_args(const fwg_handle *h) {
   a.H = p.H;
   a.Q = p.Q;
   a.L = p.L;
+  a.w = p.w;
   return a;
 }
 
@@ -360,9 +369,10 @@ int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const 
     const int32_t *lt = tab + p.nv_tab[l + 1];
     ParGemm g;
     memset(&g, 0, sizeof(g));
-    g.M = batch * n; g.N = p.Co; g.K = 2 * C; g.Tcur = n; g.C = C; g.dil = h->dil[l];
+    g.M = batch * n; g.N = p.Co; g.K = p.w * C; g.Tcur = n; g.C = C; g.dil = h->dil[l]; g.w = p.w;
     g.A = pxb[cur]; g.lda = C;
-    g.toff = lt; g.tsrc0 = lt + n; g.tsrc1 = lt + 2 * n; g.nprev = nprev; g.tnow = t;
+    g.toff = lt; g.tsrc = lt + n; g.nprev = nprev; g.tnow = t;
+    if (p.kind == FWG_RELU_RESIDUAL) g.tsrc1 = lt + (size_t)p.w * n;  // x_in: the same-time node (tap w - 1)
     g.W = ws + p.off_pconv[l];
     g.bias = (const float *)(ws + p.off_pconv_b[l]);
     int em;
@@ -382,7 +392,7 @@ int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const 
       r.W = ws + p.off_pres[l];
       r.bias = (const float *)(ws + p.off_res_b[l]);
       r.xres = px[cur]; r.xout = px[nxt]; r.oout = opnd_copy ? pxb[nxt] : nullptr; r.ldo = C;
-      r.tsrc1 = lt + 2 * n; r.nprev = nprev;
+      r.tsrc1 = lt + (size_t)p.w * n; r.nprev = nprev;
       HIP_TRY(launch_par_gemm(r, p.dtype, PAR_A_PLAIN, PAR_E_RES_ADD, st));
     }
     cur = nxt;
@@ -462,10 +472,11 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
       const int nxt = cur ^ 1;
       ParGemm g;
       memset(&g, 0, sizeof(g));
-      g.M = M; g.N = p.Co; g.K = 2 * C;
+      g.M = M; g.N = p.Co; g.K = p.w * C;
       g.A = pxb[cur]; g.lda = C;
       g.ring = ring + (size_t)p.ring_off[l] * es;
       g.t0 = t0; g.dil = h->dil[l]; g.brows = p.brows; g.Tcur = Tcur; g.C = C;
+      g.w = p.w; g.depth = (p.w - 1) * h->dil[l];
       g.W = ws + p.off_pconv[l];
       g.bias = (const float *)(ws + p.off_pconv_b[l]);
       int em;
@@ -490,7 +501,8 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
       ParRing q;
       memset(&q, 0, sizeof(q));
       q.ring = ring + (size_t)p.ring_off[l] * es; q.src = pxb[cur];
-      q.t0 = t0; q.Tcur = Tcur; q.dil = h->dil[l]; q.brows = p.brows; q.batch = batch; q.row_bytes = C * es;
+      q.t0 = t0; q.Tcur = Tcur; q.depth = (p.w - 1) * h->dil[l]; q.brows = p.brows; q.batch = batch;
+      q.row_bytes = C * es;
       HIP_TRY(launch_par_ring(q, s));
       cur = nxt;
     }
@@ -585,7 +597,7 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_copy_bias(w->embed_b, (float *)(ws + p.off_embed_b), C, s));
   std::vector<LayerDev> table(p.L);
   for (int l = 0; l < p.L; ++l) {
-    TRY_OR_FREE(launch_repack(w->conv[l], ws + p.off_conv[l], REPACK_CONV, dt, 2 * C, p.Co, C, s));
+    TRY_OR_FREE(launch_repack(w->conv[l], ws + p.off_conv[l], REPACK_CONV, dt, p.w * C, p.Co, C, s));
     TRY_OR_FREE(launch_copy_bias(w->conv_b ? w->conv_b[l] : nullptr, (float *)(ws + p.off_conv_b[l]), p.Co, s));
     LayerDev &ld = table[l];
     memset(&ld, 0, sizeof(ld));
@@ -603,6 +615,7 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     }
     ld.ring_off = p.ring_off[l];
     ld.dil = h->dil[l];
+    ld.depth = (p.w - 1) * h->dil[l];
   }
   if (p.kind == FWG_GATED) {
     TRY_OR_FREE(launch_repack(w->head, ws + p.off_head, REPACK_LINEAR, dt, p.S, p.H, C, s));
@@ -618,7 +631,8 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   if (p.par_ok) {
     const int il = p.kind == FWG_GATED;  // gated conv rows interleave tanh and sigmoid channel groups
     for (int l = 0; l < p.L; ++l) {
-      TRY_OR_FREE(launch_par_repack(w->conv[l], ws + p.off_pconv[l], PAR_REPACK_CONV, dt, p.Co, 2 * C, C, il, 0, 0, s));
+      TRY_OR_FREE(launch_par_repack(w->conv[l], ws + p.off_pconv[l], PAR_REPACK_CONV, dt, p.Co, p.w * C, C, il, 0, 0,
+                                    s));
       TRY_OR_FREE(launch_par_bias(w->conv_b ? w->conv_b[l] : nullptr, (float *)(ws + p.off_pconv_b[l]), p.Co, il, 0, s));
       if (p.kind == FWG_GATED) {
         TRY_OR_FREE(launch_par_repack(w->res[l], ws + p.off_pres[l], PAR_REPACK_COPY, dt, C, C, C, 0, C, 0, s));

@@ -19,8 +19,8 @@ struct LayerDev {
   const void *skip;     // gated: packed [S][R]
   const float *skip_b;  // [S]
   long long ring_off;   // element offset of this layer's queue inside a queue region
-  int dil;              // queue depth = dilation
-  int pad_;
+  int dil;              // dilation d
+  int depth;            // queue slots: (w - 1) d (= d for width 2)
 };
 
 // Arguments of one step-kernel launch (passed by value).
@@ -41,6 +41,7 @@ struct StepArgs {
   long long t0;            // time index of the first step of this launch
   int n_steps, batch, bmax;
   int kind, dtype, C, S, H, Q, L;
+  int w;                   // filter width (taps per dilated product)
   int mode;                // StepMode
   // MFMA family only
   const void *mf_frags;    // per-wave packed weight fragment streams
@@ -80,14 +81,14 @@ struct ValuLds {
   int xf, xo, vo, ao, zo, so, ho, h2, lg, partA, partB, slots, ins, total_floats;
 };
 __host__ __device__ inline int valu_part_cols(int N) { return N >= 256 ? N : 256; }
-__host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H, int Q, int L, int rpw) {
+__host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H, int Q, int L, int rpw, int w) {
   ValuLds o;
   int p = 0;
   auto take = [&](int n) { int at = p; p += (n + 3) & ~3; return at; };
   const int Co = kind == 2 ? 2 * C : C;
   o.xf = take(rpw * C);
   o.xo = take(rpw * C);
-  o.vo = take(rpw * C);
+  o.vo = take(rpw * (w - 1) * C);  // the w - 1 popped states per stream, oldest first
   o.ao = take(rpw * Co);
   o.zo = take(kind == 2 ? rpw * C : 0);
   o.so = take(kind == 2 ? rpw * S : 0);
@@ -132,9 +133,10 @@ struct ParGemm {
   int M, N, K;
   const void *A;           // plain: operand rows with stride lda; conv: the layer input rows (stride C)
   long long lda;
-  const void *ring;        // conv: this layer's queue, [dil][brows][C] operand-typed
+  const void *ring;        // conv: this layer's queue, [depth][brows][C] operand-typed
   long long t0;            // time of row j = 0
   int dil, brows, Tcur, C;
+  int w, depth;            // conv / tree: taps (K = w C) and queue slots ((w - 1) dil)
   const void *W;
   const float *bias;       // [N]
   const float *xres;       // residual epilogues: fp32 input rows (stride ldo)
@@ -144,11 +146,11 @@ struct ParGemm {
   int zoff;                // gate: column offset of this layer in the z rows
   float *logits;           // logits epilogue: [batch][n_steps][N]
   long long n_steps, s0;
-  // naive tree (PAR_A_TREE): row m = b * Tcur + i is the node at time tnow + toff[i]; its operands are the
-  // rows b * nprev + tsrc0[i] (time - dil) and b * nprev + tsrc1[i] (same time) of the level below, and
-  // a node before time 0 reads as zero.  When tsrc1 is set, residual epilogues read x_in from the
-  // level-below row b * nprev + tsrc1[i] instead of row m.
-  const int *toff, *tsrc0, *tsrc1;
+  // naive tree (PAR_A_TREE): row m = b * Tcur + i is the node at time tnow + toff[i]; tap k reads row
+  // b * nprev + tsrc[k * Tcur + i] of the level below (the node at time - (w - 1 - k) dil), and a node
+  // before time 0 reads as zero.  When tsrc1 is set, residual epilogues read x_in from the
+  // level-below row b * nprev + tsrc1[i] (the same-time node) instead of row m.
+  const int *toff, *tsrc, *tsrc1;
   int nprev;
   long long tnow;
   void *ztop;              // gate in tree mode: z of the node at offset 0 (i = Tcur - 1) also to ztop[b][zoff + c]
@@ -170,10 +172,10 @@ struct ParEmbed {
   int hmask;
 };
 struct ParRing {
-  void *ring;              // this layer's queue [dil][brows][row_bytes]
+  void *ring;              // this layer's queue [depth][brows][row_bytes]
   const void *src;         // the layer input rows of the chunk
   long long t0;
-  int Tcur, dil, brows, batch, row_bytes;
+  int Tcur, depth, brows, batch, row_bytes;
 };
 enum ParRepack { PAR_REPACK_CONV = 0, PAR_REPACK_COPY = 1 };
 enum ParAMode { PAR_A_PLAIN = 0, PAR_A_CONV = 1, PAR_A_TREE = 2 };
@@ -184,7 +186,7 @@ hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s);
 hipError_t launch_par_ring(const ParRing &r, hipStream_t s);
 hipError_t launch_par_set_last(const int32_t *inputs, int32_t *last, int batch, int n_steps, hipStream_t s);
 hipError_t launch_par_repack(const void *src, void *dst, int mode, int dtype, int N, int K, int C, int interleave,
-                             long long ldd, long long doff, hipStream_t s);
+                             long long ldd, long long doff, hipStream_t s);  // conv: K = w C
 hipError_t launch_par_bias(const float *src, float *dst, int N, int interleave, int accumulate, hipStream_t s);
 // Naive generator: sample each row of logits [batch][256] with uniforms[b][s], write samples[b][s] and
 // append the sample to the stream's input history at time tnext.
@@ -194,7 +196,7 @@ hipError_t launch_par_sample(const float *logits, const float *uniforms, int32_t
 // Repack modes: how W^T[k][n] is read from the caller's PyTorch layout.
 enum RepackMode {
   REPACK_LINEAR = 0,  // src [N][K] (out, in)
-  REPACK_CONV = 1,    // src [N][C][2]; k < C -> tap 0 (x_{t-d}), k >= C -> tap 1 (x_t); K = 2C
+  REPACK_CONV = 1,    // src [N][C][w]; k -> tap k / C, channel k % C; K = wC
   REPACK_EMBED = 2    // src [C][Q] -> dst [Q][C] row gather table (K = Q rows, N = C)
 };
 

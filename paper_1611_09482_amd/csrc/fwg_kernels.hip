@@ -65,12 +65,12 @@ template <> struct WTraits<uint16_t> {
 
 // ---------------------------------------------------------------------------
 // Row-block product: part[kg][r][n] = sum over this K-group of W^T[k][n] * A(r, k)
-// for r < RPW.  A(r, k) = A0[r*lda + k] for k < ksplit, else A1[r*lda + k - ksplit].
+// for r < RPW.  A(r, k) = A0[r*lda0 + k] for k < ksplit, else A1[r*lda1 + k - ksplit].
 // N >= 256: each thread owns columns tid, tid+256, ... over all of K (one group).
 // N < 256 : 256/N K-groups of N threads each.
 template <typename WT, int RPW>
-__device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K, int N, const float *A0,
-                                             const float *A1, int lda, int ksplit, float *part) {
+__device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K, int N, const float *A0, int lda0,
+                                             const float *A1, int lda1, int ksplit, float *part) {
   constexpr int KB = WTraits<WT>::KB;
   const uint4 *W = (const uint4 *)Wp;
   const int tid = threadIdx.x;
@@ -85,7 +85,9 @@ __device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K,
         float w[KB];
         WTraits<WT>::unpack(W[(long long)kb * N + n], w);
         const int k0 = kb * KB;
-        const float *A = k0 < ksplit ? A0 + k0 : A1 + (k0 - ksplit);
+        const bool lo = k0 < ksplit;
+        const float *A = lo ? A0 + k0 : A1 + (k0 - ksplit);
+        const int lda = lo ? lda0 : lda1;
 #pragma unroll
         for (int r = 0; r < RPW; ++r) {
 #pragma unroll
@@ -108,7 +110,9 @@ __device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K,
       float w[KB];
       WTraits<WT>::unpack(W[(long long)kb * N + n], w);
       const int k0 = kb * KB;
-      const float *A = k0 < ksplit ? A0 + k0 : A1 + (k0 - ksplit);
+      const bool lo = k0 < ksplit;
+      const float *A = lo ? A0 + k0 : A1 + (k0 - ksplit);
+      const int lda = lo ? lda0 : lda1;
 #pragma unroll
       for (int r = 0; r < RPW; ++r) {
 #pragma unroll
@@ -138,7 +142,7 @@ template <typename WT, int RPW>
 __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   float *lds = (float *)lds_raw;
-  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW);
+  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW, a.w);
   float *xf = lds + lay.xf, *xo = lds + lay.xo, *vo = lds + lay.vo, *ao = lds + lay.ao;
   float *zo = lds + lay.zo, *so = lds + lay.so, *ho = lds + lay.ho, *h2 = lds + lay.h2;
   float *lg = lds + lay.lg, *partA = lds + lay.partA, *partB = lds + lay.partB;
@@ -146,13 +150,13 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   int *ins = (int *)(lds + lay.ins);
 
   const int tid = threadIdx.x;
-  const int C = a.C, S = a.S, H = a.H, Q = a.Q, L = a.L;
+  const int C = a.C, S = a.S, H = a.H, Q = a.Q, L = a.L, w = a.w;
   const int Co = a.kind == 2 ? 2 * C : C;
   const int b0 = blockIdx.x * RPW;
   const int nrows = min(RPW, a.batch - b0);
   if (nrows <= 0) return;
 
-  for (int l = tid; l < L; l += kThreads) slots[l] = (int)(a.t0 % (long long)a.layers[l].dil);
+  for (int l = tid; l < L; l += kThreads) slots[l] = (int)(a.t0 % (long long)a.layers[l].depth);
   if (tid < RPW) {
     int v = 0;
     if (tid < nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(b0 + tid) * a.n_steps] : a.last[b0 + tid];
@@ -176,19 +180,23 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     for (int l = 0; l < L; ++l) {
       const LayerDev ld = a.layers[l];
       const long long qbase = ld.ring_off + (long long)slots[l] * a.bmax * C;
-      // ---- pop phase: the state pushed d_l steps ago (zeros before that)
-      for (int i = tid; i < RPW * C; i += kThreads) {
-        const int r = i / C, c = i % C;
-        vo[i] = r < nrows ? WTraits<WT>::load1(a.ring, qbase + (long long)(b0 + r) * C + c) : 0.f;
+      // ---- pop phase: slot t mod (w-1)d holds the state pushed (w-1)d steps ago (tap 0, zeros
+      // before that); for w > 2 tap k is the state k d slots further on, x^{l-1}_{t-(w-1-k)d}
+      for (int i = tid; i < RPW * (w - 1) * C; i += kThreads) {
+        const int r = i / ((w - 1) * C), kc = i % ((w - 1) * C), k = kc / C, c = kc % C;
+        int sk = slots[l] + k * ld.dil;
+        if (sk >= ld.depth) sk -= ld.depth;
+        const long long qk = ld.ring_off + (long long)sk * a.bmax * C;
+        vo[i] = r < nrows ? WTraits<WT>::load1(a.ring, qk + (long long)(b0 + r) * C + c) : 0.f;
       }
       __syncthreads();
-      // ---- push phase for this queue: the layer's input x^{l-1}_t replaces the popped slot
+      // ---- push phase for this queue: the layer's input x^{l-1}_t replaces the oldest state
       for (int i = tid; i < RPW * C; i += kThreads) {
         const int r = i / C, c = i % C;
         if (r < nrows) WTraits<WT>::store1(a.ring, qbase + (long long)(b0 + r) * C + c, xo[i]);
       }
-      // ---- dilated width-2 convolution: [v x] . [W_r ; W_e]
-      rows_product<WT, RPW>(ld.conv, 2 * C, Co, vo, xo, C, C, partA);
+      // ---- dilated convolution of width w: [v_0 .. v_{w-2} x] . [W_0 ; .. ; W_{w-1}]
+      rows_product<WT, RPW>(ld.conv, w * C, Co, vo, (w - 1) * C, xo, C, (w - 1) * C, partA);
       __syncthreads();
       if (a.kind == 2) {
         // gate: z = tanh(a[0:R]) * sigmoid(a[R:2R])
@@ -201,8 +209,8 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
         }
         __syncthreads();
         // residual and skip 1x1 products
-        rows_product<WT, RPW>(ld.res, C, C, zo, zo, C, C, partB);
-        rows_product<WT, RPW>(ld.skip, C, S, zo, zo, C, C, partA);
+        rows_product<WT, RPW>(ld.res, C, C, zo, C, zo, C, C, partB);
+        rows_product<WT, RPW>(ld.skip, C, S, zo, C, zo, C, C, partA);
         __syncthreads();
         for (int i = tid; i < RPW * C; i += kThreads) {
           const int r = i / C, c = i % C;
@@ -232,7 +240,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     if (a.kind == 2) {
       for (int i = tid; i < RPW * S; i += kThreads) ho[i] = WTraits<WT>::opnd(fmaxf(so[i], 0.f));
       __syncthreads();
-      rows_product<WT, RPW>(a.head, S, H, ho, ho, S, S, partA);
+      rows_product<WT, RPW>(a.head, S, H, ho, S, ho, S, S, partA);
       __syncthreads();
       for (int i = tid; i < RPW * H; i += kThreads) {
         const int r = i / H, n = i % H;
@@ -242,7 +250,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
       top = h2;
       Ktop = H;
     }
-    rows_product<WT, RPW>(a.out, Ktop, Q, top, top, Ktop, Ktop, partA);
+    rows_product<WT, RPW>(a.out, Ktop, Q, top, Ktop, top, Ktop, Ktop, partA);
     __syncthreads();
     for (int i = tid; i < RPW * Q; i += kThreads) {
       const int r = i / Q, q = i % Q;
@@ -275,7 +283,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     // ---- advance every queue's slot
     for (int l = tid; l < L; l += kThreads) {
       const int nx = slots[l] + 1;
-      slots[l] = nx == a.layers[l].dil ? 0 : nx;
+      slots[l] = nx == a.layers[l].depth ? 0 : nx;
     }
     __syncthreads();
   }
@@ -334,7 +342,7 @@ __global__ void repack_kernel(const T *__restrict__ src, T *__restrict__ dst, in
     const long long n = rest % N, kb = rest / N;
     const long long k = kb * KB + j;
     long long si;
-    if (mode == REPACK_CONV) si = (n * C + (k % C)) * 2 + (k >= C ? 1 : 0);
+    if (mode == REPACK_CONV) si = (n * C + (k % C)) * (K / C) + k / C;  // tap k / C of K / C
     else si = n * K + k;
     dst[i] = src[si];
   }

@@ -105,27 +105,24 @@ template <typename OT, int AM>
 __device__ __forceinline__ uint4 load_a(const ParGemm &g, int m, int k) {
   if (m >= g.M) return make_uint4(0, 0, 0, 0);
   if (AM == A_PLAIN) return *(const uint4 *)((const OT *)g.A + (long long)m * g.lda + k);
+  // tap k / C of the width-w dilated product reads the state (w - 1 - tap) d steps back
+  const int tap = k / g.C, kc = k - tap * g.C;
+  const int shift = (g.w - 1 - tap) * g.dil;
+  const int b = m / g.Tcur, j = m - b * g.Tcur;
   if (AM == A_TREE) {
-    const int b = m / g.Tcur, i = m - b * g.Tcur;
-    const long long tau = g.tnow + g.toff[i];
-    const bool tap0 = k < g.C;
-    if (tau - (tap0 ? g.dil : 0) < 0) return make_uint4(0, 0, 0, 0);  // zero padding before time 0
-    const long long row = (long long)b * g.nprev + (tap0 ? g.tsrc0[i] : g.tsrc1[i]);
-    return *(const uint4 *)((const OT *)g.A + row * g.C + (tap0 ? k : k - g.C));
+    if (g.tnow + g.toff[j] - shift < 0) return make_uint4(0, 0, 0, 0);  // zero padding before time 0
+    const long long row = (long long)b * g.nprev + g.tsrc[tap * g.Tcur + j];
+    return *(const uint4 *)((const OT *)g.A + row * g.C + kc);
   }
-  // dilated convolution: k < C is tap 0 (the state d steps back), k >= C tap 1 (the current state)
+  // dilated convolution over the chunk: the row `shift` steps back, or, before the chunk, the queue
+  // slot of that time (depth = (w - 1) d slots, slot = time mod depth)
   const OT *src;
-  if (k >= g.C) {
-    src = (const OT *)g.A + (long long)m * g.C + (k - g.C);
+  if (j >= shift) {
+    src = (const OT *)g.A + (long long)(m - shift) * g.C + kc;
   } else {
-    const int b = m / g.Tcur, j = m - b * g.Tcur;
-    if (j >= g.dil) {
-      src = (const OT *)g.A + (long long)(m - g.dil) * g.C + k;
-    } else {
-      const long long tau = g.t0 + j - g.dil;              // >= -dil: before time 0 the slot holds zeros
-      const long long slot = tau >= 0 ? tau % g.dil : tau + g.dil;
-      src = (const OT *)g.ring + (slot * g.brows + b) * (long long)g.C + k;
-    }
+    const long long tau = g.t0 + j - shift;  // >= -depth: before time 0 the slot holds zeros
+    const long long slot = tau >= 0 ? tau % g.depth : tau + g.depth;
+    src = (const OT *)g.ring + (slot * g.brows + b) * (long long)g.C + kc;
   }
   return *(const uint4 *)src;
 }
@@ -282,18 +279,18 @@ __global__ void par_embed_kernel(ParEmbed e) {
 }
 
 // Queue refresh after layer l: slot k takes the newest state of this chunk whose time is
-// k mod d (if the chunk reaches that slot); the operand rows of the layer's input are copied
+// k mod depth (if the chunk reaches that slot); the operand rows of the layer's input are copied
 // in 16-byte pieces.
 __global__ void par_ring_kernel(ParRing r) {
   const int pieces = r.row_bytes / 16;
-  const long long total = (long long)r.batch * r.dil * pieces;
+  const long long total = (long long)r.batch * r.depth * pieces;
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
     const int q = (int)(i % pieces);
     const long long bk = i / pieces;
-    const int k = (int)(bk % r.dil), b = (int)(bk / r.dil);
+    const int k = (int)(bk % r.depth), b = (int)(bk / r.depth);
     const long long last_t = r.t0 + r.Tcur - 1;
-    long long back = (last_t - k) % r.dil;                   // last_t may be below k: keep it non-negative
-    if (back < 0) back += r.dil;
+    long long back = (last_t - k) % r.depth;                 // last_t may be below k: keep it non-negative
+    if (back < 0) back += r.depth;
     const long long tnew = last_t - back;                    // newest time <= last_t with slot k
     if (tnew < r.t0) continue;                               // the chunk is shorter than d: slot kept
     const long long m = (long long)b * r.Tcur + (tnew - r.t0);
@@ -328,14 +325,14 @@ __global__ void par_repack_kernel(const T *__restrict__ src, T *__restrict__ dst
   for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long long)gridDim.x * blockDim.x) {
     const int n = (int)(i / K), k = (int)(i - (long long)n * K);
     if (mode == PAR_REPACK_CONV) {
-      // dst row n holds conv output channel o(n): [tap 0 over C | tap 1 over C]
+      // dst row n holds conv output channel o(n): [tap 0 over C | ... | tap w - 1 over C], K = w C
       int o = n;
       if (interleave) {
         const int grp = n >> 5, wi = n & 31, R = N / 2;
         o = wi < 16 ? 16 * grp + wi : R + 16 * grp + (wi - 16);
       }
-      const int tap = k >= C, c = k - tap * C;
-      dst[i] = src[((long long)o * C + c) * 2 + tap];
+      const int w = K / C, tap = k / C, c = k - tap * C;
+      dst[i] = src[((long long)o * C + c) * w + tap];
     } else {  // PAR_REPACK_COPY: src [N][K] into dst rows of stride ldd at column offset doff
       dst[(long long)n * ldd + doff + k] = src[i];
     }
@@ -383,7 +380,7 @@ hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {
 }
 
 hipError_t launch_par_ring(const ParRing &r, hipStream_t s) {
-  const int grid = grid_for((long long)r.batch * r.dil * (r.row_bytes / 16));
+  const int grid = grid_for((long long)r.batch * r.depth * (r.row_bytes / 16));
   hipLaunchKernelGGL(par::par_ring_kernel, dim3(grid), dim3(256), 0, s, r);
   return hipGetLastError();
 }

@@ -144,3 +144,27 @@ def test_naive_nodes_equal_depth_without_branching(lib):
     assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK and n.value == 15
     d = B.make_desc(W.RELU, W.F32, 32, (2, 2, 2, 2, 2), 1)
     assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK and n.value == 5 + 4 + 3 + 2 + 1
+
+
+@pytest.mark.parametrize("fw,r,L", [(3, 3, 4), (3, 5, 3), (4, 4, 3), (5, 7, 2)])
+def test_naive_tree_node_counts_width(lib, fw, r, L):
+    """Section 3.1, filter width w and dilations r^l with r >= w: the tree has w children per node
+    and no two branches meet, (w^L - 1) / (w - 1) layer nodes (O(w^L)); the queues hold
+    (w - 1)(r^L - 1) / (r - 1) states per channel and stream."""
+    dil = tuple(r ** i for i in range(L))
+    d = B.make_desc(W.RELU, W.F32, 32, dil, 1, filter_width=fw)
+    n = ctypes.c_int64(0)
+    assert lib.fwg_naive_nodes(ctypes.byref(d), ctypes.byref(n)) == B.FWG_OK
+    assert n.value == (fw ** L - 1) // (fw - 1)
+    cfg = W.ModelConfig(W.RELU, W.F32, 32, dil, filter_width=fw)
+    assert cfg.queue_total == (fw - 1) * (r ** L - 1) // (r - 1)
+    # the workspace grows with the queues: (w - 1) d_l slots per layer in two queue regions
+    d2 = B.make_desc(W.RELU, W.F32, 32, dil, 1, filter_width=2)
+    assert _rc_size(lib, d)[1] - _rc_size(lib, d2)[1] >= 2 * (fw - 2) * sum(dil) * 32 * 4
+
+
+def test_filter_width_validation(lib):
+    assert _rc_size(lib, _desc(filter_width=1))[0] == B.FWG_EINVAL
+    assert _rc_size(lib, _desc(filter_width=-3))[0] == B.FWG_EINVAL
+    assert _rc_size(lib, _desc(filter_width=17))[0] == B.FWG_EUNSUPPORTED
+    assert _rc_size(lib, _desc(filter_width=0))[1] == _rc_size(lib, _desc(filter_width=2))[1]

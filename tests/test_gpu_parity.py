@@ -60,6 +60,11 @@ FAMILIES = {
     "gated_r64_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
+    # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
+    "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
+    "gated_r32_w3_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
+    "gated_r64_w3_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
+    "relures_c64_w4_bf16": W.ModelConfig(W.RELU_RESIDUAL, W.BF16, 64, (1, 4, 16, 2), filter_width=4),
 }
 # families whose test forces the general (VALU) kernel family instead of the MFMA one
 FORCE_VALU = {"gated_r64_bf16_valu"}
@@ -83,7 +88,9 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_ro
         for k in env:
             os.environ.pop(k, None)
     if fam is not None:
-        want_valu = fam in FORCE_VALU or cfg.dtype != W.BF16
+        mfma_shape = (cfg.kind == W.GATED and cfg.dtype == W.BF16 and cfg.channels == 64 and
+                      cfg.skip_channels == 512 and cfg.head_channels == 512 and cfg.filter_width == 2)
+        want_valu = fam in FORCE_VALU or not mfma_shape
         assert (fw.regime == "valu") == want_valu, (fam, fw.regime)
     return w, fw, oracle.Oracle(w)
 
@@ -137,7 +144,8 @@ def test_teacher_forced_parity(fam, path):
 
 
 @pytest.mark.parametrize("fam,steps", [("relu_c32_f32", 7), ("gated_r32_f32", 5), ("gated_r64_bf16", 3),
-                                       ("relures_c512_f32", 64)])
+                                       ("relures_c512_f32", 64), ("gated_r32_w3_f32", 4),
+                                       ("relures_c64_w4_bf16", 6)])
 def test_parallel_chunks_across_queues(fam, steps):
     """Time-parallel path with chunks far shorter than the dilations (and a ragged last chunk):
     popped operands come from the queues written by earlier chunks; teacher forcing and online
@@ -213,7 +221,8 @@ def test_generation_parity(fam):
     check_generation(cfg, fw, orc, W.uniforms(4, B, n), B, fam)
 
 
-@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu"])
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu",
+                                 "gated_r64_w3_bf16"])
 def test_online_prediction_parity(fam):
     """Online prediction (fwg_step_forced): generate, feed observed samples from the same queues,
     generate again.  The oracle is driven through the same history (the GPU's own samples, then the
@@ -255,7 +264,8 @@ def test_online_prediction_parity(fam):
     assert np.array_equal(a, fw.teacher_forced(dev(seq)).cpu().numpy())
 
 
-@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "relures_c512_f32"])
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "relures_c512_f32",
+                                 "gated_r32_w3_f32", "relures_c64_w4_bf16"])
 def test_naive_generation_parity(fam):
     """The naive baseline (the tree of Fig. 1 recomputed for every sample, fwg_generate_naive) draws
     the oracle's samples up to near-ties, continues across calls exactly, and is reset with the
@@ -290,12 +300,17 @@ def test_naive_generation_parity(fam):
     assert np.array_equal(np.concatenate([a, c], axis=1), g)
 
 
-def test_delay_line_closed_form_gpu():
-    """W_e = 0, W_r = I, ReLU, zero biases, embeddings >= 0: logits[0:C] = x^0_{t - sum d} exactly,
-    through every queue depth up to 512 (pop before push, slot wrap-around)."""
+@pytest.mark.parametrize("fwidth,dil,path", [(2, tuple(2 ** i for i in range(10)), "step"),
+                                             (2, tuple(2 ** i for i in range(10)), "parallel"),
+                                             (3, (1, 3, 9, 27, 81, 5), "step"),
+                                             (3, (1, 3, 9, 27, 81, 5), "parallel"),
+                                             (4, (2, 7, 1), "step")])
+def test_delay_line_closed_form_gpu(fwidth, dil, path):
+    """Tap 0 (the oldest state) = I, every other tap 0, ReLU, zero biases, embeddings >= 0:
+    logits[0:C] = x^0_{t - (w - 1) sum d} exactly, through queue depths up to 512 (pop before push,
+    slot wrap-around, the w - 1 taps of wider filters)."""
     C = 32
-    dil = tuple(2 ** i for i in range(10))
-    cfg = W.ModelConfig(W.RELU, W.F32, C, dil)
+    cfg = W.ModelConfig(W.RELU, W.F32, C, dil, filter_width=fwidth)
     w = W.make_weights(cfg, 0)
     w.embed[:] = np.array([[(q * 7 + c) % 97 for q in range(256)] for c in range(C)], np.float32)
     for l in range(cfg.n_layers):
@@ -303,8 +318,12 @@ def test_delay_line_closed_form_gpu():
         w.conv[l][np.arange(C), np.arange(C), 0] = 1.0
     w.out[:] = 0
     w.out[np.arange(C), np.arange(C)] = 1.0
-    fw = binding.from_model(cfg, w, max_batch=3)
-    D = sum(dil)
+    os.environ["FWG_FORCED_PATH"] = path
+    try:
+        fw = binding.from_model(cfg, w, max_batch=3)
+    finally:
+        os.environ.pop("FWG_FORCED_PATH", None)
+    D = cfg.queue_total
     T = D + 100
     x = W.sequences(8, 3, T)
     g = fw.teacher_forced(dev(x)).cpu().numpy()
