@@ -465,3 +465,13 @@ def test_full_bytenet():
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255
     _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [31], 640)
+
+
+def test_full_gated_w3():
+    """The filter-width-3 workload at full size (64 streams x 8,000 steps): sampled streams checked
+    by the oracle over every step."""
+    wl, w, fw, orc = _full("gated_r32_s256_w3_l14_b64")
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    g = fw.generate(dev(u)).cpu().numpy()
+    assert g.min() >= 0 and g.max() <= 255
+    _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 63], wl.n_steps)

@@ -130,6 +130,13 @@ WORKLOADS: Dict[str, Workload] = {
                  ModelConfig(RELU_RESIDUAL, F32, 512, _blocks(5, 5)),
                  batch=32, n_steps=4096, weight_seed=3, uniform_seed=3,
                  description="ByteNet-decoder-style ReLU+residual 5x5 layers, C=512, fp32, batch 32, 4,096 steps"),
+        # filter width 3 with dilation rate r = w = 3 (Section 3.1: O(wL) work, O((w-1) r^L) queue space)
+        Workload("gated_r32_s256_w3_l14_b64",
+                 ModelConfig(GATED, F32, 32, tuple(3 ** i for i in range(7)) * 2, skip_channels=256,
+                             head_channels=256, filter_width=3),
+                 batch=64, n_steps=8000, weight_seed=4, uniform_seed=4,
+                 description="gated 2x7 layers of filter width 3 (dilations 1..729 per block), R=32, S=H=256, "
+                             "fp32, batch 64, 8,000 steps"),
     ]
 }
 
