@@ -40,6 +40,8 @@ size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 
 struct Plan {
   int kind, dtype, Q, C, S, H, L, bmax, seed_input, Co, es, rpw;
+  size_t valu_block;      // bytes of one layer's weight + bias block (general step kernels)
+  int valu_wbytes;        // the block when the general step kernels stage it in LDS, else 0
   int w;                  // filter width: taps per dilated product
   int regime;
   int brows;              // queue rows per slot (max_batch, padded to whole blocks for the MFMA family)
@@ -157,16 +159,44 @@ int make_plan(const fwg_desc *d, Plan *p) {
                 "divides 256 (with K/%d divisible by 256/N) or is at least 256",
                 kb, kb);
 
-  // rows per block: as many streams per block as LDS allows, at most 8, fewer for tiny batches
-  int rpw = 8;
-  while (rpw > 1 && rpw > p->bmax) rpw >>= 1;
-  for (;; rpw >>= 1) {
-    const ValuLds lay = valu_lds_layout(p->kind, p->C, p->S, p->H, p->Q, p->L, rpw, w);
-    p->lds_bytes = (size_t)lay.total_floats * 4;
-    if (p->lds_bytes <= 160 * 1024 || rpw == 1) break;
+  // one layer's block for the general step kernels: conv | res | skip weights, then the biases
+  {
+    const bool g = p->kind == FWG_GATED;
+    size_t b = (size_t)w * p->C * p->Co * p->es;
+    if (g) b += ((size_t)p->C * p->C + (size_t)p->S * p->C) * p->es;
+    b += sizeof(float) * ((size_t)p->Co + (g ? (size_t)p->C + p->S : 0));
+    p->valu_block = (b + 15) & ~(size_t)15;
   }
-  if (p->lds_bytes > 160 * 1024) return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS");
+  // rows per block and weight staging.  Staging moves a layer's weight loads off its critical path
+  // but costs the copy issue; it pays from two streams per block (measured: at one stream the
+  // layer is too short to hide the copy).  Take the most rows per block (at most 8, fewer for
+  // tiny batches) at which two layers' blocks fit in LDS, else the most rows that fit without
+  // staging.  The popped states of a layer are held in registers between layers (at most
+  // kValuPrefPops per thread).
+  int rmax = 8;
+  while (rmax > 1 && rmax > p->bmax) rmax >>= 1;
+  const char *vs = getenv("FWG_VALU_STAGE");  // "0": never stage (the variant that reads weights from L2)
+  const bool can_stage = p->valu_block <= (size_t)kValuStagePieces * 16 * kThreads && !(vs && strcmp(vs, "0") == 0);
+  const int wf = (int)(p->valu_block / 4);
+  int rpw = 0;
+  bool stage = false;
+  for (int pass = 0; pass < 2 && rpw == 0; ++pass) {
+    const bool st = pass == 0;
+    if (st && !can_stage) continue;
+    for (int r = rmax; r >= (st ? 2 : 1); r >>= 1) {
+      if (r * (w - 1) * p->C > kValuPrefPops * kThreads) continue;
+      const ValuLds lay = valu_lds_layout(p->kind, p->C, p->S, p->H, p->Q, p->L, r, w, st ? wf : 0);
+      if ((size_t)lay.total_floats * 4 <= 160 * 1024) {
+        rpw = r;
+        stage = st;
+        p->lds_bytes = (size_t)lay.total_floats * 4;
+        break;
+      }
+    }
+  }
+  if (rpw == 0) return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS and registers");
   p->rpw = rpw;
+  p->valu_wbytes = stage ? (int)p->valu_block : 0;
 
   // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512
   p->regime = REGIME_VALU;
@@ -193,13 +223,18 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_conv.resize(p->L); p->off_conv_b.resize(p->L);
   p->off_res.assign(p->L, 0); p->off_res_b.assign(p->L, 0); p->off_skip.assign(p->L, 0); p->off_skip_b.assign(p->L, 0);
   for (int l = 0; l < p->L; ++l) {
-    p->off_conv[l] = take((size_t)p->Co * w * p->C * p->es);
-    p->off_conv_b[l] = take(sizeof(float) * p->Co);
+    // the layer's block (layout read by the general step kernels)
+    const size_t base = take(p->valu_block);
+    const size_t wconv = (size_t)p->Co * w * p->C * p->es;
+    p->off_conv[l] = base;
     if (p->kind == FWG_GATED) {
-      p->off_res[l] = take((size_t)p->C * p->C * p->es);
-      p->off_res_b[l] = take(sizeof(float) * p->C);
-      p->off_skip[l] = take((size_t)p->S * p->C * p->es);
-      p->off_skip_b[l] = take(sizeof(float) * p->S);
+      p->off_res[l] = base + wconv;
+      p->off_skip[l] = p->off_res[l] + (size_t)p->C * p->C * p->es;
+      p->off_conv_b[l] = p->off_skip[l] + (size_t)p->S * p->C * p->es;
+      p->off_res_b[l] = p->off_conv_b[l] + sizeof(float) * p->Co;
+      p->off_skip_b[l] = p->off_res_b[l] + sizeof(float) * p->C;
+    } else {
+      p->off_conv_b[l] = base + wconv;
     }
   }
   p->off_head = p->kind == FWG_GATED ? take((size_t)p->H * p->S * p->es) : 0;
@@ -323,6 +358,7 @@ StepArgs base_args(const fwg_handle *h) {
   a.out_b = (const float *)(h->ws + p.off_out_b);
   a.last = (int32_t *)(h->ws + p.off_last);
   a.bmax = p.brows;
+  a.valu_wbytes = p.valu_wbytes;
   if (p.regime == REGIME_MFMA) {
     a.mf_frags = h->ws + p.off_frags;
     a.mf_embT = h->ws + p.off_embT;

@@ -12,6 +12,8 @@ constexpr int kMaxLayers = 1024;  // per-layer slot counters live in LDS
 
 // One dilated layer as the step kernels see it (device-resident table).
 struct LayerDev {
+  // general step kernels: conv, res and skip weights, then conv_b, res_b and skip_b, are one
+  // contiguous block starting at conv (staged into LDS as a unit)
   const void *conv;     // packed conv weights (W_r stacked over W_e), layout per kernel family
   const float *conv_b;  // [Cout]
   const void *res;      // gated: packed [R][R]
@@ -26,6 +28,8 @@ struct LayerDev {
 // Arguments of one step-kernel launch (passed by value).
 struct StepArgs {
   const LayerDev *layers;  // [L]
+  int valu_wbytes;         // general step kernels: bytes of one layer's weights + biases staged in LDS
+                           // one layer ahead (0: read from global memory)
   const void *embed;       // [Q][C] rows (embedding transposed for a row gather)
   const float *embed_b;    // [C]
   const void *head;        // gated: packed [H][S]
@@ -76,12 +80,26 @@ inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMf
 // Wp[kb][n][kb_elems], with W^T[k][n] the weight from input k to output n.
 inline int valu_kb_elems(int dtype) { return dtype == 1 ? 8 : 4; }
 
-// LDS layout (in floats) of the VALU step kernel for rows-per-block `rpw`.
-struct ValuLds {
-  int xf, xo, vo, ao, zo, so, ho, h2, lg, partA, partB, slots, ins, total_floats;
+// The layer fields the general step kernel reads in its loop, copied to LDS at launch.
+struct ValuLayer {
+  const void *block;    // the layer's weight + bias block
+  long long ring_off;   // element offset of the layer's queue
+  int dil, depth;
+  int pad_[2];
 };
+static_assert(sizeof(ValuLayer) == 32, "eight floats per layer in the LDS table");
+
+// LDS layout (in floats) of the VALU step kernel for rows-per-block `rpw`: two buffers of popped
+// states and, when a layer's weights are staged (wfloats > 0), two weight buffers.
+struct ValuLds {
+  int xf, xo, vo, vo2, ao, zo, so, ho, h2, lg, partA, partB, wb0, wb1, ltab, slots, ins, total_floats;
+};
+constexpr int kValuPrefPops = 8;   // popped elements per thread and layer held in registers
+// Weight staging: a layer's block, at most kValuStagePieces 16-byte pieces per thread (64 KB).
+constexpr int kValuStagePieces = 16;
 __host__ __device__ inline int valu_part_cols(int N) { return N >= 256 ? N : 256; }
-__host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H, int Q, int L, int rpw, int w) {
+__host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H, int Q, int L, int rpw, int w,
+                                                   int wfloats) {
   ValuLds o;
   int p = 0;
   auto take = [&](int n) { int at = p; p += (n + 3) & ~3; return at; };
@@ -89,6 +107,7 @@ __host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H
   o.xf = take(rpw * C);
   o.xo = take(rpw * C);
   o.vo = take(rpw * (w - 1) * C);  // the w - 1 popped states per stream, oldest first
+  o.vo2 = take(rpw * (w - 1) * C);
   o.ao = take(rpw * Co);
   o.zo = take(kind == 2 ? rpw * C : 0);
   o.so = take(kind == 2 ? rpw * S : 0);
@@ -103,6 +122,9 @@ __host__ __device__ inline ValuLds valu_lds_layout(int kind, int C, int S, int H
   partN = partN > valu_part_cols(Q) ? partN : valu_part_cols(Q);
   o.partA = take(rpw * partN);
   o.partB = take(kind == 2 ? rpw * valu_part_cols(C) : 0);
+  o.wb0 = take(wfloats);
+  o.wb1 = take(wfloats);
+  o.ltab = take(8 * L);  // per layer: weight block address, queue offset, dilation, depth (ValuLayer)
   o.slots = take(L);   // int
   o.ins = take(rpw);   // int
   o.total_floats = p;

@@ -18,8 +18,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "fwg_internal.h"
 #include "fwg_sample.h"
+
 
 namespace fwg {
 
@@ -39,10 +42,31 @@ __device__ __forceinline__ uint16_t to_bf16_bits(float x) {
   return (uint16_t)(u >> 16);
 }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// Direct global-to-LDS copy of 16 bytes per lane: lane i's bytes come from src_wave + lane_off
+// (lane_off = 16 i) and land at LDS byte address lds_dst_wave + 16 i (both bases wave-uniform).
+// Issued as inline assembly: the compiler orders every such copy after the previous one has
+// completed (it cannot tell that they write disjoint LDS), which would serialise the staging
+// stream.  The lane offset stays in one register for all copies and the bases are scalar, so no
+// register the copies read is overwritten while they are in flight; callers wait for completion
+// (vmcnt) before the data is read.
+__device__ __forceinline__ void lds_copy16(const void *src_wave, uint32_t lane_off, const void *lds_dst_wave) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void *)lds_dst_wave);
+  const uint64_t sp = (uint64_t)(uintptr_t)src_wave;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)sp), hi = __builtin_amdgcn_readfirstlane((uint32_t)(sp >> 32));
+  const uint64_t sbase = ((uint64_t)hi << 32) | lo;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(base), "v"(lane_off), "s"(sbase)
+               : "m0");
+}
+
 template <typename WT> struct WTraits;
 template <> struct WTraits<float> {
   static constexpr int KB = 4;
-  __device__ static __forceinline__ void unpack(const uint4 &v, float *w) {
+  __device__ static __forceinline__ void unpack(u32x4 v, float *w) {
     w[0] = __uint_as_float(v.x); w[1] = __uint_as_float(v.y);
     w[2] = __uint_as_float(v.z); w[3] = __uint_as_float(v.w);
   }
@@ -52,7 +76,7 @@ template <> struct WTraits<float> {
 };
 template <> struct WTraits<uint16_t> {
   static constexpr int KB = 8;
-  __device__ static __forceinline__ void unpack(const uint4 &v, float *w) {
+  __device__ static __forceinline__ void unpack(u32x4 v, float *w) {
     w[0] = bf16_lo(v.x); w[1] = bf16_hi(v.x); w[2] = bf16_lo(v.y); w[3] = bf16_hi(v.y);
     w[4] = bf16_lo(v.z); w[5] = bf16_hi(v.z); w[6] = bf16_lo(v.w); w[7] = bf16_hi(v.w);
   }
@@ -68,11 +92,12 @@ template <> struct WTraits<uint16_t> {
 // for r < RPW.  A(r, k) = A0[r*lda0 + k] for k < ksplit, else A1[r*lda1 + k - ksplit].
 // N >= 256: each thread owns columns tid, tid+256, ... over all of K (one group).
 // N < 256 : 256/N K-groups of N threads each.
-template <typename WT, int RPW>
-__device__ __forceinline__ void rows_product(const void *__restrict__ Wp, int K, int N, const float *A0, int lda0,
+// WP: the weight pointer type, a global (address space 1) or an LDS (address space 3) pointer to
+// 16-byte vectors, so that staged weights are read with LDS instructions.
+template <typename WT, int RPW, typename WP>
+__device__ __forceinline__ void rows_product(WP W, int K, int N, const float *A0, int lda0,
                                              const float *A1, int lda1, int ksplit, float *part) {
   constexpr int KB = WTraits<WT>::KB;
-  const uint4 *W = (const uint4 *)Wp;
   const int tid = threadIdx.x;
   const int nkb = K / KB;
   if (N >= kThreads) {
@@ -138,31 +163,116 @@ __device__ __forceinline__ float bias_or0(const float *b, int i) { return b ? b[
 
 // ---------------------------------------------------------------------------
 // The general step kernel.  Block = RPW streams, 256 threads.
-template <typename WT, int RPW>
+//
+// Latency hiding: the states a layer pops do not depend on the current step (they were pushed
+// at least d steps earlier), so the pops of layer l + 1 -- or of layer 0 of the next step -- are
+// loaded into registers while layer l computes and land in the second of two LDS buffers at the
+// end of the layer.  When two layers' weights fit in LDS (a.valu_wbytes > 0) the next layer's
+// weights and biases are copied into the second weight buffer meanwhile, by direct
+// global-to-LDS loads, so a layer's critical path touches LDS only.
+typedef __attribute__((address_space(3))) const u32x4 *lds_u4p;
+typedef __attribute__((address_space(1))) const u32x4 *glb_u4p;
+typedef __attribute__((address_space(3))) const float *lds_f32p;
+typedef __attribute__((address_space(1))) const float *glb_f32p;
+
+template <typename WT, int RPW, bool STAGE>
 __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   float *lds = (float *)lds_raw;
-  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW, a.w);
-  float *xf = lds + lay.xf, *xo = lds + lay.xo, *vo = lds + lay.vo, *ao = lds + lay.ao;
+  const int wfloats = a.valu_wbytes / 4;
+  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW, a.w, wfloats);
+  float *xf = lds + lay.xf, *xo = lds + lay.xo, *ao = lds + lay.ao;
   float *zo = lds + lay.zo, *so = lds + lay.so, *ho = lds + lay.ho, *h2 = lds + lay.h2;
   float *lg = lds + lay.lg, *partA = lds + lay.partA, *partB = lds + lay.partB;
+  // the two buffers of popped states and of staged weights, selected by arithmetic on the LDS base
+  // (a pointer array indexed at run time would turn LDS accesses into generic ones)
+  auto vbuf = [&](int p) { return lds + (p ? lay.vo2 : lay.vo); };
+  auto wbuf = [&](int p) { return (uint4 *)(lds + (p ? lay.wb1 : lay.wb0)); };
   int *slots = (int *)(lds + lay.slots);
   int *ins = (int *)(lds + lay.ins);
+  ValuLayer *ltab = (ValuLayer *)(lds + lay.ltab);
+  (void)ao;
 
   const int tid = threadIdx.x;
   const int C = a.C, S = a.S, H = a.H, Q = a.Q, L = a.L, w = a.w;
   const int Co = a.kind == 2 ? 2 * C : C;
+  const int K = w * C;
   const int b0 = blockIdx.x * RPW;
   const int nrows = min(RPW, a.batch - b0);
   if (nrows <= 0) return;
+  constexpr bool stage = STAGE;  // the host launches the staging variant iff a.valu_wbytes > 0
+  const int nw16 = a.valu_wbytes / 16;       // 16-byte pieces of one layer's staged block
+  const int VP = RPW * (w - 1) * C;          // popped elements per layer
+  const int es = sizeof(WT);
+  // offsets inside a layer's block: conv | res | skip weights, then conv_b | res_b | skip_b
+  const size_t o_res = (size_t)K * Co * es, o_skip = o_res + (size_t)C * C * es;
+  const size_t o_cb = a.kind == 2 ? o_skip + (size_t)S * C * es : o_res;
+  const size_t o_rb = o_cb + (size_t)Co * 4, o_sb = o_rb + (size_t)C * 4;
 
-  for (int l = tid; l < L; l += kThreads) slots[l] = (int)(a.t0 % (long long)a.layers[l].depth);
+  for (int l = tid; l < L; l += kThreads) {
+    const LayerDev ld = a.layers[l];
+    ValuLayer v;
+    v.block = ld.conv;
+    v.ring_off = ld.ring_off;
+    v.dil = ld.dil;
+    v.depth = ld.depth;
+    v.pad_[0] = v.pad_[1] = 0;
+    ltab[l] = v;
+    slots[l] = (int)(a.t0 % (long long)ld.depth);
+  }
   if (tid < RPW) {
     int v = 0;
     if (tid < nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(b0 + tid) * a.n_steps] : a.last[b0 + tid];
     ins[tid] = v;
   }
   __syncthreads();
+
+  // prefetch registers of the next layer's popped states
+  float pp[kValuPrefPops];
+  const uint32_t lane16 = 16u * (uint32_t)(tid & 63);
+  // tap k of layer l at the step whose slot is `slot`: the state k d slots after the oldest one;
+  // with staging, the layer's weight block is copied straight into weight buffer `par`
+  auto fetch = [&](int l, int slot, int par) {
+    const ValuLayer ld = ltab[l];
+#pragma unroll
+    for (int j = 0; j < kValuPrefPops; ++j) {
+      const int i = tid + j * kThreads;
+      float v = 0.f;
+      if (i < VP) {
+        const int r = i / ((w - 1) * C), kc = i - r * ((w - 1) * C), k = kc / C, c = kc - k * C;
+        int sk = slot + k * ld.dil;
+        if (sk >= ld.depth) sk -= ld.depth;
+        if (r < nrows)
+          v = WTraits<WT>::load1(a.ring, ld.ring_off + (long long)sk * a.bmax * C + (long long)(b0 + r) * C + c);
+      }
+      pp[j] = v;
+    }
+    if (stage) {
+      // each wave copies 64 consecutive 16-byte pieces per instruction
+      const uint4 *src = (const uint4 *)ld.block;
+      const int wv = tid >> 6;
+#pragma unroll
+      for (int j = 0; j < kValuStagePieces; ++j) {
+        const int base = j * kThreads + wv * 64;
+        if (base < nw16 && (tid & 63) + base < nw16) lds_copy16(src + base, lane16, wbuf(par) + base);
+      }
+    }
+  };
+  auto land = [&](int par) {
+    float *vb = vbuf(par);
+#pragma unroll
+    for (int j = 0; j < kValuPrefPops; ++j) {
+      const int i = tid + j * kThreads;
+      if (i < VP) vb[i] = pp[j];
+    }
+    // the copies into the weight buffer have completed once the memory counter drains
+    if (stage) __builtin_amdgcn_s_waitcnt(0);
+  };
+
+  fetch(0, slots[0], 0);
+  land(0);
+  __syncthreads();
+  int par = 0;  // buffer holding the current layer's pops and weights
 
   for (int s = 0; s < a.n_steps; ++s) {
     // ---- current input (h^0_e) is ins[]: set before the loop and at the end of every step
@@ -178,60 +288,75 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     __syncthreads();
 
     for (int l = 0; l < L; ++l) {
-      const LayerDev ld = a.layers[l];
+      const ValuLayer ld = ltab[l];
+      // the layer that runs next: layer l + 1 now, or layer 0 at the next step (its slot one on)
+      const bool more = l + 1 < L || s + 1 < a.n_steps;
+      const int nl = l + 1 < L ? l + 1 : 0;
+      int nslot = slots[nl];
+      if (l + 1 == L) nslot = nslot + 1 == ltab[0].depth ? 0 : nslot + 1;
+      // with one layer, the next step's pops include the state this layer pushes now: fetch after it
+      if (more && L > 1) fetch(nl, nslot, par ^ 1);
+      // ---- push phase for this queue: the layer's input x^{l-1}_t replaces the oldest state,
+      // whose pop has landed in LDS already
       const long long qbase = ld.ring_off + (long long)slots[l] * a.bmax * C;
-      // ---- pop phase: slot t mod (w-1)d holds the state pushed (w-1)d steps ago (tap 0, zeros
-      // before that); for w > 2 tap k is the state k d slots further on, x^{l-1}_{t-(w-1-k)d}
-      for (int i = tid; i < RPW * (w - 1) * C; i += kThreads) {
-        const int r = i / ((w - 1) * C), kc = i % ((w - 1) * C), k = kc / C, c = kc % C;
-        int sk = slots[l] + k * ld.dil;
-        if (sk >= ld.depth) sk -= ld.depth;
-        const long long qk = ld.ring_off + (long long)sk * a.bmax * C;
-        vo[i] = r < nrows ? WTraits<WT>::load1(a.ring, qk + (long long)(b0 + r) * C + c) : 0.f;
-      }
-      __syncthreads();
-      // ---- push phase for this queue: the layer's input x^{l-1}_t replaces the oldest state
       for (int i = tid; i < RPW * C; i += kThreads) {
         const int r = i / C, c = i % C;
         if (r < nrows) WTraits<WT>::store1(a.ring, qbase + (long long)(b0 + r) * C + c, xo[i]);
       }
+      if (more && L == 1) {
+        __syncthreads();
+        fetch(nl, nslot, par ^ 1);
+      }
+      const char *wb = stage ? (const char *)wbuf(par) : (const char *)ld.block;
+      // staged weights and biases through LDS pointers (LDS loads), else global pointers
+      typedef typename std::conditional<STAGE, lds_u4p, glb_u4p>::type WP;
+      typedef typename std::conditional<STAGE, lds_f32p, glb_f32p>::type BP;
+      auto wp = [&](size_t off) { return (WP)(wb + off); };
+      const BP cb = (BP)(wb + o_cb);
+      const float *vo = vbuf(par);
       // ---- dilated convolution of width w: [v_0 .. v_{w-2} x] . [W_0 ; .. ; W_{w-1}]
-      rows_product<WT, RPW>(ld.conv, w * C, Co, vo, (w - 1) * C, xo, C, (w - 1) * C, partA);
+      rows_product<WT, RPW, WP>(wp(0), K, Co, vo, (w - 1) * C, xo, C, (w - 1) * C, partA);
       __syncthreads();
       if (a.kind == 2) {
+        const BP rb = (BP)(wb + o_rb), sb = (BP)(wb + o_sb);
         // gate: z = tanh(a[0:R]) * sigmoid(a[R:2R])
         for (int i = tid; i < RPW * C; i += kThreads) {
           const int r = i / C, c = i % C;
-          const float af = bias_or0(ld.conv_b, c) + part_sum<RPW>(partA, Co, r, c);
-          const float ag = bias_or0(ld.conv_b, C + c) + part_sum<RPW>(partA, Co, r, C + c);
-          const float z = tanhf(af) * (1.f / (1.f + __expf(-ag)));
+          const float af = cb[c] + part_sum<RPW>(partA, Co, r, c);
+          const float ag = cb[C + c] + part_sum<RPW>(partA, Co, r, C + c);
+          // tanh(a) = 1 - 2 / (e^{2a} + 1) and sigmoid(g) = 1 / (1 + e^{-g}), one exp and one
+          // reciprocal each (absolute error ~1e-7, saturating correctly at both ends)
+          const float z = (1.f - 2.f * __builtin_amdgcn_rcpf(__expf(2.f * af) + 1.f)) *
+                          __builtin_amdgcn_rcpf(1.f + __expf(-ag));
           zo[i] = WTraits<WT>::opnd(z);
         }
         __syncthreads();
         // residual and skip 1x1 products
-        rows_product<WT, RPW>(ld.res, C, C, zo, C, zo, C, C, partB);
-        rows_product<WT, RPW>(ld.skip, C, S, zo, C, zo, C, C, partA);
+        rows_product<WT, RPW, WP>(wp(o_res), C, C, zo, C, zo, C, C, partB);
+        rows_product<WT, RPW, WP>(wp(o_skip), C, S, zo, C, zo, C, C, partA);
         __syncthreads();
         for (int i = tid; i < RPW * C; i += kThreads) {
           const int r = i / C, c = i % C;
-          const float v = xf[i] + bias_or0(ld.res_b, c) + part_sum<RPW>(partB, C, r, c);
+          const float v = xf[i] + rb[c] + part_sum<RPW>(partB, C, r, c);
           xf[i] = v;
           xo[i] = WTraits<WT>::opnd(v);
         }
         for (int i = tid; i < RPW * S; i += kThreads) {
           const int r = i / S, k = i % S;
-          so[i] += bias_or0(ld.skip_b, k) + part_sum<RPW>(partA, S, r, k);
+          so[i] += sb[k] + part_sum<RPW>(partA, S, r, k);
         }
       } else {
         for (int i = tid; i < RPW * C; i += kThreads) {
           const int r = i / C, c = i % C;
-          const float pre = bias_or0(ld.conv_b, c) + part_sum<RPW>(partA, Co, r, c);
+          const float pre = cb[c] + part_sum<RPW>(partA, Co, r, c);
           const float v = (a.kind == 1 ? xf[i] : 0.f) + fmaxf(pre, 0.f);
           xf[i] = v;
           xo[i] = WTraits<WT>::opnd(v);
         }
       }
+      if (more) land(par ^ 1);
       __syncthreads();
+      par ^= 1;
     }
 
     // ---- output head
@@ -240,7 +365,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     if (a.kind == 2) {
       for (int i = tid; i < RPW * S; i += kThreads) ho[i] = WTraits<WT>::opnd(fmaxf(so[i], 0.f));
       __syncthreads();
-      rows_product<WT, RPW>(a.head, S, H, ho, S, ho, S, S, partA);
+      rows_product<WT, RPW, glb_u4p>((glb_u4p)a.head, S, H, ho, S, ho, S, S, partA);
       __syncthreads();
       for (int i = tid; i < RPW * H; i += kThreads) {
         const int r = i / H, n = i % H;
@@ -250,7 +375,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
       top = h2;
       Ktop = H;
     }
-    rows_product<WT, RPW>(a.out, Ktop, Q, top, Ktop, top, Ktop, Ktop, partA);
+    rows_product<WT, RPW, glb_u4p>((glb_u4p)a.out, Ktop, Q, top, Ktop, top, Ktop, Ktop, partA);
     __syncthreads();
     for (int i = tid; i < RPW * Q; i += kThreads) {
       const int r = i / Q, q = i % Q;
@@ -270,8 +395,8 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
       if (tid < nrows && nx < a.n_steps) ins[tid] = a.inputs[(long long)(b0 + tid) * a.n_steps + nx];
     } else {
       // ---- sample and feed back
-      const int w = tid >> 6;
-      for (int r = w; r < nrows; r += kThreads / 64) {
+      const int wv = tid >> 6;
+      for (int r = wv; r < nrows; r += kThreads / 64) {
         const float u = a.uniforms[(long long)(b0 + r) * a.n_steps + s];
         const int k = sample_row_256(lg + r * Q, u);
         if ((tid & 63) == 0) {
@@ -283,33 +408,38 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     // ---- advance every queue's slot
     for (int l = tid; l < L; l += kThreads) {
       const int nx = slots[l] + 1;
-      slots[l] = nx == a.layers[l].depth ? 0 : nx;
+      slots[l] = nx == ltab[l].depth ? 0 : nx;
     }
     __syncthreads();
   }
   if (a.mode != MODE_TEACHER && tid < nrows) a.last[b0 + tid] = ins[tid];
 }
 
-template <typename WT>
+template <typename WT, bool STAGE>
 static hipError_t launch_valu_t(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
   const dim3 grid((a.batch + rpw - 1) / rpw), block(kThreads);
   switch (rpw) {
-    case 1: hipLaunchKernelGGL((valu_step_kernel<WT, 1>), grid, block, lds, s, a); break;
-    case 2: hipLaunchKernelGGL((valu_step_kernel<WT, 2>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((valu_step_kernel<WT, 4>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((valu_step_kernel<WT, 8>), grid, block, lds, s, a); break;
+    case 1: hipLaunchKernelGGL((valu_step_kernel<WT, 1, STAGE>), grid, block, lds, s, a); break;
+    case 2: hipLaunchKernelGGL((valu_step_kernel<WT, 2, STAGE>), grid, block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL((valu_step_kernel<WT, 4, STAGE>), grid, block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL((valu_step_kernel<WT, 8, STAGE>), grid, block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_valu_step(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
-  return a.dtype == 1 ? launch_valu_t<uint16_t>(a, rpw, lds, s) : launch_valu_t<float>(a, rpw, lds, s);
+  if (a.valu_wbytes > 0)
+    return a.dtype == 1 ? launch_valu_t<uint16_t, true>(a, rpw, lds, s) : launch_valu_t<float, true>(a, rpw, lds, s);
+  return a.dtype == 1 ? launch_valu_t<uint16_t, false>(a, rpw, lds, s) : launch_valu_t<float, false>(a, rpw, lds, s);
 }
 
 template <typename WT, int RPW>
 static hipError_t set_lds_one(size_t bytes) {
-  return hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW>,
+  hipError_t e = hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, true>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, false>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 

@@ -70,9 +70,10 @@ FAMILIES = {
 FORCE_VALU = {"gated_r64_bf16_valu"}
 
 
-def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_rows=None):
+def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_rows=None, valu_stage=None):
     """path: None (the library's choice), "step" or "parallel" for the forced calls;
-    par_rows: rows per chunk of the time-parallel path (small values force many chunks)."""
+    par_rows: rows per chunk of the time-parallel path (small values force many chunks);
+    valu_stage: "0" keeps the general step kernels from staging weights in LDS."""
     w = W.make_weights(cfg, seed, bias_scale=bias_scale)
     env = {}
     if fam in FORCE_VALU:
@@ -81,6 +82,8 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_ro
         env["FWG_FORCED_PATH"] = path
     if par_rows is not None:
         env["FWG_PAR_ROWS"] = str(par_rows)
+    if valu_stage is not None:
+        env["FWG_VALU_STAGE"] = valu_stage
     os.environ.update(env)
     try:
         fw = binding.from_model(cfg, w, max_batch=max_batch)
@@ -210,6 +213,22 @@ def test_prime_then_generate(fam):
             lo, hi = cdf_bounds(slg[b, t], so[b, t])
             assert min(u[b, t] - lo, hi - u[b, t]) < tau, (fam, b, t)
     log(f"{fam}: generation after a {prefix.shape[1]}-step prime: first divergence min {min(first)}")
+
+
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16_valu", "gated_r64_w3_bf16"])
+def test_valu_unstaged_variant(fam):
+    """The general step kernels without LDS weight staging (the variant taken at one stream per
+    block or for wide layers), at a batch that would otherwise stage: teacher-forced logits and
+    generation against the oracle."""
+    cfg = FAMILIES[fam]
+    B = 11
+    w, fw, orc = build_pair(cfg, 106, B, fam=fam, path="step", valu_stage="0")
+    T = cfg.queue_total + 45
+    x = W.sequences(20, B, T)
+    err = row_rel_err(fw.teacher_forced(dev(x)).cpu().numpy(), orc.teacher_forced(x))
+    log(f"{fam} [{fw.regime}, unstaged]: TF max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+    check_generation(cfg, fw, orc, W.uniforms(21, B, T), B, fam + " unstaged")
 
 
 @pytest.mark.parametrize("fam", list(FAMILIES))
