@@ -10,7 +10,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libfwg.so")
 SOURCES = [os.path.join(CSRC, "fwg_host.cpp"), os.path.join(CSRC, "fwg_kernels.hip"),
-           os.path.join(CSRC, "fwg_mfma.hip"), os.path.join(CSRC, "fwg_parallel.hip")]
+           os.path.join(CSRC, "fwg_mfma.hip"), os.path.join(CSRC, "fwg_parallel.hip"),
+           os.path.join(CSRC, "fwg_wave.hip")]
 HEADERS = [os.path.join(ROOT, "include", "fwg.h"), os.path.join(CSRC, "fwg_internal.h"),
            os.path.join(CSRC, "fwg_sample.h")]
 

@@ -67,7 +67,49 @@ struct Plan {
   long long nv_nodes;            // layer nodes per sample: sum of nv_n[1..L]
   int nv_hc;                     // input-history capacity per stream (power of two >= receptive field)
   size_t off_nv, off_hist, off_ztop, off_nlogits;
+  // wave-per-stream family: the weight image
+  WaveArgs wave;
+  size_t off_wave;
 };
+
+// Layout of the wave family's weight image and per-wave scratch; false when the model does not fit
+// (every product at most 256 wide, K multiples of 4, pops of a step in 16 registers per lane, image
+// and four waves' scratch in 160 KB of LDS).
+bool wave_layout(const Plan &p, WaveArgs *g) {
+  const bool gated = p.kind == FWG_GATED;
+  const int C = p.C, S = p.S, H = p.H, Q = p.Q, L = p.L, w = p.w, Co = p.Co;
+  const int Ktop = gated ? H : C;
+  if (C % 4 || (gated && (S % 4 || H % 4)) || C > 256 || (gated && (S > 256 || H > 256)) || Q != 256) return false;
+  if (L * (w - 1) > 64 || (long long)L * (w - 1) * ((C + 63) / 64) > 16) return false;
+  auto r4 = [](long long n) { return (int)((n + 3) & ~3ll); };
+  long long o = 0;
+  auto take = [&](long long n) { const long long at = o; o += r4(n); return (int)at; };
+  g->o_emb = take((long long)Q * C);
+  g->o_embb = take(C);
+  g->o_layer = (int)o;
+  long long lo = 0;
+  auto ltake = [&](long long n) { const long long at = lo; lo += r4(n); return (int)at; };
+  ltake((long long)w * C * Co);
+  g->o_convb = ltake(Co);
+  g->o_res = gated ? ltake((long long)C * C) : 0;
+  g->o_resb = gated ? ltake(C) : 0;
+  g->o_skip = gated ? ltake((long long)C * S) : 0;
+  g->o_skipb = gated ? ltake(S) : 0;
+  g->layer_floats = (int)lo;
+  o += lo * L;
+  g->o_head = gated ? take((long long)S * H) : 0;
+  g->o_headb = gated ? take(H) : 0;
+  g->o_out = take((long long)Ktop * Q);
+  g->o_outb = take(Q);
+  g->image_floats = r4(o);
+  g->ain_floats = r4((long long)L * w * C);  // the layer inputs of every layer (pops land once per step)
+  g->c_floats = r4(C);
+  g->s_floats = gated ? r4(S) : 0;
+  g->h_floats = gated ? r4(H) : 0;
+  g->scr_floats = g->ain_floats + 2 * g->c_floats + 2 * g->s_floats + g->h_floats + r4(Q);
+  const long long bytes = 4ll * ((long long)g->image_floats + 4ll * g->scr_floats);
+  return o < (1ll << 30) && bytes <= 160 * 1024;
+}
 
 // Node sets of the tree of Fig. 1 for the output at offset 0: level L holds {0}; level l - 1 holds the
 // level-l offsets minus j d_l for j = 0 .. w - 1 (each distinct offset once).  Tables per level l >= 1:
@@ -153,11 +195,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
             kblock_ok(p->kind == FWG_GATED ? p->H : p->C, p->Q, kb);
   if (p->kind == FWG_GATED)
     ok = ok && kblock_ok(p->C, p->C, kb) && kblock_ok(p->C, p->S, kb) && kblock_ok(p->S, p->H, kb);
-  if (!ok)
-    return fail(FWG_EUNSUPPORTED,
-                "unsupported shape: every product needs K a multiple of %d, and an output width that "
-                "divides 256 (with K/%d divisible by 256/N) or is at least 256",
-                kb, kb);
+  const bool valu_ok = ok;
 
   // one layer's block for the general step kernels: conv | res | skip weights, then the biases
   {
@@ -180,7 +218,8 @@ int make_plan(const fwg_desc *d, Plan *p) {
   const int wf = (int)(p->valu_block / 4);
   int rpw = 0;
   bool stage = false;
-  for (int pass = 0; pass < 2 && rpw == 0; ++pass) {
+  p->lds_bytes = 0;
+  for (int pass = 0; pass < 2 && rpw == 0 && valu_ok; ++pass) {
     const bool st = pass == 0;
     if (st && !can_stage) continue;
     for (int r = rmax; r >= (st ? 2 : 1); r >>= 1) {
@@ -194,8 +233,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
       }
     }
   }
-  if (rpw == 0) return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS and registers");
-  p->rpw = rpw;
+  p->rpw = rpw > 0 ? rpw : 1;
   p->valu_wbytes = stage ? (int)p->valu_block : 0;
 
   // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512
@@ -205,6 +243,16 @@ int make_plan(const fwg_desc *d, Plan *p) {
                           p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
                           mfma_lds_bytes(p->L) <= 160 * 1024;
   if (mfma_shape && !(force && strcmp(force, "valu") == 0)) p->regime = REGIME_MFMA;
+  // small models whose weights all fit in LDS: one wavefront per stream
+  if (p->regime == REGIME_VALU && !(force && strcmp(force, "valu") == 0) && wave_layout(*p, &p->wave))
+    p->regime = REGIME_WAVE;
+  if (p->regime == REGIME_VALU && !valu_ok)
+    return fail(FWG_EUNSUPPORTED,
+                "unsupported shape: every product needs K a multiple of %d, and an output width that "
+                "divides 256 (with K/%d divisible by 256/N) or is at least 256",
+                kb, kb);
+  if (p->regime == REGIME_VALU && rpw == 0)
+    return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS and registers");
   p->brows = p->regime == REGIME_MFMA ? (p->bmax + kMfRows - 1) / kMfRows * kMfRows : p->bmax;
 
   // workspace layout
@@ -253,6 +301,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_ring_gen = take((size_t)acc * p->es);
   p->off_ring_tf = take((size_t)acc * p->es);
   p->off_last = take(sizeof(int32_t) * p->bmax);
+  p->off_wave = p->regime == REGIME_WAVE ? take(sizeof(float) * (size_t)p->wave.image_floats) : 0;
 
   // time-parallel path: every product's K must fill whole 128-byte k-tiles, and the gate's column
   // pairs come in groups of 16 channels
@@ -466,6 +515,20 @@ int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const 
   return FWG_OK;
 }
 
+// One step-kernel launch of the handle's kernel family.
+hipError_t launch_step(const fwg_handle *h, const StepArgs &a) {
+  const Plan &p = h->plan;
+  switch (p.regime) {
+    case REGIME_MFMA: return launch_mfma_step(a, h->stream);
+    case REGIME_WAVE: {
+      WaveArgs g = p.wave;
+      g.image = (const float *)(h->ws + p.off_wave);
+      return launch_wave_step(a, g, h->stream);
+    }
+    default: return launch_valu_step(a, p.rpw, p.lds_bytes, h->stream);
+  }
+}
+
 // Forced calls shorter than this run on the step kernels (one launch) instead of the
 // time-parallel path (a few launches per layer and chunk).
 constexpr int kParMinSteps = 16;
@@ -661,6 +724,32 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_repack(w->out, ws + p.off_out, REPACK_LINEAR, dt, Kout, p.Q, C, s));
   TRY_OR_FREE(launch_copy_bias(w->out_b, (float *)(ws + p.off_out_b), p.Q, s));
   TRY_OR_FREE(hipMemcpyAsync(ws + p.off_layers, table.data(), sizeof(LayerDev) * p.L, hipMemcpyHostToDevice, s));
+  if (p.regime == REGIME_WAVE) {
+    const WaveArgs &g = p.wave;
+    float *img = (float *)(ws + p.off_wave);
+    const int Ktop = p.kind == FWG_GATED ? p.H : C;
+    TRY_OR_FREE(launch_fill_zero(img, sizeof(float) * (size_t)g.image_floats, s));
+    TRY_OR_FREE(launch_wave_image(w->embed, img + g.o_emb, dt, C, p.Q, C, 0, s));
+    TRY_OR_FREE(launch_wave_vec(w->embed_b, img + g.o_embb, C, s));
+    for (int l = 0; l < p.L; ++l) {
+      float *blk = img + g.o_layer + (size_t)l * g.layer_floats;
+      TRY_OR_FREE(launch_wave_image(w->conv[l], blk, dt, p.Co, p.w * C, C, 1, s));
+      TRY_OR_FREE(launch_wave_vec(w->conv_b ? w->conv_b[l] : nullptr, blk + g.o_convb, p.Co, s));
+      if (p.kind == FWG_GATED) {
+        TRY_OR_FREE(launch_wave_image(w->res[l], blk + g.o_res, dt, C, C, C, 0, s));
+        TRY_OR_FREE(launch_wave_vec(w->res_b ? w->res_b[l] : nullptr, blk + g.o_resb, C, s));
+        TRY_OR_FREE(launch_wave_image(w->skip[l], blk + g.o_skip, dt, p.S, C, C, 0, s));
+        TRY_OR_FREE(launch_wave_vec(w->skip_b ? w->skip_b[l] : nullptr, blk + g.o_skipb, p.S, s));
+      }
+    }
+    if (p.kind == FWG_GATED) {
+      TRY_OR_FREE(launch_wave_image(w->head, img + g.o_head, dt, p.H, p.S, C, 0, s));
+      TRY_OR_FREE(launch_wave_vec(w->head_b, img + g.o_headb, p.H, s));
+    }
+    TRY_OR_FREE(launch_wave_image(w->out, img + g.o_out, dt, p.Q, Ktop, C, 0, s));
+    TRY_OR_FREE(launch_wave_vec(w->out_b, img + g.o_outb, p.Q, s));
+    TRY_OR_FREE(set_wave_lds_limit(sizeof(float) * ((size_t)g.image_floats + 4 * (size_t)g.scr_floats)));
+  }
   if (p.nv_ok)
     TRY_OR_FREE(hipMemcpyAsync(ws + p.off_nv, p.nv_host.data(), sizeof(int32_t) * p.nv_host.size(),
                                hipMemcpyHostToDevice, s));
@@ -734,7 +823,7 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
   a.n_steps = n_steps;
   a.batch = batch;
   a.mode = MODE_GENERATE;
-  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  HIP_TRY(launch_step(h, a));
   h->bound_batch = batch;
   h->t += n_steps;
   return FWG_OK;
@@ -757,7 +846,7 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
   a.n_steps = seq_len;
   a.batch = batch;
   a.mode = MODE_TEACHER;
-  HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream) : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+  HIP_TRY(launch_step(h, a));
   return FWG_OK;
 }
 
@@ -782,8 +871,7 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
     a.n_steps = n_steps;
     a.batch = batch;
     a.mode = MODE_ONLINE;
-    HIP_TRY(p.regime == REGIME_MFMA ? launch_mfma_step(a, h->stream)
-                                    : launch_valu_step(a, p.rpw, p.lds_bytes, h->stream));
+    HIP_TRY(launch_step(h, a));
   }
   h->bound_batch = batch;
   h->t += n_steps;
@@ -828,7 +916,11 @@ int fwg_destroy(fwg_handle *h) {
 
 const char *fwg_regime(const fwg_handle *h) {
   if (!h) return "";
-  return h->plan.regime == REGIME_MFMA ? "mfma_bf16_r64_s512" : "valu";
+  switch (h->plan.regime) {
+    case REGIME_MFMA: return "mfma_bf16_r64_s512";
+    case REGIME_WAVE: return "wave";
+    default: return "valu";
+  }
 }
 
 }  // extern "C"

@@ -65,9 +65,15 @@ FAMILIES = {
     "gated_r32_w3_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r64_w3_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
     "relures_c64_w4_bf16": W.ModelConfig(W.RELU_RESIDUAL, W.BF16, 64, (1, 4, 16, 2), filter_width=4),
+    # small enough for the wave-per-stream kernels (every weight in LDS)
+    "gated_r16_s32_f32": W.ModelConfig(W.GATED, W.F32, 16, (1, 2, 4, 8, 16, 32), 32, 32),
+    "relu_c32_bf16": W.ModelConfig(W.RELU, W.BF16, 32, (1, 2, 4, 8, 16, 3)),
+    "relu_c32_f32_valu": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
 }
-# families whose test forces the general (VALU) kernel family instead of the MFMA one
-FORCE_VALU = {"gated_r64_bf16_valu"}
+# families that must run on the wave-per-stream kernels
+WAVE_FAMILIES = {"relu_c32_f32", "relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16"}
+# families whose test forces the general (VALU) kernel family instead of the MFMA or wave one
+FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu"}
 
 
 def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_rows=None, valu_stage=None):
@@ -93,8 +99,14 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, path=None, par_ro
     if fam is not None:
         mfma_shape = (cfg.kind == W.GATED and cfg.dtype == W.BF16 and cfg.channels == 64 and
                       cfg.skip_channels == 512 and cfg.head_channels == 512 and cfg.filter_width == 2)
-        want_valu = fam in FORCE_VALU or not mfma_shape
-        assert (fw.regime == "valu") == want_valu, (fam, fw.regime)
+        if fam in FORCE_VALU:
+            assert fw.regime == "valu", (fam, fw.regime)
+        elif mfma_shape:
+            assert fw.regime.startswith("mfma"), (fam, fw.regime)
+        else:
+            assert fw.regime in ("valu", "wave"), (fam, fw.regime)
+        if fam in WAVE_FAMILIES:
+            assert fw.regime == "wave", (fam, fw.regime)
     return w, fw, oracle.Oracle(w)
 
 
@@ -215,7 +227,7 @@ def test_prime_then_generate(fam):
     log(f"{fam}: generation after a {prefix.shape[1]}-step prime: first divergence min {min(first)}")
 
 
-@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16_valu", "gated_r64_w3_bf16"])
+@pytest.mark.parametrize("fam", ["relu_c32_f32_valu", "gated_r32_f32", "gated_r64_bf16_valu", "gated_r64_w3_bf16"])
 def test_valu_unstaged_variant(fam):
     """The general step kernels without LDS weight staging (the variant taken at one stream per
     block or for wide layers), at a batch that would otherwise stage: teacher-forced logits and
@@ -240,7 +252,7 @@ def test_generation_parity(fam):
     check_generation(cfg, fw, orc, W.uniforms(4, B, n), B, fam)
 
 
-@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu",
+@pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r16_s32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu",
                                  "gated_r64_w3_bf16"])
 def test_online_prediction_parity(fam):
     """Online prediction (fwg_step_forced): generate, feed observed samples from the same queues,
