@@ -7,9 +7,10 @@ pushes its new states.  The timed region is one fwg_generate call of --steps
 steps (a single persistent kernel launch), bracketed by device synchronisation
 and HIP events recorded on the launch stream, with inputs resident in HBM.
 
---mode teacher_forced times one fwg_teacher_forced call over the same batch and
-number of steps instead (a seeded random input sequence, logits for every step;
-the library evaluates it time-parallel), against the oracle's teacher-forced pass.
+--mode teacher_forced times one teacher-forced call over the same batch and number
+of steps instead (a seeded random input sequence, logits for every step): the
+time-parallel fwg_teacher_forced_parallel, or with --tf-path step the step kernels
+(fwg_teacher_forced), against the oracle's teacher-forced pass.
 
 --mode naive_vs_fast runs the paper's timing experiment (Section 3.2): models of
 2 blocks of L layers (dilations 1 .. 2^(L-1) per block), L = 1 .. 12, one stream,
@@ -118,13 +119,14 @@ def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
     x_host = W.sequences(wl.uniform_seed, B, max(K, Wu, 1))
     x = torch.from_numpy(np.ascontiguousarray(x_host[:, :K])).cuda()
     logits = torch.empty((B, K, cfg.n_classes), dtype=torch.float32, device="cuda")
+    call = fw.teacher_forced if args.tf_path == "step" else fw.teacher_forced_parallel
     if Wu > 0:
-        fw.teacher_forced(torch.from_numpy(np.ascontiguousarray(x_host[:, :Wu])).cuda())
+        call(torch.from_numpy(np.ascontiguousarray(x_host[:, :Wu])).cuda())
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     w0 = time.perf_counter()
     e0.record(stream)
-    fw.teacher_forced(x, out=logits)
+    call(x, out=logits)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -149,7 +151,8 @@ def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
         "dtype": dtype,
         "data": "synthetic",
         "config": {"workload": name, "description": wl.description, "batch": B, "seq_len": K,
-                   "mode": "teacher_forced", "path": os.environ.get("FWG_FORCED_PATH", "library default")},
+                   "mode": "teacher_forced",
+                   "path": "step kernels" if args.tf_path == "step" else "time-parallel"},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": None, "scope": "whole call (all kernels)",
                      "algorithmic_flops_per_call": flops, "call_ms": ms},
@@ -222,6 +225,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-time budget of the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["generate", "teacher_forced", "naive_vs_fast"], default="generate")
+    ap.add_argument("--tf-path", choices=["parallel", "step"], default="parallel",
+                    help="teacher_forced mode: time-parallel kernels or the step kernels")
     ap.add_argument("--naive-samples", type=int, default=50, help="samples per timed call (naive_vs_fast)")
     ap.add_argument("--repeats", type=int, default=100, help="timed calls averaged (naive_vs_fast)")
     ap.add_argument("--max-blocks-layers", type=int, default=12, help="largest L of the sweep (naive_vs_fast)")

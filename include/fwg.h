@@ -152,11 +152,10 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
 
 /* Teacher-forced evaluation from zero queues: logits[b][t][:] is the output
  * after consuming inputs[b][0..t].  inputs: DEVICE int32 [batch][seq_len];
- * logits: DEVICE float32 [batch][seq_len][n_classes].  Sequences of 16 steps
- * or more are evaluated time-parallel (each layer as one dilated convolution
- * over the sequence, Section 1), shorter ones by the step kernels with the
- * input taken from `inputs`; either way the call uses queues of its own and
- * leaves the generation state untouched.
+ * logits: DEVICE float32 [batch][seq_len][n_classes].  Runs the generation
+ * step kernels in forced mode (the input of each step taken from `inputs`
+ * instead of the previous sample), so the logits check the hot path itself;
+ * uses queues of its own and leaves the generation state untouched.
  * 1 <= batch <= max_batch; seq_len == 0 is a no-op. */
 int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
 
@@ -170,14 +169,28 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
  * inputs[b][s] becomes the pending input.  Queues and t advance exactly as in
  * fwg_generate, so generation and online prediction may alternate freely.
  * inputs: DEVICE int32 [batch][n_steps], each in [0, n_classes);
- * logits: DEVICE float32 [batch][n_steps][n_classes], or NULL to only advance
- * the state (priming the queues from a prefix before generating).  Batch
- * binding and the FWG_ESTATE rule as in fwg_generate; n_steps == 0 is a no-op.
- * Long stretches are evaluated time-parallel, every layer as one dilated
- * convolution over the stretch (the training-time view of the network,
- * Section 1), reading the states before the stretch from the queues and leaving
- * in each queue the newest d_l states, as the step-by-step loop would. */
+ * logits: DEVICE float32 [batch][n_steps][n_classes], or NULL when only the
+ * state should advance.  Runs the generation step kernels.  Batch binding and
+ * the FWG_ESTATE rule as in fwg_generate; n_steps == 0 is a no-op. */
 int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
+
+/* Time-parallel evaluation (the training-time view of the network, Section 1):
+ * with every input known, each layer is one width-w dilated convolution over
+ * the whole sequence, computed as matrix-core GEMMs over (stream, time) rows in
+ * chunks of steps, the states before a chunk read from the layer's queue.
+ * fwg_teacher_forced_parallel has the contract and results of
+ * fwg_teacher_forced (queues of its own, from zero; generation state untouched);
+ * only the order of the float32 sums differs.  FWG_EUNSUPPORTED when the model's
+ * products do not fill whole 128-byte k-tiles. */
+int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
+
+/* Priming from a prefix, time-parallel: the contract of fwg_step_forced
+ * (online prediction continuing from the generation state; logits may be NULL),
+ * evaluated like fwg_teacher_forced_parallel.  After each layer of a chunk the
+ * chunk's newest (w-1) d_l states replace the queue's contents, so the queues
+ * end in the state the step-by-step loop would leave and generation continues
+ * from the prefix.  FWG_EUNSUPPORTED as fwg_teacher_forced_parallel. */
+int fwg_prime(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
 
 /* Naive generation, the baseline the paper measures against (Section 1, Fig. 1;
  * Section 3): every sample recomputes, from the last receptive-field inputs, each

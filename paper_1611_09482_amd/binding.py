@@ -16,8 +16,8 @@ _STATUS = {FWG_EINVAL: "EINVAL", FWG_ENOSPACE: "ENOSPACE", FWG_EHIP: "EHIP", FWG
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfwg.so")
 
 EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-            "fwg_step_forced", "fwg_generate_naive", "fwg_naive_nodes", "fwg_destroy", "fwg_last_error",
-            "fwg_regime"]
+            "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive", "fwg_naive_nodes",
+            "fwg_destroy", "fwg_last_error", "fwg_regime"]
 
 
 class FwgError(RuntimeError):
@@ -63,6 +63,8 @@ def load_library(path: Optional[str] = None):
     L.fwg_generate.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_teacher_forced.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_step_forced.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_teacher_forced_parallel.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_prime.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_generate_naive.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_naive_nodes.argtypes = [ctypes.POINTER(fwg_desc), ctypes.POINTER(ctypes.c_int64)]
     L.fwg_destroy.argtypes = [vp]
@@ -70,7 +72,8 @@ def load_library(path: Optional[str] = None):
     L.fwg_regime.argtypes = [vp]
     L.fwg_regime.restype = ctypes.c_char_p
     for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
-                 "fwg_step_forced", "fwg_generate_naive", "fwg_naive_nodes", "fwg_destroy"]:
+                 "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive",
+                 "fwg_naive_nodes", "fwg_destroy"]:
         getattr(L, name).restype = ctypes.c_int
     if path is None:
         _lib = L
@@ -199,13 +202,25 @@ class FastWavenet:
         _check(self.lib.fwg_generate_naive(self.handle, B, n, uniforms.data_ptr(), out.data_ptr()))
         return out
 
-    def prime(self, inputs):
-        """Advance the state over observed samples without computing logits (fwg_step_forced with
-        logits = NULL): a prefix to continue generating from."""
+    def teacher_forced_parallel(self, inputs, out=None):
+        """Time-parallel teacher forcing (same contract as teacher_forced)."""
+        torch = self._torch
+        assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
+        B, T = inputs.shape
+        if out is None:
+            out = torch.empty((B, T, self.n_classes), dtype=torch.float32, device=inputs.device)
+        _check(self.lib.fwg_teacher_forced_parallel(self.handle, B, T, inputs.data_ptr(), out.data_ptr()))
+        return out
+
+    def prime(self, inputs, logits: bool = False):
+        """Time-parallel online prediction / priming from the current state (fwg_prime): the state
+        advances over the observed samples; returns the logits when asked for, else None."""
         torch = self._torch
         assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
         B, n = inputs.shape
-        _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), None))
+        out = torch.empty((B, n, self.n_classes), dtype=torch.float32, device=inputs.device) if logits else None
+        _check(self.lib.fwg_prime(self.handle, B, n, inputs.data_ptr(), None if out is None else out.data_ptr()))
+        return out
 
     def close(self):
         if getattr(self, "handle", None):

@@ -54,7 +54,6 @@ struct Plan {
   size_t lds_bytes;
   // time-parallel path (forced sequences): operand-typed [N][K] weights and chunk buffers
   bool par_ok;
-  bool par_force;         // every forced call takes the time-parallel path (else from kParMinSteps steps)
   int par_tc;             // steps per chunk; a chunk holds brows * par_tc rows at most
   std::vector<size_t> off_pconv, off_pconv_b, off_pres;
   size_t off_pskip, off_pskip_b, off_phead, off_pout;
@@ -309,9 +308,6 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->par_ok = p->C % kt == 0 && (p->kind != FWG_GATED ||
                                  (p->C % 16 == 0 && ((long long)p->L * p->C) % kt == 0 && p->S % kt == 0 &&
                                   p->H % kt == 0));
-  const char *pf = getenv("FWG_FORCED_PATH");
-  if (pf && strcmp(pf, "step") == 0) p->par_ok = false;
-  p->par_force = pf && strcmp(pf, "parallel") == 0;
   p->par_tc = 0;
   if (p->par_ok) {
     const bool gated = p->kind == FWG_GATED;
@@ -527,14 +523,6 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a) {
     }
     default: return launch_valu_step(a, p.rpw, p.lds_bytes, h->stream);
   }
-}
-
-// Forced calls shorter than this run on the step kernels (one launch) instead of the
-// time-parallel path (a few launches per layer and chunk).
-constexpr int kParMinSteps = 16;
-
-bool use_parallel(const fwg_handle *h, int n_steps) {
-  return h->plan.par_ok && (h->plan.par_force || n_steps >= kParMinSteps);
 }
 
 // Time-parallel evaluation of a forced sequence, chunk by chunk (MODE_TEACHER or MODE_ONLINE):
@@ -837,7 +825,6 @@ int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int3
   if (seq_len == 0) return FWG_OK;
   if (!inputs || !logits) return fail(FWG_EINVAL, "inputs and logits are required");
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_tf, (size_t)p.queue_elems * p.es, h->stream));
-  if (use_parallel(h, seq_len)) return par_forward(h, MODE_TEACHER, batch, seq_len, inputs, logits, h->ws + p.off_ring_tf, 0);
   StepArgs a = base_args(h);
   a.ring = h->ws + p.off_ring_tf;
   a.inputs = inputs;
@@ -859,20 +846,48 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
     return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
   if (n_steps == 0) return FWG_OK;
   if (!inputs) return fail(FWG_EINVAL, "inputs are required");
-  if (use_parallel(h, n_steps)) {
-    const int rc = par_forward(h, MODE_ONLINE, batch, n_steps, inputs, logits, h->ws + p.off_ring_gen, h->t);
-    if (rc != FWG_OK) return rc;
-  } else {
-    StepArgs a = base_args(h);
-    a.ring = h->ws + p.off_ring_gen;
-    a.inputs = inputs;
-    a.logits = logits;
-    a.t0 = h->t;
-    a.n_steps = n_steps;
-    a.batch = batch;
-    a.mode = MODE_ONLINE;
-    HIP_TRY(launch_step(h, a));
-  }
+  StepArgs a = base_args(h);
+  a.ring = h->ws + p.off_ring_gen;
+  a.inputs = inputs;
+  a.logits = logits;
+  a.t0 = h->t;
+  a.n_steps = n_steps;
+  a.batch = batch;
+  a.mode = MODE_ONLINE;
+  HIP_TRY(launch_step(h, a));
+  h->bound_batch = batch;
+  h->t += n_steps;
+  return FWG_OK;
+}
+
+int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits) {
+  if (!h) return fail(FWG_EINVAL, "handle is NULL");
+  const Plan &p = h->plan;
+  if (!p.par_ok)
+    return fail(FWG_EUNSUPPORTED, "no time-parallel kernels for this model (every product's K must fill whole "
+                                  "128-byte tiles)");
+  if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
+  if (seq_len < 0) return fail(FWG_EINVAL, "seq_len < 0");
+  if (seq_len == 0) return FWG_OK;
+  if (!inputs || !logits) return fail(FWG_EINVAL, "inputs and logits are required");
+  HIP_TRY(launch_fill_zero(h->ws + p.off_ring_tf, (size_t)p.queue_elems * p.es, h->stream));
+  return par_forward(h, MODE_TEACHER, batch, seq_len, inputs, logits, h->ws + p.off_ring_tf, 0);
+}
+
+int fwg_prime(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits) {
+  if (!h) return fail(FWG_EINVAL, "handle is NULL");
+  const Plan &p = h->plan;
+  if (!p.par_ok)
+    return fail(FWG_EUNSUPPORTED, "no time-parallel kernels for this model (every product's K must fill whole "
+                                  "128-byte tiles)");
+  if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
+  if (n_steps < 0) return fail(FWG_EINVAL, "n_steps < 0");
+  if (h->bound_batch >= 0 && h->bound_batch != batch)
+    return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
+  if (n_steps == 0) return FWG_OK;
+  if (!inputs) return fail(FWG_EINVAL, "inputs are required");
+  const int rc = par_forward(h, MODE_ONLINE, batch, n_steps, inputs, logits, h->ws + p.off_ring_gen, h->t);
+  if (rc != FWG_OK) return rc;
   h->bound_batch = batch;
   h->t += n_steps;
   return FWG_OK;

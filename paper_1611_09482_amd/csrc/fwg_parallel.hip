@@ -19,8 +19,8 @@
 //   par_gemm_kernel   C[m][n] = A[m][:] . W[n][:] with a row-gathering prologue
 //                     (plain rows, or the two taps of the dilated convolution)
 //                     and an epilogue per layer kind (relu, relu + residual,
-//                     gate, residual add, logits).  64 x 64 tiles, 4 waves of
-//                     32 x 32, operands staged through LDS in 128-byte k-tiles,
+//                     gate, residual add, logits).  64 x 64 or 128 x 128 tiles,
+//                     4 waves, operands staged through LDS in 128-byte k-tiles,
 //                     MFMA 16x16x32 bf16 or 16x16x4 f32 with fp32 accumulation.
 //   par_embed_kernel  x^0 rows: the 1x1 convolution of the one-hot input (a row
 //                     gather), from the forced sequence or the pending input.
@@ -42,7 +42,7 @@ namespace par {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 64, BN = 64, NT = 256;
+constexpr int NT = 256;
 constexpr int KT_BYTES = 128;            // bytes of one row inside a k-tile
 constexpr int ROWB = KT_BYTES + 16;      // LDS row stride (padding spreads the rows over banks)
 
@@ -133,90 +133,103 @@ __device__ __forceinline__ uint4 load_w(const ParGemm &g, int n, int k) {
   return *(const uint4 *)((const OT *)g.W + (long long)n * g.K + k);
 }
 
-template <typename OT, int AM, int EM>
+// Tile (64 TM) x (64 TM): 4 waves in 2 x 2, each (32 TM) x (32 TM) = (2 TM) x (2 TM) MFMA tiles.
+// TM = 2 for outputs at least 128 wide (more MFMAs per staged byte), else 1.
+template <typename OT, int AM, int EM, int TM>
 __global__ void __launch_bounds__(NT) par_gemm_kernel(ParGemm g) {
-  __shared__ __attribute__((aligned(16))) unsigned char lds_a[BM * ROWB];
-  __shared__ __attribute__((aligned(16))) unsigned char lds_b[BN * ROWB];
+  constexpr int TB = 64 * TM, TW = 32 * TM, MT = 2 * TM;
+  __shared__ __attribute__((aligned(16))) unsigned char lds_a[TB * ROWB];
+  __shared__ __attribute__((aligned(16))) unsigned char lds_b[TB * ROWB];
   constexpr int KT = Op<OT>::KT;
   constexpr int EPC = 16 / sizeof(OT);  // elements per 16-byte chunk
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wm = w & 1, wn = w >> 1;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
-  // staging: thread -> (row, 16-byte chunk) for rows r and r + 32
+  const int m0 = blockIdx.x * TB, n0 = blockIdx.y * TB;
+  // staging: thread -> (row sr + 32 i, 16-byte chunk sq)
   const int sr = tid >> 3, sq = tid & 7;
 
-  f32x4 acc[2][2];
+  f32x4 acc[MT][MT];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < MT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = g.K / KT;
-  uint4 ra0 = load_a<OT, AM>(g, m0 + sr, sq * EPC), ra1 = load_a<OT, AM>(g, m0 + sr + 32, sq * EPC);
-  uint4 rb0 = load_w<OT>(g, n0 + sr, sq * EPC), rb1 = load_w<OT>(g, n0 + sr + 32, sq * EPC);
+  uint4 ra[MT], rb[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    ra[i] = load_a<OT, AM>(g, m0 + sr + 32 * i, sq * EPC);
+    rb[i] = load_w<OT>(g, n0 + sr + 32 * i, sq * EPC);
+  }
   const int lr = lane & 15, lg = lane >> 4;
   for (int kt = 0; kt < nk; ++kt) {
-    *(uint4 *)(lds_a + sr * ROWB + sq * 16) = ra0;
-    *(uint4 *)(lds_a + (sr + 32) * ROWB + sq * 16) = ra1;
-    *(uint4 *)(lds_b + sr * ROWB + sq * 16) = rb0;
-    *(uint4 *)(lds_b + (sr + 32) * ROWB + sq * 16) = rb1;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      *(uint4 *)(lds_a + (sr + 32 * i) * ROWB + sq * 16) = ra[i];
+      *(uint4 *)(lds_b + (sr + 32 * i) * ROWB + sq * 16) = rb[i];
+    }
     __syncthreads();
     if (kt + 1 < nk) {
       const int k = (kt + 1) * KT + sq * EPC;
-      ra0 = load_a<OT, AM>(g, m0 + sr, k);
-      ra1 = load_a<OT, AM>(g, m0 + sr + 32, k);
-      rb0 = load_w<OT>(g, n0 + sr, k);
-      rb1 = load_w<OT>(g, n0 + sr + 32, k);
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        ra[i] = load_a<OT, AM>(g, m0 + sr + 32 * i, k);
+        rb[i] = load_w<OT>(g, n0 + sr + 32 * i, k);
+      }
     }
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      uint4 a[2], b[2];
+      uint4 av[MT], bv[MT];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        a[i] = *(const uint4 *)(lds_a + (32 * wm + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
-        b[i] = *(const uint4 *)(lds_b + (32 * wn + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+      for (int i = 0; i < MT; ++i) {
+        av[i] = *(const uint4 *)(lds_a + (TW * wm + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+        bv[i] = *(const uint4 *)(lds_b + (TW * wn + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
       }
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < MT; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = Op<OT>::mma(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < MT; ++j) acc[i][j] = Op<OT>::mma(av[i], bv[j], acc[i][j]);
     }
     __syncthreads();
   }
 
-  // epilogue: acc[i][j][e] is row 32 wm + 16 i + 4 lg + e, column 32 wn + 16 j + lr of the tile
+  // epilogue: acc[i][j][e] is row TW wm + 16 i + 4 lg + e, column TW wn + 16 j + lr of the tile
   if (EM == E_GATE) {
-    // columns come in groups of 32: 16 tanh columns, then the 16 sigmoid columns of the same channels
-    const int grp = (n0 + 32 * wn) >> 5;
-    if (32 * grp >= g.N) return;
-    const int ch = 16 * grp + lr;
-    const float bt = g.bias[32 * grp + lr], bs = g.bias[32 * grp + 16 + lr];
+    // columns come in groups of 32: 16 tanh columns, then the 16 sigmoid columns of the same
+    // channels; the wave's TM groups are its MFMA column tiles (2 q, 2 q + 1)
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int q = 0; q < TM; ++q) {
+      const int grp = (n0 + TW * wn) / 32 + q;
+      if (32 * grp >= g.N) continue;
+      const int ch = 16 * grp + lr;
+      const float bt = g.bias[32 * grp + lr], bs = g.bias[32 * grp + 16 + lr];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int m = m0 + 32 * wm + 16 * i + 4 * lg + e;
-        if (m < g.M) {
-          const float z = tanhf(acc[i][0][e] + bt) * sigmoid(acc[i][1][e] + bs);
-          Op<OT>::put(g.oout, (long long)m * g.ldo + g.zoff + ch, z);
-          if (AM == A_TREE && g.ztop) {
-            const int b = m / g.Tcur;
-            if (m - b * g.Tcur == g.Tcur - 1) Op<OT>::put(g.ztop, (long long)b * g.ldo + g.zoff + ch, z);
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int m = m0 + TW * wm + 16 * i + 4 * lg + e;
+          if (m < g.M) {
+            const float z = tanhf(acc[i][2 * q][e] + bt) * sigmoid(acc[i][2 * q + 1][e] + bs);
+            Op<OT>::put(g.oout, (long long)m * g.ldo + g.zoff + ch, z);
+            if (AM == A_TREE && g.ztop) {
+              const int b = m / g.Tcur;
+              if (m - b * g.Tcur == g.Tcur - 1) Op<OT>::put(g.ztop, (long long)b * g.ldo + g.zoff + ch, z);
+            }
           }
         }
-      }
+    }
     return;
   }
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + 32 * wn + 16 * j + lr;
+  for (int j = 0; j < MT; ++j) {
+    const int n = n0 + TW * wn + 16 * j + lr;
     if (n >= g.N) continue;
     const float bn = g.bias[n];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int m = m0 + 32 * wm + 16 * i + 4 * lg + e;
+        const int m = m0 + TW * wm + 16 * i + 4 * lg + e;
         if (m >= g.M) continue;
         const float v = acc[i][j][e] + bn;
         if (EM == E_RELU) {
@@ -239,17 +252,28 @@ __global__ void __launch_bounds__(NT) par_gemm_kernel(ParGemm g) {
   }
 }
 
-template <typename OT, int AM>
-static hipError_t launch_em(const ParGemm &g, int em, dim3 grid, hipStream_t s) {
+template <typename OT, int AM, int TM>
+static hipError_t launch_em_t(const ParGemm &g, int em, dim3 grid, hipStream_t s) {
   switch (em) {
-    case E_RELU: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU>), grid, dim3(NT), 0, s, g); break;
-    case E_RELU_RES: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU_RES>), grid, dim3(NT), 0, s, g); break;
-    case E_RES_ADD: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RES_ADD>), grid, dim3(NT), 0, s, g); break;
-    case E_GATE: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_GATE>), grid, dim3(NT), 0, s, g); break;
-    case E_LOGITS: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_LOGITS>), grid, dim3(NT), 0, s, g); break;
+    case E_RELU: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU, TM>), grid, dim3(NT), 0, s, g); break;
+    case E_RELU_RES: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RELU_RES, TM>), grid, dim3(NT), 0, s, g); break;
+    case E_RES_ADD: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_RES_ADD, TM>), grid, dim3(NT), 0, s, g); break;
+    case E_GATE: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_GATE, TM>), grid, dim3(NT), 0, s, g); break;
+    case E_LOGITS: hipLaunchKernelGGL((par_gemm_kernel<OT, AM, E_LOGITS, TM>), grid, dim3(NT), 0, s, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// 128-wide tiles for outputs at least 128 wide over at least 4096 rows, else 64-wide tiles
+template <typename OT, int AM>
+static hipError_t launch_em(const ParGemm &g, int em, hipStream_t s) {
+  if (g.N >= 128 && g.M >= 4096) {
+    const dim3 grid((g.M + 127) / 128, (g.N + 127) / 128);
+    return launch_em_t<OT, AM, 2>(g, em, grid, s);
+  }
+  const dim3 grid((g.M + 63) / 64, (g.N + 63) / 64);
+  return launch_em_t<OT, AM, 1>(g, em, grid, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -361,15 +385,14 @@ static int grid_for(long long total) {
 
 hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s) {
   if (g.M <= 0) return hipSuccess;
-  const dim3 grid((g.M + par::BM - 1) / par::BM, (g.N + par::BN - 1) / par::BN);
   if (dtype == 1) {
-    if (amode == par::A_CONV) return par::launch_em<uint16_t, par::A_CONV>(g, emode, grid, s);
-    if (amode == par::A_TREE) return par::launch_em<uint16_t, par::A_TREE>(g, emode, grid, s);
-    return par::launch_em<uint16_t, par::A_PLAIN>(g, emode, grid, s);
+    if (amode == par::A_CONV) return par::launch_em<uint16_t, par::A_CONV>(g, emode, s);
+    if (amode == par::A_TREE) return par::launch_em<uint16_t, par::A_TREE>(g, emode, s);
+    return par::launch_em<uint16_t, par::A_PLAIN>(g, emode, s);
   }
-  if (amode == par::A_CONV) return par::launch_em<float, par::A_CONV>(g, emode, grid, s);
-  if (amode == par::A_TREE) return par::launch_em<float, par::A_TREE>(g, emode, grid, s);
-  return par::launch_em<float, par::A_PLAIN>(g, emode, grid, s);
+  if (amode == par::A_CONV) return par::launch_em<float, par::A_CONV>(g, emode, s);
+  if (amode == par::A_TREE) return par::launch_em<float, par::A_TREE>(g, emode, s);
+  return par::launch_em<float, par::A_PLAIN>(g, emode, s);
 }
 
 hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {

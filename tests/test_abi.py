@@ -95,6 +95,8 @@ def test_null_arguments(lib):
     assert lib.fwg_teacher_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_step_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_generate_naive(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_teacher_forced_parallel(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_prime(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_naive_nodes(ctypes.byref(d), None) == B.FWG_EINVAL
     assert lib.fwg_destroy(None) == B.FWG_OK
     assert lib.fwg_regime(None) == b""
