@@ -566,16 +566,24 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
       g.w = p.w; g.depth = (p.w - 1) * h->dil[l];
       g.W = ws + p.off_pconv[l];
       g.bias = (const float *)(ws + p.off_pconv_b[l]);
-      int em;
-      if (gated) {
+      int em = PAR_E_GATE;
+      const bool fused = gated && par_gated_layer_ok(C, p.dtype);
+      if (fused) {
+        // dilated product, gate, z rows and residual 1x1 in one kernel
+        g.zout = ws + p.off_pz; g.ldz = (long long)L * C; g.zoff = l * C;
+        g.W2 = ws + p.off_pres[l];
+        g.bias2 = (const float *)(ws + p.off_res_b[l]);
+        g.xres = px[cur]; g.xout = px[nxt]; g.oout = opnd_copy ? pxb[nxt] : nullptr; g.ldo = C;
+        HIP_TRY(launch_par_gated_layer(g, p.dtype, s));
+      } else if (gated) {
         em = PAR_E_GATE; g.oout = ws + p.off_pz; g.ldo = (long long)L * C; g.zoff = l * C;
       } else if (p.kind == FWG_RELU) {
         em = PAR_E_RELU; g.oout = pxb[nxt]; g.ldo = C;
       } else {
         em = PAR_E_RELU_RES; g.xres = px[cur]; g.xout = px[nxt]; g.oout = opnd_copy ? pxb[nxt] : nullptr; g.ldo = C;
       }
-      HIP_TRY(launch_par_gemm(g, p.dtype, PAR_A_CONV, em, s));
-      if (gated && l + 1 < L) {  // the last layer's residual output feeds nothing
+      if (!fused) HIP_TRY(launch_par_gemm(g, p.dtype, PAR_A_CONV, em, s));
+      if (gated && !fused && l + 1 < L) {  // the last layer's residual output feeds nothing
         ParGemm r;
         memset(&r, 0, sizeof(r));
         r.M = M; r.N = C; r.K = C; r.Tcur = Tcur;

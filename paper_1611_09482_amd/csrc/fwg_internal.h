@@ -191,6 +191,11 @@ struct ParGemm {
   int nprev;
   long long tnow;
   void *ztop;              // gate in tree mode: z of the node at offset 0 (i = Tcur - 1) also to ztop[b][zoff + c]
+  // fused gated layer (launch_par_gated_layer): residual 1x1 weights [R][R] and bias, and the z rows
+  const void *W2;
+  const float *bias2;
+  void *zout;
+  long long ldz;
 };
 struct ParEmbed {
   int M, C, Tcur, mode;
@@ -219,6 +224,11 @@ enum ParAMode { PAR_A_PLAIN = 0, PAR_A_CONV = 1, PAR_A_TREE = 2 };
 enum ParEMode { PAR_E_RELU = 0, PAR_E_RELU_RES = 1, PAR_E_RES_ADD = 2, PAR_E_GATE = 3, PAR_E_LOGITS = 4 };
 constexpr int kParKTileBytes = 128;  // K of every product must be a multiple of 128 bytes of operands
 hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hipStream_t s);
+// One gated layer over a chunk: dilated product (A gathered as in PAR_A_CONV), gate, z rows out,
+// residual 1x1 and add.  Needs R in {32, 64} with R operands filling at most one 128-byte k-tile
+// (par_gated_layer_ok).
+bool par_gated_layer_ok(int R, int dtype);
+hipError_t launch_par_gated_layer(const ParGemm &g, int dtype, hipStream_t s);
 hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s);
 hipError_t launch_par_ring(const ParRing &r, hipStream_t s);
 hipError_t launch_par_set_last(const int32_t *inputs, int32_t *last, int batch, int n_steps, hipStream_t s);

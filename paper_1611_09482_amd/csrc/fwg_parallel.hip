@@ -277,6 +277,178 @@ static hipError_t launch_em(const ParGemm &g, int em, hipStream_t s) {
 }
 
 // ---------------------------------------------------------------------------
+// One gated layer over a block of 64 rows: conv (all 2R outputs, interleaved tanh / sigmoid
+// groups), gate, residual 1x1 from LDS, add.  Every global access is a 16-byte-per-lane row
+// access: the residual input rows are loaded during the conv, and the z, x and operand-x rows are
+// assembled in LDS and stored whole.
+template <typename OT, int RT>
+__global__ void __launch_bounds__(NT) par_gated_layer_kernel(ParGemm g) {
+  constexpr int R = 16 * RT, CO = 2 * R;
+  constexpr int XROW = R * 4 + 16;  // LDS stride of a float32 x row
+  // conv staging (A, W), later reused for the x rows
+  constexpr int STAGE_BYTES = (64 + CO) * ROWB > 64 * XROW ? (64 + CO) * ROWB : 64 * XROW;
+  __shared__ __attribute__((aligned(16))) unsigned char lds_s[STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char lds_z[64 * ROWB];
+  __shared__ __attribute__((aligned(16))) unsigned char lds_r[R * ROWB];
+  unsigned char *lds_a = lds_s, *lds_b = lds_s + 64 * ROWB, *lds_x = lds_s;
+  constexpr int KT = Op<OT>::KT;
+  constexpr int EPC = 16 / sizeof(OT);
+  constexpr int ZB = R * (int)sizeof(OT);  // bytes of a z row (<= 128)
+  constexpr int XC = R * 4 / 16;           // 16-byte chunks of a float32 x row
+  constexpr int XPT = 64 * XC / NT;        // x chunks per thread
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wm = w & 1, wn = w >> 1;
+  const int m0 = blockIdx.x * 64;
+  const int sr = tid >> 3, sq = tid & 7;
+  const int lr = lane & 15, lg = lane >> 4;
+
+  // residual weights [R][R] (one k-tile): rows sr + 32 i
+#pragma unroll
+  for (int i = 0; i < (R + 31) / 32; ++i) {
+    const int n = sr + 32 * i;
+    if (n < R) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (sq * 16 < ZB) v = *(const uint4 *)((const OT *)g.W2 + (long long)n * R + sq * EPC);
+      *(uint4 *)(lds_r + n * ROWB + sq * 16) = v;
+    }
+  }
+  // the residual input rows, in flight during the conv: chunk c of the tile = row c / XC, piece c % XC
+  uint4 xin[XPT];
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int c = tid + NT * i, r = c / XC, q = c % XC, m = m0 + r;
+    xin[i] = m < g.M ? *(const uint4 *)(g.xres + (long long)m * g.ldo + 4 * q) : make_uint4(0, 0, 0, 0);
+  }
+
+  // ---- dilated product: 64 rows x CO columns; wave (wm, wn): rows 32 wm.., columns (CO / 2) wn..
+  f32x4 acc[2][RT];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < RT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int nk = g.K / KT;
+  constexpr int WR = CO / 32;  // W staging rows per thread
+  uint4 ra[2], rb[WR];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) ra[i] = load_a<OT, A_CONV>(g, m0 + sr + 32 * i, sq * EPC);
+#pragma unroll
+  for (int i = 0; i < WR; ++i) rb[i] = load_w<OT>(g, sr + 32 * i, sq * EPC);
+  for (int kt = 0; kt < nk; ++kt) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) *(uint4 *)(lds_a + (sr + 32 * i) * ROWB + sq * 16) = ra[i];
+#pragma unroll
+    for (int i = 0; i < WR; ++i) *(uint4 *)(lds_b + (sr + 32 * i) * ROWB + sq * 16) = rb[i];
+    __syncthreads();
+    if (kt + 1 < nk) {
+      const int k = (kt + 1) * KT + sq * EPC;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) ra[i] = load_a<OT, A_CONV>(g, m0 + sr + 32 * i, k);
+#pragma unroll
+      for (int i = 0; i < WR; ++i) rb[i] = load_w<OT>(g, sr + 32 * i, k);
+    }
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      uint4 av[2], bv[RT];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) av[i] = *(const uint4 *)(lds_a + (32 * wm + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+#pragma unroll
+      for (int j = 0; j < RT; ++j)
+        bv[j] = *(const uint4 *)(lds_b + ((CO / 2) * wn + 16 * j + lr) * ROWB + kk * 64 + lg * 16);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < RT; ++j) acc[i][j] = Op<OT>::mma(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+
+  // ---- gate: the wave's column tiles (2 q, 2 q + 1) are the tanh and sigmoid halves of 16 channels;
+  // the residual input rows land in the staging area (free after the conv)
+#pragma unroll
+  for (int q = 0; q < RT / 2; ++q) {
+    const int grp = ((CO / 2) * wn) / 32 + q;
+    const int ch = 16 * grp + lr;
+    const float bt = g.bias[32 * grp + lr], bs = g.bias[32 * grp + 16 + lr];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 32 * wm + 16 * i + 4 * lg + e;
+        const float z = tanhf(acc[i][2 * q][e] + bt) * sigmoid(acc[i][2 * q + 1][e] + bs);
+        Op<OT>::put(lds_z + r * ROWB, ch, z);
+      }
+  }
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int c = tid + NT * i, r = c / XC, q = c % XC;
+    *(uint4 *)(lds_x + r * XROW + 16 * q) = xin[i];
+  }
+  // zero the padding of the z rows beyond R (read by the second half-tile when R operands < 128 B)
+  if (ZB < KT_BYTES)
+    for (int i = tid; i < 64 * ((KT_BYTES - ZB) / 16); i += NT) {
+      const int r = i / ((KT_BYTES - ZB) / 16), c = i % ((KT_BYTES - ZB) / 16);
+      *(uint4 *)(lds_z + r * ROWB + ZB + c * 16) = make_uint4(0, 0, 0, 0);
+    }
+  __syncthreads();
+
+  // ---- residual 1x1 from LDS: 64 rows x R; wave (wm, wn): rows 32 wm.., columns (R / 2) wn..
+  constexpr int RJ = RT / 2;
+  f32x4 res[2][RJ];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < RJ; ++j) res[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    uint4 av[2], bv[RJ];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) av[i] = *(const uint4 *)(lds_z + (32 * wm + 16 * i + lr) * ROWB + kk * 64 + lg * 16);
+#pragma unroll
+    for (int j = 0; j < RJ; ++j)
+      bv[j] = *(const uint4 *)(lds_r + ((R / 2) * wn + 16 * j + lr) * ROWB + kk * 64 + lg * 16);
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < RJ; ++j) res[i][j] = Op<OT>::mma(av[i], bv[j], res[i][j]);
+  }
+  // x += W_res z + b_res in the LDS rows (each element has one owner lane)
+#pragma unroll
+  for (int j = 0; j < RJ; ++j) {
+    const int n = (R / 2) * wn + 16 * j + lr;
+    const float bn = g.bias2[n];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float *px = (float *)(lds_x + (32 * wm + 16 * i + 4 * lg + e) * XROW) + n;
+        *px += res[i][j][e] + bn;
+      }
+  }
+  __syncthreads();
+
+  // ---- row stores: z rows (operand), x rows (float32) and their operand copies
+  constexpr int ZC = ZB / 16;
+  for (int c = tid; c < 64 * ZC; c += NT) {
+    const int r = c / ZC, q = c % ZC, m = m0 + r;
+    if (m < g.M) *(uint4 *)((OT *)g.zout + (long long)m * g.ldz + g.zoff + q * EPC) = *(const uint4 *)(lds_z + r * ROWB + 16 * q);
+  }
+#pragma unroll
+  for (int i = 0; i < XPT; ++i) {
+    const int c = tid + NT * i, r = c / XC, q = c % XC, m = m0 + r;
+    if (m >= g.M) continue;
+    const float4 v = *(const float4 *)(lds_x + r * XROW + 16 * q);
+    *(float4 *)(g.xout + (long long)m * g.ldo + 4 * q) = v;
+    if (g.oout) {
+      OT *o = (OT *)g.oout + (long long)m * g.ldo + 4 * q;
+      Op<OT>::put(o, 0, v.x);
+      Op<OT>::put(o, 1, v.y);
+      Op<OT>::put(o, 2, v.z);
+      Op<OT>::put(o, 3, v.w);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // x^0 rows: E[token] + b, fp32 stream and operand copy.  Tokens: the forced sequence
 // (teacher forcing) or, in online prediction, the pending input followed by the
 // observed samples.
@@ -393,6 +565,23 @@ hipError_t launch_par_gemm(const ParGemm &g, int dtype, int amode, int emode, hi
   if (amode == par::A_CONV) return par::launch_em<float, par::A_CONV>(g, emode, s);
   if (amode == par::A_TREE) return par::launch_em<float, par::A_TREE>(g, emode, s);
   return par::launch_em<float, par::A_PLAIN>(g, emode, s);
+}
+
+bool par_gated_layer_ok(int R, int dtype) {
+  const int es = dtype == 1 ? 2 : 4;
+  return (R == 32 || R == 64) && R * es <= par::KT_BYTES;
+}
+
+hipError_t launch_par_gated_layer(const ParGemm &g, int dtype, hipStream_t s) {
+  if (g.M <= 0) return hipSuccess;
+  const dim3 grid((g.M + 63) / 64);
+  if (dtype == 1) {
+    if (g.C == 64) hipLaunchKernelGGL((par::par_gated_layer_kernel<uint16_t, 4>), grid, dim3(par::NT), 0, s, g);
+    else hipLaunchKernelGGL((par::par_gated_layer_kernel<uint16_t, 2>), grid, dim3(par::NT), 0, s, g);
+  } else {
+    hipLaunchKernelGGL((par::par_gated_layer_kernel<float, 2>), grid, dim3(par::NT), 0, s, g);
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_par_embed(const ParEmbed &e, int dtype, hipStream_t s) {
