@@ -13,7 +13,8 @@ SOURCES = [os.path.join(CSRC, "fwg_host.cpp"), os.path.join(CSRC, "fwg_kernels.h
            os.path.join(CSRC, "fwg_mfma.hip"), os.path.join(CSRC, "fwg_parallel.hip"),
            os.path.join(CSRC, "fwg_wave.hip")]
 HEADERS = [os.path.join(ROOT, "include", "fwg.h"), os.path.join(CSRC, "fwg_internal.h"),
-           os.path.join(CSRC, "fwg_sample.h")]
+           os.path.join(CSRC, "fwg_sample.h"), os.path.join(CSRC, "fwg_valu.h"),
+           os.path.join(CSRC, "fwg_wave.h"), os.path.join(CSRC, "fwg_par.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -14,6 +14,9 @@
 
 #include "fwg.h"
 #include "fwg_internal.h"
+#include "fwg_par.h"
+#include "fwg_valu.h"
+#include "fwg_wave.h"
 
 using namespace fwg;
 
@@ -57,7 +60,7 @@ struct Plan {
   int par_tc;             // steps per chunk; a chunk holds brows * par_tc rows at most
   std::vector<size_t> off_pconv, off_pconv_b, off_pres;
   size_t off_pskip, off_pskip_b, off_phead, off_pout;
-  size_t off_px[2], off_pxb[2], off_pz, off_psb, off_phb;
+  size_t off_px[3], off_pxb[3], off_pz, off_psb, off_phb;  // three rotating row buffers
   // naive generator: the nodes of the output's dependency tree (Fig. 1), level 0 = inputs
   bool nv_ok;
   std::vector<int> nv_n;         // [L + 1] distinct nodes per level
@@ -335,7 +338,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
     p->off_pskip_b = gated ? take(sizeof(float) * p->S) : 0;
     p->off_phead = gated ? take((size_t)p->H * p->S * p->es) : 0;
     p->off_pout = take((size_t)p->Q * Kout * p->es);
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 3; ++i) {
       p->off_px[i] = fp32_stream ? take(R * p->C * 4) : 0;
       p->off_pxb[i] = opnd_copy ? take(R * p->C * p->es) : p->off_px[i];
     }
@@ -527,8 +530,9 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a) {
 
 // Time-parallel evaluation of a forced sequence, chunk by chunk (MODE_TEACHER or MODE_ONLINE):
 // every layer is a GEMM over the chunk's rows whose popped operand comes from the chunk or from
-// the layer's queue in `ring`; the queues are refreshed after each layer.  logits may be NULL
-// (online mode only): then the skip sum and the head are skipped.
+// the layer's queue in `ring`; a layer's queue is refreshed once its product has read it (by the
+// next layer's fused kernel when there is one, which is why the row buffers rotate over three).
+// logits may be NULL (online mode only): then the skip sum and the head are skipped.
 int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs, float *logits, char *ring,
                 long long tbase) {
   const Plan &p = h->plan;
@@ -538,8 +542,9 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
   const bool gated = p.kind == FWG_GATED;
   const bool f32s = p.kind != FWG_RELU;
   const bool opnd_copy = p.kind == FWG_RELU || p.dtype == FWG_BF16;
-  float *px[2] = {(float *)(ws + p.off_px[0]), (float *)(ws + p.off_px[1])};
-  char *pxb[2] = {ws + p.off_pxb[0], ws + p.off_pxb[1]};
+  float *px[3] = {(float *)(ws + p.off_px[0]), (float *)(ws + p.off_px[1]), (float *)(ws + p.off_px[2])};
+  char *pxb[3] = {ws + p.off_pxb[0], ws + p.off_pxb[1], ws + p.off_pxb[2]};
+  const bool fused = gated && par_gated_layer_ok(C, p.dtype);
   for (long long s0 = 0; s0 < n; s0 += p.par_tc) {
     const int Tcur = (int)(n - s0 < p.par_tc ? n - s0 : p.par_tc);
     const int M = batch * Tcur;
@@ -554,9 +559,17 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
     e.xout = f32s ? px[0] : nullptr;
     e.oout = pxb[0];
     HIP_TRY(launch_par_embed(e, p.dtype, s));
-    int cur = 0;
+    int cur = 0, prev = 0;
+    auto refresh = [&](int l, const char *src) {
+      ParRing q;
+      memset(&q, 0, sizeof(q));
+      q.ring = ring + (size_t)p.ring_off[l] * es; q.src = src;
+      q.t0 = t0; q.Tcur = Tcur; q.depth = (p.w - 1) * h->dil[l]; q.brows = p.brows; q.batch = batch;
+      q.row_bytes = C * es;
+      return launch_par_ring(q, s);
+    };
     for (int l = 0; l < L; ++l) {
-      const int nxt = cur ^ 1;
+      const int nxt = (cur + 1) % 3;
       ParGemm g;
       memset(&g, 0, sizeof(g));
       g.M = M; g.N = p.Co; g.K = p.w * C;
@@ -567,9 +580,12 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
       g.W = ws + p.off_pconv[l];
       g.bias = (const float *)(ws + p.off_pconv_b[l]);
       int em = PAR_E_GATE;
-      const bool fused = gated && par_gated_layer_ok(C, p.dtype);
       if (fused) {
-        // dilated product, gate, z rows and residual 1x1 in one kernel
+        // dilated product, gate, z rows and residual 1x1 in one kernel, with the previous layer's
+        // queue refresh
+        if (l > 0) {
+          g.qring = ring + (size_t)p.ring_off[l - 1] * es; g.qsrc = pxb[prev]; g.qdepth = (p.w - 1) * h->dil[l - 1];
+        }
         g.zout = ws + p.off_pz; g.ldz = (long long)L * C; g.zoff = l * C;
         g.W2 = ws + p.off_pres[l];
         g.bias2 = (const float *)(ws + p.off_res_b[l]);
@@ -593,12 +609,8 @@ int par_forward(fwg_handle *h, int mode, int batch, int n, const int32_t *inputs
         r.xres = px[cur]; r.xout = px[nxt]; r.oout = opnd_copy ? pxb[nxt] : nullptr; r.ldo = C;
         HIP_TRY(launch_par_gemm(r, p.dtype, PAR_A_PLAIN, PAR_E_RES_ADD, s));
       }
-      ParRing q;
-      memset(&q, 0, sizeof(q));
-      q.ring = ring + (size_t)p.ring_off[l] * es; q.src = pxb[cur];
-      q.t0 = t0; q.Tcur = Tcur; q.depth = (p.w - 1) * h->dil[l]; q.brows = p.brows; q.batch = batch;
-      q.row_bytes = C * es;
-      HIP_TRY(launch_par_ring(q, s));
+      if (!fused || l + 1 == L) HIP_TRY(refresh(l, pxb[cur]));
+      prev = cur;
       cur = nxt;
     }
     if (!logits) continue;

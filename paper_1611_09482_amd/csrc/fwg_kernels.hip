@@ -21,6 +21,7 @@
 #include <type_traits>
 
 #include "fwg_internal.h"
+#include "fwg_valu.h"
 #include "fwg_sample.h"
 
 

@@ -34,6 +34,7 @@
 #include <stdint.h>
 
 #include "fwg_internal.h"
+#include "fwg_par.h"
 #include "fwg_sample.h"
 
 namespace fwg {
@@ -318,6 +319,21 @@ __global__ void __launch_bounds__(NT) par_gated_layer_kernel(ParGemm g) {
   for (int i = 0; i < XPT; ++i) {
     const int c = tid + NT * i, r = c / XC, q = c % XC, m = m0 + r;
     xin[i] = m < g.M ? *(const uint4 *)(g.xres + (long long)m * g.ldo + 4 * q) : make_uint4(0, 0, 0, 0);
+  }
+
+  // the previous layer's queue refresh: its input rows of this block that are among the chunk's
+  // last qdepth steps, each to the slot of its time
+  if (g.qring) {
+    constexpr int RC = ZB / 16;  // 16-byte pieces of an operand row of C = R channels
+    for (int c = tid; c < 64 * RC; c += NT) {
+      const int r = c / RC, q = c % RC, m = m0 + r;
+      if (m >= g.M) break;
+      const int b = m / g.Tcur, j = m - b * g.Tcur;
+      if (j < g.Tcur - g.qdepth) continue;
+      const long long slot = (g.t0 + j) % g.qdepth;
+      *(uint4 *)((char *)g.qring + (slot * g.brows + b) * (long long)ZB + 16 * q) =
+          *(const uint4 *)((const char *)g.qsrc + (long long)m * ZB + 16 * q);
+    }
   }
 
   // ---- dilated product: 64 rows x CO columns; wave (wm, wn): rows 32 wm.., columns (CO / 2) wn..

@@ -16,6 +16,7 @@
 #include <stdint.h>
 
 #include "fwg_internal.h"
+#include "fwg_wave.h"
 #include "fwg_sample.h"
 
 namespace fwg {
