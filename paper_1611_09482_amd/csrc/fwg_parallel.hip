@@ -286,12 +286,13 @@ template <typename OT, int RT>
 __global__ void __launch_bounds__(NT) par_gated_layer_kernel(ParGemm g) {
   constexpr int R = 16 * RT, CO = 2 * R;
   constexpr int XROW = R * 4 + 16;  // LDS stride of a float32 x row
-  // conv staging (A, W), later reused for the x rows
-  constexpr int STAGE_BYTES = (64 + CO) * ROWB > 64 * XROW ? (64 + CO) * ROWB : 64 * XROW;
-  __shared__ __attribute__((aligned(16))) unsigned char lds_s[STAGE_BYTES];
-  __shared__ __attribute__((aligned(16))) unsigned char lds_z[64 * ROWB];
+  // after the conv, the z rows take the A staging area and the x rows the W staging area (37 KB in
+  // all for R = 64: four blocks per CU)
+  constexpr int WX_BYTES = CO * ROWB > 64 * XROW ? CO * ROWB : 64 * XROW;
+  __shared__ __attribute__((aligned(16))) unsigned char lds_a[64 * ROWB];
+  __shared__ __attribute__((aligned(16))) unsigned char lds_b[WX_BYTES];
   __shared__ __attribute__((aligned(16))) unsigned char lds_r[R * ROWB];
-  unsigned char *lds_a = lds_s, *lds_b = lds_s + 64 * ROWB, *lds_x = lds_s;
+  unsigned char *const lds_z = lds_a, *const lds_x = lds_b;
   constexpr int KT = Op<OT>::KT;
   constexpr int EPC = 16 / sizeof(OT);
   constexpr int ZB = R * (int)sizeof(OT);  // bytes of a z row (<= 128)
