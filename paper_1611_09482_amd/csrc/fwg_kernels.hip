@@ -176,12 +176,28 @@ typedef __attribute__((address_space(1))) const u32x4 *glb_u4p;
 typedef __attribute__((address_space(3))) const float *lds_f32p;
 typedef __attribute__((address_space(1))) const float *glb_f32p;
 
-template <typename WT, int RPW, bool STAGE>
+// Model shapes known at compile time.  The general kernel reads the shape from its launch
+// arguments; at one stream per block a layer is bound by instruction issue, and with the shape as
+// constants the index arithmetic folds and fewer values stay live.  Fields: kind (-1: runtime), C,
+// Q and w (0: runtime), S and H (-1: runtime).
+struct ShapeAny {
+  static constexpr int kind = -1, C = 0, S = -1, H = -1, Q = 0, w = 0;
+};
+template <int KIND, int C_, int S_, int H_, int W_>
+struct ShapeFixed {
+  static constexpr int kind = KIND, C = C_, S = S_, H = H_, Q = 256, w = W_;
+};
+
+template <typename WT, int RPW, bool STAGE, typename SH>
 __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   float *lds = (float *)lds_raw;
   const int wfloats = a.valu_wbytes / 4;
-  const ValuLds lay = valu_lds_layout(a.kind, a.C, a.S, a.H, a.Q, a.L, RPW, a.w, wfloats);
+  // the model shape: compile-time constants in a specialised instantiation, else launch arguments
+  const int kind = SH::kind >= 0 ? SH::kind : a.kind;
+  const int C = SH::C ? SH::C : a.C, S = SH::S >= 0 ? SH::S : a.S, H = SH::H >= 0 ? SH::H : a.H;
+  const int Q = SH::Q ? SH::Q : a.Q, w = SH::w ? SH::w : a.w, L = a.L;
+  const ValuLds lay = valu_lds_layout(kind, C, S, H, Q, L, RPW, w, wfloats);
   float *xf = lds + lay.xf, *xo = lds + lay.xo, *ao = lds + lay.ao;
   float *zo = lds + lay.zo, *so = lds + lay.so, *ho = lds + lay.ho, *h2 = lds + lay.h2;
   float *lg = lds + lay.lg, *partA = lds + lay.partA, *partB = lds + lay.partB;
@@ -195,8 +211,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   (void)ao;
 
   const int tid = threadIdx.x;
-  const int C = a.C, S = a.S, H = a.H, Q = a.Q, L = a.L, w = a.w;
-  const int Co = a.kind == 2 ? 2 * C : C;
+  const int Co = kind == 2 ? 2 * C : C;
   const int K = w * C;
   const int b0 = blockIdx.x * RPW;
   const int nrows = min(RPW, a.batch - b0);
@@ -207,7 +222,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   const int es = sizeof(WT);
   // offsets inside a layer's block: conv | res | skip weights, then conv_b | res_b | skip_b
   const size_t o_res = (size_t)K * Co * es, o_skip = o_res + (size_t)C * C * es;
-  const size_t o_cb = a.kind == 2 ? o_skip + (size_t)S * C * es : o_res;
+  const size_t o_cb = kind == 2 ? o_skip + (size_t)S * C * es : o_res;
   const size_t o_rb = o_cb + (size_t)Co * 4, o_sb = o_rb + (size_t)C * 4;
 
   for (int l = tid; l < L; l += kThreads) {
@@ -284,7 +299,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
       xf[i] = v;
       xo[i] = WTraits<WT>::opnd(v);
     }
-    if (a.kind == 2)
+    if (kind == 2)
       for (int i = tid; i < RPW * S; i += kThreads) so[i] = 0.f;
     __syncthreads();
 
@@ -318,7 +333,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
       // ---- dilated convolution of width w: [v_0 .. v_{w-2} x] . [W_0 ; .. ; W_{w-1}]
       rows_product<WT, RPW, WP>(wp(0), K, Co, vo, (w - 1) * C, xo, C, (w - 1) * C, partA);
       __syncthreads();
-      if (a.kind == 2) {
+      if (kind == 2) {
         const BP rb = (BP)(wb + o_rb), sb = (BP)(wb + o_sb);
         // gate: z = tanh(a[0:R]) * sigmoid(a[R:2R])
         for (int i = tid; i < RPW * C; i += kThreads) {
@@ -350,7 +365,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
         for (int i = tid; i < RPW * C; i += kThreads) {
           const int r = i / C, c = i % C;
           const float pre = cb[c] + part_sum<RPW>(partA, Co, r, c);
-          const float v = (a.kind == 1 ? xf[i] : 0.f) + fmaxf(pre, 0.f);
+          const float v = (kind == 1 ? xf[i] : 0.f) + fmaxf(pre, 0.f);
           xf[i] = v;
           xo[i] = WTraits<WT>::opnd(v);
         }
@@ -363,7 +378,7 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
     // ---- output head
     const float *top = xo;
     int Ktop = C;
-    if (a.kind == 2) {
+    if (kind == 2) {
       for (int i = tid; i < RPW * S; i += kThreads) ho[i] = WTraits<WT>::opnd(fmaxf(so[i], 0.f));
       __syncthreads();
       rows_product<WT, RPW, glb_u4p>((glb_u4p)a.head, S, H, ho, S, ho, S, S, partA);
@@ -416,32 +431,57 @@ __global__ void __launch_bounds__(kThreads) valu_step_kernel(StepArgs a) {
   if (a.mode != MODE_TEACHER && tid < nrows) a.last[b0 + tid] = ins[tid];
 }
 
-template <typename WT, bool STAGE>
+template <typename WT, bool STAGE, typename SH>
 static hipError_t launch_valu_t(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
   const dim3 grid((a.batch + rpw - 1) / rpw), block(kThreads);
   switch (rpw) {
-    case 1: hipLaunchKernelGGL((valu_step_kernel<WT, 1, STAGE>), grid, block, lds, s, a); break;
-    case 2: hipLaunchKernelGGL((valu_step_kernel<WT, 2, STAGE>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((valu_step_kernel<WT, 4, STAGE>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((valu_step_kernel<WT, 8, STAGE>), grid, block, lds, s, a); break;
+    case 1: hipLaunchKernelGGL((valu_step_kernel<WT, 1, STAGE, SH>), grid, block, lds, s, a); break;
+    case 2: hipLaunchKernelGGL((valu_step_kernel<WT, 2, STAGE, SH>), grid, block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL((valu_step_kernel<WT, 4, STAGE, SH>), grid, block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL((valu_step_kernel<WT, 8, STAGE, SH>), grid, block, lds, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_valu_step(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
-  if (a.valu_wbytes > 0)
-    return a.dtype == 1 ? launch_valu_t<uint16_t, true>(a, rpw, lds, s) : launch_valu_t<float, true>(a, rpw, lds, s);
-  return a.dtype == 1 ? launch_valu_t<uint16_t, false>(a, rpw, lds, s) : launch_valu_t<float, false>(a, rpw, lds, s);
+template <typename WT, typename SH>
+static hipError_t launch_valu_s(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
+  return a.valu_wbytes > 0 ? launch_valu_t<WT, true, SH>(a, rpw, lds, s) : launch_valu_t<WT, false, SH>(a, rpw, lds, s);
 }
 
-template <typename WT, int RPW>
-static hipError_t set_lds_one(size_t bytes) {
-  hipError_t e = hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, true>,
+// fp32 shapes with instantiations of their own: gated R = 32, S = H = 256 at widths 2 and 3.  (A
+// 512-channel ReLU + residual instantiation ran 3x slower than the runtime-shaped kernel.)
+typedef ShapeFixed<2, 32, 256, 256, 2> ShapeG32;
+typedef ShapeFixed<2, 32, 256, 256, 3> ShapeG32W3;
+template <typename SH>
+static bool shape_is(const StepArgs &a) {
+  return a.kind == SH::kind && a.C == SH::C && a.S == SH::S && a.H == SH::H && a.Q == SH::Q && a.w == SH::w;
+}
+
+hipError_t launch_valu_step(const StepArgs &a, int rpw, size_t lds, hipStream_t s) {
+  if (a.dtype == 1) return launch_valu_s<uint16_t, ShapeAny>(a, rpw, lds, s);
+  if (shape_is<ShapeG32>(a)) return launch_valu_s<float, ShapeG32>(a, rpw, lds, s);
+  if (shape_is<ShapeG32W3>(a)) return launch_valu_s<float, ShapeG32W3>(a, rpw, lds, s);
+  return launch_valu_s<float, ShapeAny>(a, rpw, lds, s);
+}
+
+template <typename WT, int RPW, typename SH>
+static hipError_t set_lds_sh(size_t bytes) {
+  hipError_t e = hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, true, SH>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, false>,
+  return hipFuncSetAttribute((const void *)valu_step_kernel<WT, RPW, false, SH>,
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+}
+template <typename WT, int RPW>
+static hipError_t set_lds_one(size_t bytes) {
+  hipError_t e = set_lds_sh<WT, RPW, ShapeAny>(bytes);
+  if constexpr (sizeof(WT) == 4) {
+    if (e != hipSuccess) return e;
+    if ((e = set_lds_sh<WT, RPW, ShapeG32>(bytes)) != hipSuccess) return e;
+    e = set_lds_sh<WT, RPW, ShapeG32W3>(bytes);
+  }
+  return e;
 }
 
 hipError_t set_valu_lds_limit(size_t bytes) {
