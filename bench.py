@@ -42,7 +42,7 @@ HBM_PEAK_GBS = 8000.0
 
 
 # sources of the benchmark's step kernel: the kernel file and the structures it reads
-KERNEL_SOURCES = ("fwg_mfma.hip", "fwg_internal.h")
+KERNEL_SOURCES = ("fwg_split.hip", "fwg_mfma.hip", "fwg_mfma_dev.h", "fwg_internal.h")
 
 
 def kernel_source_digest() -> str:
@@ -299,6 +299,7 @@ def main():
     wall = time.perf_counter() - w0
     ms = e0.elapsed_time(e1)
     sec = ms / 1e3
+    fw.device_status()  # raises if the launch ended without valid results
 
     dtype = "bf16" if cfg.dtype == W.BF16 else "f32"
     samples = B * K

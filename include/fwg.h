@@ -72,7 +72,8 @@ enum {
   FWG_ENOSPACE = -2,     /* workspace smaller than fwg_workspace_size() or misaligned */
   FWG_EHIP = -3,         /* a HIP runtime call failed (message has the HIP error string) */
   FWG_ESTATE = -4,       /* generate() with a batch other than the one used since the last reset */
-  FWG_EUNSUPPORTED = -5  /* a valid shape this build has no kernel for */
+  FWG_EUNSUPPORTED = -5, /* a valid shape this build has no kernel for */
+  FWG_EDEVICE = -6       /* fwg_device_status: a launch ended without valid results (see there) */
 };
 
 /* layer kinds */
@@ -219,6 +220,16 @@ const char *fwg_last_error(void);
 
 /* Short name of the kernel family a handle uses (for logs and profiles). */
 const char *fwg_regime(const fwg_handle *h);
+
+/* Wait for every call enqueued on the handle's stream, then report whether a
+ * launch since the last create/reset ended without valid results: FWG_EDEVICE
+ * when a bounded wait between the cooperating blocks of a split-family launch
+ * ran out (its blocks were not all resident on the device at once; that launch
+ * then completes quickly with invalid outputs instead of hanging), FWG_EHIP on
+ * a HIP error, else FWG_OK.  Kernel families without cross-block waits always
+ * return FWG_OK after the synchronisation.  The mark is cleared by
+ * fwg_reset_queues. */
+int fwg_device_status(fwg_handle *h);
 
 #ifdef __cplusplus
 }

@@ -6,18 +6,18 @@ import ctypes
 import os
 from typing import Optional, Sequence
 
-FWG_OK, FWG_EINVAL, FWG_ENOSPACE, FWG_EHIP, FWG_ESTATE, FWG_EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+FWG_OK, FWG_EINVAL, FWG_ENOSPACE, FWG_EHIP, FWG_ESTATE, FWG_EUNSUPPORTED, FWG_EDEVICE = 0, -1, -2, -3, -4, -5, -6
 FWG_RELU, FWG_RELU_RESIDUAL, FWG_GATED = 0, 1, 2
 FWG_F32, FWG_BF16 = 0, 1
 
 _STATUS = {FWG_EINVAL: "EINVAL", FWG_ENOSPACE: "ENOSPACE", FWG_EHIP: "EHIP", FWG_ESTATE: "ESTATE",
-           FWG_EUNSUPPORTED: "EUNSUPPORTED"}
+           FWG_EUNSUPPORTED: "EUNSUPPORTED", FWG_EDEVICE: "EDEVICE"}
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfwg.so")
 
 EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
             "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive", "fwg_naive_nodes",
-            "fwg_destroy", "fwg_last_error", "fwg_regime"]
+            "fwg_destroy", "fwg_last_error", "fwg_regime", "fwg_device_status"]
 
 
 class FwgError(RuntimeError):
@@ -71,9 +71,10 @@ def load_library(path: Optional[str] = None):
     L.fwg_last_error.restype = ctypes.c_char_p
     L.fwg_regime.argtypes = [vp]
     L.fwg_regime.restype = ctypes.c_char_p
+    L.fwg_device_status.argtypes = [vp]
     for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
                  "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive",
-                 "fwg_naive_nodes", "fwg_destroy"]:
+                 "fwg_naive_nodes", "fwg_destroy", "fwg_device_status"]:
         getattr(L, name).restype = ctypes.c_int
     if path is None:
         _lib = L
@@ -159,6 +160,11 @@ class FastWavenet:
 
     def reset(self):
         _check(self.lib.fwg_reset_queues(self.handle))
+
+    def device_status(self):
+        """Synchronise the handle's stream and raise FwgError (EDEVICE) if a launch since the last
+        reset ended without valid results."""
+        _check(self.lib.fwg_device_status(self.handle))
 
     def generate(self, uniforms, out=None):
         """uniforms: float32 CUDA tensor [batch][n_steps] -> int32 samples [batch][n_steps]."""

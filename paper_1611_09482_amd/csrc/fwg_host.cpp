@@ -49,6 +49,7 @@ struct Plan {
   int regime;
   int brows;              // queue rows per slot (max_batch, padded to whole blocks for the MFMA family)
   size_t off_frags, off_embT, off_bias, off_ptrtab;
+  size_t off_comm, off_sticky;  // split MFMA family: exchange words and the sticky abort word
   long long queue_elems;  // sum(d_l) * bmax * C
   size_t off_layers, off_embed, off_embed_b, off_head, off_head_b, off_out, off_out_b;
   std::vector<size_t> off_conv, off_conv_b, off_res, off_res_b, off_skip, off_skip_b;
@@ -244,7 +245,12 @@ int make_plan(const fwg_desc *d, Plan *p) {
   const bool mfma_shape = w == 2 && p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR && p->S == kMfS &&
                           p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
                           mfma_lds_bytes(p->L) <= 160 * 1024;
-  if (mfma_shape && !(force && strcmp(force, "valu") == 0)) p->regime = REGIME_MFMA;
+  // the split family takes the MFMA family's shape when L suits its unrolled layer loop
+  // (FWG_REGIME=mfma keeps the single-block kernel); fwg_create falls back to it when the split
+  // launch's blocks cannot all be resident at once
+  const bool split_shape = mfma_shape && split_layers_ok(p->L);
+  if (mfma_shape && !(force && strcmp(force, "valu") == 0))
+    p->regime = split_shape && !(force && strcmp(force, "mfma") == 0) ? REGIME_SPLIT : REGIME_MFMA;
   // small models whose weights all fit in LDS: one wavefront per stream
   if (p->regime == REGIME_VALU && !(force && strcmp(force, "valu") == 0) && wave_layout(*p, &p->wave))
     p->regime = REGIME_WAVE;
@@ -255,18 +261,24 @@ int make_plan(const fwg_desc *d, Plan *p) {
                 kb, kb);
   if (p->regime == REGIME_VALU && rpw == 0)
     return fail(FWG_EUNSUPPORTED, "model too wide for one block's LDS and registers");
-  p->brows = p->regime == REGIME_MFMA ? (p->bmax + kMfRows - 1) / kMfRows * kMfRows : p->bmax;
+  const bool mf_family = p->regime == REGIME_MFMA || p->regime == REGIME_SPLIT;
+  p->brows = mf_family ? (p->bmax + kMfRows - 1) / kMfRows * kMfRows : p->bmax;
 
   // workspace layout
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t at = off; off = align_up(off + bytes); return at; };
   p->off_layers = take(sizeof(LayerDev) * p->L);
-  p->off_frags = p->off_embT = p->off_bias = p->off_ptrtab = 0;
-  if (p->regime == REGIME_MFMA) {
-    p->off_frags = take(mfma_frag_bytes(p->L));
+  p->off_frags = p->off_embT = p->off_bias = p->off_ptrtab = p->off_comm = p->off_sticky = 0;
+  if (mf_family) {
+    // either family's fragment streams fit (create may fall back from the split family)
+    p->off_frags = take(std::max(mfma_frag_bytes(p->L), split_shape ? split_frag_bytes(p->L) : size_t(0)));
     p->off_embT = take((size_t)p->Q * p->C * 2);
     p->off_bias = take(sizeof(float) * mfma_bias_floats(p->L));
     p->off_ptrtab = take(sizeof(void *) * 3 * p->L);
+    if (split_shape) {
+      p->off_comm = take(split_comm_bytes(p->L, p->brows / kMfRows));
+      p->off_sticky = take(sizeof(uint32_t));
+    }
   }
   p->off_embed = take((size_t)p->Q * p->C * p->es);
   p->off_embed_b = take(sizeof(float) * p->C);
@@ -299,6 +311,8 @@ int make_plan(const fwg_desc *d, Plan *p) {
     acc += (long long)(w - 1) * d->dilations[l] * p->brows * p->C;
   }
   p->queue_elems = acc;
+  // the split family addresses a queue region with 32-bit byte offsets
+  if (p->regime == REGIME_SPLIT && (unsigned long long)acc * p->es >= (1ull << 31)) p->regime = REGIME_MFMA;
   (void)dsum;
   p->off_ring_gen = take((size_t)acc * p->es);
   p->off_ring_tf = take((size_t)acc * p->es);
@@ -384,6 +398,7 @@ int enqueue_reset(fwg_handle *h) {
   const Plan &p = h->plan;
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_gen, (size_t)p.queue_elems * p.es, h->stream));
   HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_last), p.seed_input, p.bmax, h->stream));
+  if (p.regime == REGIME_SPLIT) HIP_TRY(launch_fill_zero(h->ws + p.off_sticky, sizeof(uint32_t), h->stream));
   if (p.nv_ok)  // every history entry the seed: the entry of time 0 is the first input
     HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_hist), p.seed_input, p.bmax * p.nv_hc, h->stream));
   h->t = 0;
@@ -407,7 +422,7 @@ StepArgs base_args(const fwg_handle *h) {
   a.last = (int32_t *)(h->ws + p.off_last);
   a.bmax = p.brows;
   a.valu_wbytes = p.valu_wbytes;
-  if (p.regime == REGIME_MFMA) {
+  if (p.regime == REGIME_MFMA || p.regime == REGIME_SPLIT) {
     a.mf_frags = h->ws + p.off_frags;
     a.mf_embT = h->ws + p.off_embT;
     a.mf_bias = (const float *)(h->ws + p.off_bias);
@@ -519,6 +534,16 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a) {
   const Plan &p = h->plan;
   switch (p.regime) {
     case REGIME_MFMA: return launch_mfma_step(a, h->stream);
+    case REGIME_SPLIT: {
+      StepArgs b = a;
+      b.sp_nb = (a.batch + kMfRows - 1) / kMfRows;
+      b.sp_comm = h->ws + p.off_comm;
+      b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
+      // tags restart at 1 every launch: clear the exchange words first (a fill kernel, no memset node)
+      hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
+      if (e != hipSuccess) return e;
+      return launch_split_step(b, h->stream);
+    }
     case REGIME_WAVE: {
       WaveArgs g = p.wave;
       g.image = (const float *)(h->ws + p.off_wave);
@@ -780,12 +805,24 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     TRY_OR_FREE(launch_par_repack(w->out, ws + p.off_pout, PAR_REPACK_COPY, dt, p.Q, Kout, C, 0, Kout, 0, s));
   }
   std::vector<const void *> ptrs;
-  if (p.regime == REGIME_MFMA) {
+  if (p.regime == REGIME_SPLIT) {
+    int coresident = 0;
+    TRY_OR_FREE(split_setup(p.L, p.brows / kMfRows, &coresident));
+    if (!coresident) h->plan.regime = REGIME_MFMA;  // same workspace layout
+  }
+  if (h->plan.regime == REGIME_SPLIT) {
+    char *frags = ws + p.off_frags;
+    for (int l = 0; l < p.L; ++l)
+      TRY_OR_FREE(launch_split_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));
+    TRY_OR_FREE(launch_split_repack_head(w->head, w->out, p.L, frags, s));
+  } else if (h->plan.regime == REGIME_MFMA) {
     char *frags = ws + p.off_frags;
     // layers first: a layer also writes fragments into the previous stage and the last head stage
     for (int l = 0; l < p.L; ++l)
       TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));
     TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, p.L, frags, s));
+  }
+  if (h->plan.regime == REGIME_MFMA || h->plan.regime == REGIME_SPLIT) {
     TRY_OR_FREE(launch_mfma_embed_table(w->embed, ws + p.off_embT, s));
     ptrs.resize(3 * p.L, nullptr);
     for (int l = 0; l < p.L; ++l) {
@@ -949,10 +986,24 @@ int fwg_destroy(fwg_handle *h) {
   return FWG_OK;
 }
 
+int fwg_device_status(fwg_handle *h) {
+  if (!h) return fail(FWG_EINVAL, "handle is NULL");
+  HIP_TRY(hipStreamSynchronize(h->stream));
+  if (h->plan.regime == REGIME_SPLIT) {
+    uint32_t v = 0;
+    HIP_TRY(hipMemcpy(&v, h->ws + h->plan.off_sticky, sizeof(v), hipMemcpyDeviceToHost));
+    if (v)
+      return fail(FWG_EDEVICE, "a wait between the blocks of a split-family launch ran out (the blocks were not all "
+                               "resident at once); that launch's outputs are invalid");
+  }
+  return FWG_OK;
+}
+
 const char *fwg_regime(const fwg_handle *h) {
   if (!h) return "";
   switch (h->plan.regime) {
     case REGIME_MFMA: return "mfma_bf16_r64_s512";
+    case REGIME_SPLIT: return "mfma_split_bf16_r64_s512";
     case REGIME_WAVE: return "wave";
     default: return "valu";
   }

@@ -53,6 +53,10 @@ struct StepArgs {
   const void *mf_frags;    // per-wave packed weight fragment streams
   const void *mf_embT;     // embedding table [Q][R] (bf16)
   const float *mf_bias;    // bias block: conv [L][2R], res [L][R], skip sum [S], head [H], out [Q], embed [R]
+  // split MFMA family only
+  void *sp_comm;           // exchange words between chain and helper blocks (zeroed before each launch)
+  uint32_t *sp_sticky;     // set when a wait of a launch ran out (cleared by create and reset)
+  int sp_nb;               // chain blocks of this launch (ceil(batch / 16))
 };
 
 // What drives the input of each step.
@@ -65,7 +69,7 @@ enum StepMode {
 __host__ __device__ inline int forced_shift(int mode) { return mode == MODE_TEACHER ? 1 : 0; }
 
 // Kernel families.
-enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2 };
+enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3 };
 
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
 // 16 streams per block of 8 waves, weight fragments per wave and stage.
@@ -77,6 +81,22 @@ constexpr int kMfMaxLayers = 128;
 constexpr size_t kMfStageBytes = (size_t)kMfWaves * kMfFrags * 1024;
 __host__ __device__ inline size_t mfma_frag_bytes(int L) { return kMfStageBytes * ((size_t)L + kMfHeadStages); }
 inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
+
+// Split MFMA family (the MFMA family's model shape, L a multiple of 6 and at least 12): per 16
+// streams one chain block plus kSpHelpers helper blocks that own the skip products of S / kSpHelpers
+// channels each.  Fragments per layer of chain waves A and B, per head and chain wave, and per layer
+// and helper wave.
+constexpr int kSpHelpers = 4;
+constexpr int kSpFA = 6, kSpFB = 4, kSpFHead = 96, kSpFS = 16;
+inline bool split_layers_ok(int L) { return L % 6 == 0 && L >= 12; }
+size_t split_frag_bytes(int L);
+size_t split_comm_bytes(int L, int nb);
+size_t split_lds_bytes(int L);
+hipError_t split_setup(int L, int nb, int *coresident_ok);
+hipError_t launch_split_step(const StepArgs &a, hipStream_t s);
+hipError_t launch_split_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
+                                     hipStream_t s);
+hipError_t launch_split_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s);
 
 // Utility and MFMA-family launchers (fwg_kernels.hip, fwg_mfma.hip).
 hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K, int N, int C, hipStream_t s);

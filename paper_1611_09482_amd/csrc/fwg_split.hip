@@ -1,0 +1,770 @@
+// Split MFMA step kernel for gated stacks with bf16 operands, R = 64 residual channels,
+// S = H = 512 skip/head channels and 256 classes (gfx950, v_mfma_f32_16x16x32_bf16, fp32
+// accumulation).  Same model shape and results as the MFMA step kernel of fwg_mfma.hip.
+//
+// The work of one step of a block of 16 streams is split over 1 + kSpHelpers blocks of the same
+// launch:
+//  - the chain block runs what lies on the layer-to-layer dependency chain: per layer the pop, the
+//    dilated width-2 product, the gate, the residual 1x1 and the push (paper Section 2.2), then the
+//    head, the softmax and the inverse-CDF sample, which is the next step's input (Section 1);
+//  - helper block h accumulates, for skip channels [128h, 128h + 128), the skip 1x1 products of
+//    every layer, from the gate outputs z^l that the chain block publishes, and hands
+//    relu(skip sum) back for the head.
+// No later layer reads a skip product, and they are 49% of a step's weight bytes: the chain block
+// streams 40 KB of weights per layer instead of 104 KB, which is what bounds a step of the
+// single-block kernel (every block that owns streams streams every weight once per step).
+//
+// Hand-offs between blocks are 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed
+// device-scope atomics.  A word is fresh once its tag equals the step's tag (step index in the
+// launch + 1; the exchange buffers are zeroed before every launch), so no fence or flag has to
+// order the payload.  The blocks of a group (a chain block and its helpers) compare their XCD ids
+// at launch: when they share one, and so its L2, the words are stored with workgroup-scope
+// stores, which complete in that L2; otherwise with device-scope stores, which write through to
+// memory and whose slow completion holds up every later memory wait of the storing wave.  Every wait is bounded: a wait that runs out sets the
+// launch's abort word, which ends every other wait (the results are then invalid, and a sticky
+// word lets the host report it); every wave keeps executing its straight-line program, so the grid
+// always drains.
+//
+// Chain block: 8 waves, A = waves 0..3 and B = waves 4..7, A and B of pair p share SIMD p.
+//  - wave A (p): the current-input half of the dilated product (W_e x) for tanh tile p and
+//    sigmoid tile p, plus W_r v + b from LDS, the gate, the residual 1x1 for channel tile p;
+//  - wave B (p): W_r v + b of the next layer (v = the popped state, known early), the queue pops
+//    (issued five layers before they land in LDS) and pushes of stream rows 4p..4p+3, and the
+//    publication of z^l to the helpers.  B's memory work for layer l runs after the layer's second
+//    barrier, beside A's product for layer l + 1 (z and x are double-buffered, the popped rows
+//    triple-buffered), so its stores stay off the layer-to-layer chain;
+//  - both: the head (first 1x1: four tiles per wave, output 1x1: two tiles per wave) and two
+//    sampled rows per wave.
+// Every wave streams its own pre-packed weight fragments from L2 through a ring of registers:
+// 12 fragments (two layers) for A, 24 (six layers) for B, whose loads also queue behind the HBM
+// queue reads; a slot is refilled with the fragment one ring length ahead as soon as it is consumed.
+// The layer loop is unrolled by six layers so every ring slot is a fixed register.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fwg_internal.h"
+#include "fwg_mfma_dev.h"
+
+namespace fwg {
+namespace sp {
+
+using namespace mfd;
+
+constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
+constexpr int NT = kMfThreads, NW = kMfWaves;
+constexpr int NHLP = kSpHelpers, SL = S / NHLP;  // helper blocks per chain block, skip channels each
+constexpr int PX = R + 8;   // 64-channel activation rows (bf16)
+constexpr int PS = S + 8;   // 512-channel activation rows (bf16)
+constexpr int PL = Q + 4;   // fp32 logits rows
+constexpr int PP = 20;      // fp32 partial-tile rows
+constexpr int PH = SL + 4;  // fp32 helper partial rows
+constexpr int FA = kSpFA, FB = kSpFB, FHD = kSpFHead, FS = kSpFS;
+constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of waves A and B
+constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
+constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
+static_assert(FHD % DA == 0 && FHD % DB == 0, "the head consumes whole rings");
+static_assert(SL == 8 * 16 && FS == 16, "a helper wave covers its slice as 8 tiles x 2 k-steps");
+
+typedef unsigned long long u64;
+
+struct ChainLds {
+  uint16_t vbuf[3][ROWS * PX];     // popped queue rows, by layer index mod 3
+  uint16_t xbuf[2][ROWS * PX];     // layer inputs x^l, by layer parity
+  uint16_t zbuf[2][ROWS * PX];     // gate outputs z^l, by layer parity
+  float pbuf[2][4][2][ROWS * PP];  // W_r v + b of a layer: [layer parity][tile][tanh / sigmoid]
+  uint16_t hbuf[ROWS * PS];        // relu(head hidden)
+  union {
+    uint16_t sbuf[ROWS * PS];      // relu(skip sum)
+    float lg[ROWS * PL];           // logits
+  } u;
+  uint16_t embT[Q * R];            // embedding table, [class][channel]
+  union {
+    float u[ROWS][KCH];
+    int in[ROWS][KCH];
+  } chunk;
+  int ins[ROWS + NHLP];  // next inputs, then (at launch) the helpers' XCD ids
+  // followed by the per-layer tables: slot[L], dil[L], rbase[L], qoff[2][L] (32-bit), then the fp32
+  // bias block
+};
+struct HelperLds {
+  float part[NW][ROWS * PH];  // per-wave partial skip sums of the slice
+  int local;                  // the group's mode from the launch handshake
+};
+
+__host__ __device__ constexpr size_t chain_fixed_bytes() { return (sizeof(ChainLds) + 15) & ~size_t(15); }
+__host__ __device__ inline size_t dyn_bias_offset(int L) { return ((size_t)L * 20 + 15) & ~size_t(15); }
+
+// Fragment stream geometry (1 KB fragments): A wave p, B wave p, helper (slice h, wave w).
+__host__ __device__ inline int len_a(int L) { return FA * L + FHD; }
+__host__ __device__ inline int len_b(int L) { return FB * L + FHD; }
+__host__ __device__ inline int helper_layers(int L) { return (L + NW - 1) / NW; }
+__host__ __device__ inline size_t base_a(int L, int p) { return (size_t)p * len_a(L); }
+__host__ __device__ inline size_t base_b(int L, int p) { return 4 * (size_t)len_a(L) + (size_t)p * len_b(L); }
+__host__ __device__ inline size_t base_h(int L, int h, int w) {
+  return 4 * (size_t)len_a(L) + 4 * (size_t)len_b(L) + (size_t)(NW * h + w) * helper_layers(L) * FS;
+}
+
+// Exchange buffers: abort word, then z^l words [nb][L][512], relu(skip sum) words [nb][4096] and
+// the launch handshake [nb][8] (word 1 + h: XCD of helper h; word 5: the group's mode).
+constexpr int ZWORDS = ROWS * R / 2, SWORDS = ROWS * S / 2, HWORDS = 8;
+__host__ __device__ inline u64 *comm_z(void *comm, int L, int blk, int l) {
+  return (u64 *)((char *)comm + 256) + ((size_t)blk * L + l) * ZWORDS;
+}
+__host__ __device__ inline u64 *comm_s(void *comm, int L, int nb, int blk) {
+  return (u64 *)((char *)comm + 256) + (size_t)nb * L * ZWORDS + (size_t)blk * SWORDS;
+}
+__host__ __device__ inline u64 *comm_h(void *comm, int L, int nb, int blk) {
+  return (u64 *)((char *)comm + 256) + (size_t)nb * L * ZWORDS + (size_t)nb * SWORDS + (size_t)blk * HWORDS;
+}
+
+// `local`: the reader shares this block's XCD (and L2).
+__device__ __forceinline__ void put_word(u64 *p, uint32_t payload, uint32_t tag, bool local) {
+  const u64 v = ((u64)tag << 32) | payload;
+  if (local) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t xcd_id() {
+  return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15;  // HW_REG_XCC_ID, bits 3:0
+}
+__device__ __forceinline__ u64 get_word(const u64 *p) {
+  return __hip_atomic_load((u64 *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t get_flag(const uint32_t *p) {
+  return __hip_atomic_load((uint32_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// A wait ran out: end every other wait of the launch, and leave a sticky mark for the host.
+__device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *sticky) {
+  __hip_atomic_store(abort_word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Load N tagged words until every tag equals `tag` (or the launch is aborted).  Per lane.
+template <int N>
+__device__ __forceinline__ void wait_words(const u64 *const (&addr)[N], uint32_t tag, uint32_t (&out)[N],
+                                           uint32_t *abort_word, uint32_t *sticky) {
+  u64 v[N];
+  for (int it = 0;; ++it) {
+#pragma unroll
+    for (int e = 0; e < N; ++e) v[e] = get_word(addr[e]);
+    bool ok = true;
+#pragma unroll
+    for (int e = 0; e < N; ++e) ok = ok && (uint32_t)(v[e] >> 32) == tag;
+    if (ok) break;
+    if (get_flag(abort_word) != 0u) break;
+    if (it >= SPIN_MAX) {
+      raise_abort(abort_word, sticky);
+      break;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < N; ++e) out[e] = (uint32_t)v[e];
+}
+
+// ---------------------------------------------------------------------------
+// Chain block
+
+struct Ctx {
+  const StepArgs *a;
+  ChainLds *s;
+  int *slot, *dil;
+  uint32_t *rbase;  // byte offset of each layer's queue in the queue region
+  uint32_t *qoff;   // [2][L]: byte offset of the rows of the current slot (0) and the next step's (1)
+  char *ring;       // queue region
+  uint32_t rowb;    // byte offset of this lane's 16-byte chunk of a queue row (wave B)
+  const float *conv_b, *res_b, *head_b, *out_b, *emb_b;
+  const char *fw;   // this wave's fragment stream (wave-uniform)
+  const char *nxt;  // next fragment the ring loads (the stream is read in order, wrapping at its end)
+  int wvoff;        // 16 * lane
+  u64 *zp;          // this block's z^0 words (layer l at + l * ZWORDS)
+  const u64 *sp;    // this block's relu(skip sum) words
+  uint32_t *abort_word, *sticky;
+  bool local;       // the helpers share this block's XCD: workgroup-scope stores suffice
+  int L, w, p, lane, n, q, b0, nrows, blk;
+};
+
+__device__ __forceinline__ u32x4 frag_at(const Ctx &c, int pos) {
+  return *(const u32x4 *)(c.fw + (size_t)pos * 1024 + c.wvoff);
+}
+// Slot `f` of ring W has just been consumed: load the stream's next fragment into it.  The ring is a
+// FIFO over the stream, so the next fragment is always one ring length past the one consumed.
+// The scheduling barriers keep the load after the MFMA that still reads the slot's old contents.
+template <int D>
+__device__ __forceinline__ void refill(Ctx &c, u32x4 (&W)[D], int f) {
+  __builtin_amdgcn_sched_barrier(0);
+  W[f] = *(const u32x4 *)(c.nxt + c.wvoff);
+  c.nxt += 1024;
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Queue rows moved by wave B of pair p: stream rows 4p..4p+3, lane l handling row 4p + (l%32)/8
+// and 16-byte chunk l%8 (lanes 32..63 mirror lanes 0..31 on loads and skip the stores).  The lane
+// that pushes a row chunk is the lane that later pops it, so program order keeps every pop after
+// the push it must see.
+// Pop of layer l for the step `ahead` (0 or 1) steps after the one the offset table describes.
+__device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int l, int ahead) {
+  return *(const u32x4 *)(c.ring + (c.qoff[ahead * c.L + l] + c.rowb));
+}
+__device__ __forceinline__ void pop_land(const Ctx &c, int parity, u32x4 v) {
+  if (c.lane < 32) {
+    const int r = 4 * c.p + (c.lane >> 3);
+    *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
+  }
+}
+// Push of layer l: its input x^l replaces the slot popped for this step.
+__device__ __forceinline__ void push_rows(const Ctx &c, int l) {
+  if (c.lane < 32) {
+    const int r = 4 * c.p + (c.lane >> 3);
+    const u32x4 v = *(const u32x4 *)(c.s->xbuf[l & 1] + r * PX + 8 * (c.lane & 7));
+    *(u32x4 *)(c.ring + (c.qoff[l] + c.rowb)) = v;
+  }
+}
+// z^l of stream rows 4p..4p+3 to the helpers: lane l covers row 4p + l/16, channels 4(l%16)..+3,
+// as two words of two bf16 each (word index = row * 32 + channel / 2).
+__device__ __forceinline__ void publish_z(const Ctx &c, int l, uint32_t tag) {
+  const int r = 4 * c.p + (c.lane >> 4), cp = 2 * (c.lane & 15);
+  const u32x2 v = *(const u32x2 *)(c.s->zbuf[l & 1] + r * PX + 2 * cp);
+  u64 *zw = c.zp + (size_t)l * ZWORDS + r * (R / 2) + cp;
+  put_word(zw, v.x, tag, c.local);
+  put_word(zw + 1, v.y, tag, c.local);
+}
+
+// W_r v + b of layer ln from the popped rows in vbuf[vb3] and ring slots f0..f0+3 (tanh tile p
+// k-steps 0,1, sigmoid tile p k-steps 0,1), into pbuf[par].
+template <int D>
+__device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int vb3, int par, const u32x4 (&W)[D], int f0) {
+  ChainLds &s = *c.s;
+  const uint16_t *vb = s.vbuf[vb3] + c.n * PX;
+  const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
+  const float *cb = c.conv_b + ln * 2 * R;
+  f32x4 pt = ldsf4(cb + 16 * c.p + 4 * c.q), pg = ldsf4(cb + R + 16 * c.p + 4 * c.q);
+  pt = mfma(W[f0 + 0], bv0, pt);
+  pg = mfma(W[f0 + 2], bv0, pg);
+  pt = mfma(W[f0 + 1], bv1, pt);
+  pg = mfma(W[f0 + 3], bv1, pg);
+  stf4(s.pbuf[par][c.p][0] + c.n * PP + 4 * c.q, pt);
+  stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
+}
+
+// Per-step inputs of steps [s0, s0 + KCH) into LDS (every thread, in the head before its first
+// barrier): uniforms for generation, else the forced input that follows each step.
+__device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
+  const StepArgs &a = *c.a;
+  ChainLds &s = *c.s;
+  static_assert((ROWS * KCH) % NT == 0, "the chunk divides evenly over the threads");
+#pragma unroll
+  for (int e = 0; e < ROWS * KCH / NT; ++e) {
+    const int idx = (int)threadIdx.x + e * NT;
+    const int r = idx / KCH, j = idx % KCH;
+    const long long st = s0 + j;
+    if (a.mode != MODE_GENERATE) {
+      const long long nx = st + forced_shift(a.mode);
+      int v = 0;
+      if (r < c.nrows && nx < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + nx];
+      s.chunk.in[r][j] = v;
+    } else {
+      float v = 0.f;
+      if (r < c.nrows && st < a.n_steps) v = a.uniforms[(long long)(c.b0 + r) * a.n_steps + st];
+      s.chunk.u[r][j] = v;
+    }
+  }
+}
+
+// Layer l on wave A, ring slots PHS..PHS+5 (x-half of tanh/sigmoid tile p, residual tile p).
+template <int PHS>
+__device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xres) {
+  ChainLds &s = *c.s;
+  const int n = c.n, q = c.q, p = c.p;
+  const int par = l & 1;
+  u32x4 bx0, bx1;
+  if (l == 0) {
+    // embedding (current input x^0): row gather of the transposed 1x1 convolution plus bias
+    const uint16_t *e = s.embT + s.ins[n] * R;
+    const u32x4 r0 = lds16(e + 8 * q), r1 = lds16(e + 32 + 8 * q);
+    const float *eb = c.emb_b;
+    auto cvt = [&](u32x4 raw, int k0) {
+      u32x4 pk;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pk[j] = pack2(bf_lo(raw[j]) + eb[k0 + 2 * j], bf_hi(raw[j]) + eb[k0 + 2 * j + 1]);
+      return pk;
+    };
+    bx0 = cvt(r0, 8 * q);
+    bx1 = cvt(r1, 32 + 8 * q);
+    const int ch = 16 * p + 4 * q;
+    const u32x2 raw = *(const u32x2 *)(e + ch);
+    xres = f32x4{bf_lo(raw.x) + eb[ch], bf_hi(raw.x) + eb[ch + 1], bf_lo(raw.y) + eb[ch + 2], bf_hi(raw.y) + eb[ch + 3]};
+    lds8(s.xbuf[0] + n * PX + ch, pack4(xres));
+  } else {
+    const uint16_t *xb = s.xbuf[par] + n * PX;
+    bx0 = lds16(xb + 8 * q);
+    bx1 = lds16(xb + 32 + 8 * q);
+  }
+  f32x4 af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q);
+  f32x4 ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
+  af = mfma(W[PHS + 0], bx0, af);
+  ag = mfma(W[PHS + 2], bx0, ag);
+  af = mfma(W[PHS + 1], bx1, af);
+  ag = mfma(W[PHS + 3], bx1, ag);
+#pragma unroll
+  for (int f = 0; f < 4; ++f) refill(c, W, PHS + f);
+  f32x4 z;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) z[i] = gate(af[i], ag[i]);
+  lds8(s.zbuf[par] + n * PX + 16 * p + 4 * q, pack4(z));
+  __syncthreads();
+  const uint16_t *zb = s.zbuf[par] + n * PX;
+  const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
+  f32x4 xr = xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
+  xr = mfma(W[PHS + 4], bz0, xr);
+  xr = mfma(W[PHS + 5], bz1, xr);
+#pragma unroll
+  for (int f = 4; f < FA; ++f) refill(c, W, PHS + f);
+  xres = xr;
+  lds8(s.xbuf[par ^ 1] + n * PX + 16 * p + 4 * q, pack4(xr));
+  __syncthreads();
+}
+
+// Layer l on wave B, ring slots PBS..PBS+3 (W_r of the next layer), pop registers rotated by
+// G6 = l mod 6 (L is a multiple of 6, so this is also the global layer index mod 6): the pop of
+// global layer index g sits in P[g mod 6] from its issue, five layers ahead of landing, until it
+// lands in vbuf[g mod 3] after layer g - 3, two block barriers before its product.
+template <int PBS, int G6>
+__device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P)[6], uint32_t tag) {
+  const int L = c.L;
+  const int ln = l + 1 < L ? l + 1 : 0;
+  recurrent_half(c, ln, (G6 + 1) % 3, (l + 1) & 1, W, PBS);
+#pragma unroll
+  for (int f = 0; f < FB; ++f) refill(c, W, PBS + f);
+  __syncthreads();
+  __syncthreads();
+  // after the layer: its gate output to the helpers, its input into its queue, the pop of layer
+  // l + 3 into LDS and the pop of layer l + 8 issued
+  publish_z(c, l, tag);
+  push_rows(c, l);
+  pop_land(c, G6 % 3, P[(G6 + 3) % 6]);
+  const int j = l + 8 < L ? l + 8 : l + 8 - L;
+  P[(G6 + 2) % 6] = pop_issue(c, j, l + 8 < L ? 0 : 1);
+}
+
+// The head of step `step` on any wave (ring depth D; the head is the last FHD fragments of the
+// wave's stream): relu(skip sum) from the helpers, first 1x1 + relu, output 1x1, then the sample
+// (or the logits), the next inputs and the slot advance.  Four barriers.
+template <int D>
+__device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[D]) {
+  ChainLds &s = *c.s;
+  const StepArgs &a = *c.a;
+  const int n = c.n, q = c.q, w = c.w, tid = threadIdx.x;
+  if (step % KCH == 0) stage_chunk(c, step);
+  {
+    // thread t: stream t/32, skip channels 16 (t%32) .. +15 (8 words)
+    const int r = tid >> 5, ch = 16 * (tid & 31);
+    const u64 *addr[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) addr[e] = c.sp + r * (S / 2) + ch / 2 + e;
+    uint32_t v[8];
+    wait_words<8>(addr, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
+    *(u32x4 *)(s.u.sbuf + r * PS + ch) = u32x4{v[0], v[1], v[2], v[3]};
+    *(u32x4 *)(s.u.sbuf + r * PS + ch + 8) = u32x4{v[4], v[5], v[6], v[7]};
+  }
+  __syncthreads();
+  f32x4 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = ldsf4(c.head_b + 16 * (4 * w + j) + 4 * q);
+  u32x4 b = u32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int g = 0; g < 64; ++g) {
+    const int ks = g / 4, j = g % 4;
+    if (j == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
+    acc[j] = mfma(W[g % D], b, acc[j]);
+    if (g == FHD - D) c.nxt = c.fw;  // the ring wraps to the start of the next step
+    refill(c, W, g % D);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 16 * (4 * w + j) + 4 * q, pack4(relu4(acc[j])));
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 2; ++j) acc[j] = ldsf4(c.out_b + 16 * (2 * w + j) + 4 * q);
+#pragma unroll
+  for (int g = 64; g < FHD; ++g) {
+    const int ks = (g - 64) / 2, j = (g - 64) % 2;
+    if (j == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
+    acc[j] = mfma(W[g % D], b, acc[j]);
+    if (g == FHD - D) c.nxt = c.fw;
+    refill(c, W, g % D);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) stf4(s.u.lg + n * PL + 16 * (2 * w + j) + 4 * q, acc[j]);
+  __syncthreads();
+  // rows w and w + 8: sample (generation) or write the logits (forced modes)
+  if (a.mode != MODE_GENERATE) {
+#pragma unroll
+    for (int kk = 0; kk < ROWS / NW; ++kk) {
+      const int r = w + NW * kk;
+      if (r < c.nrows && a.logits) {
+        const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
+        *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
+      }
+    }
+    if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < ROWS / NW; ++kk) {
+      const int r = w + NW * kk;
+      if (r < c.nrows) {
+        const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
+        if (c.lane == 0) {
+          a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
+          s.ins[r] = k;
+        }
+      }
+    }
+  }
+  for (int l = tid; l < c.L; l += NT) {
+    const int nx = c.slot[l] + 1 == c.dil[l] ? 0 : c.slot[l] + 1;
+    const int nn = nx + 1 == c.dil[l] ? 0 : nx + 1;
+    c.slot[l] = nx;
+    c.qoff[l] = c.qoff[c.L + l];
+    c.qoff[c.L + l] = c.rbase[l] + (uint32_t)nn * (uint32_t)(a.bmax * R * 2);
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void a_role(Ctx &c) {
+  const int L = c.L;
+  c.fw = (const char *)c.a->mf_frags + base_a(L, c.p) * 1024;
+  u32x4 W[DA];
+#pragma unroll
+  for (int f = 0; f < DA; ++f) W[f] = frag_at(c, f);
+  c.nxt = c.fw + DA * 1024;
+  f32x4 xres = f32x4{0.f, 0.f, 0.f, 0.f};
+  __syncthreads();  // the popped rows of layers 0 and 1 are in LDS
+  __syncthreads();  // W_r v + b of layer 0 is in LDS
+  for (long long step = 0; step < c.a->n_steps; ++step) {
+    for (int l = 0; l < L; l += 6) {
+      a_layer<0>(c, l, W, xres);
+      a_layer<FA>(c, l + 1, W, xres);
+      a_layer<0>(c, l + 2, W, xres);
+      a_layer<FA>(c, l + 3, W, xres);
+      a_layer<0>(c, l + 4, W, xres);
+      a_layer<FA>(c, l + 5, W, xres);
+    }
+    head<DA>(c, step, W);
+  }
+}
+
+__device__ __forceinline__ void b_role(Ctx &c) {
+  const int L = c.L;
+  c.fw = (const char *)c.a->mf_frags + base_b(L, c.p) * 1024;
+  u32x4 W[DB], P[6];
+  // layers 0..2 of step 0 land now; layer 0's W_r v + b comes from its stream stage L - 1
+  pop_land(c, 0, pop_issue(c, 0, 0));
+  pop_land(c, 1, pop_issue(c, 1, 0));
+  pop_land(c, 2, pop_issue(c, 2, 0));
+#pragma unroll
+  for (int g = 3; g < 8; ++g) P[g % 6] = pop_issue(c, g, 0);
+  __syncthreads();
+#pragma unroll
+  for (int f = 0; f < FB; ++f) W[f] = frag_at(c, FB * (L - 1) + f);
+  recurrent_half(c, 0, 0, 0, W, 0);
+#pragma unroll
+  for (int f = 0; f < DB; ++f) W[f] = frag_at(c, f);
+  c.nxt = c.fw + DB * 1024;
+  __syncthreads();
+  for (long long step = 0; step < c.a->n_steps; ++step) {
+    const uint32_t tag = (uint32_t)(step + 1);
+    for (int l = 0; l < L; l += 6) {
+      b_layer<0, 0>(c, l, W, P, tag);
+      b_layer<FB, 1>(c, l + 1, W, P, tag);
+      b_layer<2 * FB, 2>(c, l + 2, W, P, tag);
+      b_layer<3 * FB, 3>(c, l + 3, W, P, tag);
+      b_layer<4 * FB, 4>(c, l + 4, W, P, tag);
+      b_layer<5 * FB, 5>(c, l + 5, W, P, tag);
+    }
+    head<DB>(c, step, W);
+  }
+}
+
+__device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, int blk) {
+  ChainLds &s = *(ChainLds *)lds_raw;
+  const int tid = threadIdx.x, L = a.L;
+  char *dyn = lds_raw + chain_fixed_bytes();
+  int *slot = (int *)dyn;
+  int *dil = slot + L;
+  uint32_t *rbase = (uint32_t *)(dil + L);
+  uint32_t *qoff = rbase + L;
+  float *bias = (float *)(dyn + dyn_bias_offset(L));  // conv_b [L][2R], res_b [L][R], skip sum [S], head_b, out_b, emb_b
+
+  Ctx c;
+  c.a = &a;
+  c.s = &s;
+  c.slot = slot;
+  c.dil = dil;
+  c.rbase = rbase;
+  c.qoff = qoff;
+  c.ring = (char *)a.ring;
+  c.conv_b = bias;
+  c.res_b = c.conv_b + L * 2 * R;
+  c.head_b = c.res_b + L * R + S;
+  c.out_b = c.head_b + H;
+  c.emb_b = c.out_b + Q;
+  c.L = L;
+  c.w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  c.p = c.w & 3;
+  c.lane = tid & 63;
+  c.n = c.lane & 15;
+  c.q = c.lane >> 4;
+  c.blk = blk;
+  c.b0 = blk * ROWS;
+  c.nrows = min(ROWS, a.batch - c.b0);
+  c.wvoff = 16 * c.lane;
+  c.rowb = (uint32_t)(((c.b0 + 4 * c.p + ((c.lane & 31) >> 3)) * R + 8 * (c.lane & 7)) * 2);
+  c.zp = comm_z(a.sp_comm, L, blk, 0);
+  c.sp = comm_s(a.sp_comm, L, a.sp_nb, blk);
+  c.abort_word = (uint32_t *)a.sp_comm;
+  c.sticky = a.sp_sticky;
+
+  const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
+  for (int i = tid; i < Q * R / 8; i += NT) ((u32x4 *)s.embT)[i] = embsrc[i];
+  const int nbias = L * 3 * R + S + H + Q + R;
+  for (int i = tid; i < nbias; i += NT) bias[i] = a.mf_bias[i];
+  const uint32_t slot_bytes = (uint32_t)(a.bmax * R * 2);
+  for (int l = tid; l < L; l += NT) {
+    const LayerDev ld = a.layers[l];
+    const int s0 = (int)(a.t0 % (long long)ld.dil), s1 = s0 + 1 == ld.dil ? 0 : s0 + 1;
+    rbase[l] = (uint32_t)(ld.ring_off * 2);
+    dil[l] = ld.dil;
+    slot[l] = s0;
+    qoff[l] = rbase[l] + (uint32_t)s0 * slot_bytes;
+    qoff[L + l] = rbase[l] + (uint32_t)s1 * slot_bytes;
+  }
+  if (tid < ROWS) {
+    int v = 0;
+    if (tid < c.nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
+    s.ins[tid] = v;
+  }
+  // launch handshake: read the helpers' XCD ids, publish the group's mode
+  u64 *hs = comm_h(a.sp_comm, L, a.sp_nb, blk);
+  if (tid < NHLP) {
+    const u64 *addr[1] = {hs + 1 + tid};
+    uint32_t v[1];
+    wait_words<1>(addr, 1, v, c.abort_word, c.sticky);
+    s.ins[ROWS + tid] = (int)v[0];
+  }
+  __syncthreads();
+  bool local = true;
+  for (int h = 0; h < NHLP; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
+  c.local = local;
+  if (tid == 0) put_word(hs + 5, local ? 1u : 0u, 1, false);
+  if (c.w < 4) a_role(c);
+  else b_role(c);
+  if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
+}
+
+// ---------------------------------------------------------------------------
+// Helper block (chain block blk, slice h): wave w takes layers w, w + 8, ...; for each it waits
+// for z^l, then accumulates the slice's 8 tiles x 2 k-steps.  At the end of a step the eight
+// waves' partial sums meet in LDS, get the summed skip biases, relu and bf16 rounding, and go to
+// the chain block as tagged words.
+
+__device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, int blk, int h) {
+  HelperLds &s = *(HelperLds *)lds_raw;
+  const int tid = threadIdx.x, L = a.L, nb = a.sp_nb;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, n = lane & 15, q = lane >> 4;
+  const int nl = (L - w + NW - 1) / NW;  // layers of this wave (L >= NW)
+  const char *fw = (const char *)a.mf_frags + base_h(L, h, w) * 1024;
+  const int wvoff = 16 * lane;
+  const u64 *zb = comm_z(a.sp_comm, L, blk, 0);
+  u64 *sw = comm_s(a.sp_comm, L, nb, blk);
+  uint32_t *abort_word = (uint32_t *)a.sp_comm;
+  const float *skip_sum = a.mf_bias + L * 3 * R + h * SL;
+  // launch handshake: publish this block's XCD, then learn whether the whole group shares it
+  u64 *hs = comm_h(a.sp_comm, L, nb, blk);
+  if (tid == 0) {
+    put_word(hs + 1 + h, xcd_id(), 1, false);
+    const u64 *addr[1] = {hs + 5};
+    uint32_t v[1];
+    wait_words<1>(addr, 1, v, abort_word, a.sp_sticky);
+    s.local = (int)v[0];
+  }
+  __syncthreads();
+  const bool local = s.local != 0;
+  u32x4 W[FS];
+#pragma unroll
+  for (int f = 0; f < FS; ++f) W[f] = *(const u32x4 *)(fw + f * 1024 + wvoff);
+  const char *nxt = fw + (nl > 1 ? FS * 1024 : 0);
+  for (long long step = 0; step < a.n_steps; ++step) {
+    const uint32_t tag = (uint32_t)(step + 1);
+    f32x4 acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < nl; ++i) {
+      const int l = w + NW * i;
+      // B operand rows of z^l: stream n, channels 8q..8q+7 (k-step 0) and 32 + 8q.. (k-step 1)
+      const u64 *zl = zb + (size_t)l * ZWORDS + n * (R / 2) + 4 * q;
+      const u64 *addr[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        addr[e] = zl + e;
+        addr[4 + e] = zl + 16 + e;
+      }
+      uint32_t v[8];
+      wait_words<8>(addr, tag, v, abort_word, a.sp_sticky);
+      const u32x4 b0 = u32x4{v[0], v[1], v[2], v[3]}, b1 = u32x4{v[4], v[5], v[6], v[7]};
+      if (i + 1 == nl) nxt = fw;  // the next layer of this wave is its first of the next step
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        acc[j] = mfma(W[2 * j], b0, acc[j]);
+        __builtin_amdgcn_sched_barrier(0);
+        W[2 * j] = *(const u32x4 *)(nxt + wvoff);
+        __builtin_amdgcn_sched_barrier(0);
+        acc[j] = mfma(W[2 * j + 1], b1, acc[j]);
+        __builtin_amdgcn_sched_barrier(0);
+        W[2 * j + 1] = *(const u32x4 *)(nxt + 1024 + wvoff);
+        __builtin_amdgcn_sched_barrier(0);
+        nxt += 2048;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) stf4(s.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
+    __syncthreads();
+    // thread t: words 2t, 2t+1 of the slice's 1024 (stream jw / 64, channels 2 (jw % 64), +1)
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const int jw = 2 * tid + e, r = jw >> 6, cp = jw & 63;
+      float v0 = skip_sum[2 * cp], v1 = skip_sum[2 * cp + 1];
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) {
+        v0 += s.part[ww][r * PH + 2 * cp];
+        v1 += s.part[ww][r * PH + 2 * cp + 1];
+      }
+      put_word(sw + r * (S / 2) + h * (SL / 2) + cp, pack2(fmaxf(v0, 0.f), fmaxf(v1, 0.f)), tag, local);
+    }
+    __syncthreads();
+  }
+}
+
+__global__ void __launch_bounds__(NT) split_step_kernel(StepArgs a) {
+  extern __shared__ float4 lds_raw[];
+  const int nb = a.sp_nb;
+  if ((int)blockIdx.x < nb) {
+    chain_block(a, (char *)lds_raw, blockIdx.x);
+  } else {
+    const int e = (int)blockIdx.x - nb;
+    helper_block(a, (char *)lds_raw, e % nb, e / nb);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Repacking into the per-wave fragment streams.  Fragment (tile t, k-step ks) of a matrix
+// M[out][k] gives lane l the 8 values M[16t + l%16][32ks + 8(l/16) + j].
+
+__device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int o, int k) {
+  return conv[(o * R + (k % R)) * 2 + (k >= R ? 1 : 0)];
+}
+__device__ __forceinline__ uint4 pack8(const uint16_t *v) {
+  return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
+}
+
+// Layer l: A wave p stream position 6l + f (f 0..3: x-half of tanh tile p k-steps 2,3 and sigmoid
+// tile p k-steps 2,3; f 4,5: residual tile p k-steps 0,1); B wave p stream position 4 ((l-1) mod L)
+// + f (v-half of tanh tile p k-steps 0,1, sigmoid tile p k-steps 0,1); helper (h, l % 8) position
+// 16 (l / 8) + 2j + ks (skip tile 8h + j, k-step ks).
+constexpr int LAYER_FRAGS = 4 * FA + 4 * FB + NHLP * FS;
+__global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, int l, int L,
+                                   uint4 *frags) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= LAYER_FRAGS * 64) return;
+  const int lane = e % 64, m = lane % 16, kq = 8 * (lane / 16);
+  int fi = e / 64;
+  uint16_t v[8];
+  size_t dst;
+  if (fi < 4 * FA) {
+    const int p = fi / FA, f = fi % FA;
+    for (int j = 0; j < 8; ++j)
+      v[j] = f < 4 ? conv_elem(conv, (f < 2 ? 0 : R) + 16 * p + m, R + 32 * (f & 1) + kq + j)
+                   : res[(16 * p + m) * R + 32 * (f - 4) + kq + j];
+    dst = base_a(L, p) + (size_t)FA * l + f;
+  } else if ((fi -= 4 * FA) < 4 * FB) {
+    const int p = fi / FB, f = fi % FB;
+    for (int j = 0; j < 8; ++j) v[j] = conv_elem(conv, (f < 2 ? 0 : R) + 16 * p + m, 32 * (f & 1) + kq + j);
+    dst = base_b(L, p) + (size_t)FB * ((l + L - 1) % L) + f;
+  } else {
+    fi -= 4 * FB;
+    const int h = fi / FS, f = fi % FS, t = NW * h + f / 2, ks = f % 2;
+    for (int j = 0; j < 8; ++j) v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
+    dst = base_h(L, h, l % NW) + (size_t)FS * (l / NW) + f;
+  }
+  frags[dst * 64 + lane] = pack8(v);
+}
+
+// Head of wave w (A for w < 4, B otherwise), stream positions FA L + g (A) or FB L + g (B):
+// g < 64 first 1x1 tile 4w + g%4, k-step g/4; g >= 64 output tile 2w + (g-64)%2, k-step (g-64)/2.
+__global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, int L, uint4 *frags) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= NW * FHD * 64) return;
+  const int lane = e % 64, g = (e / 64) % FHD, w = e / (64 * FHD);
+  const int m = lane % 16, kq = 8 * (lane / 16);
+  uint16_t v[8];
+  for (int j = 0; j < 8; ++j) {
+    if (g < 64) {
+      const int t = 4 * w + g % 4, ks = g / 4;
+      v[j] = head[(16 * t + m) * S + 32 * ks + kq + j];
+    } else {
+      const int t = 2 * w + (g - 64) % 2, ks = (g - 64) / 2;
+      v[j] = out[(16 * t + m) * H + 32 * ks + kq + j];
+    }
+  }
+  const size_t dst = w < 4 ? base_a(L, w) + (size_t)FA * L + g : base_b(L, w - 4) + (size_t)FB * L + g;
+  frags[dst * 64 + lane] = pack8(v);
+}
+
+}  // namespace sp
+
+size_t split_frag_bytes(int L) { return sp::base_h(L, sp::NHLP, 0) * 1024; }
+
+size_t split_comm_bytes(int L, int nb) {
+  return 256 + ((size_t)nb * L * sp::ZWORDS + (size_t)nb * sp::SWORDS + (size_t)nb * sp::HWORDS) *
+                   sizeof(unsigned long long);
+}
+
+size_t split_lds_bytes(int L) {
+  const size_t chain = sp::chain_fixed_bytes() + sp::dyn_bias_offset(L) + sizeof(float) * mfma_bias_floats(L);
+  const size_t helper = sizeof(sp::HelperLds);
+  return chain > helper ? chain : helper;
+}
+
+hipError_t launch_split_step(const StepArgs &a, hipStream_t s) {
+  const dim3 grid(a.sp_nb * (1 + kSpHelpers)), block(kMfThreads);
+  hipLaunchKernelGGL(sp::split_step_kernel, grid, block, split_lds_bytes(a.L), s, a);
+  return hipGetLastError();
+}
+
+hipError_t split_setup(int L, int nb, int *coresident_ok) {
+  const size_t lds = split_lds_bytes(L);
+  hipError_t e = hipFuncSetAttribute((const void *)sp::split_step_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)lds);
+  if (e != hipSuccess) return e;
+  int per_cu = 0, dev = 0, cus = 0;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, sp::split_step_kernel, kMfThreads, lds)) != hipSuccess)
+    return e;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  *coresident_ok = (long long)per_cu * cus >= (long long)nb * (1 + kSpHelpers);
+  return hipSuccess;
+}
+
+hipError_t launch_split_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
+                                     hipStream_t s) {
+  const int n = sp::LAYER_FRAGS * 64;
+  hipLaunchKernelGGL(sp::repack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)conv,
+                     (const uint16_t *)res, (const uint16_t *)skip, l, L, (uint4 *)frags);
+  return hipGetLastError();
+}
+
+hipError_t launch_split_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s) {
+  const int n = kMfWaves * kSpFHead * 64;
+  hipLaunchKernelGGL(sp::repack_head_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)head,
+                     (const uint16_t *)out, L, (uint4 *)frags);
+  return hipGetLastError();
+}
+
+}  // namespace fwg

@@ -59,6 +59,8 @@ FAMILIES = {
     "gated_r64_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
+    # 12 layers: the split MFMA kernels (chain block + skip helper blocks; L a multiple of 6, >= 12)
+    "gated_r64_bf16_split": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 2, 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
     "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
@@ -79,7 +81,9 @@ FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu"}
 def tf(fw, x, path):
     """Teacher forcing through the step kernels ("step", fwg_teacher_forced) or the time-parallel
     kernels ("parallel", fwg_teacher_forced_parallel)."""
-    return (fw.teacher_forced if path == "step" else fw.teacher_forced_parallel)(dev(x)).cpu().numpy()
+    out = (fw.teacher_forced if path == "step" else fw.teacher_forced_parallel)(dev(x)).cpu().numpy()
+    fw.device_status()
+    return out
 
 
 def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, valu_stage=None):
@@ -105,7 +109,9 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
         if fam in FORCE_VALU:
             assert fw.regime == "valu", (fam, fw.regime)
         elif mfma_shape:
-            assert fw.regime.startswith("mfma"), (fam, fw.regime)
+            # the split kernels take layer counts that are multiples of 6, at least 12
+            split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
+            assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
             assert fw.regime in ("valu", "wave"), (fam, fw.regime)
         if fam in WAVE_FAMILIES:
@@ -117,6 +123,7 @@ def check_generation(cfg, fw, orc, u, batch, label):
     """Sampled-sequence parity with near-tie accounting + whole-sequence admissibility."""
     tau = TAU[cfg.dtype]
     g = fw.generate(dev(u)).cpu().numpy()
+    fw.device_status()
     so, lo_ = orc.state(batch).generate(u, return_logits=True)
     n = u.shape[1]
     first = []
@@ -277,7 +284,7 @@ def test_generation_parity(fam):
 
 
 @pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r16_s32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu",
-                                 "gated_r64_w3_bf16"])
+                                 "gated_r64_w3_bf16", "gated_r64_bf16_split"])
 def test_online_prediction_parity(fam):
     """Online prediction (fwg_step_forced): generate, feed observed samples from the same queues,
     generate again.  The oracle is driven through the same history (the GPU's own samples, then the
@@ -398,7 +405,7 @@ def test_uniform_logits_sampler_gpu():
     assert np.array_equal(g, np.floor(u.astype(np.float64) * 256).astype(np.int32))
 
 
-@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd"])
+@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split"])
 def test_continuation_reset_and_determinism_gpu(fam):
     cfg = FAMILIES[fam]
     w, fw, _ = build_pair(cfg, 7, 9, fam=fam)
@@ -505,7 +512,8 @@ def test_full_bench_workload():
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     t0 = time.time()
     g = fw.generate(dev(u)).cpu().numpy()
-    log(f"{wl.name}: GPU generation {wl.batch}x{wl.n_steps} in {time.time() - t0:.1f}s")
+    fw.device_status()
+    log(f"{wl.name}: GPU generation {wl.batch}x{wl.n_steps} in {time.time() - t0:.1f}s ({fw.regime})")
     assert g.min() >= 0 and g.max() <= 255
     _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 255], wl.n_steps)
 
