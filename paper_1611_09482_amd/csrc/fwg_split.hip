@@ -28,17 +28,17 @@
 // Chain block: 8 waves, A = waves 0..3 and B = waves 4..7, A and B of pair p share SIMD p.
 //  - wave A (p): the current-input half of the dilated product (W_e x) for tanh tile p and
 //    sigmoid tile p, plus W_r v + b from LDS, the gate, the residual 1x1 for channel tile p;
-//  - wave B (p): W_r v + b of the next layer (v = the popped state, known early), the queue pops
-//    (issued five layers before they land in LDS) and pushes of stream rows 4p..4p+3, and the
-//    publication of z^l to the helpers.  B's memory work for layer l runs after the layer's second
-//    barrier, beside A's product for layer l + 1 (z and x are double-buffered, the popped rows
-//    triple-buffered), so its stores stay off the layer-to-layer chain;
+//  - wave B (p): W_r v + b of the next layer (v = the popped state, known early); between the
+//    layer's two barriers, while A runs the residual product, the publication of z^l to the
+//    helpers, the push of the layer input (stream rows 4p..4p+3) and the queue pops, issued five
+//    layers before they land in LDS;
 //  - both: the head (first 1x1: four tiles per wave, output 1x1: two tiles per wave) and two
 //    sampled rows per wave.
 // Every wave streams its own pre-packed weight fragments from L2 through a ring of registers:
-// 12 fragments (two layers) for A, 24 (six layers) for B, whose loads also queue behind the HBM
-// queue reads; a slot is refilled with the fragment one ring length ahead as soon as it is consumed.
-// The layer loop is unrolled by six layers so every ring slot is a fixed register.
+// 12 fragments (two layers) for A, 24 (six layers) for B, whose loads also queue behind the queue
+// reads; a slot is refilled with the fragment one ring length ahead as soon as it is consumed.  The
+// head, a pure stream of 96 fragments per wave, runs both rings 24 deep.  The layer loop is
+// unrolled by six layers so every ring slot is a fixed register.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -62,7 +62,8 @@ constexpr int FA = kSpFA, FB = kSpFB, FHD = kSpFHead, FS = kSpFS;
 constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
 constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
-static_assert(FHD % DA == 0 && FHD % DB == 0, "the head consumes whole rings");
+constexpr int DHEAD = 24;                // ring depth of every wave in the head
+static_assert(FHD % DHEAD == 0 && DHEAD % DA == 0 && DHEAD == DB, "the head consumes whole rings");
 static_assert(SL == 8 * 16 && FS == 16, "a helper wave covers its slice as 8 tiles x 2 k-steps");
 
 typedef unsigned long long u64;
@@ -271,7 +272,7 @@ __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
 
 // Layer l on wave A, ring slots PHS..PHS+5 (x-half of tanh/sigmoid tile p, residual tile p).
 template <int PHS>
-__device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xres) {
+__device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DHEAD], f32x4 &xres) {
   ChainLds &s = *c.s;
   const int n = c.n, q = c.q, p = c.p;
   const int par = l & 1;
@@ -335,24 +336,26 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
 #pragma unroll
   for (int f = 0; f < FB; ++f) refill(c, W, PBS + f);
   __syncthreads();
-  __syncthreads();
-  // after the layer: its gate output to the helpers, its input into its queue, the pop of layer
-  // l + 3 into LDS and the pop of layer l + 8 issued
   publish_z(c, l, tag);
   push_rows(c, l);
   pop_land(c, G6 % 3, P[(G6 + 3) % 6]);
   const int j = l + 8 < L ? l + 8 : l + 8 - L;
   P[(G6 + 2) % 6] = pop_issue(c, j, l + 8 < L ? 0 : 1);
+  __syncthreads();
 }
 
-// The head of step `step` on any wave (ring depth D; the head is the last FHD fragments of the
-// wave's stream): relu(skip sum) from the helpers, first 1x1 + relu, output 1x1, then the sample
-// (or the logits), the next inputs and the slot advance.  Four barriers.
-template <int D>
-__device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[D]) {
+// The head of step `step` on any wave (layer ring depth D, head ring depth DH; the head is the
+// last FHD fragments of the wave's stream): relu(skip sum) from the helpers, first 1x1 + relu,
+// output 1x1, then the sample (or the logits), the next inputs and the slot advance.  Four
+// barriers.  Slots D..DH-1 are loaded before the wait for the skip sums; the last refills load the
+// next step's first D fragments only, where the layer loop expects them.
+template <int D, int DH>
+__device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[DH]) {
   ChainLds &s = *c.s;
   const StepArgs &a = *c.a;
   const int n = c.n, q = c.q, w = c.w, tid = threadIdx.x;
+#pragma unroll
+  for (int f = D; f < DH; ++f) refill(c, W, f);
   if (step % KCH == 0) stage_chunk(c, step);
   {
     // thread t: stream t/32, skip channels 16 (t%32) .. +15 (8 words)
@@ -374,9 +377,9 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[D]) {
   for (int g = 0; g < 64; ++g) {
     const int ks = g / 4, j = g % 4;
     if (j == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
-    acc[j] = mfma(W[g % D], b, acc[j]);
-    if (g == FHD - D) c.nxt = c.fw;  // the ring wraps to the start of the next step
-    refill(c, W, g % D);
+    acc[j] = mfma(W[g % DH], b, acc[j]);
+    if (g == FHD - DH) c.nxt = c.fw;  // the ring wraps to the start of the next step
+    if (g < FHD - DH + D) refill(c, W, g % DH);
   }
 #pragma unroll
   for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 16 * (4 * w + j) + 4 * q, pack4(relu4(acc[j])));
@@ -387,9 +390,9 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[D]) {
   for (int g = 64; g < FHD; ++g) {
     const int ks = (g - 64) / 2, j = (g - 64) % 2;
     if (j == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
-    acc[j] = mfma(W[g % D], b, acc[j]);
-    if (g == FHD - D) c.nxt = c.fw;
-    refill(c, W, g % D);
+    acc[j] = mfma(W[g % DH], b, acc[j]);
+    if (g == FHD - DH) c.nxt = c.fw;
+    if (g < FHD - DH + D) refill(c, W, g % DH);
   }
 #pragma unroll
   for (int j = 0; j < 2; ++j) stf4(s.u.lg + n * PL + 16 * (2 * w + j) + 4 * q, acc[j]);
@@ -431,7 +434,7 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[D]) {
 __device__ __forceinline__ void a_role(Ctx &c) {
   const int L = c.L;
   c.fw = (const char *)c.a->mf_frags + base_a(L, c.p) * 1024;
-  u32x4 W[DA];
+  u32x4 W[DHEAD];  // slots DA.. are used by the head only
 #pragma unroll
   for (int f = 0; f < DA; ++f) W[f] = frag_at(c, f);
   c.nxt = c.fw + DA * 1024;
@@ -447,7 +450,7 @@ __device__ __forceinline__ void a_role(Ctx &c) {
       a_layer<0>(c, l + 4, W, xres);
       a_layer<FA>(c, l + 5, W, xres);
     }
-    head<DA>(c, step, W);
+    head<DA, DHEAD>(c, step, W);
   }
 }
 
@@ -479,7 +482,7 @@ __device__ __forceinline__ void b_role(Ctx &c) {
       b_layer<4 * FB, 4>(c, l + 4, W, P, tag);
       b_layer<5 * FB, 5>(c, l + 5, W, P, tag);
     }
-    head<DB>(c, step, W);
+    head<DB, DHEAD>(c, step, W);
   }
 }
 
