@@ -83,11 +83,11 @@ __host__ __device__ inline size_t mfma_frag_bytes(int L) { return kMfStageBytes 
 inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Split MFMA family (the MFMA family's model shape, L a multiple of 6 and at least 12): per 16
-// streams one chain block plus kSpHelpers helper blocks that own the skip products of S / kSpHelpers
-// channels each.  Fragments per layer of chain waves A and B, per head and chain wave, and per layer
-// and helper wave.
-constexpr int kSpHelpers = 4;
-constexpr int kSpFA = 6, kSpFB = 4, kSpFHead = 96, kSpFS = 16;
+// streams one chain block (layers and sampling) plus kSpHelpers helper blocks, each owning
+// S / kSpHelpers skip channels, H / kSpHelpers hidden channels and 256 / kSpHelpers classes.
+// Fragments per layer of chain waves A and B, and per layer and helper wave.
+constexpr int kSpHelpers = 8;
+constexpr int kSpFA = 6, kSpFB = 4, kSpFS = 8;
 inline bool split_layers_ok(int L) { return L % 6 == 0 && L >= 12; }
 size_t split_frag_bytes(int L);
 size_t split_comm_bytes(int L, int nb);

@@ -3,25 +3,28 @@
 // accumulation).  Same model shape and results as the MFMA step kernel of fwg_mfma.hip.
 //
 // The work of one step of a block of 16 streams is split over 1 + kSpHelpers blocks of the same
-// launch:
+// launch (a group):
 //  - the chain block runs what lies on the layer-to-layer dependency chain: per layer the pop, the
-//    dilated width-2 product, the gate, the residual 1x1 and the push (paper Section 2.2), then the
-//    head, the softmax and the inverse-CDF sample, which is the next step's input (Section 1);
-//  - helper block h accumulates, for skip channels [128h, 128h + 128), the skip 1x1 products of
-//    every layer, from the gate outputs z^l that the chain block publishes, and hands
-//    relu(skip sum) back for the head.
-// No later layer reads a skip product, and they are 49% of a step's weight bytes: the chain block
-// streams 40 KB of weights per layer instead of 104 KB, which is what bounds a step of the
-// single-block kernel (every block that owns streams streams every weight once per step).
+//    dilated width-2 product, the gate, the residual 1x1 and the push (paper Section 2.2), then
+//    the softmax and inverse-CDF sample of the logits the helpers return, which is the next step's
+//    input (Section 1);
+//  - helper h owns 64 of the 512 channels of the skip sum, of the head's hidden layer, and 32 of
+//    the 256 classes.  Per step it accumulates sum_l W_skip^l z^l + b for its skip channels from
+//    the gate outputs z^l the chain block publishes, then (after gathering the whole relu(skip
+//    sum) from the group) its rows of the first head 1x1, then (after gathering the whole hidden
+//    layer) its classes of the output 1x1.  Its head weights stay in LDS for the whole launch.
+// No later layer reads a skip product and the head follows the last layer, so the chain block
+// streams only the 40 KB of conv and residual weights per layer; in the single-block kernel every
+// block that owns streams streams all 4 MB of weights once per step, which bounds its step.
 //
 // Hand-offs between blocks are 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed
 // device-scope atomics.  A word is fresh once its tag equals the step's tag (step index in the
 // launch + 1; the exchange buffers are zeroed before every launch), so no fence or flag has to
-// order the payload.  The blocks of a group (a chain block and its helpers) compare their XCD ids
-// at launch: when they share one, and so its L2, the words are stored with workgroup-scope
-// stores, which complete in that L2; otherwise with device-scope stores, which write through to
-// memory and whose slow completion holds up every later memory wait of the storing wave.  Every wait is bounded: a wait that runs out sets the
-// launch's abort word, which ends every other wait (the results are then invalid, and a sticky
+// order the payload.  The blocks of a group compare their XCD ids at launch: when they share one,
+// and so its L2, the words are stored with workgroup-scope stores, which complete in that L2;
+// otherwise with device-scope stores, which write through to memory and whose slow completion holds
+// up every later memory wait of the storing wave.  Every wait is bounded: a wait that runs out sets
+// the launch's abort word, which ends every other wait (the results are then invalid, and a sticky
 // word lets the host report it); every wave keeps executing its straight-line program, so the grid
 // always drains.
 //
@@ -32,13 +35,11 @@
 //    layer's two barriers, while A runs the residual product, the publication of z^l to the
 //    helpers, the push of the layer input (stream rows 4p..4p+3) and the queue pops, issued five
 //    layers before they land in LDS;
-//  - both: the head (first 1x1: four tiles per wave, output 1x1: two tiles per wave) and two
-//    sampled rows per wave.
-// Every wave streams its own pre-packed weight fragments from L2 through a ring of registers:
-// 12 fragments (two layers) for A, 24 (six layers) for B, whose loads also queue behind the queue
-// reads; a slot is refilled with the fragment one ring length ahead as soon as it is consumed.  The
-// head, a pure stream of 96 fragments per wave, runs both rings 24 deep.  The layer loop is
-// unrolled by six layers so every ring slot is a fixed register.
+//  - both: two sampled rows per wave.
+// Every chain wave streams its own pre-packed weight fragments from L2 through a ring of registers,
+// 12 fragments (two layers) for A and 24 (six layers) for B, whose loads also queue behind the
+// queue reads; a slot is refilled with the fragment one ring length ahead as soon as it is
+// consumed.  The layer loop is unrolled by six layers so every ring slot is a fixed register.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -52,19 +53,19 @@ using namespace mfd;
 
 constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
 constexpr int NT = kMfThreads, NW = kMfWaves;
-constexpr int NHLP = kSpHelpers, SL = S / NHLP;  // helper blocks per chain block, skip channels each
+constexpr int NHLP = kSpHelpers;          // helpers per group
+constexpr int SL = S / NHLP, HL = H / NHLP, QL = Q / NHLP;  // skip / hidden / class slice of a helper
 constexpr int PX = R + 8;   // 64-channel activation rows (bf16)
 constexpr int PS = S + 8;   // 512-channel activation rows (bf16)
 constexpr int PL = Q + 4;   // fp32 logits rows
 constexpr int PP = 20;      // fp32 partial-tile rows
-constexpr int PH = SL + 4;  // fp32 helper partial rows
-constexpr int FA = kSpFA, FB = kSpFB, FHD = kSpFHead, FS = kSpFS;
-constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of waves A and B
+constexpr int PH = SL + 4;  // fp32 helper skip-partial rows
+constexpr int FA = kSpFA, FB = kSpFB, FS = kSpFS;
+constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);  // head fragments of a helper
+constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
 constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
-constexpr int DHEAD = 24;                // ring depth of every wave in the head
-static_assert(FHD % DHEAD == 0 && DHEAD % DA == 0 && DHEAD == DB, "the head consumes whole rings");
-static_assert(SL == 8 * 16 && FS == 16, "a helper wave covers its slice as 8 tiles x 2 k-steps");
+static_assert(SL == 64 && FS == 8 && HL == 64 && QL == 32, "helper slices of 4 skip, 4 hidden and 2 class tiles");
 
 typedef unsigned long long u64;
 
@@ -73,11 +74,7 @@ struct ChainLds {
   uint16_t xbuf[2][ROWS * PX];     // layer inputs x^l, by layer parity
   uint16_t zbuf[2][ROWS * PX];     // gate outputs z^l, by layer parity
   float pbuf[2][4][2][ROWS * PP];  // W_r v + b of a layer: [layer parity][tile][tanh / sigmoid]
-  uint16_t hbuf[ROWS * PS];        // relu(head hidden)
-  union {
-    uint16_t sbuf[ROWS * PS];      // relu(skip sum)
-    float lg[ROWS * PL];           // logits
-  } u;
+  float lg[ROWS * PL];             // logits
   uint16_t embT[Q * R];            // embedding table, [class][channel]
   union {
     float u[ROWS][KCH];
@@ -88,37 +85,49 @@ struct ChainLds {
   // bias block
 };
 struct HelperLds {
-  float part[NW][ROWS * PH];  // per-wave partial skip sums of the slice
-  int local;                  // the group's mode from the launch handshake
+  u32x4 w1[FW1 * 64];  // first head 1x1, rows of the hidden slice: [tile][k-step][lane]
+  u32x4 w2[FW2 * 64];  // output 1x1, rows of the class slice: [tile][k-step][lane]
+  union {
+    float part[NW][ROWS * PH];  // per-wave partial skip sums of the slice
+    uint16_t act[ROWS * PS];    // gathered relu(skip sum), then relu(hidden)
+  } u;
+  float pw[6][ROWS * PP];       // k-split partial tiles of the head products
+  float bias[SL + HL + QL];     // the slice's summed skip biases, hidden biases, class biases
+  int local;                    // the group's mode from the launch handshake
 };
 
 __host__ __device__ constexpr size_t chain_fixed_bytes() { return (sizeof(ChainLds) + 15) & ~size_t(15); }
 __host__ __device__ inline size_t dyn_bias_offset(int L) { return ((size_t)L * 20 + 15) & ~size_t(15); }
 
-// Fragment stream geometry (1 KB fragments): A wave p, B wave p, helper (slice h, wave w).
-__host__ __device__ inline int len_a(int L) { return FA * L + FHD; }
-__host__ __device__ inline int len_b(int L) { return FB * L + FHD; }
+// Fragment stream geometry (1 KB fragments): chain wave A p, chain wave B p, helper (h, wave w)
+// skip stream, then the helpers' head slices.
+__host__ __device__ inline int len_a(int L) { return FA * L; }
+__host__ __device__ inline int len_b(int L) { return FB * L; }
 __host__ __device__ inline int helper_layers(int L) { return (L + NW - 1) / NW; }
 __host__ __device__ inline size_t base_a(int L, int p) { return (size_t)p * len_a(L); }
 __host__ __device__ inline size_t base_b(int L, int p) { return 4 * (size_t)len_a(L) + (size_t)p * len_b(L); }
 __host__ __device__ inline size_t base_h(int L, int h, int w) {
   return 4 * (size_t)len_a(L) + 4 * (size_t)len_b(L) + (size_t)(NW * h + w) * helper_layers(L) * FS;
 }
+__host__ __device__ inline size_t base_w1(int L, int h) { return base_h(L, NHLP, 0) + (size_t)h * FW1; }
+__host__ __device__ inline size_t base_w2(int L, int h) { return base_w1(L, NHLP) + (size_t)h * FW2; }
+__host__ __device__ inline size_t frag_count(int L) { return base_w2(L, NHLP); }
 
-// Exchange buffers: abort word, then z^l words [nb][L][512], relu(skip sum) words [nb][4096] and
-// the launch handshake [nb][8] (word 1 + h: XCD of helper h; word 5: the group's mode).
-constexpr int ZWORDS = ROWS * R / 2, SWORDS = ROWS * S / 2, HWORDS = 8;
-__host__ __device__ inline u64 *comm_z(void *comm, int L, int blk, int l) {
-  return (u64 *)((char *)comm + 256) + ((size_t)blk * L + l) * ZWORDS;
+// Exchange buffers: abort word, then per group: z^l words [L][512]; relu(skip sum), relu(hidden)
+// and logits words [16 streams][256] each; the launch handshake [16] (word 1 + h: XCD of helper
+// h; word 15: the group's mode).
+constexpr int ZWORDS = ROWS * R / 2, XWORDS = ROWS * 256, HWORDS = 16;
+__host__ __device__ inline size_t group_words(int L) { return (size_t)L * ZWORDS + 3 * (size_t)XWORDS + HWORDS; }
+__host__ __device__ inline u64 *comm_group(void *comm, int L, int blk) {
+  return (u64 *)((char *)comm + 256) + (size_t)blk * group_words(L);
 }
-__host__ __device__ inline u64 *comm_s(void *comm, int L, int nb, int blk) {
-  return (u64 *)((char *)comm + 256) + (size_t)nb * L * ZWORDS + (size_t)blk * SWORDS;
-}
-__host__ __device__ inline u64 *comm_h(void *comm, int L, int nb, int blk) {
-  return (u64 *)((char *)comm + 256) + (size_t)nb * L * ZWORDS + (size_t)nb * SWORDS + (size_t)blk * HWORDS;
-}
+__host__ __device__ inline u64 *comm_z(void *comm, int L, int blk) { return comm_group(comm, L, blk); }
+__host__ __device__ inline u64 *comm_s(void *comm, int L, int blk) { return comm_group(comm, L, blk) + (size_t)L * ZWORDS; }
+__host__ __device__ inline u64 *comm_hid(void *comm, int L, int blk) { return comm_s(comm, L, blk) + XWORDS; }
+__host__ __device__ inline u64 *comm_lg(void *comm, int L, int blk) { return comm_hid(comm, L, blk) + XWORDS; }
+__host__ __device__ inline u64 *comm_hs(void *comm, int L, int blk) { return comm_lg(comm, L, blk) + XWORDS; }
 
-// `local`: the reader shares this block's XCD (and L2).
+// `local`: every reader shares this block's XCD (and L2).
 __device__ __forceinline__ void put_word(u64 *p, uint32_t payload, uint32_t tag, bool local) {
   const u64 v = ((u64)tag << 32) | payload;
   if (local) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -139,14 +148,15 @@ __device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *stic
   __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Load N tagged words until every tag equals `tag` (or the launch is aborted).  Per lane.
+// Load N consecutive tagged words at p until every tag equals `tag` (or the launch is aborted).
+// Per lane.
 template <int N>
-__device__ __forceinline__ void wait_words(const u64 *const (&addr)[N], uint32_t tag, uint32_t (&out)[N],
-                                           uint32_t *abort_word, uint32_t *sticky) {
+__device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t (&out)[N], uint32_t *abort_word,
+                                           uint32_t *sticky) {
   u64 v[N];
   for (int it = 0;; ++it) {
 #pragma unroll
-    for (int e = 0; e < N; ++e) v[e] = get_word(addr[e]);
+    for (int e = 0; e < N; ++e) v[e] = get_word(p + e);
     bool ok = true;
 #pragma unroll
     for (int e = 0; e < N; ++e) ok = ok && (uint32_t)(v[e] >> 32) == tag;
@@ -172,12 +182,13 @@ struct Ctx {
   uint32_t *qoff;   // [2][L]: byte offset of the rows of the current slot (0) and the next step's (1)
   char *ring;       // queue region
   uint32_t rowb;    // byte offset of this lane's 16-byte chunk of a queue row (wave B)
-  const float *conv_b, *res_b, *head_b, *out_b, *emb_b;
+  const float *conv_b, *res_b, *emb_b;
   const char *fw;   // this wave's fragment stream (wave-uniform)
-  const char *nxt;  // next fragment the ring loads (the stream is read in order, wrapping at its end)
+  const char *fend; // its end: the stream holds one step and is read cyclically
+  const char *nxt;  // next fragment the ring loads
   int wvoff;        // 16 * lane
-  u64 *zp;          // this block's z^0 words (layer l at + l * ZWORDS)
-  const u64 *sp;    // this block's relu(skip sum) words
+  u64 *zp;          // this group's z^0 words (layer l at + l * ZWORDS)
+  const u64 *lgp;   // this group's logits words
   uint32_t *abort_word, *sticky;
   bool local;       // the helpers share this block's XCD: workgroup-scope stores suffice
   int L, w, p, lane, n, q, b0, nrows, blk;
@@ -186,12 +197,13 @@ struct Ctx {
 __device__ __forceinline__ u32x4 frag_at(const Ctx &c, int pos) {
   return *(const u32x4 *)(c.fw + (size_t)pos * 1024 + c.wvoff);
 }
-// Slot `f` of ring W has just been consumed: load the stream's next fragment into it.  The ring is a
-// FIFO over the stream, so the next fragment is always one ring length past the one consumed.
-// The scheduling barriers keep the load after the MFMA that still reads the slot's old contents.
+// Slot `f` of ring W has just been consumed: load the stream's next fragment into it (the ring is a
+// FIFO over the cyclic stream).  The scheduling barriers keep the load after the MFMA that still
+// reads the slot's old contents.
 template <int D>
 __device__ __forceinline__ void refill(Ctx &c, u32x4 (&W)[D], int f) {
   __builtin_amdgcn_sched_barrier(0);
+  if (c.nxt == c.fend) c.nxt = c.fw;
   W[f] = *(const u32x4 *)(c.nxt + c.wvoff);
   c.nxt += 1024;
   __builtin_amdgcn_sched_barrier(0);
@@ -205,10 +217,10 @@ __device__ __forceinline__ void refill(Ctx &c, u32x4 (&W)[D], int f) {
 __device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int l, int ahead) {
   return *(const u32x4 *)(c.ring + (c.qoff[ahead * c.L + l] + c.rowb));
 }
-__device__ __forceinline__ void pop_land(const Ctx &c, int parity, u32x4 v) {
+__device__ __forceinline__ void pop_land(const Ctx &c, int buf, u32x4 v) {
   if (c.lane < 32) {
     const int r = 4 * c.p + (c.lane >> 3);
-    *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
+    *(u32x4 *)(c.s->vbuf[buf] + r * PX + 8 * (c.lane & 7)) = v;
   }
 }
 // Push of layer l: its input x^l replaces the slot popped for this step.
@@ -246,8 +258,8 @@ __device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int vb3, in
   stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
 }
 
-// Per-step inputs of steps [s0, s0 + KCH) into LDS (every thread, in the head before its first
-// barrier): uniforms for generation, else the forced input that follows each step.
+// Per-step inputs of steps [s0, s0 + KCH) into LDS (every thread, before the end-of-step barriers):
+// uniforms for generation, else the forced input that follows each step.
 __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
   ChainLds &s = *c.s;
@@ -272,7 +284,7 @@ __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
 
 // Layer l on wave A, ring slots PHS..PHS+5 (x-half of tanh/sigmoid tile p, residual tile p).
 template <int PHS>
-__device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DHEAD], f32x4 &xres) {
+__device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xres) {
   ChainLds &s = *c.s;
   const int n = c.n, q = c.q, p = c.p;
   const int par = l & 1;
@@ -327,7 +339,7 @@ __device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DHEAD], f32x4 
 // Layer l on wave B, ring slots PBS..PBS+3 (W_r of the next layer), pop registers rotated by
 // G6 = l mod 6 (L is a multiple of 6, so this is also the global layer index mod 6): the pop of
 // global layer index g sits in P[g mod 6] from its issue, five layers ahead of landing, until it
-// lands in vbuf[g mod 3] after layer g - 3, two block barriers before its product.
+// lands in vbuf[g mod 3] during layer g - 3, two block barriers before its product.
 template <int PBS, int G6>
 __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P)[6], uint32_t tag) {
   const int L = c.L;
@@ -336,6 +348,8 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
 #pragma unroll
   for (int f = 0; f < FB; ++f) refill(c, W, PBS + f);
   __syncthreads();
+  // while wave A runs the residual product: the layer's gate output to the helpers, its input into
+  // its queue, the pop of layer l + 3 into LDS and the pop of layer l + 8 issued
   publish_z(c, l, tag);
   push_rows(c, l);
   pop_land(c, G6 % 3, P[(G6 + 3) % 6]);
@@ -344,58 +358,22 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
   __syncthreads();
 }
 
-// The head of step `step` on any wave (layer ring depth D, head ring depth DH; the head is the
-// last FHD fragments of the wave's stream): relu(skip sum) from the helpers, first 1x1 + relu,
-// output 1x1, then the sample (or the logits), the next inputs and the slot advance.  Four
-// barriers.  Slots D..DH-1 are loaded before the wait for the skip sums; the last refills load the
-// next step's first D fragments only, where the layer loop expects them.
-template <int D, int DH>
-__device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[DH]) {
+// End of step `step` on every chain wave: the logits the helpers return, then the sample (or the
+// logits written out), the next inputs and the slot advance.  Two barriers.
+__device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   ChainLds &s = *c.s;
   const StepArgs &a = *c.a;
-  const int n = c.n, q = c.q, w = c.w, tid = threadIdx.x;
-#pragma unroll
-  for (int f = D; f < DH; ++f) refill(c, W, f);
+  const int w = c.w, tid = threadIdx.x;
   if (step % KCH == 0) stage_chunk(c, step);
   {
-    // thread t: stream t/32, skip channels 16 (t%32) .. +15 (8 words)
-    const int r = tid >> 5, ch = 16 * (tid & 31);
-    const u64 *addr[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) addr[e] = c.sp + r * (S / 2) + ch / 2 + e;
+    // thread t: stream t/32, classes 8 (t%32) .. +7
+    const int r = tid >> 5, k0 = 8 * (tid & 31);
     uint32_t v[8];
-    wait_words<8>(addr, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
-    *(u32x4 *)(s.u.sbuf + r * PS + ch) = u32x4{v[0], v[1], v[2], v[3]};
-    *(u32x4 *)(s.u.sbuf + r * PS + ch + 8) = u32x4{v[4], v[5], v[6], v[7]};
+    wait_words<8>(c.lgp + r * 256 + k0, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
+    float *dst = s.lg + r * PL + k0;
+    *(float4 *)dst = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+    *(float4 *)(dst + 4) = make_float4(__uint_as_float(v[4]), __uint_as_float(v[5]), __uint_as_float(v[6]), __uint_as_float(v[7]));
   }
-  __syncthreads();
-  f32x4 acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) acc[j] = ldsf4(c.head_b + 16 * (4 * w + j) + 4 * q);
-  u32x4 b = u32x4{0, 0, 0, 0};
-#pragma unroll
-  for (int g = 0; g < 64; ++g) {
-    const int ks = g / 4, j = g % 4;
-    if (j == 0) b = lds16(s.u.sbuf + n * PS + 32 * ks + 8 * q);
-    acc[j] = mfma(W[g % DH], b, acc[j]);
-    if (g == FHD - DH) c.nxt = c.fw;  // the ring wraps to the start of the next step
-    if (g < FHD - DH + D) refill(c, W, g % DH);
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) lds8(s.hbuf + n * PS + 16 * (4 * w + j) + 4 * q, pack4(relu4(acc[j])));
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < 2; ++j) acc[j] = ldsf4(c.out_b + 16 * (2 * w + j) + 4 * q);
-#pragma unroll
-  for (int g = 64; g < FHD; ++g) {
-    const int ks = (g - 64) / 2, j = (g - 64) % 2;
-    if (j == 0) b = lds16(s.hbuf + n * PS + 32 * ks + 8 * q);
-    acc[j] = mfma(W[g % DH], b, acc[j]);
-    if (g == FHD - DH) c.nxt = c.fw;
-    if (g < FHD - DH + D) refill(c, W, g % DH);
-  }
-#pragma unroll
-  for (int j = 0; j < 2; ++j) stf4(s.u.lg + n * PL + 16 * (2 * w + j) + 4 * q, acc[j]);
   __syncthreads();
   // rows w and w + 8: sample (generation) or write the logits (forced modes)
   if (a.mode != MODE_GENERATE) {
@@ -403,7 +381,7 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[DH]) {
     for (int kk = 0; kk < ROWS / NW; ++kk) {
       const int r = w + NW * kk;
       if (r < c.nrows && a.logits) {
-        const float4 v = *(const float4 *)(s.u.lg + r * PL + 4 * c.lane);
+        const float4 v = *(const float4 *)(s.lg + r * PL + 4 * c.lane);
         *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
       }
     }
@@ -413,7 +391,7 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[DH]) {
     for (int kk = 0; kk < ROWS / NW; ++kk) {
       const int r = w + NW * kk;
       if (r < c.nrows) {
-        const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
+        const int k = sample256(s.lg + r * PL, s.chunk.u[r][step % KCH]);
         if (c.lane == 0) {
           a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
           s.ins[r] = k;
@@ -434,12 +412,13 @@ __device__ __forceinline__ void head(Ctx &c, long long step, u32x4 (&W)[DH]) {
 __device__ __forceinline__ void a_role(Ctx &c) {
   const int L = c.L;
   c.fw = (const char *)c.a->mf_frags + base_a(L, c.p) * 1024;
-  u32x4 W[DHEAD];  // slots DA.. are used by the head only
+  c.fend = c.fw + (size_t)len_a(L) * 1024;
+  u32x4 W[DA];
 #pragma unroll
   for (int f = 0; f < DA; ++f) W[f] = frag_at(c, f);
   c.nxt = c.fw + DA * 1024;
   f32x4 xres = f32x4{0.f, 0.f, 0.f, 0.f};
-  __syncthreads();  // the popped rows of layers 0 and 1 are in LDS
+  __syncthreads();  // the popped rows of layers 0..2 are in LDS
   __syncthreads();  // W_r v + b of layer 0 is in LDS
   for (long long step = 0; step < c.a->n_steps; ++step) {
     for (int l = 0; l < L; l += 6) {
@@ -450,13 +429,14 @@ __device__ __forceinline__ void a_role(Ctx &c) {
       a_layer<0>(c, l + 4, W, xres);
       a_layer<FA>(c, l + 5, W, xres);
     }
-    head<DA, DHEAD>(c, step, W);
+    finish_step(c, step);
   }
 }
 
 __device__ __forceinline__ void b_role(Ctx &c) {
   const int L = c.L;
   c.fw = (const char *)c.a->mf_frags + base_b(L, c.p) * 1024;
+  c.fend = c.fw + (size_t)len_b(L) * 1024;
   u32x4 W[DB], P[6];
   // layers 0..2 of step 0 land now; layer 0's W_r v + b comes from its stream stage L - 1
   pop_land(c, 0, pop_issue(c, 0, 0));
@@ -482,7 +462,7 @@ __device__ __forceinline__ void b_role(Ctx &c) {
       b_layer<4 * FB, 4>(c, l + 4, W, P, tag);
       b_layer<5 * FB, 5>(c, l + 5, W, P, tag);
     }
-    head<DB, DHEAD>(c, step, W);
+    finish_step(c, step);
   }
 }
 
@@ -494,7 +474,7 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   int *dil = slot + L;
   uint32_t *rbase = (uint32_t *)(dil + L);
   uint32_t *qoff = rbase + L;
-  float *bias = (float *)(dyn + dyn_bias_offset(L));  // conv_b [L][2R], res_b [L][R], skip sum [S], head_b, out_b, emb_b
+  float *bias = (float *)(dyn + dyn_bias_offset(L));  // conv_b [L][2R], res_b [L][R], emb_b [R]
 
   Ctx c;
   c.a = &a;
@@ -506,9 +486,7 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   c.ring = (char *)a.ring;
   c.conv_b = bias;
   c.res_b = c.conv_b + L * 2 * R;
-  c.head_b = c.res_b + L * R + S;
-  c.out_b = c.head_b + H;
-  c.emb_b = c.out_b + Q;
+  c.emb_b = c.res_b + L * R;
   c.L = L;
   c.w = __builtin_amdgcn_readfirstlane(tid >> 6);
   c.p = c.w & 3;
@@ -520,15 +498,16 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   c.nrows = min(ROWS, a.batch - c.b0);
   c.wvoff = 16 * c.lane;
   c.rowb = (uint32_t)(((c.b0 + 4 * c.p + ((c.lane & 31) >> 3)) * R + 8 * (c.lane & 7)) * 2);
-  c.zp = comm_z(a.sp_comm, L, blk, 0);
-  c.sp = comm_s(a.sp_comm, L, a.sp_nb, blk);
+  c.zp = comm_z(a.sp_comm, L, blk);
+  c.lgp = comm_lg(a.sp_comm, L, blk);
   c.abort_word = (uint32_t *)a.sp_comm;
   c.sticky = a.sp_sticky;
 
   const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
   for (int i = tid; i < Q * R / 8; i += NT) ((u32x4 *)s.embT)[i] = embsrc[i];
-  const int nbias = L * 3 * R + S + H + Q + R;
-  for (int i = tid; i < nbias; i += NT) bias[i] = a.mf_bias[i];
+  // conv and residual biases, then the embedding bias (the last R floats of the bias block)
+  for (int i = tid; i < L * 3 * R; i += NT) bias[i] = a.mf_bias[i];
+  for (int i = tid; i < R; i += NT) bias[L * 3 * R + i] = a.mf_bias[L * 3 * R + S + H + Q + i];
   const uint32_t slot_bytes = (uint32_t)(a.bmax * R * 2);
   for (int l = tid; l < L; l += NT) {
     const LayerDev ld = a.layers[l];
@@ -545,47 +524,72 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
     s.ins[tid] = v;
   }
   // launch handshake: read the helpers' XCD ids, publish the group's mode
-  u64 *hs = comm_h(a.sp_comm, L, a.sp_nb, blk);
+  u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid < NHLP) {
-    const u64 *addr[1] = {hs + 1 + tid};
     uint32_t v[1];
-    wait_words<1>(addr, 1, v, c.abort_word, c.sticky);
+    wait_words<1>(hs + 1 + tid, 1, v, c.abort_word, c.sticky);
     s.ins[ROWS + tid] = (int)v[0];
   }
   __syncthreads();
   bool local = true;
   for (int h = 0; h < NHLP; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
   c.local = local;
-  if (tid == 0) put_word(hs + 5, local ? 1u : 0u, 1, false);
+  if (tid == 0) put_word(hs + 15, local ? 1u : 0u, 1, false);
   if (c.w < 4) a_role(c);
   else b_role(c);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
 }
 
 // ---------------------------------------------------------------------------
-// Helper block (chain block blk, slice h): wave w takes layers w, w + 8, ...; for each it waits
-// for z^l, then accumulates the slice's 8 tiles x 2 k-steps.  At the end of a step the eight
-// waves' partial sums meet in LDS, get the summed skip biases, relu and bf16 rounding, and go to
-// the chain block as tagged words.
+// Helper h of group blk.  Per step:
+//  1. skip: wave w takes layers w, w + 8, ...; for each it waits for z^l and accumulates the 4 tiles
+//     x 2 k-steps of its 64 skip channels (weights streamed from L2, one layer ahead); the eight
+//     waves' partials meet in LDS, get the summed skip biases, relu and bf16 rounding, and go out
+//     as words;
+//  2. hidden: gather relu(skip sum) of all 512 channels; 64 hidden rows = 4 tiles, each over two
+//     waves that split the 16 k-steps; + bias, relu, bf16, out as words;
+//  3. classes: gather relu(hidden); 32 classes = 2 tiles, each over four waves splitting the 16
+//     k-steps; + bias, out as fp32 words to the chain block.
+
+// Gather 16 x 512 bf16 activations (4096 words) into act: thread t takes stream t/32, channels
+// 16 (t%32) .. +15.
+__device__ __forceinline__ void gather_act(uint16_t *act, const u64 *src, uint32_t tag, uint32_t *abort_word,
+                                           uint32_t *sticky) {
+  const int tid = threadIdx.x, r = tid >> 5, ch = 16 * (tid & 31);
+  uint32_t v[8];
+  wait_words<8>(src + r * 256 + ch / 2, tag, v, abort_word, sticky);
+  *(u32x4 *)(act + r * PS + ch) = u32x4{v[0], v[1], v[2], v[3]};
+  *(u32x4 *)(act + r * PS + ch + 8) = u32x4{v[4], v[5], v[6], v[7]};
+}
 
 __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, int blk, int h) {
   HelperLds &s = *(HelperLds *)lds_raw;
-  const int tid = threadIdx.x, L = a.L, nb = a.sp_nb;
+  const int tid = threadIdx.x, L = a.L;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, n = lane & 15, q = lane >> 4;
   const int nl = (L - w + NW - 1) / NW;  // layers of this wave (L >= NW)
   const char *fw = (const char *)a.mf_frags + base_h(L, h, w) * 1024;
   const int wvoff = 16 * lane;
-  const u64 *zb = comm_z(a.sp_comm, L, blk, 0);
-  u64 *sw = comm_s(a.sp_comm, L, nb, blk);
+  const u64 *zb = comm_z(a.sp_comm, L, blk);
+  u64 *sw = comm_s(a.sp_comm, L, blk), *hw = comm_hid(a.sp_comm, L, blk), *lw = comm_lg(a.sp_comm, L, blk);
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
-  const float *skip_sum = a.mf_bias + L * 3 * R + h * SL;
+  const float *skip_sum = s.bias, *head_b = s.bias + SL, *out_b = s.bias + SL + HL;
+  // bias and head slices into LDS for the whole launch
+  {
+    const float *src = a.mf_bias + L * 3 * R;  // skip sum [S], head [H], out [Q]
+    for (int i = tid; i < SL; i += NT) s.bias[i] = src[h * SL + i];
+    for (int i = tid; i < HL; i += NT) s.bias[SL + i] = src[S + h * HL + i];
+    for (int i = tid; i < QL; i += NT) s.bias[SL + HL + i] = src[S + H + h * QL + i];
+    const u32x4 *w1 = (const u32x4 *)((const char *)a.mf_frags + base_w1(L, h) * 1024);
+    const u32x4 *w2 = (const u32x4 *)((const char *)a.mf_frags + base_w2(L, h) * 1024);
+    for (int i = tid; i < FW1 * 64; i += NT) s.w1[i] = w1[i];
+    for (int i = tid; i < FW2 * 64; i += NT) s.w2[i] = w2[i];
+  }
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
-  u64 *hs = comm_h(a.sp_comm, L, nb, blk);
+  u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid == 0) {
     put_word(hs + 1 + h, xcd_id(), 1, false);
-    const u64 *addr[1] = {hs + 5};
     uint32_t v[1];
-    wait_words<1>(addr, 1, v, abort_word, a.sp_sticky);
+    wait_words<1>(hs + 15, 1, v, abort_word, a.sp_sticky);
     s.local = (int)v[0];
   }
   __syncthreads();
@@ -596,25 +600,21 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   const char *nxt = fw + (nl > 1 ? FS * 1024 : 0);
   for (long long step = 0; step < a.n_steps; ++step) {
     const uint32_t tag = (uint32_t)(step + 1);
-    f32x4 acc[8];
+    // ---- 1. skip sums of the slice
+    f32x4 acc[4];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int i = 0; i < nl; ++i) {
       const int l = w + NW * i;
       // B operand rows of z^l: stream n, channels 8q..8q+7 (k-step 0) and 32 + 8q.. (k-step 1)
       const u64 *zl = zb + (size_t)l * ZWORDS + n * (R / 2) + 4 * q;
-      const u64 *addr[8];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        addr[e] = zl + e;
-        addr[4 + e] = zl + 16 + e;
-      }
-      uint32_t v[8];
-      wait_words<8>(addr, tag, v, abort_word, a.sp_sticky);
-      const u32x4 b0 = u32x4{v[0], v[1], v[2], v[3]}, b1 = u32x4{v[4], v[5], v[6], v[7]};
+      uint32_t v0[4], v1[4];
+      wait_words<4>(zl, tag, v0, abort_word, a.sp_sticky);
+      wait_words<4>(zl + 16, tag, v1, abort_word, a.sp_sticky);
+      const u32x4 b0 = u32x4{v0[0], v0[1], v0[2], v0[3]}, b1 = u32x4{v1[0], v1[1], v1[2], v1[3]};
       if (i + 1 == nl) nxt = fw;  // the next layer of this wave is its first of the next step
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < 4; ++j) {
         acc[j] = mfma(W[2 * j], b0, acc[j]);
         __builtin_amdgcn_sched_barrier(0);
         W[2 * j] = *(const u32x4 *)(nxt + wvoff);
@@ -627,21 +627,64 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
       }
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) stf4(s.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
+    for (int j = 0; j < 4; ++j) stf4(s.u.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
     __syncthreads();
-    // thread t: words 2t, 2t+1 of the slice's 1024 (stream jw / 64, channels 2 (jw % 64), +1)
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int jw = 2 * tid + e, r = jw >> 6, cp = jw & 63;
+    {
+      // thread t: stream t/32, slice channels 2 (t%32), +1
+      const int r = tid >> 5, cp = tid & 31;
       float v0 = skip_sum[2 * cp], v1 = skip_sum[2 * cp + 1];
 #pragma unroll
       for (int ww = 0; ww < NW; ++ww) {
-        v0 += s.part[ww][r * PH + 2 * cp];
-        v1 += s.part[ww][r * PH + 2 * cp + 1];
+        v0 += s.u.part[ww][r * PH + 2 * cp];
+        v1 += s.u.part[ww][r * PH + 2 * cp + 1];
       }
-      put_word(sw + r * (S / 2) + h * (SL / 2) + cp, pack2(fmaxf(v0, 0.f), fmaxf(v1, 0.f)), tag, local);
+      put_word(sw + r * 256 + (h * SL) / 2 + cp, pack2(fmaxf(v0, 0.f), fmaxf(v1, 0.f)), tag, local);
     }
     __syncthreads();
+    // ---- 2. hidden rows of the slice: tile j = w % 4, k-steps 8 (w / 4) .. +7
+    gather_act(s.u.act, sw, tag, abort_word, a.sp_sticky);
+    __syncthreads();
+    {
+      const int j = w & 3, k0 = 8 * (w >> 2);
+      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = k0; ks < k0 + 8; ++ks)
+        t = mfma(s.w1[(j * (S / 32) + ks) * 64 + lane], lds16(s.u.act + n * PS + 32 * ks + 8 * q), t);
+      if (w >= 4) stf4(s.pw[w - 4] + n * PP + 4 * q, t);
+      acc[0] = t;
+    }
+    __syncthreads();
+    if (w < 4) {
+      const int ch = 16 * w + 4 * q;
+      f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t[i] = fmaxf(t[i] + head_b[ch + i], 0.f);
+      const u32x2 pk = pack4(t);
+      u64 *dst = hw + n * 256 + (h * HL + ch) / 2;
+      put_word(dst, pk.x, tag, local);
+      put_word(dst + 1, pk.y, tag, local);
+    }
+    // ---- 3. classes of the slice: tile j = w % 2, k-steps 4 (w / 2) .. +3
+    gather_act(s.u.act, hw, tag, abort_word, a.sp_sticky);
+    __syncthreads();
+    {
+      const int j = w & 1, k0 = 4 * (w >> 1);
+      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = k0; ks < k0 + 4; ++ks)
+        t = mfma(s.w2[(j * (H / 32) + ks) * 64 + lane], lds16(s.u.act + n * PS + 32 * ks + 8 * q), t);
+      if (w >= 2) stf4(s.pw[w - 2] + n * PP + 4 * q, t);
+      acc[0] = t;
+    }
+    __syncthreads();
+    if (w < 2) {
+      const int k = 16 * w + 4 * q;
+      f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q) + ldsf4(s.pw[w + 2] + n * PP + 4 * q) +
+                ldsf4(s.pw[w + 4] + n * PP + 4 * q);
+      u64 *dst = lw + n * 256 + h * QL + k;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) put_word(dst + i, __float_as_uint(t[i] + out_b[k + i]), tag, local);
+    }
   }
 }
 
@@ -651,14 +694,15 @@ __global__ void __launch_bounds__(NT) split_step_kernel(StepArgs a) {
   if ((int)blockIdx.x < nb) {
     chain_block(a, (char *)lds_raw, blockIdx.x);
   } else {
+    // helper h of group b sits at nb + h nb + b: with nb a multiple of 8, on the XCD of chain block b
     const int e = (int)blockIdx.x - nb;
     helper_block(a, (char *)lds_raw, e % nb, e / nb);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Repacking into the per-wave fragment streams.  Fragment (tile t, k-step ks) of a matrix
-// M[out][k] gives lane l the 8 values M[16t + l%16][32ks + 8(l/16) + j].
+// Repacking into the fragment streams.  Fragment (tile t, k-step ks) of a matrix M[out][k] gives
+// lane l the 8 values M[16t + l%16][32ks + 8(l/16) + j].
 
 __device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int o, int k) {
   return conv[(o * R + (k % R)) * 2 + (k >= R ? 1 : 0)];
@@ -670,10 +714,10 @@ __device__ __forceinline__ uint4 pack8(const uint16_t *v) {
 // Layer l: A wave p stream position 6l + f (f 0..3: x-half of tanh tile p k-steps 2,3 and sigmoid
 // tile p k-steps 2,3; f 4,5: residual tile p k-steps 0,1); B wave p stream position 4 ((l-1) mod L)
 // + f (v-half of tanh tile p k-steps 0,1, sigmoid tile p k-steps 0,1); helper (h, l % 8) position
-// 16 (l / 8) + 2j + ks (skip tile 8h + j, k-step ks).
+// 8 (l / 8) + 2j + ks (skip tile 4h + j, k-step ks).
 constexpr int LAYER_FRAGS = 4 * FA + 4 * FB + NHLP * FS;
 __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, int l, int L,
-                                   uint4 *frags) {
+                                    uint4 *frags) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= LAYER_FRAGS * 64) return;
   const int lane = e % 64, m = lane % 16, kq = 8 * (lane / 16);
@@ -692,45 +736,42 @@ __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, c
     dst = base_b(L, p) + (size_t)FB * ((l + L - 1) % L) + f;
   } else {
     fi -= 4 * FB;
-    const int h = fi / FS, f = fi % FS, t = NW * h + f / 2, ks = f % 2;
+    const int h = fi / FS, f = fi % FS, t = (SL / 16) * h + f / 2, ks = f % 2;
     for (int j = 0; j < 8; ++j) v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
     dst = base_h(L, h, l % NW) + (size_t)FS * (l / NW) + f;
   }
   frags[dst * 64 + lane] = pack8(v);
 }
 
-// Head of wave w (A for w < 4, B otherwise), stream positions FA L + g (A) or FB L + g (B):
-// g < 64 first 1x1 tile 4w + g%4, k-step g/4; g >= 64 output tile 2w + (g-64)%2, k-step (g-64)/2.
+// Head slices of helper h: first 1x1 fragment (tile j, k-step ks) of rows 64h + 16j.. at
+// j * 16 + ks; output 1x1 fragment (tile j, k-step ks) of classes 32h + 16j.. at j * 16 + ks.
 __global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, int L, uint4 *frags) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= NW * FHD * 64) return;
-  const int lane = e % 64, g = (e / 64) % FHD, w = e / (64 * FHD);
-  const int m = lane % 16, kq = 8 * (lane / 16);
+  if (e >= NHLP * (FW1 + FW2) * 64) return;
+  const int lane = e % 64, m = lane % 16, kq = 8 * (lane / 16);
+  const int fi = e / 64, h = fi / (FW1 + FW2), f = fi % (FW1 + FW2);
   uint16_t v[8];
-  for (int j = 0; j < 8; ++j) {
-    if (g < 64) {
-      const int t = 4 * w + g % 4, ks = g / 4;
-      v[j] = head[(16 * t + m) * S + 32 * ks + kq + j];
-    } else {
-      const int t = 2 * w + (g - 64) % 2, ks = (g - 64) / 2;
-      v[j] = out[(16 * t + m) * H + 32 * ks + kq + j];
-    }
+  size_t dst;
+  if (f < FW1) {
+    const int j = f / (S / 32), ks = f % (S / 32);
+    for (int i = 0; i < 8; ++i) v[i] = head[(h * HL + 16 * j + m) * S + 32 * ks + kq + i];
+    dst = base_w1(L, h) + f;
+  } else {
+    const int g = f - FW1, j = g / (H / 32), ks = g % (H / 32);
+    for (int i = 0; i < 8; ++i) v[i] = out[(h * QL + 16 * j + m) * H + 32 * ks + kq + i];
+    dst = base_w2(L, h) + g;
   }
-  const size_t dst = w < 4 ? base_a(L, w) + (size_t)FA * L + g : base_b(L, w - 4) + (size_t)FB * L + g;
   frags[dst * 64 + lane] = pack8(v);
 }
 
 }  // namespace sp
 
-size_t split_frag_bytes(int L) { return sp::base_h(L, sp::NHLP, 0) * 1024; }
+size_t split_frag_bytes(int L) { return sp::frag_count(L) * 1024; }
 
-size_t split_comm_bytes(int L, int nb) {
-  return 256 + ((size_t)nb * L * sp::ZWORDS + (size_t)nb * sp::SWORDS + (size_t)nb * sp::HWORDS) *
-                   sizeof(unsigned long long);
-}
+size_t split_comm_bytes(int L, int nb) { return 256 + (size_t)nb * sp::group_words(L) * sizeof(unsigned long long); }
 
 size_t split_lds_bytes(int L) {
-  const size_t chain = sp::chain_fixed_bytes() + sp::dyn_bias_offset(L) + sizeof(float) * mfma_bias_floats(L);
+  const size_t chain = sp::chain_fixed_bytes() + sp::dyn_bias_offset(L) + sizeof(float) * ((size_t)L * 3 * kMfR + kMfR);
   const size_t helper = sizeof(sp::HelperLds);
   return chain > helper ? chain : helper;
 }
@@ -764,7 +805,7 @@ hipError_t launch_split_repack_layer(const void *conv, const void *res, const vo
 }
 
 hipError_t launch_split_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s) {
-  const int n = kMfWaves * kSpFHead * 64;
+  const int n = sp::NHLP * (sp::FW1 + sp::FW2) * 64;
   hipLaunchKernelGGL(sp::repack_head_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)head,
                      (const uint16_t *)out, L, (uint4 *)frags);
   return hipGetLastError();
