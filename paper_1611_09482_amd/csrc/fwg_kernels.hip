@@ -533,9 +533,12 @@ hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K,
 
 // ---------------------------------------------------------------------------
 // Fills (used instead of memset nodes so the calls stay safe under stream capture).
-__global__ void fill_zero_kernel(uint4 *dst, size_t n16) {
+// Zero `bytes` bytes at dst (16-byte aligned): whole 16-byte units, then the tail byte by byte.
+__global__ void fill_zero_kernel(uint4 *dst, size_t bytes) {
+  const size_t n16 = bytes / 16;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x)
     dst[i] = make_uint4(0, 0, 0, 0);
+  if (blockIdx.x == 0 && threadIdx.x < bytes % 16) ((unsigned char *)dst)[n16 * 16 + threadIdx.x] = 0;
 }
 __global__ void fill_i32_kernel(int32_t *dst, int32_t v, int n) {
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) dst[i] = v;
@@ -545,10 +548,10 @@ __global__ void copy_bias_kernel(const float *src, float *dst, int n) {
 }
 
 hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s) {
-  const size_t n16 = bytes / 16;  // regions are 256-byte aligned and sized
-  if (n16 == 0) return hipSuccess;
+  if (bytes == 0) return hipSuccess;
+  const size_t n16 = bytes / 16;  // regions start 256-byte aligned
   const int blocks = (int)(n16 / 256 + 1 < 8192 ? n16 / 256 + 1 : 8192);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, (uint4 *)dst, n16);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, s, (uint4 *)dst, bytes);
   return hipGetLastError();
 }
 hipError_t launch_fill_i32(int32_t *dst, int32_t v, int n, hipStream_t s) {

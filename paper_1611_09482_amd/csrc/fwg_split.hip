@@ -31,10 +31,10 @@
 // Chain block: 8 waves, A = waves 0..3 and B = waves 4..7, A and B of pair p share SIMD p.
 //  - wave A (p): the current-input half of the dilated product (W_e x) for tanh tile p and
 //    sigmoid tile p, plus W_r v + b from LDS, the gate, the residual 1x1 for channel tile p;
-//  - wave B (p): W_r v + b of the next layer (v = the popped state, known early); between the
-//    layer's two barriers, while A runs the residual product, the publication of z^l to the
-//    helpers, the push of the layer input (stream rows 4p..4p+3) and the queue pops, issued five
-//    layers before they land in LDS;
+//  - wave B (p): W_r v + b of the next layer (v = the popped state, known early) and the queue
+//    pops of stream rows 4p..4p+3, issued five layers before they land in LDS; between the layer's
+//    two barriers, while A runs the residual product, the publication of z^l to the helpers and the
+//    push of the layer input;
 //  - both: two sampled rows per wave.
 // Every chain wave streams its own pre-packed weight fragments from L2 through a ring of registers,
 // 12 fragments (two layers) for A and 24 (six layers) for B, whose loads also queue behind the
@@ -114,9 +114,14 @@ __host__ __device__ inline size_t base_w2(int L, int h) { return base_w1(L, NHLP
 __host__ __device__ inline size_t frag_count(int L) { return base_w2(L, NHLP); }
 
 // Exchange buffers: abort word, then per group: z^l words [L][512]; relu(skip sum), relu(hidden)
-// and logits words [16 streams][256] each; the launch handshake [16] (word 1 + h: XCD of helper
-// h; word 15: the group's mode).
-constexpr int ZWORDS = ROWS * R / 2, XWORDS = ROWS * 256, HWORDS = 16;
+// and logits words [16 streams][256] each; the launch handshake (slot h: XCD of helper h; slot
+// NHLP: the group's mode).  A device-scope load is served by the reader's own L2 when that L2 holds
+// the line from the reader's own store, so no block ever reads a line another block writes after
+// it has written to that line itself: every helper slice of a word array spans whole 256-byte
+// lines, and every handshake word has a 256-byte slot of its own.
+constexpr int ZWORDS = ROWS * R / 2, XWORDS = ROWS * 256, HSLOT = 32, HWORDS = (NHLP + 1) * HSLOT;
+static_assert((SL / 2) % 32 == 0 && (HL / 2) % 32 == 0 && QL % 32 == 0 && HSLOT == 32,
+              "helper slices and handshake slots span whole 256-byte lines");
 __host__ __device__ inline size_t group_words(int L) { return (size_t)L * ZWORDS + 3 * (size_t)XWORDS + HWORDS; }
 __host__ __device__ inline u64 *comm_group(void *comm, int L, int blk) {
   return (u64 *)((char *)comm + 256) + (size_t)blk * group_words(L);
@@ -132,6 +137,16 @@ __device__ __forceinline__ void put_word(u64 *p, uint32_t payload, uint32_t tag,
   const u64 v = ((u64)tag << 32) | payload;
   if (local) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Two consecutive words (p 16-byte aligned).  Within one XCD a single 16-byte store carries both:
+// it lands in one L2 line, so each 8-byte word (tag with its payload) becomes visible whole.
+__device__ __forceinline__ void put_words2(u64 *p, uint32_t pa, uint32_t pb, uint32_t tag, bool local) {
+  if (local) {
+    *(u32x4 *)p = u32x4{pa, tag, pb, tag};
+  } else {
+    put_word(p, pa, tag, false);
+    put_word(p + 1, pb, tag, false);
+  }
 }
 __device__ __forceinline__ uint32_t xcd_id() {
   return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15;  // HW_REG_XCC_ID, bits 3:0
@@ -236,9 +251,7 @@ __device__ __forceinline__ void push_rows(const Ctx &c, int l) {
 __device__ __forceinline__ void publish_z(const Ctx &c, int l, uint32_t tag) {
   const int r = 4 * c.p + (c.lane >> 4), cp = 2 * (c.lane & 15);
   const u32x2 v = *(const u32x2 *)(c.s->zbuf[l & 1] + r * PX + 2 * cp);
-  u64 *zw = c.zp + (size_t)l * ZWORDS + r * (R / 2) + cp;
-  put_word(zw, v.x, tag, c.local);
-  put_word(zw + 1, v.y, tag, c.local);
+  put_words2(c.zp + (size_t)l * ZWORDS + r * (R / 2) + cp, v.x, v.y, tag, c.local);
 }
 
 // W_r v + b of layer ln from the popped rows in vbuf[vb3] and ring slots f0..f0+3 (tanh tile p
@@ -339,7 +352,8 @@ __device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xr
 // Layer l on wave B, ring slots PBS..PBS+3 (W_r of the next layer), pop registers rotated by
 // G6 = l mod 6 (L is a multiple of 6, so this is also the global layer index mod 6): the pop of
 // global layer index g sits in P[g mod 6] from its issue, five layers ahead of landing, until it
-// lands in vbuf[g mod 3] during layer g - 3, two block barriers before its product.
+// lands in vbuf[g mod 3] before the first barrier of layer g - 3, four block barriers before its
+// product.
 template <int PBS, int G6>
 __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P)[6], uint32_t tag) {
   const int L = c.L;
@@ -347,14 +361,16 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
   recurrent_half(c, ln, (G6 + 1) % 3, (l + 1) & 1, W, PBS);
 #pragma unroll
   for (int f = 0; f < FB; ++f) refill(c, W, PBS + f);
-  __syncthreads();
-  // while wave A runs the residual product: the layer's gate output to the helpers, its input into
-  // its queue, the pop of layer l + 3 into LDS and the pop of layer l + 8 issued
-  publish_z(c, l, tag);
-  push_rows(c, l);
+  // the pop of layer l + 3 into LDS (its buffer was last read before the previous layer's first
+  // barrier) and the pop of layer l + 8 issued
   pop_land(c, G6 % 3, P[(G6 + 3) % 6]);
   const int j = l + 8 < L ? l + 8 : l + 8 - L;
   P[(G6 + 2) % 6] = pop_issue(c, j, l + 8 < L ? 0 : 1);
+  __syncthreads();
+  // while wave A runs the residual product: the layer's gate output to the helpers and its input
+  // into its queue
+  publish_z(c, l, tag);
+  push_rows(c, l);
   __syncthreads();
 }
 
@@ -527,14 +543,14 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid < NHLP) {
     uint32_t v[1];
-    wait_words<1>(hs + 1 + tid, 1, v, c.abort_word, c.sticky);
+    wait_words<1>(hs + HSLOT * tid, 1, v, c.abort_word, c.sticky);
     s.ins[ROWS + tid] = (int)v[0];
   }
   __syncthreads();
   bool local = true;
   for (int h = 0; h < NHLP; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
   c.local = local;
-  if (tid == 0) put_word(hs + 15, local ? 1u : 0u, 1, false);
+  if (tid == 0) put_word(hs + HSLOT * NHLP, local ? 1u : 0u, 1, false);
   if (c.w < 4) a_role(c);
   else b_role(c);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
@@ -587,9 +603,9 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
   u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid == 0) {
-    put_word(hs + 1 + h, xcd_id(), 1, false);
+    put_word(hs + HSLOT * h, xcd_id(), 1, false);
     uint32_t v[1];
-    wait_words<1>(hs + 15, 1, v, abort_word, a.sp_sticky);
+    wait_words<1>(hs + HSLOT * NHLP, 1, v, abort_word, a.sp_sticky);
     s.local = (int)v[0];
   }
   __syncthreads();
@@ -629,16 +645,14 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
 #pragma unroll
     for (int j = 0; j < 4; ++j) stf4(s.u.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
     __syncthreads();
-    {
-      // thread t: stream t/32, slice channels 2 (t%32), +1
-      const int r = tid >> 5, cp = tid & 31;
-      float v0 = skip_sum[2 * cp], v1 = skip_sum[2 * cp + 1];
+    if (tid < ROWS * SL / 4) {
+      // thread t: stream t/16, slice channels 4 (t%16) .. +3
+      const int r = tid >> 4, c4 = 4 * (tid & 15);
+      f32x4 v = ldsf4(skip_sum + c4);
 #pragma unroll
-      for (int ww = 0; ww < NW; ++ww) {
-        v0 += s.u.part[ww][r * PH + 2 * cp];
-        v1 += s.u.part[ww][r * PH + 2 * cp + 1];
-      }
-      put_word(sw + r * 256 + (h * SL) / 2 + cp, pack2(fmaxf(v0, 0.f), fmaxf(v1, 0.f)), tag, local);
+      for (int ww = 0; ww < NW; ++ww) v += ldsf4(s.u.part[ww] + r * PH + c4);
+      const u32x2 pk = pack4(relu4(v));
+      put_words2(sw + r * 256 + (h * SL + c4) / 2, pk.x, pk.y, tag, local);
     }
     __syncthreads();
     // ---- 2. hidden rows of the slice: tile j = w % 4, k-steps 8 (w / 4) .. +7
@@ -660,9 +674,7 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
 #pragma unroll
       for (int i = 0; i < 4; ++i) t[i] = fmaxf(t[i] + head_b[ch + i], 0.f);
       const u32x2 pk = pack4(t);
-      u64 *dst = hw + n * 256 + (h * HL + ch) / 2;
-      put_word(dst, pk.x, tag, local);
-      put_word(dst + 1, pk.y, tag, local);
+      put_words2(hw + n * 256 + (h * HL + ch) / 2, pk.x, pk.y, tag, local);
     }
     // ---- 3. classes of the slice: tile j = w % 2, k-steps 4 (w / 2) .. +3
     gather_act(s.u.act, hw, tag, abort_word, a.sp_sticky);
@@ -682,8 +694,8 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
       f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q) + ldsf4(s.pw[w + 2] + n * PP + 4 * q) +
                 ldsf4(s.pw[w + 4] + n * PP + 4 * q);
       u64 *dst = lw + n * 256 + h * QL + k;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) put_word(dst + i, __float_as_uint(t[i] + out_b[k + i]), tag, local);
+      put_words2(dst, __float_as_uint(t[0] + out_b[k]), __float_as_uint(t[1] + out_b[k + 1]), tag, local);
+      put_words2(dst + 2, __float_as_uint(t[2] + out_b[k + 2]), __float_as_uint(t[3] + out_b[k + 3]), tag, local);
     }
   }
 }

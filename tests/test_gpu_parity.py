@@ -421,6 +421,27 @@ def test_continuation_reset_and_determinism_gpu(fam):
     assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), full)
 
 
+def test_split_state_cleared_on_poisoned_workspace():
+    """The split kernels' launch state (exchange words, abort mark) is set up by the library itself:
+    a handle created on memory that held 0xFF bytes (the caching allocator hands the freed block back)
+    generates valid samples and reports a clean device status."""
+    cfg = FAMILIES["gated_r64_bf16_split"]
+    B, n = 11, 40
+    w = W.make_weights(cfg, 5, bias_scale=0.1)
+    ws = binding.from_model(cfg, w, max_batch=B).ws_bytes
+    poison = torch.full((ws,), 0xFF, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    del poison
+    fw = binding.from_model(cfg, w, max_batch=B)
+    assert fw.regime == "mfma_split_bf16_r64_s512"
+    u = W.uniforms(12, B, n)
+    g = fw.generate(dev(u)).cpu().numpy()
+    fw.device_status()
+    so = oracle.Oracle(w).state(B).generate(u)
+    agree = (g == so).all(axis=0)
+    assert agree[:8].all(), "first samples must match the oracle"
+
+
 def test_streams_independent_gpu():
     cfg = FAMILIES["gated_r64_bf16"]
     w, fw, _ = build_pair(cfg, 8, 13)
