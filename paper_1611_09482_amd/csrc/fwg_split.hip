@@ -176,10 +176,13 @@ __device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t 
 #pragma unroll
     for (int e = 0; e < N; ++e) ok = ok && (uint32_t)(v[e] >> 32) == tag;
     if (ok) break;
-    if (get_flag(abort_word) != 0u) break;
-    if (it >= SPIN_MAX) {
-      raise_abort(abort_word, sticky);
-      break;
+    // the abort word every 16 polls: a stale poll then costs one round trip, not two
+    if ((it & 15) == 15) {
+      if (get_flag(abort_word) != 0u) break;
+      if (it >= SPIN_MAX) {
+        raise_abort(abort_word, sticky);
+        break;
+      }
     }
   }
 #pragma unroll
