@@ -237,15 +237,18 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
     }
     if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
-#pragma unroll
-    for (int kk = 0; kk < ROWS / kMfWaves; ++kk) {
-      const int r = c.w + kMfWaves * kk;
-      if (r < c.nrows) {
-        const int k = sample256(s.u.lg + r * PL, s.chunk.u[r][step % KCH]);
-        if (c.lane == 0) {
-          a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
-          s.ins[r] = k;
-        }
+    // rows c.w and c.w + 8 in one pass
+    static_assert(ROWS == 2 * kMfWaves, "two rows per wave");
+    const int r0 = c.w, r1 = c.w + kMfWaves;
+    const int2 k = sample256x2(s.u.lg + r0 * PL, s.u.lg + r1 * PL, s.chunk.u[r0][step % KCH], s.chunk.u[r1][step % KCH]);
+    if (c.lane == 0) {
+      if (r0 < c.nrows) {
+        a.samples[(long long)(c.b0 + r0) * a.n_steps + step] = k.x;
+        s.ins[r0] = k.x;
+      }
+      if (r1 < c.nrows) {
+        a.samples[(long long)(c.b0 + r1) * a.n_steps + step] = k.y;
+        s.ins[r1] = k.y;
       }
     }
   }

@@ -58,42 +58,57 @@ __device__ __forceinline__ float lane_f(float v, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
 }
 
-// Inverse-CDF sample of one row of 256 logits by one wavefront (each lane holds 4 consecutive
-// classes): max-subtracted exp, inclusive prefix sum over the classes in order, first class k with
-// u * Z < S_k (255 if none).
-__device__ __forceinline__ int sample256(const float *lg, float u) {
-  const int lane = threadIdx.x & 63;
-  const float4 l4 = *(const float4 *)(lg + 4 * lane);
-  // wave max: butterfly inside each row of 16, then the four row maxima
-  float m = fmaxf(fmaxf(l4.x, l4.y), fmaxf(l4.z, l4.w));
+// Inverse-CDF samples of two rows of 256 logits by one wavefront: lanes 0..31 take row A,
+// lanes 32..63 row B, each lane 8 consecutive classes.  Per row: max-subtracted exp, inclusive
+// prefix sum over the classes in order, first class k with u * Z < S_k (255 if none).  The two
+// rows' dependent chains of cross-lane moves run together.  Returns (class of A, class of B), wave-uniform.
+__device__ __forceinline__ int2 sample256x2(const float *lgA, const float *lgB, float uA, float uB) {
+  const int lane = threadIdx.x & 63, half = lane >> 5, row = lane >> 4;
+  const float *lg = (half ? lgB : lgA) + 8 * (lane & 31);
+  const float4 la = *(const float4 *)lg, lb = *(const float4 *)(lg + 4);
+  float m = fmaxf(fmaxf(fmaxf(la.x, la.y), fmaxf(la.z, la.w)), fmaxf(fmaxf(lb.x, lb.y), fmaxf(lb.z, lb.w)));
   m = fmaxf(m, dpp<0xB1>(m));   // quad_perm [1,0,3,2]
   m = fmaxf(m, dpp<0x4E>(m));   // quad_perm [2,3,0,1]
   m = fmaxf(m, dpp<0x141>(m));  // row_half_mirror
   m = fmaxf(m, dpp<0x140>(m));  // row_mirror
-  m = fmaxf(fmaxf(lane_f(m, 0), lane_f(m, 16)), fmaxf(lane_f(m, 32), lane_f(m, 48)));
-  const float e0 = __expf(l4.x - m), e1 = __expf(l4.y - m), e2 = __expf(l4.z - m), e3 = __expf(l4.w - m);
-  const float c0 = e0, c1 = c0 + e1, c2 = c1 + e2, c3 = c2 + e3;
-  // inclusive scan of the lane sums: inside each row of 16, then the preceding rows' totals
-  float incl = c3;
+  // rows of 16 lanes 0, 1 hold row A, rows 2, 3 row B
+  const float mA = fmaxf(lane_f(m, 0), lane_f(m, 16)), mB = fmaxf(lane_f(m, 32), lane_f(m, 48));
+  m = half ? mB : mA;
+  float c[8];
+  c[0] = __expf(la.x - m);
+  c[1] = c[0] + __expf(la.y - m);
+  c[2] = c[1] + __expf(la.z - m);
+  c[3] = c[2] + __expf(la.w - m);
+  c[4] = c[3] + __expf(lb.x - m);
+  c[5] = c[4] + __expf(lb.y - m);
+  c[6] = c[5] + __expf(lb.z - m);
+  c[7] = c[6] + __expf(lb.w - m);
+  // inclusive scan of the lane sums inside each row of 16, then row 1 (3) adds row 0's (2's) total
+  float incl = c[7];
   incl += dpp<0x111>(incl);  // row_shr:1
   incl += dpp<0x112>(incl);  // row_shr:2
   incl += dpp<0x114>(incl);  // row_shr:4
   incl += dpp<0x118>(incl);  // row_shr:8
   const float t0 = lane_f(incl, 15), t1 = lane_f(incl, 31), t2 = lane_f(incl, 47), t3 = lane_f(incl, 63);
-  const int row = lane >> 4;
-  incl += (row >= 1 ? t0 : 0.f) + (row >= 2 ? t1 : 0.f) + (row >= 3 ? t2 : 0.f);
-  const float excl = incl - c3;
-  const float Z = ((t0 + t1) + t2) + t3;
-  const float target = u * Z;
-  int first = 4;
-  if (target < excl + c3) first = 3;
-  if (target < excl + c2) first = 2;
-  if (target < excl + c1) first = 1;
-  if (target < excl + c0) first = 0;
-  const unsigned long long hit = __ballot(first < 4);
-  if (hit == 0ull) return 255;
-  const int src = __ffsll((long long)hit) - 1;
-  return 4 * src + __builtin_amdgcn_readlane(first, src);
+  incl += (row == 1 ? t0 : 0.f) + (row == 3 ? t2 : 0.f);
+  const float excl = incl - c[7];
+  const float target = half ? uB * (t2 + t3) : uA * (t0 + t1);
+  int first = 8;
+#pragma unroll
+  for (int k = 7; k >= 0; --k)
+    if (target < excl + c[k]) first = k;
+  const unsigned long long hit = __ballot(first < 8);
+  const unsigned int hA = (unsigned int)hit, hB = (unsigned int)(hit >> 32);
+  int kA = 255, kB = 255;
+  if (hA != 0u) {
+    const int src = __ffs((int)hA) - 1;
+    kA = 8 * src + __builtin_amdgcn_readlane(first, src);
+  }
+  if (hB != 0u) {
+    const int src = __ffs((int)hB) - 1;
+    kB = 8 * src + __builtin_amdgcn_readlane(first, 32 + src);
+  }
+  return make_int2(kA, kB);
 }
 
 }  // namespace mfd

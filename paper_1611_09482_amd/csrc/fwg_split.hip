@@ -60,11 +60,13 @@ constexpr int PS = S + 8;   // 512-channel activation rows (bf16)
 constexpr int PL = Q + 4;   // fp32 logits rows
 constexpr int PP = 20;      // fp32 partial-tile rows
 constexpr int PH = SL + 4;  // fp32 helper skip-partial rows
+constexpr int ZST = R / 2 + 4;  // staged z^l rows of a helper wave (32-bit words)
 constexpr int FA = kSpFA, FB = kSpFB, FS = kSpFS;
 constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);  // head fragments of a helper
 constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
 constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
+static_assert(ZST <= PH && ZST % 4 == 0, "a wave's staged z^l rows fit its partial-sum area, 16-byte aligned");
 static_assert(SL == 64 && FS == 8 && HL == 64 && QL == 32, "helper slices of 4 skip, 4 hidden and 2 class tiles");
 
 typedef unsigned long long u64;
@@ -163,15 +165,18 @@ __device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *stic
   __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Load N consecutive tagged words at p until every tag equals `tag` (or the launch is aborted).
-// Per lane.
-template <int N>
+// Load the N tagged words p[e STRIDE] until every tag equals `tag` (or the launch is aborted).
+// Per lane.  Every wait of a tile uses STRIDE = the number of lanes polling it, so that each load
+// instruction reads consecutive words: a poll whose lanes each take a run of consecutive words
+// touches a cache line per lane and instruction, and those requests (not the L2's latency) made
+// the tile gathers 2-3x slower.
+template <int N, int STRIDE = 1>
 __device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t (&out)[N], uint32_t *abort_word,
                                            uint32_t *sticky) {
   u64 v[N];
   for (int it = 0;; ++it) {
 #pragma unroll
-    for (int e = 0; e < N; ++e) v[e] = get_word(p + e);
+    for (int e = 0; e < N; ++e) v[e] = get_word(p + e * STRIDE);
     bool ok = true;
 #pragma unroll
     for (int e = 0; e < N; ++e) ok = ok && (uint32_t)(v[e] >> 32) == tag;
@@ -385,13 +390,14 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   const int w = c.w, tid = threadIdx.x;
   if (step % KCH == 0) stage_chunk(c, step);
   {
-    // thread t: stream t/32, classes 8 (t%32) .. +7
-    const int r = tid >> 5, k0 = 8 * (tid & 31);
+    // word i = e NT + t of the 16 x 256 logits: stream i / 256, class i % 256
     uint32_t v[8];
-    wait_words<8>(c.lgp + r * 256 + k0, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
-    float *dst = s.lg + r * PL + k0;
-    *(float4 *)dst = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
-    *(float4 *)(dst + 4) = make_float4(__uint_as_float(v[4]), __uint_as_float(v[5]), __uint_as_float(v[6]), __uint_as_float(v[7]));
+    wait_words<8, NT>(c.lgp + tid, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int i = e * NT + tid;
+      s.lg[(i >> 8) * PL + (i & 255)] = __uint_as_float(v[e]);
+    }
   }
   __syncthreads();
   // rows w and w + 8: sample (generation) or write the logits (forced modes)
@@ -406,15 +412,18 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
     }
     if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
   } else {
-#pragma unroll
-    for (int kk = 0; kk < ROWS / NW; ++kk) {
-      const int r = w + NW * kk;
-      if (r < c.nrows) {
-        const int k = sample256(s.lg + r * PL, s.chunk.u[r][step % KCH]);
-        if (c.lane == 0) {
-          a.samples[(long long)(c.b0 + r) * a.n_steps + step] = k;
-          s.ins[r] = k;
-        }
+    // rows w and w + 8 in one pass
+    static_assert(ROWS == 2 * NW, "two rows per wave");
+    const int r0 = w, r1 = w + NW;
+    const int2 k = sample256x2(s.lg + r0 * PL, s.lg + r1 * PL, s.chunk.u[r0][step % KCH], s.chunk.u[r1][step % KCH]);
+    if (c.lane == 0) {
+      if (r0 < c.nrows) {
+        a.samples[(long long)(c.b0 + r0) * a.n_steps + step] = k.x;
+        s.ins[r0] = k.x;
+      }
+      if (r1 < c.nrows) {
+        a.samples[(long long)(c.b0 + r1) * a.n_steps + step] = k.y;
+        s.ins[r1] = k.y;
       }
     }
   }
@@ -570,15 +579,18 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
 //  3. classes: gather relu(hidden); 32 classes = 2 tiles, each over four waves splitting the 16
 //     k-steps; + bias, out as fp32 words to the chain block.
 
-// Gather 16 x 512 bf16 activations (4096 words) into act: thread t takes stream t/32, channels
-// 16 (t%32) .. +15.
+// Gather 16 x 512 bf16 activations (4096 words of two channels each) into act: word i = e NT + t
+// holds stream i / 256, channels 2 (i % 256) and 2 (i % 256) + 1.
 __device__ __forceinline__ void gather_act(uint16_t *act, const u64 *src, uint32_t tag, uint32_t *abort_word,
                                            uint32_t *sticky) {
-  const int tid = threadIdx.x, r = tid >> 5, ch = 16 * (tid & 31);
+  const int tid = threadIdx.x;
   uint32_t v[8];
-  wait_words<8>(src + r * 256 + ch / 2, tag, v, abort_word, sticky);
-  *(u32x4 *)(act + r * PS + ch) = u32x4{v[0], v[1], v[2], v[3]};
-  *(u32x4 *)(act + r * PS + ch + 8) = u32x4{v[4], v[5], v[6], v[7]};
+  wait_words<8, NT>(src + tid, tag, v, abort_word, sticky);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int i = e * NT + tid;
+    ((uint32_t *)(act + (i >> 8) * PS))[i & 255] = v[e];
+  }
 }
 
 __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, int blk, int h) {
@@ -625,12 +637,16 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
     for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
     for (int i = 0; i < nl; ++i) {
       const int l = w + NW * i;
-      // B operand rows of z^l: stream n, channels 8q..8q+7 (k-step 0) and 32 + 8q.. (k-step 1)
-      const u64 *zl = zb + (size_t)l * ZWORDS + n * (R / 2) + 4 * q;
-      uint32_t v0[4], v1[4];
-      wait_words<4>(zl, tag, v0, abort_word, a.sp_sticky);
-      wait_words<4>(zl + 16, tag, v1, abort_word, a.sp_sticky);
-      const u32x4 b0 = u32x4{v0[0], v0[1], v0[2], v0[3]}, b1 = u32x4{v1[0], v1[1], v1[2], v1[3]};
+      // z^l (512 words): lane takes words e 64 + lane (stream 2e + lane / 32, channel pair lane % 32)
+      // and turns them into B operand rows (stream n, channels 8q..8q+7 for k-step 0, 32 + 8q.. for
+      // k-step 1) through its wave's partial-sum area, which the wave next writes after its last
+      // layer of the step (LDS operations of one wave complete in order)
+      uint32_t zv[8];
+      wait_words<8, 64>(zb + (size_t)l * ZWORDS + lane, tag, zv, abort_word, a.sp_sticky);
+      uint32_t *stg = (uint32_t *)s.u.part[w];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) stg[(2 * e + (lane >> 5)) * ZST + (lane & 31)] = zv[e];
+      const u32x4 b0 = *(const u32x4 *)(stg + n * ZST + 4 * q), b1 = *(const u32x4 *)(stg + n * ZST + 16 + 4 * q);
       if (i + 1 == nl) nxt = fw;  // the next layer of this wave is its first of the next step
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
