@@ -63,7 +63,7 @@ constexpr int PH = SL + 4;  // fp32 helper skip-partial rows
 constexpr int ZST = R / 2 + 4;  // staged z^l rows of a helper wave (32-bit words)
 constexpr int FA = kSpFA, FB = kSpFB, FS = kSpFS;
 constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);  // head fragments of a helper
-constexpr int DA = 2 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
+constexpr int DA = 3 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
 constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
 static_assert(ZST <= PH && ZST % 4 == 0, "a wave's staged z^l rows fit its partial-sum area, 16-byte aligned");
@@ -240,26 +240,29 @@ __device__ __forceinline__ void refill(Ctx &c, u32x4 (&W)[D], int f) {
 __device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int l, int ahead) {
   return *(const u32x4 *)(c.ring + (c.qoff[ahead * c.L + l] + c.rowb));
 }
+// The same load from an offset read from the table earlier.
+__device__ __forceinline__ u32x4 pop_issue_at(const Ctx &c, uint32_t off) {
+  return *(const u32x4 *)(c.ring + (off + c.rowb));
+}
 __device__ __forceinline__ void pop_land(const Ctx &c, int buf, u32x4 v) {
   if (c.lane < 32) {
     const int r = 4 * c.p + (c.lane >> 3);
     *(u32x4 *)(c.s->vbuf[buf] + r * PX + 8 * (c.lane & 7)) = v;
   }
 }
-// Push of layer l: its input x^l replaces the slot popped for this step.
-__device__ __forceinline__ void push_rows(const Ctx &c, int l) {
-  if (c.lane < 32) {
-    const int r = 4 * c.p + (c.lane >> 3);
-    const u32x4 v = *(const u32x4 *)(c.s->xbuf[l & 1] + r * PX + 8 * (c.lane & 7));
-    *(u32x4 *)(c.ring + (c.qoff[l] + c.rowb)) = v;
-  }
-}
-// z^l of stream rows 4p..4p+3 to the helpers: lane l covers row 4p + l/16, channels 4(l%16)..+3,
-// as two words of two bf16 each (word index = row * 32 + channel / 2).
-__device__ __forceinline__ void publish_z(const Ctx &c, int l, uint32_t tag) {
-  const int r = 4 * c.p + (c.lane >> 4), cp = 2 * (c.lane & 15);
-  const u32x2 v = *(const u32x2 *)(c.s->zbuf[l & 1] + r * PX + 2 * cp);
-  put_words2(c.zp + (size_t)l * ZWORDS + r * (R / 2) + cp, v.x, v.y, tag, c.local);
+// Between the layer's barriers: z^l of stream rows 4p..4p+3 to the helpers (lane l covers row
+// 4p + l/16, channels 4(l%16)..+3, as two words of two bf16 each; word index = row * 32 +
+// channel / 2), and the push of layer l (its input x^l replaces the slot popped for this step).
+// All LDS reads are issued before either store, so the wave waits for LDS once.
+__device__ __forceinline__ void publish_and_push(const Ctx &c, int l, uint32_t tag) {
+  const int rz = 4 * c.p + (c.lane >> 4), cp = 2 * (c.lane & 15);
+  const int rx = 4 * c.p + ((c.lane & 31) >> 3);
+  const u32x2 zv = *(const u32x2 *)(c.s->zbuf[l & 1] + rz * PX + 2 * cp);
+  const u32x4 xv = *(const u32x4 *)(c.s->xbuf[l & 1] + rx * PX + 8 * (c.lane & 7));
+  const uint32_t off = c.qoff[l];
+  __builtin_amdgcn_sched_barrier(0);
+  put_words2(c.zp + (size_t)l * ZWORDS + rz * (R / 2) + cp, zv.x, zv.y, tag, c.local);
+  if (c.lane < 32) *(u32x4 *)(c.ring + (off + c.rowb)) = xv;
 }
 
 // W_r v + b of layer ln from the popped rows in vbuf[vb3] and ring slots f0..f0+3 (tanh tile p
@@ -271,6 +274,8 @@ __device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int vb3, in
   const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
   const float *cb = c.conv_b + ln * 2 * R;
   f32x4 pt = ldsf4(cb + 16 * c.p + 4 * c.q), pg = ldsf4(cb + R + 16 * c.p + 4 * c.q);
+  // the four LDS reads in flight together (one wait), not one round trip per product
+  __builtin_amdgcn_sched_barrier(0);
   pt = mfma(W[f0 + 0], bv0, pt);
   pg = mfma(W[f0 + 2], bv0, pg);
   pt = mfma(W[f0 + 1], bv1, pt);
@@ -366,19 +371,20 @@ template <int PBS, int G6>
 __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P)[6], uint32_t tag) {
   const int L = c.L;
   const int ln = l + 1 < L ? l + 1 : 0;
+  // queue offset of the pop issued below, read with the product's LDS reads
+  const int j = l + 8 < L ? l + 8 : l + 8 - L;
+  const uint32_t joff = c.qoff[(l + 8 < L ? 0 : L) + j];
   recurrent_half(c, ln, (G6 + 1) % 3, (l + 1) & 1, W, PBS);
 #pragma unroll
   for (int f = 0; f < FB; ++f) refill(c, W, PBS + f);
   // the pop of layer l + 3 into LDS (its buffer was last read before the previous layer's first
   // barrier) and the pop of layer l + 8 issued
   pop_land(c, G6 % 3, P[(G6 + 3) % 6]);
-  const int j = l + 8 < L ? l + 8 : l + 8 - L;
-  P[(G6 + 2) % 6] = pop_issue(c, j, l + 8 < L ? 0 : 1);
+  P[(G6 + 2) % 6] = pop_issue_at(c, joff);
   __syncthreads();
   // while wave A runs the residual product: the layer's gate output to the helpers and its input
   // into its queue
-  publish_z(c, l, tag);
-  push_rows(c, l);
+  publish_and_push(c, l, tag);
   __syncthreads();
 }
 
@@ -452,10 +458,10 @@ __device__ __forceinline__ void a_role(Ctx &c) {
     for (int l = 0; l < L; l += 6) {
       a_layer<0>(c, l, W, xres);
       a_layer<FA>(c, l + 1, W, xres);
-      a_layer<0>(c, l + 2, W, xres);
-      a_layer<FA>(c, l + 3, W, xres);
-      a_layer<0>(c, l + 4, W, xres);
-      a_layer<FA>(c, l + 5, W, xres);
+      a_layer<2 * FA>(c, l + 2, W, xres);
+      a_layer<0>(c, l + 3, W, xres);
+      a_layer<FA>(c, l + 4, W, xres);
+      a_layer<2 * FA>(c, l + 5, W, xres);
     }
     finish_step(c, step);
   }
