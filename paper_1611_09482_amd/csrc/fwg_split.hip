@@ -388,13 +388,22 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
   __syncthreads();
 }
 
-// End of step `step` on every chain wave: the logits the helpers return, then the sample (or the
-// logits written out), the next inputs and the slot advance.  Two barriers.
+// End of step `step` on every chain wave: the slot advance, the logits the helpers return, then
+// the sample (or the logits written out) and the next inputs.  Two barriers.
 __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   ChainLds &s = *c.s;
   const StepArgs &a = *c.a;
   const int w = c.w, tid = threadIdx.x;
   if (step % KCH == 0) stage_chunk(c, step);
+  // the slot advance first, while the logits are still on their way: after the last layer's push
+  // no wave reads the offset table before the next step's first layer (two barriers away)
+  for (int l = tid; l < c.L; l += NT) {
+    const int nx = c.slot[l] + 1 == c.dil[l] ? 0 : c.slot[l] + 1;
+    const int nn = nx + 1 == c.dil[l] ? 0 : nx + 1;
+    c.slot[l] = nx;
+    c.qoff[l] = c.qoff[c.L + l];
+    c.qoff[c.L + l] = c.rbase[l] + (uint32_t)nn * (uint32_t)(a.bmax * R * 2);
+  }
   {
     // word i = e NT + t of the 16 x 256 logits: stream i / 256, class i % 256
     uint32_t v[8];
@@ -432,13 +441,6 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
         s.ins[r1] = k.y;
       }
     }
-  }
-  for (int l = tid; l < c.L; l += NT) {
-    const int nx = c.slot[l] + 1 == c.dil[l] ? 0 : c.slot[l] + 1;
-    const int nn = nx + 1 == c.dil[l] ? 0 : nx + 1;
-    c.slot[l] = nx;
-    c.qoff[l] = c.qoff[c.L + l];
-    c.qoff[c.L + l] = c.rbase[l] + (uint32_t)nn * (uint32_t)(a.bmax * R * 2);
   }
   __syncthreads();
 }
@@ -702,6 +704,7 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
       put_words2(hw + n * 256 + (h * HL + ch) / 2, pk.x, pk.y, tag, local);
     }
     // ---- 3. classes of the slice: tile j = w % 2, k-steps 4 (w / 2) .. +3
+    __syncthreads();
     gather_act(s.u.act, hw, tag, abort_word, a.sp_sticky);
     __syncthreads();
     {
