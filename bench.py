@@ -65,6 +65,52 @@ def stored_traffic(workload: str, steps: int):
     return rec.get("hbm_bytes_per_launch")
 
 
+def _counter_rows(path: str, counter: str):
+    """(dispatch id, kernel name, value) of every dispatch in a rocprofv3 --pmc CSV directory."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise SystemExit(f"expected one counter_collection.csv under {path}, found {len(files)}")
+    per = {}
+    for r in csv.DictReader(open(files[0])):
+        if r["Counter_Name"] == counter:
+            key = int(r["Dispatch_Id"])
+            name, val = per.get(key, (r["Kernel_Name"], 0.0))
+            per[key] = (name, val + float(r["Counter_Value"]))
+    return [(k, n, v) for k, (n, v) in sorted(per.items())]
+
+
+def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_step_kernel") -> dict:
+    """Write profiles/traffic_<workload>.json from four rocprofv3 counter passes under `root`:
+    FETCH_SIZE/ and WRITE_SIZE/ of `python bench.py --no-cpu-baseline` (the last dispatch of the
+    step kernel is the timed launch) and copy_FETCH_SIZE/, copy_WRITE_SIZE/ of
+    `python bench.py --copy-calibration` (a 256 MiB device copy: the factor that turns each counter
+    into bytes moved)."""
+    copy_bytes_kib = (256 << 20) / 1024.0
+    rec = {"kernel": kernel, "kernel_digest": kernel_source_digest(), "workload": workload, "steps": steps}
+    total = 0.0
+    for counter, key in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        launches = [v for _, n, v in _counter_rows(os.path.join(root, counter), counter) if kernel in n]
+        copies = [v for _, n, v in _counter_rows(os.path.join(root, "copy_" + counter), counter)
+                  if "copyBuffer" in n and v > 0.25 * copy_bytes_kib]
+        if not launches or not copies:
+            raise SystemExit(f"{counter}: no {kernel} dispatch or no copy dispatch found under {root}")
+        factor = copy_bytes_kib / (sum(copies) / len(copies))
+        rec[f"{key}_size_kib"] = launches[-1]
+        rec[f"{key}_factor"] = factor
+        total += launches[-1] * 1024.0 * factor
+    rec["hbm_bytes_per_launch"] = total
+    rec["command"] = ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir>/<COUNTER> -o <COUNTER> "
+                      "-- python bench.py --no-cpu-baseline; copy factors: rocprofv3 --pmc <COUNTER> --output-format csv "
+                      "-d <dir>/copy_<COUNTER> -o copy_<COUNTER> -- python bench.py --copy-calibration; then "
+                      "python bench.py --record-traffic <dir>")
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    with open(path, "w") as f:
+        json.dump(rec, f, indent=1)
+    return rec
+
+
 def cpu_baseline(wl, weights, u, target_seconds: float):
     """The oracle as it stands, on this host's cores, on a bounded sample of the workload:
     the first streams (one per thread) for as many leading steps as fit the time budget."""
@@ -232,7 +278,16 @@ def main():
     ap.add_argument("--max-blocks-layers", type=int, default=12, help="largest L of the sweep (naive_vs_fast)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device copy (counter calibration for rocprofv3)")
+    ap.add_argument("--record-traffic", metavar="DIR", default=None,
+                    help="write the traffic record of the benchmark launch from rocprofv3 counter passes under DIR "
+                         "(no GPU needed)")
     args = ap.parse_args()
+
+    if args.record_traffic:
+        import workloads as W
+        name = args.workload or W.BENCH_WORKLOAD
+        print(json.dumps(record_traffic(args.record_traffic, name, args.steps or W.WORKLOADS[name].n_steps), indent=1))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
