@@ -12,7 +12,8 @@
 //    the 256 classes.  Per step it accumulates sum_l W_skip^l z^l + b for its skip channels from
 //    the gate outputs z^l the chain block publishes, then (after gathering the whole relu(skip
 //    sum) from the group) its rows of the first head 1x1, then (after gathering the whole hidden
-//    layer) its classes of the output 1x1.  Its head weights stay in LDS for the whole launch.
+//    layer) its classes of the output 1x1.  Its head weights stay in its waves' registers for the
+//    whole launch.
 // No later layer reads a skip product and the head follows the last layer, so the chain block
 // streams only the 40 KB of conv and residual weights per layer; in the single-block kernel every
 // block that owns streams streams all 4 MB of weights once per step, which bounds its step.
@@ -87,8 +88,6 @@ struct ChainLds {
   // bias block
 };
 struct HelperLds {
-  u32x4 w1[FW1 * 64];  // first head 1x1, rows of the hidden slice: [tile][k-step][lane]
-  u32x4 w2[FW2 * 64];  // output 1x1, rows of the class slice: [tile][k-step][lane]
   union {
     float part[NW][ROWS * PH];  // per-wave partial skip sums of the slice
     uint16_t act[ROWS * PS];    // gathered relu(skip sum), then relu(hidden)
@@ -612,16 +611,24 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   u64 *sw = comm_s(a.sp_comm, L, blk), *hw = comm_hid(a.sp_comm, L, blk), *lw = comm_lg(a.sp_comm, L, blk);
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
   const float *skip_sum = s.bias, *head_b = s.bias + SL, *out_b = s.bias + SL + HL;
-  // bias and head slices into LDS for the whole launch
+  // the slice's biases into LDS for the whole launch
   {
     const float *src = a.mf_bias + L * 3 * R;  // skip sum [S], head [H], out [Q]
     for (int i = tid; i < SL; i += NT) s.bias[i] = src[h * SL + i];
     for (int i = tid; i < HL; i += NT) s.bias[SL + i] = src[S + h * HL + i];
     for (int i = tid; i < QL; i += NT) s.bias[SL + HL + i] = src[S + H + h * QL + i];
+  }
+  // this wave's head fragments, in registers for the whole launch (read from LDS, they and the
+  // activations made both head products bound by LDS bandwidth): first 1x1 tile w % 4, k-steps
+  // 8 (w / 4) .. +7; output 1x1 tile w % 2, k-steps 4 (w / 2) .. +3
+  u32x4 hw1[8], hw2[4];
+  {
     const u32x4 *w1 = (const u32x4 *)((const char *)a.mf_frags + base_w1(L, h) * 1024);
     const u32x4 *w2 = (const u32x4 *)((const char *)a.mf_frags + base_w2(L, h) * 1024);
-    for (int i = tid; i < FW1 * 64; i += NT) s.w1[i] = w1[i];
-    for (int i = tid; i < FW2 * 64; i += NT) s.w2[i] = w2[i];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) hw1[i] = w1[((w & 3) * (S / 32) + 8 * (w >> 2) + i) * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hw2[i] = w2[((w & 1) * (H / 32) + 4 * (w >> 1) + i) * 64 + lane];
   }
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
   u64 *hs = comm_hs(a.sp_comm, L, blk);
@@ -686,11 +693,15 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
     gather_act(s.u.act, sw, tag, abort_word, a.sp_sticky);
     __syncthreads();
     {
-      const int j = w & 3, k0 = 8 * (w >> 2);
-      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int k0 = 8 * (w >> 2);
+      // two accumulators (even and odd k-steps): two dependent chains of four MFMAs, not one of eight
+      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t;
 #pragma unroll
-      for (int ks = k0; ks < k0 + 8; ++ks)
-        t = mfma(s.w1[(j * (S / 32) + ks) * 64 + lane], lds16(s.u.act + n * PS + 32 * ks + 8 * q), t);
+      for (int i = 0; i < 8; i += 2) {
+        t = mfma(hw1[i], lds16(s.u.act + n * PS + 32 * (k0 + i) + 8 * q), t);
+        t1 = mfma(hw1[i + 1], lds16(s.u.act + n * PS + 32 * (k0 + i + 1) + 8 * q), t1);
+      }
+      t += t1;
       if (w >= 4) stf4(s.pw[w - 4] + n * PP + 4 * q, t);
       acc[0] = t;
     }
@@ -708,11 +719,14 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
     gather_act(s.u.act, hw, tag, abort_word, a.sp_sticky);
     __syncthreads();
     {
-      const int j = w & 1, k0 = 4 * (w >> 1);
-      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int k0 = 4 * (w >> 1);
+      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t;
 #pragma unroll
-      for (int ks = k0; ks < k0 + 4; ++ks)
-        t = mfma(s.w2[(j * (H / 32) + ks) * 64 + lane], lds16(s.u.act + n * PS + 32 * ks + 8 * q), t);
+      for (int i = 0; i < 4; i += 2) {
+        t = mfma(hw2[i], lds16(s.u.act + n * PS + 32 * (k0 + i) + 8 * q), t);
+        t1 = mfma(hw2[i + 1], lds16(s.u.act + n * PS + 32 * (k0 + i + 1) + 8 * q), t1);
+      }
+      t += t1;
       if (w >= 2) stf4(s.pw[w - 2] + n * PP + 4 * q, t);
       acc[0] = t;
     }

@@ -391,18 +391,28 @@ def test_delay_line_closed_form_gpu(fwidth, dil, path):
     assert np.array_equal(g[:, :, C:], np.zeros_like(g[:, :, C:]))
 
 
-def test_uniform_logits_sampler_gpu():
-    """All-equal logits: the sample is floor(256 u), bit-exact."""
-    cfg = FAMILIES["gated_r64_bf16"]
+@pytest.mark.parametrize("fam,B,regime", [("gated_r64_bf16", 16, "mfma_bf16_r64_s512"),
+                                          ("gated_r64_bf16_split", 13, "mfma_split_bf16_r64_s512"),
+                                          ("gated_r32_f32", 5, None)])
+def test_uniform_logits_sampler_gpu(fam, B, regime):
+    """All-equal logits: the sample is floor(256 u), bit-exact, in both halves of the MFMA
+    kernels' two-rows-per-wave sampler (rows w and w + 8) and with a ragged last block."""
+    cfg = FAMILIES[fam]
     w = W.make_weights(cfg, 5, bias_scale=0.1)
     w.out[:] = 0
     w.out_b[:] = 0
-    B, n = 16, 400
+    n = 400
     fw = binding.from_model(cfg, w, max_batch=B)
+    if regime is not None:
+        assert fw.regime == regime
     u = W.uniforms(9, B, n)
-    u[0, :6] = [0.0, 0.5, 1 - 2 ** -24, 3 / 256, 3 / 256 - 2 ** -24, 255 / 256]
+    edge = [0.0, 0.5, 1 - 2 ** -24, 3 / 256, 3 / 256 - 2 ** -24, 255 / 256]
+    u[0, :6] = edge
+    u[B - 1, :6] = edge[::-1]
     g = fw.generate(dev(u)).cpu().numpy()
     assert np.array_equal(g, np.floor(u.astype(np.float64) * 256).astype(np.int32))
+    if regime == "mfma_split_bf16_r64_s512":
+        fw.device_status()
 
 
 @pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split"])
