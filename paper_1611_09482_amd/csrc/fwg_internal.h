@@ -83,8 +83,8 @@ __host__ __device__ inline size_t mfma_frag_bytes(int L) { return kMfStageBytes 
 inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Split MFMA family (the MFMA family's model shape, L a multiple of 6 and at least 12): per 16
-// streams one chain block (layers and sampling) plus kSpHelpers helper blocks, each owning
-// S / kSpHelpers skip channels, H / kSpHelpers hidden channels and 256 / kSpHelpers classes.
+// streams one chain block (the layers), kSpHelpers helper blocks, each owning S / kSpHelpers skip
+// channels and H / kSpHelpers hidden channels, and one class block (output 1x1 and sampling).
 // Fragments per layer of chain waves A and B, and per layer and helper wave.
 constexpr int kSpHelpers = 8;
 constexpr int kSpFA = 6, kSpFB = 4, kSpFS = 8;

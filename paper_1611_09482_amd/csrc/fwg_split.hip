@@ -2,18 +2,19 @@
 // S = H = 512 skip/head channels and 256 classes (gfx950, v_mfma_f32_16x16x32_bf16, fp32
 // accumulation).  Same model shape and results as the MFMA step kernel of fwg_mfma.hip.
 //
-// The work of one step of a block of 16 streams is split over 1 + kSpHelpers blocks of the same
+// The work of one step of a block of 16 streams is split over 2 + kSpHelpers blocks of the same
 // launch (a group):
 //  - the chain block runs what lies on the layer-to-layer dependency chain: per layer the pop, the
-//    dilated width-2 product, the gate, the residual 1x1 and the push (paper Section 2.2), then
-//    the softmax and inverse-CDF sample of the logits the helpers return, which is the next step's
-//    input (Section 1);
-//  - helper h owns 64 of the 512 channels of the skip sum, of the head's hidden layer, and 32 of
-//    the 256 classes.  Per step it accumulates sum_l W_skip^l z^l + b for its skip channels from
-//    the gate outputs z^l the chain block publishes, then (after gathering the whole relu(skip
-//    sum) from the group) its rows of the first head 1x1, then (after gathering the whole hidden
-//    layer) its classes of the output 1x1.  Its head weights stay in its waves' registers for the
-//    whole launch.
+//    dilated width-2 product, the gate, the residual 1x1 and the push (paper Section 2.2); the
+//    sample the class block returns is the next step's input (Section 1);
+//  - helper h owns 64 of the 512 channels of the skip sum and of the head's hidden layer.  Per
+//    step it accumulates sum_l W_skip^l z^l + b for its skip channels from the gate outputs z^l
+//    the chain block publishes, then (after gathering the whole relu(skip sum) from the group) its
+//    rows of the first head 1x1.  Its head weights stay in its waves' registers for the launch;
+//  - the class block gathers the whole hidden layer, computes all 256 logits (the output 1x1 is in
+//    its waves' registers for the launch), draws the softmax / inverse-CDF sample of every stream
+//    and returns the samples to the chain block (forced modes: writes the logits out and returns a
+//    mark that the step's head is done).
 // No later layer reads a skip product and the head follows the last layer, so the chain block
 // streams only the 40 KB of conv and residual weights per layer; in the single-block kernel every
 // block that owns streams streams all 4 MB of weights once per step, which bounds its step.
@@ -36,7 +37,6 @@
 //    pops of stream rows 4p..4p+3, issued five layers before they land in LDS; between the layer's
 //    two barriers, while A runs the residual product, the publication of z^l to the helpers and the
 //    push of the layer input;
-//  - both: two sampled rows per wave.
 // Every chain wave streams its own pre-packed weight fragments from L2 through a ring of registers,
 // 12 fragments (two layers) for A and 24 (six layers) for B, whose loads also queue behind the
 // queue reads; a slot is refilled with the fragment one ring length ahead as soon as it is
@@ -77,13 +77,9 @@ struct ChainLds {
   uint16_t xbuf[2][ROWS * PX];     // layer inputs x^l, by layer parity
   uint16_t zbuf[2][ROWS * PX];     // gate outputs z^l, by layer parity
   float pbuf[2][4][2][ROWS * PP];  // W_r v + b of a layer: [layer parity][tile][tanh / sigmoid]
-  float lg[ROWS * PL];             // logits
   uint16_t embT[Q * R];            // embedding table, [class][channel]
-  union {
-    float u[ROWS][KCH];
-    int in[ROWS][KCH];
-  } chunk;
-  int ins[ROWS + NHLP];  // next inputs, then (at launch) the helpers' XCD ids
+  int in[ROWS][KCH];               // forced inputs (forced modes)
+  int ins[ROWS + NHLP + 1];        // next inputs, then (at launch) the helpers' and the class block's XCD ids
   // followed by the per-layer tables: slot[L], dil[L], rbase[L], qoff[2][L] (32-bit), then the fp32
   // bias block
 };
@@ -92,9 +88,16 @@ struct HelperLds {
     float part[NW][ROWS * PH];  // per-wave partial skip sums of the slice
     uint16_t act[ROWS * PS];    // gathered relu(skip sum), then relu(hidden)
   } u;
-  float pw[6][ROWS * PP];       // k-split partial tiles of the head products
-  float bias[SL + HL + QL];     // the slice's summed skip biases, hidden biases, class biases
+  float pw[4][ROWS * PP];       // k-split partial tiles of the first head product
+  float bias[SL + HL];          // the slice's summed skip biases and hidden biases
   int local;                    // the group's mode from the launch handshake
+};
+struct ClassLds {
+  uint16_t act[ROWS * PS];  // gathered relu(hidden)
+  float lg[ROWS * PL];      // logits
+  float u[ROWS][KCH];       // uniforms (generation)
+  float bias[Q];            // output biases
+  int local;                // the group's mode from the launch handshake
 };
 
 __host__ __device__ constexpr size_t chain_fixed_bytes() { return (sizeof(ChainLds) + 15) & ~size_t(15); }
@@ -114,24 +117,25 @@ __host__ __device__ inline size_t base_w1(int L, int h) { return base_h(L, NHLP,
 __host__ __device__ inline size_t base_w2(int L, int h) { return base_w1(L, NHLP) + (size_t)h * FW2; }
 __host__ __device__ inline size_t frag_count(int L) { return base_w2(L, NHLP); }
 
-// Exchange buffers: abort word, then per group: z^l words [L][512]; relu(skip sum), relu(hidden)
-// and logits words [16 streams][256] each; the launch handshake (slot h: XCD of helper h; slot
-// NHLP: the group's mode).  A device-scope load is served by the reader's own L2 when that L2 holds
+// Exchange buffers: abort word, then per group: z^l words [L][512]; relu(skip sum) and relu(hidden)
+// words [16 streams][256] each; the step's samples (forced modes: step-done marks) [16] in a
+// 256-byte line of their own; the launch handshake (slot h: XCD of helper h; slot NHLP: XCD of the
+// class block; slot NHLP + 1: the group's mode).  A device-scope load is served by the reader's own L2 when that L2 holds
 // the line from the reader's own store, so no block ever reads a line another block writes after
 // it has written to that line itself: every helper slice of a word array spans whole 256-byte
 // lines, and every handshake word has a 256-byte slot of its own.
-constexpr int ZWORDS = ROWS * R / 2, XWORDS = ROWS * 256, HSLOT = 32, HWORDS = (NHLP + 1) * HSLOT;
-static_assert((SL / 2) % 32 == 0 && (HL / 2) % 32 == 0 && QL % 32 == 0 && HSLOT == 32,
-              "helper slices and handshake slots span whole 256-byte lines");
-__host__ __device__ inline size_t group_words(int L) { return (size_t)L * ZWORDS + 3 * (size_t)XWORDS + HWORDS; }
+constexpr int ZWORDS = ROWS * R / 2, XWORDS = ROWS * 256, SWORDS = 32, HSLOT = 32, HWORDS = (NHLP + 2) * HSLOT;
+static_assert((SL / 2) % 32 == 0 && (HL / 2) % 32 == 0 && SWORDS == 32 && HSLOT == 32,
+              "helper slices, the sample line and handshake slots span whole 256-byte lines");
+__host__ __device__ inline size_t group_words(int L) { return (size_t)L * ZWORDS + 2 * (size_t)XWORDS + SWORDS + HWORDS; }
 __host__ __device__ inline u64 *comm_group(void *comm, int L, int blk) {
   return (u64 *)((char *)comm + 256) + (size_t)blk * group_words(L);
 }
 __host__ __device__ inline u64 *comm_z(void *comm, int L, int blk) { return comm_group(comm, L, blk); }
 __host__ __device__ inline u64 *comm_s(void *comm, int L, int blk) { return comm_group(comm, L, blk) + (size_t)L * ZWORDS; }
 __host__ __device__ inline u64 *comm_hid(void *comm, int L, int blk) { return comm_s(comm, L, blk) + XWORDS; }
-__host__ __device__ inline u64 *comm_lg(void *comm, int L, int blk) { return comm_hid(comm, L, blk) + XWORDS; }
-__host__ __device__ inline u64 *comm_hs(void *comm, int L, int blk) { return comm_lg(comm, L, blk) + XWORDS; }
+__host__ __device__ inline u64 *comm_smp(void *comm, int L, int blk) { return comm_hid(comm, L, blk) + XWORDS; }
+__host__ __device__ inline u64 *comm_hs(void *comm, int L, int blk) { return comm_smp(comm, L, blk) + SWORDS; }
 
 // `local`: every reader shares this block's XCD (and L2).
 __device__ __forceinline__ void put_word(u64 *p, uint32_t payload, uint32_t tag, bool local) {
@@ -210,7 +214,7 @@ struct Ctx {
   const char *nxt;  // next fragment the ring loads
   int wvoff;        // 16 * lane
   u64 *zp;          // this group's z^0 words (layer l at + l * ZWORDS)
-  const u64 *lgp;   // this group's logits words
+  const u64 *smp;   // this group's sample words
   uint32_t *abort_word, *sticky;
   bool local;       // the helpers share this block's XCD: workgroup-scope stores suffice
   int L, w, p, lane, n, q, b0, nrows, blk;
@@ -283,9 +287,9 @@ __device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int vb3, in
   stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
 }
 
-// Per-step inputs of steps [s0, s0 + KCH) into LDS (every thread, before the end-of-step barriers):
-// uniforms for generation, else the forced input that follows each step.
-__device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
+// Forced inputs of steps [s0, s0 + KCH) into LDS (forced modes; every thread): the input that
+// follows each step.
+__device__ __forceinline__ void stage_inputs(const Ctx &c, long long s0) {
   const StepArgs &a = *c.a;
   ChainLds &s = *c.s;
   static_assert((ROWS * KCH) % NT == 0, "the chunk divides evenly over the threads");
@@ -293,17 +297,10 @@ __device__ __forceinline__ void stage_chunk(const Ctx &c, long long s0) {
   for (int e = 0; e < ROWS * KCH / NT; ++e) {
     const int idx = (int)threadIdx.x + e * NT;
     const int r = idx / KCH, j = idx % KCH;
-    const long long st = s0 + j;
-    if (a.mode != MODE_GENERATE) {
-      const long long nx = st + forced_shift(a.mode);
-      int v = 0;
-      if (r < c.nrows && nx < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + nx];
-      s.chunk.in[r][j] = v;
-    } else {
-      float v = 0.f;
-      if (r < c.nrows && st < a.n_steps) v = a.uniforms[(long long)(c.b0 + r) * a.n_steps + st];
-      s.chunk.u[r][j] = v;
-    }
+    const long long nx = s0 + j + forced_shift(a.mode);
+    int v = 0;
+    if (r < c.nrows && nx < a.n_steps) v = a.inputs[(long long)(c.b0 + r) * a.n_steps + nx];
+    s.in[r][j] = v;
   }
 }
 
@@ -387,15 +384,20 @@ __device__ __forceinline__ void b_layer(Ctx &c, int l, u32x4 (&W)[DB], u32x4 (&P
   __syncthreads();
 }
 
-// End of step `step` on every chain wave: the slot advance, the logits the helpers return, then
-// the sample (or the logits written out) and the next inputs.  Two barriers.
+// End of step `step` on every chain wave: the slot advance, then the class block's word for each
+// stream (the sample in generation, which becomes the next input; a step-done mark in forced modes,
+// where the next input is the forced one).  Waiting for it in every mode also keeps the chain from
+// rewriting the z^l words before the helpers have read this step's.  One barrier (two when forced
+// inputs are staged).
 __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   ChainLds &s = *c.s;
   const StepArgs &a = *c.a;
-  const int w = c.w, tid = threadIdx.x;
-  if (step % KCH == 0) stage_chunk(c, step);
-  // the slot advance first, while the logits are still on their way: after the last layer's push
-  // no wave reads the offset table before the next step's first layer (two barriers away)
+  const int tid = threadIdx.x;
+  if (a.mode != MODE_GENERATE && step % KCH == 0) {
+    stage_inputs(c, step);
+    __syncthreads();
+  }
+  // no wave reads the offset table between the last layer's push and the next step's first layer
   for (int l = tid; l < c.L; l += NT) {
     const int nx = c.slot[l] + 1 == c.dil[l] ? 0 : c.slot[l] + 1;
     const int nn = nx + 1 == c.dil[l] ? 0 : nx + 1;
@@ -403,42 +405,13 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
     c.qoff[l] = c.qoff[c.L + l];
     c.qoff[c.L + l] = c.rbase[l] + (uint32_t)nn * (uint32_t)(a.bmax * R * 2);
   }
-  {
-    // word i = e NT + t of the 16 x 256 logits: stream i / 256, class i % 256
-    uint32_t v[8];
-    wait_words<8, NT>(c.lgp + tid, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int i = e * NT + tid;
-      s.lg[(i >> 8) * PL + (i & 255)] = __uint_as_float(v[e]);
-    }
-  }
-  __syncthreads();
-  // rows w and w + 8: sample (generation) or write the logits (forced modes)
-  if (a.mode != MODE_GENERATE) {
-#pragma unroll
-    for (int kk = 0; kk < ROWS / NW; ++kk) {
-      const int r = w + NW * kk;
-      if (r < c.nrows && a.logits) {
-        const float4 v = *(const float4 *)(s.lg + r * PL + 4 * c.lane);
-        *(float4 *)(a.logits + ((long long)(c.b0 + r) * a.n_steps + step) * Q + 4 * c.lane) = v;
-      }
-    }
-    if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) s.ins[tid] = s.chunk.in[tid][step % KCH];
-  } else {
-    // rows w and w + 8 in one pass
-    static_assert(ROWS == 2 * NW, "two rows per wave");
-    const int r0 = w, r1 = w + NW;
-    const int2 k = sample256x2(s.lg + r0 * PL, s.lg + r1 * PL, s.chunk.u[r0][step % KCH], s.chunk.u[r1][step % KCH]);
-    if (c.lane == 0) {
-      if (r0 < c.nrows) {
-        a.samples[(long long)(c.b0 + r0) * a.n_steps + step] = k.x;
-        s.ins[r0] = k.x;
-      }
-      if (r1 < c.nrows) {
-        a.samples[(long long)(c.b0 + r1) * a.n_steps + step] = k.y;
-        s.ins[r1] = k.y;
-      }
+  if (tid < ROWS) {
+    uint32_t v[1];
+    wait_words<1>(c.smp + tid, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
+    if (a.mode == MODE_GENERATE) {
+      s.ins[tid] = (int)v[0];
+    } else if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) {
+      s.ins[tid] = s.in[tid][step % KCH];
     }
   }
   __syncthreads();
@@ -534,7 +507,7 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   c.wvoff = 16 * c.lane;
   c.rowb = (uint32_t)(((c.b0 + 4 * c.p + ((c.lane & 31) >> 3)) * R + 8 * (c.lane & 7)) * 2);
   c.zp = comm_z(a.sp_comm, L, blk);
-  c.lgp = comm_lg(a.sp_comm, L, blk);
+  c.smp = comm_smp(a.sp_comm, L, blk);
   c.abort_word = (uint32_t *)a.sp_comm;
   c.sticky = a.sp_sticky;
 
@@ -558,18 +531,18 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
     if (tid < c.nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
     s.ins[tid] = v;
   }
-  // launch handshake: read the helpers' XCD ids, publish the group's mode
+  // launch handshake: read the helpers' and the class block's XCD ids, publish the group's mode
   u64 *hs = comm_hs(a.sp_comm, L, blk);
-  if (tid < NHLP) {
+  if (tid < NHLP + 1) {
     uint32_t v[1];
     wait_words<1>(hs + HSLOT * tid, 1, v, c.abort_word, c.sticky);
     s.ins[ROWS + tid] = (int)v[0];
   }
   __syncthreads();
   bool local = true;
-  for (int h = 0; h < NHLP; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
+  for (int h = 0; h < NHLP + 1; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
   c.local = local;
-  if (tid == 0) put_word(hs + HSLOT * NHLP, local ? 1u : 0u, 1, false);
+  if (tid == 0) put_word(hs + HSLOT * (NHLP + 1), local ? 1u : 0u, 1, false);
   if (c.w < 4) a_role(c);
   else b_role(c);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
@@ -582,9 +555,7 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
 //     waves' partials meet in LDS, get the summed skip biases, relu and bf16 rounding, and go out
 //     as words;
 //  2. hidden: gather relu(skip sum) of all 512 channels; 64 hidden rows = 4 tiles, each over two
-//     waves that split the 16 k-steps; + bias, relu, bf16, out as words;
-//  3. classes: gather relu(hidden); 32 classes = 2 tiles, each over four waves splitting the 16
-//     k-steps; + bias, out as fp32 words to the chain block.
+//     waves that split the 16 k-steps; + bias, relu, bf16, out as words to the class block.
 
 // Gather 16 x 512 bf16 activations (4096 words of two channels each) into act: word i = e NT + t
 // holds stream i / 256, channels 2 (i % 256) and 2 (i % 256) + 1.
@@ -608,34 +579,29 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   const char *fw = (const char *)a.mf_frags + base_h(L, h, w) * 1024;
   const int wvoff = 16 * lane;
   const u64 *zb = comm_z(a.sp_comm, L, blk);
-  u64 *sw = comm_s(a.sp_comm, L, blk), *hw = comm_hid(a.sp_comm, L, blk), *lw = comm_lg(a.sp_comm, L, blk);
+  u64 *sw = comm_s(a.sp_comm, L, blk), *hw = comm_hid(a.sp_comm, L, blk);
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
-  const float *skip_sum = s.bias, *head_b = s.bias + SL, *out_b = s.bias + SL + HL;
+  const float *skip_sum = s.bias, *head_b = s.bias + SL;
   // the slice's biases into LDS for the whole launch
   {
     const float *src = a.mf_bias + L * 3 * R;  // skip sum [S], head [H], out [Q]
     for (int i = tid; i < SL; i += NT) s.bias[i] = src[h * SL + i];
     for (int i = tid; i < HL; i += NT) s.bias[SL + i] = src[S + h * HL + i];
-    for (int i = tid; i < QL; i += NT) s.bias[SL + HL + i] = src[S + H + h * QL + i];
   }
-  // this wave's head fragments, in registers for the whole launch (read from LDS, they and the
-  // activations made both head products bound by LDS bandwidth): first 1x1 tile w % 4, k-steps
-  // 8 (w / 4) .. +7; output 1x1 tile w % 2, k-steps 4 (w / 2) .. +3
-  u32x4 hw1[8], hw2[4];
+  // this wave's fragments of the first head 1x1 (tile w % 4, k-steps 8 (w / 4) .. +7), in registers
+  // for the whole launch
+  u32x4 hw1[8];
   {
     const u32x4 *w1 = (const u32x4 *)((const char *)a.mf_frags + base_w1(L, h) * 1024);
-    const u32x4 *w2 = (const u32x4 *)((const char *)a.mf_frags + base_w2(L, h) * 1024);
 #pragma unroll
     for (int i = 0; i < 8; ++i) hw1[i] = w1[((w & 3) * (S / 32) + 8 * (w >> 2) + i) * 64 + lane];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) hw2[i] = w2[((w & 1) * (H / 32) + 4 * (w >> 1) + i) * 64 + lane];
   }
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
   u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid == 0) {
     put_word(hs + HSLOT * h, xcd_id(), 1, false);
     uint32_t v[1];
-    wait_words<1>(hs + HSLOT * NHLP, 1, v, abort_word, a.sp_sticky);
+    wait_words<1>(hs + HSLOT * (NHLP + 1), 1, v, abort_word, a.sp_sticky);
     s.local = (int)v[0];
   }
   __syncthreads();
@@ -714,30 +680,95 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
       const u32x2 pk = pack4(t);
       put_words2(hw + n * 256 + (h * HL + ch) / 2, pk.x, pk.y, tag, local);
     }
-    // ---- 3. classes of the slice: tile j = w % 2, k-steps 4 (w / 2) .. +3
-    __syncthreads();
-    gather_act(s.u.act, hw, tag, abort_word, a.sp_sticky);
-    __syncthreads();
-    {
-      const int k0 = 4 * (w >> 1);
-      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Class block of group blk.  Per step: gather relu(hidden) of all 512 channels; wave w computes
+// classes 32w .. 32w + 31 (output 1x1 tiles 2w, 2w + 1 over all 16 k-steps, its fragments in
+// registers for the whole launch) + bias into LDS; then each wave takes streams w and w + 8:
+// generation draws their samples (written out and returned to the chain block), forced modes write
+// their logits out and return a step-done mark.
+
+__device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, int blk) {
+  ClassLds &s = *(ClassLds *)lds_raw;
+  const int tid = threadIdx.x, L = a.L;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, n = lane & 15, q = lane >> 4;
+  const int b0 = blk * ROWS, nrows = min(ROWS, a.batch - b0);
+  const u64 *hw = comm_hid(a.sp_comm, L, blk);
+  u64 *sm = comm_smp(a.sp_comm, L, blk);
+  uint32_t *abort_word = (uint32_t *)a.sp_comm;
+  for (int i = tid; i < Q; i += NT) s.bias[i] = a.mf_bias[L * 3 * R + S + H + i];
+  // output 1x1 fragments of classes 32w .. 32w + 31: tile j, k-step ks at j * 16 + ks of slice w
+  u32x4 wo[2][H / 32];
+  {
+    const u32x4 *src = (const u32x4 *)((const char *)a.mf_frags + base_w2(L, w) * 1024);
 #pragma unroll
-      for (int i = 0; i < 4; i += 2) {
-        t = mfma(hw2[i], lds16(s.u.act + n * PS + 32 * (k0 + i) + 8 * q), t);
-        t1 = mfma(hw2[i + 1], lds16(s.u.act + n * PS + 32 * (k0 + i + 1) + 8 * q), t1);
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int ks = 0; ks < H / 32; ++ks) wo[j][ks] = src[(j * (H / 32) + ks) * 64 + lane];
+  }
+  // launch handshake: publish this block's XCD, then learn whether the whole group shares it
+  u64 *hs = comm_hs(a.sp_comm, L, blk);
+  if (tid == 0) {
+    put_word(hs + HSLOT * NHLP, xcd_id(), 1, false);
+    uint32_t v[1];
+    wait_words<1>(hs + HSLOT * (NHLP + 1), 1, v, abort_word, a.sp_sticky);
+    s.local = (int)v[0];
+  }
+  __syncthreads();
+  const bool local = s.local != 0;
+  for (long long step = 0; step < a.n_steps; ++step) {
+    const uint32_t tag = (uint32_t)(step + 1);
+    gather_act(s.act, hw, tag, abort_word, a.sp_sticky);
+    __syncthreads();
+    // uniforms of steps [step, step + KCH): every wave has sampled the previous chunk's last step
+    // before the barrier above
+    if (a.mode == MODE_GENERATE && step % KCH == 0) {
+#pragma unroll
+      for (int e = 0; e < ROWS * KCH / NT; ++e) {
+        const int idx = tid + e * NT, r = idx / KCH, j = idx % KCH;
+        float v = 0.f;
+        if (r < nrows && step + j < a.n_steps) v = a.uniforms[(long long)(b0 + r) * a.n_steps + step + j];
+        s.u[r][j] = v;
       }
-      t += t1;
-      if (w >= 2) stf4(s.pw[w - 2] + n * PP + 4 * q, t);
-      acc[0] = t;
+    }
+    // classes 32w + 16j + 4q .. +3 of stream n; two accumulators per tile (even and odd k-steps)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      f32x4 t0 = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t0;
+#pragma unroll
+      for (int ks = 0; ks < H / 32; ks += 2) {
+        t0 = mfma(wo[j][ks], lds16(s.act + n * PS + 32 * ks + 8 * q), t0);
+        t1 = mfma(wo[j][ks + 1], lds16(s.act + n * PS + 32 * (ks + 1) + 8 * q), t1);
+      }
+      const int k = 32 * w + 16 * j + 4 * q;
+      stf4(s.lg + n * PL + k, t0 + t1 + ldsf4(s.bias + k));
     }
     __syncthreads();
-    if (w < 2) {
-      const int k = 16 * w + 4 * q;
-      f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q) + ldsf4(s.pw[w + 2] + n * PP + 4 * q) +
-                ldsf4(s.pw[w + 4] + n * PP + 4 * q);
-      u64 *dst = lw + n * 256 + h * QL + k;
-      put_words2(dst, __float_as_uint(t[0] + out_b[k]), __float_as_uint(t[1] + out_b[k + 1]), tag, local);
-      put_words2(dst + 2, __float_as_uint(t[2] + out_b[k + 2]), __float_as_uint(t[3] + out_b[k + 3]), tag, local);
+    const int r0 = w, r1 = w + NW;
+    static_assert(ROWS == 2 * NW, "two rows per wave");
+    if (a.mode == MODE_GENERATE) {
+      const int2 k = sample256x2(s.lg + r0 * PL, s.lg + r1 * PL, s.u[r0][step % KCH], s.u[r1][step % KCH]);
+      if (lane == 0) {
+        if (r0 < nrows) a.samples[(long long)(b0 + r0) * a.n_steps + step] = k.x;
+        if (r1 < nrows) a.samples[(long long)(b0 + r1) * a.n_steps + step] = k.y;
+        put_word(sm + r0, (uint32_t)k.x, tag, local);
+        put_word(sm + r1, (uint32_t)k.y, tag, local);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+        const int r = kk ? r1 : r0;
+        if (r < nrows && a.logits) {
+          const float4 v = *(const float4 *)(s.lg + r * PL + 4 * lane);
+          *(float4 *)(a.logits + ((long long)(b0 + r) * a.n_steps + step) * Q + 4 * lane) = v;
+        }
+      }
+      if (lane == 0) {
+        put_word(sm + r0, 0u, tag, local);
+        put_word(sm + r1, 0u, tag, local);
+      }
     }
   }
 }
@@ -745,12 +776,15 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
 __global__ void __launch_bounds__(NT) split_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   const int nb = a.sp_nb;
-  if ((int)blockIdx.x < nb) {
+  // helper h of group b sits at nb + h nb + b and its class block at (1 + NHLP) nb + b: with nb a
+  // multiple of 8, all on the XCD of chain block b
+  const int e = (int)blockIdx.x - nb;
+  if (e < 0) {
     chain_block(a, (char *)lds_raw, blockIdx.x);
-  } else {
-    // helper h of group b sits at nb + h nb + b: with nb a multiple of 8, on the XCD of chain block b
-    const int e = (int)blockIdx.x - nb;
+  } else if (e < NHLP * nb) {
     helper_block(a, (char *)lds_raw, e % nb, e / nb);
+  } else {
+    class_block(a, (char *)lds_raw, e - NHLP * nb);
   }
 }
 
@@ -797,8 +831,9 @@ __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, c
   frags[dst * 64 + lane] = pack8(v);
 }
 
-// Head slices of helper h: first 1x1 fragment (tile j, k-step ks) of rows 64h + 16j.. at
-// j * 16 + ks; output 1x1 fragment (tile j, k-step ks) of classes 32h + 16j.. at j * 16 + ks.
+// Head slices h: first 1x1 fragment (tile j, k-step ks) of rows 64h + 16j.. at j * 16 + ks (helper
+// h); output 1x1 fragment (tile j, k-step ks) of classes 32h + 16j.. at j * 16 + ks (class block
+// wave h).
 __global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, int L, uint4 *frags) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= NHLP * (FW1 + FW2) * 64) return;
@@ -826,12 +861,13 @@ size_t split_comm_bytes(int L, int nb) { return 256 + (size_t)nb * sp::group_wor
 
 size_t split_lds_bytes(int L) {
   const size_t chain = sp::chain_fixed_bytes() + sp::dyn_bias_offset(L) + sizeof(float) * ((size_t)L * 3 * kMfR + kMfR);
-  const size_t helper = sizeof(sp::HelperLds);
-  return chain > helper ? chain : helper;
+  const size_t helper = sizeof(sp::HelperLds), cls = sizeof(sp::ClassLds);
+  const size_t m = chain > helper ? chain : helper;
+  return m > cls ? m : cls;
 }
 
 hipError_t launch_split_step(const StepArgs &a, hipStream_t s) {
-  const dim3 grid(a.sp_nb * (1 + kSpHelpers)), block(kMfThreads);
+  const dim3 grid(a.sp_nb * (2 + kSpHelpers)), block(kMfThreads);
   hipLaunchKernelGGL(sp::split_step_kernel, grid, block, split_lds_bytes(a.L), s, a);
   return hipGetLastError();
 }
@@ -846,7 +882,7 @@ hipError_t split_setup(int L, int nb, int *coresident_ok) {
     return e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
-  *coresident_ok = (long long)per_cu * cus >= (long long)nb * (1 + kSpHelpers);
+  *coresident_ok = (long long)per_cu * cus >= (long long)nb * (2 + kSpHelpers);
   return hipSuccess;
 }
 
