@@ -431,6 +431,24 @@ def test_continuation_reset_and_determinism_gpu(fam):
     assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), full)
 
 
+def test_split_multi_group_ragged():
+    """The split kernels over three groups with a ragged last one (37 streams = 16 + 16 + 5): the
+    helpers and class blocks of groups 1 and 2 sit on other XCDs than their chain blocks, so those
+    groups exchange words with device-scope stores while group 0 uses workgroup-scope ones; teacher
+    forcing through the step kernels and generation against the oracle, across several 64-step
+    input chunks."""
+    cfg = FAMILIES["gated_r64_bf16_split"]
+    B, n = 37, 200
+    w, fw, orc = build_pair(cfg, 102, B, fam="gated_r64_bf16_split")
+    assert fw.regime == "mfma_split_bf16_r64_s512"
+    x = W.sequences(5, B, n)
+    err = row_rel_err(fw.teacher_forced(dev(x)).cpu().numpy(), orc.teacher_forced(x))
+    fw.device_status()
+    log(f"split B={B}: TF max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+    check_generation(cfg, fw, orc, W.uniforms(6, B, n), B, "split multi-group")
+
+
 def test_split_state_cleared_on_poisoned_workspace():
     """The split kernels' launch state (exchange words, abort mark) is set up by the library itself:
     a handle created on memory that held 0xFF bytes (the caching allocator hands the freed block back)
