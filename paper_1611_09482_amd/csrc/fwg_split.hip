@@ -25,7 +25,8 @@
 // order the payload.  The blocks of a group compare their XCD ids at launch: when they share one,
 // and so its L2, the words are stored with workgroup-scope stores, which complete in that L2;
 // otherwise with device-scope stores, which write through to memory and whose slow completion holds
-// up every later memory wait of the storing wave.  Every wait is bounded: a wait that runs out sets
+// up every later memory wait of the storing wave.  Each load instruction of a poll reads
+// consecutive words across the polling lanes.  Every wait is bounded: a wait that runs out sets
 // the launch's abort word, which ends every other wait (the results are then invalid, and a sticky
 // word lets the host report it); every wave keeps executing its straight-line program, so the grid
 // always drains.
@@ -36,9 +37,9 @@
 //  - wave B (p): W_r v + b of the next layer (v = the popped state, known early) and the queue
 //    pops of stream rows 4p..4p+3, issued five layers before they land in LDS; between the layer's
 //    two barriers, while A runs the residual product, the publication of z^l to the helpers and the
-//    push of the layer input;
+//    push of the layer input.
 // Every chain wave streams its own pre-packed weight fragments from L2 through a ring of registers,
-// 12 fragments (two layers) for A and 24 (six layers) for B, whose loads also queue behind the
+// 18 fragments (three layers) for A and 24 (six layers) for B, whose loads also queue behind the
 // queue reads; a slot is refilled with the fragment one ring length ahead as soon as it is
 // consumed.  The layer loop is unrolled by six layers so every ring slot is a fixed register.
 #include <hip/hip_runtime.h>
@@ -55,7 +56,8 @@ using namespace mfd;
 constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
 constexpr int NT = kMfThreads, NW = kMfWaves;
 constexpr int NHLP = kSpHelpers;          // helpers per group
-constexpr int SL = S / NHLP, HL = H / NHLP, QL = Q / NHLP;  // skip / hidden / class slice of a helper
+// skip and hidden slices of a helper; classes of a class-block wave (one per helper index)
+constexpr int SL = S / NHLP, HL = H / NHLP, QL = Q / NHLP;
 constexpr int PX = R + 8;   // 64-channel activation rows (bf16)
 constexpr int PS = S + 8;   // 512-channel activation rows (bf16)
 constexpr int PL = Q + 4;   // fp32 logits rows
@@ -63,12 +65,14 @@ constexpr int PP = 20;      // fp32 partial-tile rows
 constexpr int PH = SL + 4;  // fp32 helper skip-partial rows
 constexpr int ZST = R / 2 + 4;  // staged z^l rows of a helper wave (32-bit words)
 constexpr int FA = kSpFA, FB = kSpFB, FS = kSpFS;
-constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);  // head fragments of a helper
+// fragments of a helper's first-1x1 slice and of a class-block wave's output-1x1 slice
+constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);
 constexpr int DA = 3 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
 constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
 static_assert(ZST <= PH && ZST % 4 == 0, "a wave's staged z^l rows fit its partial-sum area, 16-byte aligned");
-static_assert(SL == 64 && FS == 8 && HL == 64 && QL == 32, "helper slices of 4 skip, 4 hidden and 2 class tiles");
+static_assert(SL == 64 && FS == 8 && HL == 64 && QL == 32 && NHLP == NW,
+              "helper slices of 4 skip and 4 hidden tiles; 2 class tiles per class-block wave");
 
 typedef unsigned long long u64;
 
@@ -216,7 +220,7 @@ struct Ctx {
   u64 *zp;          // this group's z^0 words (layer l at + l * ZWORDS)
   const u64 *smp;   // this group's sample words
   uint32_t *abort_word, *sticky;
-  bool local;       // the helpers share this block's XCD: workgroup-scope stores suffice
+  bool local;       // the helpers and the class block share this XCD: workgroup-scope stores suffice
   int L, w, p, lane, n, q, b0, nrows, blk;
 };
 
