@@ -737,17 +737,22 @@ __device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, in
         s.u[r][j] = v;
       }
     }
-    // classes 32w + 16j + 4q .. +3 of stream n; two accumulators per tile (even and odd k-steps)
+    // classes 32w + 16j + 4q .. +3 of stream n; two accumulators per tile (even and odd k-steps),
+    // the k-step loop outermost: each activation read feeds both tiles and four independent
+    // accumulation chains keep the matrix core busy
+    f32x4 acc[2][2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[j][0] = acc[j][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < H / 32; ++ks) {
+      const u32x4 b = lds16(s.act + n * PS + 32 * ks + 8 * q);
+      acc[0][ks & 1] = mfma(wo[0][ks], b, acc[0][ks & 1]);
+      acc[1][ks & 1] = mfma(wo[1][ks], b, acc[1][ks & 1]);
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      f32x4 t0 = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t0;
-#pragma unroll
-      for (int ks = 0; ks < H / 32; ks += 2) {
-        t0 = mfma(wo[j][ks], lds16(s.act + n * PS + 32 * ks + 8 * q), t0);
-        t1 = mfma(wo[j][ks + 1], lds16(s.act + n * PS + 32 * (ks + 1) + 8 * q), t1);
-      }
       const int k = 32 * w + 16 * j + 4 * q;
-      stf4(s.lg + n * PL + k, t0 + t1 + ldsf4(s.bias + k));
+      stf4(s.lg + n * PL + k, acc[j][0] + acc[j][1] + ldsf4(s.bias + k));
     }
     __syncthreads();
     const int r0 = w, r1 = w + NW;
