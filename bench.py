@@ -81,7 +81,7 @@ def _counter_rows(path: str, counter: str):
     return [(k, n, v) for k, (n, v) in sorted(per.items())]
 
 
-def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_step_kernel") -> dict:
+def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_step_kernel", out_path=None) -> dict:
     """Write profiles/traffic_<workload>.json from four rocprofv3 counter passes under `root`:
     FETCH_SIZE/ and WRITE_SIZE/ of `python bench.py --no-cpu-baseline` (the last dispatch of the
     step kernel is the timed launch) and copy_FETCH_SIZE/, copy_WRITE_SIZE/ of
@@ -105,7 +105,7 @@ def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_st
                       "-- python bench.py --no-cpu-baseline; copy factors: rocprofv3 --pmc <COUNTER> --output-format csv "
                       "-d <dir>/copy_<COUNTER> -o copy_<COUNTER> -- python bench.py --copy-calibration; then "
                       "python bench.py --record-traffic <dir>")
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    path = out_path or os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     with open(path, "w") as f:
         json.dump(rec, f, indent=1)
     return rec
