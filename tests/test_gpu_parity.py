@@ -431,14 +431,15 @@ def test_continuation_reset_and_determinism_gpu(fam):
     assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), full)
 
 
-def test_split_multi_group_ragged():
+@pytest.mark.parametrize("B", [1, 37])
+def test_split_multi_group_ragged(B):
     """The split kernels over three groups with a ragged last one (37 streams = 16 + 16 + 5): the
     helpers and class blocks of groups 1 and 2 sit on other XCDs than their chain blocks, so those
-    groups exchange words with device-scope stores while group 0 uses workgroup-scope ones; teacher
-    forcing through the step kernels and generation against the oracle, across several 64-step
-    input chunks."""
+    groups exchange words with device-scope stores while group 0 uses workgroup-scope ones; and one
+    stream (a single group with 15 padded rows).  Teacher forcing through the step kernels and
+    generation against the oracle, across several 64-step input chunks."""
     cfg = FAMILIES["gated_r64_bf16_split"]
-    B, n = 37, 200
+    n = 200
     w, fw, orc = build_pair(cfg, 102, B, fam="gated_r64_bf16_split")
     assert fw.regime == "mfma_split_bf16_r64_s512"
     x = W.sequences(5, B, n)
