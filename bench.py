@@ -53,16 +53,25 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload: str, steps: int):
-    """HBM bytes per launch from committed rocprofv3 counter passes, if they were taken on the
-    current kernel sources and the same launch size; else None."""
+def stored_traffic(workload: str):
+    """The committed traffic record of the workload's benchmark kernel (rocprofv3 counter passes
+    over one long launch), if it was taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("kernel_digest") != kernel_source_digest() or rec.get("steps") != steps:
+    if rec.get("kernel_digest") != kernel_source_digest() or not rec.get("steps"):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
+
+
+def traffic_for(rec, steps: int):
+    """HBM bytes of a launch of `steps` steps from a traffic record: the record's bytes per step
+    (its launch's bytes over its steps; the launch-fixed part, the weights each block reads once, is
+    below 0.1% of an 8,000-step launch) times `steps`."""
+    if rec is None:
+        return None
+    return rec["hbm_bytes_per_launch"] / rec["steps"] * steps
 
 
 def _counter_rows(path: str, counter: str):
@@ -101,6 +110,7 @@ def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_st
         rec[f"{key}_factor"] = factor
         total += launches[-1] * 1024.0 * factor
     rec["hbm_bytes_per_launch"] = total
+    rec["hbm_bytes_per_step"] = total / steps
     rec["command"] = ("rocprofv3 --pmc FETCH_SIZE (then WRITE_SIZE) --output-format csv -d <dir>/<COUNTER> -o <COUNTER> "
                       "-- python bench.py --no-cpu-baseline; copy factors: rocprofv3 --pmc <COUNTER> --output-format csv "
                       "-d <dir>/copy_<COUNTER> -o copy_<COUNTER> -- python bench.py --copy-calibration; then "
@@ -111,49 +121,65 @@ def record_traffic(root: str, workload: str, steps: int, kernel: str = "split_st
     return rec
 
 
-def cpu_baseline(wl, weights, u, target_seconds: float):
-    """The oracle as it stands, on this host's cores, on a bounded sample of the workload:
-    the first streams (one per thread) for as many leading steps as fit the time budget."""
+def _oracle_build_note() -> str:
     import oracle
+    return "float64 CPU oracle (" + " ".join(oracle.GCC_CMD[:4]) + ", no BLAS)"
+
+
+def cpu_baseline(wl, weights, target_seconds: float):
+    """The oracle as it stands, on this host's cores, on a bounded sample of the workload: the first
+    streams (one per thread) generate a few calibration steps, then as many further steps as fit the
+    time budget.  It draws its own uniforms (the workload's seed, those streams and steps), so the
+    steps it runs do not depend on the GPU run's length; the rate counts exactly the steps the
+    oracle's state advanced over in the timed call."""
+    import oracle
+    import workloads as W
     threads = oracle.max_threads()
     streams = max(1, min(wl.batch, threads))
     o = oracle.Oracle(weights)
     calib = 4
     st = o.state(streams)
     t0 = time.perf_counter()
-    st.generate(u[:streams, :calib].copy())
+    st.generate(W.uniforms(wl.uniform_seed, streams, calib))
     per_step = (time.perf_counter() - t0) / calib
     steps = int(max(8, min(wl.n_steps - calib, target_seconds / max(per_step, 1e-9))))
+    u = W.uniforms(wl.uniform_seed, streams, steps, t0=calib)
+    t_before = st.t
     t0 = time.perf_counter()
-    st.generate(u[:streams, calib:calib + steps].copy())
+    st.generate(u)
     dt = time.perf_counter() - t0
-    return {"value": streams * steps / dt, "unit": "samples/s", "cores": min(threads, streams),
-            "kind": "oracle",
-            "sample": f"float64 CPU oracle generating streams 0..{streams - 1} of the {wl.batch}-stream workload "
-                      f"for steps {calib}..{calib + steps - 1} of {wl.n_steps} (per-step cost is constant), "
-                      f"OpenMP over streams, {dt:.1f} s wall"}
+    ran = st.t - t_before
+    assert ran == steps == u.shape[1], (ran, steps, u.shape)
+    return {"value": streams * ran / dt, "unit": "samples/s", "cores": min(threads, streams),
+            "kind": "oracle", "streams": streams, "steps_run": ran, "seconds": dt,
+            "sample": f"{_oracle_build_note()} generating streams 0..{streams - 1} of the {wl.batch}-stream "
+                      f"workload for steps {calib}..{calib + ran - 1} of {wl.n_steps} (per-step cost does not "
+                      f"depend on t), OpenMP over streams, {streams} x {ran} samples in {dt:.1f} s wall"}
 
 
-def cpu_baseline_tf(wl, weights, x, target_seconds: float):
-    """The oracle's teacher-forced pass on a bounded sample: the first streams (one per thread) for
-    as many leading steps as fit the time budget."""
+def cpu_baseline_tf(wl, weights, target_seconds: float):
+    """The oracle's teacher-forced pass on a bounded sample: the first streams (one per thread) over
+    as many leading steps of the workload's seeded sequence as fit the time budget."""
     import oracle
+    import workloads as W
     threads = oracle.max_threads()
     streams = max(1, min(wl.batch, threads))
     o = oracle.Oracle(weights)
     calib = 8
     t0 = time.perf_counter()
-    o.teacher_forced(x[:streams, :calib].copy())
+    o.teacher_forced(W.sequences(wl.uniform_seed, streams, calib))
     per_step = (time.perf_counter() - t0) / calib
-    steps = int(max(16, min(x.shape[1], target_seconds / max(per_step, 1e-9))))
+    steps = int(max(16, min(wl.n_steps, target_seconds / max(per_step, 1e-9))))
+    x = W.sequences(wl.uniform_seed, streams, steps)
     t0 = time.perf_counter()
-    o.teacher_forced(x[:streams, :steps].copy())
+    lg = o.teacher_forced(x)
     dt = time.perf_counter() - t0
+    assert lg.shape[:2] == (streams, steps), lg.shape
     return {"value": streams * steps / dt, "unit": "samples/s", "cores": min(threads, streams),
-            "kind": "oracle",
-            "sample": f"float64 CPU oracle teacher-forcing streams 0..{streams - 1} of the {wl.batch}-stream "
-                      f"workload over steps 0..{steps - 1} of {x.shape[1]} (cached form, per-step cost constant), "
-                      f"OpenMP over streams, {dt:.1f} s wall"}
+            "kind": "oracle", "streams": streams, "steps_run": steps, "seconds": dt,
+            "sample": f"{_oracle_build_note()} teacher-forcing streams 0..{streams - 1} of the {wl.batch}-stream "
+                      f"workload over steps 0..{steps - 1} of {wl.n_steps} (cached form, per-step cost constant), "
+                      f"OpenMP over streams, {streams} x {steps} samples in {dt:.1f} s wall"}
 
 
 def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
@@ -205,7 +231,7 @@ def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
         "wall_s": wall,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline_tf(wl, weights, x_host, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline_tf(wl, weights, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
@@ -339,7 +365,7 @@ def main():
     out = torch.empty((B, K), dtype=torch.int32, device="cuda")
 
     if Wu > 0:
-        fw.generate(u_warm)
+        fw.generate(u_warm, check=False)
     torch.cuda.synchronize()
     fw.reset()
     torch.cuda.synchronize()
@@ -348,7 +374,7 @@ def main():
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     e0.record(stream)
-    fw.generate(u_timed, out=out)
+    fw.generate(u_timed, out=out, check=False)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -365,7 +391,8 @@ def main():
     mfma = fw.regime.startswith("mfma")
     bound = "mfma" if mfma else "alu"
     peak = PEAK_TFLOPS[dtype] if mfma else VALU_F32_PEAK_TFLOPS
-    traffic = stored_traffic(name, K)
+    rec = stored_traffic(name)
+    traffic = traffic_for(rec, K)
 
     result = {
         "metric": METRIC,
@@ -394,13 +421,16 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / peak,
             "traffic": traffic,
+            "traffic_gbs": traffic / sec / 1e9 if traffic is not None and sec > 0 else None,
+            "traffic_basis": None if rec is None else
+            f"rocprofv3 FETCH_SIZE + WRITE_SIZE of a {rec['steps']}-step launch (copy-calibrated), per step x {K}",
             "algorithmic_flops_per_launch": flops,
             "launch_ms": ms,
         },
         "wall_s": wall,
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, weights, u_host, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(wl, weights, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 

@@ -5,9 +5,9 @@
  * The library implements cached autoregressive generation through a stack of
  * width-2 dilated causal convolutions, the method of "Fast Wavenet Generation
  * Algorithm" (Paine et al., 2016):
- *   - the generation model is one step of a multi-layer RNN: it maps the current
- *     input and the recurrent states popped from the convolution queues to the
- *     current output and the new recurrent states (Section 2.2, Fig. 4);
+ *   - one generation step behaves like one step of a multi-layer recurrent net:
+ *     (input, states popped from the queues) -> (logits, states to push)
+ *     (Section 2.2, Fig. 4);
  *   - there is one FIFO convolution queue per layer, its depth equal to the
  *     dilation of the layer it feeds (Section 2.1, Fig. 3), initialised with
  *     zeros (Section 2.2);
@@ -139,20 +139,25 @@ int fwg_workspace_size(const fwg_desc *desc, size_t *bytes);
 int fwg_create(const fwg_desc *desc, const fwg_weights *weights, void *workspace, size_t ws_bytes,
                void *hip_stream, fwg_handle **out);
 
-/* Zero every convolution queue, set t = 0 and every stream's next input to
- * seed_input, and unbind the batch size. */
+/* Zero every convolution queue (the queues start empty, i.e. all zeros,
+ * Section 2.2), set t = 0 and every stream's next input to seed_input, and
+ * unbind the batch size. */
 int fwg_reset_queues(fwg_handle *h);
 
 /* Generate n_steps samples for each of `batch` independent streams, continuing
- * from the current state (pop, compute, push per sample; each sample is fed
- * back as the next input).  uniforms: DEVICE float32 [batch][n_steps];
+ * from the current state: per sample the pop phase, the layer computations and
+ * the push phase of Section 2.2 (Fig. 5, Fig. 6), then the sample drawn from the
+ * output distribution becomes the next input (Section 1).  uniforms: DEVICE float32 [batch][n_steps];
  * samples: DEVICE int32 [batch][n_steps], samples[b][s] drawn for time t0+s.
  * The first call after a reset binds the batch size; later calls with another
  * batch return FWG_ESTATE.  n_steps == 0 is a no-op. */
 int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples);
 
 /* Teacher-forced evaluation from zero queues: logits[b][t][:] is the output
- * after consuming inputs[b][0..t].  inputs: DEVICE int32 [batch][seq_len];
+ * after consuming inputs[b][0..t], i.e. the cached step of Section 2.2 with
+ * each step's input given instead of sampled; it equals the dilated causal
+ * convolution evaluated over the whole sequence (the training-time view of
+ * Section 1).  inputs: DEVICE int32 [batch][seq_len];
  * logits: DEVICE float32 [batch][seq_len][n_classes].  Runs the generation
  * step kernels in forced mode (the input of each step taken from `inputs`
  * instead of the previous sample), so the logits check the hot path itself;

@@ -153,6 +153,13 @@ class FastWavenet:
         _check(self.lib.fwg_create(ctypes.byref(self.desc), ctypes.byref(fw), self.workspace.data_ptr(),
                                    self.ws_bytes, self.stream.cuda_stream, ctypes.byref(h)))
         self.handle = h
+        # kernel families whose launches wait on each other's blocks: a wait that ran out leaves
+        # invalid outputs and a sticky device mark, which the calls below check by default
+        self._waits = self.regime.startswith("mfma_split")
+
+    def _after(self, check: bool):
+        if check and self._waits:
+            self.device_status()
 
     @property
     def regime(self) -> str:
@@ -166,36 +173,42 @@ class FastWavenet:
         reset ended without valid results."""
         _check(self.lib.fwg_device_status(self.handle))
 
-    def generate(self, uniforms, out=None):
-        """uniforms: float32 CUDA tensor [batch][n_steps] -> int32 samples [batch][n_steps]."""
+    def generate(self, uniforms, out=None, check: bool = True):
+        """uniforms: float32 CUDA tensor [batch][n_steps] -> int32 samples [batch][n_steps].
+        check: for kernel families with cross-block waits, synchronise and raise FwgError (EDEVICE)
+        if the launch ended without valid results (False: return right after the enqueue)."""
         torch = self._torch
         assert uniforms.dtype == torch.float32 and uniforms.is_cuda and uniforms.is_contiguous()
         B, n = uniforms.shape
         if out is None:
             out = torch.empty((B, n), dtype=torch.int32, device=uniforms.device)
         _check(self.lib.fwg_generate(self.handle, B, n, uniforms.data_ptr(), out.data_ptr()))
+        self._after(check)
         return out
 
-    def teacher_forced(self, inputs, out=None):
-        """inputs: int32 CUDA tensor [batch][T] -> float32 logits [batch][T][n_classes]."""
+    def teacher_forced(self, inputs, out=None, check: bool = True):
+        """inputs: int32 CUDA tensor [batch][T] -> float32 logits [batch][T][n_classes] (check as in
+        generate)."""
         torch = self._torch
         assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
         B, T = inputs.shape
         if out is None:
             out = torch.empty((B, T, self.n_classes), dtype=torch.float32, device=inputs.device)
         _check(self.lib.fwg_teacher_forced(self.handle, B, T, inputs.data_ptr(), out.data_ptr()))
+        self._after(check)
         return out
 
-    def step_forced(self, inputs, out=None):
+    def step_forced(self, inputs, out=None, check: bool = True):
         """Online prediction from the current state.  inputs: int32 CUDA tensor [batch][n_steps] of
         observed samples -> float32 logits [batch][n_steps][n_classes]; logits[b][s] is the
-        distribution predicted for inputs[b][s]."""
+        distribution predicted for inputs[b][s] (check as in generate)."""
         torch = self._torch
         assert inputs.dtype == torch.int32 and inputs.is_cuda and inputs.is_contiguous()
         B, n = inputs.shape
         if out is None:
             out = torch.empty((B, n, self.n_classes), dtype=torch.float32, device=inputs.device)
         _check(self.lib.fwg_step_forced(self.handle, B, n, inputs.data_ptr(), out.data_ptr()))
+        self._after(check)
         return out
 
     def generate_naive(self, uniforms, out=None):

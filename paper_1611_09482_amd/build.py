@@ -15,7 +15,8 @@ SOURCES = [os.path.join(CSRC, "fwg_host.cpp"), os.path.join(CSRC, "fwg_kernels.h
            os.path.join(CSRC, "fwg_wave.hip"), os.path.join(CSRC, "fwg_split.hip")]
 HEADERS = [os.path.join(ROOT, "include", "fwg.h"), os.path.join(CSRC, "fwg_internal.h"),
            os.path.join(CSRC, "fwg_sample.h"), os.path.join(CSRC, "fwg_valu.h"),
-           os.path.join(CSRC, "fwg_wave.h"), os.path.join(CSRC, "fwg_par.h"), os.path.join(CSRC, "fwg_mfma_dev.h")]
+           os.path.join(CSRC, "fwg_wave.h"), os.path.join(CSRC, "fwg_par.h"), os.path.join(CSRC, "fwg_mfma_dev.h"),
+           os.path.join(CSRC, "fwg_bf16.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -20,28 +20,13 @@
 
 #include <type_traits>
 
+#include "fwg_bf16.h"
 #include "fwg_internal.h"
 #include "fwg_valu.h"
 #include "fwg_sample.h"
 
 
 namespace fwg {
-
-// ---------------------------------------------------------------------------
-// bf16 helpers (operands are bf16 bit patterns in uint16 storage)
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
-// round to the nearest bf16 value (ties to even), returned as float
-__device__ __forceinline__ float round_bf16(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return __uint_as_float(u & 0xffff0000u);
-}
-__device__ __forceinline__ uint16_t to_bf16_bits(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -84,7 +69,7 @@ template <> struct WTraits<uint16_t> {
   __device__ static __forceinline__ float load1(const void *p, long long i) {
     return __uint_as_float(((uint32_t)((const uint16_t *)p)[i]) << 16);
   }
-  __device__ static __forceinline__ void store1(void *p, long long i, float v) { ((uint16_t *)p)[i] = to_bf16_bits(v); }
+  __device__ static __forceinline__ void store1(void *p, long long i, float v) { ((uint16_t *)p)[i] = bf16_bits(v); }
   __device__ static __forceinline__ float opnd(float x) { return round_bf16(x); }
 };
 

@@ -33,6 +33,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fwg_bf16.h"
 #include "fwg_internal.h"
 #include "fwg_par.h"
 #include "fwg_sample.h"
@@ -46,17 +47,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int NT = 256;
 constexpr int KT_BYTES = 128;            // bytes of one row inside a k-tile
 constexpr int ROWB = KT_BYTES + 16;      // LDS row stride (padding spreads the rows over banks)
-
-__device__ __forceinline__ float round_bf16(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return __uint_as_float(u & 0xffff0000u);
-}
-__device__ __forceinline__ uint16_t bf16_bits(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 // Operand types: float (f32 models) or uint16_t (bf16 bit patterns).
 template <typename OT> struct Op;

@@ -15,23 +15,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "fwg_bf16.h"
 #include "fwg_internal.h"
 #include "fwg_wave.h"
 #include "fwg_sample.h"
 
 namespace fwg {
 namespace wv {
-
-__device__ __forceinline__ float round_bf16(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return __uint_as_float(u & 0xffff0000u);
-}
-__device__ __forceinline__ uint16_t bf16_bits(float x) {
-  uint32_t u = __float_as_uint(x);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
 
 // Orders this wave's LDS writes before its later reads by other lanes: LDS instructions of one wave
 // execute in order, so only the compiler has to be kept from moving accesses across this point.

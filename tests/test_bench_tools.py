@@ -44,11 +44,28 @@ def test_record_traffic(tmp_path):
 
 def test_stored_traffic_matches_sources():
     """The committed traffic record of the benchmark workload is reported only while it was taken on
-    the current step-kernel sources; it is the one bench.py reports."""
+    the current step-kernel sources, and scales per step to any launch length."""
     rec = json.load(open(os.path.join(bench.ROOT, "profiles", "traffic_gated_r64_s512_l30_b256_bf16.json")))
-    v = bench.stored_traffic("gated_r64_s512_l30_b256_bf16", rec["steps"])
+    v = bench.stored_traffic("gated_r64_s512_l30_b256_bf16")
     if rec["kernel_digest"] == bench.kernel_source_digest():
-        assert v == rec["hbm_bytes_per_launch"]
+        assert v == rec
+        assert bench.traffic_for(v, rec["steps"]) == rec["hbm_bytes_per_launch"]
+        assert abs(bench.traffic_for(v, 20) - rec["hbm_bytes_per_launch"] * 20 / rec["steps"]) < 1.0
     else:
-        assert v is None
-    assert bench.stored_traffic("gated_r64_s512_l30_b256_bf16", rec["steps"] + 1) is None
+        assert v is None and bench.traffic_for(v, 20) is None
+
+
+def test_cpu_baseline_counts_the_steps_it_runs():
+    """The CPU baseline draws its own uniforms and divides by exactly the steps the oracle ran,
+    whatever the GPU run's length (a 20-step GPU run once made it divide 16 steps' time by 7,996)."""
+    import workloads as W
+    wl = W.WORKLOADS["toy_relu_c32_l5_b1"]
+    w = W.make_weights(wl.model, wl.weight_seed)
+    for budget in (0.0, 0.05):
+        r = bench.cpu_baseline(wl, w, budget)
+        assert r["steps_run"] >= 8 and r["steps_run"] <= wl.n_steps - 4
+        assert abs(r["value"] - r["streams"] * r["steps_run"] / r["seconds"]) <= 1e-9 * r["value"]
+        assert f"{r['streams']} x {r['steps_run']} samples" in r["sample"]
+    r = bench.cpu_baseline_tf(wl, w, 0.0)
+    assert r["steps_run"] == 16
+    assert abs(r["value"] - r["streams"] * 16 / r["seconds"]) <= 1e-9 * r["value"]
