@@ -15,7 +15,8 @@ _STATUS = {FWG_EINVAL: "EINVAL", FWG_ENOSPACE: "ENOSPACE", FWG_EHIP: "EHIP", FWG
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libfwg.so")
 
-EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
+EXPORTED = ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_generate_noalloc",
+            "fwg_teacher_forced",
             "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive", "fwg_naive_nodes",
             "fwg_destroy", "fwg_last_error", "fwg_regime", "fwg_device_status"]
 
@@ -61,6 +62,7 @@ def load_library(path: Optional[str] = None):
                              ctypes.POINTER(vp)]
     L.fwg_reset_queues.argtypes = [vp]
     L.fwg_generate.argtypes = [vp, i32, i32, vp, vp]
+    L.fwg_generate_noalloc.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_teacher_forced.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_step_forced.argtypes = [vp, i32, i32, vp, vp]
     L.fwg_teacher_forced_parallel.argtypes = [vp, i32, i32, vp, vp]
@@ -72,7 +74,8 @@ def load_library(path: Optional[str] = None):
     L.fwg_regime.argtypes = [vp]
     L.fwg_regime.restype = ctypes.c_char_p
     L.fwg_device_status.argtypes = [vp]
-    for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_teacher_forced",
+    for name in ["fwg_workspace_size", "fwg_create", "fwg_reset_queues", "fwg_generate", "fwg_generate_noalloc",
+                 "fwg_teacher_forced",
                  "fwg_step_forced", "fwg_teacher_forced_parallel", "fwg_prime", "fwg_generate_naive",
                  "fwg_naive_nodes", "fwg_destroy", "fwg_device_status"]:
         getattr(L, name).restype = ctypes.c_int
@@ -183,6 +186,17 @@ class FastWavenet:
         if out is None:
             out = torch.empty((B, n), dtype=torch.int32, device=uniforms.device)
         _check(self.lib.fwg_generate(self.handle, B, n, uniforms.data_ptr(), out.data_ptr()))
+        self._after(check)
+        return out
+
+    def generate_noalloc(self, uniforms, out, check: bool = True):
+        """fwg_generate_noalloc: generate() for callers that cannot allocate (the split family's
+        exchange words in the library's static device array); `out` is required."""
+        torch = self._torch
+        assert uniforms.dtype == torch.float32 and uniforms.is_cuda and uniforms.is_contiguous()
+        B, n = uniforms.shape
+        assert out.dtype == torch.int32 and out.is_cuda and out.is_contiguous() and tuple(out.shape) == (B, n)
+        _check(self.lib.fwg_generate_noalloc(self.handle, B, n, uniforms.data_ptr(), out.data_ptr()))
         self._after(check)
         return out
 

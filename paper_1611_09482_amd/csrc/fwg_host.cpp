@@ -390,6 +390,7 @@ struct fwg_handle {
   int bound_batch;  // -1: not bound since the last reset
   long long nv_t;   // naive generator: its own time and batch binding (its state is the input history)
   int nv_bound_batch;
+  void *static_scratch;  // split family: this device's static exchange-word array (fwg_generate_noalloc)
 };
 
 namespace {
@@ -529,15 +530,16 @@ int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const 
   return FWG_OK;
 }
 
-// One step-kernel launch of the handle's kernel family.
-hipError_t launch_step(const fwg_handle *h, const StepArgs &a) {
+// One step-kernel launch of the handle's kernel family.  comm: where the split family's exchange
+// words go (NULL: the workspace's region).
+hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = nullptr) {
   const Plan &p = h->plan;
   switch (p.regime) {
     case REGIME_MFMA: return launch_mfma_step(a, h->stream);
     case REGIME_SPLIT: {
       StepArgs b = a;
       b.sp_nb = (a.batch + kMfRows - 1) / kMfRows;
-      b.sp_comm = h->ws + p.off_comm;
+      b.sp_comm = comm ? comm : h->ws + p.off_comm;
       b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
       // tags restart at 1 every launch: clear the exchange words first (a fill kernel, no memset node)
       hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
@@ -811,6 +813,8 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     if (!coresident) h->plan.regime = REGIME_MFMA;  // same workspace layout
   }
   if (h->plan.regime == REGIME_SPLIT) {
+    // set-up of fwg_generate_noalloc: this device's static exchange-word array, looked up once
+    TRY_OR_FREE(split_static_scratch(&h->static_scratch));
     char *frags = ws + p.off_frags;
     for (int l = 0; l < p.L; ++l)
       TRY_OR_FREE(launch_split_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));
@@ -851,13 +855,24 @@ int fwg_reset_queues(fwg_handle *h) {
   return enqueue_reset(h);
 }
 
-int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples) {
+namespace {
+int generate_impl(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples,
+                  bool noalloc) {
   if (!h) return fail(FWG_EINVAL, "handle is NULL");
   const Plan &p = h->plan;
   if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
   if (n_steps < 0) return fail(FWG_EINVAL, "n_steps < 0");
   if (h->bound_batch >= 0 && h->bound_batch != batch)
     return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
+  void *comm = nullptr;
+  if (noalloc && p.regime == REGIME_SPLIT) {
+    const size_t need = split_comm_bytes(p.L, (batch + kMfRows - 1) / kMfRows);
+    if (need > kStaticScratchBytes)
+      return fail(FWG_ENOSPACE, "the exchange words of %d streams x %d layers need %zu bytes; the static scratch "
+                  "array holds %zu", batch, p.L, need, kStaticScratchBytes);
+    if (!h->static_scratch) return fail(FWG_ESTATE, "no static scratch address was set up for this handle");
+    comm = h->static_scratch;
+  }
   if (n_steps == 0) return FWG_OK;
   if (!uniforms || !samples) return fail(FWG_EINVAL, "uniforms and samples are required");
   StepArgs a = base_args(h);
@@ -868,10 +883,19 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
   a.n_steps = n_steps;
   a.batch = batch;
   a.mode = MODE_GENERATE;
-  HIP_TRY(launch_step(h, a));
+  HIP_TRY(launch_step(h, a, comm));
   h->bound_batch = batch;
   h->t += n_steps;
   return FWG_OK;
+}
+}  // namespace
+
+int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples) {
+  return generate_impl(h, batch, n_steps, uniforms, samples, false);
+}
+
+int fwg_generate_noalloc(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples) {
+  return generate_impl(h, batch, n_steps, uniforms, samples, true);
 }
 
 int fwg_teacher_forced(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits) {

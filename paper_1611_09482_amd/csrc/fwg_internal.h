@@ -97,6 +97,12 @@ hipError_t launch_split_step(const StepArgs &a, hipStream_t s);
 hipError_t launch_split_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
                                      hipStream_t s);
 hipError_t launch_split_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s);
+// Allocation-free generation: the split family's per-launch exchange words in a static device array
+// of this many bytes (one per device, held until the process ends) instead of the workspace.
+constexpr size_t kStaticScratchBytes = (size_t)4 << 20;
+// Device address of that array on the current device (looked up once per device; never the host-side
+// name of the array, which is not a device address).
+hipError_t split_static_scratch(void **ptr);
 
 // Utility and MFMA-family launchers (fwg_kernels.hip, fwg_mfma.hip).
 hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K, int N, int C, hipStream_t s);

@@ -45,6 +45,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "fwg_internal.h"
 #include "fwg_mfma_dev.h"
 
@@ -863,6 +865,29 @@ __global__ void repack_head_kernel(const uint16_t *head, const uint16_t *out, in
 }
 
 }  // namespace sp
+
+// Exchange words of fwg_generate_noalloc (callers that cannot allocate): every launch of that entry
+// point on a device uses this device's copy, so such launches that overlap on one device race.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+hipError_t split_static_scratch(void **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 size_t split_frag_bytes(int L) { return sp::frag_count(L) * 1024; }
 

@@ -92,6 +92,7 @@ def test_null_arguments(lib):
     assert lib.fwg_create(ctypes.byref(d), ctypes.byref(w), 1 << 20, 1 << 40, None, None) == B.FWG_EINVAL
     assert lib.fwg_reset_queues(None) == B.FWG_EINVAL
     assert lib.fwg_generate(None, 1, 1, None, None) == B.FWG_EINVAL
+    assert lib.fwg_generate_noalloc(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_teacher_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_step_forced(None, 1, 1, None, None) == B.FWG_EINVAL
     assert lib.fwg_generate_naive(None, 1, 1, None, None) == B.FWG_EINVAL
