@@ -17,6 +17,7 @@
 #include "fwg_par.h"
 #include "fwg_valu.h"
 #include "fwg_wave.h"
+#include "fwg_chain.h"
 
 using namespace fwg;
 
@@ -73,6 +74,9 @@ struct Plan {
   // wave-per-stream family: the weight image
   WaveArgs wave;
   size_t off_wave;
+  // chain family: the weight image and the launch's LDS bytes
+  ChainArgs chain;
+  size_t off_chain, chain_lds;
 };
 
 // Layout of the wave family's weight image and per-wave scratch; false when the model does not fit
@@ -251,6 +255,12 @@ int make_plan(const fwg_desc *d, Plan *p) {
   const bool split_shape = mfma_shape && split_layers_ok(p->L);
   if (mfma_shape && !(force && strcmp(force, "valu") == 0))
     p->regime = split_shape && !(force && strcmp(force, "mfma") == 0) ? REGIME_SPLIT : REGIME_MFMA;
+  // small float32 ReLU stacks: one block per stream with the layer chain on one wavefront (chain
+  // family; FWG_REGIME=wave keeps the wave-per-stream kernel)
+  const bool forced_other = force && (strcmp(force, "valu") == 0 || strcmp(force, "wave") == 0);
+  if (p->regime == REGIME_VALU && !forced_other &&
+      chain_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, d->dilations, &p->chain, &p->chain_lds))
+    p->regime = REGIME_CHAIN;
   // small models whose weights all fit in LDS: one wavefront per stream
   if (p->regime == REGIME_VALU && !(force && strcmp(force, "valu") == 0) && wave_layout(*p, &p->wave))
     p->regime = REGIME_WAVE;
@@ -318,6 +328,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_ring_tf = take((size_t)acc * p->es);
   p->off_last = take(sizeof(int32_t) * p->bmax);
   p->off_wave = p->regime == REGIME_WAVE ? take(sizeof(float) * (size_t)p->wave.image_floats) : 0;
+  p->off_chain = p->regime == REGIME_CHAIN ? take(sizeof(float) * (size_t)p->chain.image_floats) : 0;
 
   // time-parallel path: every product's K must fill whole 128-byte k-tiles, and the gate's column
   // pairs come in groups of 16 channels
@@ -546,6 +557,11 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
       if (e != hipSuccess) return e;
       return launch_split_step(b, h->stream);
     }
+    case REGIME_CHAIN: {
+      ChainArgs g = p.chain;
+      g.image = (const float *)(h->ws + p.off_chain);
+      return launch_chain_step(a, g, p.chain_lds, h->stream);
+    }
     case REGIME_WAVE: {
       WaveArgs g = p.wave;
       g.image = (const float *)(h->ws + p.off_wave);
@@ -759,6 +775,11 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   TRY_OR_FREE(launch_repack(w->out, ws + p.off_out, REPACK_LINEAR, dt, Kout, p.Q, C, s));
   TRY_OR_FREE(launch_copy_bias(w->out_b, (float *)(ws + p.off_out_b), p.Q, s));
   TRY_OR_FREE(hipMemcpyAsync(ws + p.off_layers, table.data(), sizeof(LayerDev) * p.L, hipMemcpyHostToDevice, s));
+  if (p.regime == REGIME_CHAIN) {
+    TRY_OR_FREE(launch_chain_image(w->embed, w->embed_b, w->conv, w->conv_b, w->out, w->out_b, p.L, p.chain,
+                                   (float *)(ws + p.off_chain), s));
+    TRY_OR_FREE(set_chain_lds_limit(p.chain_lds));
+  }
   if (p.regime == REGIME_WAVE) {
     const WaveArgs &g = p.wave;
     float *img = (float *)(ws + p.off_wave);
@@ -1029,6 +1050,7 @@ const char *fwg_regime(const fwg_handle *h) {
     case REGIME_MFMA: return "mfma_bf16_r64_s512";
     case REGIME_SPLIT: return "mfma_split_bf16_r64_s512";
     case REGIME_WAVE: return "wave";
+    case REGIME_CHAIN: return "chain_f32_c32";
     default: return "valu";
   }
 }

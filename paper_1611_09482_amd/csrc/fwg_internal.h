@@ -69,7 +69,7 @@ enum StepMode {
 __host__ __device__ inline int forced_shift(int mode) { return mode == MODE_TEACHER ? 1 : 0; }
 
 // Kernel families.
-enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3 };
+enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3, REGIME_CHAIN = 4 };
 
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
 // 16 streams per block of 8 waves, weight fragments per wave and stage.

@@ -124,11 +124,18 @@ FAMILIES = {
     "gated_r16_s32_f32": W.ModelConfig(W.GATED, W.F32, 16, (1, 2, 4, 8, 16, 32), 32, 32),
     "relu_c32_bf16": W.ModelConfig(W.RELU, W.BF16, 32, (1, 2, 4, 8, 16, 3)),
     "relu_c32_f32_valu": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
+    "relu_c32_f32_wave": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
+    # float32 ReLU + residual, C = 32: the chain kernel (one block per stream, weights and queues in LDS)
+    "relures_c32_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 32, (1, 2, 4, 8, 16, 3, 1)),
 }
 # families that must run on the wave-per-stream kernels
-WAVE_FAMILIES = {"relu_c32_f32", "relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16"}
+WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_c32_f32_wave"}
+# families that must run on the chain kernels (float32 ReLU stacks with C = 32, width 2)
+CHAIN_FAMILIES = {"relu_c32_f32", "relures_c32_f32"}
 # families whose test forces the general (VALU) kernel family instead of the MFMA or wave one
 FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu"}
+# families whose test forces the wave-per-stream family instead of the chain one
+FORCE_WAVE = {"relu_c32_f32_wave"}
 
 
 def tf(fw, x, path):
@@ -146,6 +153,8 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
     env = {}
     if fam in FORCE_VALU:
         env["FWG_REGIME"] = "valu"
+    if fam in FORCE_WAVE:
+        env["FWG_REGIME"] = "wave"
     if par_rows is not None:
         env["FWG_PAR_ROWS"] = str(par_rows)
     if valu_stage is not None:
@@ -166,9 +175,11 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
             split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
             assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
-            assert fw.regime in ("valu", "wave"), (fam, fw.regime)
+            assert fw.regime in ("valu", "wave", "chain_f32_c32"), (fam, fw.regime)
         if fam in WAVE_FAMILIES:
             assert fw.regime == "wave", (fam, fw.regime)
+        if fam in CHAIN_FAMILIES:
+            assert fw.regime == "chain_f32_c32", (fam, fw.regime)
     return w, fw, oracle.Oracle(w)
 
 
@@ -449,7 +460,8 @@ def test_delay_line_closed_form_gpu(fwidth, dil, path):
 
 @pytest.mark.parametrize("fam,B,regime", [("gated_r64_bf16", 16, "mfma_bf16_r64_s512"),
                                           ("gated_r64_bf16_split", 13, "mfma_split_bf16_r64_s512"),
-                                          ("gated_r32_f32", 5, None)])
+                                          ("gated_r32_f32", 5, None),
+                                          ("relu_c32_f32", 3, "chain_f32_c32")])
 def test_uniform_logits_sampler_gpu(fam, B, regime):
     """All-equal logits: the sample is floor(256 u), bit-exact, in both halves of the MFMA
     kernels' two-rows-per-wave sampler (rows w and w + 8) and with a ragged last block."""
@@ -471,7 +483,8 @@ def test_uniform_logits_sampler_gpu(fam, B, regime):
         fw.device_status()
 
 
-@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split"])
+@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split",
+                                 "relu_c32_f32", "relures_c32_f32"])
 def test_continuation_reset_and_determinism_gpu(fam):
     cfg = FAMILIES[fam]
     w, fw, _ = build_pair(cfg, 7, 9, fam=fam)
