@@ -6,7 +6,8 @@
 
 namespace fwg {
 
-constexpr int kChainC = 32;  // channels the chain kernel is built for
+constexpr int kChainC = 32;         // channels the chain kernel is built for
+constexpr int kChainMaxLayers = 6;  // layers whose weights its waves hold in registers
 
 // The weight image (offsets in floats): embedding [Q][C] and bias, per layer W_r^T [C][C], W_e^T
 // [C][C] and bias, output 1x1 transposed [C][Q] and bias.

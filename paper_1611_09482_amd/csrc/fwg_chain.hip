@@ -1,14 +1,16 @@
-// Chain step kernel for small float32 ReLU stacks (channels C = 32, filter width 2): one block per
-// stream, every weight and every queue of the stream in LDS for the whole launch.
+// Chain step kernel for small float32 ReLU stacks (channels C = 32, filter width 2, at most six
+// layers): one block per stream, every weight and every queue of the stream in LDS for the whole
+// launch, each wave's half of the dilated products in its registers.
 //
 // A sample's work is a chain of dependent steps (the layers in order, then the output 1x1 and the
 // sample, which is the next input: Section 1, Section 2.2); at one stream nothing else can run beside
 // it, so the kernel shortens that chain instead of widening it:
-//  - wave 0 (the chain) keeps the layer input in lanes 0..31 (lane o holds channel o) and computes
-//    each output o in lane o: the input values reach every lane as scalars read from their lanes
-//    (v_readlane), the weights W_e^T[k][o] come from LDS (consecutive lanes, consecutive words);
-//    the output 1x1 gives lane l the classes 4l..4l+3, and the sampler reduces them with DPP row
-//    moves and lane reads;
+//  - wave 0 (the chain) holds the layer input as lane o -> channel o % 32 and computes output o in
+//    lanes o and o + 32, each over half of K: the lane's 16 weights stay in its registers for the
+//    launch, the 16 inputs of its half are read back from the queue row it has just pushed (one
+//    LDS broadcast per half-wave), and the halves' partial sums meet with one cross-half lane
+//    swap; the output 1x1 gives lane l the classes 4l..4l+3, and the sampler reduces them with DPP
+//    row moves and lane reads;
 //  - wave 1 computes W_r v + b of every layer for the next step (v = the state popped from the
 //    layer's queue: pushed d_l >= 1 steps earlier, so known before that step starts; for d_l = 1 it
 //    waits for the chain's push of this step through an LDS flag) and stages the per-step uniforms
@@ -25,6 +27,8 @@ namespace fwg {
 namespace ch {
 
 constexpr int C = kChainC, Q = 256;
+constexpr int LR = kChainMaxLayers;  // layers whose weights the waves hold in registers
+static_assert(LR <= 8, "the per-layer flags fit the 8 words before the broadcast row");
 constexpr int NT = 128;      // wave 0: the chain; wave 1: recurrent halves and staging
 constexpr int KCH = 64;      // steps per chunk of staged uniforms / forced inputs
 constexpr int SPIN_MAX = 1 << 24;
@@ -35,6 +39,29 @@ __device__ __forceinline__ float dpp(float v) {
 }
 __device__ __forceinline__ float lane_f(float v, int l) {
   return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// v of lane i plus v of lane i ^ 32, in every lane (the two half-waves' partial sums of one dot product).
+__device__ __forceinline__ float halves_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, v), __builtin_bit_cast(unsigned, v),
+                                                 false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+// Dot product of a register row (this lane's half: 16 weights) with 16 values read from LDS as a
+// broadcast within the half-wave (v points at the half's first value), two accumulation chains.
+__device__ __forceinline__ float half_dot(const float (&w)[C / 2], const float *v) {
+  const float4 *v4 = (const float4 *)v;
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < C / 8; ++i) {
+    const float4 x = v4[i];
+    a0 = fmaf(w[4 * i], x.x, a0);
+    a1 = fmaf(w[4 * i + 1], x.y, a1);
+    a0 = fmaf(w[4 * i + 2], x.z, a0);
+    a1 = fmaf(w[4 * i + 3], x.w, a1);
+  }
+  return a0 + a1;
 }
 
 // Inverse-CDF sample of one row of 256 logits held 4 per lane (lane l: classes 4l..4l+3): max, exp,
@@ -72,16 +99,15 @@ __device__ __forceinline__ int sample_row(float4 lg, float u, int lane) {
   return 4 * src + __builtin_amdgcn_readlane(first, src);
 }
 
-// The queue slot of layer l at time t, and byte offsets into the LDS image.
+// LDS areas of a launch (offsets from the ChainArgs layout, in floats).
 struct Lay {
-  const float *img;   // LDS image (ChainArgs offsets, in floats)
-  float *ring;        // LDS queues: layer l at ring + qoff[l] floats, [slot][C]
-  float *pbuf;        // [2][L][C]: W_r v + b of every layer, by step parity
-  int *qoff, *dil, *slot;  // per layer: float offset of the queue, dilation, slot at the current step
-  volatile int *flag;      // per layer: step index + 1 once the chain pushed this step's input
+  const float *img;   // the weight image
+  float *ring;        // queues: layer l at ring + qoff[l], [slot][C]
+  float *pbuf;        // [2][LR][C]: W_r v + b of every layer, by step parity
+  volatile int *flag; // per layer: step index + 1 once the chain pushed this step's input
+  float *xrow;        // [C] the last layer's output, broadcast to the output 1x1
   float *u;           // [2][KCH] staged uniforms (generation)
   int *fin;           // [2][KCH] staged forced next inputs
-  float *lgs;         // [Q] logits of the step (forced modes, for the store)
 };
 
 __global__ void __launch_bounds__(NT) chain_step_kernel(StepArgs a, ChainArgs g) {
@@ -93,37 +119,37 @@ __global__ void __launch_bounds__(NT) chain_step_kernel(StepArgs a, ChainArgs g)
   s.img = lds;
   s.ring = lds + g.image_floats;
   s.pbuf = s.ring + g.ring_floats;
-  s.u = s.pbuf + 2 * L * C;
+  s.u = s.pbuf + 2 * LR * C;
   s.fin = (int *)(s.u + 2 * KCH);
-  s.qoff = s.fin + 2 * KCH;
-  s.dil = s.qoff + L;
-  s.slot = s.dil + L;
-  s.flag = s.slot + L;
-  int *cur_in = (int *)(s.flag + L);
-  s.lgs = (float *)(cur_in + 4);
+  s.flag = (volatile int *)(s.fin + 2 * KCH);
+  s.xrow = (float *)(s.fin + 2 * KCH + 8);  // 16-byte aligned after the flags
 
-  // ---- launch: image, queues of this stream, per-layer tables, first input
-  for (int i = tid; i < g.image_floats / 4; i += NT) lds4[i] = ((const float4 *)g.image)[i];
+  // per-layer queue offsets, dilations and slots, in wave-uniform registers
+  int qoff[LR], dil[LR], slot[LR];
   {
     int off = 0;
-    for (int l = 0; l < L; ++l) {
-      const int d = a.layers[l].dil;
-      if (tid == 0) {
-        s.qoff[l] = off;
-        s.dil[l] = d;
-        s.slot[l] = (int)(a.t0 % (long long)d);
-        s.flag[l] = 0;
-      }
-      const float *src = (const float *)a.ring + a.layers[l].ring_off;
-      for (int i = tid; i < d * C; i += NT) {
-        const int sl = i / C, ch = i % C;
-        s.ring[off + i] = src[((long long)sl * a.bmax + b) * C + ch];
-      }
-      off += d * C;
+#pragma unroll
+    for (int l = 0; l < LR; ++l) {
+      const int d = l < L ? a.layers[l].dil : 1;
+      qoff[l] = off;
+      dil[l] = d;
+      slot[l] = (int)(a.t0 % (long long)d);
+      off += l < L ? d * C : 0;
     }
   }
-  if (tid == 0) cur_in[0] = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
-  // stage chunk 0
+  // ---- launch: image, queues of this stream, flags, first chunk of per-step inputs
+  for (int i = tid; i < g.image_floats / 4; i += NT) lds4[i] = ((const float4 *)g.image)[i];
+#pragma unroll
+  for (int l = 0; l < LR; ++l) {
+    if (l < L) {
+      const float *src = (const float *)a.ring + a.layers[l].ring_off;
+      for (int i = tid; i < dil[l] * C; i += NT) {
+        const int sl = i / C, ch = i % C;
+        s.ring[qoff[l] + i] = src[((long long)sl * a.bmax + b) * C + ch];
+      }
+    }
+  }
+  if (tid < LR) s.flag[tid] = 0;
   for (int j = tid; j < KCH; j += NT) {
     if (a.mode == MODE_GENERATE) s.u[j] = j < a.n_steps ? a.uniforms[(long long)b * a.n_steps + j] : 0.f;
     else {
@@ -133,82 +159,48 @@ __global__ void __launch_bounds__(NT) chain_step_kernel(StepArgs a, ChainArgs g)
   }
   __syncthreads();
 
-  const float *embT = s.img + g.o_emb;    // [Q][C]
-  const float *embb = s.img + g.o_embb;   // [C]
-  const float *woT = s.img + g.o_out;     // [C][Q]
-  const float *wob = s.img + g.o_outb;    // [Q]
   const int o = lane & (C - 1);
   const bool residual = a.kind == 1;  // relu + residual (FWG_RELU_RESIDUAL)
+  // this wave's half of every layer's dilated product, in registers for the launch: lanes o and
+  // o + 32 hold row o over K halves 0 and 1 (wave 0: W_e, the current-input tap; wave 1: W_r, the
+  // popped tap)
+  const int h = lane >> 5;
+  float wt[LR][C / 2];
+#pragma unroll
+  for (int l = 0; l < LR; ++l)
+#pragma unroll
+    for (int j = 0; j < C / 2; ++j)
+      wt[l][j] = l < L ? s.img[g.o_layer + l * g.layer_floats + (1 - wave) * C * C + (16 * h + j) * C + o] : 0.f;
 
   if (wave == 1) {
-    // W_r v + b of every layer for step 0 (pops of step 0: all pushed before the launch)
-    for (int l = 0; l < L; ++l) {
-      const float *wrT = s.img + g.o_layer + l * g.layer_floats;  // W_r^T [C][C], then W_e^T, then b
-      const float *v = s.ring + s.qoff[l] + s.slot[l] * C;
-      float acc = wrT[2 * C * C + o];
-      for (int k = 0; k < C; ++k) acc = fmaf(wrT[k * C + o], v[k], acc);
-      if (lane < C) s.pbuf[l * C + o] = acc;
+    // ---- W_r v + b of every layer for step 0 (its pops were all pushed before the launch)
+#pragma unroll
+    for (int l = 0; l < LR; ++l) {
+      if (l < L) {
+        const float acc = halves_sum(half_dot(wt[l], s.ring + qoff[l] + slot[l] * C + 16 * h)) +
+                          s.img[g.o_layer + l * g.layer_floats + 2 * C * C + o];
+        if (lane < C) s.pbuf[l * C + o] = acc;
+      }
     }
   }
-  __syncthreads();
-
-  for (int step = 0; step < a.n_steps; ++step) {
-    const int par = step & 1;
-    if (wave == 0) {
-      // ---- the chain: embedding, layers, output 1x1, sample
-      const int in = cur_in[0];
-      float x = embT[in * C + o] + embb[o];
-      for (int l = 0; l < L; ++l) {
-        const float *we = s.img + g.o_layer + l * g.layer_floats + C * C;  // W_e^T [C][C]
-        // push: this layer's input replaces the slot the step pops (its value was read for this
-        // step's W_r v one step earlier)
-        if (lane < C) s.ring[s.qoff[l] + s.slot[l] * C + o] = x;
-        if (lane == 0) s.flag[l] = step + 1;
-        float w[C];
-#pragma unroll
-        for (int k = 0; k < C; ++k) w[k] = we[k * C + o];
-        float acc = s.pbuf[(par * L + l) * C + o];
-#pragma unroll
-        for (int k = 0; k < C; ++k) acc = fmaf(w[k], lane_f(x, k), acc);
-        const float r = fmaxf(acc, 0.f);
-        x = residual ? x + r : r;
-      }
-      // output 1x1: lane l takes classes 4l..4l+3
-      float4 lg = ((const float4 *)wob)[lane];
-#pragma unroll 8
-      for (int k = 0; k < C; ++k) {
-        const float4 wv = ((const float4 *)(woT + k * Q))[lane];
-        const float xk = lane_f(x, k);
-        lg.x = fmaf(wv.x, xk, lg.x);
-        lg.y = fmaf(wv.y, xk, lg.y);
-        lg.z = fmaf(wv.z, xk, lg.z);
-        lg.w = fmaf(wv.w, xk, lg.w);
-      }
-      int nxt;
-      if (a.mode == MODE_GENERATE) {
-        nxt = sample_row(lg, s.u[(step / KCH & 1) * KCH + step % KCH], lane);
-        if (lane == 0) a.samples[(long long)b * a.n_steps + step] = nxt;
-      } else {
-        if (a.logits) ((float4 *)(a.logits + ((long long)b * a.n_steps + step) * Q))[lane] = lg;
-        nxt = s.fin[(step / KCH & 1) * KCH + step % KCH];
-      }
-      if (lane == 0) cur_in[0] = nxt;
-    } else {
+  __syncthreads();  // step 0's W_r v + b is in LDS
+  if (wave == 1) {
+    for (int step = 0; step < a.n_steps; ++step) {
       // ---- W_r v + b of every layer for the next step, into the other parity
-      const int np = par ^ 1;
-      for (int l = 0; l < L; ++l) {
-        const int d = s.dil[l];
-        const int sl = s.slot[l] + 1 == d ? 0 : s.slot[l] + 1;
-        if (d == 1) {
-          // the state popped next step is this step's input of the layer: wait for the chain's push
-          for (int it = 0; s.flag[l] != step + 1 && it < SPIN_MAX; ++it) __builtin_amdgcn_s_sleep(1);
+      const int np = (step & 1) ^ 1;
+#pragma unroll
+      for (int l = 0; l < LR; ++l) {
+        if (l < L) {
+          const int sl = slot[l] + 1 == dil[l] ? 0 : slot[l] + 1;
+          if (dil[l] == 1) {
+            // the state popped next step is this step's input of the layer: wait for the chain's push
+            for (int it = 0; s.flag[l] != step + 1 && it < SPIN_MAX; ++it) __builtin_amdgcn_s_sleep(1);
+          }
+          const float acc = halves_sum(half_dot(wt[l], s.ring + qoff[l] + sl * C + 16 * h)) +
+                            s.img[g.o_layer + l * g.layer_floats + 2 * C * C + o];
+          if (lane < C) s.pbuf[(np * LR + l) * C + o] = acc;
+          slot[l] = sl;
         }
-        const float *wrT = s.img + g.o_layer + l * g.layer_floats;
-        const float *v = s.ring + s.qoff[l] + sl * C;
-        float acc = wrT[2 * C * C + o];
-#pragma unroll 8
-        for (int k = 0; k < C; ++k) acc = fmaf(wrT[k * C + o], v[k], acc);
-        if (lane < C) s.pbuf[(np * L + l) * C + o] = acc;
       }
       // staging of the next chunk, one chunk ahead
       if (step % KCH == 0) {
@@ -223,24 +215,94 @@ __global__ void __launch_bounds__(NT) chain_step_kernel(StepArgs a, ChainArgs g)
           }
         }
       }
+      __syncthreads();
     }
-    __syncthreads();
-    // slot advance (wave 1 read slot + 1 above; the chain reads the slots during the step)
-    if (tid < L) s.slot[tid] = s.slot[tid] + 1 == s.dil[tid] ? 0 : s.slot[tid] + 1;
-    __syncthreads();
+  } else {
+    // ---- the chain: embedding, layers, output 1x1, sample
+    const float *embT = s.img + g.o_emb;                  // [Q][C]
+    const float *embb = s.img + g.o_embb;                 // [C]
+    const float4 *woT4 = (const float4 *)(s.img + g.o_out);  // [C][Q / 4]
+    const float4 *wob4 = (const float4 *)(s.img + g.o_outb);
+    int in = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
+    for (int step = 0; step < a.n_steps; ++step) {
+      const int par = step & 1;
+      float x = embT[in * C + o] + embb[o];
+      float pv[LR];
+#pragma unroll
+      for (int l = 0; l < LR; ++l) pv[l] = l < L ? s.pbuf[(par * LR + l) * C + o] : 0.f;
+      float4 wo[2][4];
+#pragma unroll
+      for (int l = 0; l < LR; ++l) {
+        if (l < L) {
+          // push: this layer's input replaces the slot the step pops (its value was read for this
+          // step's W_r v one step earlier)
+          if (lane < C) s.ring[qoff[l] + slot[l] * C + o] = x;
+          if (lane == 0) s.flag[l] = step + 1;
+          const int slot_pushed = slot[l];
+          slot[l] = slot[l] + 1 == dil[l] ? 0 : slot[l] + 1;
+          if (l + 1 == L) {
+            // the output 1x1's first weights, read while the last layer computes
+#pragma unroll
+            for (int j = 0; j < 4; ++j) wo[0][j] = woT4[j * (Q / 4) + lane];
+          }
+          // the pushed row read back as this half's 16 inputs (LDS operations of a wave execute in order)
+          const float acc = halves_sum(half_dot(wt[l], s.ring + qoff[l] + slot_pushed * C + 16 * h)) + pv[l];
+          const float r = fmaxf(acc, 0.f);
+          x = residual ? x + r : r;
+        }
+      }
+      // output 1x1: lane l takes classes 4l..4l+3; the last layer's output reaches every lane through
+      // an LDS row, the weights are read four k-steps ahead
+      if (lane < C) s.xrow[o] = x;
+      float xs[C];
+#pragma unroll
+      for (int i = 0; i < C / 4; ++i) {
+        const float4 v = ((const float4 *)s.xrow)[i];
+        xs[4 * i] = v.x;
+        xs[4 * i + 1] = v.y;
+        xs[4 * i + 2] = v.z;
+        xs[4 * i + 3] = v.w;
+      }
+      float4 lg = wob4[lane];
+#pragma unroll
+      for (int kb = 0; kb < C / 4; ++kb) {
+        if (kb + 1 < C / 4) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) wo[(kb + 1) & 1][j] = woT4[((kb + 1) * 4 + j) * (Q / 4) + lane];
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float xk = xs[kb * 4 + j];
+          const float4 wv = wo[kb & 1][j];
+          lg.x = fmaf(wv.x, xk, lg.x);
+          lg.y = fmaf(wv.y, xk, lg.y);
+          lg.z = fmaf(wv.z, xk, lg.z);
+          lg.w = fmaf(wv.w, xk, lg.w);
+        }
+      }
+      if (a.mode == MODE_GENERATE) {
+        in = sample_row(lg, s.u[(step / KCH & 1) * KCH + step % KCH], lane);
+        if (lane == 0) a.samples[(long long)b * a.n_steps + step] = in;
+      } else {
+        if (a.logits) ((float4 *)(a.logits + ((long long)b * a.n_steps + step) * Q))[lane] = lg;
+        in = s.fin[(step / KCH & 1) * KCH + step % KCH];
+      }
+      __syncthreads();
+    }
+    if (tid == 0 && a.mode != MODE_TEACHER) a.last[b] = in;
   }
+  __syncthreads();
 
-  // ---- launch end: queues and the pending input back to the workspace
-  {
-    for (int l = 0; l < L; ++l) {
-      const int d = s.dil[l];
+  // ---- launch end: queues back to the workspace
+#pragma unroll
+  for (int l = 0; l < LR; ++l) {
+    if (l < L) {
       float *dst = (float *)a.ring + a.layers[l].ring_off;
-      for (int i = tid; i < d * C; i += NT) {
+      for (int i = tid; i < dil[l] * C; i += NT) {
         const int sl = i / C, ch = i % C;
-        dst[((long long)sl * a.bmax + b) * C + ch] = s.ring[s.qoff[l] + i];
+        dst[((long long)sl * a.bmax + b) * C + ch] = s.ring[qoff[l] + i];
       }
     }
-    if (tid == 0 && a.mode != MODE_TEACHER) a.last[b] = cur_in[0];
   }
 }
 
@@ -273,7 +335,8 @@ __global__ void chain_vec_kernel(const float *src, float *dst, int n) {
 }  // namespace ch
 
 bool chain_layout(int kind, int dtype, int C, int Q, int L, int w, const int32_t *dil, ChainArgs *g, size_t *lds) {
-  if ((kind != 0 && kind != 1) || dtype != 0 || C != kChainC || Q != 256 || w != 2 || L < 1 || L > 64) return false;
+  if ((kind != 0 && kind != 1) || dtype != 0 || C != kChainC || Q != 256 || w != 2 || L < 1 || L > kChainMaxLayers)
+    return false;
   long long ring = 0;
   for (int l = 0; l < L; ++l) ring += (long long)dil[l] * C;
   g->o_emb = 0;
@@ -284,8 +347,8 @@ bool chain_layout(int kind, int dtype, int C, int Q, int L, int w, const int32_t
   g->o_outb = g->o_out + C * Q;
   g->image_floats = (g->o_outb + Q + 3) & ~3;
   g->ring_floats = (int)((ring + 3) & ~3ll);
-  const long long floats = (long long)g->image_floats + g->ring_floats + 2LL * L * C + 2 * ch::KCH +
-                           2 * ch::KCH + 4LL * L + 4 + Q;
+  const long long floats = (long long)g->image_floats + g->ring_floats + 2LL * kChainMaxLayers * C + 2 * ch::KCH +
+                           2 * ch::KCH + 8 + kChainC;
   *lds = (size_t)floats * 4;
   return ring < (1 << 20) && *lds <= 160 * 1024;
 }

@@ -125,8 +125,8 @@ FAMILIES = {
     "relu_c32_bf16": W.ModelConfig(W.RELU, W.BF16, 32, (1, 2, 4, 8, 16, 3)),
     "relu_c32_f32_valu": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
     "relu_c32_f32_wave": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
-    # float32 ReLU + residual, C = 32: the chain kernel (one block per stream, weights and queues in LDS)
-    "relures_c32_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 32, (1, 2, 4, 8, 16, 3, 1)),
+    # float32 ReLU + residual, C = 32, six layers (the most the chain kernels hold): the chain kernel
+    "relures_c32_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 32, (1, 2, 4, 16, 3, 1)),
 }
 # families that must run on the wave-per-stream kernels
 WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_c32_f32_wave"}
