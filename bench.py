@@ -42,7 +42,7 @@ HBM_PEAK_GBS = 8000.0
 
 
 # sources of the benchmark's step kernel: the kernel file and the structures it reads
-KERNEL_SOURCES = ("fwg_split.hip", "fwg_mfma.hip", "fwg_mfma_dev.h", "fwg_internal.h")
+KERNEL_SOURCES = ("fwg_split.hip", "fwg_mfma.hip", "fwg_mfma_dev.h", "fwg_internal.h", "fwg_xchg.h")
 
 
 def kernel_source_digest() -> str:

@@ -13,11 +13,12 @@ LIB = os.path.join(PKG, "libfwg.so")
 SOURCES = [os.path.join(CSRC, "fwg_host.cpp"), os.path.join(CSRC, "fwg_kernels.hip"),
            os.path.join(CSRC, "fwg_mfma.hip"), os.path.join(CSRC, "fwg_parallel.hip"),
            os.path.join(CSRC, "fwg_wave.hip"), os.path.join(CSRC, "fwg_split.hip"),
-           os.path.join(CSRC, "fwg_chain.hip")]
+           os.path.join(CSRC, "fwg_chain.hip"), os.path.join(CSRC, "fwg_wide.hip")]
 HEADERS = [os.path.join(ROOT, "include", "fwg.h"), os.path.join(CSRC, "fwg_internal.h"),
            os.path.join(CSRC, "fwg_sample.h"), os.path.join(CSRC, "fwg_valu.h"),
            os.path.join(CSRC, "fwg_wave.h"), os.path.join(CSRC, "fwg_par.h"), os.path.join(CSRC, "fwg_mfma_dev.h"),
-           os.path.join(CSRC, "fwg_bf16.h"), os.path.join(CSRC, "fwg_chain.h")]
+           os.path.join(CSRC, "fwg_bf16.h"), os.path.join(CSRC, "fwg_chain.h"),
+           os.path.join(CSRC, "fwg_xchg.h"), os.path.join(CSRC, "fwg_wide.h")]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

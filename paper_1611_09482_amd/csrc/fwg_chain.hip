@@ -22,6 +22,7 @@
 
 #include "fwg_chain.h"
 #include "fwg_internal.h"
+#include "fwg_sample.h"
 
 namespace fwg {
 namespace ch {
@@ -32,14 +33,6 @@ static_assert(LR <= 8, "the per-layer flags fit the 8 words before the broadcast
 constexpr int NT = 128;      // wave 0: the chain; wave 1: recurrent halves and staging
 constexpr int KCH = 64;      // steps per chunk of staged uniforms / forced inputs
 constexpr int SPIN_MAX = 1 << 24;
-
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-__device__ __forceinline__ float lane_f(float v, int l) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
-}
 
 // v of lane i plus v of lane i ^ 32, in every lane (the two half-waves' partial sums of one dot product).
 __device__ __forceinline__ float halves_sum(float v) {
@@ -62,41 +55,6 @@ __device__ __forceinline__ float half_dot(const float (&w)[C / 2], const float *
     a1 = fmaf(w[4 * i + 3], x.w, a1);
   }
   return a0 + a1;
-}
-
-// Inverse-CDF sample of one row of 256 logits held 4 per lane (lane l: classes 4l..4l+3): max, exp,
-// inclusive prefix sums in class order (in-lane, then DPP shifts inside rows of 16 lanes, then the
-// row totals), and the first class k with u Z < S_k, else the last class.  Wave-uniform result.
-__device__ __forceinline__ int sample_row(float4 lg, float u, int lane) {
-  float m = fmaxf(fmaxf(lg.x, lg.y), fmaxf(lg.z, lg.w));
-  m = fmaxf(m, dpp<0xB1>(m));   // quad_perm [1,0,3,2]
-  m = fmaxf(m, dpp<0x4E>(m));   // quad_perm [2,3,0,1]
-  m = fmaxf(m, dpp<0x141>(m));  // row_half_mirror
-  m = fmaxf(m, dpp<0x140>(m));  // row_mirror
-  m = fmaxf(fmaxf(lane_f(m, 0), lane_f(m, 16)), fmaxf(lane_f(m, 32), lane_f(m, 48)));
-  float c[4];
-  c[0] = __expf(lg.x - m);
-  c[1] = c[0] + __expf(lg.y - m);
-  c[2] = c[1] + __expf(lg.z - m);
-  c[3] = c[2] + __expf(lg.w - m);
-  float incl = c[3];
-  incl += dpp<0x111>(incl);  // row_shr:1
-  incl += dpp<0x112>(incl);  // row_shr:2
-  incl += dpp<0x114>(incl);  // row_shr:4
-  incl += dpp<0x118>(incl);  // row_shr:8
-  const float t0 = lane_f(incl, 15), t1 = lane_f(incl, 31), t2 = lane_f(incl, 47), t3 = lane_f(incl, 63);
-  const int row = lane >> 4;
-  incl += (row >= 1 ? t0 : 0.f) + (row >= 2 ? t1 : 0.f) + (row >= 3 ? t2 : 0.f);
-  const float excl = incl - c[3];
-  const float target = u * (((t0 + t1) + t2) + t3);
-  int first = 4;
-#pragma unroll
-  for (int k = 3; k >= 0; --k)
-    if (target < excl + c[k]) first = k;
-  const unsigned long long hit = __ballot(first < 4);
-  if (hit == 0ull) return Q - 1;
-  const int src = __ffsll((long long)hit) - 1;
-  return 4 * src + __builtin_amdgcn_readlane(first, src);
 }
 
 // LDS areas of a launch (offsets from the ChainArgs layout, in floats).
@@ -281,7 +239,7 @@ __global__ void __launch_bounds__(NT) chain_step_kernel(StepArgs a, ChainArgs g)
         }
       }
       if (a.mode == MODE_GENERATE) {
-        in = sample_row(lg, s.u[(step / KCH & 1) * KCH + step % KCH], lane);
+        in = sample_row4(lg, s.u[(step / KCH & 1) * KCH + step % KCH]);
         if (lane == 0) a.samples[(long long)b * a.n_steps + step] = in;
       } else {
         if (a.logits) ((float4 *)(a.logits + ((long long)b * a.n_steps + step) * Q))[lane] = lg;

@@ -18,6 +18,7 @@
 #include "fwg_valu.h"
 #include "fwg_wave.h"
 #include "fwg_chain.h"
+#include "fwg_wide.h"
 
 using namespace fwg;
 
@@ -77,6 +78,10 @@ struct Plan {
   // chain family: the weight image and the launch's LDS bytes
   ChainArgs chain;
   size_t off_chain, chain_lds;
+  // wide family: packed weights and tables, the launch's LDS and exchange-region bytes
+  WideArgs wide;
+  size_t wide_lds, wide_comm;
+  size_t off_wl, off_wo, off_wembT, off_wembb, off_wconvb, off_woutb;
 };
 
 // Layout of the wave family's weight image and per-wave scratch; false when the model does not fit
@@ -261,6 +266,11 @@ int make_plan(const fwg_desc *d, Plan *p) {
   if (p->regime == REGIME_VALU && !forced_other &&
       chain_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, d->dilations, &p->chain, &p->chain_lds))
     p->regime = REGIME_CHAIN;
+  // float32 ReLU stacks of 512 channels: each layer spread over a group of 32 blocks per XCD
+  if (p->regime == REGIME_VALU && !forced_other &&
+      wide_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, p->bmax, d->dilations, &p->wide, &p->wide_lds,
+                  &p->wide_comm))
+    p->regime = REGIME_WIDE;
   // small models whose weights all fit in LDS: one wavefront per stream
   if (p->regime == REGIME_VALU && !(force && strcmp(force, "valu") == 0) && wave_layout(*p, &p->wave))
     p->regime = REGIME_WAVE;
@@ -289,6 +299,17 @@ int make_plan(const fwg_desc *d, Plan *p) {
       p->off_comm = take(split_comm_bytes(p->L, p->brows / kMfRows));
       p->off_sticky = take(sizeof(uint32_t));
     }
+  }
+  p->off_wl = p->off_wo = p->off_wembT = p->off_wembb = p->off_wconvb = p->off_woutb = 0;
+  if (p->regime == REGIME_WIDE) {
+    p->off_wl = take(p->wide.wl_bytes);
+    p->off_wo = take(p->wide.wo_bytes);
+    p->off_wembT = take(sizeof(float) * (size_t)p->Q * p->C);
+    p->off_wembb = take(sizeof(float) * p->C);
+    p->off_wconvb = take(sizeof(float) * (size_t)p->L * p->C);
+    p->off_woutb = take(sizeof(float) * p->Q);
+    p->off_comm = take(p->wide_comm);
+    p->off_sticky = take(sizeof(uint32_t));
   }
   p->off_embed = take((size_t)p->Q * p->C * p->es);
   p->off_embed_b = take(sizeof(float) * p->C);
@@ -410,7 +431,8 @@ int enqueue_reset(fwg_handle *h) {
   const Plan &p = h->plan;
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_gen, (size_t)p.queue_elems * p.es, h->stream));
   HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_last), p.seed_input, p.bmax, h->stream));
-  if (p.regime == REGIME_SPLIT) HIP_TRY(launch_fill_zero(h->ws + p.off_sticky, sizeof(uint32_t), h->stream));
+  if (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE)
+    HIP_TRY(launch_fill_zero(h->ws + p.off_sticky, sizeof(uint32_t), h->stream));
   if (p.nv_ok)  // every history entry the seed: the entry of time 0 is the first input
     HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_hist), p.seed_input, p.bmax * p.nv_hc, h->stream));
   h->t = 0;
@@ -556,6 +578,23 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
       hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
       if (e != hipSuccess) return e;
       return launch_split_step(b, h->stream);
+    }
+    case REGIME_WIDE: {
+      StepArgs b = a;
+      b.sp_nb = (a.batch + kWideStreams - 1) / kWideStreams;
+      b.sp_comm = comm ? comm : h->ws + p.off_comm;
+      b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
+      // tags restart at 1 every launch: clear the exchange words first (a fill kernel, no memset node)
+      hipError_t e = launch_fill_zero(b.sp_comm, p.wide_comm, h->stream);
+      if (e != hipSuccess) return e;
+      WideArgs g = p.wide;
+      g.wl = h->ws + p.off_wl;
+      g.wo = h->ws + p.off_wo;
+      g.embT = (float *)(h->ws + p.off_wembT);
+      g.embb = (float *)(h->ws + p.off_wembb);
+      g.convb = (float *)(h->ws + p.off_wconvb);
+      g.outb = (float *)(h->ws + p.off_woutb);
+      return launch_wide_step(b, g, p.wide_lds, h->stream);
     }
     case REGIME_CHAIN: {
       ChainArgs g = p.chain;
@@ -828,6 +867,24 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     TRY_OR_FREE(launch_par_repack(w->out, ws + p.off_pout, PAR_REPACK_COPY, dt, p.Q, Kout, C, 0, Kout, 0, s));
   }
   std::vector<const void *> ptrs;
+  if (p.regime == REGIME_WIDE) {
+    int coresident = 0;
+    TRY_OR_FREE(wide_setup(p.wide_lds, &coresident));
+    if (!coresident) {
+      h->plan.regime = REGIME_VALU;  // the general kernels' weights are in the workspace as well
+    } else {
+      WideArgs g = p.wide;
+      g.wl = ws + p.off_wl;
+      g.wo = ws + p.off_wo;
+      g.embT = (float *)(ws + p.off_wembT);
+      g.embb = (float *)(ws + p.off_wembb);
+      g.convb = (float *)(ws + p.off_wconvb);
+      g.outb = (float *)(ws + p.off_woutb);
+      TRY_OR_FREE(launch_wide_pack(w->embed, w->embed_b, w->conv, w->conv_b, w->out, w->out_b, p.L, g, s));
+      // set-up of fwg_generate_noalloc: this device's static exchange-word array, looked up once
+      TRY_OR_FREE(split_static_scratch(&h->static_scratch));
+    }
+  }
   if (p.regime == REGIME_SPLIT) {
     int coresident = 0;
     TRY_OR_FREE(split_setup(p.L, p.brows / kMfRows, &coresident));
@@ -886,8 +943,9 @@ int generate_impl(fwg_handle *h, int32_t batch, int32_t n_steps, const float *un
   if (h->bound_batch >= 0 && h->bound_batch != batch)
     return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
   void *comm = nullptr;
-  if (noalloc && p.regime == REGIME_SPLIT) {
-    const size_t need = split_comm_bytes(p.L, (batch + kMfRows - 1) / kMfRows);
+  if (noalloc && (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE)) {
+    const size_t need =
+        p.regime == REGIME_SPLIT ? split_comm_bytes(p.L, (batch + kMfRows - 1) / kMfRows) : p.wide_comm;
     if (need > kStaticScratchBytes)
       return fail(FWG_ENOSPACE, "the exchange words of %d streams x %d layers need %zu bytes; the static scratch "
                   "array holds %zu", batch, p.L, need, kStaticScratchBytes);
@@ -1034,11 +1092,11 @@ int fwg_destroy(fwg_handle *h) {
 int fwg_device_status(fwg_handle *h) {
   if (!h) return fail(FWG_EINVAL, "handle is NULL");
   HIP_TRY(hipStreamSynchronize(h->stream));
-  if (h->plan.regime == REGIME_SPLIT) {
+  if (h->plan.regime == REGIME_SPLIT || h->plan.regime == REGIME_WIDE) {
     uint32_t v = 0;
     HIP_TRY(hipMemcpy(&v, h->ws + h->plan.off_sticky, sizeof(v), hipMemcpyDeviceToHost));
     if (v)
-      return fail(FWG_EDEVICE, "a wait between the blocks of a split-family launch ran out (the blocks were not all "
+      return fail(FWG_EDEVICE, "a wait between the cooperating blocks of a launch ran out (the blocks were not all "
                                "resident at once); that launch's outputs are invalid");
   }
   return FWG_OK;
@@ -1051,6 +1109,7 @@ const char *fwg_regime(const fwg_handle *h) {
     case REGIME_SPLIT: return "mfma_split_bf16_r64_s512";
     case REGIME_WAVE: return "wave";
     case REGIME_CHAIN: return "chain_f32_c32";
+    case REGIME_WIDE: return "wide_f32_c512";
     default: return "valu";
   }
 }

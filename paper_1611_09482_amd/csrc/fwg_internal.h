@@ -54,9 +54,10 @@ struct StepArgs {
   const void *mf_embT;     // embedding table [Q][R] (bf16)
   const float *mf_bias;    // bias block: conv [L][2R], res [L][R], skip sum [S], head [H], out [Q], embed [R]
   // split MFMA family only
-  void *sp_comm;           // exchange words between chain and helper blocks (zeroed before each launch)
+  void *sp_comm;           // exchange words between cooperating blocks (zeroed before each launch)
   uint32_t *sp_sticky;     // set when a wait of a launch ran out (cleared by create and reset)
-  int sp_nb;               // chain blocks of this launch (ceil(batch / 16))
+  int sp_nb;               // split family: chain blocks of this launch (ceil(batch / 16)); wide family:
+                           // stream groups (ceil(batch / 4))
 };
 
 // What drives the input of each step.
@@ -69,7 +70,7 @@ enum StepMode {
 __host__ __device__ inline int forced_shift(int mode) { return mode == MODE_TEACHER ? 1 : 0; }
 
 // Kernel families.
-enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3, REGIME_CHAIN = 4 };
+enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3, REGIME_CHAIN = 4, REGIME_WIDE = 5 };
 
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
 // 16 streams per block of 8 waves, weight fragments per wave and stage.

@@ -1,4 +1,5 @@
-// Inverse-CDF sampling shared by the general step kernels and the naive generator.
+// Inverse-CDF sampling shared by the general step kernels, the naive generator, and (the DPP form)
+// the chain and wide step kernels.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -35,6 +36,50 @@ __device__ __forceinline__ int sample_row_256(const float *lg, float u) {
   if (hit == 0ull) return 255;
   const int src = __ffsll((long long)hit) - 1;
   return 4 * src + __shfl(first, src, 64);
+}
+
+// The same rule for a row held 4 classes per lane (lane l: classes 4l..4l+3) with DPP row moves and
+// lane reads instead of LDS shuffles: max, exp, inclusive prefix sums in class order (in-lane, then
+// shifts inside rows of 16 lanes, then the row totals), the first class k with u Z < S_k, else the
+// last class.  Wave-uniform result.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float read_lane(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+__device__ __forceinline__ int sample_row4(float4 lg, float u) {
+  const int lane = threadIdx.x & 63;
+  float m = fmaxf(fmaxf(lg.x, lg.y), fmaxf(lg.z, lg.w));
+  m = fmaxf(m, dpp_move<0xB1>(m));   // quad_perm [1,0,3,2]
+  m = fmaxf(m, dpp_move<0x4E>(m));   // quad_perm [2,3,0,1]
+  m = fmaxf(m, dpp_move<0x141>(m));  // row_half_mirror
+  m = fmaxf(m, dpp_move<0x140>(m));  // row_mirror
+  m = fmaxf(fmaxf(read_lane(m, 0), read_lane(m, 16)), fmaxf(read_lane(m, 32), read_lane(m, 48)));
+  float c[4];
+  c[0] = __expf(lg.x - m);
+  c[1] = c[0] + __expf(lg.y - m);
+  c[2] = c[1] + __expf(lg.z - m);
+  c[3] = c[2] + __expf(lg.w - m);
+  float incl = c[3];
+  incl += dpp_move<0x111>(incl);  // row_shr:1
+  incl += dpp_move<0x112>(incl);  // row_shr:2
+  incl += dpp_move<0x114>(incl);  // row_shr:4
+  incl += dpp_move<0x118>(incl);  // row_shr:8
+  const float t0 = read_lane(incl, 15), t1 = read_lane(incl, 31), t2 = read_lane(incl, 47), t3 = read_lane(incl, 63);
+  const int row = lane >> 4;
+  incl += (row >= 1 ? t0 : 0.f) + (row >= 2 ? t1 : 0.f) + (row >= 3 ? t2 : 0.f);
+  const float excl = incl - c[3];
+  const float target = u * (((t0 + t1) + t2) + t3);
+  int first = 4;
+#pragma unroll
+  for (int k = 3; k >= 0; --k)
+    if (target < excl + c[k]) first = k;
+  const unsigned long long hit = __ballot(first < 4);
+  if (hit == 0ull) return 255;
+  const int src = __ffsll((long long)hit) - 1;
+  return 4 * src + __builtin_amdgcn_readlane(first, src);
 }
 
 }  // namespace fwg

@@ -49,11 +49,13 @@
 
 #include "fwg_internal.h"
 #include "fwg_mfma_dev.h"
+#include "fwg_xchg.h"
 
 namespace fwg {
 namespace sp {
 
 using namespace mfd;
+using namespace xg;
 
 constexpr int R = kMfR, S = kMfS, H = kMfH, Q = 256, ROWS = kMfRows;
 constexpr int NT = kMfThreads, NW = kMfWaves;
@@ -71,12 +73,9 @@ constexpr int FA = kSpFA, FB = kSpFB, FS = kSpFS;
 constexpr int FW1 = (HL / 16) * (S / 32), FW2 = (QL / 16) * (H / 32);
 constexpr int DA = 3 * FA, DB = 6 * FB;  // ring depths (fragments) of chain waves A and B
 constexpr int KCH = 64;                  // steps per chunk of per-step inputs staged in LDS
-constexpr int SPIN_MAX = 1 << 21;        // polls of one wait before the launch is aborted
 static_assert(ZST <= PH && ZST % 4 == 0, "a wave's staged z^l rows fit its partial-sum area, 16-byte aligned");
 static_assert(SL == 64 && FS == 8 && HL == 64 && QL == 32 && NHLP == NW,
               "helper slices of 4 skip and 4 hidden tiles; 2 class tiles per class-block wave");
-
-typedef unsigned long long u64;
 
 struct ChainLds {
   uint16_t vbuf[3][ROWS * PX];     // popped queue rows, by layer index mod 3
@@ -142,66 +141,6 @@ __host__ __device__ inline u64 *comm_s(void *comm, int L, int blk) { return comm
 __host__ __device__ inline u64 *comm_hid(void *comm, int L, int blk) { return comm_s(comm, L, blk) + XWORDS; }
 __host__ __device__ inline u64 *comm_smp(void *comm, int L, int blk) { return comm_hid(comm, L, blk) + XWORDS; }
 __host__ __device__ inline u64 *comm_hs(void *comm, int L, int blk) { return comm_smp(comm, L, blk) + SWORDS; }
-
-// `local`: every reader shares this block's XCD (and L2).
-__device__ __forceinline__ void put_word(u64 *p, uint32_t payload, uint32_t tag, bool local) {
-  const u64 v = ((u64)tag << 32) | payload;
-  if (local) __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  else __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Two consecutive words (p 16-byte aligned).  Within one XCD a single 16-byte store carries both:
-// it lands in one L2 line, so each 8-byte word (tag with its payload) becomes visible whole.
-__device__ __forceinline__ void put_words2(u64 *p, uint32_t pa, uint32_t pb, uint32_t tag, bool local) {
-  if (local) {
-    *(u32x4 *)p = u32x4{pa, tag, pb, tag};
-  } else {
-    put_word(p, pa, tag, false);
-    put_word(p + 1, pb, tag, false);
-  }
-}
-__device__ __forceinline__ uint32_t xcd_id() {
-  return __builtin_amdgcn_s_getreg((3 << 11) | (0 << 6) | 20) & 15;  // HW_REG_XCC_ID, bits 3:0
-}
-__device__ __forceinline__ u64 get_word(const u64 *p) {
-  return __hip_atomic_load((u64 *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint32_t get_flag(const uint32_t *p) {
-  return __hip_atomic_load((uint32_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// A wait ran out: end every other wait of the launch, and leave a sticky mark for the host.
-__device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *sticky) {
-  __hip_atomic_store(abort_word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Load the N tagged words p[e STRIDE] until every tag equals `tag` (or the launch is aborted).
-// Per lane.  Every wait of a tile uses STRIDE = the number of lanes polling it, so that each load
-// instruction reads consecutive words: a poll whose lanes each take a run of consecutive words
-// touches a cache line per lane and instruction, and those requests (not the L2's latency) made
-// the tile gathers 2-3x slower.
-template <int N, int STRIDE = 1>
-__device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t (&out)[N], uint32_t *abort_word,
-                                           uint32_t *sticky) {
-  u64 v[N];
-  for (int it = 0;; ++it) {
-#pragma unroll
-    for (int e = 0; e < N; ++e) v[e] = get_word(p + e * STRIDE);
-    bool ok = true;
-#pragma unroll
-    for (int e = 0; e < N; ++e) ok = ok && (uint32_t)(v[e] >> 32) == tag;
-    if (ok) break;
-    // the abort word every 16 polls: a stale poll then costs one round trip, not two
-    if ((it & 15) == 15) {
-      if (get_flag(abort_word) != 0u) break;
-      if (it >= SPIN_MAX) {
-        raise_abort(abort_word, sticky);
-        break;
-      }
-    }
-  }
-#pragma unroll
-  for (int e = 0; e < N; ++e) out[e] = (uint32_t)v[e];
-}
 
 // ---------------------------------------------------------------------------
 // Chain block

@@ -56,9 +56,12 @@ def test_workspace_size_for_every_workload(lib):
         queues = m.queue_total * wl.batch * m.channels * es
         # two queue regions (generation, teacher-forced) plus weights
         assert n >= 2 * queues + W.make_weights(m, 0).nbytes()
+        # twice the streams: the queue regions grow with the batch (the kernel family, and with it the
+        # packed weight arrays, may change: the 512-channel family takes at most 32 streams)
         d2 = B.make_desc(m.kind, m.dtype, m.channels, m.dilations, 2 * wl.batch, m.skip_channels,
                          m.head_channels, m.n_classes, m.seed_input)
-        assert _rc_size(lib, d2)[1] > n
+        rc2, n2 = _rc_size(lib, d2)
+        assert rc2 == B.FWG_OK and n2 >= 4 * queues + W.make_weights(m, 0).nbytes()
 
 
 @pytest.mark.parametrize("kw,code", [

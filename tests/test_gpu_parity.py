@@ -115,6 +115,7 @@ FAMILIES = {
     # 12 layers: the split MFMA kernels (chain block + skip helper blocks; L a multiple of 6, >= 12)
     "gated_r64_bf16_split": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 2, 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
+    "relures_c512_f32_valu": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
     "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
     "gated_r32_w3_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
@@ -132,8 +133,12 @@ FAMILIES = {
 WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_c32_f32_wave"}
 # families that must run on the chain kernels (float32 ReLU stacks with C = 32, width 2)
 CHAIN_FAMILIES = {"relu_c32_f32", "relures_c32_f32"}
-# families whose test forces the general (VALU) kernel family instead of the MFMA or wave one
-FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu"}
+# families that must run on the wide kernels (float32 ReLU stacks with C = 512: each layer spread
+# over a group of 32 blocks)
+WIDE_FAMILIES = {"relures_c512_f32"}
+# families whose test forces the general (VALU) kernel family instead of the MFMA, wave, chain or
+# wide one
+FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu"}
 # families whose test forces the wave-per-stream family instead of the chain one
 FORCE_WAVE = {"relu_c32_f32_wave"}
 
@@ -175,7 +180,9 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
             split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
             assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
-            assert fw.regime in ("valu", "wave", "chain_f32_c32"), (fam, fw.regime)
+            assert fw.regime in ("valu", "wave", "chain_f32_c32", "wide_f32_c512"), (fam, fw.regime)
+        if fam in WIDE_FAMILIES:
+            assert fw.regime == "wide_f32_c512", (fam, fw.regime)
         if fam in WAVE_FAMILIES:
             assert fw.regime == "wave", (fam, fw.regime)
         if fam in CHAIN_FAMILIES:
@@ -484,7 +491,7 @@ def test_uniform_logits_sampler_gpu(fam, B, regime):
 
 
 @pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split",
-                                 "relu_c32_f32", "relures_c32_f32"])
+                                 "relu_c32_f32", "relures_c32_f32", "relures_c512_f32"])
 def test_continuation_reset_and_determinism_gpu(fam):
     cfg = FAMILIES[fam]
     w, fw, _ = build_pair(cfg, 7, 9, fam=fam)

@@ -58,6 +58,29 @@ def test_noalloc_matches_generate_split():
     assert np.array_equal(a, b)
 
 
+def test_noalloc_matches_generate_wide():
+    """The wide kernels (512-channel float32 ReLU + residual stack, groups of 32 blocks exchanging the
+    layer outputs as words): exchange words in the static array, three stream groups with a ragged last
+    one, then one group after a reset."""
+    cfg = W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2))
+    ref, na = _pair(cfg, 11)
+    assert ref.regime == na.regime == "wide_f32_c512"
+    u = W.uniforms(45, 11, 70)
+    want = ref.generate(_dev(u)).cpu().numpy()
+    out = torch.empty((11, 70), dtype=torch.int32, device="cuda")
+    got = na.generate_noalloc(_dev(u), out).cpu().numpy()
+    print(f"noalloc wide call 1: 11 x 70, equal {np.array_equal(got, want)}", flush=True)
+    assert np.array_equal(got, want)
+    ref.reset()
+    na.reset()
+    u2 = W.uniforms(46, 3, 40)
+    want2 = ref.generate(_dev(u2)).cpu().numpy()
+    out2 = torch.empty((3, 40), dtype=torch.int32, device="cuda")
+    got2 = na.generate_noalloc(_dev(u2), out2).cpu().numpy()
+    print(f"noalloc wide call 2: 3 x 40, equal {np.array_equal(got2, want2)}", flush=True)
+    assert np.array_equal(got2, want2)
+
+
 def test_noalloc_other_family_and_errors():
     """Kernel families without per-launch scratch run exactly as fwg_generate; host-side errors
     (batch binding, range) come before anything is enqueued."""
