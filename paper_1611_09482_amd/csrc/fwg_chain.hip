@@ -338,3 +338,546 @@ hipError_t launch_chain_image(const void *embed, const float *embed_b, const voi
 }
 
 }  // namespace fwg
+
+// ---------------------------------------------------------------------------
+// Gated variant: float32 gated stacks with R = 32, S = H = 256 (the WaveNet-style unit: z =
+// tanh(a[0:R]) sigmoid(a[R:2R]), residual and skip 1x1s, the skip sum through relu -> 1x1 -> relu
+// -> 1x1 to the logits; Section 2.1, Fig. 2), at most 64 layers.  One block of four waves per stream:
+//  - wave 0 (the chain): lane o computes gate pre-activation o (tanh half for o < 32, sigmoid half
+//    for o >= 32) from the layer input broadcast through LDS; the halves meet with one cross-half
+//    lane swap, which leaves z in both halves; the residual 1x1 splits K over the half-waves.  It
+//    pushes each layer input to the layer's queue in the workspace and to an LDS row;
+//  - wave 1: W_r v + b of every layer for the next step: the pops of layers with d >= 2 (pushed at
+//    least one step earlier, before a block barrier) are read from the workspace queues, those of
+//    layers with d = 1 are this step's LDS rows (an LDS flag per layer);
+//  - waves 2, 3: the skip sum, two of the 256 skip channels per lane, each layer as soon as its z
+//    row is in LDS (an LDS flag per layer);
+//  - then all four waves compute the head, one hidden channel and then one class per thread, and
+//    wave 0 draws the sample.
+// Every weight is streamed from the workspace once per step (the model, about 1.6 MB at 20 layers,
+// stays in L2), into registers one layer ahead.  The per-layer queue offset and slot of layer l live
+// in lane l of the waves that need them and are read with lane reads.
+namespace fwg {
+namespace chg {
+
+constexpr int R = kChainGR, S = kChainGS, H = kChainGS, Q = 256, NT = 256, KCH = 64;
+constexpr int FCH = 12, FREC = 8, FSK = 16, FH = 64, FHR = 8;  // float4 chunks per lane (FHR: per head round)
+constexpr int SPIN_MAX = 1 << 20;
+
+// Flags in LDS, addressed as LDS: through a generic pointer a volatile access stays a flat access,
+// whose wait also drains every global load in flight (the weights fetched one layer ahead).
+typedef __attribute__((address_space(3))) volatile int lds_flag;
+
+struct Lay {
+  float *embT, *embb;   // [Q][R], [R]
+  float *P;             // [2][L][2R]: W_r v + b by step parity
+  float *xrow, *zrow;   // [L][R]: this step's layer inputs and gate outputs
+  float *resb;          // [L][R]
+  float *srow, *hrow, *lrow;  // [S]: relu(skip sum); [H]: relu(hidden); [Q]: logits
+  float *u;             // [2][KCH]
+  int *fin;             // [2][KCH]
+  lds_flag *fx, *fz;     // [L]: step + 1 once the chain wrote xrow[l] / zrow[l]
+  lds_flag *abort_;      // set once a flag wait ran out: later waits of the launch return at once
+};
+
+__host__ __device__ inline size_t lds_floats(int L) {
+  return (size_t)Q * R + R + 2ull * L * 2 * R + 3ull * L * R + S + H + Q + 2 * KCH + 2 * KCH + 2ull * L + 4;
+}
+
+// Weight streams are read as raw buffer loads from one resource over the packed weights: the
+// per-lane part of the address is one constant VGPR offset and the per-chunk part an SGPR offset,
+// so that no 64-bit address per chunk is kept in registers.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, 0x00020000);
+}
+template <int N>
+__device__ __forceinline__ void load_chunks(float4 (&dst)[N], Rsrc r, int voff, int soff, int stride) {
+#pragma unroll
+  for (int i = 0; i < N; ++i)
+    dst[i] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff + i * stride, 0));
+}
+// keeps the compiler from moving LDS accesses across a flag store or a flag wait (the hardware runs
+// a wave's LDS operations in order)
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// Waits until flag == want, at most SPIN_MAX polls (the chain wave sets every flag of a step
+// unconditionally; the bound only keeps a fault from turning into a hang).
+__device__ __forceinline__ void wait_flag(const Lay &s, lds_flag *flag, int want) {
+  for (int it = 0; *flag != want; ++it) {
+    if (it >= SPIN_MAX || *s.abort_) {
+      *s.abort_ = 1;
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  compiler_fence();
+}
+
+__device__ __forceinline__ float gate_half(float a, bool tanh_half) {
+  // tanh(a) = 1 - 2 / (exp(2a) + 1) for the first half, sigmoid(a) = 1 / (1 + exp(-a)) for the second
+  const float e = __expf(tanh_half ? 2.f * a : -a);
+  const float r = __builtin_amdgcn_rcpf(e + 1.f);
+  return tanh_half ? 1.f - 2.f * r : r;
+}
+
+__device__ __forceinline__ long long lane_i64(long long v, int l) {
+  const int lo = __builtin_amdgcn_readlane((int)(unsigned)(v & 0xffffffffll), l);
+  const int hi = __builtin_amdgcn_readlane((int)(v >> 32), l);
+  return (long long)(((unsigned long long)(unsigned)hi << 32) | (unsigned)lo);
+}
+
+// The chain wave's layer l with its weights in Wc (W_e row chunks, then W_res half-row chunks); the
+// next layer's weights are fetched into Wn first.  x: the layer input in (lane o and o + 32 both
+// hold channel o), the layer output out.  qptr: this step's push address of the layer's queue.
+__device__ __forceinline__ void chain_gated_layer(const Lay &s, float4 (&Wc)[FCH], float4 (&Wn)[FCH], Rsrc rw,
+                                                  int next_off, float *qptr, int l, int L, int par, int step,
+                                                  int lane, float &x) {
+  const int o = lane & (R - 1), h = lane >> 5;
+  if (lane < R) {
+    qptr[o] = x;
+    s.xrow[l * R + o] = x;
+  }
+  compiler_fence();
+  if (lane == 0) s.fx[l] = step + 1;
+  load_chunks(Wn, rw, lane * 16, next_off, 1024);
+  const float4 *xr4 = (const float4 *)(s.xrow + l * R);
+  float a0 = s.P[(par * L + l) * 2 * R + lane], a1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < R / 4; ++c) {
+    const float4 xv = xr4[c];
+    a0 = fmaf(Wc[c].x, xv.x, a0);
+    a1 = fmaf(Wc[c].y, xv.y, a1);
+    a0 = fmaf(Wc[c].z, xv.z, a0);
+    a1 = fmaf(Wc[c].w, xv.w, a1);
+  }
+  const float v = gate_half(a0 + a1, lane < R);
+  const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, v), __builtin_bit_cast(unsigned, v),
+                                                   false, false);
+  // lanes o and o + 32 both hold tanh(a_o) and sigmoid(a_{o+32})
+  const float z = __builtin_bit_cast(float, (unsigned)sw[0]) * __builtin_bit_cast(float, (unsigned)sw[1]);
+  if (lane < R) s.zrow[l * R + o] = z;
+  compiler_fence();
+  if (lane == 0) s.fz[l] = step + 1;
+  // the residual 1x1 over this half of K, z read back from its row
+  const float4 *zr4 = (const float4 *)(s.zrow + l * R + 16 * h);
+  float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float4 zv = zr4[c];
+    r0 = fmaf(Wc[8 + c].x, zv.x, r0);
+    r1 = fmaf(Wc[8 + c].y, zv.y, r1);
+    r0 = fmaf(Wc[8 + c].z, zv.z, r0);
+    r1 = fmaf(Wc[8 + c].w, zv.w, r1);
+  }
+  x = x + s.resb[l * R + o] + ch::halves_sum(r0 + r1);
+}
+
+// Wave 1's layer l: W_r v + b for the next step, v = the state the layer pops then (qrow: a queue
+// row in the workspace, loaded before the next layer's weights so that its wait leaves them in
+// flight, or, with from_row, this step's LDS row of the layer once the chain has written it).
+__device__ __forceinline__ void rec_layer(const Lay &s, const float4 (&Wc)[FREC], float4 (&Wn)[FREC], Rsrc rw,
+                                          int next_off, const float *qrow, bool from_row, const float *convb, int l,
+                                          int L, int np, int step, int lane) {
+  float4 vv[FREC];
+  if (!from_row) {
+#pragma unroll
+    for (int c = 0; c < FREC; ++c) vv[c] = ((const float4 *)qrow)[c];
+  }
+  load_chunks(Wn, rw, lane * 16, next_off, 1024);
+  if (from_row) {
+    // the state popped next step is this step's input of the layer
+    wait_flag(s, s.fx + l, step + 1);
+    const float4 *x4 = (const float4 *)(s.xrow + l * R);
+#pragma unroll
+    for (int c = 0; c < FREC; ++c) vv[c] = x4[c];
+  }
+  float a0 = convb[l * 2 * R + lane], a1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < FREC; ++c) {
+    a0 = fmaf(Wc[c].x, vv[c].x, a0);
+    a1 = fmaf(Wc[c].y, vv[c].y, a1);
+    a0 = fmaf(Wc[c].z, vv[c].z, a0);
+    a1 = fmaf(Wc[c].w, vv[c].w, a1);
+  }
+  s.P[(np * L + l) * 2 * R + lane] = a0 + a1;
+}
+
+// A skip wave's layer l: skip channels m0 and m0 + 1 accumulate W_s z of the layer.
+__device__ __forceinline__ void skip_layer(const Lay &s, const float4 (&Wc)[FSK], float4 (&Wn)[FSK], Rsrc rw,
+                                           int next_off, int lane, int l, int step, float &s0, float &s1) {
+  load_chunks(Wn, rw, lane * 16, next_off, 1024);
+  wait_flag(s, s.fz + l, step + 1);
+  const float4 *zr4 = (const float4 *)(s.zrow + l * R);
+  float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < R / 4; ++c) {
+    const float4 zv = zr4[c];
+    s0 = fmaf(Wc[c].x, zv.x, s0);
+    s1 = fmaf(Wc[8 + c].x, zv.x, s1);
+    p0 = fmaf(Wc[c].y, zv.y, p0);
+    p1 = fmaf(Wc[8 + c].y, zv.y, p1);
+    s0 = fmaf(Wc[c].z, zv.z, s0);
+    s1 = fmaf(Wc[8 + c].z, zv.z, s1);
+    p0 = fmaf(Wc[c].w, zv.w, p0);
+    p1 = fmaf(Wc[8 + c].w, zv.w, p1);
+  }
+  s0 += p0;
+  s1 += p1;
+}
+
+// One head 1x1 for output channel tid: the row (chunk c of thread t = 64 w + lane at byte
+// off + 65536 w + 1024 c + 16 lane) streamed in rounds of FHR chunks (the first round already in HA),
+// the input vector broadcast from LDS.  voff: this thread's 65536 w + 16 lane.
+__device__ __forceinline__ void head_round(const float4 (&Wc)[FHR], const float *in, float &a0, float &a1) {
+  const float4 *in4 = (const float4 *)in;
+#pragma unroll
+  for (int c = 0; c < FHR; ++c) {
+    const float4 xv = in4[c];
+    a0 = fmaf(Wc[c].x, xv.x, a0);
+    a1 = fmaf(Wc[c].y, xv.y, a1);
+    a0 = fmaf(Wc[c].z, xv.z, a0);
+    a1 = fmaf(Wc[c].w, xv.w, a1);
+  }
+}
+__device__ __forceinline__ float head_row(float4 (&HA)[FHR], float4 (&HB)[FHR], Rsrc rw, int voff, int off,
+                                          const float *inrow, float bias) {
+  constexpr int NR = FH / FHR;  // rounds, an even number
+  float a0 = bias, a1 = 0.f;
+  // two rounds per iteration, not unrolled: the compiler cannot hoist later rounds' loads and LDS
+  // reads (their registers would spill)
+#pragma unroll 1
+  for (int r = 0; r < NR; r += 2) {
+    load_chunks(HB, rw, voff, off + (r + 1) * FHR * 1024, 1024);
+    head_round(HA, inrow + r * FHR * 4, a0, a1);
+    if (r + 2 < NR) load_chunks(HA, rw, voff, off + (r + 2) * FHR * 1024, 1024);
+    head_round(HB, inrow + (r + 1) * FHR * 4, a0, a1);
+  }
+  return a0 + a1;
+}
+
+__global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedArgs g) {
+  extern __shared__ float4 lds4[];
+  float *lds = (float *)lds4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int b = blockIdx.x, L = a.L;
+  Lay s;
+  s.embT = lds;
+  s.embb = s.embT + Q * R;
+  s.P = s.embb + R;
+  s.xrow = s.P + 2 * L * 2 * R;
+  s.zrow = s.xrow + L * R;
+  s.resb = s.zrow + L * R;
+  s.srow = s.resb + L * R;
+  s.hrow = s.srow + S;
+  s.lrow = s.hrow + H;
+  s.u = s.lrow + Q;
+  s.fin = (int *)(s.u + 2 * KCH);
+  s.fx = (lds_flag *)(s.fin + 2 * KCH);
+  s.fz = s.fx + L;
+  s.abort_ = s.fz + L;
+
+  // ---- launch: tables into LDS, flags, the first chunk of per-step inputs
+  for (int i = tid; i < Q * R / 4; i += NT) ((float4 *)s.embT)[i] = ((const float4 *)g.embT)[i];
+  for (int i = tid; i < R; i += NT) s.embb[i] = g.embb[i];
+  for (int i = tid; i < L * R; i += NT) s.resb[i] = g.resb[i];
+  for (int i = tid; i < L; i += NT) {
+    s.fx[i] = 0;
+    s.fz[i] = 0;
+  }
+  if (tid == 0) *s.abort_ = 0;
+  for (int j = tid; j < KCH; j += NT) {
+    if (a.mode == MODE_GENERATE) s.u[j] = j < a.n_steps ? a.uniforms[(long long)b * a.n_steps + j] : 0.f;
+    else {
+      const long long nx = j + forced_shift(a.mode);
+      s.fin[j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
+    }
+  }
+  // lane l: layer l's queue (element offset of this stream's row in slot 0), dilation and the slot
+  // of the current step (wave 1 keeps the slot of the next step)
+  const long long slot_stride = (long long)a.bmax * R;
+  long long qoff = 0;
+  int qdil = 1, qslot = 0;
+  if (lane < L) {
+    const LayerDev ld = a.layers[lane];
+    qoff = ld.ring_off + (long long)b * R;
+    qdil = ld.dil;
+    qslot = (int)(a.t0 % (long long)qdil);
+  }
+  float *ring = (float *)a.ring;
+  // W_r v + b of every layer for step 0 (wave 1; every pop of step 0 was pushed before the launch)
+  if (wave == 1) {
+    for (int l = 0; l < L; ++l) {
+      const float *v = ring + lane_i64(qoff + qslot * slot_stride, l);
+      const float4 *w = g.wrec + (size_t)l * FREC * 64 + lane;
+      float acc = g.convb[l * 2 * R + lane];
+#pragma unroll
+      for (int c = 0; c < FREC; ++c) {
+        const float4 wv = w[c * 64];
+        const float4 vv = *(const float4 *)(v + 4 * c);
+        acc = fmaf(wv.x, vv.x, acc);
+        acc = fmaf(wv.y, vv.y, acc);
+        acc = fmaf(wv.z, vv.z, acc);
+        acc = fmaf(wv.w, vv.w, acc);
+      }
+      s.P[l * 2 * R + lane] = acc;
+    }
+    qslot = qslot + 1 == qdil ? 0 : qslot + 1;  // wave 1 works one step ahead
+  }
+  __syncthreads();
+
+  int in = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
+  const int o = lane & (R - 1);
+  // the packed weights, wchain first: byte offsets of the streams
+  const char *wbase = (const char *)g.wchain;
+  const Rsrc rw = make_rsrc(wbase, (int)((const char *)g.convb - wbase));
+  const int o_rec = (int)((const char *)g.wrec - wbase), o_skip = (int)((const char *)g.wskip - wbase);
+  const int o_head = (int)((const char *)g.whead - wbase), o_out = (int)((const char *)g.wout - wbase);
+  const int hvoff = wave * 65536 + lane * 16;  // this thread's part of a head chunk address
+  const float hbias = g.headb[tid], obias = g.outb[tid];
+  float4 HA[FHR], HB[FHR];
+  if (wave == 0) {
+    // ---------------- the chain, then its share of the head
+    const int lstr = FCH * 1024;
+    float4 WA[FCH], WB[FCH];
+    load_chunks(WA, rw, lane * 16, 0, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      const int par = step & 1;
+      float x = s.embT[in * R + o] + s.embb[o];
+      for (int l = 0; l < L; l += 2) {
+        {
+          float *qp = ring + lane_i64(qoff + qslot * slot_stride, l);
+          const int ln = l + 1 < L ? l + 1 : 0;
+          chain_gated_layer(s, WA, WB, rw, ln * lstr, qp, l, L, par, step, lane, x);
+        }
+        if (l + 1 < L) {
+          float *qp = ring + lane_i64(qoff + qslot * slot_stride, l + 1);
+          const int ln = l + 2 < L ? l + 2 : 0;
+          chain_gated_layer(s, WB, WA, rw, ln * lstr, qp, l + 1, L, par, step, lane, x);
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FCH; ++c) WA[c] = WB[c];
+      }
+      qslot = qslot + 1 == qdil ? 0 : qslot + 1;
+      load_chunks(HA, rw, hvoff, o_head, 1024);
+      __syncthreads();  // the skip sum is in LDS
+      const float hv = head_row(HA, HB, rw, hvoff, o_head, s.srow, hbias);
+      s.hrow[tid] = fmaxf(hv, 0.f);
+      load_chunks(HA, rw, hvoff, o_out, 1024);
+      __syncthreads();
+      const float lv = head_row(HA, HB, rw, hvoff, o_out, s.hrow, obias);
+      s.lrow[tid] = lv;
+      if (a.mode != MODE_GENERATE && a.logits) a.logits[((long long)b * a.n_steps + step) * Q + tid] = lv;
+      __syncthreads();
+      if (a.mode == MODE_GENERATE) {
+        const float4 lg = ((const float4 *)s.lrow)[lane];
+        in = sample_row4(lg, s.u[(step / KCH & 1) * KCH + step % KCH]);
+        if (lane == 0) a.samples[(long long)b * a.n_steps + step] = in;
+      } else {
+        in = s.fin[(step / KCH & 1) * KCH + step % KCH];
+      }
+      __syncthreads();  // the step's LDS rows and logits are consumed
+    }
+    if (lane == 0 && a.mode != MODE_TEACHER) a.last[b] = in;
+  } else if (wave == 1) {
+    // ---------------- W_r v + b for the next step, staging, its share of the head
+    const int lstr = FREC * 1024;
+    float4 WA[FREC], WB[FREC];
+    load_chunks(WA, rw, lane * 16, o_rec, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      const int np = (step & 1) ^ 1;
+      for (int l = 0; l < L; l += 2) {
+        {
+          const int d = __builtin_amdgcn_readlane(qdil, l);
+          const float *v = ring + lane_i64(qoff + qslot * slot_stride, l);
+          const int ln = l + 1 < L ? l + 1 : 0;
+          rec_layer(s, WA, WB, rw, o_rec + ln * lstr, v, d == 1, g.convb, l, L, np, step, lane);
+        }
+        if (l + 1 < L) {
+          const int d = __builtin_amdgcn_readlane(qdil, l + 1);
+          const float *v = ring + lane_i64(qoff + qslot * slot_stride, l + 1);
+          const int ln = l + 2 < L ? l + 2 : 0;
+          rec_layer(s, WB, WA, rw, o_rec + ln * lstr, v, d == 1, g.convb, l + 1, L, np, step, lane);
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FREC; ++c) WA[c] = WB[c];
+      }
+      qslot = qslot + 1 == qdil ? 0 : qslot + 1;
+      // staging of the next chunk of per-step inputs, one chunk ahead
+      if (step % KCH == 0) {
+        const int base = step + KCH, buf = (step / KCH + 1) & 1;
+        for (int j = lane; j < KCH; j += 64) {
+          const long long sj = base + j;
+          if (a.mode == MODE_GENERATE) {
+            s.u[buf * KCH + j] = sj < a.n_steps ? a.uniforms[(long long)b * a.n_steps + sj] : 0.f;
+          } else {
+            const long long nx = sj + forced_shift(a.mode);
+            s.fin[buf * KCH + j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
+          }
+        }
+      }
+      load_chunks(HA, rw, hvoff, o_head, 1024);
+      __syncthreads();
+      const float hv = head_row(HA, HB, rw, hvoff, o_head, s.srow, hbias);
+      s.hrow[tid] = fmaxf(hv, 0.f);
+      load_chunks(HA, rw, hvoff, o_out, 1024);
+      __syncthreads();
+      const float lv = head_row(HA, HB, rw, hvoff, o_out, s.hrow, obias);
+      s.lrow[tid] = lv;
+      if (a.mode != MODE_GENERATE && a.logits) a.logits[((long long)b * a.n_steps + step) * Q + tid] = lv;
+      __syncthreads();
+      __syncthreads();
+    }
+  } else {
+    // ---------------- the skip sum: channels 128 (wave - 2) + 2 lane and + 1, then the head
+    const int wst = o_skip + (wave - 2) * FSK * 1024;
+    const int lstr = 2 * FSK * 1024;
+    const int m0 = 128 * (wave - 2) + 2 * lane;
+    const float b0 = g.skipb[m0], b1 = g.skipb[m0 + 1];
+    float4 WA[FSK], WB[FSK];
+    load_chunks(WA, rw, lane * 16, wst, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      float s0 = b0, s1 = b1;
+      for (int l = 0; l < L; l += 2) {
+        skip_layer(s, WA, WB, rw, wst + (l + 1 < L ? l + 1 : 0) * lstr, lane, l, step, s0, s1);
+        if (l + 1 < L) skip_layer(s, WB, WA, rw, wst + (l + 2 < L ? l + 2 : 0) * lstr, lane, l + 1, step, s0, s1);
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FSK; ++c) WA[c] = WB[c];
+      }
+      s.srow[m0] = fmaxf(s0, 0.f);
+      s.srow[m0 + 1] = fmaxf(s1, 0.f);
+      load_chunks(HA, rw, hvoff, o_head, 1024);
+      __syncthreads();
+      const float hv = head_row(HA, HB, rw, hvoff, o_head, s.srow, hbias);
+      s.hrow[tid] = fmaxf(hv, 0.f);
+      load_chunks(HA, rw, hvoff, o_out, 1024);
+      __syncthreads();
+      const float lv = head_row(HA, HB, rw, hvoff, o_out, s.hrow, obias);
+      s.lrow[tid] = lv;
+      if (a.mode != MODE_GENERATE && a.logits) a.logits[((long long)b * a.n_steps + step) * Q + tid] = lv;
+      __syncthreads();
+      __syncthreads();
+    }
+  }
+}
+
+// ---- packing (once per fwg_create)
+__global__ void pack_layer_kernel(const float *conv, const float *res, const float *skip, int l, ChainGatedArgs g) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  const int nchain = FCH * 64, nrec = FREC * 64, nskip = 2 * FSK * 64;
+  float v[4];
+  if (e < nchain) {
+    const int c = e / 64, ln = e % 64;
+    for (int q = 0; q < 4; ++q) {
+      if (c < 8) v[q] = conv[((size_t)ln * R + 4 * c + q) * 2 + 1];               // W_e[ln][k] (current-input tap)
+      else v[q] = res[(size_t)(ln % R) * R + 16 * (ln / R) + 4 * (c - 8) + q];    // W_res row, this lane's half
+    }
+    ((float4 *)g.wchain)[(size_t)l * nchain + e] = make_float4(v[0], v[1], v[2], v[3]);
+  } else if (e < nchain + nrec) {
+    const int f = e - nchain, c = f / 64, ln = f % 64;
+    for (int q = 0; q < 4; ++q) v[q] = conv[((size_t)ln * R + 4 * c + q) * 2];   // W_r[ln][k] (popped tap)
+    ((float4 *)g.wrec)[(size_t)l * nrec + f] = make_float4(v[0], v[1], v[2], v[3]);
+  } else if (e < nchain + nrec + nskip) {
+    const int f = e - nchain - nrec, wv = f / (FSK * 64), c = (f / 64) % FSK, ln = f % 64;
+    const int m = 128 * wv + 2 * ln + (c >= 8 ? 1 : 0);
+    for (int q = 0; q < 4; ++q) v[q] = skip[(size_t)m * R + 4 * (c & 7) + q];
+    ((float4 *)g.wskip)[(size_t)l * nskip + f] = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+__global__ void pack_head_kernel(const float *head, const float *out, ChainGatedArgs g) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= 2 * FH * NT) return;
+  // f = (wave, chunk, lane): row t = 64 wave + lane, columns 4 chunk .. 4 chunk + 3
+  const int which = e / (FH * NT), f = e % (FH * NT), wv = f / (FH * 64), c = (f / 64) % FH, t = 64 * wv + f % 64;
+  const float *src = which ? out : head;
+  float v[4];
+  for (int q = 0; q < 4; ++q) v[q] = src[(size_t)t * 256 + 4 * c + q];
+  ((float4 *)(which ? g.wout : g.whead))[f] = make_float4(v[0], v[1], v[2], v[3]);
+}
+__global__ void pack_vec_kernel(const float *src, float *dst, int n, int accumulate) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n) return;
+  const float v = src ? src[e] : 0.f;
+  dst[e] = accumulate ? dst[e] + v : v;
+}
+
+}  // namespace chg
+
+bool chain_gated_ok(int kind, int dtype, int C, int S, int H, int Q, int L, int w, size_t *img_bytes, size_t *lds) {
+  if (kind != 2 || dtype != 0 || C != kChainGR || S != kChainGS || H != kChainGS || Q != 256 || w != 2 || L < 1 ||
+      L > kChainGMaxLayers)
+    return false;
+  const ChainGatedArgs g = chain_gated_arrays(nullptr, L);
+  *img_bytes = (size_t)(uintptr_t)(g.embb + kChainGR);
+  *lds = chg::lds_floats(L) * 4;
+  return *lds <= 160 * 1024;
+}
+
+ChainGatedArgs chain_gated_arrays(void *base, int L) {
+  using namespace chg;
+  uintptr_t p = (uintptr_t)base;
+  auto take = [&](size_t bytes) {
+    const uintptr_t at = p;
+    p += (bytes + 255) & ~(size_t)255;
+    return at;
+  };
+  ChainGatedArgs g;
+  g.wchain = (const float4 *)take((size_t)L * FCH * 64 * 16);
+  g.wrec = (const float4 *)take((size_t)L * FREC * 64 * 16);
+  g.wskip = (const float4 *)take((size_t)L * 2 * FSK * 64 * 16);
+  g.whead = (const float4 *)take((size_t)FH * NT * 16);
+  g.wout = (const float4 *)take((size_t)FH * NT * 16);
+  g.convb = (const float *)take((size_t)L * 2 * R * 4);
+  g.resb = (const float *)take((size_t)L * R * 4);
+  g.skipb = (const float *)take((size_t)S * 4);
+  g.headb = (const float *)take((size_t)H * 4);
+  g.outb = (const float *)take((size_t)Q * 4);
+  g.embT = (const float *)take((size_t)Q * R * 4);
+  g.embb = (const float *)take((size_t)R * 4);
+  return g;
+}
+
+hipError_t set_chain_gated_lds_limit(size_t bytes) {
+  return hipFuncSetAttribute((const void *)chg::chain_gated_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)bytes);
+}
+
+hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s) {
+  hipLaunchKernelGGL(chg::chain_gated_kernel, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, const void *const *conv,
+                                   const float *const *conv_b, const void *const *res, const float *const *res_b,
+                                   const void *const *skip, const float *const *skip_b, const void *head,
+                                   const float *head_b, const void *out, const float *out_b, int L,
+                                   const ChainGatedArgs &g, hipStream_t s) {
+  using namespace chg;
+  const int n = FCH * 64 + FREC * 64 + 2 * FSK * 64;
+  for (int l = 0; l < L; ++l) {
+    hipLaunchKernelGGL(pack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const float *)conv[l],
+                       (const float *)res[l], (const float *)skip[l], l, g);
+    hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, conv_b ? conv_b[l] : nullptr,
+                       (float *)g.convb + (size_t)l * 2 * R, 2 * R, 0);
+    hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, res_b ? res_b[l] : nullptr,
+                       (float *)g.resb + (size_t)l * R, R, 0);
+    hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, skip_b ? skip_b[l] : nullptr, (float *)g.skipb, S,
+                       l > 0);
+  }
+  hipLaunchKernelGGL(pack_head_kernel, dim3((2 * FH * NT + 255) / 256), dim3(256), 0, s, (const float *)head,
+                     (const float *)out, g);
+  hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, head_b, (float *)g.headb, H, 0);
+  hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, out_b, (float *)g.outb, Q, 0);
+  hipLaunchKernelGGL(ch::chain_transpose_kernel, dim3((R * Q + 255) / 256), dim3(256), 0, s, (const float *)embed,
+                     (float *)g.embT, R, Q);
+  hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, embed_b, (float *)g.embb, R, 0);
+  return hipGetLastError();
+}
+
+}  // namespace fwg

@@ -78,6 +78,8 @@ struct Plan {
   // chain family: the weight image and the launch's LDS bytes
   ChainArgs chain;
   size_t off_chain, chain_lds;
+  // gated chain family: packed weights (bytes) and the launch's LDS bytes
+  size_t off_cg, cg_bytes, cg_lds;
   // wide family: packed weights and tables, the launch's LDS and exchange-region bytes
   WideArgs wide;
   size_t wide_lds, wide_comm;
@@ -266,6 +268,11 @@ int make_plan(const fwg_desc *d, Plan *p) {
   if (p->regime == REGIME_VALU && !forced_other &&
       chain_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, d->dilations, &p->chain, &p->chain_lds))
     p->regime = REGIME_CHAIN;
+  // float32 gated stacks with R = 32, S = H = 256: one block per stream, the layer chain on one
+  // wavefront, the recurrent halves, the skip sum and the head on the block's other waves
+  if (p->regime == REGIME_VALU && !forced_other &&
+      chain_gated_ok(p->kind, p->dtype, p->C, p->S, p->H, p->Q, p->L, w, &p->cg_bytes, &p->cg_lds))
+    p->regime = REGIME_CHAIN_GATED;
   // float32 ReLU stacks of 512 channels: each layer spread over a group of 32 blocks per XCD
   if (p->regime == REGIME_VALU && !forced_other &&
       wide_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, p->bmax, d->dilations, &p->wide, &p->wide_lds,
@@ -350,6 +357,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_last = take(sizeof(int32_t) * p->bmax);
   p->off_wave = p->regime == REGIME_WAVE ? take(sizeof(float) * (size_t)p->wave.image_floats) : 0;
   p->off_chain = p->regime == REGIME_CHAIN ? take(sizeof(float) * (size_t)p->chain.image_floats) : 0;
+  p->off_cg = p->regime == REGIME_CHAIN_GATED ? take(p->cg_bytes) : 0;
 
   // time-parallel path: every product's K must fill whole 128-byte k-tiles, and the gate's column
   // pairs come in groups of 16 channels
@@ -601,6 +609,8 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
       g.image = (const float *)(h->ws + p.off_chain);
       return launch_chain_step(a, g, p.chain_lds, h->stream);
     }
+    case REGIME_CHAIN_GATED:
+      return launch_chain_gated_step(a, chain_gated_arrays(h->ws + p.off_cg, p.L), p.cg_lds, h->stream);
     case REGIME_WAVE: {
       WaveArgs g = p.wave;
       g.image = (const float *)(h->ws + p.off_wave);
@@ -818,6 +828,12 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     TRY_OR_FREE(launch_chain_image(w->embed, w->embed_b, w->conv, w->conv_b, w->out, w->out_b, p.L, p.chain,
                                    (float *)(ws + p.off_chain), s));
     TRY_OR_FREE(set_chain_lds_limit(p.chain_lds));
+  }
+  if (p.regime == REGIME_CHAIN_GATED) {
+    TRY_OR_FREE(launch_chain_gated_pack(w->embed, w->embed_b, w->conv, w->conv_b, w->res, w->res_b, w->skip,
+                                        w->skip_b, w->head, w->head_b, w->out, w->out_b, p.L,
+                                        chain_gated_arrays(ws + p.off_cg, p.L), s));
+    TRY_OR_FREE(set_chain_gated_lds_limit(p.cg_lds));
   }
   if (p.regime == REGIME_WAVE) {
     const WaveArgs &g = p.wave;
@@ -1109,6 +1125,7 @@ const char *fwg_regime(const fwg_handle *h) {
     case REGIME_SPLIT: return "mfma_split_bf16_r64_s512";
     case REGIME_WAVE: return "wave";
     case REGIME_CHAIN: return "chain_f32_c32";
+    case REGIME_CHAIN_GATED: return "chain_gated_f32_r32";
     case REGIME_WIDE: return "wide_f32_c512";
     default: return "valu";
   }

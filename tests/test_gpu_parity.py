@@ -109,6 +109,9 @@ def first_divergence(olg, g, u, tau, label):
 FAMILIES = {
     "relu_c32_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8, 16)),
     "gated_r32_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
+    "gated_r32_f32_valu": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
+    # odd layer count, repeated and non-power-of-two dilations (the gated chain kernel's buffer swap)
+    "gated_r32_f32_odd": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 1, 7, 2), 256, 256),
     "gated_r64_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
@@ -133,12 +136,14 @@ FAMILIES = {
 WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_c32_f32_wave"}
 # families that must run on the chain kernels (float32 ReLU stacks with C = 32, width 2)
 CHAIN_FAMILIES = {"relu_c32_f32", "relures_c32_f32"}
+# families that must run on the gated chain kernel (float32 gated stacks with R = 32, S = H = 256)
+CHAIN_GATED_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd"}
 # families that must run on the wide kernels (float32 ReLU stacks with C = 512: each layer spread
 # over a group of 32 blocks)
 WIDE_FAMILIES = {"relures_c512_f32"}
 # families whose test forces the general (VALU) kernel family instead of the MFMA, wave, chain or
 # wide one
-FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu"}
+FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu", "gated_r32_f32_valu"}
 # families whose test forces the wave-per-stream family instead of the chain one
 FORCE_WAVE = {"relu_c32_f32_wave"}
 
@@ -180,13 +185,16 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
             split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
             assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
-            assert fw.regime in ("valu", "wave", "chain_f32_c32", "wide_f32_c512"), (fam, fw.regime)
+            assert fw.regime in ("valu", "wave", "chain_f32_c32", "chain_gated_f32_r32", "wide_f32_c512"), (
+                fam, fw.regime)
         if fam in WIDE_FAMILIES:
             assert fw.regime == "wide_f32_c512", (fam, fw.regime)
         if fam in WAVE_FAMILIES:
             assert fw.regime == "wave", (fam, fw.regime)
         if fam in CHAIN_FAMILIES:
             assert fw.regime == "chain_f32_c32", (fam, fw.regime)
+        if fam in CHAIN_GATED_FAMILIES:
+            assert fw.regime == "chain_gated_f32_r32", (fam, fw.regime)
     return w, fw, oracle.Oracle(w)
 
 
@@ -467,7 +475,7 @@ def test_delay_line_closed_form_gpu(fwidth, dil, path):
 
 @pytest.mark.parametrize("fam,B,regime", [("gated_r64_bf16", 16, "mfma_bf16_r64_s512"),
                                           ("gated_r64_bf16_split", 13, "mfma_split_bf16_r64_s512"),
-                                          ("gated_r32_f32", 5, None),
+                                          ("gated_r32_f32", 5, "chain_gated_f32_r32"),
                                           ("relu_c32_f32", 3, "chain_f32_c32")])
 def test_uniform_logits_sampler_gpu(fam, B, regime):
     """All-equal logits: the sample is floor(256 u), bit-exact, in both halves of the MFMA
@@ -615,12 +623,14 @@ def test_full_toy_relu():
 
 def test_full_gated_b1():
     wl, w, fw, orc = _full("gated_r32_s256_l20_b1")
+    assert fw.regime == "chain_gated_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     check_generation(wl.model, fw, orc, u, wl.batch, wl.name)
 
 
 def test_full_gated_b64():
     wl, w, fw, orc = _full("gated_r32_s256_l20_b64")
+    assert fw.regime == "chain_gated_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255
