@@ -29,13 +29,14 @@ hipError_t launch_chain_image(const void *embed, const float *embed_b, const voi
 namespace fwg {
 
 // Gated variant (fwg_chain.hip): float32 gated stacks with R = 32 residual channels, S = H = 256,
-// filter width 2, at most 64 layers: one block per stream, the weights streamed from the workspace
+// filter width 2 or 3, at most 64 layers: one block per stream, the weights streamed from the workspace
 // per step, the queues in the workspace.
 constexpr int kChainGR = 32, kChainGS = 256;
 constexpr int kChainGMaxLayers = 64;  // per-layer queue tables live in one lane each
+constexpr int kChainGMaxWidth = 3;    // filter widths 2 and 3
 struct ChainGatedArgs {
   const float4 *wchain;  // [L][12][64]: wave 0's W_e row chunks (8), then W_res half-row chunks (4)
-  const float4 *wrec;    // [L][8][64]: wave 1's W_r row chunks
+  const float4 *wrec;    // [L][8 (w - 1)][64]: wave 1's row chunks of the recurrent taps, oldest first
   const float4 *wskip;   // [L][2][16][64]: the skip waves' two rows each (8 chunks per row)
   const float4 *whead;   // [4][64][64]: row t = 64 w + l of the first head 1x1, chunk c at [w][c][l]
   const float4 *wout;    // [4][64][64]: row t of the output 1x1, the same way
@@ -49,12 +50,12 @@ struct ChainGatedArgs {
 bool chain_gated_ok(int kind, int dtype, int C, int S, int H, int Q, int L, int w, size_t *img_bytes, size_t *lds);
 hipError_t set_chain_gated_lds_limit(size_t bytes);
 // The arrays of ChainGatedArgs laid out from `base` (the workspace region of img_bytes).
-ChainGatedArgs chain_gated_arrays(void *base, int L);
+ChainGatedArgs chain_gated_arrays(void *base, int L, int w);
 hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s);
 hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, const void *const *conv,
                                    const float *const *conv_b, const void *const *res, const float *const *res_b,
                                    const void *const *skip, const float *const *skip_b, const void *head,
-                                   const float *head_b, const void *out, const float *out_b, int L,
+                                   const float *head_b, const void *out, const float *out_b, int L, int w,
                                    const ChainGatedArgs &g, hipStream_t s);
 
 }  // namespace fwg

@@ -342,14 +342,15 @@ hipError_t launch_chain_image(const void *embed, const float *embed_b, const voi
 // ---------------------------------------------------------------------------
 // Gated variant: float32 gated stacks with R = 32, S = H = 256 (the WaveNet-style unit: z =
 // tanh(a[0:R]) sigmoid(a[R:2R]), residual and skip 1x1s, the skip sum through relu -> 1x1 -> relu
-// -> 1x1 to the logits; Section 2.1, Fig. 2), at most 64 layers.  One block of four waves per stream:
+// -> 1x1 to the logits; Section 2.1, Fig. 2), at most 64 layers, filter width 2 or 3 (Section 3.1).
+// One block of four waves per stream:
 //  - wave 0 (the chain): lane o computes gate pre-activation o (tanh half for o < 32, sigmoid half
 //    for o >= 32) from the layer input broadcast through LDS; the halves meet with one cross-half
 //    lane swap, which leaves z in both halves; the residual 1x1 splits K over the half-waves.  It
 //    pushes each layer input to the layer's queue in the workspace and to an LDS row;
-//  - wave 1: W_r v + b of every layer for the next step: the pops of layers with d >= 2 (pushed at
-//    least one step earlier, before a block barrier) are read from the workspace queues, those of
-//    layers with d = 1 are this step's LDS rows (an LDS flag per layer);
+//  - wave 1: the recurrent taps of every layer's product for the next step (W_r v + b at width 2):
+//    states pushed at least one step earlier (before a block barrier) are read from the workspace
+//    queues; the newest tap of a layer with d = 1 is this step's LDS row (an LDS flag per layer);
 //  - waves 2, 3: the skip sum, two of the 256 skip channels per lane, each layer as soon as its z
 //    row is in LDS (an LDS flag per layer);
 //  - then all four waves compute the head, one hidden channel and then one class per thread, and
@@ -473,28 +474,36 @@ __device__ __forceinline__ void chain_gated_layer(const Lay &s, float4 (&Wc)[FCH
   x = x + s.resb[l * R + o] + ch::halves_sum(r0 + r1);
 }
 
-// Wave 1's layer l: W_r v + b for the next step, v = the state the layer pops then (qrow: a queue
-// row in the workspace, loaded before the next layer's weights so that its wait leaves them in
-// flight, or, with from_row, this step's LDS row of the layer once the chain has written it).
-__device__ __forceinline__ void rec_layer(const Lay &s, const float4 (&Wc)[FREC], float4 (&Wn)[FREC], Rsrc rw,
-                                          int next_off, const float *qrow, bool from_row, const float *convb, int l,
+// Wave 1's layer l: the recurrent taps of the dilated product for the next step, sum over k < W - 1
+// of W_k v_k + b, v_k = the state tap k reads then (x_{t+1-(W-1-k)d}, Section 3.1; W = 2: the one
+// popped state).  taps[k]: the state's queue row in the workspace, loaded before the next layer's
+// weights so that its wait leaves them in flight; with last_row, the newest tap (distance d = 1) is
+// this step's LDS row of the layer instead, read once the chain has written it.
+template <int W>
+__device__ __forceinline__ void rec_layer(const Lay &s, const float4 (&Wc)[FREC * (W - 1)],
+                                          float4 (&Wn)[FREC * (W - 1)], Rsrc rw, int next_off,
+                                          const float *const (&taps)[W - 1], bool last_row, const float *convb, int l,
                                           int L, int np, int step, int lane) {
-  float4 vv[FREC];
-  if (!from_row) {
+  constexpr int F = FREC * (W - 1);
+  float4 vv[F];
 #pragma unroll
-    for (int c = 0; c < FREC; ++c) vv[c] = ((const float4 *)qrow)[c];
+  for (int k = 0; k < W - 1; ++k) {
+    if (k + 2 < W || !last_row) {
+#pragma unroll
+      for (int c = 0; c < FREC; ++c) vv[FREC * k + c] = ((const float4 *)taps[k])[c];
+    }
   }
   load_chunks(Wn, rw, lane * 16, next_off, 1024);
-  if (from_row) {
-    // the state popped next step is this step's input of the layer
+  if (last_row) {
+    // the newest state tapped next step is this step's input of the layer
     wait_flag(s, s.fx + l, step + 1);
     const float4 *x4 = (const float4 *)(s.xrow + l * R);
 #pragma unroll
-    for (int c = 0; c < FREC; ++c) vv[c] = x4[c];
+    for (int c = 0; c < FREC; ++c) vv[FREC * (W - 2) + c] = x4[c];
   }
   float a0 = convb[l * 2 * R + lane], a1 = 0.f;
 #pragma unroll
-  for (int c = 0; c < FREC; ++c) {
+  for (int c = 0; c < F; ++c) {
     a0 = fmaf(Wc[c].x, vv[c].x, a0);
     a1 = fmaf(Wc[c].y, vv[c].y, a1);
     a0 = fmaf(Wc[c].z, vv[c].z, a0);
@@ -556,7 +565,9 @@ __device__ __forceinline__ float head_row(float4 (&HA)[FHR], float4 (&HB)[FHR], 
   return a0 + a1;
 }
 
+template <int W>
 __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedArgs g) {
+  constexpr int FR = FREC * (W - 1);  // wave 1's weight chunks per layer
   extern __shared__ float4 lds4[];
   float *lds = (float *)lds4;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -593,36 +604,44 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
       s.fin[j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
     }
   }
-  // lane l: layer l's queue (element offset of this stream's row in slot 0), dilation and the slot
-  // of the current step (wave 1 keeps the slot of the next step)
+  // lane l: layer l's queue (element offset of this stream's row in slot 0), dilation d, depth
+  // (W - 1) d and the slot of the current step, t mod depth (wave 1 keeps the slot of the next
+  // step); at slot t mod depth the queue holds x_{t-(W-1)d}, and tap k reads the state k d slots on
   const long long slot_stride = (long long)a.bmax * R;
   long long qoff = 0;
-  int qdil = 1, qslot = 0;
+  int qdil = 1, qdep = W - 1, qslot = 0;
   if (lane < L) {
     const LayerDev ld = a.layers[lane];
     qoff = ld.ring_off + (long long)b * R;
     qdil = ld.dil;
-    qslot = (int)(a.t0 % (long long)qdil);
+    qdep = ld.depth;
+    qslot = (int)(a.t0 % (long long)qdep);
   }
   float *ring = (float *)a.ring;
-  // W_r v + b of every layer for step 0 (wave 1; every pop of step 0 was pushed before the launch)
+  // the recurrent taps of every layer for step 0 (wave 1; every state they read was pushed before
+  // the launch)
   if (wave == 1) {
     for (int l = 0; l < L; ++l) {
-      const float *v = ring + lane_i64(qoff + qslot * slot_stride, l);
-      const float4 *w = g.wrec + (size_t)l * FREC * 64 + lane;
+      const float4 *w = g.wrec + (size_t)l * FR * 64 + lane;
       float acc = g.convb[l * 2 * R + lane];
 #pragma unroll
-      for (int c = 0; c < FREC; ++c) {
-        const float4 wv = w[c * 64];
-        const float4 vv = *(const float4 *)(v + 4 * c);
-        acc = fmaf(wv.x, vv.x, acc);
-        acc = fmaf(wv.y, vv.y, acc);
-        acc = fmaf(wv.z, vv.z, acc);
-        acc = fmaf(wv.w, vv.w, acc);
+      for (int k = 0; k < W - 1; ++k) {
+        int sk = qslot + k * qdil;
+        sk = sk >= qdep ? sk - qdep : sk;
+        const float *v = ring + lane_i64(qoff + sk * slot_stride, l);
+#pragma unroll
+        for (int c = 0; c < FREC; ++c) {
+          const float4 wv = w[(FREC * k + c) * 64];
+          const float4 vv = *(const float4 *)(v + 4 * c);
+          acc = fmaf(wv.x, vv.x, acc);
+          acc = fmaf(wv.y, vv.y, acc);
+          acc = fmaf(wv.z, vv.z, acc);
+          acc = fmaf(wv.w, vv.w, acc);
+        }
       }
       s.P[l * 2 * R + lane] = acc;
     }
-    qslot = qslot + 1 == qdil ? 0 : qslot + 1;  // wave 1 works one step ahead
+    qslot = qslot + 1 == qdep ? 0 : qslot + 1;  // wave 1 works one step ahead
   }
   __syncthreads();
 
@@ -660,7 +679,7 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
 #pragma unroll
         for (int c = 0; c < FCH; ++c) WA[c] = WB[c];
       }
-      qslot = qslot + 1 == qdil ? 0 : qslot + 1;
+      qslot = qslot + 1 == qdep ? 0 : qslot + 1;
       load_chunks(HA, rw, hvoff, o_head, 1024);
       __syncthreads();  // the skip sum is in LDS
       const float hv = head_row(HA, HB, rw, hvoff, o_head, s.srow, hbias);
@@ -682,31 +701,43 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
     }
     if (lane == 0 && a.mode != MODE_TEACHER) a.last[b] = in;
   } else if (wave == 1) {
-    // ---------------- W_r v + b for the next step, staging, its share of the head
-    const int lstr = FREC * 1024;
-    float4 WA[FREC], WB[FREC];
+    // ---------------- the recurrent taps for the next step, staging, its share of the head
+    const int lstr = FR * 1024;
+    float4 WA[FR], WB[FR];
     load_chunks(WA, rw, lane * 16, o_rec, 1024);
     for (int step = 0; step < a.n_steps; ++step) {
       const int np = (step & 1) ^ 1;
+      // lane l: the queue rows layer l's taps read next step
+      long long toff[W - 1];
+#pragma unroll
+      for (int k = 0; k < W - 1; ++k) {
+        int sk = qslot + k * qdil;
+        sk = sk >= qdep ? sk - qdep : sk;
+        toff[k] = qoff + sk * slot_stride;
+      }
       for (int l = 0; l < L; l += 2) {
         {
-          const int d = __builtin_amdgcn_readlane(qdil, l);
-          const float *v = ring + lane_i64(qoff + qslot * slot_stride, l);
+          const float *taps[W - 1];
+#pragma unroll
+          for (int k = 0; k < W - 1; ++k) taps[k] = ring + lane_i64(toff[k], l);
           const int ln = l + 1 < L ? l + 1 : 0;
-          rec_layer(s, WA, WB, rw, o_rec + ln * lstr, v, d == 1, g.convb, l, L, np, step, lane);
+          rec_layer<W>(s, WA, WB, rw, o_rec + ln * lstr, taps, __builtin_amdgcn_readlane(qdil, l) == 1, g.convb, l,
+                       L, np, step, lane);
         }
         if (l + 1 < L) {
-          const int d = __builtin_amdgcn_readlane(qdil, l + 1);
-          const float *v = ring + lane_i64(qoff + qslot * slot_stride, l + 1);
+          const float *taps[W - 1];
+#pragma unroll
+          for (int k = 0; k < W - 1; ++k) taps[k] = ring + lane_i64(toff[k], l + 1);
           const int ln = l + 2 < L ? l + 2 : 0;
-          rec_layer(s, WB, WA, rw, o_rec + ln * lstr, v, d == 1, g.convb, l + 1, L, np, step, lane);
+          rec_layer<W>(s, WB, WA, rw, o_rec + ln * lstr, taps, __builtin_amdgcn_readlane(qdil, l + 1) == 1,
+                       g.convb, l + 1, L, np, step, lane);
         }
       }
       if (L & 1) {
 #pragma unroll
-        for (int c = 0; c < FREC; ++c) WA[c] = WB[c];
+        for (int c = 0; c < FR; ++c) WA[c] = WB[c];
       }
-      qslot = qslot + 1 == qdil ? 0 : qslot + 1;
+      qslot = qslot + 1 == qdep ? 0 : qslot + 1;
       // staging of the next chunk of per-step inputs, one chunk ahead
       if (step % KCH == 0) {
         const int base = step + KCH, buf = (step / KCH + 1) & 1;
@@ -768,20 +799,22 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
 }
 
 // ---- packing (once per fwg_create)
-__global__ void pack_layer_kernel(const float *conv, const float *res, const float *skip, int l, ChainGatedArgs g) {
+__global__ void pack_layer_kernel(const float *conv, const float *res, const float *skip, int l, int w,
+                                  ChainGatedArgs g) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  const int nchain = FCH * 64, nrec = FREC * 64, nskip = 2 * FSK * 64;
+  const int nchain = FCH * 64, nrec = FREC * (w - 1) * 64, nskip = 2 * FSK * 64;
   float v[4];
   if (e < nchain) {
     const int c = e / 64, ln = e % 64;
     for (int q = 0; q < 4; ++q) {
-      if (c < 8) v[q] = conv[((size_t)ln * R + 4 * c + q) * 2 + 1];               // W_e[ln][k] (current-input tap)
+      if (c < 8) v[q] = conv[((size_t)ln * R + 4 * c + q) * w + w - 1];           // W_e[ln][k] (current-input tap)
       else v[q] = res[(size_t)(ln % R) * R + 16 * (ln / R) + 4 * (c - 8) + q];    // W_res row, this lane's half
     }
     ((float4 *)g.wchain)[(size_t)l * nchain + e] = make_float4(v[0], v[1], v[2], v[3]);
   } else if (e < nchain + nrec) {
-    const int f = e - nchain, c = f / 64, ln = f % 64;
-    for (int q = 0; q < 4; ++q) v[q] = conv[((size_t)ln * R + 4 * c + q) * 2];   // W_r[ln][k] (popped tap)
+    // recurrent tap t = c / 8 (t = 0: the oldest state), columns 4 (c mod 8) ..
+    const int f = e - nchain, c = f / 64, ln = f % 64, t = c / FREC, cc = c % FREC;
+    for (int q = 0; q < 4; ++q) v[q] = conv[((size_t)ln * R + 4 * cc + q) * w + t];
     ((float4 *)g.wrec)[(size_t)l * nrec + f] = make_float4(v[0], v[1], v[2], v[3]);
   } else if (e < nchain + nrec + nskip) {
     const int f = e - nchain - nrec, wv = f / (FSK * 64), c = (f / 64) % FSK, ln = f % 64;
@@ -810,16 +843,16 @@ __global__ void pack_vec_kernel(const float *src, float *dst, int n, int accumul
 }  // namespace chg
 
 bool chain_gated_ok(int kind, int dtype, int C, int S, int H, int Q, int L, int w, size_t *img_bytes, size_t *lds) {
-  if (kind != 2 || dtype != 0 || C != kChainGR || S != kChainGS || H != kChainGS || Q != 256 || w != 2 || L < 1 ||
-      L > kChainGMaxLayers)
+  if (kind != 2 || dtype != 0 || C != kChainGR || S != kChainGS || H != kChainGS || Q != 256 || w < 2 ||
+      w > kChainGMaxWidth || L < 1 || L > kChainGMaxLayers)
     return false;
-  const ChainGatedArgs g = chain_gated_arrays(nullptr, L);
+  const ChainGatedArgs g = chain_gated_arrays(nullptr, L, w);
   *img_bytes = (size_t)(uintptr_t)(g.embb + kChainGR);
   *lds = chg::lds_floats(L) * 4;
   return *lds <= 160 * 1024;
 }
 
-ChainGatedArgs chain_gated_arrays(void *base, int L) {
+ChainGatedArgs chain_gated_arrays(void *base, int L, int w) {
   using namespace chg;
   uintptr_t p = (uintptr_t)base;
   auto take = [&](size_t bytes) {
@@ -829,7 +862,7 @@ ChainGatedArgs chain_gated_arrays(void *base, int L) {
   };
   ChainGatedArgs g;
   g.wchain = (const float4 *)take((size_t)L * FCH * 64 * 16);
-  g.wrec = (const float4 *)take((size_t)L * FREC * 64 * 16);
+  g.wrec = (const float4 *)take((size_t)L * FREC * (w - 1) * 64 * 16);
   g.wskip = (const float4 *)take((size_t)L * 2 * FSK * 64 * 16);
   g.whead = (const float4 *)take((size_t)FH * NT * 16);
   g.wout = (const float4 *)take((size_t)FH * NT * 16);
@@ -843,26 +876,31 @@ ChainGatedArgs chain_gated_arrays(void *base, int L) {
   return g;
 }
 
+static_assert(kChainGMaxWidth == 3, "the launcher instantiates filter widths 2 and 3");
 hipError_t set_chain_gated_lds_limit(size_t bytes) {
-  return hipFuncSetAttribute((const void *)chg::chain_gated_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+  hipError_t e = hipFuncSetAttribute((const void *)chg::chain_gated_kernel<2>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void *)chg::chain_gated_kernel<3>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)bytes);
 }
 
 hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s) {
-  hipLaunchKernelGGL(chg::chain_gated_kernel, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
+  if (a.w == 3) hipLaunchKernelGGL(chg::chain_gated_kernel<3>, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
+  else hipLaunchKernelGGL(chg::chain_gated_kernel<2>, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
   return hipGetLastError();
 }
 
 hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, const void *const *conv,
                                    const float *const *conv_b, const void *const *res, const float *const *res_b,
                                    const void *const *skip, const float *const *skip_b, const void *head,
-                                   const float *head_b, const void *out, const float *out_b, int L,
+                                   const float *head_b, const void *out, const float *out_b, int L, int w,
                                    const ChainGatedArgs &g, hipStream_t s) {
   using namespace chg;
-  const int n = FCH * 64 + FREC * 64 + 2 * FSK * 64;
+  const int n = FCH * 64 + FREC * (w - 1) * 64 + 2 * FSK * 64;
   for (int l = 0; l < L; ++l) {
     hipLaunchKernelGGL(pack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const float *)conv[l],
-                       (const float *)res[l], (const float *)skip[l], l, g);
+                       (const float *)res[l], (const float *)skip[l], l, w, g);
     hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, conv_b ? conv_b[l] : nullptr,
                        (float *)g.convb + (size_t)l * 2 * R, 2 * R, 0);
     hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, res_b ? res_b[l] : nullptr,

@@ -268,7 +268,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   if (p->regime == REGIME_VALU && !forced_other &&
       chain_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, d->dilations, &p->chain, &p->chain_lds))
     p->regime = REGIME_CHAIN;
-  // float32 gated stacks with R = 32, S = H = 256: one block per stream, the layer chain on one
+  // float32 gated stacks with R = 32, S = H = 256, width 2 or 3: one block per stream, the layer chain on one
   // wavefront, the recurrent halves, the skip sum and the head on the block's other waves
   if (p->regime == REGIME_VALU && !forced_other &&
       chain_gated_ok(p->kind, p->dtype, p->C, p->S, p->H, p->Q, p->L, w, &p->cg_bytes, &p->cg_lds))
@@ -610,7 +610,7 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
       return launch_chain_step(a, g, p.chain_lds, h->stream);
     }
     case REGIME_CHAIN_GATED:
-      return launch_chain_gated_step(a, chain_gated_arrays(h->ws + p.off_cg, p.L), p.cg_lds, h->stream);
+      return launch_chain_gated_step(a, chain_gated_arrays(h->ws + p.off_cg, p.L, p.w), p.cg_lds, h->stream);
     case REGIME_WAVE: {
       WaveArgs g = p.wave;
       g.image = (const float *)(h->ws + p.off_wave);
@@ -831,8 +831,8 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   }
   if (p.regime == REGIME_CHAIN_GATED) {
     TRY_OR_FREE(launch_chain_gated_pack(w->embed, w->embed_b, w->conv, w->conv_b, w->res, w->res_b, w->skip,
-                                        w->skip_b, w->head, w->head_b, w->out, w->out_b, p.L,
-                                        chain_gated_arrays(ws + p.off_cg, p.L), s));
+                                        w->skip_b, w->head, w->head_b, w->out, w->out_b, p.L, p.w,
+                                        chain_gated_arrays(ws + p.off_cg, p.L, p.w), s));
     TRY_OR_FREE(set_chain_gated_lds_limit(p.cg_lds));
   }
   if (p.regime == REGIME_WAVE) {

@@ -122,6 +122,7 @@ FAMILIES = {
     # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
     "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
     "gated_r32_w3_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
+    "gated_r32_w3_f32_valu": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r64_w3_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
     "relures_c64_w4_bf16": W.ModelConfig(W.RELU_RESIDUAL, W.BF16, 64, (1, 4, 16, 2), filter_width=4),
     # small enough for the wave-per-stream kernels (every weight in LDS)
@@ -137,13 +138,14 @@ WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_
 # families that must run on the chain kernels (float32 ReLU stacks with C = 32, width 2)
 CHAIN_FAMILIES = {"relu_c32_f32", "relures_c32_f32"}
 # families that must run on the gated chain kernel (float32 gated stacks with R = 32, S = H = 256)
-CHAIN_GATED_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd"}
+CHAIN_GATED_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd", "gated_r32_w3_f32"}
 # families that must run on the wide kernels (float32 ReLU stacks with C = 512: each layer spread
 # over a group of 32 blocks)
 WIDE_FAMILIES = {"relures_c512_f32"}
 # families whose test forces the general (VALU) kernel family instead of the MFMA, wave, chain or
 # wide one
-FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu", "gated_r32_f32_valu"}
+FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu", "gated_r32_f32_valu",
+              "gated_r32_w3_f32_valu"}
 # families whose test forces the wave-per-stream family instead of the chain one
 FORCE_WAVE = {"relu_c32_f32_wave"}
 
@@ -669,6 +671,7 @@ def test_full_gated_w3():
     """The filter-width-3 workload at full size (64 streams x 8,000 steps): sampled streams checked
     by the oracle over every step."""
     wl, w, fw, orc = _full("gated_r32_s256_w3_l14_b64")
+    assert fw.regime == "chain_gated_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255
