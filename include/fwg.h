@@ -155,14 +155,16 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
 
 /* fwg_generate for callers that cannot allocate device memory, e.g. code under
  * HIP graph capture, tight serving loops, or harnesses that forbid hipMalloc.
- * Same arguments, state, results and errors as fwg_generate.  The split
- * kernel family (fwg_regime "mfma_split_bf16_r64_s512") keeps the words its
- * cooperating blocks exchange during a launch in a static device array of
- * 4 MiB (one per device, set up by fwg_create and held until the process ends)
- * instead of the workspace; a batch whose words do not fit (more than
- * 4 MiB / (8 x (512 L + 8544)) groups of 16 streams, about 21 groups at
- * L = 30) returns FWG_ENOSPACE before anything is enqueued.  The other kernel
- * families use no per-launch scratch and run exactly as fwg_generate.  The
+ * Same arguments, state, results and errors as fwg_generate.  The kernel
+ * families whose blocks cooperate within a launch (fwg_regime
+ * "mfma_split_bf16_r64_s512" and "wide_f32_c512") keep the words they exchange
+ * in a static device array of 4 MiB (one per device, set up by fwg_create and
+ * held until the process ends) instead of the workspace; a batch whose words
+ * do not fit (split family: more than 4 MiB / (8 x (512 L + 8544)) groups of
+ * 16 streams, about 21 groups at L = 30; wide family: 256 + 8 x (16,384 L +
+ * 17,664) bytes whatever the batch, so L <= 30) returns FWG_ENOSPACE before
+ * anything is enqueued.  The other kernel families use no per-launch scratch
+ * and run exactly as fwg_generate.  The
  * array is cleared by a fill kernel at the start of every launch, but every
  * call on a device shares it: calls of this entry point that overlap on one
  * device (other streams, other handles, other threads) race and must be
