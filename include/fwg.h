@@ -205,8 +205,9 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
  * chunks of steps, the states before a chunk read from the layer's queue.
  * fwg_teacher_forced_parallel has the contract and results of
  * fwg_teacher_forced (queues of its own, from zero; generation state untouched);
- * only the order of the float32 sums differs.  FWG_EUNSUPPORTED when the model's
- * products do not fill whole 128-byte k-tiles. */
+ * only the order of the float32 sums differs.  Models whose products do not
+ * fill whole 128-byte k-tiles (K of 16 float32 or 32 bf16 values) have no
+ * time-parallel kernels: for them this call runs fwg_teacher_forced itself. */
 int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits);
 
 /* Priming from a prefix, time-parallel: the contract of fwg_step_forced
@@ -214,7 +215,8 @@ int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, c
  * evaluated like fwg_teacher_forced_parallel.  After each layer of a chunk the
  * chunk's newest (w-1) d_l states replace the queue's contents, so the queues
  * end in the state the step-by-step loop would leave and generation continues
- * from the prefix.  FWG_EUNSUPPORTED as fwg_teacher_forced_parallel. */
+ * from the prefix.  Where fwg_teacher_forced_parallel runs the step kernels,
+ * so does this call (fwg_step_forced itself). */
 int fwg_prime(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits);
 
 /* Naive generation, the baseline the paper measures against (Section 1, Fig. 1;

@@ -158,7 +158,7 @@ class FastWavenet:
         self.handle = h
         # kernel families whose launches wait on each other's blocks: a wait that ran out leaves
         # invalid outputs and a sticky device mark, which the calls below check by default
-        self._waits = self.regime.startswith("mfma_split") or self.regime.startswith("wide")
+        self._waits = self.regime.startswith(("mfma_split", "wide", "chain_pair"))
 
     def _after(self, check: bool):
         if check and self._waits:

@@ -40,7 +40,8 @@ struct ChainGatedArgs {
   const float4 *wskip;   // [L][2][16][64]: the skip waves' two rows each (8 chunks per row)
   const float4 *whead;   // [4][64][64]: row t = 64 w + l of the first head 1x1, chunk c at [w][c][l]
   const float4 *wout;    // [4][64][64]: row t of the output 1x1, the same way
-  const float *convb;    // [L][64]
+  const float4 *wm;      // pair variant: [L][8][64], slot l: rows of W_e^l W_res^{l-1} (slot 0 unused)
+  const float *convb;    // [L][64] (pair variant: + W_e^l b_res^{l-1})
   const float *resb;     // [L][32]
   const float *skipb;    // [256]: the skip biases summed over the layers
   const float *headb, *outb;  // [256] each
@@ -55,7 +56,16 @@ hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, s
 hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, const void *const *conv,
                                    const float *const *conv_b, const void *const *res, const float *const *res_b,
                                    const void *const *skip, const float *const *skip_b, const void *head,
-                                   const float *head_b, const void *out, const float *out_b, int L, int w,
+                                   const float *head_b, const void *out, const float *out_b, int L, int w, bool pair,
                                    const ChainGatedArgs &g, hipStream_t s);
+// Pair variant (two blocks of one XCD per stream, exchanging tagged words; pack with pair = true):
+// LDS bytes of a launch, exchange-region bytes for `batch` streams (zeroed before every launch;
+// an abort word, then 736 + 32 L words per stream), grid blocks, set-up (LDS limit; whether every
+// block of a launch of bmax streams can be resident at once) and launch (a.sp_comm, a.sp_sticky).
+size_t chain_pair_lds_bytes(int L);
+size_t chain_pair_comm_bytes(int L, int batch);
+int chain_pair_grid(int batch);
+hipError_t chain_pair_setup(size_t lds, int bmax, int *coresident_ok);
+hipError_t launch_chain_pair_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s);
 
 }  // namespace fwg

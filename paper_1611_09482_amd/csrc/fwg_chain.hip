@@ -20,9 +20,12 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "fwg_chain.h"
 #include "fwg_internal.h"
 #include "fwg_sample.h"
+#include "fwg_xchg.h"
 
 namespace fwg {
 namespace ch {
@@ -363,6 +366,7 @@ namespace chg {
 
 constexpr int R = kChainGR, S = kChainGS, H = kChainGS, Q = 256, NT = 256, KCH = 64;
 constexpr int FCH = 12, FREC = 8, FSK = 16, FH = 64, FHR = 8;  // float4 chunks per lane (FHR: per head round)
+constexpr int FZ = R / 4;  // float4 chunks of one 32-wide row
 constexpr int SPIN_MAX = 1 << 20;
 
 // Flags in LDS, addressed as LDS: through a generic pointer a volatile access stays a flat access,
@@ -384,6 +388,26 @@ struct Lay {
 __host__ __device__ inline size_t lds_floats(int L) {
   return (size_t)Q * R + R + 2ull * L * 2 * R + 3ull * L * R + S + H + Q + 2 * KCH + 2 * KCH + 2ull * L + 4;
 }
+// offset (in 4-byte words) of the flags
+__host__ __device__ inline int lay_flag_off(int L) { return Q * R + R + 2 * L * 2 * R + 3 * L * R + S + H + Q + 4 * KCH; }
+__device__ __forceinline__ Lay make_lay(float *lds, int L) {
+  Lay s;
+  s.embT = lds;
+  s.embb = s.embT + Q * R;
+  s.P = s.embb + R;
+  s.xrow = s.P + 2 * L * 2 * R;
+  s.zrow = s.xrow + L * R;
+  s.resb = s.zrow + L * R;
+  s.srow = s.resb + L * R;
+  s.hrow = s.srow + S;
+  s.lrow = s.hrow + H;
+  s.u = s.lrow + Q;
+  s.fin = (int *)(s.u + 2 * KCH);
+  s.fx = (lds_flag *)(lds + lay_flag_off(L));
+  s.fz = s.fx + L;
+  s.abort_ = s.fz + L;
+  return s;
+}
 
 // Weight streams are read as raw buffer loads from one resource over the packed weights: the
 // per-lane part of the address is one constant VGPR offset and the per-chunk part an SGPR offset,
@@ -404,7 +428,8 @@ __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory")
 
 // Waits until flag == want, at most SPIN_MAX polls (the chain wave sets every flag of a step
 // unconditionally; the bound only keeps a fault from turning into a hang).
-__device__ __forceinline__ void wait_flag(const Lay &s, lds_flag *flag, int want) {
+template <class S>
+__device__ __forceinline__ void wait_flag(const S &s, lds_flag *flag, int want) {
   for (int it = 0; *flag != want; ++it) {
     if (it >= SPIN_MAX || *s.abort_) {
       *s.abort_ = 1;
@@ -431,9 +456,11 @@ __device__ __forceinline__ long long lane_i64(long long v, int l) {
 // The chain wave's layer l with its weights in Wc (W_e row chunks, then W_res half-row chunks); the
 // next layer's weights are fetched into Wn first.  x: the layer input in (lane o and o + 32 both
 // hold channel o), the layer output out.  qptr: this step's push address of the layer's queue.
+// zw (pair variant): z of the layer also goes out as 32 tagged words zw[32 l + o].
 __device__ __forceinline__ void chain_gated_layer(const Lay &s, float4 (&Wc)[FCH], float4 (&Wn)[FCH], Rsrc rw,
                                                   int next_off, float *qptr, int l, int L, int par, int step,
-                                                  int lane, float &x) {
+                                                  int lane, float &x, xg::u64 *zw = nullptr,
+                                                  bool local = false) {
   const int o = lane & (R - 1), h = lane >> 5;
   if (lane < R) {
     qptr[o] = x;
@@ -460,6 +487,7 @@ __device__ __forceinline__ void chain_gated_layer(const Lay &s, float4 (&Wc)[FCH
   if (lane < R) s.zrow[l * R + o] = z;
   compiler_fence();
   if (lane == 0) s.fz[l] = step + 1;
+  if (zw != nullptr && lane < R) xg::put_word(zw + l * R + o, __builtin_bit_cast(uint32_t, z), step + 1, local);
   // the residual 1x1 over this half of K, z read back from its row
   const float4 *zr4 = (const float4 *)(s.zrow + l * R + 16 * h);
   float r0 = 0.f, r1 = 0.f;
@@ -479,8 +507,8 @@ __device__ __forceinline__ void chain_gated_layer(const Lay &s, float4 (&Wc)[FCH
 // popped state).  taps[k]: the state's queue row in the workspace, loaded before the next layer's
 // weights so that its wait leaves them in flight; with last_row, the newest tap (distance d = 1) is
 // this step's LDS row of the layer instead, read once the chain has written it.
-template <int W>
-__device__ __forceinline__ void rec_layer(const Lay &s, const float4 (&Wc)[FREC * (W - 1)],
+template <int W, class S>
+__device__ __forceinline__ void rec_layer(const S &s, const float4 (&Wc)[FREC * (W - 1)],
                                           float4 (&Wn)[FREC * (W - 1)], Rsrc rw, int next_off,
                                           const float *const (&taps)[W - 1], bool last_row, const float *convb, int l,
                                           int L, int np, int step, int lane) {
@@ -572,21 +600,7 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
   float *lds = (float *)lds4;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = blockIdx.x, L = a.L;
-  Lay s;
-  s.embT = lds;
-  s.embb = s.embT + Q * R;
-  s.P = s.embb + R;
-  s.xrow = s.P + 2 * L * 2 * R;
-  s.zrow = s.xrow + L * R;
-  s.resb = s.zrow + L * R;
-  s.srow = s.resb + L * R;
-  s.hrow = s.srow + S;
-  s.lrow = s.hrow + H;
-  s.u = s.lrow + Q;
-  s.fin = (int *)(s.u + 2 * KCH);
-  s.fx = (lds_flag *)(s.fin + 2 * KCH);
-  s.fz = s.fx + L;
-  s.abort_ = s.fz + L;
+  const Lay s = make_lay(lds, L);
 
   // ---- launch: tables into LDS, flags, the first chunk of per-step inputs
   for (int i = tid; i < Q * R / 4; i += NT) ((float4 *)s.embT)[i] = ((const float4 *)g.embT)[i];
@@ -798,8 +812,491 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
   }
 }
 
+// ---------------------------------------------------------------------------
+// Pair variant: the step of a stream on two blocks of one XCD, with the layer recurrence taken one
+// layer ahead so that a single 32-wide product lies between consecutive gates.
+//
+// With x^l the input of layer l, z^l its gate output and x^{l+1} = x^l + W_res^l z^l + b_res^l, the
+// gate pre-activation of layer l + 1 is
+//   a^{l+1} = [W_r v + b + W_e^{l+1} b_res^l] + W_e^{l+1} x^l + (W_e^{l+1} W_res^l) z^l,
+// the same sum regrouped (float32, products of the layer's weights formed once per fwg_create in
+// float64).  The first bracket is the recurrent part (its constant folded into the bias), the
+// second is known once x^l is, a layer before z^l; only M^l z^l (M^l = W_e^{l+1} W_res^l, 64 x 32)
+// waits for the gate of layer l.
+//
+// Chain block (h = 0), four waves:
+//  - wave 0, the gates: a^l = P^l + U^l + M^{l-1} z^{l-1} (z^{l-1} broadcast from its LDS row), the
+//    gate, z^l to LDS (+ flag) and to the helper as 32 tagged words;
+//  - wave 1, the residual stream: x^0 from the embedding, then x^{l+1} = x^l + W_res^l z^l + b_res^l
+//    (K split over the half-waves), each layer input to LDS (+ flag) and pushed to its queue;
+//  - wave 2: the recurrent taps of every layer for the next step (as in the one-block kernel) and
+//    the staging of per-step inputs;
+//  - wave 3: U^l = W_e^l x^{l-1} (x^0 for l = 0), to LDS (+ flag).
+// Helper block (h = 1): the skip sum, 64 channels per wave (wave 0 also receives the z words into
+// its LDS row).  Head, both blocks, with each thread's weights resident in registers for the launch
+// (one K half of one row of each head 1x1): the helper publishes relu(skip sum), both compute half of
+// the hidden channels and exchange them, then half of the classes; in generation the helper
+// publishes its logits and the chain block samples.
+//
+// Hand-offs are the tagged words of fwg_xchg.h (tag = step index in the launch + 1; zeroed before
+// every launch).  No block overwrites a word before the other has read it: each block's next write
+// of a word depends, through the step's hand-offs, on the other's read of the previous one.  Block i
+// of the launch: XCD slot i mod 8, pair (i / 16) 8 + i mod 8, role (i / 8) mod 2, so a pair's blocks
+// i and i + 8 share an XCD under round-robin dispatch (a launch handshake checks; words go through
+// memory when they do not).
+
+constexpr int PH = FH / 2;  // head chunks per thread (one K half of a 256-wide row)
+__host__ __device__ inline size_t pair_words(int L) { return 736 + (size_t)32 * L; }
+constexpr int PW_HS = 0, PW_Z = 96;  // handshake slots (chain block, helper, mode: 32 words each), z rows
+__host__ __device__ inline int pw_s(int L) { return 96 + 32 * L; }                // 256: relu(skip sum)
+__host__ __device__ inline int pw_h(int L, int h) { return 96 + 32 * L + 256 + 128 * h; }
+__host__ __device__ inline int pw_l(int L) { return 96 + 32 * L + 512; }           // the helper's logits
+
+// LDS of the pair variant (in 4-byte words): embedding table and bias, P [2][L][64], U [L][64],
+// xrow, zrow, resb [L][32], srow, hrow, lrow, part [256], u, fin [2][KCH], flags.
+struct PL {
+  float *embT, *embb, *P, *U, *xrow, *zrow, *resb, *srow, *hrow, *lrow, *part, *u;
+  int *fin;
+  lds_flag *fx, *fz, *fu;  // [L]: step + 1 once x^l / z^l / U^l of the step is in LDS
+  lds_flag *abort_, *mode, *inval;
+};
+__host__ __device__ inline int pl_flag_off(int L) {
+  return Q * R + R + 2 * L * 2 * R + L * 2 * R + 3 * L * R + 4 * 256 + 4 * KCH;
+}
+__host__ __device__ inline size_t pair_lds_floats(int L) { return (size_t)pl_flag_off(L) + 3 * L + 8; }
+__device__ __forceinline__ PL make_pl(float *lds, int L) {
+  PL s;
+  s.embT = lds;
+  s.embb = s.embT + Q * R;
+  s.P = s.embb + R;
+  s.U = s.P + 2 * L * 2 * R;
+  s.xrow = s.U + L * 2 * R;
+  s.zrow = s.xrow + L * R;
+  s.resb = s.zrow + L * R;
+  s.srow = s.resb + L * R;
+  s.hrow = s.srow + 256;
+  s.lrow = s.hrow + 256;
+  s.part = s.lrow + 256;
+  s.u = s.part + 256;
+  s.fin = (int *)(s.u + 2 * KCH);
+  s.fx = (lds_flag *)(lds + pl_flag_off(L));
+  s.fz = s.fx + L;
+  s.fu = s.fz + L;
+  s.abort_ = s.fu + L;
+  s.mode = s.abort_ + 1;
+  s.inval = s.abort_ + 2;
+  return s;
+}
+
+// 32-wide dot product of 8 weight chunks with a row broadcast from LDS, two accumulation chains.
+__device__ __forceinline__ float dot32(const float4 (&w)[FZ], const float *row, float acc) {
+  const float4 *r4 = (const float4 *)row;
+  float a1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < FZ; ++c) {
+    const float4 v = r4[c];
+    acc = fmaf(w[c].x, v.x, acc);
+    a1 = fmaf(w[c].y, v.y, a1);
+    acc = fmaf(w[c].z, v.z, acc);
+    a1 = fmaf(w[c].w, v.w, a1);
+  }
+  return acc + a1;
+}
+
+struct PairX {
+  xg::u64 *pw;            // this pair's words
+  uint32_t *abort_w, *sticky;
+  bool local;             // both blocks on one XCD
+};
+
+// Half of a head 1x1 from resident weights: output 128 h + t mod 128 over K half t / 128 (PH
+// chunks), the input vector broadcast from LDS.
+__device__ __forceinline__ float head_dot(const float4 (&Wt)[PH], const float *in) {
+  const float4 *i4 = (const float4 *)in;
+  float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+  for (int c = 0; c < PH; ++c) {
+    const float4 v = i4[c];
+    a0 = fmaf(Wt[c].x, v.x, a0);
+    a1 = fmaf(Wt[c].y, v.y, a1);
+    a0 = fmaf(Wt[c].z, v.z, a0);
+    a1 = fmaf(Wt[c].w, v.w, a1);
+  }
+  return a0 + a1;
+}
+
+// The head of one step in block h (every thread of both blocks); on return the chain block holds all
+// 256 logits in LDS in generation, and in forced modes each block has written its 128 classes out.
+// The helper's relu(skip sum) is already in its srow.
+__device__ __forceinline__ void pair_head(const PL &s, const float4 (&W1)[PH], const float4 (&W2)[PH],
+                                          const PairX &px, const StepArgs &a, int L, int b, int h, int step,
+                                          float hbias, float obias) {
+  const int tid = threadIdx.x, kh = tid >> 7, t2 = tid & 127;
+  const uint32_t tag = step + 1;
+  __syncthreads();  // the helper: every skip channel in LDS
+  if (h == 1) {
+    xg::put_word(px.pw + pw_s(L) + tid, __builtin_bit_cast(uint32_t, s.srow[tid]), tag, px.local);
+  } else {
+    uint32_t v[1];
+    xg::wait_words<1, 1>(px.pw + pw_s(L) + tid, tag, v, px.abort_w, px.sticky);
+    s.srow[tid] = __builtin_bit_cast(float, v[0]);
+    __syncthreads();  // relu(skip sum) of all 256 channels
+  }
+  s.part[tid] = head_dot(W1, s.srow + 128 * kh);
+  __syncthreads();
+  if (tid < 128) {
+    const float hv = fmaxf(s.part[tid] + s.part[tid + 128] + hbias, 0.f);
+    s.hrow[128 * h + tid] = hv;
+    xg::put_word(px.pw + pw_h(L, h) + tid, __builtin_bit_cast(uint32_t, hv), tag, px.local);
+  } else {
+    uint32_t v[1];
+    xg::wait_words<1, 1>(px.pw + pw_h(L, 1 - h) + t2, tag, v, px.abort_w, px.sticky);
+    s.hrow[128 * (1 - h) + t2] = __builtin_bit_cast(float, v[0]);
+  }
+  __syncthreads();  // the hidden layer
+  s.part[tid] = head_dot(W2, s.hrow + 128 * kh);
+  __syncthreads();
+  if (tid < 128) {
+    const float lv = s.part[tid] + s.part[tid + 128] + obias;
+    s.lrow[128 * h + tid] = lv;
+    if (a.mode != MODE_GENERATE) {
+      if (a.logits) a.logits[((long long)b * a.n_steps + step) * Q + 128 * h + tid] = lv;
+    } else if (h == 1) {
+      xg::put_word(px.pw + pw_l(L) + tid, __builtin_bit_cast(uint32_t, lv), tag, px.local);
+    }
+  } else if (h == 0 && a.mode == MODE_GENERATE) {
+    uint32_t v[1];
+    xg::wait_words<1, 1>(px.pw + pw_l(L) + t2, tag, v, px.abort_w, px.sticky);
+    s.lrow[128 + t2] = __builtin_bit_cast(float, v[0]);
+  }
+  __syncthreads();  // the chain block has every logit in generation
+}
+
+template <int W>
+__global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedArgs g) {
+  constexpr int FR = FREC * (W - 1);  // wave 2's weight chunks per layer
+  extern __shared__ float4 lds4[];
+  float *lds = (float *)lds4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kq = blockIdx.x >> 3, h = kq & 1, b = (kq >> 1) * 8 + (blockIdx.x & 7);
+  if (b >= a.batch) return;  // the last pairs of the grid beyond the batch
+  const int L = a.L;
+  const PL s = make_pl(lds, L);
+  PairX px;
+  px.pw = (xg::u64 *)((char *)a.sp_comm + 256) + (size_t)b * pair_words(L);
+  px.abort_w = (uint32_t *)a.sp_comm;
+  px.sticky = a.sp_sticky;
+
+  // ---- launch handshake: both blocks report their XCD; the chain block tells the helper whether
+  // they share one
+  if (tid == 0) {
+    xg::put_word(px.pw + PW_HS + 32 * h, xg::xcd_id(), 1, false);
+    uint32_t v[1];
+    if (h == 0) {
+      xg::wait_words<1, 1>(px.pw + PW_HS + 32, 1, v, px.abort_w, px.sticky);
+      const uint32_t loc = v[0] == xg::xcd_id() ? 1u : 0u;
+      xg::put_word(px.pw + PW_HS + 64, loc, 1, false);
+      *s.mode = (int)loc;
+    } else {
+      xg::wait_words<1, 1>(px.pw + PW_HS + 64, 1, v, px.abort_w, px.sticky);
+      *s.mode = (int)v[0];
+    }
+  }
+  // ---- tables into LDS (the chain block), flags, the first chunk of per-step inputs
+  if (h == 0) {
+    for (int i = tid; i < Q * R / 4; i += NT) ((float4 *)s.embT)[i] = ((const float4 *)g.embT)[i];
+    for (int i = tid; i < R; i += NT) s.embb[i] = g.embb[i];
+    for (int i = tid; i < L * R; i += NT) s.resb[i] = g.resb[i];
+    for (int j = tid; j < KCH; j += NT) {
+      if (a.mode == MODE_GENERATE) s.u[j] = j < a.n_steps ? a.uniforms[(long long)b * a.n_steps + j] : 0.f;
+      else {
+        const long long nx = j + forced_shift(a.mode);
+        s.fin[j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
+      }
+    }
+    if (tid == 0) *s.inval = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
+  }
+  for (int i = tid; i < L; i += NT) {
+    s.fx[i] = 0;
+    s.fz[i] = 0;
+    s.fu[i] = 0;
+  }
+  if (tid == 0) *s.abort_ = 0;
+  // lane l: layer l's queue (row offset of slot 0), dilation, depth (W - 1) d, slot of the step
+  const long long slot_stride = (long long)a.bmax * R;
+  long long qoff = 0;
+  int qdil = 1, qdep = W - 1, qslot = 0;
+  if (lane < L) {
+    const LayerDev ld = a.layers[lane];
+    qoff = ld.ring_off + (long long)b * R;
+    qdil = ld.dil;
+    qdep = ld.depth;
+    qslot = (int)(a.t0 % (long long)qdep);
+  }
+  float *ring = (float *)a.ring;
+  if (h == 0 && wave == 2) {
+    // the recurrent taps of every layer for step 0 (bias with the folded W_e b_res term)
+    for (int l = 0; l < L; ++l) {
+      const float4 *w = g.wrec + (size_t)l * FR * 64 + lane;
+      float acc = g.convb[l * 2 * R + lane];
+#pragma unroll
+      for (int k = 0; k < W - 1; ++k) {
+        int sk = qslot + k * qdil;
+        sk = sk >= qdep ? sk - qdep : sk;
+        const float *v = ring + lane_i64(qoff + sk * slot_stride, l);
+#pragma unroll
+        for (int c = 0; c < FREC; ++c) {
+          const float4 wv = w[(FREC * k + c) * 64];
+          const float4 vv = *(const float4 *)(v + 4 * c);
+          acc = fmaf(wv.x, vv.x, acc);
+          acc = fmaf(wv.y, vv.y, acc);
+          acc = fmaf(wv.z, vv.z, acc);
+          acc = fmaf(wv.w, vv.w, acc);
+        }
+      }
+      s.P[l * 2 * R + lane] = acc;
+    }
+    qslot = qslot + 1 == qdep ? 0 : qslot + 1;  // wave 2 works one step ahead
+  }
+  // this thread's K half of its rows of both head 1x1s, resident for the launch
+  const char *wbase = (const char *)g.wchain;
+  const Rsrc rw = make_rsrc(wbase, (int)((const char *)g.convb - wbase));
+  const int o_rec = (int)((const char *)g.wrec - wbase), o_skip = (int)((const char *)g.wskip - wbase);
+  const int o_head = (int)((const char *)g.whead - wbase), o_out = (int)((const char *)g.wout - wbase);
+  const int o_m = (int)((const char *)g.wm - wbase);
+  float4 W1[PH], W2[PH];
+  load_chunks(W1, rw, lane * 16, o_head + (h * 4 + wave) * PH * 1024, 1024);
+  load_chunks(W2, rw, lane * 16, o_out + (h * 4 + wave) * PH * 1024, 1024);
+  const float hbias = g.headb[128 * h + (tid & 127)], obias = g.outb[128 * h + (tid & 127)];
+  __syncthreads();
+  px.local = *s.mode != 0;
+  const int o = lane & (R - 1), hl = lane >> 5;
+
+  if (h == 1) {
+    // ---------------- helper: skip channel 64 wave + lane (wave 0 receives z), then the head
+    const int wst = o_skip + wave * FZ * 1024, lstr = 4 * FZ * 1024;
+    const int m = 64 * wave + lane;
+    const float bm = g.skipb[m];
+    float4 WA[FZ], WB[FZ];
+    load_chunks(WA, rw, lane * 16, wst, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      float s0 = bm;
+      for (int l = 0; l < L; l += 2) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int le = l + e;
+          if (le < L) {
+            float4 (&Wc)[FZ] = e ? WB : WA;
+            float4 (&Wn)[FZ] = e ? WA : WB;
+            load_chunks(Wn, rw, lane * 16, wst + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
+            if (wave == 0) {
+              if (lane < R) {
+                uint32_t v[1];
+                xg::wait_words<1, 1>(px.pw + PW_Z + le * R + lane, step + 1, v, px.abort_w, px.sticky);
+                s.zrow[le * R + lane] = __builtin_bit_cast(float, v[0]);
+              }
+              compiler_fence();
+              if (lane == 0) s.fz[le] = step + 1;
+            } else {
+              wait_flag(s, s.fz + le, step + 1);
+            }
+            s0 = dot32(Wc, s.zrow + le * R, s0);
+          }
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
+      }
+      s.srow[m] = fmaxf(s0, 0.f);
+      pair_head(s, W1, W2, px, a, L, b, 1, step, hbias, obias);
+      __syncthreads();
+    }
+  } else if (wave == 0) {
+    // ---------------- the gates (publishing z), then the head and the sample
+    const int lstr = FZ * 1024;
+    float4 WA[FZ], WB[FZ];  // M^{l-1} rows at slot l
+    load_chunks(WA, rw, lane * 16, o_m, 1024);
+    int in = *s.inval;
+    for (int step = 0; step < a.n_steps; ++step) {
+      const int par = step & 1;
+      float z = 0.f;
+      for (int l = 0; l < L; l += 2) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int le = l + e;
+          if (le < L) {
+            float4 (&Wc)[FZ] = e ? WB : WA;
+            float4 (&Wn)[FZ] = e ? WA : WB;
+            load_chunks(Wn, rw, lane * 16, o_m + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
+            wait_flag(s, s.fu + le, step + 1);
+            float acc = s.P[(par * L + le) * 2 * R + lane] + s.U[le * 2 * R + lane];
+            if (le > 0) acc = dot32(Wc, s.zrow + (le - 1) * R, acc);
+            const float v = gate_half(acc, lane < R);
+            const auto sw = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, v),
+                                                             __builtin_bit_cast(unsigned, v), false, false);
+            z = __builtin_bit_cast(float, (unsigned)sw[0]) * __builtin_bit_cast(float, (unsigned)sw[1]);
+            if (lane < R) s.zrow[le * R + o] = z;
+            compiler_fence();
+            if (lane == 0) s.fz[le] = step + 1;
+            if (lane < R) xg::put_word(px.pw + PW_Z + le * R + o, __builtin_bit_cast(uint32_t, z), step + 1, px.local);
+          }
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
+      }
+      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      if (a.mode == MODE_GENERATE) {
+        const float4 lg = ((const float4 *)s.lrow)[lane];
+        in = sample_row4(lg, s.u[(step / KCH & 1) * KCH + step % KCH]);
+        if (lane == 0) a.samples[(long long)b * a.n_steps + step] = in;
+      } else {
+        in = s.fin[(step / KCH & 1) * KCH + step % KCH];
+      }
+      if (lane == 0) *s.inval = in;
+      __syncthreads();  // the step's LDS rows and logits are consumed; the next input is in LDS
+    }
+    if (lane == 0 && a.mode != MODE_TEACHER) a.last[b] = in;
+  } else if (wave == 1) {
+    // ---------------- the residual stream and the pushes, then the head
+    const int lstr = FCH * 1024;
+    float4 WA[4], WB[4];  // W_res half rows: chunks 8..11 of the layer's chain block
+    load_chunks(WA, rw, lane * 16, 8 * 1024, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      const long long qrow = qoff + qslot * slot_stride;  // lane l: layer l's push row of this step
+      const int in = *s.inval;
+      float x = s.embT[in * R + o] + s.embb[o];
+      for (int l = 0; l < L; l += 2) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int le = l + e;
+          if (le < L) {
+            float4 (&Wc)[4] = e ? WB : WA;
+            float4 (&Wn)[4] = e ? WA : WB;
+            // x = x^le, the input of layer le: to LDS, to its queue
+            if (lane < R) {
+              s.xrow[le * R + o] = x;
+              ring[lane_i64(qrow, le) + o] = x;
+            }
+            compiler_fence();
+            if (lane == 0) s.fx[le] = step + 1;
+            if (le + 1 < L) {
+              load_chunks(Wn, rw, lane * 16, (le + 1) * lstr + 8 * 1024, 1024);
+              wait_flag(s, s.fz + le, step + 1);
+              const float4 *z4 = (const float4 *)(s.zrow + le * R + 16 * hl);
+              float r0 = 0.f, r1 = 0.f;
+#pragma unroll
+              for (int c = 0; c < 4; ++c) {
+                const float4 zv = z4[c];
+                r0 = fmaf(Wc[c].x, zv.x, r0);
+                r1 = fmaf(Wc[c].y, zv.y, r1);
+                r0 = fmaf(Wc[c].z, zv.z, r0);
+                r1 = fmaf(Wc[c].w, zv.w, r1);
+              }
+              x = x + s.resb[le * R + o] + ch::halves_sum(r0 + r1);
+            } else {
+              load_chunks(Wn, rw, lane * 16, 8 * 1024, 1024);  // layer 0's, for the next step
+            }
+          }
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) WA[c] = WB[c];
+      }
+      qslot = qslot + 1 == qdep ? 0 : qslot + 1;
+      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      __syncthreads();
+    }
+  } else if (wave == 2) {
+    // ---------------- the recurrent taps for the next step, staging, then the head
+    const int lstr = FR * 1024;
+    float4 WA[FR], WB[FR];
+    load_chunks(WA, rw, lane * 16, o_rec, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      const int np = (step & 1) ^ 1;
+      long long toff[W - 1];
+#pragma unroll
+      for (int k = 0; k < W - 1; ++k) {
+        int sk = qslot + k * qdil;
+        sk = sk >= qdep ? sk - qdep : sk;
+        toff[k] = qoff + sk * slot_stride;
+      }
+      for (int l = 0; l < L; l += 2) {
+        {
+          const float *taps[W - 1];
+#pragma unroll
+          for (int k = 0; k < W - 1; ++k) taps[k] = ring + lane_i64(toff[k], l);
+          const int ln = l + 1 < L ? l + 1 : 0;
+          rec_layer<W>(s, WA, WB, rw, o_rec + ln * lstr, taps, __builtin_amdgcn_readlane(qdil, l) == 1, g.convb, l,
+                       L, np, step, lane);
+        }
+        if (l + 1 < L) {
+          const float *taps[W - 1];
+#pragma unroll
+          for (int k = 0; k < W - 1; ++k) taps[k] = ring + lane_i64(toff[k], l + 1);
+          const int ln = l + 2 < L ? l + 2 : 0;
+          rec_layer<W>(s, WB, WA, rw, o_rec + ln * lstr, taps, __builtin_amdgcn_readlane(qdil, l + 1) == 1,
+                       g.convb, l + 1, L, np, step, lane);
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FR; ++c) WA[c] = WB[c];
+      }
+      qslot = qslot + 1 == qdep ? 0 : qslot + 1;
+      if (step % KCH == 0) {
+        const int base = step + KCH, buf = (step / KCH + 1) & 1;
+        for (int j = lane; j < KCH; j += 64) {
+          const long long sj = base + j;
+          if (a.mode == MODE_GENERATE) {
+            s.u[buf * KCH + j] = sj < a.n_steps ? a.uniforms[(long long)b * a.n_steps + sj] : 0.f;
+          } else {
+            const long long nx = sj + forced_shift(a.mode);
+            s.fin[buf * KCH + j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
+          }
+        }
+      }
+      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      __syncthreads();
+    }
+  } else {
+    // ---------------- U^l = W_e^l x^{l-1} (x^0 for l = 0), then the head
+    const int lstr = FCH * 1024;
+    float4 WA[FZ], WB[FZ];  // W_e rows: chunks 0..7 of the layer's chain block
+    load_chunks(WA, rw, lane * 16, 0, 1024);
+    for (int step = 0; step < a.n_steps; ++step) {
+      for (int l = 0; l < L; l += 2) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int le = l + e;
+          if (le < L) {
+            float4 (&Wc)[FZ] = e ? WB : WA;
+            float4 (&Wn)[FZ] = e ? WA : WB;
+            load_chunks(Wn, rw, lane * 16, (le + 1 < L ? le + 1 : 0) * lstr, 1024);
+            const int src = le > 0 ? le - 1 : 0;
+            wait_flag(s, s.fx + src, step + 1);
+            s.U[le * 2 * R + lane] = dot32(Wc, s.xrow + src * R, 0.f);
+            compiler_fence();
+            if (lane == 0) s.fu[le] = step + 1;
+          }
+        }
+      }
+      if (L & 1) {
+#pragma unroll
+        for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
+      }
+      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      __syncthreads();
+    }
+  }
+}
+
 // ---- packing (once per fwg_create)
-__global__ void pack_layer_kernel(const float *conv, const float *res, const float *skip, int l, int w,
+// pair: the pair variant's skip layout ([L][4 waves][8 chunks][64]: channel 64 wave + lane).
+__global__ void pack_layer_kernel(const float *conv, const float *res, const float *skip, int l, int w, int pair,
                                   ChainGatedArgs g) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   const int nchain = FCH * 64, nrec = FREC * (w - 1) * 64, nskip = 2 * FSK * 64;
@@ -817,21 +1314,65 @@ __global__ void pack_layer_kernel(const float *conv, const float *res, const flo
     for (int q = 0; q < 4; ++q) v[q] = conv[((size_t)ln * R + 4 * cc + q) * w + t];
     ((float4 *)g.wrec)[(size_t)l * nrec + f] = make_float4(v[0], v[1], v[2], v[3]);
   } else if (e < nchain + nrec + nskip) {
-    const int f = e - nchain - nrec, wv = f / (FSK * 64), c = (f / 64) % FSK, ln = f % 64;
-    const int m = 128 * wv + 2 * ln + (c >= 8 ? 1 : 0);
-    for (int q = 0; q < 4; ++q) v[q] = skip[(size_t)m * R + 4 * (c & 7) + q];
+    const int f = e - nchain - nrec;
+    int m, k0;
+    if (pair) {
+      const int wv = f / (FZ * 64), c = (f / 64) % FZ, ln = f % 64;
+      m = 64 * wv + ln;
+      k0 = 4 * c;
+    } else {
+      const int wv = f / (FSK * 64), c = (f / 64) % FSK, ln = f % 64;
+      m = 128 * wv + 2 * ln + (c >= 8 ? 1 : 0);
+      k0 = 4 * (c & 7);
+    }
+    for (int q = 0; q < 4; ++q) v[q] = skip[(size_t)m * R + k0 + q];
     ((float4 *)g.wskip)[(size_t)l * nskip + f] = make_float4(v[0], v[1], v[2], v[3]);
   }
 }
-__global__ void pack_head_kernel(const float *head, const float *out, ChainGatedArgs g) {
+// Single block: f = (wave, chunk, lane), row t = 64 wave + lane, columns 4 chunk .. 4 chunk + 3.
+// Pair: f = (block h, wave, j, lane), thread t = 64 wave + lane, row 128 h + t mod 128, chunk
+// PH (t / 128) + j (the thread's K half).
+__global__ void pack_head_kernel(const float *head, const float *out, int pair, ChainGatedArgs g) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= 2 * FH * NT) return;
-  // f = (wave, chunk, lane): row t = 64 wave + lane, columns 4 chunk .. 4 chunk + 3
-  const int which = e / (FH * NT), f = e % (FH * NT), wv = f / (FH * 64), c = (f / 64) % FH, t = 64 * wv + f % 64;
+  const int which = e / (FH * NT), f = e % (FH * NT);
+  int t, c;
+  if (pair) {
+    const int hb = f / (4 * PH * 64), wv = (f / (PH * 64)) % 4, j = (f / 64) % PH, tt = 64 * wv + f % 64;
+    t = 128 * hb + (tt & 127);
+    c = PH * (tt >> 7) + j;
+  } else {
+    const int wv = f / (FH * 64);
+    c = (f / 64) % FH;
+    t = 64 * wv + f % 64;
+  }
   const float *src = which ? out : head;
   float v[4];
   for (int q = 0; q < 4; ++q) v[q] = src[(size_t)t * 256 + 4 * c + q];
   ((float4 *)(which ? g.wout : g.whead))[f] = make_float4(v[0], v[1], v[2], v[3]);
+}
+// Pair variant: M^l = W_e^{l+1} W_res^l (64 x 32, float64 sums) at slot l + 1 of wm, rows per lane.
+__global__ void pack_m_kernel(const float *conv_next, const float *res, int slot, int w, ChainGatedArgs g) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= FZ * 64) return;
+  const int c = e / 64, o = e % 64;
+  float v[4];
+  for (int q = 0; q < 4; ++q) {
+    const int k = 4 * c + q;
+    double acc = 0.0;
+    for (int j = 0; j < R; ++j) acc += (double)conv_next[((size_t)o * R + j) * w + w - 1] * (double)res[(size_t)j * R + k];
+    v[q] = (float)acc;
+  }
+  ((float4 *)g.wm)[(size_t)slot * FZ * 64 + e] = make_float4(v[0], v[1], v[2], v[3]);
+}
+// Pair variant: the bias of layer l's recurrent part gains W_e^l b_res^{l-1} (float64 sum).
+__global__ void pack_fold_kernel(const float *conv, const float *res_b_prev, int l, int w, ChainGatedArgs g) {
+  const int o = blockIdx.x * blockDim.x + threadIdx.x;
+  if (o >= 2 * R || res_b_prev == nullptr) return;
+  double acc = 0.0;
+  for (int j = 0; j < R; ++j) acc += (double)conv[((size_t)o * R + j) * w + w - 1] * (double)res_b_prev[j];
+  float *cb = (float *)g.convb + (size_t)l * 2 * R;
+  cb[o] = (float)((double)cb[o] + acc);
 }
 __global__ void pack_vec_kernel(const float *src, float *dst, int n, int accumulate) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -866,6 +1407,7 @@ ChainGatedArgs chain_gated_arrays(void *base, int L, int w) {
   g.wskip = (const float4 *)take((size_t)L * 2 * FSK * 64 * 16);
   g.whead = (const float4 *)take((size_t)FH * NT * 16);
   g.wout = (const float4 *)take((size_t)FH * NT * 16);
+  g.wm = (const float4 *)take((size_t)L * FZ * 64 * 16);
   g.convb = (const float *)take((size_t)L * 2 * R * 4);
   g.resb = (const float *)take((size_t)L * R * 4);
   g.skipb = (const float *)take((size_t)S * 4);
@@ -885,6 +1427,38 @@ hipError_t set_chain_gated_lds_limit(size_t bytes) {
                              (int)bytes);
 }
 
+size_t chain_pair_lds_bytes(int L) { return chg::pair_lds_floats(L) * 4; }
+size_t chain_pair_comm_bytes(int L, int batch) { return 256 + chg::pair_words(L) * 8 * (size_t)batch; }
+int chain_pair_grid(int batch) { return 16 * ((batch + 7) / 8); }
+
+hipError_t chain_pair_setup(size_t lds, int bmax, int *coresident_ok) {
+  *coresident_ok = 0;
+  hipError_t e;
+  if ((e = hipFuncSetAttribute((const void *)chg::chain_pair_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)lds)) != hipSuccess)
+    return e;
+  if ((e = hipFuncSetAttribute((const void *)chg::chain_pair_kernel<3>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)lds)) != hipSuccess)
+    return e;
+  int dev = 0, cus = 0, per2 = 0, per3 = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per2, chg::chain_pair_kernel<2>, chg::NT, lds)) != hipSuccess)
+    return e;
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per3, chg::chain_pair_kernel<3>, chg::NT, lds)) != hipSuccess)
+    return e;
+  // every block of the largest launch resident at once (the blocks of a pair wait for each other)
+  *coresident_ok = (long long)std::min(per2, per3) * cus >= (long long)chain_pair_grid(bmax);
+  return hipSuccess;
+}
+
+hipError_t launch_chain_pair_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s) {
+  const dim3 grid(chain_pair_grid(a.batch));
+  if (a.w == 3) hipLaunchKernelGGL(chg::chain_pair_kernel<3>, grid, dim3(chg::NT), lds, s, a, g);
+  else hipLaunchKernelGGL(chg::chain_pair_kernel<2>, grid, dim3(chg::NT), lds, s, a, g);
+  return hipGetLastError();
+}
+
 hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, size_t lds, hipStream_t s) {
   if (a.w == 3) hipLaunchKernelGGL(chg::chain_gated_kernel<3>, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
   else hipLaunchKernelGGL(chg::chain_gated_kernel<2>, dim3(a.batch), dim3(chg::NT), lds, s, a, g);
@@ -894,13 +1468,13 @@ hipError_t launch_chain_gated_step(const StepArgs &a, const ChainGatedArgs &g, s
 hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, const void *const *conv,
                                    const float *const *conv_b, const void *const *res, const float *const *res_b,
                                    const void *const *skip, const float *const *skip_b, const void *head,
-                                   const float *head_b, const void *out, const float *out_b, int L, int w,
+                                   const float *head_b, const void *out, const float *out_b, int L, int w, bool pair,
                                    const ChainGatedArgs &g, hipStream_t s) {
   using namespace chg;
   const int n = FCH * 64 + FREC * (w - 1) * 64 + 2 * FSK * 64;
   for (int l = 0; l < L; ++l) {
     hipLaunchKernelGGL(pack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const float *)conv[l],
-                       (const float *)res[l], (const float *)skip[l], l, w, g);
+                       (const float *)res[l], (const float *)skip[l], l, w, pair ? 1 : 0, g);
     hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, conv_b ? conv_b[l] : nullptr,
                        (float *)g.convb + (size_t)l * 2 * R, 2 * R, 0);
     hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, res_b ? res_b[l] : nullptr,
@@ -909,12 +1483,23 @@ hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, cons
                        l > 0);
   }
   hipLaunchKernelGGL(pack_head_kernel, dim3((2 * FH * NT + 255) / 256), dim3(256), 0, s, (const float *)head,
-                     (const float *)out, g);
+                     (const float *)out, pair ? 1 : 0, g);
   hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, head_b, (float *)g.headb, H, 0);
   hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, out_b, (float *)g.outb, Q, 0);
   hipLaunchKernelGGL(ch::chain_transpose_kernel, dim3((R * Q + 255) / 256), dim3(256), 0, s, (const float *)embed,
                      (float *)g.embT, R, Q);
   hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, embed_b, (float *)g.embb, R, 0);
+  if (pair) {
+    // slot 0 of wm is never read; zero it all the same
+    hipLaunchKernelGGL(pack_vec_kernel, dim3(FZ * 64 * 4 / 256), dim3(256), 0, s, nullptr, (float *)g.wm, FZ * 64 * 4,
+                       0);
+    for (int l = 0; l + 1 < L; ++l)
+      hipLaunchKernelGGL(pack_m_kernel, dim3((FZ * 64 + 255) / 256), dim3(256), 0, s, (const float *)conv[l + 1],
+                         (const float *)res[l], l + 1, w, g);
+    for (int l = 1; l < L; ++l)
+      hipLaunchKernelGGL(pack_fold_kernel, dim3(1), dim3(2 * R), 0, s, (const float *)conv[l],
+                         res_b ? res_b[l - 1] : nullptr, l, w, g);
+  }
   return hipGetLastError();
 }
 

@@ -80,6 +80,7 @@ struct Plan {
   size_t off_chain, chain_lds;
   // gated chain family: packed weights (bytes) and the launch's LDS bytes
   size_t off_cg, cg_bytes, cg_lds;
+  size_t cp_lds;  // pair variant: the launch's LDS bytes
   // wide family: packed weights and tables, the launch's LDS and exchange-region bytes
   WideArgs wide;
   size_t wide_lds, wide_comm;
@@ -271,8 +272,13 @@ int make_plan(const fwg_desc *d, Plan *p) {
   // float32 gated stacks with R = 32, S = H = 256, width 2 or 3: one block per stream, the layer chain on one
   // wavefront, the recurrent halves, the skip sum and the head on the block's other waves
   if (p->regime == REGIME_VALU && !forced_other &&
-      chain_gated_ok(p->kind, p->dtype, p->C, p->S, p->H, p->Q, p->L, w, &p->cg_bytes, &p->cg_lds))
-    p->regime = REGIME_CHAIN_GATED;
+      chain_gated_ok(p->kind, p->dtype, p->C, p->S, p->H, p->Q, p->L, w, &p->cg_bytes, &p->cg_lds)) {
+    // two blocks of one XCD per stream (chain block and helper) unless FWG_REGIME=chain1 keeps one;
+    // fwg_create falls back to one block when the pairs cannot all be resident at once
+    p->cp_lds = chain_pair_lds_bytes(p->L);
+    const bool one = force && strcmp(force, "chain1") == 0;
+    p->regime = !one && p->cp_lds <= 160 * 1024 ? REGIME_CHAIN_PAIR : REGIME_CHAIN_GATED;
+  }
   // float32 ReLU stacks of 512 channels: each layer spread over a group of 32 blocks per XCD
   if (p->regime == REGIME_VALU && !forced_other &&
       wide_layout(p->kind, p->dtype, p->C, p->Q, p->L, w, p->bmax, d->dilations, &p->wide, &p->wide_lds,
@@ -357,7 +363,12 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_last = take(sizeof(int32_t) * p->bmax);
   p->off_wave = p->regime == REGIME_WAVE ? take(sizeof(float) * (size_t)p->wave.image_floats) : 0;
   p->off_chain = p->regime == REGIME_CHAIN ? take(sizeof(float) * (size_t)p->chain.image_floats) : 0;
-  p->off_cg = p->regime == REGIME_CHAIN_GATED ? take(p->cg_bytes) : 0;
+  const bool cg_family = p->regime == REGIME_CHAIN_GATED || p->regime == REGIME_CHAIN_PAIR;
+  p->off_cg = cg_family ? take(p->cg_bytes) : 0;
+  if (p->regime == REGIME_CHAIN_PAIR) {
+    p->off_comm = take(chain_pair_comm_bytes(p->L, p->bmax));
+    p->off_sticky = take(sizeof(uint32_t));
+  }
 
   // time-parallel path: every product's K must fill whole 128-byte k-tiles, and the gate's column
   // pairs come in groups of 16 channels
@@ -439,7 +450,7 @@ int enqueue_reset(fwg_handle *h) {
   const Plan &p = h->plan;
   HIP_TRY(launch_fill_zero(h->ws + p.off_ring_gen, (size_t)p.queue_elems * p.es, h->stream));
   HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_last), p.seed_input, p.bmax, h->stream));
-  if (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE)
+  if (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE || p.regime == REGIME_CHAIN_PAIR)
     HIP_TRY(launch_fill_zero(h->ws + p.off_sticky, sizeof(uint32_t), h->stream));
   if (p.nv_ok)  // every history entry the seed: the entry of time 0 is the first input
     HIP_TRY(launch_fill_i32((int32_t *)(h->ws + p.off_hist), p.seed_input, p.bmax * p.nv_hc, h->stream));
@@ -611,6 +622,15 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
     }
     case REGIME_CHAIN_GATED:
       return launch_chain_gated_step(a, chain_gated_arrays(h->ws + p.off_cg, p.L, p.w), p.cg_lds, h->stream);
+    case REGIME_CHAIN_PAIR: {
+      StepArgs b = a;
+      b.sp_comm = comm ? comm : h->ws + p.off_comm;
+      b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
+      // tags restart at 1 every launch: clear the exchange words first (a fill kernel, no memset node)
+      hipError_t e = launch_fill_zero(b.sp_comm, chain_pair_comm_bytes(p.L, a.batch), h->stream);
+      if (e != hipSuccess) return e;
+      return launch_chain_pair_step(b, chain_gated_arrays(h->ws + p.off_cg, p.L, p.w), p.cp_lds, h->stream);
+    }
     case REGIME_WAVE: {
       WaveArgs g = p.wave;
       g.image = (const float *)(h->ws + p.off_wave);
@@ -829,10 +849,18 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
                                    (float *)(ws + p.off_chain), s));
     TRY_OR_FREE(set_chain_lds_limit(p.chain_lds));
   }
-  if (p.regime == REGIME_CHAIN_GATED) {
+  if (p.regime == REGIME_CHAIN_PAIR) {
+    int coresident = 0;
+    TRY_OR_FREE(chain_pair_setup(p.cp_lds, p.bmax, &coresident));
+    if (!coresident) h->plan.regime = REGIME_CHAIN_GATED;  // same workspace; the one-block layout below
+    // set-up of fwg_generate_noalloc: this device's static exchange-word array, looked up once
+    else TRY_OR_FREE(split_static_scratch(&h->static_scratch));
+  }
+  if (h->plan.regime == REGIME_CHAIN_GATED || h->plan.regime == REGIME_CHAIN_PAIR) {
     TRY_OR_FREE(launch_chain_gated_pack(w->embed, w->embed_b, w->conv, w->conv_b, w->res, w->res_b, w->skip,
                                         w->skip_b, w->head, w->head_b, w->out, w->out_b, p.L, p.w,
-                                        chain_gated_arrays(ws + p.off_cg, p.L, p.w), s));
+                                        h->plan.regime == REGIME_CHAIN_PAIR, chain_gated_arrays(ws + p.off_cg, p.L, p.w),
+                                        s));
     TRY_OR_FREE(set_chain_gated_lds_limit(p.cg_lds));
   }
   if (p.regime == REGIME_WAVE) {
@@ -959,9 +987,10 @@ int generate_impl(fwg_handle *h, int32_t batch, int32_t n_steps, const float *un
   if (h->bound_batch >= 0 && h->bound_batch != batch)
     return fail(FWG_ESTATE, "batch %d differs from %d used since the last reset", batch, h->bound_batch);
   void *comm = nullptr;
-  if (noalloc && (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE)) {
-    const size_t need =
-        p.regime == REGIME_SPLIT ? split_comm_bytes(p.L, (batch + kMfRows - 1) / kMfRows) : p.wide_comm;
+  if (noalloc && (p.regime == REGIME_SPLIT || p.regime == REGIME_WIDE || p.regime == REGIME_CHAIN_PAIR)) {
+    const size_t need = p.regime == REGIME_SPLIT ? split_comm_bytes(p.L, (batch + kMfRows - 1) / kMfRows)
+                        : p.regime == REGIME_WIDE ? p.wide_comm
+                                                  : chain_pair_comm_bytes(p.L, batch);
     if (need > kStaticScratchBytes)
       return fail(FWG_ENOSPACE, "the exchange words of %d streams x %d layers need %zu bytes; the static scratch "
                   "array holds %zu", batch, p.L, need, kStaticScratchBytes);
@@ -1039,9 +1068,8 @@ int fwg_step_forced(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t
 int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, const int32_t *inputs, float *logits) {
   if (!h) return fail(FWG_EINVAL, "handle is NULL");
   const Plan &p = h->plan;
-  if (!p.par_ok)
-    return fail(FWG_EUNSUPPORTED, "no time-parallel kernels for this model (every product's K must fill whole "
-                                  "128-byte tiles)");
+  // products narrower than one 128-byte k-tile: the step kernels evaluate the sequence instead
+  if (!p.par_ok) return fwg_teacher_forced(h, batch, seq_len, inputs, logits);
   if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
   if (seq_len < 0) return fail(FWG_EINVAL, "seq_len < 0");
   if (seq_len == 0) return FWG_OK;
@@ -1053,9 +1081,8 @@ int fwg_teacher_forced_parallel(fwg_handle *h, int32_t batch, int32_t seq_len, c
 int fwg_prime(fwg_handle *h, int32_t batch, int32_t n_steps, const int32_t *inputs, float *logits) {
   if (!h) return fail(FWG_EINVAL, "handle is NULL");
   const Plan &p = h->plan;
-  if (!p.par_ok)
-    return fail(FWG_EUNSUPPORTED, "no time-parallel kernels for this model (every product's K must fill whole "
-                                  "128-byte tiles)");
+  // products narrower than one 128-byte k-tile: the step kernels run the prefix instead
+  if (!p.par_ok) return fwg_step_forced(h, batch, n_steps, inputs, logits);
   if (batch < 1 || batch > p.bmax) return fail(FWG_EINVAL, "batch %d outside [1, %d]", batch, p.bmax);
   if (n_steps < 0) return fail(FWG_EINVAL, "n_steps < 0");
   if (h->bound_batch >= 0 && h->bound_batch != batch)
@@ -1108,7 +1135,7 @@ int fwg_destroy(fwg_handle *h) {
 int fwg_device_status(fwg_handle *h) {
   if (!h) return fail(FWG_EINVAL, "handle is NULL");
   HIP_TRY(hipStreamSynchronize(h->stream));
-  if (h->plan.regime == REGIME_SPLIT || h->plan.regime == REGIME_WIDE) {
+  if (h->plan.regime == REGIME_SPLIT || h->plan.regime == REGIME_WIDE || h->plan.regime == REGIME_CHAIN_PAIR) {
     uint32_t v = 0;
     HIP_TRY(hipMemcpy(&v, h->ws + h->plan.off_sticky, sizeof(v), hipMemcpyDeviceToHost));
     if (v)
@@ -1126,6 +1153,7 @@ const char *fwg_regime(const fwg_handle *h) {
     case REGIME_WAVE: return "wave";
     case REGIME_CHAIN: return "chain_f32_c32";
     case REGIME_CHAIN_GATED: return "chain_gated_f32_r32";
+    case REGIME_CHAIN_PAIR: return "chain_pair_f32_r32";
     case REGIME_WIDE: return "wide_f32_c512";
     default: return "valu";
   }

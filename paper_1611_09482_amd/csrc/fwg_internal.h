@@ -71,7 +71,7 @@ __host__ __device__ inline int forced_shift(int mode) { return mode == MODE_TEAC
 
 // Kernel families.
 enum Regime { REGIME_VALU = 0, REGIME_MFMA = 1, REGIME_WAVE = 2, REGIME_SPLIT = 3, REGIME_CHAIN = 4, REGIME_WIDE = 5,
-             REGIME_CHAIN_GATED = 6 };
+             REGIME_CHAIN_GATED = 6, REGIME_CHAIN_PAIR = 7 };
 
 // MFMA family shape (gated, bf16 operands): R residual, S skip, H head channels,
 // 16 streams per block of 8 waves, weight fragments per wave and stage.

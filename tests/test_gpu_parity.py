@@ -112,6 +112,9 @@ FAMILIES = {
     "gated_r32_f32_valu": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
     # odd layer count, repeated and non-power-of-two dilations (the gated chain kernel's buffer swap)
     "gated_r32_f32_odd": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 1, 7, 2), 256, 256),
+    # the same shapes on the one-block gated chain kernel (FWG_REGIME=chain1)
+    "gated_r32_f32_one": W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16, 32, 64, 128), 256, 256),
+    "gated_r32_f32_odd_one": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 1, 7, 2), 256, 256),
     "gated_r64_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32, 64, 128), 512, 512),
     "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
@@ -123,6 +126,7 @@ FAMILIES = {
     "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
     "gated_r32_w3_f32": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r32_w3_f32_valu": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
+    "gated_r32_w3_f32_one": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r64_w3_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
     "relures_c64_w4_bf16": W.ModelConfig(W.RELU_RESIDUAL, W.BF16, 64, (1, 4, 16, 2), filter_width=4),
     # small enough for the wave-per-stream kernels (every weight in LDS)
@@ -137,8 +141,10 @@ FAMILIES = {
 WAVE_FAMILIES = {"relu_c32_w3_f32", "gated_r16_s32_f32", "relu_c32_bf16", "relu_c32_f32_wave"}
 # families that must run on the chain kernels (float32 ReLU stacks with C = 32, width 2)
 CHAIN_FAMILIES = {"relu_c32_f32", "relures_c32_f32"}
-# families that must run on the gated chain kernel (float32 gated stacks with R = 32, S = H = 256)
-CHAIN_GATED_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd", "gated_r32_w3_f32"}
+# families that must run on the gated chain kernels (float32 gated stacks with R = 32, S = H = 256):
+# the pair variant (two blocks per stream) by default, the one-block kernel when forced
+CHAIN_PAIR_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd", "gated_r32_w3_f32"}
+FORCE_CHAIN1 = {"gated_r32_f32_one", "gated_r32_f32_odd_one", "gated_r32_w3_f32_one"}
 # families that must run on the wide kernels (float32 ReLU stacks with C = 512: each layer spread
 # over a group of 32 blocks)
 WIDE_FAMILIES = {"relures_c512_f32"}
@@ -167,6 +173,8 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
         env["FWG_REGIME"] = "valu"
     if fam in FORCE_WAVE:
         env["FWG_REGIME"] = "wave"
+    if fam in FORCE_CHAIN1:
+        env["FWG_REGIME"] = "chain1"
     if par_rows is not None:
         env["FWG_PAR_ROWS"] = str(par_rows)
     if valu_stage is not None:
@@ -187,15 +195,17 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
             split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
             assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
-            assert fw.regime in ("valu", "wave", "chain_f32_c32", "chain_gated_f32_r32", "wide_f32_c512"), (
-                fam, fw.regime)
+            assert fw.regime in ("valu", "wave", "chain_f32_c32", "chain_gated_f32_r32", "chain_pair_f32_r32",
+                                 "wide_f32_c512"), (fam, fw.regime)
         if fam in WIDE_FAMILIES:
             assert fw.regime == "wide_f32_c512", (fam, fw.regime)
         if fam in WAVE_FAMILIES:
             assert fw.regime == "wave", (fam, fw.regime)
         if fam in CHAIN_FAMILIES:
             assert fw.regime == "chain_f32_c32", (fam, fw.regime)
-        if fam in CHAIN_GATED_FAMILIES:
+        if fam in CHAIN_PAIR_FAMILIES:
+            assert fw.regime == "chain_pair_f32_r32", (fam, fw.regime)
+        if fam in FORCE_CHAIN1:
             assert fw.regime == "chain_gated_f32_r32", (fam, fw.regime)
     return w, fw, oracle.Oracle(w)
 
@@ -244,12 +254,9 @@ def test_teacher_forced_parity(fam, path):
     w, fw, orc = build_pair(cfg, 100, B, fam=fam)
     x = W.sequences(3, B, T)
     t0 = time.time()
-    try:
-        g = tf(fw, x, path)
-    except binding.FwgError as e:
-        # the time-parallel kernels need every product's K in whole 128-byte tiles
-        assert path == "parallel" and e.code == binding.FWG_EUNSUPPORTED and cfg.channels * (4 if cfg.dtype == W.F32 else 2) % 128
-        pytest.skip(f"no time-parallel kernels for {fam}")
+    # models whose products are narrower than a 128-byte k-tile run the "parallel" call through
+    # the step kernels
+    g = tf(fw, x, path)
     o = orc.teacher_forced(x)
     err = row_rel_err(g, o)
     log(f"{fam} [{fw.regime}, {path}]: TF B={B} T={T} max row rel err {err.max():.3e} "
@@ -477,7 +484,8 @@ def test_delay_line_closed_form_gpu(fwidth, dil, path):
 
 @pytest.mark.parametrize("fam,B,regime", [("gated_r64_bf16", 16, "mfma_bf16_r64_s512"),
                                           ("gated_r64_bf16_split", 13, "mfma_split_bf16_r64_s512"),
-                                          ("gated_r32_f32", 5, "chain_gated_f32_r32"),
+                                          ("gated_r32_f32", 5, "chain_pair_f32_r32"),
+                                          ("gated_r32_f32_one", 3, "chain_gated_f32_r32"),
                                           ("relu_c32_f32", 3, "chain_f32_c32")])
 def test_uniform_logits_sampler_gpu(fam, B, regime):
     """All-equal logits: the sample is floor(256 u), bit-exact, in both halves of the MFMA
@@ -487,7 +495,12 @@ def test_uniform_logits_sampler_gpu(fam, B, regime):
     w.out[:] = 0
     w.out_b[:] = 0
     n = 400
-    fw = binding.from_model(cfg, w, max_batch=B)
+    if fam in FORCE_CHAIN1:
+        os.environ["FWG_REGIME"] = "chain1"
+    try:
+        fw = binding.from_model(cfg, w, max_batch=B)
+    finally:
+        os.environ.pop("FWG_REGIME", None)
     if regime is not None:
         assert fw.regime == regime
     u = W.uniforms(9, B, n)
@@ -496,7 +509,7 @@ def test_uniform_logits_sampler_gpu(fam, B, regime):
     u[B - 1, :6] = edge[::-1]
     g = fw.generate(dev(u)).cpu().numpy()
     assert np.array_equal(g, np.floor(u.astype(np.float64) * 256).astype(np.int32))
-    if regime == "mfma_split_bf16_r64_s512":
+    if regime in ("mfma_split_bf16_r64_s512", "chain_pair_f32_r32"):
         fw.device_status()
 
 
@@ -625,14 +638,14 @@ def test_full_toy_relu():
 
 def test_full_gated_b1():
     wl, w, fw, orc = _full("gated_r32_s256_l20_b1")
-    assert fw.regime == "chain_gated_f32_r32"
+    assert fw.regime == "chain_pair_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     check_generation(wl.model, fw, orc, u, wl.batch, wl.name)
 
 
 def test_full_gated_b64():
     wl, w, fw, orc = _full("gated_r32_s256_l20_b64")
-    assert fw.regime == "chain_gated_f32_r32"
+    assert fw.regime == "chain_pair_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255
@@ -671,7 +684,7 @@ def test_full_gated_w3():
     """The filter-width-3 workload at full size (64 streams x 8,000 steps): sampled streams checked
     by the oracle over every step."""
     wl, w, fw, orc = _full("gated_r32_s256_w3_l14_b64")
-    assert fw.regime == "chain_gated_f32_r32"
+    assert fw.regime == "chain_pair_f32_r32"
     u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255

@@ -1,6 +1,7 @@
 """The allocation-free generation entry point (fwg_generate_noalloc) against fwg_generate, through
-the C ABI: the split kernels with their exchange words in the library's static device array must
-draw exactly the samples the workspace-backed launch draws (integer outputs: bit-exact), on two
+the C ABI: the kernel families whose blocks exchange words (split, wide, gated chain pair), with those
+words in the library's static device array, must draw exactly the samples the workspace-backed launch
+draws (integer outputs: bit-exact), on two
 calls in a row, the second with a smaller batch after a reset (fewer groups, so a smaller part of
 the array), and with a continuation across calls."""
 import numpy as np
@@ -81,11 +82,39 @@ def test_noalloc_matches_generate_wide():
     assert np.array_equal(got2, want2)
 
 
+def test_noalloc_matches_generate_chain_pair():
+    """The gated chain kernels' pair variant (two blocks per stream exchanging z rows, skip halves,
+    hidden halves and logits as words): exchange words in the static array, 9 streams (pairs on
+    every XCD slot and one more), then 2 streams after a reset in two calls."""
+    cfg = W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8, 16), 256, 256)
+    ref, na = _pair(cfg, 9)
+    assert ref.regime == na.regime == "chain_pair_f32_r32"
+    u = W.uniforms(47, 9, 80)
+    want = ref.generate(_dev(u)).cpu().numpy()
+    out = torch.empty((9, 80), dtype=torch.int32, device="cuda")
+    got = na.generate_noalloc(_dev(u), out).cpu().numpy()
+    print(f"noalloc pair call 1: 9 x 80, equal {np.array_equal(got, want)}", flush=True)
+    assert np.array_equal(got, want)
+    ref.reset()
+    na.reset()
+    u2 = W.uniforms(48, 2, 60)
+    want2 = ref.generate(_dev(u2)).cpu().numpy()
+    o1 = torch.empty((2, 25), dtype=torch.int32, device="cuda")
+    o2 = torch.empty((2, 35), dtype=torch.int32, device="cuda")
+    g1 = na.generate_noalloc(_dev(u2[:, :25]), o1).cpu().numpy()
+    g2 = na.generate_noalloc(_dev(u2[:, 25:]), o2).cpu().numpy()
+    got2 = np.concatenate([g1, g2], axis=1)
+    print(f"noalloc pair call 2: 2 x 60 in two calls, equal {np.array_equal(got2, want2)}", flush=True)
+    assert np.array_equal(got2, want2)
+    na.device_status()
+
+
 def test_noalloc_other_family_and_errors():
     """Kernel families without per-launch scratch run exactly as fwg_generate; host-side errors
     (batch binding, range) come before anything is enqueued."""
-    cfg = W.ModelConfig(W.GATED, W.F32, 32, (1, 2, 4, 8), 256, 256)
+    cfg = W.ModelConfig(W.RELU, W.F32, 32, (1, 2, 4, 8))
     ref, na = _pair(cfg, 6)
+    assert ref.regime == "chain_f32_c32"
     u = W.uniforms(44, 6, 70)
     want = ref.generate(_dev(u)).cpu().numpy()
     out = torch.empty((6, 70), dtype=torch.int32, device="cuda")
