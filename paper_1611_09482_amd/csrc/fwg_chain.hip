@@ -1088,7 +1088,6 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
           if (le < L) {
             float4 (&Wc)[FZ] = e ? WB : WA;
             float4 (&Wn)[FZ] = e ? WA : WB;
-            load_chunks(Wn, rw, lane * 16, wst + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
             if (wave == 0) {
               if (lane < R) {
                 uint32_t v[1];
@@ -1101,6 +1100,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
               wait_flag(s, s.fz + le, step + 1);
             }
             s0 = dot32(Wc, s.zrow + le * R, s0);
+            load_chunks(Wn, rw, lane * 16, wst + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
           }
         }
       }
@@ -1128,7 +1128,6 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
           if (le < L) {
             float4 (&Wc)[FZ] = e ? WB : WA;
             float4 (&Wn)[FZ] = e ? WA : WB;
-            load_chunks(Wn, rw, lane * 16, o_m + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
             wait_flag(s, s.fu + le, step + 1);
             float acc = s.P[(par * L + le) * 2 * R + lane] + s.U[le * 2 * R + lane];
             if (le > 0) acc = dot32(Wc, s.zrow + (le - 1) * R, acc);
@@ -1140,6 +1139,8 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
             compiler_fence();
             if (lane == 0) s.fz[le] = step + 1;
             if (lane < R) xg::put_word(px.pw + PW_Z + le * R + o, __builtin_bit_cast(uint32_t, z), step + 1, px.local);
+            // the next layer's weights, fetched once this layer's result is out
+            load_chunks(Wn, rw, lane * 16, o_m + (le + 1 < L ? le + 1 : 0) * lstr, 1024);
           }
         }
       }
@@ -1175,15 +1176,15 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
           if (le < L) {
             float4 (&Wc)[4] = e ? WB : WA;
             float4 (&Wn)[4] = e ? WA : WB;
-            // x = x^le, the input of layer le: to LDS, to its queue
+            // x = x^le, the input of layer le, to its queue (and, for layer 0, to LDS: the rows of later
+            // layers are written as soon as they are computed)
             if (lane < R) {
-              s.xrow[le * R + o] = x;
+              if (le == 0) s.xrow[o] = x;
               ring[lane_i64(qrow, le) + o] = x;
             }
             compiler_fence();
-            if (lane == 0) s.fx[le] = step + 1;
+            if (le == 0 && lane == 0) s.fx[0] = step + 1;
             if (le + 1 < L) {
-              load_chunks(Wn, rw, lane * 16, (le + 1) * lstr + 8 * 1024, 1024);
               wait_flag(s, s.fz + le, step + 1);
               const float4 *z4 = (const float4 *)(s.zrow + le * R + 16 * hl);
               float r0 = 0.f, r1 = 0.f;
@@ -1196,6 +1197,10 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
                 r1 = fmaf(Wc[c].w, zv.w, r1);
               }
               x = x + s.resb[le * R + o] + ch::halves_sum(r0 + r1);
+              if (lane < R) s.xrow[(le + 1) * R + o] = x;
+              compiler_fence();
+              if (lane == 0) s.fx[le + 1] = step + 1;
+              load_chunks(Wn, rw, lane * 16, (le + 1) * lstr + 8 * 1024, 1024);
             } else {
               load_chunks(Wn, rw, lane * 16, 8 * 1024, 1024);  // layer 0's, for the next step
             }
@@ -1275,12 +1280,12 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
           if (le < L) {
             float4 (&Wc)[FZ] = e ? WB : WA;
             float4 (&Wn)[FZ] = e ? WA : WB;
-            load_chunks(Wn, rw, lane * 16, (le + 1 < L ? le + 1 : 0) * lstr, 1024);
             const int src = le > 0 ? le - 1 : 0;
             wait_flag(s, s.fx + src, step + 1);
             s.U[le * 2 * R + lane] = dot32(Wc, s.xrow + src * R, 0.f);
             compiler_fence();
             if (lane == 0) s.fu[le] = step + 1;
+            load_chunks(Wn, rw, lane * 16, (le + 1 < L ? le + 1 : 0) * lstr, 1024);
           }
         }
       }
