@@ -74,16 +74,20 @@ __host__ __device__ inline size_t lds_queues(int L) { return lds_tables(L) + (((
 // wl + ((size_t)l * NBG + j) * NCH * NT float4 (chunk i of thread t at [i][t]); the output 1x1 at
 // wo + (size_t)j * NCO * NT float4.
 
+// Weight registers are native 4-vectors: arrays of the HIP float4 struct live across the step loop
+// were copied member-wise and kept in scratch memory.
+typedef float wv4 __attribute__((ext_vector_type(4)));
+
 // Products of the block's 16 channels for the 4 streams over its thread's K part, both taps, from the
 // gathered layer input xs (x[s][kp][i]); partial sums into red.
-__device__ __forceinline__ void layer_products(const float4 (&w)[NCH], const float (*xs)[KP][XP], int oc, int kp,
+__device__ __forceinline__ void layer_products(const wv4 (&w)[NCH], const float (*xs)[KP][XP], int oc, int kp,
                                                float (*red)[OC][2 * SG]) {
   float e[SG], r[SG];
 #pragma unroll
   for (int s = 0; s < SG; ++s) e[s] = r[s] = 0.f;
 #pragma unroll
   for (int i = 0; i < KW / 4; ++i) {
-    const float4 we = w[i], wr = w[8 + i];
+    const wv4 we = w[i], wr = w[8 + i];
 #pragma unroll
     for (int s = 0; s < SG; ++s) {
       const float4 x = *(const float4 *)&xs[s][kp][4 * i];
@@ -104,10 +108,84 @@ __device__ __forceinline__ void layer_products(const float4 (&w)[NCH], const flo
   }
 }
 
-__device__ __forceinline__ void load_layer_weights(float4 (&w)[NCH], const float4 *wl, int l, int j, int tid) {
-  const float4 *src = wl + ((size_t)l * NBG + j) * NCH * NT + tid;
+__device__ __forceinline__ void load_layer_weights(wv4 (&w)[NCH], const float4 *wl, int l, int j, int tid) {
+  const wv4 *src = (const wv4 *)(wl + ((size_t)l * NBG + j) * NCH * NT + tid);
 #pragma unroll
   for (int i = 0; i < NCH; ++i) w[i] = src[i * NT];
+}
+
+// The weights of index t of the per-step sequence (layer t for t < L, the output 1x1's NCO chunks
+// for t == L, nothing beyond).
+__device__ __forceinline__ void load_seq_weights(wv4 (&w)[NCH], const float4 *wl, const float4 *wo4, int t, int L,
+                                                 int j, int tid) {
+  if (t < L) {
+    load_layer_weights(w, wl, t, j, tid);
+  } else if (t == L) {
+    const wv4 *src = (const wv4 *)(wo4 + (size_t)j * NCO * NT + tid);
+#pragma unroll
+    for (int i = 0; i < NCO; ++i) w[i] = src[i * NT];
+    // the rest of the buffer is written too (a buffer written in part on one path stayed in scratch)
+#pragma unroll
+    for (int i = NCO; i < NCH; ++i) w[i] = wv4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
+// (plain values and pointers only: a reference to a by-value kernel argument would move the argument
+// to scratch memory)
+struct WideLayerCtx {
+  void *comm;
+  const float *convb;
+  Lds *sp;
+  const int *qoff, *slot;
+  float *Pq, *Xq;
+  const float4 *wl, *wo4;
+  uint32_t *abort_word, *sticky;
+  int L, g, j, tid, wave, oc, kp;
+  bool local, residual;
+};
+
+// One layer: products from the weights in wc (the next-but-one index of the sequence fetched into
+// wp first), the epilogue of the block's channels, the gather of the layer output.
+__device__ __forceinline__ void wide_layer(const WideLayerCtx &c, int l, const wv4 (&wc)[NCH], wv4 (&wp)[NCH],
+                                           uint32_t tag) {
+  Lds &s = *c.sp;
+  const int cur = l & 1, L = c.L, tid = c.tid, j = c.j, g = c.g;
+  load_seq_weights(wp, c.wl, c.wo4, l + 2, L, j, tid);
+  layer_products(wc, s.xg[cur], c.oc, c.kp, s.red);
+  __syncthreads();
+  // epilogue of the block's channels (wave 0, lane = (s, oc)): pop the product pushed d steps ago,
+  // push this step's
+  if (c.wave == 0) {
+    const int o2 = tid & (OC - 1), st = tid >> 4, ch = 16 * j + o2;
+    float e = 0.f, r = 0.f;
+#pragma unroll
+    for (int p = 0; p < KP; ++p) {
+      e += s.red[p][o2][st];
+      r += s.red[p][o2][SG + st];
+    }
+    const size_t ent = ((size_t)(c.qoff[l] + c.slot[l]) * OC + o2) * SG + st;
+    const float xin = s.xg[cur][st][ch / KW][ch % KW];
+    const float act = fmaxf(e + c.Pq[ent] + c.convb[l * C + ch], 0.f);
+    const float xo = c.residual ? xin + act : act;
+    c.Pq[ent] = r;
+    c.Xq[ent] = xin;
+    // the layer output to the group: word (s, oc) of this block's slice, two per store
+    const float xo1 = __shfl_down(xo, 1, 64);
+    if (o2 % 2 == 0)
+      put_words2(g_x(c.comm, L, g, l) + j * OC * SG + st * OC + o2, __float_as_uint(xo), __float_as_uint(xo1),
+                 tag, c.local);
+  }
+  // gather the whole layer output into the other buffer (this block's own slice included)
+  {
+    uint32_t v[8];
+    wait_words<8, NT>(g_x(c.comm, L, g, l) + tid, tag, v, c.abort_word, c.sticky);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int wi = e * NT + tid, jb = wi / (OC * SG), rr = wi % (OC * SG), st = rr / OC, ch = 16 * jb + rr % OC;
+      s.xg[cur ^ 1][st][ch / KW][ch % KW] = __uint_as_float(v[e]);
+    }
+  }
+  __syncthreads();
 }
 
 __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
@@ -176,7 +254,7 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
   // ---- the launch's state: the states of this block's channels from the workspace queues, and the
   // products W_r x of every queued state (a pass over each layer's slots with the layer's weights)
   {
-    float4 wv[NCH];
+    wv4 wv[NCH];
     for (int l = 0; l < L; ++l) {
       load_layer_weights(wv, wl, l, j, tid);
       const float *src = (const float *)a.ring + a.layers[l].ring_off;
@@ -204,8 +282,12 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
   }
 
   const float *embT = w.embT, *embb = w.embb, *convb = w.convb, *outb = w.outb;
-  float4 wa[NCH], wb[NCH];
-  load_layer_weights(wa, wl, 0, j, tid);
+  // weights stream through three register buffers, two layers ahead (index t of the step's
+  // sequence in buffer t mod 3: layers 0..L-1, then the output 1x1): with one layer in flight the
+  // group's loads did not cover the latency of the last-level cache
+  wv4 W0[NCH], W1[NCH], W2[NCH];
+  load_seq_weights(W0, wl, wo4, 0, L, j, tid);
+  load_seq_weights(W1, wl, wo4, 1, L, j, tid);
 
   for (int step = 0; step < a.n_steps; ++step) {
     const uint32_t tag = (uint32_t)(step + 1);
@@ -215,56 +297,12 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       s.xg[0][st][c / KW][c % KW] = embT[(size_t)s.in[st] * C + c] + embb[c];
     }
     __syncthreads();
-    for (int l = 0; l < L; ++l) {
-      const int cur = l & 1;
-      // the next layer's weights (the output 1x1's after the last layer) into the other buffer
-      if (l + 1 < L) {
-        if (cur == 0) load_layer_weights(wb, wl, l + 1, j, tid);
-        else load_layer_weights(wa, wl, l + 1, j, tid);
-      } else {
-        const float4 *src = wo4 + (size_t)j * NCO * NT + tid;
-#pragma unroll
-        for (int i = 0; i < NCO; ++i) {
-          if (cur == 0) wb[i] = src[i * NT];
-          else wa[i] = src[i * NT];
-        }
-      }
-      if (cur == 0) layer_products(wa, s.xg[cur], oc, kp, s.red);
-      else layer_products(wb, s.xg[cur], oc, kp, s.red);
-      __syncthreads();
-      // epilogue of the block's channels (wave 0, lane = (s, oc)): pop the product pushed d steps
-      // ago, push this step's
-      if (wave == 0) {
-        const int o2 = tid & (OC - 1), st = tid >> 4, ch = 16 * j + o2;
-        float e = 0.f, r = 0.f;
-#pragma unroll
-        for (int p = 0; p < KP; ++p) {
-          e += s.red[p][o2][st];
-          r += s.red[p][o2][SG + st];
-        }
-        const size_t ent = ((size_t)(qoff[l] + slot[l]) * OC + o2) * SG + st;
-        const float xin = s.xg[cur][st][ch / KW][ch % KW];
-        const float act = fmaxf(e + Pq[ent] + convb[l * C + ch], 0.f);
-        const float xo = residual ? xin + act : act;
-        Pq[ent] = r;
-        Xq[ent] = xin;
-        // the layer output to the group: word (s, oc) of this block's slice, two per store
-        const float xo1 = __shfl_down(xo, 1, 64);
-        if (o2 % 2 == 0)
-          put_words2(g_x(a.sp_comm, L, g, l) + j * OC * SG + st * OC + o2, __float_as_uint(xo), __float_as_uint(xo1),
-                     tag, local);
-      }
-      // gather the whole layer output into the other buffer (this block's own slice included)
-      {
-        uint32_t v[8];
-        wait_words<8, NT>(g_x(a.sp_comm, L, g, l) + tid, tag, v, abort_word, sticky);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int wi = e * NT + tid, jb = wi / (OC * SG), rr = wi % (OC * SG), st = rr / OC, c = 16 * jb + rr % OC;
-          s.xg[cur ^ 1][st][c / KW][c % KW] = __uint_as_float(v[e]);
-        }
-      }
-      __syncthreads();
+    const WideLayerCtx cx{a.sp_comm, w.convb, &s, qoff, slot, Pq, Xq, wl, wo4, abort_word, sticky,
+                          L, g, j, tid, wave, oc, kp, local, residual};
+    for (int l = 0; l < L; l += 3) {
+      wide_layer(cx, l, W0, W2, tag);
+      if (l + 1 < L) wide_layer(cx, l + 1, W1, W0, tag);
+      if (l + 2 < L) wide_layer(cx, l + 2, W2, W1, tag);
     }
     // ---- output 1x1: classes 8j..8j+7; thread (c8, kq) covers K part kq (16 channels)
     {
@@ -273,10 +311,10 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       float acc[SG];
 #pragma unroll
       for (int st = 0; st < SG; ++st) acc[st] = 0.f;
+      const int ob = L % 3;  // the output 1x1's weights: index L of the sequence
 #pragma unroll
       for (int i = 0; i < NCO; ++i) {
-        // the output 1x1's weights sit in the buffer layer L - 1 did not use
-        const float4 wv = lastp ? wb[i] : wa[i];
+        const wv4 wv = ob == 0 ? W0[i] : ob == 1 ? W1[i] : W2[i];
         const int k = 16 * kq + 4 * i;
 #pragma unroll
         for (int st = 0; st < SG; ++st) {
@@ -291,8 +329,9 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       float *r2 = &s.red[0][0][0];
 #pragma unroll
       for (int st = 0; st < SG; ++st) r2[(kq * QB + c8) * SG + st] = acc[st];
-      // weights of layer 0 for the next step, read while the logits are summed and sampled
-      load_layer_weights(wa, wl, 0, j, tid);
+      // the next step's first two indices, read while the logits are summed and sampled
+      load_seq_weights(W0, wl, wo4, 0, L, j, tid);
+      load_seq_weights(W1, wl, wo4, 1, L, j, tid);
       __syncthreads();
       if (wave == 0) {
         // lanes 0..31: (s, class); lanes 32..63 repeat them and store nothing
