@@ -10,13 +10,15 @@
 //  - helper h owns 64 of the 512 channels of the skip sum and of the head's hidden layer.  Per
 //    step it accumulates sum_l W_skip^l z^l + b for its skip channels from the gate outputs z^l
 //    the chain block publishes, then (after gathering the whole relu(skip sum) from the group) its
-//    rows of the first head 1x1.  Its head weights stay in its waves' registers for the launch;
+//    rows of the first head 1x1.  Its head weights, and up to 32 layers its skip weights, stay in
+//    its waves' registers for the launch;
 //  - the class block gathers the whole hidden layer, computes all 256 logits (the output 1x1 is in
 //    its waves' registers for the launch), draws the softmax / inverse-CDF sample of every stream
 //    and returns the samples to the chain block (forced modes: writes the logits out and returns a
 //    mark that the step's head is done).
 // No later layer reads a skip product and the head follows the last layer, so the chain block
-// streams only the 40 KB of conv and residual weights per layer; in the single-block kernel every
+// streams only the 40 KB of conv and residual weights per layer from the L2, which then also keeps
+// the exchange words that are rewritten every step; in the single-block kernel every
 // block that owns streams streams all 4 MB of weights once per step, which bounds its step.
 //
 // Hand-offs between blocks are 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed
@@ -516,17 +518,142 @@ __device__ __forceinline__ void gather_act(uint16_t *act, const u64 *src, uint32
   }
 }
 
+// Values of a helper wave for its step loop (plain values and pointers).
+struct HelperCtx {
+  const StepArgs *a;
+  HelperLds *s;
+  const char *fw;  // this wave's skip fragment stream (layers w, w + 8, ...)
+  const u64 *zb;
+  u64 *sw, *hw;
+  uint32_t *abort_word;
+  int tid, w, lane, n, q, nl, wvoff, h;
+  bool local;
+};
+
+// z^l (512 words) as this wave's two B operand rows: lane takes words e 64 + lane (stream
+// 2e + lane / 32, channel pair lane % 32) and turns them into rows (stream n, channels 8q..8q+7 for
+// k-step 0, 32 + 8q.. for k-step 1) through its wave's partial-sum area, which the wave next writes
+// after its last layer of the step (LDS operations of one wave complete in order).
+__device__ __forceinline__ void z_operands(const HelperCtx &c, int l, uint32_t tag, u32x4 &b0, u32x4 &b1) {
+  uint32_t zv[8];
+  wait_words<8, 64>(c.zb + (size_t)l * ZWORDS + c.lane, tag, zv, c.abort_word, c.a->sp_sticky);
+  uint32_t *stg = (uint32_t *)c.s->u.part[c.w];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) stg[(2 * e + (c.lane >> 5)) * ZST + (c.lane & 31)] = zv[e];
+  b0 = *(const u32x4 *)(stg + c.n * ZST + 4 * c.q);
+  b1 = *(const u32x4 *)(stg + c.n * ZST + 16 + 4 * c.q);
+}
+
+// Skip fragments kept in a helper wave's registers for the whole launch when it has at most this
+// many layers (L <= 32): streamed every step they filled most of the XCD's L2, and the exchange
+// words, rewritten every step, were evicted to memory.
+constexpr int NRES = 4;
+
+// The helper's step loop.  RES: this wave's skip fragments (at most NRES layers) stay in registers;
+// otherwise they stream from L2 through an 8-fragment ring, one layer ahead.
+template <bool RES>
+__device__ __forceinline__ void helper_steps(const HelperCtx &c, const u32x4 (&hw1)[8]) {
+  const StepArgs &a = *c.a;
+  HelperLds &s = *c.s;
+  const int tid = c.tid, w = c.w, n = c.n, q = c.q, nl = c.nl, wvoff = c.wvoff, h = c.h;
+  const float *skip_sum = s.bias, *head_b = s.bias + SL;
+  constexpr int NW_ = RES ? NRES : 1;
+  u32x4 W[NW_][FS];
+  if (RES) {
+#pragma unroll
+    for (int i = 0; i < NW_; ++i)
+#pragma unroll
+      for (int f = 0; f < FS; ++f)
+        W[i][f] = i < nl ? *(const u32x4 *)(c.fw + (size_t)(i * FS + f) * 1024 + wvoff) : u32x4{0u, 0u, 0u, 0u};
+  } else {
+#pragma unroll
+    for (int f = 0; f < FS; ++f) W[0][f] = *(const u32x4 *)(c.fw + f * 1024 + wvoff);
+  }
+  const char *nxt = c.fw + (nl > 1 ? FS * 1024 : 0);
+  for (long long step = 0; step < a.n_steps; ++step) {
+    const uint32_t tag = (uint32_t)(step + 1);
+    // ---- 1. skip sums of the slice
+    f32x4 acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (RES) {
+#pragma unroll
+      for (int i = 0; i < NW_; ++i) {
+        if (i < nl) {
+          u32x4 b0, b1;
+          z_operands(c, w + NW * i, tag, b0, b1);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            acc[j] = mfma(W[i][2 * j], b0, acc[j]);
+            acc[j] = mfma(W[i][2 * j + 1], b1, acc[j]);
+          }
+        }
+      }
+    } else {
+      for (int i = 0; i < nl; ++i) {
+        u32x4 b0, b1;
+        z_operands(c, w + NW * i, tag, b0, b1);
+        if (i + 1 == nl) nxt = c.fw;  // the next layer of this wave is its first of the next step
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          acc[j] = mfma(W[0][2 * j], b0, acc[j]);
+          __builtin_amdgcn_sched_barrier(0);
+          W[0][2 * j] = *(const u32x4 *)(nxt + wvoff);
+          __builtin_amdgcn_sched_barrier(0);
+          acc[j] = mfma(W[0][2 * j + 1], b1, acc[j]);
+          __builtin_amdgcn_sched_barrier(0);
+          W[0][2 * j + 1] = *(const u32x4 *)(nxt + 1024 + wvoff);
+          __builtin_amdgcn_sched_barrier(0);
+          nxt += 2048;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) stf4(s.u.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
+    __syncthreads();
+    if (tid < ROWS * SL / 4) {
+      // thread t: stream t/16, slice channels 4 (t%16) .. +3
+      const int r = tid >> 4, c4 = 4 * (tid & 15);
+      f32x4 v = ldsf4(skip_sum + c4);
+#pragma unroll
+      for (int ww = 0; ww < NW; ++ww) v += ldsf4(s.u.part[ww] + r * PH + c4);
+      const u32x2 pk = pack4(relu4(v));
+      put_words2(c.sw + r * 256 + (h * SL + c4) / 2, pk.x, pk.y, tag, c.local);
+    }
+    __syncthreads();
+    // ---- 2. hidden rows of the slice: tile j = w % 4, k-steps 8 (w / 4) .. +7
+    gather_act(s.u.act, c.sw, tag, c.abort_word, a.sp_sticky);
+    __syncthreads();
+    {
+      const int k0 = 8 * (w >> 2);
+      // two accumulators (even and odd k-steps): two dependent chains of four MFMAs, not one of eight
+      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t;
+#pragma unroll
+      for (int i = 0; i < 8; i += 2) {
+        t = mfma(hw1[i], lds16(s.u.act + n * PS + 32 * (k0 + i) + 8 * q), t);
+        t1 = mfma(hw1[i + 1], lds16(s.u.act + n * PS + 32 * (k0 + i + 1) + 8 * q), t1);
+      }
+      t += t1;
+      if (w >= 4) stf4(s.pw[w - 4] + n * PP + 4 * q, t);
+      acc[0] = t;
+    }
+    __syncthreads();
+    if (w < 4) {
+      const int ch = 16 * w + 4 * q;
+      f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t[i] = fmaxf(t[i] + head_b[ch + i], 0.f);
+      const u32x2 pk = pack4(t);
+      put_words2(c.hw + n * 256 + (h * HL + ch) / 2, pk.x, pk.y, tag, c.local);
+    }
+  }
+}
+
 __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, int blk, int h) {
   HelperLds &s = *(HelperLds *)lds_raw;
   const int tid = threadIdx.x, L = a.L;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63, n = lane & 15, q = lane >> 4;
-  const int nl = (L - w + NW - 1) / NW;  // layers of this wave (L >= NW)
-  const char *fw = (const char *)a.mf_frags + base_h(L, h, w) * 1024;
-  const int wvoff = 16 * lane;
-  const u64 *zb = comm_z(a.sp_comm, L, blk);
-  u64 *sw = comm_s(a.sp_comm, L, blk), *hw = comm_hid(a.sp_comm, L, blk);
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
-  const float *skip_sum = s.bias, *head_b = s.bias + SL;
   // the slice's biases into LDS for the whole launch
   {
     const float *src = a.mf_bias + L * 3 * R;  // skip sum [S], head [H], out [Q]
@@ -550,82 +677,25 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
     s.local = (int)v[0];
   }
   __syncthreads();
-  const bool local = s.local != 0;
-  u32x4 W[FS];
-#pragma unroll
-  for (int f = 0; f < FS; ++f) W[f] = *(const u32x4 *)(fw + f * 1024 + wvoff);
-  const char *nxt = fw + (nl > 1 ? FS * 1024 : 0);
-  for (long long step = 0; step < a.n_steps; ++step) {
-    const uint32_t tag = (uint32_t)(step + 1);
-    // ---- 1. skip sums of the slice
-    f32x4 acc[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int i = 0; i < nl; ++i) {
-      const int l = w + NW * i;
-      // z^l (512 words): lane takes words e 64 + lane (stream 2e + lane / 32, channel pair lane % 32)
-      // and turns them into B operand rows (stream n, channels 8q..8q+7 for k-step 0, 32 + 8q.. for
-      // k-step 1) through its wave's partial-sum area, which the wave next writes after its last
-      // layer of the step (LDS operations of one wave complete in order)
-      uint32_t zv[8];
-      wait_words<8, 64>(zb + (size_t)l * ZWORDS + lane, tag, zv, abort_word, a.sp_sticky);
-      uint32_t *stg = (uint32_t *)s.u.part[w];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) stg[(2 * e + (lane >> 5)) * ZST + (lane & 31)] = zv[e];
-      const u32x4 b0 = *(const u32x4 *)(stg + n * ZST + 4 * q), b1 = *(const u32x4 *)(stg + n * ZST + 16 + 4 * q);
-      if (i + 1 == nl) nxt = fw;  // the next layer of this wave is its first of the next step
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        acc[j] = mfma(W[2 * j], b0, acc[j]);
-        __builtin_amdgcn_sched_barrier(0);
-        W[2 * j] = *(const u32x4 *)(nxt + wvoff);
-        __builtin_amdgcn_sched_barrier(0);
-        acc[j] = mfma(W[2 * j + 1], b1, acc[j]);
-        __builtin_amdgcn_sched_barrier(0);
-        W[2 * j + 1] = *(const u32x4 *)(nxt + 1024 + wvoff);
-        __builtin_amdgcn_sched_barrier(0);
-        nxt += 2048;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) stf4(s.u.part[w] + n * PH + 16 * j + 4 * q, acc[j]);
-    __syncthreads();
-    if (tid < ROWS * SL / 4) {
-      // thread t: stream t/16, slice channels 4 (t%16) .. +3
-      const int r = tid >> 4, c4 = 4 * (tid & 15);
-      f32x4 v = ldsf4(skip_sum + c4);
-#pragma unroll
-      for (int ww = 0; ww < NW; ++ww) v += ldsf4(s.u.part[ww] + r * PH + c4);
-      const u32x2 pk = pack4(relu4(v));
-      put_words2(sw + r * 256 + (h * SL + c4) / 2, pk.x, pk.y, tag, local);
-    }
-    __syncthreads();
-    // ---- 2. hidden rows of the slice: tile j = w % 4, k-steps 8 (w / 4) .. +7
-    gather_act(s.u.act, sw, tag, abort_word, a.sp_sticky);
-    __syncthreads();
-    {
-      const int k0 = 8 * (w >> 2);
-      // two accumulators (even and odd k-steps): two dependent chains of four MFMAs, not one of eight
-      f32x4 t = f32x4{0.f, 0.f, 0.f, 0.f}, t1 = t;
-#pragma unroll
-      for (int i = 0; i < 8; i += 2) {
-        t = mfma(hw1[i], lds16(s.u.act + n * PS + 32 * (k0 + i) + 8 * q), t);
-        t1 = mfma(hw1[i + 1], lds16(s.u.act + n * PS + 32 * (k0 + i + 1) + 8 * q), t1);
-      }
-      t += t1;
-      if (w >= 4) stf4(s.pw[w - 4] + n * PP + 4 * q, t);
-      acc[0] = t;
-    }
-    __syncthreads();
-    if (w < 4) {
-      const int ch = 16 * w + 4 * q;
-      f32x4 t = acc[0] + ldsf4(s.pw[w] + n * PP + 4 * q);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) t[i] = fmaxf(t[i] + head_b[ch + i], 0.f);
-      const u32x2 pk = pack4(t);
-      put_words2(hw + n * 256 + (h * HL + ch) / 2, pk.x, pk.y, tag, local);
-    }
-  }
+  HelperCtx c;
+  c.a = &a;
+  c.s = &s;
+  c.fw = (const char *)a.mf_frags + base_h(L, h, w) * 1024;
+  c.zb = comm_z(a.sp_comm, L, blk);
+  c.sw = comm_s(a.sp_comm, L, blk);
+  c.hw = comm_hid(a.sp_comm, L, blk);
+  c.abort_word = abort_word;
+  c.tid = tid;
+  c.w = w;
+  c.lane = lane;
+  c.n = lane & 15;
+  c.q = lane >> 4;
+  c.nl = (L - w + NW - 1) / NW;  // layers of this wave (L >= NW)
+  c.wvoff = 16 * lane;
+  c.h = h;
+  c.local = s.local != 0;
+  if (helper_layers(L) <= NRES) helper_steps<true>(c, hw1);
+  else helper_steps<false>(c, hw1);
 }
 
 // ---------------------------------------------------------------------------

@@ -120,6 +120,9 @@ FAMILIES = {
     "gated_r64_bf16_odd": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 1, 7, 2), 512, 512),
     # 12 layers: the split MFMA kernels (chain block + skip helper blocks; L a multiple of 6, >= 12)
     "gated_r64_bf16_split": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 2, 512, 512),
+    # 36 layers: more than four layers per helper wave, so the helpers stream their skip fragments
+    # (at most 32 layers they keep them in registers)
+    "gated_r64_bf16_split36": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 6, 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     "relures_c512_f32_valu": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
