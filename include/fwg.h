@@ -157,13 +157,14 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
  * HIP graph capture, tight serving loops, or harnesses that forbid hipMalloc.
  * Same arguments, state, results and errors as fwg_generate.  The kernel
  * families whose blocks cooperate within a launch (fwg_regime
- * "mfma_split_bf16_r64_s512" and "wide_f32_c512") keep the words they exchange
- * in a static device array of 4 MiB (one per device, set up by fwg_create and
- * held until the process ends) instead of the workspace; a batch whose words
- * do not fit (split family: more than 4 MiB / (8 x (512 L + 8544)) groups of
- * 16 streams, about 21 groups at L = 30; wide family: 256 + 8 x (16,384 L +
- * 17,664) bytes whatever the batch, so L <= 30) returns FWG_ENOSPACE before
- * anything is enqueued.  The other kernel families use no per-launch scratch
+ * "mfma_split_bf16_r64_s512", "wide_f32_c512" and "chain_pair_f32_r32") keep
+ * the words they exchange in a static device array of 4 MiB (one per device,
+ * set up by fwg_create and held until the process ends) instead of the
+ * workspace; a batch whose words do not fit (split family: more than 4 MiB /
+ * (8 x (512 L + 8544)) groups of 16 streams, about 21 groups at L = 30; wide
+ * family: 256 + 8 x (16,384 L + 17,664) bytes whatever the batch, so L <= 30;
+ * gated chain pair family: 256 + 8 x (736 + 32 L) bytes per stream, 381
+ * streams at L = 20) returns FWG_ENOSPACE before anything is enqueued.  The other kernel families use no per-launch scratch
  * and run exactly as fwg_generate.  The
  * array is cleared by a fill kernel at the start of every launch, but every
  * call on a device shares it: calls of this entry point that overlap on one
