@@ -221,9 +221,10 @@ template <int D>
 __device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int vb3, int par, const u32x4 (&W)[D], int f0) {
   ChainLds &s = *c.s;
   const uint16_t *vb = s.vbuf[vb3] + c.n * PX;
-  const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
   const float *cb = c.conv_b + ln * 2 * R;
+  // the biases (C operands) first, so the two products interleave (the LDS reads land in order)
   f32x4 pt = ldsf4(cb + 16 * c.p + 4 * c.q), pg = ldsf4(cb + R + 16 * c.p + 4 * c.q);
+  const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
   // the four LDS reads in flight together (one wait), not one round trip per product
   __builtin_amdgcn_sched_barrier(0);
   pt = mfma(W[f0 + 0], bv0, pt);
@@ -257,6 +258,10 @@ __device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xr
   ChainLds &s = *c.s;
   const int n = c.n, q = c.q, p = c.p;
   const int par = l & 1;
+  // W_r v + b first: the LDS reads land in order, and with both C operands in before the layer input
+  // the tanh and sigmoid products interleave instead of running as two dependent pairs
+  f32x4 af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q);
+  f32x4 ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
   u32x4 bx0, bx1;
   if (l == 0) {
     // embedding (current input x^0): row gather of the transposed 1x1 convolution plus bias
@@ -280,14 +285,14 @@ __device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xr
     bx0 = lds16(xb + 8 * q);
     bx1 = lds16(xb + 32 + 8 * q);
   }
-  f32x4 af = ldsf4(s.pbuf[par][p][0] + n * PP + 4 * q);
-  f32x4 ag = ldsf4(s.pbuf[par][p][1] + n * PP + 4 * q);
   af = mfma(W[PHS + 0], bx0, af);
   ag = mfma(W[PHS + 2], bx0, ag);
   af = mfma(W[PHS + 1], bx1, af);
   ag = mfma(W[PHS + 3], bx1, ag);
 #pragma unroll
   for (int f = 0; f < 4; ++f) refill(c, W, PHS + f);
+  // x^l + b_res while the gate runs, so the residual product starts as soon as z^l lands
+  f32x4 xr = xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
   f32x4 z;
 #pragma unroll
   for (int i = 0; i < 4; ++i) z[i] = gate(af[i], ag[i]);
@@ -295,7 +300,6 @@ __device__ __forceinline__ void a_layer(Ctx &c, int l, u32x4 (&W)[DA], f32x4 &xr
   __syncthreads();
   const uint16_t *zb = s.zbuf[par] + n * PX;
   const u32x4 bz0 = lds16(zb + 8 * q), bz1 = lds16(zb + 32 + 8 * q);
-  f32x4 xr = xres + ldsf4(c.res_b + l * R + 16 * p + 4 * q);
   xr = mfma(W[PHS + 4], bz0, xr);
   xr = mfma(W[PHS + 5], bz1, xr);
 #pragma unroll
