@@ -164,12 +164,12 @@ int fwg_generate(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uni
  * (8 x (512 L + 8544)) groups of 16 streams, about 21 groups at L = 30; wide
  * family: 256 + 8 x (16,384 L + 17,664) bytes whatever the batch, so L <= 30;
  * gated chain pair family: 256 + 8 x (736 + 32 L) bytes per stream, 381
- * streams at L = 20) returns FWG_ENOSPACE before anything is enqueued.  The other kernel families use no per-launch scratch
- * and run exactly as fwg_generate.  The
- * array is cleared by a fill kernel at the start of every launch, but every
- * call on a device shares it: calls of this entry point that overlap on one
- * device (other streams, other handles, other threads) race and must be
- * serialised by the caller.  Allocates nothing and calls no allocating
+ * streams at L = 20) returns FWG_ENOSPACE before anything is enqueued.  The
+ * other kernel families use no per-launch scratch and run exactly as
+ * fwg_generate.  The array is cleared by a fill kernel at the start of every
+ * launch, but every call on a device shares it: calls of this entry point that
+ * overlap on one device (other streams, other handles, other threads) race and
+ * must be serialised by the caller.  Allocates nothing and calls no allocating
  * routine. */
 int fwg_generate_noalloc(fwg_handle *h, int32_t batch, int32_t n_steps, const float *uniforms, int32_t *samples);
 
