@@ -21,6 +21,7 @@ struct WideArgs {
   float *convb;    // [L][C]
   float *outb;     // [Q]
   int entries;     // sum of the dilations
+  int nslots;      // weight chunks the LDS ring of a block holds
   size_t wl_bytes, wo_bytes;
 };
 // Whether a model fits the family (fills the array sizes, the launch's LDS bytes and its exchange

@@ -5,16 +5,23 @@
 // the graph are matrix products), then the output 1x1 and the sample fed back (Section 1).  A single
 // block would stream 2 MB of weights per layer; here block j of a group owns output channels
 // 16j..16j+15 of every layer:
-//  - per layer it reads its 64 KB of weights (W_e and W_r rows, packed per thread, prefetched into
-//    registers one layer ahead; the whole model stays resident in the 256 MB last-level cache) and
-//    computes both products of its 16 channels for the group's 4 streams over the whole layer
-//    input: thread (oc, kp) covers channel oc over K part kp (32 channels), and the 16 K parts meet
-//    in LDS;
+//  - per layer it reads its 64 KB of weights (W_e and W_r rows; the whole model stays resident in
+//    the 256 MB last-level cache) and computes both products of its 16 channels for the group's 4
+//    streams over the whole layer input: thread (oc, kp) of the four compute waves covers channel oc
+//    over K part kp (32 channels), and the 16 K parts meet in LDS;
+//  - a fifth wave only streams weights: it copies the step's sequence of 16 KB chunks (each layer's
+//    weights as four chunks, then the output 1x1's) into a ring of LDS slots, one chunk in flight,
+//    and the compute waves take each chunk from its slot.  The weight stream of an XCD is bound by
+//    what the XCD can fetch beyond its L2, and a wave that issues a layer's loads itself stalls at
+//    the issue until the compute unit's memory queue drains; with the loads on their own wave the
+//    products, the exchange and the polls run while the next weights arrive.  The compute waves
+//    synchronise through LDS counters, not block barriers, so the streaming wave never waits for
+//    them except for a free slot;
 //  - the queue (Section 2.2) keeps, per block, the product W_r x of its own channels instead of the
 //    state x: a = W_e x_t + (W_r x_{t-d}) + b pops the product pushed d steps earlier, so no block
-//    reads another block's queue.  The states of its own channels are kept beside them and written
-//    back to the workspace queues at the end of the launch (the generation state every kernel
-//    family shares); at launch the products are recomputed from those states;
+//    reads another block's queue.  The states of its own channels are pushed to the workspace queues
+//    (the generation state every kernel family shares); at launch the products are recomputed from
+//    them;
 //  - the layer output goes to the group's other blocks as tagged words (fwg_xchg.h); with the whole
 //    group on one XCD they stay in that XCD's L2;
 //  - the output 1x1 is spread the same way (8 classes per block); block s < 4 of the group gathers
@@ -36,11 +43,16 @@ using namespace xg;
 
 constexpr int C = kWideC, NBG = kWideBlocks, OC = C / NBG, SG = kWideStreams, NG = kWideGroups;
 constexpr int NT = 256, KP = NT / OC, KW = C / KP, Q = 256, QB = Q / NBG;
+constexpr int NTL = 64;       // the streaming wave
 constexpr int XP = KW + 4;    // floats per (stream, K part) row of the gathered layer input (padding spreads banks)
 constexpr int KCH = 64;       // steps per chunk of staged uniforms / forced inputs
-constexpr int NCH = 16;       // packed weight chunks (float4) per thread and layer: 8 of W_e, 8 of W_r
-constexpr int NCO = 4;        // packed output-1x1 chunks per thread
+constexpr int CPL = 4;        // weight chunks per layer
+constexpr int CF4 = 4;        // float4 per compute thread and chunk
+constexpr int CHUNK = CF4 * NT;  // float4 per chunk (16 KB)
+constexpr int NCO = 4;        // float4 per compute thread of the output 1x1 (one chunk)
+constexpr int MAXSLOT = 8;    // ring slots at most
 static_assert(OC == 16 && KP == 16 && KW == 32 && QB == 8, "block geometry");
+static_assert(NCO == CF4 && (KW / 4) == 2 * CPL, "a layer is four chunks, the output 1x1 one");
 
 // Exchange words of a group (u64): handshake slots, the layer outputs, the logits, the samples.
 constexpr int HSLOT = 32;                          // words per handshake slot (a 256-byte line)
@@ -56,6 +68,8 @@ __host__ __device__ inline u64 *g_x(void *comm, int L, int g, int l) {
 __host__ __device__ inline u64 *g_lg(void *comm, int L, int g) { return g_x(comm, L, g, L); }
 __host__ __device__ inline u64 *g_smp(void *comm, int L, int g) { return g_lg(comm, L, g) + NBG * QB * SG; }
 
+typedef __attribute__((address_space(3))) volatile int lds_flag;
+
 // LDS of a block.
 struct Lds {
   float xg[2][SG][KP][XP];  // layer input (all 512 channels) by layer parity: stream s, channel 32 kp + i
@@ -64,33 +78,87 @@ struct Lds {
   int fin[2][KCH][SG];      // staged forced next inputs
   int in[SG];               // the step's inputs
   int mode;                 // handshake result: the group shares one XCD
-  // followed by the per-layer tables dil[L], qoff[L], slot[L] and the queues:
-  // P[entries][OC][SG] (products W_r x) and X[entries][OC][SG] (states), entries = sum of dilations
+  int ready[MAXSLOT];       // ring slot s holds chunk k of the launch once ready[s] == k + 1
+  int cons[4];              // chunks each compute wave has finished reading
+  int cbar;                 // compute-wave barrier counter (each wave adds 1 per barrier)
+  int abort_;               // an LDS wait ran out: later LDS waits return at once
+  // followed by the per-layer tables dil[L], qoff[L], slot[L], the ring of weight slots and the
+  // queue P[entries][OC][SG] (products W_r x), entries = sum of dilations
 };
 __host__ __device__ inline size_t lds_tables(int L) { return (sizeof(Lds) + 15) & ~(size_t)15; }
-__host__ __device__ inline size_t lds_queues(int L) { return lds_tables(L) + (((size_t)3 * L * 4 + 15) & ~(size_t)15); }
+__host__ __device__ inline size_t lds_ring(int L) { return lds_tables(L) + (((size_t)3 * L * 4 + 15) & ~(size_t)15); }
+__host__ __device__ inline size_t lds_queue(int L, int ns) { return lds_ring(L) + (size_t)ns * CHUNK * 16; }
 
-// ---- packed weights (per block j, same for every group): layer l at
-// wl + ((size_t)l * NBG + j) * NCH * NT float4 (chunk i of thread t at [i][t]); the output 1x1 at
-// wo + (size_t)j * NCO * NT float4.
+// ---- packed weights (per block j, same for every group): chunk c of layer l at
+// wl + ((size_t)(CPL l + c) * NBG + j) * CHUNK float4, float4 i of compute thread t at [i][t]:
+// i = 0, 1: W_e row chunks 2c, 2c + 1 of the thread's K part, i = 2, 3: W_r likewise; the output
+// 1x1 at wo + (size_t)j * CHUNK float4 (thread (c8, kq): class 8j + c8, channels 16 kq + 4i ..).
 
-// Weight registers are native 4-vectors: arrays of the HIP float4 struct live across the step loop
-// were copied member-wise and kept in scratch memory.
-typedef float wv4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
-// Products of the block's 16 channels for the 4 streams over its thread's K part, both taps, from the
-// gathered layer input xs (x[s][kp][i]); partial sums into red.
-__device__ __forceinline__ void layer_products(const wv4 (&w)[NCH], const float (*xs)[KP][XP], int oc, int kp,
-                                               float (*red)[OC][2 * SG]) {
-  float e[SG], r[SG];
+// Waits until *flag >= want (every LDS wait of the launch is bounded: one that runs out marks the
+// block's LDS abort word and the launch's sticky word, and every later LDS wait returns at once).
+__device__ __forceinline__ void wait_ge(Lds &s, lds_flag *flag, int want, uint32_t *sticky) {
+  lds_flag *ab = (lds_flag *)&s.abort_;
+  for (int it = 0; *flag < want; ++it) {
+    if (*ab) break;
+    if (it >= kSpinMax) {
+      *ab = 1;
+      __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  compiler_fence();
+}
+
+// Barrier of the four compute waves (the streaming wave takes no part): each wave adds 1 and waits
+// for the count of this barrier.  A wave's LDS operations run in order, so its writes before the
+// add are visible to a wave that has seen the count.
+__device__ __forceinline__ void cbar(Lds &s, int &ph, int lane, uint32_t *sticky) {
+  ph += 4;
+  compiler_fence();
+  if (lane == 0) __hip_atomic_fetch_add((__attribute__((address_space(3))) int *)&s.cbar, 1, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_WORKGROUP);
+  wait_ge(s, (lds_flag *)&s.cbar, ph, sticky);
+}
+
+// Compute wave: chunk k of the launch is in its slot; afterwards the slot may be refilled.
+__device__ __forceinline__ const float4 *take_chunk(Lds &s, const float4 *ring, long long k, int ns, uint32_t *sticky) {
+  const int slot = (int)(k % ns);
+  lds_flag *f = (lds_flag *)&s.ready[slot];
+  lds_flag *ab = (lds_flag *)&s.abort_;
+  for (int it = 0; *f != (int)(k + 1); ++it) {
+    if (*ab) break;
+    if (it >= kSpinMax) {
+      *ab = 1;
+      __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      break;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  compiler_fence();
+  return ring + (size_t)slot * CHUNK;
+}
+__device__ __forceinline__ void done_chunk(Lds &s, int wave, int lane, long long k) {
+  compiler_fence();
+  if (lane == 0) *(lds_flag *)&s.cons[wave] = (int)(k + 1);
+}
+
+// Products of the block's 16 channels for the 4 streams over chunk c of the thread's K part (K
+// 8c .. 8c + 7), both taps, accumulated into e and r (the same order of operations as one pass
+// over the eight K groups of the part).
+__device__ __forceinline__ void chunk_products(const float4 *ch, const float (*xs)[KP][XP], int tid, int kp, int c,
+                                               float (&e)[SG], float (&r)[SG]) {
+  float4 w[CF4];
 #pragma unroll
-  for (int s = 0; s < SG; ++s) e[s] = r[s] = 0.f;
+  for (int i = 0; i < CF4; ++i) w[i] = ch[i * NT + tid];
 #pragma unroll
-  for (int i = 0; i < KW / 4; ++i) {
-    const wv4 we = w[i], wr = w[8 + i];
+  for (int h = 0; h < 2; ++h) {
+    const float4 we = w[h], wr = w[2 + h];
 #pragma unroll
     for (int s = 0; s < SG; ++s) {
-      const float4 x = *(const float4 *)&xs[s][kp][4 * i];
+      const float4 x = *(const float4 *)&xs[s][kp][8 * c + 4 * h];
       e[s] = fmaf(we.x, x.x, e[s]);
       e[s] = fmaf(we.y, x.y, e[s]);
       e[s] = fmaf(we.z, x.z, e[s]);
@@ -101,94 +169,37 @@ __device__ __forceinline__ void layer_products(const wv4 (&w)[NCH], const float 
       r[s] = fmaf(wr.w, x.w, r[s]);
     }
   }
-#pragma unroll
-  for (int s = 0; s < SG; ++s) {
-    red[kp][oc][s] = e[s];
-    red[kp][oc][SG + s] = r[s];
-  }
 }
 
-__device__ __forceinline__ void load_layer_weights(wv4 (&w)[NCH], const float4 *wl, int l, int j, int tid) {
-  const wv4 *src = (const wv4 *)(wl + ((size_t)l * NBG + j) * NCH * NT + tid);
+// The streaming wave: every chunk of the launch (n_steps x (4 L + 1)) into ring slot k mod ns, one
+// chunk in flight; a slot is refilled once every compute wave has finished reading its last chunk.
+__device__ __forceinline__ void stream_weights(Lds &s, float4 *ring, const float4 *wl, const float4 *wo4, int L,
+                                               int j, int ns, long long n_steps, int lane, uint32_t *sticky) {
+  const int per_step = CPL * L + 1;
+  const long long total = n_steps * per_step;
+  int q = 0, slot = 0;
+  for (long long k = 0; k < total; ++k) {
+    if (k >= ns) {
+      // the slot's previous chunk (k - ns) read by all four compute waves
+      const int want = (int)(k - ns + 1);
 #pragma unroll
-  for (int i = 0; i < NCH; ++i) w[i] = src[i * NT];
-}
-
-// The weights of index t of the per-step sequence (layer t for t < L, the output 1x1's NCO chunks
-// for t == L, nothing beyond).
-__device__ __forceinline__ void load_seq_weights(wv4 (&w)[NCH], const float4 *wl, const float4 *wo4, int t, int L,
-                                                 int j, int tid) {
-  if (t < L) {
-    load_layer_weights(w, wl, t, j, tid);
-  } else if (t == L) {
-    const wv4 *src = (const wv4 *)(wo4 + (size_t)j * NCO * NT + tid);
-#pragma unroll
-    for (int i = 0; i < NCO; ++i) w[i] = src[i * NT];
-    // the rest of the buffer is written too (a buffer written in part on one path stayed in scratch)
-#pragma unroll
-    for (int i = NCO; i < NCH; ++i) w[i] = wv4{0.f, 0.f, 0.f, 0.f};
-  }
-}
-
-// (plain values and pointers only: a reference to a by-value kernel argument would move the argument
-// to scratch memory)
-struct WideLayerCtx {
-  void *comm;
-  const float *convb;
-  Lds *sp;
-  const int *qoff, *slot;
-  float *Pq, *Xq;
-  const float4 *wl, *wo4;
-  uint32_t *abort_word, *sticky;
-  int L, g, j, tid, wave, oc, kp;
-  bool local, residual;
-};
-
-// One layer: products from the weights in wc (the next-but-one index of the sequence fetched into
-// wp first), the epilogue of the block's channels, the gather of the layer output.
-__device__ __forceinline__ void wide_layer(const WideLayerCtx &c, int l, const wv4 (&wc)[NCH], wv4 (&wp)[NCH],
-                                           uint32_t tag) {
-  Lds &s = *c.sp;
-  const int cur = l & 1, L = c.L, tid = c.tid, j = c.j, g = c.g;
-  load_seq_weights(wp, c.wl, c.wo4, l + 2, L, j, tid);
-  layer_products(wc, s.xg[cur], c.oc, c.kp, s.red);
-  __syncthreads();
-  // epilogue of the block's channels (wave 0, lane = (s, oc)): pop the product pushed d steps ago,
-  // push this step's
-  if (c.wave == 0) {
-    const int o2 = tid & (OC - 1), st = tid >> 4, ch = 16 * j + o2;
-    float e = 0.f, r = 0.f;
-#pragma unroll
-    for (int p = 0; p < KP; ++p) {
-      e += s.red[p][o2][st];
-      r += s.red[p][o2][SG + st];
+      for (int w = 0; w < 4; ++w) wait_ge(s, (lds_flag *)&s.cons[w], want, sticky);
     }
-    const size_t ent = ((size_t)(c.qoff[l] + c.slot[l]) * OC + o2) * SG + st;
-    const float xin = s.xg[cur][st][ch / KW][ch % KW];
-    const float act = fmaxf(e + c.Pq[ent] + c.convb[l * C + ch], 0.f);
-    const float xo = c.residual ? xin + act : act;
-    c.Pq[ent] = r;
-    c.Xq[ent] = xin;
-    // the layer output to the group: word (s, oc) of this block's slice, two per store
-    const float xo1 = __shfl_down(xo, 1, 64);
-    if (o2 % 2 == 0)
-      put_words2(g_x(c.comm, L, g, l) + j * OC * SG + st * OC + o2, __float_as_uint(xo), __float_as_uint(xo1),
-                 tag, c.local);
-  }
-  // gather the whole layer output into the other buffer (this block's own slice included)
-  {
-    uint32_t v[8];
-    wait_words<8, NT>(g_x(c.comm, L, g, l) + tid, tag, v, c.abort_word, c.sticky);
+    const float4 *src = q < CPL * L ? wl + ((size_t)q * NBG + j) * CHUNK : wo4 + (size_t)j * CHUNK;
+    float4 v[CHUNK / NTL];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int wi = e * NT + tid, jb = wi / (OC * SG), rr = wi % (OC * SG), st = rr / OC, ch = 16 * jb + rr % OC;
-      s.xg[cur ^ 1][st][ch / KW][ch % KW] = __uint_as_float(v[e]);
-    }
+    for (int u = 0; u < CHUNK / NTL; ++u) v[u] = src[u * NTL + lane];
+    float4 *dst = ring + (size_t)slot * CHUNK;
+#pragma unroll
+    for (int u = 0; u < CHUNK / NTL; ++u) dst[u * NTL + lane] = v[u];
+    compiler_fence();
+    if (lane == 0) *(lds_flag *)&s.ready[slot] = (int)(k + 1);
+    q = q + 1 == per_step ? 0 : q + 1;
+    slot = slot + 1 == ns ? 0 : slot + 1;
   }
-  __syncthreads();
 }
 
-__global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
+__global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArgs w) {
   extern __shared__ float4 lds_raw[];
   Lds &s = *(Lds *)lds_raw;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -196,22 +207,29 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
   if (g >= G) return;  // this group has no streams (all of its threads leave before any barrier)
   const int b0 = g * SG;                       // the group's first stream
   const int nval = min(SG, a.batch - b0);      // its valid streams
+  const int ns = w.nslots;
   int *dil = (int *)((char *)lds_raw + lds_tables(L));
   int *qoff = dil + L, *slot = qoff + L;
-  float *Pq = (float *)((char *)lds_raw + lds_queues(L));  // [entries][OC][SG]
-  float *Xq = Pq + (size_t)w.entries * OC * SG;
+  float4 *ring = (float4 *)((char *)lds_raw + lds_ring(L));
+  float *Pq = (float *)((char *)lds_raw + lds_queue(L, ns));  // [entries][OC][SG]
   uint32_t *abort_word = (uint32_t *)a.sp_comm, *sticky = a.sp_sticky;
   const float4 *wl = (const float4 *)w.wl, *wo4 = (const float4 *)w.wo;
   const int oc = tid & (OC - 1), kp = tid >> 4;
   const bool residual = a.kind == 1;  // relu + residual (FWG_RELU_RESIDUAL)
 
-  // ---- per-layer tables
-  for (int l = tid; l < L; l += NT) {
+  // ---- per-layer tables, ring flags and counters
+  for (int l = tid; l < L; l += NT + NTL) {
     int off = 0;
     for (int i = 0; i < l; ++i) off += a.layers[i].dil;
     dil[l] = a.layers[l].dil;
     qoff[l] = off;
     slot[l] = (int)(a.t0 % (long long)a.layers[l].dil);
+  }
+  if (tid < MAXSLOT) s.ready[tid] = 0;
+  if (tid < 4) s.cons[tid] = 0;
+  if (tid == 0) {
+    s.cbar = 0;
+    s.abort_ = 0;
   }
   // ---- launch handshake: every block reports its XCD; block 0 tells the group whether all share one
   u64 *hs = g_hs(a.sp_comm, L, g);
@@ -239,7 +257,7 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
     if (tid < nval) v = a.mode == MODE_TEACHER ? a.inputs[(long long)bb * a.n_steps] : a.last[bb];
     s.in[tid] = v;
   }
-  for (int e = tid; e < KCH * SG; e += NT) {
+  for (int e = tid; e < KCH * SG; e += NT + NTL) {
     const int jj = e / SG, st = e % SG, bb = b0 + st;
     const long long nx = jj + forced_shift(a.mode);
     s.fin[0][jj][st] = (a.mode != MODE_GENERATE && st < nval && nx < a.n_steps) ? a.inputs[(long long)bb * a.n_steps + nx] : 0;
@@ -251,44 +269,59 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
   __syncthreads();
   const bool local = s.mode != 0;
 
-  // ---- the launch's state: the states of this block's channels from the workspace queues, and the
-  // products W_r x of every queued state (a pass over each layer's slots with the layer's weights)
-  {
-    wv4 wv[NCH];
-    for (int l = 0; l < L; ++l) {
-      load_layer_weights(wv, wl, l, j, tid);
-      const float *src = (const float *)a.ring + a.layers[l].ring_off;
-      for (int sl = 0; sl < dil[l]; ++sl) {
-        // the whole queued state (all 512 channels, 4 streams) into xg[0]
-        for (int e = tid; e < SG * C; e += NT) {
-          const int st = e / C, c = e % C;
-          s.xg[0][st][c / KW][c % KW] = st < nval ? src[((long long)sl * a.bmax + b0 + st) * C + c] : 0.f;
-        }
-        __syncthreads();
-        layer_products(wv, s.xg[0], oc, kp, s.red);
-        __syncthreads();
-        if (tid < OC * SG) {
-          const int o2 = tid & (OC - 1), st = tid >> 4;
-          float r = 0.f;
+  // ---- the streaming wave: from here on it runs on its own
+  if (tid >= NT) {
+    stream_weights(s, ring, wl, wo4, L, j, ns, a.n_steps, lane, sticky);
+    return;
+  }
+
+  int ph = 0;  // compute-wave barrier count
+  // ---- the launch's state: the products W_r x of every queued state of this block's channels (a
+  // pass over each layer's slots with the layer's W_r rows, read straight from the packed weights)
+  for (int l = 0; l < L; ++l) {
+    float4 wr[2 * CPL];
 #pragma unroll
-          for (int p = 0; p < KP; ++p) r += s.red[p][o2][SG + st];
-          const size_t ent = ((size_t)(qoff[l] + sl) * OC + o2) * SG + st;
-          Pq[ent] = r;
-          Xq[ent] = s.xg[0][st][(16 * j + o2) / KW][(16 * j + o2) % KW];
-        }
-        __syncthreads();
+    for (int c = 0; c < CPL; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) wr[2 * c + h] = wl[((size_t)(CPL * l + c) * NBG + j) * CHUNK + (2 + h) * NT + tid];
+    const float *src = (const float *)a.ring + a.layers[l].ring_off;
+    for (int sl = 0; sl < dil[l]; ++sl) {
+      // the whole queued state (all 512 channels, 4 streams) into xg[0]
+      for (int e = tid; e < SG * C; e += NT) {
+        const int st = e / C, c = e % C;
+        s.xg[0][st][c / KW][c % KW] = st < nval ? src[((long long)sl * a.bmax + b0 + st) * C + c] : 0.f;
       }
+      cbar(s, ph, lane, sticky);
+      float r[SG];
+#pragma unroll
+      for (int st = 0; st < SG; ++st) r[st] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 2 * CPL; ++i) {
+#pragma unroll
+        for (int st = 0; st < SG; ++st) {
+          const float4 x = *(const float4 *)&s.xg[0][st][kp][4 * i];
+          r[st] = fmaf(wr[i].x, x.x, r[st]);
+          r[st] = fmaf(wr[i].y, x.y, r[st]);
+          r[st] = fmaf(wr[i].z, x.z, r[st]);
+          r[st] = fmaf(wr[i].w, x.w, r[st]);
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < SG; ++st) s.red[kp][oc][SG + st] = r[st];
+      cbar(s, ph, lane, sticky);
+      if (tid < OC * SG) {
+        const int o2 = tid & (OC - 1), st = tid >> 4;
+        float rr = 0.f;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) rr += s.red[p][o2][SG + st];
+        Pq[((size_t)(qoff[l] + sl) * OC + o2) * SG + st] = rr;
+      }
+      cbar(s, ph, lane, sticky);
     }
   }
 
   const float *embT = w.embT, *embb = w.embb, *convb = w.convb, *outb = w.outb;
-  // weights stream through three register buffers, two layers ahead (index t of the step's
-  // sequence in buffer t mod 3: layers 0..L-1, then the output 1x1): with one layer in flight the
-  // group's loads did not cover the latency of the last-level cache
-  wv4 W0[NCH], W1[NCH], W2[NCH];
-  load_seq_weights(W0, wl, wo4, 0, L, j, tid);
-  load_seq_weights(W1, wl, wo4, 1, L, j, tid);
-
+  long long k = 0;  // chunk of the launch the compute waves take next
   for (int step = 0; step < a.n_steps; ++step) {
     const uint32_t tag = (uint32_t)(step + 1);
     // ---- layer input x^0 (the embedding of the step's inputs), all 512 channels
@@ -296,13 +329,65 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       const int st = e / C, c = e % C;
       s.xg[0][st][c / KW][c % KW] = embT[(size_t)s.in[st] * C + c] + embb[c];
     }
-    __syncthreads();
-    const WideLayerCtx cx{a.sp_comm, w.convb, &s, qoff, slot, Pq, Xq, wl, wo4, abort_word, sticky,
-                          L, g, j, tid, wave, oc, kp, local, residual};
-    for (int l = 0; l < L; l += 3) {
-      wide_layer(cx, l, W0, W2, tag);
-      if (l + 1 < L) wide_layer(cx, l + 1, W1, W0, tag);
-      if (l + 2 < L) wide_layer(cx, l + 2, W2, W1, tag);
+    cbar(s, ph, lane, sticky);
+    for (int l = 0; l < L; ++l) {
+      const int cur = l & 1;
+      float e[SG], r[SG];
+#pragma unroll
+      for (int st = 0; st < SG; ++st) e[st] = r[st] = 0.f;
+#pragma unroll
+      for (int c = 0; c < CPL; ++c) {
+        const float4 *ch = take_chunk(s, ring, k, ns, sticky);
+        chunk_products(ch, s.xg[cur], tid, kp, c, e, r);
+        done_chunk(s, wave, lane, k);
+        ++k;
+      }
+#pragma unroll
+      for (int st = 0; st < SG; ++st) {
+        s.red[kp][oc][st] = e[st];
+        s.red[kp][oc][SG + st] = r[st];
+      }
+      cbar(s, ph, lane, sticky);
+      // epilogue of the block's channels (wave 0, lane = (s, oc)): pop the product pushed d steps
+      // ago, push this step's
+      float xin = 0.f;
+      if (wave == 0) {
+        const int o2 = tid & (OC - 1), st = tid >> 4, ch = 16 * j + o2;
+        float ee = 0.f, rr = 0.f;
+#pragma unroll
+        for (int p = 0; p < KP; ++p) {
+          ee += s.red[p][o2][st];
+          rr += s.red[p][o2][SG + st];
+        }
+        const size_t ent = ((size_t)(qoff[l] + slot[l]) * OC + o2) * SG + st;
+        xin = s.xg[cur][st][ch / KW][ch % KW];
+        const float act = fmaxf(ee + Pq[ent] + convb[l * C + ch], 0.f);
+        const float xo = residual ? xin + act : act;
+        Pq[ent] = rr;
+        // the layer output to the group: word (s, oc) of this block's slice, two per store
+        const float xo1 = __shfl_down(xo, 1, 64);
+        if (o2 % 2 == 0)
+          put_words2(g_x(a.sp_comm, L, g, l) + j * OC * SG + st * OC + o2, __float_as_uint(xo), __float_as_uint(xo1),
+                     tag, local);
+      }
+      // gather the whole layer output into the other buffer (this block's own slice included)
+      {
+        uint32_t v[8];
+        wait_words<8, NT>(g_x(a.sp_comm, L, g, l) + tid, tag, v, abort_word, sticky);
+#pragma unroll
+        for (int ee = 0; ee < 8; ++ee) {
+          const int wi = ee * NT + tid, jb = wi / (OC * SG), rr = wi % (OC * SG), st = rr / OC, ch = 16 * jb + rr % OC;
+          s.xg[cur ^ 1][st][ch / KW][ch % KW] = __uint_as_float(v[ee]);
+        }
+      }
+      // the layer input of the block's channels to the workspace queue, once every block of the
+      // group has published this layer (so none is still reading the queues in its state pass)
+      if (wave == 0) {
+        const int o2 = tid & (OC - 1), st = tid >> 4;
+        if (st < nval)
+          ((float *)a.ring)[a.layers[l].ring_off + ((long long)slot[l] * a.bmax + b0 + st) * C + 16 * j + o2] = xin;
+      }
+      cbar(s, ph, lane, sticky);
     }
     // ---- output 1x1: classes 8j..8j+7; thread (c8, kq) covers K part kq (16 channels)
     {
@@ -311,28 +396,29 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       float acc[SG];
 #pragma unroll
       for (int st = 0; st < SG; ++st) acc[st] = 0.f;
-      const int ob = L % 3;  // the output 1x1's weights: index L of the sequence
+      const float4 *ch = take_chunk(s, ring, k, ns, sticky);
+      float4 wv[NCO];
+#pragma unroll
+      for (int i = 0; i < NCO; ++i) wv[i] = ch[i * NT + tid];
+      done_chunk(s, wave, lane, k);
+      ++k;
 #pragma unroll
       for (int i = 0; i < NCO; ++i) {
-        const wv4 wv = ob == 0 ? W0[i] : ob == 1 ? W1[i] : W2[i];
-        const int k = 16 * kq + 4 * i;
+        const int kk = 16 * kq + 4 * i;
 #pragma unroll
         for (int st = 0; st < SG; ++st) {
-          const float4 x = *(const float4 *)&s.xg[lastp][st][k / KW][k % KW];
-          acc[st] = fmaf(wv.x, x.x, acc[st]);
-          acc[st] = fmaf(wv.y, x.y, acc[st]);
-          acc[st] = fmaf(wv.z, x.z, acc[st]);
-          acc[st] = fmaf(wv.w, x.w, acc[st]);
+          const float4 x = *(const float4 *)&s.xg[lastp][st][kk / KW][kk % KW];
+          acc[st] = fmaf(wv[i].x, x.x, acc[st]);
+          acc[st] = fmaf(wv[i].y, x.y, acc[st]);
+          acc[st] = fmaf(wv[i].z, x.z, acc[st]);
+          acc[st] = fmaf(wv[i].w, x.w, acc[st]);
         }
       }
       // 32 K parts x 8 classes x 4 streams of partial sums (the layer scratch viewed flat)
       float *r2 = &s.red[0][0][0];
 #pragma unroll
       for (int st = 0; st < SG; ++st) r2[(kq * QB + c8) * SG + st] = acc[st];
-      // the next step's first two indices, read while the logits are summed and sampled
-      load_seq_weights(W0, wl, wo4, 0, L, j, tid);
-      load_seq_weights(W1, wl, wo4, 1, L, j, tid);
-      __syncthreads();
+      cbar(s, ph, lane, sticky);
       if (wave == 0) {
         // lanes 0..31: (s, class); lanes 32..63 repeat them and store nothing
         const int cc = tid & (QB - 1), st = (tid >> 3) & (SG - 1), cls = QB * j + cc;
@@ -358,9 +444,9 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
       if (a.mode == MODE_GENERATE) {
         const float4 lg4 = make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
                                        __uint_as_float(v[3]));
-        const int k = sample_row4(lg4, s.u[(step / KCH) & 1][step % KCH]);
-        if (lane == 0 && j < nval) a.samples[(long long)(b0 + j) * a.n_steps + step] = k;
-        res = (uint32_t)k;
+        const int kc = sample_row4(lg4, s.u[(step / KCH) & 1][step % KCH]);
+        if (lane == 0 && j < nval) a.samples[(long long)(b0 + j) * a.n_steps + step] = kc;
+        res = (uint32_t)kc;
       }
       if (lane == 0) put_word(g_smp(a.sp_comm, L, g) + HSLOT * j, res, tag, local);
     }
@@ -385,42 +471,34 @@ __global__ void __launch_bounds__(NT) wide_step_kernel(StepArgs a, WideArgs w) {
                             ? a.uniforms[(long long)bb * a.n_steps + base + tid] : 0.f;
       }
     }
-    __syncthreads();
+    cbar(s, ph, lane, sticky);
   }
-
-  // ---- launch end: the states of this block's channels back to the workspace queues; the pending
-  // inputs (block 0 of the group)
-  for (int l = 0; l < L; ++l) {
-    float *dst = (float *)a.ring + a.layers[l].ring_off;
-    for (int e = tid; e < dil[l] * OC * SG; e += NT) {
-      const int sl = e / (OC * SG), rr = e % (OC * SG), o2 = rr / SG, st = rr % SG;
-      if (st < nval) dst[((long long)sl * a.bmax + b0 + st) * C + 16 * j + o2] = Xq[(size_t)(qoff[l] + sl) * OC * SG + rr];
-    }
-  }
+  // the pending inputs (block 0 of the group)
   if (j == 0 && tid < nval && a.mode != MODE_TEACHER) a.last[b0 + tid] = s.in[tid];
 }
 
 // ---- repacking (once per fwg_create)
 __global__ void wide_pack_layer_kernel(const float *conv, int l, float4 *wl) {
-  // chunk i of thread t of block j: oc = t % 16, kp = t / 16; i < 8: W_e[16j + oc][32 kp + 4i ..],
-  // i >= 8: W_r[16j + oc][32 kp + 4(i - 8) ..]; conv is [C][C][2] (tap 0 = W_r, tap 1 = W_e)
+  // float4 i of compute thread t of block j in chunk c: oc = t % 16, kp = t / 16; i < 2:
+  // W_e[16j + oc][32 kp + 8c + 4i ..], i >= 2: W_r[16j + oc][32 kp + 8c + 4(i - 2) ..]; conv is
+  // [C][C][2] (tap 0 = W_r, tap 1 = W_e)
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= NBG * NCH * NT) return;
-  const int t = e % NT, i = (e / NT) % NCH, jb = e / (NT * NCH);
-  const int o = 16 * jb + (t & (OC - 1)), k0 = KW * (t >> 4) + 4 * (i & 7), tap = i < 8 ? 1 : 0;
+  if (e >= NBG * CPL * CHUNK) return;
+  const int t = e % NT, i = (e / NT) % CF4, jb = (e / CHUNK) % NBG, c = e / (CHUNK * NBG);
+  const int o = 16 * jb + (t & (OC - 1)), k0 = KW * (t >> 4) + 8 * c + 4 * (i & 1), tap = i < 2 ? 1 : 0;
   float v[4];
   for (int q = 0; q < 4; ++q) v[q] = conv[((size_t)o * C + k0 + q) * 2 + tap];
-  wl[((size_t)l * NBG + jb) * NCH * NT + (size_t)i * NT + t] = make_float4(v[0], v[1], v[2], v[3]);
+  wl[((size_t)(CPL * l + c) * NBG + jb) * CHUNK + (size_t)i * NT + t] = make_float4(v[0], v[1], v[2], v[3]);
 }
 __global__ void wide_pack_out_kernel(const float *out, float4 *wo) {
-  // chunk i of thread t of block j: class 8j + t % 8, channels 16 (t / 8) + 4i ..
+  // float4 i of thread t of block j: class 8j + t % 8, channels 16 (t / 8) + 4i ..
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= NBG * NCO * NT) return;
-  const int t = e % NT, i = (e / NT) % NCO, jb = e / (NT * NCO);
+  if (e >= NBG * CHUNK) return;
+  const int t = e % NT, i = (e / NT) % NCO, jb = e / CHUNK;
   const int cls = QB * jb + (t & (QB - 1)), k0 = 16 * (t >> 3) + 4 * i;
   float v[4];
   for (int q = 0; q < 4; ++q) v[q] = out[(size_t)cls * C + k0 + q];
-  wo[((size_t)jb * NCO + i) * NT + t] = make_float4(v[0], v[1], v[2], v[3]);
+  wo[(size_t)jb * CHUNK + (size_t)i * NT + t] = make_float4(v[0], v[1], v[2], v[3]);
 }
 __global__ void wide_transpose_kernel(const float *src, float *dst, int rows, int cols) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
@@ -441,12 +519,19 @@ bool wide_layout(int kind, int dtype, int C, int Q, int L, int w, int bmax, cons
     return false;
   long long ent = 0;
   for (int l = 0; l < L; ++l) ent += dil[l];
+  if (ent >= (1 << 20)) return false;
   g->entries = (int)ent;
-  g->wl_bytes = (size_t)L * wd::NBG * wd::NCH * wd::NT * 16;
-  g->wo_bytes = (size_t)wd::NBG * wd::NCO * wd::NT * 16;
-  *lds = wd::lds_queues(L) + (size_t)2 * ent * wd::OC * wd::SG * 4;
+  g->wl_bytes = (size_t)L * wd::CPL * wd::NBG * wd::CHUNK * 16;
+  g->wo_bytes = (size_t)wd::NBG * wd::CHUNK * 16;
+  // the ring takes what LDS is left after the tables and the queue, at most MAXSLOT slots; at least
+  // three keep the stream ahead of the products
+  const size_t limit = 160 * 1024, fixed = wd::lds_ring(L) + (size_t)ent * wd::OC * wd::SG * 4;
+  if (fixed + (size_t)3 * wd::CHUNK * 16 > limit) return false;
+  const size_t ns = (limit - fixed) / ((size_t)wd::CHUNK * 16);
+  g->nslots = (int)(ns < (size_t)wd::MAXSLOT ? ns : wd::MAXSLOT);
+  *lds = fixed + (size_t)g->nslots * wd::CHUNK * 16;
   *comm_bytes = 256 + (size_t)wd::NG * wd::group_words(L) * 8;
-  return ent < (1 << 20) && *lds <= 160 * 1024;
+  return true;
 }
 
 size_t wide_comm_bytes(int L) { return 256 + (size_t)wd::NG * wd::group_words(L) * 8; }
@@ -456,7 +541,8 @@ hipError_t wide_setup(size_t lds, int *coresident_ok) {
                                      (int)lds);
   if (e != hipSuccess) return e;
   int per_cu = 0, dev = 0, cus = 0;
-  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wd::wide_step_kernel, wd::NT, lds)) != hipSuccess)
+  if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wd::wide_step_kernel, wd::NT + wd::NTL, lds)) !=
+      hipSuccess)
     return e;
   if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
   if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
@@ -465,7 +551,7 @@ hipError_t wide_setup(size_t lds, int *coresident_ok) {
 }
 
 hipError_t launch_wide_step(const StepArgs &a, const WideArgs &g, size_t lds, hipStream_t s) {
-  hipLaunchKernelGGL(wd::wide_step_kernel, dim3(wd::NG * wd::NBG), dim3(wd::NT), lds, s, a, g);
+  hipLaunchKernelGGL(wd::wide_step_kernel, dim3(wd::NG * wd::NBG), dim3(wd::NT + wd::NTL), lds, s, a, g);
   return hipGetLastError();
 }
 
@@ -474,12 +560,12 @@ hipError_t launch_wide_pack(const void *embed, const float *embed_b, const void 
                             hipStream_t s) {
   const int C = kWideC, Q = 256;
   for (int l = 0; l < L; ++l) {
-    hipLaunchKernelGGL(wd::wide_pack_layer_kernel, dim3((wd::NBG * wd::NCH * wd::NT + 255) / 256), dim3(256), 0, s,
+    hipLaunchKernelGGL(wd::wide_pack_layer_kernel, dim3((wd::NBG * wd::CPL * wd::CHUNK + 255) / 256), dim3(256), 0, s,
                        (const float *)conv[l], l, (float4 *)g.wl);
     hipLaunchKernelGGL(wd::wide_vec_kernel, dim3((C + 255) / 256), dim3(256), 0, s, conv_b ? conv_b[l] : nullptr,
                        (float *)g.convb + (size_t)l * C, C);
   }
-  hipLaunchKernelGGL(wd::wide_pack_out_kernel, dim3((wd::NBG * wd::NCO * wd::NT + 255) / 256), dim3(256), 0, s,
+  hipLaunchKernelGGL(wd::wide_pack_out_kernel, dim3((wd::NBG * wd::CHUNK + 255) / 256), dim3(256), 0, s,
                      (const float *)out, (float4 *)g.wo);
   hipLaunchKernelGGL(wd::wide_transpose_kernel, dim3((C * Q + 255) / 256), dim3(256), 0, s, (const float *)embed,
                      (float *)g.embT, C, Q);
