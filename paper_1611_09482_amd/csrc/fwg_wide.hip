@@ -82,11 +82,14 @@ struct Lds {
   int cons[4];              // chunks each compute wave has finished reading
   int cbar;                 // compute-wave barrier counter (each wave adds 1 per barrier)
   int abort_;               // an LDS wait ran out: later LDS waits return at once
-  // followed by the per-layer tables dil[L], qoff[L], slot[L], the ring of weight slots and the
-  // queue P[entries][OC][SG] (products W_r x), entries = sum of dilations
+  // followed by the per-layer tables dil[L], qoff[L], slot[L], the conv biases of the block's
+  // channels [L][OC], the ring of weight slots and the queue P[entries][OC][SG] (products W_r x),
+  // entries = sum of dilations
 };
 __host__ __device__ inline size_t lds_tables(int L) { return (sizeof(Lds) + 15) & ~(size_t)15; }
-__host__ __device__ inline size_t lds_ring(int L) { return lds_tables(L) + (((size_t)3 * L * 4 + 15) & ~(size_t)15); }
+__host__ __device__ inline size_t lds_ring(int L) {
+  return lds_tables(L) + (((size_t)(3 + OC) * L * 4 + 15) & ~(size_t)15);
+}
 __host__ __device__ inline size_t lds_queue(int L, int ns) { return lds_ring(L) + (size_t)ns * CHUNK * 16; }
 
 // ---- packed weights (per block j, same for every group): chunk c of layer l at
@@ -171,31 +174,41 @@ __device__ __forceinline__ void chunk_products(const float4 *ch, const float (*x
   }
 }
 
-// The streaming wave: every chunk of the launch (n_steps x (4 L + 1)) into ring slot k mod ns, one
-// chunk in flight; a slot is refilled once every compute wave has finished reading its last chunk.
-__device__ __forceinline__ void stream_weights(Lds &s, float4 *ring, const float4 *wl, const float4 *wo4, int L,
-                                               int j, int ns, long long n_steps, int lane, uint32_t *sticky) {
-  const int per_step = CPL * L + 1;
-  const long long total = n_steps * per_step;
-  int q = 0, slot = 0;
+// The streaming wave: every chunk of the launch (n_steps x (4 L + 1)) into ring slot k mod ns with
+// loads that write LDS directly (no register copy), one chunk in flight (a second one made the
+// compute waves' polls wait longer behind the stream's loads and the step slower); a slot is
+// loaded once every compute wave has finished reading its last chunk.
+struct Stream {
+  const float4 *wl, *wo4;
+  int L, j, ns, per_step;
+};
+__device__ __forceinline__ const float4 *chunk_src(const Stream &m, int q) {
+  return q < CPL * m.L ? m.wl + ((size_t)q * NBG + m.j) * CHUNK : m.wo4 + (size_t)m.j * CHUNK;
+}
+__device__ __forceinline__ void stream_weights(Lds &s, float4 *ring, const Stream &m, long long n_steps, int lane,
+                                               uint32_t *sticky) {
+  const long long total = n_steps * m.per_step;
+  int q = 0, slot = 0;  // chunk of the step and ring slot of chunk k
   for (long long k = 0; k < total; ++k) {
-    if (k >= ns) {
+    if (k >= m.ns) {
       // the slot's previous chunk (k - ns) read by all four compute waves
-      const int want = (int)(k - ns + 1);
+      const int want = (int)(k - m.ns + 1);
 #pragma unroll
       for (int w = 0; w < 4; ++w) wait_ge(s, (lds_flag *)&s.cons[w], want, sticky);
     }
-    const float4 *src = q < CPL * L ? wl + ((size_t)q * NBG + j) * CHUNK : wo4 + (size_t)j * CHUNK;
-    float4 v[CHUNK / NTL];
-#pragma unroll
-    for (int u = 0; u < CHUNK / NTL; ++u) v[u] = src[u * NTL + lane];
+    const float4 *src = chunk_src(m, q) + lane;
     float4 *dst = ring + (size_t)slot * CHUNK;
+    // lane i's 16 bytes of each load land at dst + 16 i (64 lanes: 1 KB per load)
 #pragma unroll
-    for (int u = 0; u < CHUNK / NTL; ++u) dst[u * NTL + lane] = v[u];
+    for (int u = 0; u < CHUNK / NTL; ++u)
+      __builtin_amdgcn_global_load_lds((const void *)(src + u * NTL), (__attribute__((address_space(3))) void *)(dst + u * NTL),
+                                       16, 0, 0);
+    // vmcnt(0): the chunk is in LDS (the count drops once a load's data is written there)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     compiler_fence();
     if (lane == 0) *(lds_flag *)&s.ready[slot] = (int)(k + 1);
-    q = q + 1 == per_step ? 0 : q + 1;
-    slot = slot + 1 == ns ? 0 : slot + 1;
+    q = q + 1 == m.per_step ? 0 : q + 1;
+    slot = slot + 1 == m.ns ? 0 : slot + 1;
   }
 }
 
@@ -210,6 +223,7 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
   const int ns = w.nslots;
   int *dil = (int *)((char *)lds_raw + lds_tables(L));
   int *qoff = dil + L, *slot = qoff + L;
+  float *cb = (float *)(slot + L);  // [L][OC]: conv biases of the block's channels (no global load per layer)
   float4 *ring = (float4 *)((char *)lds_raw + lds_ring(L));
   float *Pq = (float *)((char *)lds_raw + lds_queue(L, ns));  // [entries][OC][SG]
   uint32_t *abort_word = (uint32_t *)a.sp_comm, *sticky = a.sp_sticky;
@@ -225,6 +239,7 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
     qoff[l] = off;
     slot[l] = (int)(a.t0 % (long long)a.layers[l].dil);
   }
+  for (int i = tid; i < L * OC; i += NT + NTL) cb[i] = w.convb[(i / OC) * C + 16 * j + i % OC];
   if (tid < MAXSLOT) s.ready[tid] = 0;
   if (tid < 4) s.cons[tid] = 0;
   if (tid == 0) {
@@ -271,7 +286,8 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
 
   // ---- the streaming wave: from here on it runs on its own
   if (tid >= NT) {
-    stream_weights(s, ring, wl, wo4, L, j, ns, a.n_steps, lane, sticky);
+    const Stream m{wl, wo4, L, j, ns, CPL * L + 1};
+    stream_weights(s, ring, m, a.n_steps, lane, sticky);
     return;
   }
 
@@ -320,7 +336,7 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
     }
   }
 
-  const float *embT = w.embT, *embb = w.embb, *convb = w.convb, *outb = w.outb;
+  const float *embT = w.embT, *embb = w.embb, *outb = w.outb;
   long long k = 0;  // chunk of the launch the compute waves take next
   for (int step = 0; step < a.n_steps; ++step) {
     const uint32_t tag = (uint32_t)(step + 1);
@@ -335,13 +351,15 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
       float e[SG], r[SG];
 #pragma unroll
       for (int st = 0; st < SG; ++st) e[st] = r[st] = 0.f;
+      // one wait for the layer's last chunk: the stream writes chunks in order, and none of the
+      // layer's slots is refilled before this wave has read it (at least four slots), so the LDS reads
+      // of all four chunks can run ahead of their products
+      take_chunk(s, ring, k + CPL - 1, ns, sticky);
 #pragma unroll
-      for (int c = 0; c < CPL; ++c) {
-        const float4 *ch = take_chunk(s, ring, k, ns, sticky);
-        chunk_products(ch, s.xg[cur], tid, kp, c, e, r);
-        done_chunk(s, wave, lane, k);
-        ++k;
-      }
+      for (int c = 0; c < CPL; ++c)
+        chunk_products(ring + (size_t)((k + c) % ns) * CHUNK, s.xg[cur], tid, kp, c, e, r);
+      done_chunk(s, wave, lane, k + CPL - 1);
+      k += CPL;
 #pragma unroll
       for (int st = 0; st < SG; ++st) {
         s.red[kp][oc][st] = e[st];
@@ -361,7 +379,7 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
         }
         const size_t ent = ((size_t)(qoff[l] + slot[l]) * OC + o2) * SG + st;
         xin = s.xg[cur][st][ch / KW][ch % KW];
-        const float act = fmaxf(ee + Pq[ent] + convb[l * C + ch], 0.f);
+        const float act = fmaxf(ee + Pq[ent] + cb[l * OC + o2], 0.f);
         const float xo = residual ? xin + act : act;
         Pq[ent] = rr;
         // the layer output to the group: word (s, oc) of this block's slice, two per store
@@ -524,9 +542,9 @@ bool wide_layout(int kind, int dtype, int C, int Q, int L, int w, int bmax, cons
   g->wl_bytes = (size_t)L * wd::CPL * wd::NBG * wd::CHUNK * 16;
   g->wo_bytes = (size_t)wd::NBG * wd::CHUNK * 16;
   // the ring takes what LDS is left after the tables and the queue, at most MAXSLOT slots; at least
-  // three keep the stream ahead of the products
+  // four: a compute wave waits once per layer, for its last chunk, with the other three in their slots
   const size_t limit = 160 * 1024, fixed = wd::lds_ring(L) + (size_t)ent * wd::OC * wd::SG * 4;
-  if (fixed + (size_t)3 * wd::CHUNK * 16 > limit) return false;
+  if (fixed + (size_t)wd::CPL * wd::CHUNK * 16 > limit) return false;
   const size_t ns = (limit - fixed) / ((size_t)wd::CHUNK * 16);
   g->nslots = (int)(ns < (size_t)wd::MAXSLOT ? ns : wd::MAXSLOT);
   *lds = fixed + (size_t)g->nslots * wd::CHUNK * 16;
