@@ -124,6 +124,9 @@ FAMILIES = {
     # (at most 32 layers they keep them in registers)
     "gated_r64_bf16_split36": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 6, 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
+    # dilations 1..128: queues of 255 entries leave LDS for the wide kernel's smallest weight ring
+    # (four 16 KB slots, a whole layer's chunks)
+    "relures_c512_f32_q255": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 32, 64, 128)),
     "relures_c512_f32_valu": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     # filter width w > 2 (Section 3.1): queues of (w - 1) d states, w taps per product
     "relu_c32_w3_f32": W.ModelConfig(W.RELU, W.F32, 32, (1, 3, 9, 1, 3), filter_width=3),
@@ -150,7 +153,7 @@ CHAIN_PAIR_FAMILIES = {"gated_r32_f32", "gated_r32_f32_odd", "gated_r32_w3_f32"}
 FORCE_CHAIN1 = {"gated_r32_f32_one", "gated_r32_f32_odd_one", "gated_r32_w3_f32_one"}
 # families that must run on the wide kernels (float32 ReLU stacks with C = 512: each layer spread
 # over a group of 32 blocks)
-WIDE_FAMILIES = {"relures_c512_f32"}
+WIDE_FAMILIES = {"relures_c512_f32", "relures_c512_f32_q255"}
 # families whose test forces the general (VALU) kernel family instead of the MFMA, wave, chain or
 # wide one
 FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu", "gated_r32_f32_valu",
@@ -378,7 +381,7 @@ def test_generation_parity(fam):
 
 
 @pytest.mark.parametrize("fam", ["relu_c32_f32", "gated_r16_s32_f32", "gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_valu",
-                                 "gated_r64_w3_bf16", "gated_r64_bf16_split"])
+                                 "gated_r64_w3_bf16", "gated_r64_bf16_split", "relures_c512_f32"])
 def test_online_prediction_parity(fam):
     """Online prediction (fwg_step_forced): generate, feed observed samples from the same queues,
     generate again.  The oracle is driven through the same history (the GPU's own samples, then the
