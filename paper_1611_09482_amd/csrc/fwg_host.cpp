@@ -251,16 +251,16 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->rpw = rpw > 0 ? rpw : 1;
   p->valu_wbytes = stage ? (int)p->valu_block : 0;
 
-  // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512
+  // kernel family: the MFMA kernel covers gated bf16 stacks with R=64, S=H=512, filter width 2 or 3
   p->regime = REGIME_VALU;
   const char *force = getenv("FWG_REGIME");
-  const bool mfma_shape = w == 2 && p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR && p->S == kMfS &&
-                          p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
-                          mfma_lds_bytes(p->L) <= 160 * 1024;
-  // the split family takes the MFMA family's shape when L suits its unrolled layer loop
+  const bool mfma_shape = (w == 2 || w == 3) && p->kind == FWG_GATED && p->dtype == FWG_BF16 && p->C == kMfR &&
+                          p->S == kMfS && p->H == kMfH && p->Q == 256 && p->L <= kMfMaxLayers &&
+                          mfma_lds_bytes(p->L, w) <= 160 * 1024;
+  // the split family takes the MFMA family's shape at width 2 when L suits its unrolled layer loop
   // (FWG_REGIME=mfma keeps the single-block kernel); fwg_create falls back to it when the split
   // launch's blocks cannot all be resident at once
-  const bool split_shape = mfma_shape && split_layers_ok(p->L);
+  const bool split_shape = mfma_shape && w == 2 && split_layers_ok(p->L);
   if (mfma_shape && !(force && strcmp(force, "valu") == 0))
     p->regime = split_shape && !(force && strcmp(force, "mfma") == 0) ? REGIME_SPLIT : REGIME_MFMA;
   // small float32 ReLU stacks: one block per stream with the layer chain on one wavefront (chain
@@ -304,7 +304,7 @@ int make_plan(const fwg_desc *d, Plan *p) {
   p->off_frags = p->off_embT = p->off_bias = p->off_ptrtab = p->off_comm = p->off_sticky = 0;
   if (mf_family) {
     // either family's fragment streams fit (create may fall back from the split family)
-    p->off_frags = take(std::max(mfma_frag_bytes(p->L), split_shape ? split_frag_bytes(p->L) : size_t(0)));
+    p->off_frags = take(std::max(mfma_all_frag_bytes(p->L, w), split_shape ? split_frag_bytes(p->L) : size_t(0)));
     p->off_embT = take((size_t)p->Q * p->C * 2);
     p->off_bias = take(sizeof(float) * mfma_bias_floats(p->L));
     p->off_ptrtab = take(sizeof(void *) * 3 * p->L);
@@ -945,7 +945,7 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     char *frags = ws + p.off_frags;
     // layers first: a layer also writes fragments into the previous stage and the last head stage
     for (int l = 0; l < p.L; ++l)
-      TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));
+      TRY_OR_FREE(launch_mfma_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, p.w, frags, s));
     TRY_OR_FREE(launch_mfma_repack_head(w->head, w->out, p.L, frags, s));
   }
   if (h->plan.regime == REGIME_MFMA || h->plan.regime == REGIME_SPLIT) {
@@ -960,7 +960,7 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
     const float *const *pt = (const float *const *)(ws + p.off_ptrtab);
     TRY_OR_FREE(launch_mfma_bias_block(pt, pt + p.L, pt + 2 * p.L, w->head_b, w->out_b, w->embed_b, p.L,
                                        (float *)(ws + p.off_bias), s));
-    TRY_OR_FREE(set_mfma_lds_limit(mfma_lds_bytes(p.L)));
+    TRY_OR_FREE(set_mfma_lds_limit(mfma_lds_bytes(p.L, p.w)));
   }
   if (p.lds_bytes > 64 * 1024) TRY_OR_FREE(set_valu_lds_limit(p.lds_bytes));
   int rr = enqueue_reset(h);

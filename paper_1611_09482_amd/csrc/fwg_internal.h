@@ -82,7 +82,13 @@ constexpr int kMfHeadStages = 8;   // head: 96 fragments per wave (+ padding), 8
 constexpr int kMfMaxLayers = 128;
 constexpr size_t kMfStageBytes = (size_t)kMfWaves * kMfFrags * 1024;
 __host__ __device__ inline size_t mfma_frag_bytes(int L) { return kMfStageBytes * ((size_t)L + kMfHeadStages); }
-inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
+// Width 3: the oldest tap's recurrent fragments of each layer follow the stage streams, 4 per B wave
+// (tanh and sigmoid tile, two k-steps each).
+constexpr size_t kMfTapBytes = (size_t)4 * 4 * 1024;
+__host__ __device__ inline size_t mfma_all_frag_bytes(int L, int w) {
+  return mfma_frag_bytes(L) + (w == 3 ? kMfTapBytes * (size_t)L : 0);
+}
+__host__ __device__ inline size_t mfma_bias_floats(int L) { return (size_t)L * 3 * kMfR + kMfS + kMfH + 256 + kMfR; }
 
 // Split MFMA family (the MFMA family's model shape, L a multiple of 6 and at least 12): per 16
 // streams one chain block (the layers), kSpHelpers helper blocks, each owning S / kSpHelpers skip
@@ -111,11 +117,11 @@ hipError_t launch_repack(const void *src, void *dst, int mode, int dtype, int K,
 hipError_t launch_fill_zero(void *dst, size_t bytes, hipStream_t s);
 hipError_t launch_fill_i32(int32_t *dst, int32_t value, int n, hipStream_t s);
 hipError_t launch_copy_bias(const float *src, float *dst, int n, hipStream_t s);
-size_t mfma_lds_bytes(int L);
+size_t mfma_lds_bytes(int L, int w);
 hipError_t launch_mfma_step(const StepArgs &a, hipStream_t s);
 hipError_t set_mfma_lds_limit(size_t bytes);
-hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
-                                    hipStream_t s);
+hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, int w,
+                                    void *frags, hipStream_t s);
 hipError_t launch_mfma_repack_head(const void *head, const void *out, int L, void *frags, hipStream_t s);
 hipError_t launch_mfma_embed_table(const void *embed, void *dst, hipStream_t s);
 hipError_t launch_mfma_bias_block(const float *const *conv_b, const float *const *res_b, const float *const *skip_b,

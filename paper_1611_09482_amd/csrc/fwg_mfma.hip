@@ -4,9 +4,10 @@
 //
 // One block of 8 waves owns 16 independent streams; one launch runs n_steps
 // whole generation steps.  Per step and layer (paper Section 2.2): pop the
-// layer's queue (the state pushed d_l steps earlier), compute the dilated
-// width-2 product [W_r W_e] [v; x], the gate, the residual and skip 1x1
-// products, then push the layer's input into the slot just popped.  After the
+// layer's queue (the state pushed d_l steps earlier; at filter width 3 also the
+// one pushed 2 d_l steps earlier, Section 3.1), compute the dilated product
+// [W_r W_e] [v; x], the gate, the residual and skip 1x1 products, then push the
+// layer's input into the slot of the oldest state popped.  After the
 // last layer: relu(skip sum) -> 1x1 -> relu -> 1x1 -> logits, softmax and the
 // inverse-CDF sample, which becomes the next step's input (Section 1).
 //
@@ -19,9 +20,10 @@
 //  - wave p ("A", on the layer-to-layer dependency chain): the current-input half of the
 //    dilated product (W_e x) for tanh tile p and sigmoid tile p, the gate, the residual
 //    1x1 for tile p, and 7 of the 16 skip fragments of skip tiles 8p..8p+7;
-//  - wave p + 4 ("B"): the recurrent half (W_r v, v = the popped state, known early) of the
+//  - wave p + 4 ("B"): the recurrent half (W_r v, v = the popped states, known early) of the
 //    NEXT layer plus its bias, handed to A through LDS, the other 9 skip fragments, and the
-//    queue pops and pushes of rows 4p..4p+3.
+//    queue pops and pushes of rows 4p..4p+3.  At width 3 the oldest tap's fragments come from a
+//    stream of their own (4 per layer and wave), loaded one recurrent product ahead.
 // Both halves of the head are split the same way.  Every wave streams its own pre-packed
 // weight fragments from L2 (13 per stage, refilled one stage ahead as soon as consumed); a
 // wave stalls while the load unit is saturated, and the second wave on the SIMD keeps the
@@ -53,6 +55,7 @@ constexpr int KCH = 64;  // steps per chunk of per-step inputs staged in LDS
 
 struct Lds {
   uint16_t vbuf[2][ROWS * PX];     // popped queue rows (layer input d steps ago), by stage parity
+                                   // (width 3: the rows 2d steps ago follow the bias block)
   uint16_t xbuf[2][ROWS * PX];     // layer inputs x^l, by layer parity
   uint16_t zbuf[ROWS * PX];        // gate output of the current layer
   float pbuf[2][4][2][ROWS * PP];  // W_r v + b of a layer: [stage parity][tile][tanh / sigmoid]
@@ -71,25 +74,36 @@ struct Lds {
   } chunk;
   int ins[ROWS];
   int pad_[ROWS];
-  // followed by the per-layer tables (dynamic part): roff[L] (int64), slot[L], dil[L], then fp32 biases
+  // followed by the per-layer tables (dynamic part): roff[L] (int64), slot[L], dep[L], then fp32 biases,
+  // then (width 3) the second popped-row buffer [2][ROWS * PX]
 };
 
 __host__ __device__ constexpr size_t lds_fixed_bytes() { return (sizeof(Lds) + 15) & ~size_t(15); }
-// dynamic part: roff[L] (8 B), slot[L], dil[L] (4 B each), then the bias block at a 16-byte boundary
+// dynamic part: roff[L] (8 B), slot[L], dep[L] (4 B each; dep = queue depth (w - 1) d), then the
+// bias block at a 16-byte boundary, then (width 3) the rows popped 2d steps back
 __host__ __device__ inline size_t lds_dyn_bias_offset(int L) { return ((size_t)L * 16 + 15) & ~size_t(15); }
+__host__ __device__ inline size_t lds_dyn_vb1_offset(int L) {
+  return (lds_dyn_bias_offset(L) + sizeof(float) * mfma_bias_floats(L) + 15) & ~size_t(15);
+}
 
 struct Frags {
   u32x4 f[F];
+};
+// the oldest tap's recurrent fragments of one layer (width 3)
+struct TapFrags {
+  u32x4 f[4];
 };
 
 // Stage k of a step is layer k (k < L) or head stage k - L.
 struct Ctx {
   const StepArgs *a;
   Lds *s;
-  int *slot, *dil;
+  uint16_t *vb1;  // width 3: popped rows of the oldest tap, [2][ROWS * PX]
+  int *slot, *dep;
   const long long *roff;
   const float *conv_b, *res_b, *skip_sum, *head_b, *out_b, *emb_b;
   const char *frags;  // fragment streams (wave-uniform base)
+  const char *tapfrags;  // width 3: the oldest tap's fragments, [L][4 B waves][4] x 1 KB
   int wvoff;          // this lane's byte offset inside a fragment (16 * lane)
   int L, NS, w, p, lane, n, q, b0, nrows;
 };
@@ -126,18 +140,32 @@ __device__ __forceinline__ long long ring_elem(const Ctx &c, int l, int slotv) {
   return c.roff[l] + ((long long)slotv * c.a->bmax + (c.b0 + r)) * R + 8 * (c.lane & 7);
 }
 // Issue the pop of stage k (a layer) for step offset `ahead` (0: the step the slot table
-// describes, 1: the next one).  Head stages pop layer 0 as a harmless placeholder.
+// describes, 1: the next one).  Head stages pop layer 0 as a harmless placeholder.  The queue of
+// a layer holds its last (w - 1) d inputs; the slot of the step holds the oldest, tap j sits j d
+// slots after it.  Width 2 (TP = 1): lanes 32..63 repeat the loads of lanes 0..31; width 3
+// (TP = 2): lanes 0..31 load the oldest rows (2d steps back), lanes 32..63 those d steps back.
+template <int TP>
 __device__ __forceinline__ u32x4 pop_issue(const Ctx &c, int k, int ahead) {
   const int l = k < c.L ? k : 0;
+  const int dep = c.dep[l];
   int sl = c.slot[l] + ahead;
-  if (sl >= c.dil[l]) sl -= c.dil[l];
+  if (sl >= dep) sl -= dep;
+  if (TP == 2 && c.lane >= 32) {
+    sl += dep >> 1;
+    if (sl >= dep) sl -= dep;
+  }
   const uint16_t *ring = (const uint16_t *)c.a->ring;
   return __builtin_nontemporal_load((const u32x4 *)(ring + ring_elem(c, l, sl)));
 }
+// vbuf holds the rows d steps back; at width 3 vb1 the rows 2d steps back
+template <int TP>
 __device__ __forceinline__ void pop_land(const Ctx &c, int parity, u32x4 v) {
-  if (c.lane < 32) {
-    const int r = 4 * c.p + (c.lane >> 3);
-    *(u32x4 *)(c.s->vbuf[parity] + r * PX + 8 * (c.lane & 7)) = v;
+  const int r = 4 * c.p + ((c.lane & 31) >> 3);
+  const int e = r * PX + 8 * (c.lane & 7);
+  if (TP == 1) {
+    if (c.lane < 32) *(u32x4 *)(c.s->vbuf[parity] + e) = v;
+  } else {
+    *(u32x4 *)((c.lane < 32 ? c.vb1 + parity * ROWS * PX : c.s->vbuf[parity]) + e) = v;
   }
 }
 // push phase of layer l: its input x^l replaces the slot popped for this step
@@ -159,18 +187,43 @@ struct Acc {
   f32x4 acc[5];
 };
 
+// The oldest tap's fragments of layer l for this B wave (width 3).
+__device__ __forceinline__ void load_tap(const Ctx &c, int l, TapFrags &X) {
+#pragma unroll
+  for (int f = 0; f < 4; ++f)
+    X.f[f] = *(const u32x4 *)(c.tapfrags + ((size_t)(l * 4 + c.p) * 4 + f) * 1024 + c.wvoff);
+}
+
 // W_r v + b for layer `ln`, computed by wave B one stage ahead from fragments f0..f0+3 (tanh tile
 // p k-steps 0,1, sigmoid tile p k-steps 0,1) and the popped rows in vbuf[par]; stored in pbuf[par].
-__device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int par, const Frags &W, int f0) {
+// Width 3 (TP = 2) adds the oldest tap's product (fragments X, rows in vb1), then loads X with the
+// next recurrent product's fragments (layer ln + 1, or layer 0 of the next step).
+template <int TP>
+__device__ __forceinline__ void recurrent_half(const Ctx &c, int ln, int par, const Frags &W, int f0, TapFrags &X) {
   Lds &s = *c.s;
   const uint16_t *vb = s.vbuf[par] + c.n * PX;
   const u32x4 bv0 = lds16(vb + 8 * c.q), bv1 = lds16(vb + 32 + 8 * c.q);
+  u32x4 bo0, bo1;
+  if (TP == 2) {
+    const uint16_t *vo = c.vb1 + par * ROWS * PX + c.n * PX;
+    bo0 = lds16(vo + 8 * c.q);
+    bo1 = lds16(vo + 32 + 8 * c.q);
+  }
   const float *cb = c.conv_b + ln * 2 * R;
   f32x4 pt = ldsf4(cb + 16 * c.p + 4 * c.q), pg = ldsf4(cb + R + 16 * c.p + 4 * c.q);
   pt = mfma(W.f[f0 + 0], bv0, pt);
   pg = mfma(W.f[f0 + 2], bv0, pg);
   pt = mfma(W.f[f0 + 1], bv1, pt);
   pg = mfma(W.f[f0 + 3], bv1, pg);
+  if (TP == 2) {
+    pt = mfma(X.f[0], bo0, pt);
+    pg = mfma(X.f[2], bo0, pg);
+    pt = mfma(X.f[1], bo1, pt);
+    pg = mfma(X.f[3], bo1, pg);
+    __builtin_amdgcn_sched_barrier(0);
+    load_tap(c, ln + 1 < c.L ? ln + 1 : 0, X);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   stf4(s.pbuf[par][c.p][0] + c.n * PP + 4 * c.q, pt);
   stf4(s.pbuf[par][c.p][1] + c.n * PP + 4 * c.q, pg);
 }
@@ -255,7 +308,7 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
   // waves A cover threads 0..255, more than the layer count
   for (int l = tid; l < c.L; l += NT) {
     const int nx = c.slot[l] + 1;
-    c.slot[l] = nx == c.dil[l] ? 0 : nx;
+    c.slot[l] = nx == c.dep[l] ? 0 : nx;
   }
   __syncthreads();
 }
@@ -264,8 +317,8 @@ __device__ __forceinline__ void finish_step(const Ctx &c, long long step, Acc &A
 // tiles 8p..8p+3 and output tiles 4p, 4p+1; wave B tiles 8p+4..8p+7 and 4p+2, 4p+3.  One barrier
 // at the first output fragment (g = GH1, in head stage 4).
 static_assert(F * 4 + 12 == GH1, "the head's hidden-layer barrier sits in head stage 4");
-template <int C, bool ISA, int F0, int F1>
-__device__ __forceinline__ void head_frags(const Ctx &c, long long i, const Frags &W, Acc &A) {
+template <int TP, int C, bool ISA, int F0, int F1>
+__device__ __forceinline__ void head_frags(const Ctx &c, long long i, const Frags &W, Acc &A, TapFrags &X) {
   Lds &s = *c.s;
   const int n = c.n, q = c.q, p = c.p;
   constexpr int hoff = ISA ? 0 : 64;  // channel offset of this wave's half inside the pair's 128
@@ -292,7 +345,7 @@ __device__ __forceinline__ void head_frags(const Ctx &c, long long i, const Frag
       A.acc[j] = mfma(W.f[f], b, A.acc[j]);
     } else if (g == GCV && !ISA) {
       // W_r v + b of the next step's layer 0
-      recurrent_half(c, 0, (int)((i + 1) & 1), W, f);
+      recurrent_half<TP>(c, 0, (int)((i + 1) & 1), W, f, X);
     }
   }
 }
@@ -323,20 +376,20 @@ __device__ __forceinline__ void head_start(const Ctx &c, Pos p0, Acc &A) {
   __syncthreads();
 }
 
-template <bool ISA, int F0, int F1>
-__device__ __forceinline__ void head_part(const Ctx &c, Pos p0, long long i, const Frags &W, Acc &A) {
+template <int TP, bool ISA, int F0, int F1>
+__device__ __forceinline__ void head_part(const Ctx &c, Pos p0, long long i, const Frags &W, Acc &A, TapFrags &X) {
   switch (p0.k - c.L) {
     case 0:
       if (F0 == 0) head_start<ISA>(c, p0, A);
-      head_frags<0, ISA, F0, F1>(c, i, W, A);
+      head_frags<TP, 0, ISA, F0, F1>(c, i, W, A, X);
       break;
-    case 1: head_frags<1, ISA, F0, F1>(c, i, W, A); break;
-    case 2: head_frags<2, ISA, F0, F1>(c, i, W, A); break;
-    case 3: head_frags<3, ISA, F0, F1>(c, i, W, A); break;
-    case 4: head_frags<4, ISA, F0, F1>(c, i, W, A); break;
-    case 5: head_frags<5, ISA, F0, F1>(c, i, W, A); break;
-    case 6: head_frags<6, ISA, F0, F1>(c, i, W, A); break;
-    default: head_frags<7, ISA, F0, F1>(c, i, W, A); break;
+    case 1: head_frags<TP, 1, ISA, F0, F1>(c, i, W, A, X); break;
+    case 2: head_frags<TP, 2, ISA, F0, F1>(c, i, W, A, X); break;
+    case 3: head_frags<TP, 3, ISA, F0, F1>(c, i, W, A, X); break;
+    case 4: head_frags<TP, 4, ISA, F0, F1>(c, i, W, A, X); break;
+    case 5: head_frags<TP, 5, ISA, F0, F1>(c, i, W, A, X); break;
+    case 6: head_frags<TP, 6, ISA, F0, F1>(c, i, W, A, X); break;
+    default: head_frags<TP, 7, ISA, F0, F1>(c, i, W, A, X); break;
   }
 }
 static_assert(NHEAD == 8, "head_part dispatches eight head stages");
@@ -358,6 +411,7 @@ __device__ __forceinline__ void refill_range(const Ctx &c, Frags &W, int nx) {
 // barrier | residual 1x1 -> x^{l+1}, skip fragments.
 __device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags &W, int nx, Acc &A) {
   Lds &s = *c.s;
+  TapFrags X;  // unused: wave A computes no recurrent half
   const int n = c.n, q = c.q, p = c.p;
   const int par = (int)(i & 1);
   const int l = p0.k;
@@ -400,7 +454,7 @@ __device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags
     af = mfma(W.f[1], bx1, af);
     ag = mfma(W.f[3], bx1, ag);
   } else {
-    head_part<true, 0, 4>(c, p0, i, W, A);
+    head_part<1, true, 0, 4>(c, p0, i, W, A, X);
   }
   refill_range<0, 4>(c, W, nx);
   u32x4 bz0, bz1;
@@ -420,7 +474,7 @@ __device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags
     A.xres = xr;
     lds8(s.xbuf[(l + 1) & 1] + n * PX + 16 * p + 4 * q, pack4(xr));
   } else {
-    head_part<true, 4, 6>(c, p0, i, W, A);
+    head_part<1, true, 4, 6>(c, p0, i, W, A, X);
   }
   refill_range<4, 6>(c, W, nx);
   // ---- slots 6..12: skip tiles 8p..8p+2 (both k-steps) and the k-step-0 half of tile 8p+3
@@ -431,7 +485,7 @@ __device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags
     for (int j = 0; j < 3; ++j) A.acc[j] = mfma(W.f[9 + j], bz1, A.acc[j]);
     A.acc[3] = mfma(W.f[12], bz0, A.acc[3]);
   } else {
-    head_part<true, 6, F>(c, p0, i, W, A);
+    head_part<1, true, 6, F>(c, p0, i, W, A, X);
   }
   refill_range<6, F>(c, W, nx);
   if (p0.k == c.NS - 1) finish_step<true>(c, p0.step, A);
@@ -440,7 +494,8 @@ __device__ __forceinline__ void a_stage(const Ctx &c, Pos p0, long long i, Frags
 // Stage of wave B.  Layer: W_r v + b of the next layer (its popped rows are already in LDS) |
 // barrier | push of the layer input, skip fragments.  `W` is the buffer of this stage's parity
 // and `nx` the fragment stream of the stage two ahead.
-__device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags &W, int nx, Acc &A) {
+template <int TP>
+__device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags &W, int nx, Acc &A, TapFrags &X) {
   Lds &s = *c.s;
   const int n = c.n, q = c.q, p = c.p;
   const int par = (int)(i & 1);
@@ -453,9 +508,9 @@ __device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags
 #pragma unroll
       for (int j = 0; j < 4; ++j) A.acc[1 + j] = ldsf4(c.skip_sum + 128 * p + 64 + 16 * j + 4 * q);
     }
-    if (l + 1 < c.L) recurrent_half(c, l + 1, par ^ 1, W, 0);
+    if (l + 1 < c.L) recurrent_half<TP>(c, l + 1, par ^ 1, W, 0, X);
   } else {
-    head_part<false, 0, 4>(c, p0, i, W, A);
+    head_part<TP, false, 0, 4>(c, p0, i, W, A, X);
   }
   refill_range<0, 4>(c, W, nx);
   u32x4 bz0, bz1;
@@ -469,7 +524,7 @@ __device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags
     A.acc[0] = mfma(W.f[4], bz1, A.acc[0]);
     A.acc[1] = mfma(W.f[5], bz0, A.acc[1]);
   } else {
-    head_part<false, 4, 6>(c, p0, i, W, A);
+    head_part<TP, false, 4, 6>(c, p0, i, W, A, X);
   }
   refill_range<4, 6>(c, W, nx);
   // ---- slots 6..12: skip tiles 8p+5..8p+7 k-step 0, tiles 8p+4..8p+7 k-step 1
@@ -479,7 +534,7 @@ __device__ __forceinline__ void b_stage(const Ctx &c, Pos p0, long long i, Frags
 #pragma unroll
     for (int j = 0; j < 4; ++j) A.acc[1 + j] = mfma(W.f[9 + j], bz1, A.acc[1 + j]);
   } else {
-    head_part<false, 6, F>(c, p0, i, W, A);
+    head_part<TP, false, 6, F>(c, p0, i, W, A, X);
   }
   refill_range<6, F>(c, W, nx);
   if (p0.k == c.NS - 1) finish_step<false>(c, p0.step, A);
@@ -504,21 +559,24 @@ __device__ __forceinline__ void a_role(const Ctx &c, long long total) {
 // Main loop of wave B: two fragment buffers by stage parity, each slot refilled with the stage two
 // ahead; queue rows of stage i+3 are read at the start of stage i and land in LDS at the end of
 // stage i+1, for the W_r v of stage i+3 computed during stage i+2.
+template <int TP>
 __device__ __forceinline__ void b_role(const Ctx &c, long long total) {
   Acc A;
   Frags W0, W1;
+  TapFrags X;
   const Pos p0i{0, 0};
   const Pos p1i = advance(c, p0i, 1), p2i = advance(c, p0i, 2);
-  pop_land(c, 0, pop_issue(c, 0, 0));
-  pop_land(c, 1, pop_issue(c, p1i.k, (int)p1i.step));
-  u32x4 vA, vB = pop_issue(c, p2i.k, (int)p2i.step);
+  pop_land<TP>(c, 0, pop_issue<TP>(c, 0, 0));
+  pop_land<TP>(c, 1, pop_issue<TP>(c, p1i.k, (int)p1i.step));
+  u32x4 vA, vB = pop_issue<TP>(c, p2i.k, (int)p2i.step);
   __syncthreads();
   {
     // W_r v + b of layer 0 from this wave's fragments in the last head stage
     const int off = stage_off(c, c.NS - 1);
 #pragma unroll
     for (int f = 0; f < 4; ++f) W0.f[f] = load_frag(c, off, GCV - F * (NHEAD - 1) + f);
-    recurrent_half(c, 0, 0, W0, 0);
+    if (TP == 2) load_tap(c, 0, X);
+    recurrent_half<TP>(c, 0, 0, W0, 0, X);
   }
   load_stage(c, 0, W0);
   load_stage(c, p1i.k, W1);
@@ -527,26 +585,28 @@ __device__ __forceinline__ void b_role(const Ctx &c, long long total) {
   long long i = 0;
   for (; i + 1 < total; i += 2) {
     const Pos p1 = advance(c, p0, 1), p2 = advance(c, p0, 2), p3 = advance(c, p0, 3), p4 = advance(c, p0, 4);
-    vA = pop_issue(c, p3.k, (int)(p3.step - p0.step));
+    vA = pop_issue<TP>(c, p3.k, (int)(p3.step - p0.step));
     __builtin_amdgcn_sched_barrier(0);
-    b_stage(c, p0, i, W0, stage_off(c, p2.k), A);
-    if (p2.k < c.L && i + 2 < total) pop_land(c, 0, vB);
+    b_stage<TP>(c, p0, i, W0, stage_off(c, p2.k), A, X);
+    if (p2.k < c.L && i + 2 < total) pop_land<TP>(c, 0, vB);
     __syncthreads();
-    vB = pop_issue(c, p4.k, (int)(p4.step - p1.step));
+    vB = pop_issue<TP>(c, p4.k, (int)(p4.step - p1.step));
     __builtin_amdgcn_sched_barrier(0);
-    b_stage(c, p1, i + 1, W1, stage_off(c, p3.k), A);
-    if (p3.k < c.L && i + 3 < total) pop_land(c, 1, vA);
+    b_stage<TP>(c, p1, i + 1, W1, stage_off(c, p3.k), A, X);
+    if (p3.k < c.L && i + 3 < total) pop_land<TP>(c, 1, vA);
     __syncthreads();
     p0 = p2;
   }
   if (i < total) {
     // odd stage count: the last stage (its queue rows for later stages are not needed)
     const Pos p2 = advance(c, p0, 2);
-    b_stage(c, p0, i, W0, stage_off(c, p2.k), A);
+    b_stage<TP>(c, p0, i, W0, stage_off(c, p2.k), A, X);
     __syncthreads();
   }
 }
 
+// TP = recurrent taps per dilated product (filter width - 1): 1 or 2.
+template <int TP>
 __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   extern __shared__ float4 lds_raw[];
   Lds &s = *(Lds *)lds_raw;
@@ -555,7 +615,7 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   char *dyn = (char *)lds_raw + lds_fixed_bytes();
   long long *roff = (long long *)dyn;
   int *slot = (int *)(roff + L);
-  int *dil = slot + L;
+  int *dep = slot + L;
   // conv_b [L][2R], res_b [L][R], skip_sum [S], head_b [H], out_b [Q], emb_b [R]; 16-byte aligned
   float *bias = (float *)(dyn + lds_dyn_bias_offset(L));
 
@@ -563,7 +623,8 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   c.a = &a;
   c.s = &s;
   c.slot = slot;
-  c.dil = dil;
+  c.dep = dep;
+  c.vb1 = (uint16_t *)(dyn + lds_dyn_vb1_offset(L));
   c.roff = roff;
   c.conv_b = bias;
   c.res_b = c.conv_b + L * 2 * R;
@@ -581,6 +642,7 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   c.b0 = blockIdx.x * ROWS;
   c.nrows = min(ROWS, a.batch - c.b0);
   c.frags = (const char *)a.mf_frags;
+  c.tapfrags = c.frags + mfma_frag_bytes(L);
   c.wvoff = 16 * c.lane;
 
   // tables: embedding [Q][R], biases, queue offsets, dilations and slots
@@ -591,8 +653,8 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
   for (int l = tid; l < L; l += NT) {
     const LayerDev ld = a.layers[l];
     roff[l] = ld.ring_off;
-    dil[l] = ld.dil;
-    slot[l] = (int)(a.t0 % (long long)ld.dil);
+    dep[l] = ld.depth;
+    slot[l] = (int)(a.t0 % (long long)ld.depth);
   }
   if (tid < ROWS) {
     int v = 0;
@@ -603,25 +665,30 @@ __global__ void __launch_bounds__(NT) mfma_step_kernel(StepArgs a) {
 
   const long long total = (long long)a.n_steps * c.NS;
   if (c.w < 4) a_role(c, total);
-  else b_role(c, total);
+  else b_role<TP>(c, total);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
 }
 
 }  // namespace mf
 
-size_t mfma_lds_bytes(int L) {
+size_t mfma_lds_bytes(int L, int w) {
+  if (w == 3) return mf::lds_fixed_bytes() + mf::lds_dyn_vb1_offset(L) + sizeof(uint16_t) * 2 * mf::ROWS * mf::PX;
   return mf::lds_fixed_bytes() + mf::lds_dyn_bias_offset(L) + sizeof(float) * mfma_bias_floats(L);
 }
 
 hipError_t launch_mfma_step(const StepArgs &a, hipStream_t s) {
-  const size_t lds = mfma_lds_bytes(a.L);
+  const size_t lds = mfma_lds_bytes(a.L, a.w);
   const dim3 grid((a.batch + kMfRows - 1) / kMfRows), block(kMfThreads);
-  hipLaunchKernelGGL(mf::mfma_step_kernel, grid, block, lds, s, a);
+  if (a.w == 3) hipLaunchKernelGGL(mf::mfma_step_kernel<2>, grid, block, lds, s, a);
+  else hipLaunchKernelGGL(mf::mfma_step_kernel<1>, grid, block, lds, s, a);
   return hipGetLastError();
 }
 
 hipError_t set_mfma_lds_limit(size_t bytes) {
-  return hipFuncSetAttribute((const void *)mf::mfma_step_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+  hipError_t e = hipFuncSetAttribute((const void *)mf::mfma_step_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     (int)bytes);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void *)mf::mfma_step_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)bytes);
 }
 
@@ -631,39 +698,41 @@ hipError_t set_mfma_lds_limit(size_t bytes) {
 // Stage k of the stream holds, for each of the 8 waves, F fragments of 1 KB.
 namespace mf {
 
-// element of the conv matrix [2R][2R] with k < R the recurrent tap and k >= R the current tap
-__device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int o, int k) {
-  return conv[(o * R + (k % R)) * 2 + (k >= R ? 1 : 0)];
+// element (output o, input channel c, tap j) of the conv weights [2R][R][w] (tap w - 1 multiplies the
+// current input, tap w - 2 the input d steps back, tap 0 at width 3 the input 2d steps back)
+__device__ __forceinline__ uint16_t conv_elem(const uint16_t *conv, int w, int o, int c, int j) {
+  return conv[(o * R + c) * w + j];
 }
 
 __device__ __forceinline__ uint4 pack8(const uint16_t *v) {
   return make_uint4(v[0] | (v[1] << 16), v[2] | (v[3] << 16), v[4] | (v[5] << 16), v[6] | (v[7] << 16));
 }
 
-// Layer l's fragments.  Wave A (p = w < 4), stage l: f0..f3 conv x-half (tanh tile p k-steps 2,3,
-// sigmoid tile p k-steps 2,3), f4..f5 residual tile p, f6..f8 skip tiles 8p..8p+2 k-step 0,
-// f9..f11 the same tiles k-step 1, f12 skip tile 8p+3 k-step 0.  Wave B (p = w - 4), stage l:
-// f4 skip tile 8p+3 k-step 1, f5..f8 skip tiles 8p+4..8p+7 k-step 0, f9..f12 k-step 1; its conv
-// v-half of layer l (tanh tile p k-steps 0,1, sigmoid tile p k-steps 0,1) goes to f0..f3 of stage
+// Layer l's fragments.  Wave A (p = wave < 4), stage l: f0..f3 the conv's current-input tap (tanh
+// tile p k-steps 0,1, sigmoid tile p k-steps 0,1), f4..f5 residual tile p, f6..f8 skip tiles 8p..8p+2 k-step 0,
+// f9..f11 the same tiles k-step 1, f12 skip tile 8p+3 k-step 0.  Wave B (p = wave - 4), stage l:
+// f4 skip tile 8p+3 k-step 1, f5..f8 skip tiles 8p+4..8p+7 k-step 0, f9..f12 k-step 1; the conv
+// tap d steps back of layer l (tanh tile p k-steps 0,1, sigmoid tile p k-steps 0,1) goes to f0..f3 of stage
 // l - 1, or for layer 0 to the last head stage (head stream positions GCV..GCV+3).  The last
-// layer also zeroes its own wave-B f0..f3 (no next layer inside the step).
+// layer also zeroes its own wave-B f0..f3 (no next layer inside the step).  Width 3: the same four
+// fragments of the oldest tap go to the tap stream after the stage streams, [l][p][f].
 __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, const uint16_t *skip, int l, int L,
-                                    uint4 *frags) {
+                                    int w, uint4 *frags) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= kMfWaves * F * 64) return;
-  const int lane = e % 64, f = (e / 64) % F, w = e / (64 * F);
+  const int lane = e % 64, f = (e / 64) % F, wv = e / (64 * F);
   const int m = lane % 16, kq = 8 * (lane / 16);
   const int NS = L + NHEAD;
   auto at = [&](int stage, int wave, int frag) {
     return frags + ((size_t)(stage * kMfWaves + wave) * F + frag) * 64 + lane;
   };
   uint16_t v[8];
-  if (w < 4) {
-    const int p = w;
+  if (wv < 4) {
+    const int p = wv;
     for (int j = 0; j < 8; ++j) {
       if (f < 4) {
         const int o = (f < 2 ? 0 : R) + 16 * p + m;
-        v[j] = conv_elem(conv, o, R + 32 * (f & 1) + kq + j);
+        v[j] = conv_elem(conv, w, o, 32 * (f & 1) + kq + j, w - 1);
       } else if (f < 6) {
         v[j] = res[(16 * p + m) * R + 32 * (f - 4) + kq + j];
       } else {
@@ -672,24 +741,27 @@ __global__ void repack_layer_kernel(const uint16_t *conv, const uint16_t *res, c
         v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
       }
     }
-    *at(l, w, f) = pack8(v);
+    *at(l, wv, f) = pack8(v);
   } else {
-    const int p = w - 4;
+    const int p = wv - 4;
     if (f < 4) {
-      for (int j = 0; j < 8; ++j) {
-        const int o = (f < 2 ? 0 : R) + 16 * p + m;
-        v[j] = conv_elem(conv, o, 32 * (f & 1) + kq + j);
+      const int o = (f < 2 ? 0 : R) + 16 * p + m;
+      for (int j = 0; j < 8; ++j) v[j] = conv_elem(conv, w, o, 32 * (f & 1) + kq + j, w - 2);
+      if (l > 0) *at(l - 1, wv, f) = pack8(v);
+      else *at(NS - 1, wv, GCV - F * (NHEAD - 1) + f) = pack8(v);
+      if (l == L - 1) *at(l, wv, f) = make_uint4(0, 0, 0, 0);
+      if (w == 3) {
+        for (int j = 0; j < 8; ++j) v[j] = conv_elem(conv, w, o, 32 * (f & 1) + kq + j, 0);
+        uint4 *tap = frags + mfma_frag_bytes(L) / 16;
+        tap[((size_t)(l * 4 + p) * 4 + f) * 64 + lane] = pack8(v);
       }
-      if (l > 0) *at(l - 1, w, f) = pack8(v);
-      else *at(NS - 1, w, GCV - F * (NHEAD - 1) + f) = pack8(v);
-      if (l == L - 1) *at(l, w, f) = make_uint4(0, 0, 0, 0);
     } else {
       for (int j = 0; j < 8; ++j) {
         const int t = f == 4 ? 8 * p + 3 : f < 9 ? 8 * p + 4 + (f - 5) : 8 * p + 4 + (f - 9);
         const int ks = (f == 4 || f >= 9) ? 1 : 0;
         v[j] = skip[(16 * t + m) * R + 32 * ks + kq + j];
       }
-      *at(l, w, f) = pack8(v);
+      *at(l, wv, f) = pack8(v);
     }
   }
 }
@@ -761,11 +833,11 @@ __global__ void bias_block_kernel(const float *const *conv_b, const float *const
 
 }  // namespace mf
 
-hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, void *frags,
-                                    hipStream_t s) {
+hipError_t launch_mfma_repack_layer(const void *conv, const void *res, const void *skip, int l, int L, int w,
+                                    void *frags, hipStream_t s) {
   const int n = kMfWaves * kMfFrags * 64;
   hipLaunchKernelGGL(mf::repack_layer_kernel, dim3((n + 255) / 256), dim3(256), 0, s, (const uint16_t *)conv,
-                     (const uint16_t *)res, (const uint16_t *)skip, l, L, (uint4 *)frags);
+                     (const uint16_t *)res, (const uint16_t *)skip, l, L, w, (uint4 *)frags);
   return hipGetLastError();
 }
 

@@ -134,6 +134,11 @@ FAMILIES = {
     "gated_r32_w3_f32_valu": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r32_w3_f32_one": W.ModelConfig(W.GATED, W.F32, 32, (1, 3, 9, 27, 1, 3, 9), 256, 256, filter_width=3),
     "gated_r64_w3_bf16": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
+    # width 3 on the MFMA kernel with a layer count the split kernels would take at width 2, and
+    # one layer (the oldest tap's fragments of the next step's layer 0 reloaded every step)
+    "gated_r64_w3_bf16_l12": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 2, 512, 512, filter_width=3),
+    "gated_r64_w3_bf16_l1": W.ModelConfig(W.GATED, W.BF16, 64, (3,), 512, 512, filter_width=3),
+    "gated_r64_w3_bf16_valu": W.ModelConfig(W.GATED, W.BF16, 64, (1, 3, 9, 27, 2), 512, 512, filter_width=3),
     "relures_c64_w4_bf16": W.ModelConfig(W.RELU_RESIDUAL, W.BF16, 64, (1, 4, 16, 2), filter_width=4),
     # small enough for the wave-per-stream kernels (every weight in LDS)
     "gated_r16_s32_f32": W.ModelConfig(W.GATED, W.F32, 16, (1, 2, 4, 8, 16, 32), 32, 32),
@@ -157,7 +162,7 @@ WIDE_FAMILIES = {"relures_c512_f32", "relures_c512_f32_q255"}
 # families whose test forces the general (VALU) kernel family instead of the MFMA, wave, chain or
 # wide one
 FORCE_VALU = {"gated_r64_bf16_valu", "relu_c32_f32_valu", "relures_c512_f32_valu", "gated_r32_f32_valu",
-              "gated_r32_w3_f32_valu"}
+              "gated_r32_w3_f32_valu", "gated_r64_w3_bf16_valu"}
 # families whose test forces the wave-per-stream family instead of the chain one
 FORCE_WAVE = {"relu_c32_f32_wave"}
 
@@ -193,12 +198,12 @@ def build_pair(cfg, seed, max_batch, bias_scale=0.1, fam=None, par_rows=None, va
             os.environ.pop(k, None)
     if fam is not None:
         mfma_shape = (cfg.kind == W.GATED and cfg.dtype == W.BF16 and cfg.channels == 64 and
-                      cfg.skip_channels == 512 and cfg.head_channels == 512 and cfg.filter_width == 2)
+                      cfg.skip_channels == 512 and cfg.head_channels == 512 and cfg.filter_width in (2, 3))
         if fam in FORCE_VALU:
             assert fw.regime == "valu", (fam, fw.regime)
         elif mfma_shape:
-            # the split kernels take layer counts that are multiples of 6, at least 12
-            split = cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
+            # the split kernels take width 2 and layer counts that are multiples of 6, at least 12
+            split = cfg.filter_width == 2 and cfg.n_layers % 6 == 0 and cfg.n_layers >= 12
             assert fw.regime == ("mfma_split_bf16_r64_s512" if split else "mfma_bf16_r64_s512"), (fam, fw.regime)
         else:
             assert fw.regime in ("valu", "wave", "chain_f32_c32", "chain_gated_f32_r32", "chain_pair_f32_r32",
@@ -322,7 +327,7 @@ def test_parallel_wide_tiles(fam):
     assert err.max() <= TOL[cfg.dtype]
 
 
-@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "relu_c32_f32"])
+@pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "relu_c32_f32", "gated_r64_w3_bf16"])
 def test_prime_then_generate(fam):
     """Priming from a prefix (fwg_prime, time-parallel) leaves the same state with or without
     logits (the generation that follows is bit-identical), matches the oracle primed with the same
@@ -355,7 +360,7 @@ def test_prime_then_generate(fam):
     log(f"{fam}: generation after a {prefix.shape[1]}-step prime: first divergence min {min(first)}")
 
 
-@pytest.mark.parametrize("fam", ["relu_c32_f32_valu", "gated_r32_f32", "gated_r64_bf16_valu", "gated_r64_w3_bf16"])
+@pytest.mark.parametrize("fam", ["relu_c32_f32_valu", "gated_r32_f32", "gated_r64_bf16_valu", "gated_r64_w3_bf16_valu"])
 def test_valu_unstaged_variant(fam):
     """The general step kernels without LDS weight staging (the variant taken at one stream per
     block or for wide layers), at a batch that would otherwise stage: teacher-forced logits and
@@ -520,7 +525,7 @@ def test_uniform_logits_sampler_gpu(fam, B, regime):
 
 
 @pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "gated_r64_bf16_odd", "gated_r64_bf16_split",
-                                 "relu_c32_f32", "relures_c32_f32", "relures_c512_f32"])
+                                 "relu_c32_f32", "relures_c32_f32", "relures_c512_f32", "gated_r64_w3_bf16"])
 def test_continuation_reset_and_determinism_gpu(fam):
     cfg = FAMILIES[fam]
     w, fw, _ = build_pair(cfg, 7, 9, fam=fam)
@@ -695,3 +700,16 @@ def test_full_gated_w3():
     g = fw.generate(dev(u)).cpu().numpy()
     assert g.min() >= 0 and g.max() <= 255
     _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 63], wl.n_steps)
+
+
+def test_full_gated_w3_bf16():
+    """Width 3 on the benchmark's layer shape at full size (256 streams x 8,000 steps, queues up to
+    1,458 deep) on the MFMA step kernel: sampled streams checked by the oracle over every step."""
+    wl, w, fw, orc = _full("gated_r64_s512_w3_l14_b256_bf16")
+    assert fw.regime == "mfma_bf16_r64_s512"
+    u = W.uniforms(wl.uniform_seed, wl.batch, wl.n_steps)
+    t0 = time.time()
+    g = fw.generate(dev(u)).cpu().numpy()
+    log(f"{wl.name}: GPU generation {wl.batch}x{wl.n_steps} in {time.time() - t0:.1f}s ({fw.regime})")
+    assert g.min() >= 0 and g.max() <= 255
+    _check_streams_on_gpu_sequence(wl, fw, orc, u, g, [0, 255], wl.n_steps)

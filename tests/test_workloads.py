@@ -61,7 +61,7 @@ def test_weight_shapes_and_scale():
 
 def test_workload_table():
     t = W.WORKLOADS
-    assert [w.model.queue_total for w in t.values()] == [31, 2046, 2046, 3069, 155, 4372]
+    assert [w.model.queue_total for w in t.values()] == [31, 2046, 2046, 3069, 155, 4372, 4372]
     assert [w.model.flops_per_sample() for w in t.values()] == [36_864, 794_624, 794_624, 3_981_312, 26_476_544,
-                                                                692_224]
+                                                                692_224, 2_506_752]
     assert W.BENCH_WORKLOAD in t

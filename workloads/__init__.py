@@ -137,6 +137,13 @@ WORKLOADS: Dict[str, Workload] = {
                  batch=64, n_steps=8000, weight_seed=4, uniform_seed=4,
                  description="gated 2x7 layers of filter width 3 (dilations 1..729 per block), R=32, S=H=256, "
                              "fp32, batch 64, 8,000 steps"),
+        # the same width-3 layer pattern on the benchmark's layer shape (bf16 operands, R = 64)
+        Workload("gated_r64_s512_w3_l14_b256_bf16",
+                 ModelConfig(GATED, BF16, 64, tuple(3 ** i for i in range(7)) * 2, skip_channels=512,
+                             head_channels=512, filter_width=3),
+                 batch=256, n_steps=8000, weight_seed=5, uniform_seed=5,
+                 description="gated 2x7 layers of filter width 3 (dilations 1..729 per block), R=64, S=H=512, "
+                             "bf16 operands / fp32 accumulation, batch 256, 8,000 steps"),
     ]
 }
 
