@@ -833,10 +833,15 @@ __global__ void __launch_bounds__(NT) chain_gated_kernel(StepArgs a, ChainGatedA
 //    the staging of per-step inputs;
 //  - wave 3: U^l = W_e^l x^{l-1} (x^0 for l = 0), to LDS (+ flag).
 // Helper block (h = 1): the skip sum, 64 channels per wave (wave 0 also receives the z words into
-// its LDS row).  Head, both blocks, with each thread's weights resident in registers for the launch
-// (one K half of one row of each head 1x1): the helper publishes relu(skip sum), both compute half of
-// the hidden channels and exchange them, then half of the classes; in generation the helper
-// publishes its logits and the chain block samples.
+// its LDS row).  Head, both blocks, with each thread's weights resident in registers for the launch:
+// the helper publishes relu(skip sum) and each block computes half of the hidden channels (thread:
+// one K half of one row of the first 1x1).  Width 2: from its half of the hidden channels alone each
+// block forms the partial logits of every class (thread: one class row of the output 1x1 over that
+// half), the helper publishes its partials and the chain block adds them, so the hidden channels
+// never cross between the blocks.  Width 3 (whose other weights leave no room for the output 1x1's
+// partial products without spilling): the blocks exchange their hidden halves, each computes half of
+// the classes (thread: one K half of one class row) and in generation the helper publishes its
+// logits.  The chain block samples.
 //
 // Hand-offs are the tagged words of fwg_xchg.h (tag = step index in the launch + 1; zeroed before
 // every launch).  No block overwrites a word before the other has read it: each block's next write
@@ -851,6 +856,7 @@ constexpr int PW_HS = 0, PW_Z = 96;  // handshake slots (chain block, helper, mo
 __host__ __device__ inline int pw_s(int L) { return 96 + 32 * L; }                // 256: relu(skip sum)
 __host__ __device__ inline int pw_h(int L, int h) { return 96 + 32 * L + 256 + 128 * h; }
 __host__ __device__ inline int pw_l(int L) { return 96 + 32 * L + 512; }           // the helper's logits
+__host__ __device__ inline int pw_p(int L) { return pw_h(L, 0); }  // 256: the helper's partial logits (width 2)
 
 // LDS of the pair variant (in 4-byte words): embedding table and bias, P [2][L][64], U [L][64],
 // xrow, zrow, resb [L][32], srow, hrow, lrow, part [256], u, fin [2][KCH], flags.
@@ -909,7 +915,7 @@ struct PairX {
   bool local;             // both blocks on one XCD
 };
 
-// Half of a head 1x1 from resident weights: output 128 h + t mod 128 over K half t / 128 (PH
+// Half of a head 1x1 from resident weights: one row over one half of the input channels (PH
 // chunks), the input vector broadcast from LDS.
 __device__ __forceinline__ float head_dot(const float4 (&Wt)[PH], const float *in) {
   const float4 *i4 = (const float4 *)in;
@@ -925,9 +931,16 @@ __device__ __forceinline__ float head_dot(const float4 (&Wt)[PH], const float *i
   return a0 + a1;
 }
 
-// The head of one step in block h (every thread of both blocks); on return the chain block holds all
-// 256 logits in LDS in generation, and in forced modes each block has written its 128 classes out.
-// The helper's relu(skip sum) is already in its srow.
+// The head of one step in block h (every thread of both blocks).  Block h computes hidden channels
+// 128 h .. 128 h + 127 (thread t: K half t / 128 of row t mod 128).  KS (width 2): over those
+// channels alone, thread t computes the partial logit of class t; the helper publishes its partials
+// and the chain block adds them to its own, so a logit is (hidden half 0 + hidden half 1) + bias, and
+// on return the chain block holds all 256 logits in LDS and in forced modes has written them out.
+// Otherwise the blocks exchange their hidden halves and block h computes classes 128 h .. 128 h + 127
+// (thread t: K half t / 128 of class row t mod 128); on return the chain block holds all 256 logits
+// in LDS in generation, and in forced modes each block has written its 128 classes out.  The helper's
+// relu(skip sum) is already in its srow.
+template <bool KS>
 __device__ __forceinline__ void pair_head(const PL &s, const float4 (&W1)[PH], const float4 (&W2)[PH],
                                           const PairX &px, const StepArgs &a, int L, int b, int h, int step,
                                           float hbias, float obias) {
@@ -944,6 +957,22 @@ __device__ __forceinline__ void pair_head(const PL &s, const float4 (&W1)[PH], c
   }
   s.part[tid] = head_dot(W1, s.srow + 128 * kh);
   __syncthreads();
+  if (KS) {
+    if (tid < 128) s.hrow[128 * h + tid] = fmaxf(s.part[tid] + s.part[tid + 128] + hbias, 0.f);
+    __syncthreads();  // this block's half of the hidden layer
+    const float pl = head_dot(W2, s.hrow + 128 * h);
+    if (h == 1) {
+      xg::put_word(px.pw + pw_p(L) + tid, __builtin_bit_cast(uint32_t, pl), tag, px.local);
+    } else {
+      uint32_t v[1];
+      xg::wait_words<1, 1>(px.pw + pw_p(L) + tid, tag, v, px.abort_w, px.sticky);
+      const float lv = pl + __builtin_bit_cast(float, v[0]) + obias;
+      s.lrow[tid] = lv;
+      if (a.mode != MODE_GENERATE && a.logits) a.logits[((long long)b * a.n_steps + step) * Q + tid] = lv;
+    }
+    __syncthreads();  // the chain block has every logit
+    return;
+  }
   if (tid < 128) {
     const float hv = fmaxf(s.part[tid] + s.part[tid + 128] + hbias, 0.f);
     s.hrow[128 * h + tid] = hv;
@@ -1067,7 +1096,8 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
   float4 W1[PH], W2[PH];
   load_chunks(W1, rw, lane * 16, o_head + (h * 4 + wave) * PH * 1024, 1024);
   load_chunks(W2, rw, lane * 16, o_out + (h * 4 + wave) * PH * 1024, 1024);
-  const float hbias = g.headb[128 * h + (tid & 127)], obias = g.outb[128 * h + (tid & 127)];
+  constexpr bool KS = W == 2;  // the output 1x1 split by K (partial logits of every class per block)
+  const float hbias = g.headb[128 * h + (tid & 127)], obias = KS ? g.outb[tid] : g.outb[128 * h + (tid & 127)];
   __syncthreads();
   px.local = *s.mode != 0;
   const int o = lane & (R - 1), hl = lane >> 5;
@@ -1109,7 +1139,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
         for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
       }
       s.srow[m] = fmaxf(s0, 0.f);
-      pair_head(s, W1, W2, px, a, L, b, 1, step, hbias, obias);
+      pair_head<KS>(s, W1, W2, px, a, L, b, 1, step, hbias, obias);
       __syncthreads();
     }
   } else if (wave == 0) {
@@ -1148,7 +1178,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
 #pragma unroll
         for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
       }
-      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      pair_head<KS>(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
       if (a.mode == MODE_GENERATE) {
         const float4 lg = ((const float4 *)s.lrow)[lane];
         in = sample_row4(lg, s.u[(step / KCH & 1) * KCH + step % KCH]);
@@ -1212,7 +1242,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
         for (int c = 0; c < 4; ++c) WA[c] = WB[c];
       }
       qslot = qslot + 1 == qdep ? 0 : qslot + 1;
-      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      pair_head<KS>(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
       __syncthreads();
     }
   } else if (wave == 2) {
@@ -1264,7 +1294,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
           }
         }
       }
-      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      pair_head<KS>(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
       __syncthreads();
     }
   } else {
@@ -1293,7 +1323,7 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
 #pragma unroll
         for (int c = 0; c < FZ; ++c) WA[c] = WB[c];
       }
-      pair_head(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
+      pair_head<KS>(s, W1, W2, px, a, L, b, 0, step, hbias, obias);
       __syncthreads();
     }
   }
@@ -1335,8 +1365,9 @@ __global__ void pack_layer_kernel(const float *conv, const float *res, const flo
   }
 }
 // Single block: f = (wave, chunk, lane), row t = 64 wave + lane, columns 4 chunk .. 4 chunk + 3.
-// Pair: f = (block h, wave, j, lane), thread t = 64 wave + lane, row 128 h + t mod 128, chunk
-// PH (t / 128) + j (the thread's K half).
+// Pair (pair = 1, 2): f = (block h, wave, j, lane), thread t = 64 wave + lane, row 128 h + t mod 128,
+// chunk PH (t / 128) + j (the thread's K half); with pair = 2 the output 1x1 instead gives thread t
+// class row t, chunk PH h + j (the block's half of the hidden channels).
 __global__ void pack_head_kernel(const float *head, const float *out, int pair, ChainGatedArgs g) {
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= 2 * FH * NT) return;
@@ -1344,8 +1375,9 @@ __global__ void pack_head_kernel(const float *head, const float *out, int pair, 
   int t, c;
   if (pair) {
     const int hb = f / (4 * PH * 64), wv = (f / (PH * 64)) % 4, j = (f / 64) % PH, tt = 64 * wv + f % 64;
-    t = 128 * hb + (tt & 127);
-    c = PH * (tt >> 7) + j;
+    const bool ks = pair == 2 && which;
+    t = ks ? tt : 128 * hb + (tt & 127);
+    c = ks ? PH * hb + j : PH * (tt >> 7) + j;
   } else {
     const int wv = f / (FH * 64);
     c = (f / 64) % FH;
@@ -1487,8 +1519,9 @@ hipError_t launch_chain_gated_pack(const void *embed, const float *embed_b, cons
     hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, skip_b ? skip_b[l] : nullptr, (float *)g.skipb, S,
                        l > 0);
   }
+  // the pair kernel's output 1x1 is split by K at width 2 (pair_head)
   hipLaunchKernelGGL(pack_head_kernel, dim3((2 * FH * NT + 255) / 256), dim3(256), 0, s, (const float *)head,
-                     (const float *)out, pair ? 1 : 0, g);
+                     (const float *)out, pair ? (w == 2 ? 2 : 1) : 0, g);
   hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, head_b, (float *)g.headb, H, 0);
   hipLaunchKernelGGL(pack_vec_kernel, dim3(1), dim3(256), 0, s, out_b, (float *)g.outb, Q, 0);
   hipLaunchKernelGGL(ch::chain_transpose_kernel, dim3((R * Q + 255) / 256), dim3(256), 0, s, (const float *)embed,
