@@ -442,6 +442,10 @@ struct fwg_handle {
   long long nv_t;   // naive generator: its own time and batch binding (its state is the input history)
   int nv_bound_batch;
   void *static_scratch;  // split family: this device's static exchange-word array (fwg_generate_noalloc)
+  // split family, the workspace's exchange words: the next launch's tag base (every tag written since
+  // the region was last zeroed is at most this), and whether the region has been zeroed since create
+  uint32_t sp_tag = 0;
+  bool sp_comm_zeroed = false;
 };
 
 namespace {
@@ -584,7 +588,7 @@ int naive_step(fwg_handle *h, int batch, long long t, int n_steps, int s, const 
 
 // One step-kernel launch of the handle's kernel family.  comm: where the split family's exchange
 // words go (NULL: the workspace's region).
-hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = nullptr) {
+hipError_t launch_step(fwg_handle *h, const StepArgs &a, void *comm = nullptr) {
   const Plan &p = h->plan;
   switch (p.regime) {
     case REGIME_MFMA: return launch_mfma_step(a, h->stream);
@@ -593,9 +597,22 @@ hipError_t launch_step(const fwg_handle *h, const StepArgs &a, void *comm = null
       b.sp_nb = (a.batch + kMfRows - 1) / kMfRows;
       b.sp_comm = comm ? comm : h->ws + p.off_comm;
       b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
-      // tags restart at 1 every launch: clear the exchange words first (a fill kernel, no memset node)
-      hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
-      if (e != hipSuccess) return e;
+      // Tags are never reused between two zero fills of the exchange words (a fill kernel, no memset
+      // node).  The static array of fwg_generate_noalloc is shared by every handle on the device: it
+      // is zeroed before every launch, whose tags then start at 1.  The workspace's region belongs
+      // to this handle: zeroed before its first launch and when the tags would wrap; every launch
+      // takes the tags above the previous launch's (handshake base + 1, step s base + 2 + s).
+      const uint32_t need = (uint32_t)a.n_steps + 2u;
+      if (comm || !h->sp_comm_zeroed || h->sp_tag > 0xFFFFFFFFu - need) {
+        hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
+        if (e != hipSuccess) return e;
+        if (!comm) {
+          h->sp_comm_zeroed = true;
+          h->sp_tag = 0;
+        }
+      }
+      b.sp_tag0 = comm ? 0u : h->sp_tag;
+      if (!comm) h->sp_tag += need - 1u;
       return launch_split_step(b, h->stream);
     }
     case REGIME_WIDE: {
@@ -937,6 +954,13 @@ int fwg_create(const fwg_desc *desc, const fwg_weights *w, void *workspace, size
   if (h->plan.regime == REGIME_SPLIT) {
     // set-up of fwg_generate_noalloc: this device's static exchange-word array, looked up once
     TRY_OR_FREE(split_static_scratch(&h->static_scratch));
+    // test hook: the workspace's exchange words zeroed now and the tag base started at the given
+    // value (e.g. just below the 32-bit wrap, so that later launches cross it)
+    if (const char *tb = getenv("FWG_SPLIT_TAG_BASE")) {
+      TRY_OR_FREE(launch_fill_zero(ws + p.off_comm, split_comm_bytes(p.L, p.brows / kMfRows), s));
+      h->sp_comm_zeroed = true;
+      h->sp_tag = (uint32_t)strtoul(tb, nullptr, 0);
+    }
     char *frags = ws + p.off_frags;
     for (int l = 0; l < p.L; ++l)
       TRY_OR_FREE(launch_split_repack_layer(w->conv[l], w->res[l], w->skip[l], l, p.L, frags, s));

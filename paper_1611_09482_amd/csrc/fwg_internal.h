@@ -54,10 +54,12 @@ struct StepArgs {
   const void *mf_embT;     // embedding table [Q][R] (bf16)
   const float *mf_bias;    // bias block: conv [L][2R], res [L][R], skip sum [S], head [H], out [Q], embed [R]
   // split MFMA family only
-  void *sp_comm;           // exchange words between cooperating blocks (zeroed before each launch)
+  void *sp_comm;           // exchange words between cooperating blocks
   uint32_t *sp_sticky;     // set when a wait of a launch ran out (cleared by create and reset)
   int sp_nb;               // split family: chain blocks of this launch (ceil(batch / 16)); wide family:
                            // stream groups (ceil(batch / 4))
+  uint32_t sp_tag0;        // split family: tag base of this launch, above every tag written to sp_comm
+                           // since it was last zeroed (handshake and abort mark + 1, step s + 2 + s)
 };
 
 // What drives the input of each step.

@@ -22,14 +22,17 @@
 // block that owns streams streams all 4 MB of weights once per step, which bounds its step.
 //
 // Hand-offs between blocks are 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed
-// device-scope atomics.  A word is fresh once its tag equals the step's tag (step index in the
-// launch + 1; the exchange buffers are zeroed before every launch), so no fence or flag has to
-// order the payload.  The blocks of a group compare their XCD ids at launch: when they share one,
+// device-scope atomics.  A word is fresh once its tag equals the step's tag, so no fence or flag
+// has to order the payload.  Tags are never reused between two zero fills of the exchange buffers:
+// the host passes each launch a tag base above every tag written since the last fill (the launch
+// handshake uses base + 1, step s base + 2 + s), so a handle's exchange buffers are zeroed only
+// before its first launch and when the 32-bit tags would wrap, not before every launch.  The blocks of a group compare their XCD ids at launch: when they share one,
 // and so its L2, the words are stored with workgroup-scope stores, which complete in that L2;
 // otherwise with device-scope stores, which write through to memory and whose slow completion holds
 // up every later memory wait of the storing wave.  Each load instruction of a poll reads
 // consecutive words across the polling lanes.  Every wait is bounded: a wait that runs out sets
-// the launch's abort word, which ends every other wait (the results are then invalid, and a sticky
+// the launch's mark (base + 1) in the abort word, which ends every other wait of that launch and of
+// no later one (the results are then invalid, and a sticky
 // word lets the host report it); every wave keeps executing its straight-line program, so the grid
 // always drains.
 //
@@ -143,6 +146,11 @@ __host__ __device__ inline u64 *comm_s(void *comm, int L, int blk) { return comm
 __host__ __device__ inline u64 *comm_hid(void *comm, int L, int blk) { return comm_s(comm, L, blk) + XWORDS; }
 __host__ __device__ inline u64 *comm_smp(void *comm, int L, int blk) { return comm_hid(comm, L, blk) + XWORDS; }
 __host__ __device__ inline u64 *comm_hs(void *comm, int L, int blk) { return comm_smp(comm, L, blk) + SWORDS; }
+// Tags of a launch: the handshake words and the abort mark use base + 1, step s uses base + 2 + s.
+__device__ __forceinline__ uint32_t launch_mark(const StepArgs &a) { return a.sp_tag0 + 1u; }
+__device__ __forceinline__ uint32_t step_tag(const StepArgs &a, long long step) {
+  return a.sp_tag0 + 2u + (uint32_t)step;
+}
 
 // ---------------------------------------------------------------------------
 // Chain block
@@ -163,6 +171,7 @@ struct Ctx {
   u64 *zp;          // this group's z^0 words (layer l at + l * ZWORDS)
   const u64 *smp;   // this group's sample words
   uint32_t *abort_word, *sticky;
+  uint32_t mark;    // this launch's abort mark
   bool local;       // the helpers and the class block share this XCD: workgroup-scope stores suffice
   int L, w, p, lane, n, q, b0, nrows, blk;
 };
@@ -358,7 +367,7 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   }
   if (tid < ROWS) {
     uint32_t v[1];
-    wait_words<1>(c.smp + tid, (uint32_t)(step + 1), v, c.abort_word, c.sticky);
+    wait_words<1>(c.smp + tid, step_tag(a, step), v, c.abort_word, c.sticky, c.mark);
     if (a.mode == MODE_GENERATE) {
       s.ins[tid] = (int)v[0];
     } else if (tid < c.nrows && step + forced_shift(a.mode) < a.n_steps) {
@@ -412,7 +421,7 @@ __device__ __forceinline__ void b_role(Ctx &c) {
   c.nxt = c.fw + DB * 1024;
   __syncthreads();
   for (long long step = 0; step < c.a->n_steps; ++step) {
-    const uint32_t tag = (uint32_t)(step + 1);
+    const uint32_t tag = step_tag(*c.a, step);
     for (int l = 0; l < L; l += 6) {
       b_layer<0, 0>(c, l, W, P, tag);
       b_layer<FB, 1>(c, l + 1, W, P, tag);
@@ -461,6 +470,7 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   c.smp = comm_smp(a.sp_comm, L, blk);
   c.abort_word = (uint32_t *)a.sp_comm;
   c.sticky = a.sp_sticky;
+  c.mark = launch_mark(a);
 
   const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
   for (int i = tid; i < Q * R / 8; i += NT) ((u32x4 *)s.embT)[i] = embsrc[i];
@@ -486,14 +496,14 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   u64 *hs = comm_hs(a.sp_comm, L, blk);
   if (tid < NHLP + 1) {
     uint32_t v[1];
-    wait_words<1>(hs + HSLOT * tid, 1, v, c.abort_word, c.sticky);
+    wait_words<1>(hs + HSLOT * tid, c.mark, v, c.abort_word, c.sticky, c.mark);
     s.ins[ROWS + tid] = (int)v[0];
   }
   __syncthreads();
   bool local = true;
   for (int h = 0; h < NHLP + 1; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
   c.local = local;
-  if (tid == 0) put_word(hs + HSLOT * (NHLP + 1), local ? 1u : 0u, 1, false);
+  if (tid == 0) put_word(hs + HSLOT * (NHLP + 1), local ? 1u : 0u, c.mark, false);
   if (c.w < 4) a_role(c);
   else b_role(c);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
@@ -511,10 +521,10 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
 // Gather 16 x 512 bf16 activations (4096 words of two channels each) into act: word i = e NT + t
 // holds stream i / 256, channels 2 (i % 256) and 2 (i % 256) + 1.
 __device__ __forceinline__ void gather_act(uint16_t *act, const u64 *src, uint32_t tag, uint32_t *abort_word,
-                                           uint32_t *sticky) {
+                                           uint32_t *sticky, uint32_t mark) {
   const int tid = threadIdx.x;
   uint32_t v[8];
-  wait_words<8, NT>(src + tid, tag, v, abort_word, sticky);
+  wait_words<8, NT>(src + tid, tag, v, abort_word, sticky, mark);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int i = e * NT + tid;
@@ -530,6 +540,7 @@ struct HelperCtx {
   const u64 *zb;
   u64 *sw, *hw;
   uint32_t *abort_word;
+  uint32_t mark;  // this launch's abort mark
   int tid, w, lane, n, q, nl, wvoff, h;
   bool local;
 };
@@ -540,7 +551,7 @@ struct HelperCtx {
 // after its last layer of the step (LDS operations of one wave complete in order).
 __device__ __forceinline__ void z_operands(const HelperCtx &c, int l, uint32_t tag, u32x4 &b0, u32x4 &b1) {
   uint32_t zv[8];
-  wait_words<8, 64>(c.zb + (size_t)l * ZWORDS + c.lane, tag, zv, c.abort_word, c.a->sp_sticky);
+  wait_words<8, 64>(c.zb + (size_t)l * ZWORDS + c.lane, tag, zv, c.abort_word, c.a->sp_sticky, c.mark);
   uint32_t *stg = (uint32_t *)c.s->u.part[c.w];
 #pragma unroll
   for (int e = 0; e < 8; ++e) stg[(2 * e + (c.lane >> 5)) * ZST + (c.lane & 31)] = zv[e];
@@ -575,7 +586,7 @@ __device__ __forceinline__ void helper_steps(const HelperCtx &c, const u32x4 (&h
   }
   const char *nxt = c.fw + (nl > 1 ? FS * 1024 : 0);
   for (long long step = 0; step < a.n_steps; ++step) {
-    const uint32_t tag = (uint32_t)(step + 1);
+    const uint32_t tag = step_tag(a, step);
     // ---- 1. skip sums of the slice
     f32x4 acc[4];
 #pragma unroll
@@ -626,7 +637,7 @@ __device__ __forceinline__ void helper_steps(const HelperCtx &c, const u32x4 (&h
     }
     __syncthreads();
     // ---- 2. hidden rows of the slice: tile j = w % 4, k-steps 8 (w / 4) .. +7
-    gather_act(s.u.act, c.sw, tag, c.abort_word, a.sp_sticky);
+    gather_act(s.u.act, c.sw, tag, c.abort_word, a.sp_sticky, c.mark);
     __syncthreads();
     {
       const int k0 = 8 * (w >> 2);
@@ -674,10 +685,11 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   }
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
   u64 *hs = comm_hs(a.sp_comm, L, blk);
+  const uint32_t mark = launch_mark(a);
   if (tid == 0) {
-    put_word(hs + HSLOT * h, xcd_id(), 1, false);
+    put_word(hs + HSLOT * h, xcd_id(), mark, false);
     uint32_t v[1];
-    wait_words<1>(hs + HSLOT * (NHLP + 1), 1, v, abort_word, a.sp_sticky);
+    wait_words<1>(hs + HSLOT * (NHLP + 1), mark, v, abort_word, a.sp_sticky, mark);
     s.local = (int)v[0];
   }
   __syncthreads();
@@ -689,6 +701,7 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   c.sw = comm_s(a.sp_comm, L, blk);
   c.hw = comm_hid(a.sp_comm, L, blk);
   c.abort_word = abort_word;
+  c.mark = mark;
   c.tid = tid;
   c.w = w;
   c.lane = lane;
@@ -729,17 +742,18 @@ __device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, in
   }
   // launch handshake: publish this block's XCD, then learn whether the whole group shares it
   u64 *hs = comm_hs(a.sp_comm, L, blk);
+  const uint32_t mark = launch_mark(a);
   if (tid == 0) {
-    put_word(hs + HSLOT * NHLP, xcd_id(), 1, false);
+    put_word(hs + HSLOT * NHLP, xcd_id(), mark, false);
     uint32_t v[1];
-    wait_words<1>(hs + HSLOT * (NHLP + 1), 1, v, abort_word, a.sp_sticky);
+    wait_words<1>(hs + HSLOT * (NHLP + 1), mark, v, abort_word, a.sp_sticky, mark);
     s.local = (int)v[0];
   }
   __syncthreads();
   const bool local = s.local != 0;
   for (long long step = 0; step < a.n_steps; ++step) {
-    const uint32_t tag = (uint32_t)(step + 1);
-    gather_act(s.act, hw, tag, abort_word, a.sp_sticky);
+    const uint32_t tag = step_tag(a, step);
+    gather_act(s.act, hw, tag, abort_word, a.sp_sticky, mark);
     __syncthreads();
     // uniforms of steps [step, step + KCH): every wave has sampled the previous chunk's last step
     // before the barrier above

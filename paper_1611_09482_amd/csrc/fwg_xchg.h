@@ -1,9 +1,10 @@
-// Hand-offs between the cooperating blocks of one launch (the split and wide step-kernel families):
-// 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed device-scope atomics.  A word is
-// fresh once its tag equals the step's tag (the exchange region is zeroed before every launch), so
-// no fence or flag has to order the payload.  Every wait is bounded: a wait that runs out sets the
-// launch's abort word, which ends every other wait, and a sticky word the host reports.  Not part
-// of the public ABI.
+// Hand-offs between the cooperating blocks of one launch (the split, wide and gated chain pair
+// step-kernel families): 8-byte words of (32-bit payload, 32-bit tag), loaded with relaxed
+// device-scope atomics.  A word is fresh once its tag equals the step's tag (no tag is used twice
+// between two zero fills of the exchange region), so no fence or flag has to order the payload.
+// Every wait is bounded: a wait that runs out writes the launch's abort mark into the abort word,
+// which ends every other wait of that launch, and sets a sticky word the host reports.  Not part of
+// the public ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -43,20 +44,22 @@ __device__ __forceinline__ u64 get_word(const u64 *p) {
 __device__ __forceinline__ uint32_t get_flag(const uint32_t *p) {
   return __hip_atomic_load((uint32_t *)p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// A wait ran out: end every other wait of the launch, and leave a sticky mark for the host.
-__device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *sticky) {
-  __hip_atomic_store(abort_word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// A wait ran out: end every other wait of the launch, and leave a sticky mark for the host.  `mark`
+// identifies the launch (families that zero the region before every launch use 1).
+__device__ __forceinline__ void raise_abort(uint32_t *abort_word, uint32_t *sticky, uint32_t mark = 1u) {
+  __hip_atomic_store(abort_word, mark, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __hip_atomic_store(sticky, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Load the N tagged words p[e STRIDE] until every tag equals `tag` (or the launch is aborted).
+// Load the N tagged words p[e STRIDE] until every tag equals `tag` (or the abort word holds this
+// launch's `mark`).
 // Per lane.  Every wait of a tile uses STRIDE = the number of lanes polling it, so that each load
 // instruction reads consecutive words: a poll whose lanes each take a run of consecutive words
 // touches a cache line per lane and instruction, and those requests (not the L2's latency) made
 // the tile gathers 2-3x slower.
 template <int N, int STRIDE = 1>
 __device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t (&out)[N], uint32_t *abort_word,
-                                           uint32_t *sticky) {
+                                           uint32_t *sticky, uint32_t mark = 1u) {
   u64 v[N];
   for (int it = 0;; ++it) {
 #pragma unroll
@@ -67,9 +70,9 @@ __device__ __forceinline__ void wait_words(const u64 *p, uint32_t tag, uint32_t 
     if (ok) break;
     // the abort word every 16 polls: a stale poll then costs one round trip, not two
     if ((it & 15) == 15) {
-      if (get_flag(abort_word) != 0u) break;
+      if (get_flag(abort_word) == mark) break;
       if (it >= kSpinMax) {
-        raise_abort(abort_word, sticky);
+        raise_abort(abort_word, sticky, mark);
         break;
       }
     }

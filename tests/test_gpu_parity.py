@@ -560,6 +560,34 @@ def test_split_multi_group_ragged(B):
     check_generation(cfg, fw, orc, W.uniforms(6, B, n), B, "split multi-group")
 
 
+def test_split_tags_cross_launches_and_wrap():
+    """The split kernels' exchange-word tags continue from launch to launch (a handle's exchange
+    region is zeroed only before its first launch and when the 32-bit tags would wrap): a handle
+    whose tag base starts just below the wrap generates, in three launches of which the third
+    crosses it, exactly the samples of a fresh handle's single launch; teacher forcing in between
+    takes tags from the same sequence."""
+    cfg = FAMILIES["gated_r64_bf16_split"]
+    B = 13
+    w = W.make_weights(cfg, 31)
+    u = W.uniforms(32, B, 300)
+    ref = binding.from_model(cfg, w, max_batch=B)
+    assert ref.regime == "mfma_split_bf16_r64_s512"
+    g_ref = ref.generate(dev(u)).cpu().numpy()
+    x = W.sequences(33, B, 40)
+    lg_ref = ref.teacher_forced(dev(x)).cpu().numpy()
+    os.environ["FWG_SPLIT_TAG_BASE"] = str(0xFFFFFFFF - 250)
+    try:
+        fw = binding.from_model(cfg, w, max_batch=B)
+    finally:
+        os.environ.pop("FWG_SPLIT_TAG_BASE", None)
+    g = [fw.generate(dev(u[:, :100].copy())).cpu().numpy()]
+    assert np.array_equal(fw.teacher_forced(dev(x)).cpu().numpy(), lg_ref)
+    g.append(fw.generate(dev(u[:, 100:200].copy())).cpu().numpy())
+    g.append(fw.generate(dev(u[:, 200:].copy())).cpu().numpy())
+    fw.device_status()
+    assert np.array_equal(np.concatenate(g, axis=1), g_ref)
+
+
 def test_split_state_cleared_on_poisoned_workspace():
     """The split kernels' launch state (exchange words, abort mark) is set up by the library itself:
     a handle created on memory that held 0xFF bytes (the caching allocator hands the freed block back)
