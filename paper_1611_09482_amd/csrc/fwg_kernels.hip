@@ -30,23 +30,13 @@ namespace fwg {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// Direct global-to-LDS copy of 16 bytes per lane: lane i's bytes come from src_wave + lane_off
-// (lane_off = 16 i) and land at LDS byte address lds_dst_wave + 16 i (both bases wave-uniform).
-// Issued as inline assembly: the compiler orders every such copy after the previous one has
-// completed (it cannot tell that they write disjoint LDS), which would serialise the staging
-// stream.  The lane offset stays in one register for all copies and the bases are scalar, so no
-// register the copies read is overwritten while they are in flight; callers wait for completion
-// (vmcnt) before the data is read.
+// Direct global-to-LDS copy of 16 bytes per lane (global_load_lds_dwordx4): lane i's bytes come
+// from src_wave + lane_off (lane_off = 16 i) and land at LDS byte address lds_dst_wave + 16 i (the
+// LDS base wave-uniform; the compiler sets M0 from it).  Consecutive copies issue back to back;
+// callers wait for completion (vmcnt) before the data is read.
 __device__ __forceinline__ void lds_copy16(const void *src_wave, uint32_t lane_off, const void *lds_dst_wave) {
-  const uint32_t base = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void *)lds_dst_wave);
-  const uint64_t sp = (uint64_t)(uintptr_t)src_wave;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)sp), hi = __builtin_amdgcn_readfirstlane((uint32_t)(sp >> 32));
-  const uint64_t sbase = ((uint64_t)hi << 32) | lo;
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
-               :
-               : "s"(base), "v"(lane_off), "s"(sbase)
-               : "m0");
+  __builtin_amdgcn_global_load_lds((const char *)src_wave + lane_off,
+                                   (__attribute__((address_space(3))) void *)lds_dst_wave, 16, 0, 0);
 }
 
 template <typename WT> struct WTraits;

@@ -86,9 +86,9 @@ struct Lds {
   // channels [L][OC], the ring of weight slots and the queue P[entries][OC][SG] (products W_r x),
   // entries = sum of dilations
 };
-__host__ __device__ inline size_t lds_tables(int L) { return (sizeof(Lds) + 15) & ~(size_t)15; }
+__host__ __device__ inline size_t lds_tables() { return (sizeof(Lds) + 15) & ~(size_t)15; }
 __host__ __device__ inline size_t lds_ring(int L) {
-  return lds_tables(L) + (((size_t)(3 + OC) * L * 4 + 15) & ~(size_t)15);
+  return lds_tables() + (((size_t)(3 + OC) * L * 4 + 15) & ~(size_t)15);
 }
 __host__ __device__ inline size_t lds_queue(int L, int ns) { return lds_ring(L) + (size_t)ns * CHUNK * 16; }
 
@@ -221,7 +221,7 @@ __global__ void __launch_bounds__(NT + NTL) wide_step_kernel(StepArgs a, WideArg
   const int b0 = g * SG;                       // the group's first stream
   const int nval = min(SG, a.batch - b0);      // its valid streams
   const int ns = w.nslots;
-  int *dil = (int *)((char *)lds_raw + lds_tables(L));
+  int *dil = (int *)((char *)lds_raw + lds_tables());
   int *qoff = dil + L, *slot = qoff + L;
   float *cb = (float *)(slot + L);  // [L][OC]: conv biases of the block's channels (no global load per layer)
   float4 *ring = (float4 *)((char *)lds_raw + lds_ring(L));
