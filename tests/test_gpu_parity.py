@@ -560,6 +560,34 @@ def test_split_multi_group_ragged(B):
     check_generation(cfg, fw, orc, W.uniforms(6, B, n), B, "split multi-group")
 
 
+@pytest.mark.parametrize("n_layers,regime", [(12, "mfma_split_bf16_r64_s512"), (12, "mfma_bf16_r64_s512"),
+                                             (2, "mfma_bf16_r64_s512")])
+def test_bf16_rounding_points_closed_form_gpu(n_layers, regime):
+    """Where the bf16 kernels round: on the closed-form model of tests/rounding_model.py the logits
+    must be exactly bf16(relu(bf16(z0) + bf16(z1))) (z rounded as the skip product's operand,
+    relu(skip sum) and the hidden layer rounded, sums in float32), which differs in every one of
+    the 64 channels from the form without the rounding of z; a bar on relative error could not
+    tell the two apart."""
+    import rounding_model as RM
+    cfg, w = RM.make_model(n_layers)
+    want, alt = RM.closed_form()
+    env = {"FWG_REGIME": "mfma"} if regime == "mfma_bf16_r64_s512" and n_layers % 6 == 0 else {}
+    os.environ.update(env)
+    try:
+        fw = binding.from_model(cfg, w, max_batch=5)
+    finally:
+        for k in env:
+            os.environ.pop(k, None)
+    assert fw.regime == regime
+    x = W.sequences(6, 5, 9)
+    lg = fw.teacher_forced(dev(x)).cpu().numpy()
+    fw.device_status()
+    assert np.array_equal(lg, np.broadcast_to(want.astype(np.float32), lg.shape))
+    assert (want[:RM.R] != alt[:RM.R]).all()
+    log(f"bf16 rounding points [{fw.regime}, L={n_layers}]: logits equal the closed form in all "
+        f"{lg.shape[0] * lg.shape[1]} rows")
+
+
 def test_split_tags_cross_launches_and_wrap():
     """The split kernels' exchange-word tags continue from launch to launch (a handle's exchange
     region is zeroed only before its first launch and when the 32-bit tags would wrap): a handle

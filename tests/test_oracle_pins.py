@@ -450,3 +450,19 @@ def test_bf16_rounding_matches_torch_on_random_doubles(oracle_lib):
     ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
     got = np.array([oracle_lib.bf16_round(float(v)) for v in x])
     np.testing.assert_array_equal(got, ref)
+
+
+# ---------------------------------------------------------------- bf16 rounding points
+def test_bf16_rounding_points_closed_form(oracle_lib):
+    """The oracle rounds z (an operand of the skip product) and relu(s) to bf16 and sums at full
+    precision: on a model whose logits have a closed form (tests/rounding_model.py) it returns
+    bf16(relu(bf16(z0) + bf16(z1))) exactly, which differs from the form without the rounding of z
+    in every one of the 64 channels."""
+    import rounding_model as RM
+    want, alt = RM.closed_form()
+    assert (want[:RM.R] != alt[:RM.R]).all()
+    for n_layers in (2, 12):
+        cfg, w = RM.make_model(n_layers)
+        x = W.sequences(5, 3, 7)
+        lg = oracle_lib.Oracle(w).teacher_forced(x)
+        assert np.array_equal(lg, np.broadcast_to(want, lg.shape))
