@@ -454,15 +454,17 @@ def test_bf16_rounding_matches_torch_on_random_doubles(oracle_lib):
 
 # ---------------------------------------------------------------- bf16 rounding points
 def test_bf16_rounding_points_closed_form(oracle_lib):
-    """The oracle rounds z (an operand of the skip product) and relu(s) to bf16 and sums at full
-    precision: on a model whose logits have a closed form (tests/rounding_model.py) it returns
-    bf16(relu(bf16(z0) + bf16(z1))) exactly, which differs from the form without the rounding of z
-    in every one of the 64 channels."""
+    """The oracle rounds exactly the operands of the weight products to bf16 (the current input, the
+    popped state, z, relu(s), the hidden layer) and keeps the residual stream and every sum at full
+    precision: on the closed-form model of tests/rounding_model.py its logits equal the closed form
+    in every row (the first rows pop zeros), and moving any one rounding point changes many logits."""
     import rounding_model as RM
-    want, alt = RM.closed_form()
-    assert (want[:RM.R] != alt[:RM.R]).all()
-    for n_layers in (2, 12):
+    T = 7
+    want, alts = RM.closed_form(T)
+    for name, alt in alts.items():
+        for t in (0, T - 1):  # both kinds of rows: layer 1 pops zeros, then x1
+            assert (alt[t, :RM.R] != want[t, :RM.R]).sum() >= 16, name
+    for n_layers in (3, 12):
         cfg, w = RM.make_model(n_layers)
-        x = W.sequences(5, 3, 7)
-        lg = oracle_lib.Oracle(w).teacher_forced(x)
-        assert np.array_equal(lg, np.broadcast_to(want, lg.shape))
+        lg = oracle_lib.Oracle(w).teacher_forced(W.sequences(5, 3, T))
+        assert np.array_equal(lg, np.broadcast_to(want, lg.shape)), n_layers
