@@ -49,7 +49,7 @@ def test_workspace_size_for_every_workload(lib):
     for name, wl in W.WORKLOADS.items():
         m = wl.model
         d = B.make_desc(m.kind, m.dtype, m.channels, m.dilations, wl.batch, m.skip_channels,
-                        m.head_channels, m.n_classes, m.seed_input)
+                        m.head_channels, m.n_classes, m.seed_input, filter_width=m.filter_width)
         rc, n = _rc_size(lib, d)
         assert rc == B.FWG_OK, (name, lib.fwg_last_error())
         es = 2 if m.dtype == W.BF16 else 4
@@ -59,7 +59,7 @@ def test_workspace_size_for_every_workload(lib):
         # twice the streams: the queue regions grow with the batch (the kernel family, and with it the
         # packed weight arrays, may change: the 512-channel family takes at most 32 streams)
         d2 = B.make_desc(m.kind, m.dtype, m.channels, m.dilations, 2 * wl.batch, m.skip_channels,
-                         m.head_channels, m.n_classes, m.seed_input)
+                         m.head_channels, m.n_classes, m.seed_input, filter_width=m.filter_width)
         rc2, n2 = _rc_size(lib, d2)
         assert rc2 == B.FWG_OK and n2 >= 4 * queues + W.make_weights(m, 0).nbytes()
 
