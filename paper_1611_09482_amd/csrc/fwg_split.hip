@@ -669,6 +669,11 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
   const int tid = threadIdx.x, L = a.L;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
+  // launch handshake, first half: publish this block's XCD before loading anything, so that the
+  // chain block's wait for it overlaps the loads below
+  u64 *hs = comm_hs(a.sp_comm, L, blk);
+  const uint32_t mark = launch_mark(a);
+  if (tid == 0) put_word(hs + HSLOT * h, xcd_id(), mark, false);
   // the slice's biases into LDS for the whole launch
   {
     const float *src = a.mf_bias + L * 3 * R;  // skip sum [S], head [H], out [Q]
@@ -683,11 +688,8 @@ __device__ __forceinline__ void helper_block(const StepArgs &a, char *lds_raw, i
 #pragma unroll
     for (int i = 0; i < 8; ++i) hw1[i] = w1[((w & 3) * (S / 32) + 8 * (w >> 2) + i) * 64 + lane];
   }
-  // launch handshake: publish this block's XCD, then learn whether the whole group shares it
-  u64 *hs = comm_hs(a.sp_comm, L, blk);
-  const uint32_t mark = launch_mark(a);
+  // launch handshake, second half: learn whether the whole group shares one XCD
   if (tid == 0) {
-    put_word(hs + HSLOT * h, xcd_id(), mark, false);
     uint32_t v[1];
     wait_words<1>(hs + HSLOT * (NHLP + 1), mark, v, abort_word, a.sp_sticky, mark);
     s.local = (int)v[0];
@@ -730,6 +732,10 @@ __device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, in
   const u64 *hw = comm_hid(a.sp_comm, L, blk);
   u64 *sm = comm_smp(a.sp_comm, L, blk);
   uint32_t *abort_word = (uint32_t *)a.sp_comm;
+  // launch handshake, first half: publish this block's XCD before loading anything
+  u64 *hs = comm_hs(a.sp_comm, L, blk);
+  const uint32_t mark = launch_mark(a);
+  if (tid == 0) put_word(hs + HSLOT * NHLP, xcd_id(), mark, false);
   for (int i = tid; i < Q; i += NT) s.bias[i] = a.mf_bias[L * 3 * R + S + H + i];
   // output 1x1 fragments of classes 32w .. 32w + 31: tile j, k-step ks at j * 16 + ks of slice w
   u32x4 wo[2][H / 32];
@@ -740,11 +746,8 @@ __device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, in
 #pragma unroll
       for (int ks = 0; ks < H / 32; ++ks) wo[j][ks] = src[(j * (H / 32) + ks) * 64 + lane];
   }
-  // launch handshake: publish this block's XCD, then learn whether the whole group shares it
-  u64 *hs = comm_hs(a.sp_comm, L, blk);
-  const uint32_t mark = launch_mark(a);
+  // launch handshake, second half: learn whether the whole group shares one XCD
   if (tid == 0) {
-    put_word(hs + HSLOT * NHLP, xcd_id(), mark, false);
     uint32_t v[1];
     wait_words<1>(hs + HSLOT * (NHLP + 1), mark, v, abort_word, a.sp_sticky, mark);
     s.local = (int)v[0];
