@@ -117,11 +117,13 @@ class FastWavenet:
 
     weights: an object with the attributes of `fwg_weights` holding torch CUDA
     tensors in PyTorch layouts (per-layer attributes are lists), see
-    include/fwg.h.  The library copies and repacks them at creation."""
+    include/fwg.h.  The library copies and repacks them at creation.
+    workspace: optional caller-owned uint8 CUDA tensor of at least ws_bytes (default: allocated
+    here); it must outlive the handle."""
 
     def __init__(self, kind: int, dtype: int, channels: int, dilations: Sequence[int], max_batch: int,
                  weights, skip_channels: int = 0, head_channels: int = 0, n_classes: int = 256,
-                 seed_input: int = 128, stream=None, filter_width: int = 2):
+                 seed_input: int = 128, stream=None, filter_width: int = 2, workspace=None):
         import torch
         self._torch = torch
         self.lib = load_library()
@@ -132,7 +134,11 @@ class FastWavenet:
         self.ws_bytes = workspace_size(self.desc)
         self.device = torch.device("cuda", torch.cuda.current_device())
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        if workspace is None:
+            workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        assert workspace.dtype == torch.uint8 and workspace.is_cuda and workspace.is_contiguous()
+        assert workspace.numel() >= self.ws_bytes
+        self.workspace = workspace
 
         def ptr(t):
             return None if t is None else t.data_ptr()
@@ -298,11 +304,12 @@ def upload_weights(w, dtype: int, device=None) -> DeviceWeights:
     return d
 
 
-def from_model(cfg, weights, max_batch: int, stream=None) -> FastWavenet:
+def from_model(cfg, weights, max_batch: int, stream=None, workspace=None) -> FastWavenet:
     """Build a FastWavenet from a model description with the fields kind, dtype, channels,
-    dilations, skip_channels, head_channels, n_classes, seed_input and host weights."""
+    dilations, skip_channels, head_channels, n_classes, seed_input and host weights (workspace: as
+    for FastWavenet)."""
     dw = upload_weights(weights, cfg.dtype)
     return FastWavenet(cfg.kind, cfg.dtype, cfg.channels, cfg.dilations, max_batch, dw,
                        skip_channels=cfg.skip_channels, head_channels=cfg.head_channels,
                        n_classes=cfg.n_classes, seed_input=cfg.seed_input, stream=stream,
-                       filter_width=getattr(cfg, "filter_width", 2))
+                       filter_width=getattr(cfg, "filter_width", 2), workspace=workspace)

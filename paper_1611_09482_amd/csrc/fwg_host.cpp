@@ -599,12 +599,15 @@ hipError_t launch_step(fwg_handle *h, const StepArgs &a, void *comm = nullptr) {
       b.sp_sticky = (uint32_t *)(h->ws + p.off_sticky);
       // Tags are never reused between two zero fills of the exchange words (a fill kernel, no memset
       // node).  The static array of fwg_generate_noalloc is shared by every handle on the device: it
-      // is zeroed before every launch, whose tags then start at 1.  The workspace's region belongs
-      // to this handle: zeroed before its first launch and when the tags would wrap; every launch
-      // takes the tags above the previous launch's (handshake base + 1, step s base + 2 + s).
+      // is zeroed before every launch (this launch's groups), whose tags then start at 1.  The
+      // workspace's region belongs to this handle: zeroed whole (every group the handle's largest
+      // batch uses, since a later call may use more groups than this one) before its first launch
+      // and when the tags would wrap; every launch takes the tags above the previous launch's
+      // (handshake base + 1, step s base + 2 + s).
       const uint32_t need = (uint32_t)a.n_steps + 2u;
       if (comm || !h->sp_comm_zeroed || h->sp_tag > 0xFFFFFFFFu - need) {
-        hipError_t e = launch_fill_zero(b.sp_comm, split_comm_bytes(p.L, b.sp_nb), h->stream);
+        const size_t bytes = split_comm_bytes(p.L, comm ? b.sp_nb : p.brows / kMfRows);
+        hipError_t e = launch_fill_zero(b.sp_comm, bytes, h->stream);
         if (e != hipSuccess) return e;
         if (!comm) {
           h->sp_comm_zeroed = true;

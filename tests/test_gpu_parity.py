@@ -617,16 +617,15 @@ def test_split_tags_cross_launches_and_wrap():
 
 def test_split_state_cleared_on_poisoned_workspace():
     """The split kernels' launch state (exchange words, abort mark) is set up by the library itself:
-    a handle created on memory that held 0xFF bytes (the caching allocator hands the freed block back)
-    generates valid samples and reports a clean device status."""
+    a handle created on a workspace that holds 0xFF bytes generates valid samples and reports a clean
+    device status."""
     cfg = FAMILIES["gated_r64_bf16_split"]
     B, n = 11, 40
     w = W.make_weights(cfg, 5, bias_scale=0.1)
     ws = binding.from_model(cfg, w, max_batch=B).ws_bytes
     poison = torch.full((ws,), 0xFF, dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
-    del poison
-    fw = binding.from_model(cfg, w, max_batch=B)
+    fw = binding.from_model(cfg, w, max_batch=B, workspace=poison)
     assert fw.regime == "mfma_split_bf16_r64_s512"
     u = W.uniforms(12, B, n)
     g = fw.generate(dev(u)).cpu().numpy()
@@ -634,6 +633,28 @@ def test_split_state_cleared_on_poisoned_workspace():
     so = oracle.Oracle(w).state(B).generate(u)
     agree = (g == so).all(axis=0)
     assert agree[:8].all(), "first samples must match the oracle"
+
+
+def test_split_exchange_region_zeroed_for_every_group():
+    """The exchange words of every group a handle may use are zeroed before its first launch, not
+    only those of that launch's batch: on a workspace whose old contents look like tagged words with
+    small tags (1..64, payload 5), a first launch of 3 streams (one group) and then teacher forcing
+    of 37 streams (three groups) give the logits of a handle created on clean memory."""
+    cfg = FAMILIES["gated_r64_bf16_split"]
+    B = 37
+    w = W.make_weights(cfg, 5, bias_scale=0.1)
+    x = W.sequences(13, B, 12)
+    ref = binding.from_model(cfg, w, max_batch=B)
+    want = ref.teacher_forced(dev(x)).cpu().numpy()
+    words = (ref.ws_bytes + 7) // 8
+    poison = ((torch.arange(words, dtype=torch.int64, device="cuda") % 64 + 1) << 32) | 5
+    torch.cuda.synchronize()
+    fw = binding.from_model(cfg, w, max_batch=B, workspace=poison.view(torch.uint8))
+    assert fw.regime == "mfma_split_bf16_r64_s512"
+    fw.generate(dev(W.uniforms(14, 3, 10)))
+    got = fw.teacher_forced(dev(x)).cpu().numpy()
+    fw.device_status()
+    assert np.array_equal(got, want)
 
 
 def test_streams_independent_gpu():
