@@ -560,6 +560,26 @@ def test_split_multi_group_ragged(B):
     check_generation(cfg, fw, orc, W.uniforms(6, B, n), B, "split multi-group")
 
 
+@pytest.mark.parametrize("B,regime", [(400, "mfma_split_bf16_r64_s512"), (512, "mfma_bf16_r64_s512")])
+def test_split_largest_resident_batch_and_fallback(B, regime):
+    """The largest batches: 400 streams (25 groups, 250 blocks: every block resident at once on the
+    256 compute units, groups spanning XCDs) run on the split kernels; 512 streams (320 blocks) do
+    not fit at once and fwg_create falls back to the single-block kernel.  Teacher forcing of every
+    stream through the step kernels, the oracle on sampled streams."""
+    cfg = FAMILIES["gated_r64_bf16_split"]
+    w = W.make_weights(cfg, 110, bias_scale=0.1)
+    fw = binding.from_model(cfg, w, max_batch=B)
+    assert fw.regime == regime
+    T = 40
+    x = W.sequences(111, B, T)
+    lg = fw.teacher_forced(dev(x)).cpu().numpy()
+    fw.device_status()
+    sel = [0, 17, B // 2 + 3, B - 1]
+    err = row_rel_err(lg[sel], oracle.Oracle(w).teacher_forced(x[sel]))
+    log(f"B={B} [{fw.regime}]: TF streams {sel} max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+
+
 @pytest.mark.parametrize("n_layers,regime", [(12, "mfma_split_bf16_r64_s512"), (12, "mfma_bf16_r64_s512"),
                                              (3, "mfma_bf16_r64_s512")])
 def test_bf16_rounding_points_closed_form_gpu(n_layers, regime):
