@@ -580,6 +580,29 @@ def test_split_largest_resident_batch_and_fallback(B, regime):
     assert err.max() <= TOL[cfg.dtype]
 
 
+@pytest.mark.parametrize("fam,B,regime", [("gated_r32_f32", 128, "chain_pair_f32_r32"),
+                                          ("gated_r32_f32", 136, "chain_gated_f32_r32"),
+                                          ("relures_c512_f32", 32, "wide_f32_c512"),
+                                          ("relures_c512_f32", 33, "valu")])
+def test_cooperative_families_at_their_largest_batch(fam, B, regime):
+    """The kernel families whose blocks wait for each other at the batch where they stop fitting:
+    the gated chain pair kernel (two blocks per stream) up to 128 streams, then the one-block gated
+    chain kernel; the wide kernel (a group of 32 blocks per 4 streams, one group per XCD) up to 32
+    streams, then the general kernel.  Teacher forcing of every stream, the oracle on sampled ones."""
+    cfg = FAMILIES[fam]
+    w = W.make_weights(cfg, 112, bias_scale=0.1)
+    fw = binding.from_model(cfg, w, max_batch=B)
+    assert fw.regime == regime
+    T = 24
+    x = W.sequences(113, B, T)
+    lg = fw.teacher_forced(dev(x)).cpu().numpy()
+    fw.device_status()
+    sel = [0, B // 2, B - 1]
+    err = row_rel_err(lg[sel], oracle.Oracle(w).teacher_forced(x[sel]))
+    log(f"{fam} B={B} [{fw.regime}]: TF streams {sel} max row rel err {err.max():.3e}")
+    assert err.max() <= TOL[cfg.dtype]
+
+
 @pytest.mark.parametrize("n_layers,regime", [(12, "mfma_split_bf16_r64_s512"), (12, "mfma_bf16_r64_s512"),
                                              (3, "mfma_bf16_r64_s512")])
 def test_bf16_rounding_points_closed_form_gpu(n_layers, regime):
