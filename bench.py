@@ -390,11 +390,18 @@ def main():
     samples = B * K
     flops = float(cfg.flops_per_sample()) * samples
     achieved = flops / sec / 1e12 if sec > 0 else 0.0
-    # the MFMA step kernel is bound by matrix-core work; the general step kernels multiply on the
-    # vector ALUs in fp32
+    # the MFMA step kernels are bound by matrix-core work, the other step kernels multiply on the
+    # vector ALUs in fp32; one stream (batch 1) takes the decode-style HBM roofline instead: every
+    # step reads all weights once, pops and pushes its queue rows, reads a uniform, writes a sample
     mfma = fw.regime.startswith("mfma")
-    bound = "mfma" if mfma else "alu"
-    peak = PEAK_TFLOPS[dtype] if mfma else VALU_F32_PEAK_TFLOPS
+    es = 2 if cfg.dtype == W.BF16 else 4
+    decode_bytes = (weights.nbytes() + cfg.n_layers * cfg.filter_width * cfg.channels * es * B + 8 * B) * K
+    if B == 1:
+        bound, peak, unit = "hbm", HBM_PEAK_GBS, "GB/s"
+        achieved = decode_bytes / sec / 1e9 if sec > 0 else 0.0
+    else:
+        bound = "mfma" if mfma else "alu"
+        peak, unit = (PEAK_TFLOPS[dtype] if mfma else VALU_F32_PEAK_TFLOPS), "TFLOP/s"
     rec = stored_traffic(name)
     traffic = traffic_for(rec, K)
 
@@ -422,13 +429,15 @@ def main():
             "bound": bound,
             "achieved": achieved,
             "peak": peak,
-            "unit": "TFLOP/s",
+            "unit": unit,
             "frac": achieved / peak,
             "traffic": traffic,
             "traffic_gbs": traffic / sec / 1e9 if traffic is not None and sec > 0 else None,
             "traffic_basis": None if rec is None else
             f"rocprofv3 FETCH_SIZE + WRITE_SIZE of a {rec['steps']}-step launch (copy-calibrated), per step x {K}",
             "algorithmic_flops_per_launch": flops,
+            "algorithmic_tflops": flops / sec / 1e12 if sec > 0 else 0.0,
+            "decode_bytes_per_launch": decode_bytes,
             "launch_ms": ms,
         },
         "wall_s": wall,
