@@ -3,14 +3,15 @@
  * Instinct MI355X (gfx950).
  *
  * The library implements cached autoregressive generation through a stack of
- * width-2 dilated causal convolutions, the method of "Fast Wavenet Generation
- * Algorithm" (Paine et al., 2016):
+ * dilated causal convolutions (width 2 as in Sections 2.1-2.2, wider filters
+ * as in Section 3.1), the method of "Fast Wavenet Generation Algorithm"
+ * (Paine et al., 2016):
  *   - one generation step behaves like one step of a multi-layer recurrent net:
  *     (input, states popped from the queues) -> (logits, states to push)
  *     (Section 2.2, Fig. 4);
  *   - there is one FIFO convolution queue per layer, its depth equal to the
- *     dilation of the layer it feeds (Section 2.1, Fig. 3), initialised with
- *     zeros (Section 2.2);
+ *     dilation of the layer it feeds (Section 2.1, Fig. 3; (w - 1) times the
+ *     dilation for width w), initialised with zeros (Section 2.2);
  *   - each generated sample runs a pop phase, the computation and a push phase
  *     (Section 2.2, Fig. 5, Fig. 6), so a sample costs O(L) work instead of the
  *     O(2^L) of recomputing the tree of Fig. 1 (Section 3.1);

@@ -377,6 +377,16 @@ __device__ __forceinline__ void finish_step(Ctx &c, long long step) {
   __syncthreads();
 }
 
+// Launch handshake, second half (after the barrier that follows wave A's poll of the XCD ids):
+// whether the whole group shares this block's XCD, which decides the scope of every word the block
+// stores; thread 0 publishes it to the group.
+__device__ __forceinline__ void set_mode(Ctx &c) {
+  bool local = true;
+  for (int h = 0; h < NHLP + 1; ++h) local = local && (uint32_t)c.s->ins[ROWS + h] == xcd_id();
+  c.local = local;
+  if (threadIdx.x == 0) put_word(comm_hs(c.a->sp_comm, c.L, c.blk) + HSLOT * (NHLP + 1), local ? 1u : 0u, c.mark, false);
+}
+
 __device__ __forceinline__ void a_role(Ctx &c) {
   const int L = c.L;
   c.fw = (const char *)c.a->mf_frags + base_a(L, c.p) * 1024;
@@ -386,7 +396,15 @@ __device__ __forceinline__ void a_role(Ctx &c) {
   for (int f = 0; f < DA; ++f) W[f] = frag_at(c, f);
   c.nxt = c.fw + DA * 1024;
   f32x4 xres = f32x4{0.f, 0.f, 0.f, 0.f};
-  __syncthreads();  // the popped rows of layers 0..2 are in LDS
+  // launch handshake, first half: the XCD ids of the group's other blocks (published at their start)
+  const int tid = threadIdx.x;
+  if (tid < NHLP + 1) {
+    uint32_t v[1];
+    wait_words<1>(comm_hs(c.a->sp_comm, L, c.blk) + HSLOT * tid, c.mark, v, c.abort_word, c.sticky, c.mark);
+    c.s->ins[ROWS + tid] = (int)v[0];
+  }
+  __syncthreads();  // the popped rows of layers 0..2 and the XCD ids are in LDS
+  set_mode(c);
   __syncthreads();  // W_r v + b of layer 0 is in LDS
   for (long long step = 0; step < c.a->n_steps; ++step) {
     for (int l = 0; l < L; l += 6) {
@@ -406,15 +424,18 @@ __device__ __forceinline__ void b_role(Ctx &c) {
   c.fw = (const char *)c.a->mf_frags + base_b(L, c.p) * 1024;
   c.fend = c.fw + (size_t)len_b(L) * 1024;
   u32x4 W[DB], P[6];
-  // layers 0..2 of step 0 land now; layer 0's W_r v + b comes from its stream stage L - 1
-  pop_land(c, 0, pop_issue(c, 0, 0));
-  pop_land(c, 1, pop_issue(c, 1, 0));
-  pop_land(c, 2, pop_issue(c, 2, 0));
+  // layers 0..2 of step 0 land now and layers 3..7 are issued; layer 0's W_r v + b comes from its
+  // stream stage L - 1 (all of these loads in flight together)
+  const u32x4 v0 = pop_issue(c, 0, 0), v1 = pop_issue(c, 1, 0), v2 = pop_issue(c, 2, 0);
 #pragma unroll
   for (int g = 3; g < 8; ++g) P[g % 6] = pop_issue(c, g, 0);
-  __syncthreads();
 #pragma unroll
   for (int f = 0; f < FB; ++f) W[f] = frag_at(c, FB * (L - 1) + f);
+  pop_land(c, 0, v0);
+  pop_land(c, 1, v1);
+  pop_land(c, 2, v2);
+  __syncthreads();  // the popped rows of layers 0..2 and the XCD ids are in LDS
+  set_mode(c);
   recurrent_half(c, 0, 0, 0, W, 0);
 #pragma unroll
   for (int f = 0; f < DB; ++f) W[f] = frag_at(c, f);
@@ -472,38 +493,60 @@ __device__ __forceinline__ void chain_block(const StepArgs &a, char *lds_raw, in
   c.sticky = a.sp_sticky;
   c.mark = launch_mark(a);
 
-  const u32x4 *embsrc = (const u32x4 *)a.mf_embT;
-  for (int i = tid; i < Q * R / 8; i += NT) ((u32x4 *)s.embT)[i] = embsrc[i];
-  // conv and residual biases, then the embedding bias (the last R floats of the bias block)
-  for (int i = tid; i < L * 3 * R; i += NT) bias[i] = a.mf_bias[i];
-  for (int i = tid; i < R; i += NT) bias[L * 3 * R + i] = a.mf_bias[L * 3 * R + S + H + Q + i];
-  const uint32_t slot_bytes = (uint32_t)(a.bmax * R * 2);
-  for (int l = tid; l < L; l += NT) {
-    const LayerDev ld = a.layers[l];
-    const int s0 = (int)(a.t0 % (long long)ld.dil), s1 = s0 + 1 == ld.dil ? 0 : s0 + 1;
-    rbase[l] = (uint32_t)(ld.ring_off * 2);
-    dil[l] = ld.dil;
-    slot[l] = s0;
-    qoff[l] = rbase[l] + (uint32_t)s0 * slot_bytes;
-    qoff[L + l] = rbase[l] + (uint32_t)s1 * slot_bytes;
+  // What the block keeps in LDS for the launch: the embedding table, the conv and residual biases,
+  // the embedding bias (the last R floats of the bias block), the per-layer queue tables and the
+  // first inputs.  Every thread issues all of its loads before its first LDS store, so the launch
+  // waits for one memory round trip here instead of one per loop iteration (a 30-layer launch
+  // spent ~5 us in these loops).
+  {
+    constexpr int NE = Q * R / 8 / NT;  // 16-byte pieces of the embedding table per thread
+    static_assert(Q * R / 8 == NE * NT, "the embedding table splits evenly over the block");
+    constexpr int NB4 = 4;              // 16-byte pieces of the bias block per thread in the first batch
+    const u32x4 *esrc = (const u32x4 *)a.mf_embT;
+    const u32x4 *bsrc = (const u32x4 *)a.mf_bias;  // L * 3 * R floats, a multiple of 4
+    const int nb4 = L * 3 * R / 4;
+    u32x4 ev[NE];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) ev[k] = esrc[tid + k * NT];
+    u32x4 bv[NB4];
+#pragma unroll
+    for (int k = 0; k < NB4; ++k)
+      if (tid + k * NT < nb4) bv[k] = bsrc[tid + k * NT];
+    const float eb = tid < R ? a.mf_bias[L * 3 * R + S + H + Q + tid] : 0.f;
+    long long roff = 0;  // the layer's queue offset and dilation (first batch of layers)
+    int ldil = 1;
+    if (tid < L) {
+      roff = a.layers[tid].ring_off;
+      ldil = a.layers[tid].dil;
+    }
+    int in0 = 0;
+    if (tid < c.nrows) in0 = a.mode == MODE_TEACHER ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) ((u32x4 *)s.embT)[tid + k * NT] = ev[k];
+#pragma unroll
+    for (int k = 0; k < NB4; ++k)
+      if (tid + k * NT < nb4) ((u32x4 *)bias)[tid + k * NT] = bv[k];
+    for (int i = tid + NB4 * NT; i < nb4; i += NT) ((u32x4 *)bias)[i] = bsrc[i];  // more than 42 layers
+    if (tid < R) bias[L * 3 * R + tid] = eb;
+    const uint32_t slot_bytes = (uint32_t)(a.bmax * R * 2);
+    for (int l = tid; l < L; l += NT) {
+      if (l >= NT) {  // more than NT layers
+        roff = a.layers[l].ring_off;
+        ldil = a.layers[l].dil;
+      }
+      const int s0 = (int)(a.t0 % (long long)ldil), s1 = s0 + 1 == ldil ? 0 : s0 + 1;
+      rbase[l] = (uint32_t)(roff * 2);
+      dil[l] = ldil;
+      slot[l] = s0;
+      qoff[l] = rbase[l] + (uint32_t)s0 * slot_bytes;
+      qoff[L + l] = rbase[l] + (uint32_t)s1 * slot_bytes;
+    }
+    if (tid < ROWS) s.ins[tid] = in0;
   }
-  if (tid < ROWS) {
-    int v = 0;
-    if (tid < c.nrows) v = a.mode == MODE_TEACHER ? a.inputs[(long long)(c.b0 + tid) * a.n_steps] : a.last[c.b0 + tid];
-    s.ins[tid] = v;
-  }
-  // launch handshake: read the helpers' and the class block's XCD ids, publish the group's mode
-  u64 *hs = comm_hs(a.sp_comm, L, blk);
-  if (tid < NHLP + 1) {
-    uint32_t v[1];
-    wait_words<1>(hs + HSLOT * tid, c.mark, v, c.abort_word, c.sticky, c.mark);
-    s.ins[ROWS + tid] = (int)v[0];
-  }
-  __syncthreads();
-  bool local = true;
-  for (int h = 0; h < NHLP + 1; ++h) local = local && (uint32_t)s.ins[ROWS + h] == xcd_id();
-  c.local = local;
-  if (tid == 0) put_word(hs + HSLOT * (NHLP + 1), local ? 1u : 0u, c.mark, false);
+  __syncthreads();  // the tables are in LDS
+  // The launch handshake (the helpers' and the class block's XCD ids, then the group's mode) runs
+  // inside the roles' first loads: wave A polls the ids while its weight loads and wave B's first
+  // pops are in flight.
   if (c.w < 4) a_role(c);
   else b_role(c);
   if (a.mode != MODE_TEACHER && tid < c.nrows) a.last[c.b0 + tid] = s.ins[tid];
