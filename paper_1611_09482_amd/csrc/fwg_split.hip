@@ -799,17 +799,26 @@ __device__ __forceinline__ void class_block(const StepArgs &a, char *lds_raw, in
   const bool local = s.local != 0;
   for (long long step = 0; step < a.n_steps; ++step) {
     const uint32_t tag = step_tag(a, step);
+    // uniforms of steps [step, step + KCH): loaded before the wait for the hidden layer (their
+    // latency hides behind it), stored after the barrier below, by which every wave has sampled the
+    // previous chunk's last step
+    constexpr int NU = ROWS * KCH / NT;
+    static_assert(ROWS * KCH == NU * NT, "uniform chunk splits evenly over the block");
+    const bool stage = a.mode == MODE_GENERATE && step % KCH == 0;
+    float uv[NU];
+#pragma unroll
+    for (int e = 0; e < NU; ++e) {
+      const int idx = tid + e * NT, r = idx / KCH, j = idx % KCH;
+      uv[e] = 0.f;
+      if (stage && r < nrows && step + j < a.n_steps) uv[e] = a.uniforms[(long long)(b0 + r) * a.n_steps + step + j];
+    }
     gather_act(s.act, hw, tag, abort_word, a.sp_sticky, mark);
     __syncthreads();
-    // uniforms of steps [step, step + KCH): every wave has sampled the previous chunk's last step
-    // before the barrier above
-    if (a.mode == MODE_GENERATE && step % KCH == 0) {
+    if (stage) {
 #pragma unroll
-      for (int e = 0; e < ROWS * KCH / NT; ++e) {
-        const int idx = tid + e * NT, r = idx / KCH, j = idx % KCH;
-        float v = 0.f;
-        if (r < nrows && step + j < a.n_steps) v = a.uniforms[(long long)(b0 + r) * a.n_steps + step + j];
-        s.u[r][j] = v;
+      for (int e = 0; e < NU; ++e) {
+        const int idx = tid + e * NT;
+        s.u[idx / KCH][idx % KCH] = uv[e];
       }
     }
     // classes 32w + 16j + 4q .. +3 of stream n; two accumulators per tile (even and odd k-steps),
