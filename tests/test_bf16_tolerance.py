@@ -8,7 +8,8 @@ compound over the layers.  This test evaluates the benchmark model with float32 
 summation order and exactly the oracle's rounding points (plain numpy, time-parallel form: each
 layer over the whole sequence with zero history, Section 2.2) and measures its distance to the
 float64 oracle: ~1.4e-2 on the 30-layer stack, the spread the GPU kernels show too (~1.7e-2 at full
-size), below the 2e-2 bar.  The bar does not tell the rounding points apart: the same float32
+size), below the 2e-2 bar; deeper stacks spread further (~2.2e-2 at 48 layers), so the GPU tests scale
+the bar with depth beyond 30 layers.  The bar does not tell the rounding points apart: the same float32
 evaluation with no bf16 rounding at all lands ~1.2e-2 from the oracle as well (printed, not
 asserted); the bf16 rounding function itself is pinned by the golden vectors.
 """
@@ -59,3 +60,18 @@ def test_float32_accumulation_spread_of_the_bf16_reading(oracle_lib):
     assert 3e-3 < e.max() < TOL_BF16
     e_plain = _row_rel_err(_float32_teacher_forced(w, x, operands_bf16=False), o)
     print(f"float32 with no bf16 rounding at all vs the float64 oracle: max {e_plain.max():.3e}")
+
+
+def test_float32_spread_grows_with_depth(oracle_lib):
+    """The same float32 evaluation on the 48-layer split-kernel test stack (dilations 1..32 eight
+    times, the GPU tests' weights and inputs): past the benchmark's 30 layers the spread of a correct
+    float32 implementation exceeds 2e-2, and stays within the depth-scaled bar the GPU tests use
+    (2e-2 x L / 30)."""
+    cfg = W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 8, 512, 512)
+    w = W.make_weights(cfg, 100, bias_scale=0.1)
+    x = W.sequences(3, 11, cfg.queue_total + 60)
+    o = oracle_lib.Oracle(w).teacher_forced(x)
+    e = _row_rel_err(_float32_teacher_forced(w, x), o)
+    print(f"48 layers: float32 with the oracle's bf16 rounding points vs the float64 oracle: max "
+          f"{e.max():.3e}, p99.9 {np.quantile(e, 0.999):.3e}")
+    assert TOL_BF16 < e.max() < TOL_BF16 * cfg.n_layers / 30

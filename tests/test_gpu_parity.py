@@ -36,6 +36,17 @@ import oracle  # noqa: E402
 from paper_1611_09482_amd import binding  # noqa: E402
 
 TOL = {W.F32: 1e-4, W.BF16: 2e-2}
+
+
+def tol(cfg):
+    """Per-row logit bar of a model.  The bf16 bar holds for stacks up to the benchmark's 30 layers;
+    deeper stacks compound more operand-rounding flips (a correct float32 evaluation of the bf16
+    reading lands at ~2.2e-2 on 36- and 48-layer stacks, test_bf16_tolerance.py), so beyond 30
+    layers the bar grows linearly with depth."""
+    t = TOL[cfg.dtype]
+    return t * max(1.0, cfg.n_layers / 30) if cfg.dtype == W.BF16 else t
+
+
 TAU = {W.F32: 1e-4, W.BF16: 5e-2}
 # summation-order ties of the GPU's float32 sampler: u within this distance of a CDF boundary
 EXACT_EPS = 1e-5
@@ -123,6 +134,9 @@ FAMILIES = {
     # 36 layers: more than four layers per helper wave, so the helpers stream their skip fragments
     # (at most 32 layers they keep them in registers)
     "gated_r64_bf16_split36": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 6, 512, 512),
+    # 48 layers: the chain block's bias block (L x 3R floats) exceeds what its threads load in the
+    # first batch at launch (more than 42 layers), so the rest is copied by the loop after it
+    "gated_r64_bf16_split48": W.ModelConfig(W.GATED, W.BF16, 64, (1, 2, 4, 8, 16, 32) * 8, 512, 512),
     "relures_c512_f32": W.ModelConfig(W.RELU_RESIDUAL, W.F32, 512, (1, 2, 4, 8, 16, 1, 2)),
     # dilations 1..128: queues of 255 entries leave LDS for the wide kernel's smallest weight ring
     # (four 16 KB slots, a whole layer's chunks)
@@ -245,7 +259,7 @@ def check_generation(cfg, fw, orc, u, batch, label):
     err = row_rel_err(glg, olg)
     log(f"{label}: teacher-forced logits on the GPU sequence: max row rel err {err.max():.3e}, "
         f"p99.9 {np.quantile(err, 0.999):.3e}")
-    assert err.max() <= TOL[cfg.dtype], f"{label}: teacher-forced logits on GPU sequence: {err.max():.3e}"
+    assert err.max() <= tol(cfg), f"{label}: teacher-forced logits on GPU sequence: {err.max():.3e}"
     check_samples_exact(g, glg, u, label)
     bad = 0
     for b in range(batch):
@@ -272,7 +286,7 @@ def test_teacher_forced_parity(fam, path):
     err = row_rel_err(g, o)
     log(f"{fam} [{fw.regime}, {path}]: TF B={B} T={T} max row rel err {err.max():.3e} "
         f"p99.9 {np.quantile(err, 0.999):.3e} ({time.time() - t0:.1f}s)")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
 
 
 @pytest.mark.parametrize("fam,steps", [("relu_c32_f32", 7), ("gated_r32_f32", 5), ("gated_r64_bf16", 3),
@@ -290,7 +304,7 @@ def test_parallel_chunks_across_queues(fam, steps):
     x = W.sequences(14, B, T)
     err = row_rel_err(tf(fw, x, "parallel"), orc.teacher_forced(x))
     log(f"{fam}: parallel TF in chunks of {steps} steps, T={T}: max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
     # online prediction over two forced stretches around a generated one, then generation again
     u = W.uniforms(15, B, 40)
     x = W.sequences(18, B, 177)
@@ -302,7 +316,7 @@ def test_parallel_chunks_across_queues(fam, steps):
     st.step_forced(g)
     o_b = st.step_forced(x[:, 100:177])
     err = max(row_rel_err(lg_a, o_a).max(), row_rel_err(lg_b, o_b).max())
-    assert err <= TOL[cfg.dtype], err
+    assert err <= tol(cfg), err
     g2 = fw.generate(dev(u[:, 20:].copy())).cpu().numpy()
     so, slg = st.generate(u[:, 20:], return_logits=True)
     tau = TAU[cfg.dtype]
@@ -324,7 +338,7 @@ def test_parallel_wide_tiles(fam):
     x = W.sequences(23, B, T)
     err = row_rel_err(tf(fw, x, "parallel"), orc.teacher_forced(x))
     log(f"{fam}: parallel TF B={B} T={T} ({B * T} rows): max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
 
 
 @pytest.mark.parametrize("fam", ["gated_r32_f32", "gated_r64_bf16", "relu_c32_f32", "gated_r64_w3_bf16"])
@@ -344,7 +358,7 @@ def test_prime_then_generate(fam):
     assert np.array_equal(fw.generate(dev(u)).cpu().numpy(), g)
     fw.reset()
     ls = fw.step_forced(dev(prefix)).cpu().numpy()
-    assert row_rel_err(lp, ls).max() <= TOL[cfg.dtype]
+    assert row_rel_err(lp, ls).max() <= tol(cfg)
     st = orc.state(B)
     st.step_forced(prefix)
     so, slg = st.generate(u, return_logits=True)
@@ -372,7 +386,7 @@ def test_valu_unstaged_variant(fam):
     x = W.sequences(20, B, T)
     err = row_rel_err(fw.teacher_forced(dev(x)).cpu().numpy(), orc.teacher_forced(x))
     log(f"{fam} [{fw.regime}, unstaged]: TF max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
     check_generation(cfg, fw, orc, W.uniforms(21, B, T), B, fam + " unstaged")
 
 
@@ -411,7 +425,7 @@ def test_online_prediction_parity(fam):
             assert lo - tau <= u[b, t] < hi + tau, (fam, b, t)
     err = row_rel_err(glg, olg)
     log(f"{fam} [{fw.regime}]: online B={B} n={n2} after {n1} generated: max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
     # generation resumes from the last observed sample
     so, slg = st.generate(u[:, n1:], return_logits=True)
     for b in range(B):
@@ -556,7 +570,7 @@ def test_split_multi_group_ragged(B):
     err = row_rel_err(fw.teacher_forced(dev(x)).cpu().numpy(), orc.teacher_forced(x))
     fw.device_status()
     log(f"split B={B}: TF max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
     check_generation(cfg, fw, orc, W.uniforms(6, B, n), B, "split multi-group")
 
 
@@ -577,7 +591,7 @@ def test_split_largest_resident_batch_and_fallback(B, regime):
     sel = [0, 17, B // 2 + 3, B - 1]
     err = row_rel_err(lg[sel], oracle.Oracle(w).teacher_forced(x[sel]))
     log(f"B={B} [{fw.regime}]: TF streams {sel} max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
 
 
 @pytest.mark.parametrize("fam,B,regime", [("gated_r32_f32", 128, "chain_pair_f32_r32"),
@@ -600,7 +614,7 @@ def test_cooperative_families_at_their_largest_batch(fam, B, regime):
     sel = [0, B // 2, B - 1]
     err = row_rel_err(lg[sel], oracle.Oracle(w).teacher_forced(x[sel]))
     log(f"{fam} B={B} [{fw.regime}]: TF streams {sel} max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
 
 
 @pytest.mark.parametrize("n_layers,regime", [(12, "mfma_split_bf16_r64_s512"), (12, "mfma_bf16_r64_s512"),
@@ -753,7 +767,7 @@ def _check_streams_on_gpu_sequence(wl, fw, orc, u, g, streams, steps):
             bad += not (lo - tau <= u[b, t] < hi + tau)
     log(f"{wl.name}: streams {streams} x {steps} steps: TF rel err max {err.max():.3e} "
         f"p99.9 {np.quantile(err, 0.999):.3e}, inadmissible {bad} ({time.time() - t0:.1f}s)")
-    assert err.max() <= TOL[cfg.dtype]
+    assert err.max() <= tol(cfg)
     assert bad == 0
     gs, us = g[streams, :steps], u[streams, :steps]
     check_samples_exact(gs, glg, us, wl.name)
@@ -787,7 +801,7 @@ def test_full_gated_b64():
     o = orc.teacher_forced(x[sel])
     err = row_rel_err(glg[sel].cpu().numpy(), o)
     log(f"{wl.name}: teacher-forced seeded sequence, streams {sel}: max row rel err {err.max():.3e}")
-    assert err.max() <= TOL[wl.model.dtype]
+    assert err.max() <= tol(wl.model)
 
 
 def test_full_bench_workload():
