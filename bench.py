@@ -182,6 +182,89 @@ def cpu_baseline_tf(wl, weights, target_seconds: float):
                       f"OpenMP over streams, {streams} x {steps} samples in {dt:.1f} s wall"}
 
 
+def cpu_baseline_online(wl, weights, target_seconds: float):
+    """The oracle's online prediction (fwo_step_forced) on a bounded sample: the first streams (one
+    per thread) over as many leading steps of the workload's seeded observed sequence as fit the time
+    budget."""
+    import oracle
+    import workloads as W
+    threads = oracle.max_threads()
+    streams = max(1, min(wl.batch, threads))
+    o = oracle.Oracle(weights)
+    calib = 8
+    t0 = time.perf_counter()
+    oracle.OracleState(o, streams, wl.model.seed_input).step_forced(W.sequences(wl.uniform_seed, streams, calib))
+    per_step = (time.perf_counter() - t0) / calib
+    steps = int(max(16, min(wl.n_steps, target_seconds / max(per_step, 1e-9))))
+    x = W.sequences(wl.uniform_seed, streams, steps)
+    st = oracle.OracleState(o, streams, wl.model.seed_input)
+    t0 = time.perf_counter()
+    lg = st.step_forced(x)
+    dt = time.perf_counter() - t0
+    assert lg.shape[:2] == (streams, steps), lg.shape
+    return {"value": streams * steps / dt, "unit": "samples/s", "cores": min(threads, streams),
+            "kind": "oracle", "streams": streams, "steps_run": steps, "seconds": dt,
+            "sample": f"{_oracle_build_note()} online prediction over streams 0..{streams - 1} of the "
+                      f"{wl.batch}-stream workload for steps 0..{steps - 1} of {wl.n_steps} (per-step cost "
+                      f"constant), OpenMP over streams, {streams} x {steps} samples in {dt:.1f} s wall"}
+
+
+def bench_online(args, wl, name, fw, weights, stream, K, Wu):
+    """One fwg_step_forced call (online prediction: each step reports the logits that predict the
+    next observed sample, then takes that sample as its input) over the workload's batch and steps,
+    on the same step kernels as generation."""
+    import numpy as np
+    import torch
+    import workloads as W
+    cfg = wl.model
+    B = wl.batch
+    x_host = W.sequences(wl.uniform_seed, B, max(K, Wu, 1))
+    x = torch.from_numpy(np.ascontiguousarray(x_host[:, :K])).cuda()
+    logits = torch.empty((B, K, cfg.n_classes), dtype=torch.float32, device="cuda")
+    if Wu > 0:
+        fw.step_forced(torch.from_numpy(np.ascontiguousarray(x_host[:, :Wu])).cuda(), check=False)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    fw.step_forced(x, out=logits, check=False)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = e0.elapsed_time(e1)
+    sec = ms / 1e3
+    fw.device_status()  # raises if the launch ended without valid results
+    dtype = "bf16" if cfg.dtype == W.BF16 else "f32"
+    samples = B * K
+    flops = float(cfg.flops_per_sample()) * samples
+    achieved = flops / sec / 1e12 if sec > 0 else 0.0
+    mfma = fw.regime.startswith("mfma")
+    peak = PEAK_TFLOPS[dtype] if mfma else VALU_F32_PEAK_TFLOPS
+    result = {
+        "metric": "online-prediction samples/sec (batch x steps/s)",
+        "value": samples / sec if sec > 0 else 0.0,
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wu,
+        "ms_per_step": ms / max(K, 1),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtype,
+        "data": "synthetic",
+        "config": {"workload": name, "description": wl.description, "batch": B, "seq_len": K,
+                   "mode": "online", "regime": fw.regime},
+        "roofline": {"bound": "mfma" if mfma else "alu", "achieved": achieved, "peak": peak,
+                     "unit": "TFLOP/s", "frac": achieved / peak, "traffic": None,
+                     "algorithmic_flops_per_launch": flops, "launch_ms": ms},
+        "wall_s": wall,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_online(wl, weights, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
 def bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu):
     import numpy as np
     import torch
@@ -300,7 +383,7 @@ def main():
     ap.add_argument("--workload", default=None)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="wall-time budget of the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", choices=["generate", "teacher_forced", "naive_vs_fast"], default="generate")
+    ap.add_argument("--mode", choices=["generate", "teacher_forced", "online", "naive_vs_fast"], default="generate")
     ap.add_argument("--tf-path", choices=["parallel", "step"], default="parallel",
                     help="teacher_forced mode: time-parallel kernels or the step kernels")
     ap.add_argument("--naive-samples", type=int, default=50, help="samples per timed call (naive_vs_fast)")
@@ -360,6 +443,11 @@ def main():
         stream = torch.cuda.current_stream()
         fw = binding.from_model(cfg, weights, max_batch=B, stream=stream)
         bench_teacher_forced(args, wl, name, fw, weights, stream, K, Wu)
+        return
+    if args.mode == "online":
+        stream = torch.cuda.current_stream()
+        fw = binding.from_model(cfg, weights, max_batch=B, stream=stream)
+        bench_online(args, wl, name, fw, weights, stream, K, Wu)
         return
     u_host = W.uniforms(wl.uniform_seed, B, max(K, Wu, 1))
     u_timed = torch.from_numpy(np.ascontiguousarray(u_host[:, :K])).cuda()
