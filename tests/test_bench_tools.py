@@ -69,3 +69,7 @@ def test_cpu_baseline_counts_the_steps_it_runs():
     r = bench.cpu_baseline_tf(wl, w, 0.0)
     assert r["steps_run"] == 16
     assert abs(r["value"] - r["streams"] * 16 / r["seconds"]) <= 1e-9 * r["value"]
+    r = bench.cpu_baseline_online(wl, w, 0.0)
+    assert r["steps_run"] == 16
+    assert abs(r["value"] - r["streams"] * 16 / r["seconds"]) <= 1e-9 * r["value"]
+    assert f"{r['streams']} x 16 samples" in r["sample"]
