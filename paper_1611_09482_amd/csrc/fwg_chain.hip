@@ -1031,19 +1031,45 @@ __global__ void __launch_bounds__(NT) chain_pair_kernel(StepArgs a, ChainGatedAr
       *s.mode = (int)v[0];
     }
   }
-  // ---- tables into LDS (the chain block), flags, the first chunk of per-step inputs
+  // ---- tables into LDS (the chain block), flags, the first chunk of per-step inputs.  Every
+  // thread issues all of its loads before its first LDS store, so the launch waits for one memory
+  // round trip here instead of one per loop iteration.
   if (h == 0) {
-    for (int i = tid; i < Q * R / 4; i += NT) ((float4 *)s.embT)[i] = ((const float4 *)g.embT)[i];
-    for (int i = tid; i < R; i += NT) s.embb[i] = g.embb[i];
-    for (int i = tid; i < L * R; i += NT) s.resb[i] = g.resb[i];
-    for (int j = tid; j < KCH; j += NT) {
-      if (a.mode == MODE_GENERATE) s.u[j] = j < a.n_steps ? a.uniforms[(long long)b * a.n_steps + j] : 0.f;
-      else {
-        const long long nx = j + forced_shift(a.mode);
-        s.fin[j] = nx < a.n_steps ? a.inputs[(long long)b * a.n_steps + nx] : 0;
+    typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+    constexpr int NE = Q * R / 4 / NT;  // 16-byte pieces of the embedding table per thread
+    constexpr int NRB = 4;              // residual biases per thread in the first batch
+    static_assert(Q * R / 4 == NE * NT && R <= NT && KCH <= NT, "tables split over the block");
+    v4u ev[NE];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) ev[k] = ((const v4u *)g.embT)[tid + k * NT];
+    const float eb = tid < R ? g.embb[tid] : 0.f;
+    float rb[NRB];
+#pragma unroll
+    for (int k = 0; k < NRB; ++k) rb[k] = tid + k * NT < L * R ? g.resb[tid + k * NT] : 0.f;
+    float uj = 0.f;
+    int fj = 0;
+    if (tid < KCH) {
+      if (a.mode == MODE_GENERATE) {
+        if (tid < a.n_steps) uj = a.uniforms[(long long)b * a.n_steps + tid];
+      } else {
+        const long long nx = tid + forced_shift(a.mode);
+        if (nx < a.n_steps) fj = a.inputs[(long long)b * a.n_steps + nx];
       }
     }
-    if (tid == 0) *s.inval = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
+    int in0 = 0;
+    if (tid == 0) in0 = a.mode == MODE_TEACHER ? a.inputs[(long long)b * a.n_steps] : a.last[b];
+#pragma unroll
+    for (int k = 0; k < NE; ++k) ((v4u *)s.embT)[tid + k * NT] = ev[k];
+    if (tid < R) s.embb[tid] = eb;
+#pragma unroll
+    for (int k = 0; k < NRB; ++k)
+      if (tid + k * NT < L * R) s.resb[tid + k * NT] = rb[k];
+    for (int i = tid + NRB * NT; i < L * R; i += NT) s.resb[i] = g.resb[i];  // more than 32 layers
+    if (tid < KCH) {
+      if (a.mode == MODE_GENERATE) s.u[tid] = uj;
+      else s.fin[tid] = fj;
+    }
+    if (tid == 0) *s.inval = in0;
   }
   for (int i = tid; i < L; i += NT) {
     s.fx[i] = 0;
